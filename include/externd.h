@@ -1,0 +1,173 @@
+/*
+ * externd.h -- C ABI of the MI355X (gfx950) ExTernD factorizer.
+ *
+ * ExTernD approximates a matrix A (m x n) as A ~= B diag(D) C with ternary
+ * factors B in {-1,0,1}^{m x k}, C in {-1,0,1}^{k x n} and real scales D,
+ * k = mu * min(m, n) (paper: "ExTernD: Expanded-Rank Ternary
+ * Decomposition", Sec. 2.1, Eq. (1)).  Components are extracted by greedy
+ * alternating least squares with sequential deflation (Sec. 2.3), in blocks
+ * of b components with decorrelated least-squares targets (Sec. 2.4,
+ * Eq. (3)) and a joint exact scale solve (Eq. (4)); optionally with
+ * per-column importance weights (Sec. 2.5, lambda = 0).
+ *
+ * Conventions for every entry point:
+ *  - "device" pointers are HIP device memory on the current device (for
+ *    example torch.cuda tensor data pointers); "host" pointers are ordinary
+ *    CPU memory.
+ *  - Matrices are row-major and dense (leading dimension = column count).
+ *  - The caller owns every buffer.  The library keeps no pointer after a
+ *    call returns, allocates no device memory and has no global state
+ *    besides the loaded code object; calls on distinct workspaces and
+ *    streams are independent.  Calls sharing a workspace must be ordered
+ *    (same stream or synchronised by the caller).
+ *  - `stream` is a hipStream_t (NULL = the default stream).  All device work
+ *    is enqueued on it.
+ *  - Errors are returned as negative status codes; no exception crosses the
+ *    ABI.  Argument errors are detected on the host before any device work
+ *    is enqueued.  On error the contents of output buffers are unspecified
+ *    (host energy outputs are set to NaN where given).
+ *
+ * Packed trit format (B and C outputs): 2 bits per element, element j of a
+ * row in byte (j >> 2) at bits 2*(j & 3) .. 2*(j & 3)+1; bit 0 = nonzero,
+ * bit 1 = negative: 00 -> 0, 01 -> +1, 11 -> -1 (10 is never written).
+ * Each row is padded to a whole byte with zero bits.
+ */
+#ifndef EXTERND_H
+#define EXTERND_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EXTERND_OK            0
+#define EXTERND_EINVAL       -1  /* bad scalar argument or NULL required pointer        */
+#define EXTERND_ENONFINITE   -2  /* NaN/Inf in A (detected on the device)               */
+#define EXTERND_EWORKSPACE   -3  /* workspace smaller than externd_workspace_bytes()    */
+#define EXTERND_EHIP         -4  /* HIP runtime or launch failure                       */
+#define EXTERND_EUNSUPPORTED -5  /* shape outside the supported range                   */
+
+/* Largest block width the kernels handle; larger requests are clamped. */
+#define EXTERND_MAX_BLOCK 64
+
+/* Ridge of the decorrelated targets, Eq. (3): eps = EXTERND_RIDGE_REL *
+ * trace(G) / bb for each Gram matrix G of a block of bb components.      */
+#define EXTERND_RIDGE_REL 1e-6
+/* Guard of the joint scale solve, Eq. (4): (M + delta I) d = g with
+ * delta = EXTERND_SCALE_GUARD_REL * trace(M) / bb.                       */
+#define EXTERND_SCALE_GUARD_REL 1e-12
+
+/* Human-readable name of a status code (static string). */
+const char* externd_strerror(int status);
+
+/* Inner rank k = floor(mu * min(m, n) + 0.5) (Sec. 2.1); -1 if k < 1 or
+ * the arguments are invalid.                                             */
+int64_t externd_rank(int64_t m, int64_t n, double mu);
+
+/* Block width actually used: min(block, floor(min(m, n) / 8),
+ * EXTERND_MAX_BLOCK), at least 1 (Sec. 2.4 caps b at min(m, n) / 8).
+ * -1 on invalid arguments.                                               */
+int32_t externd_effective_block(int64_t m, int64_t n, int32_t block);
+
+/* Device workspace, in bytes, for an m x n matrix and inner rank k:
+ * k = externd_rank(m, n, mu) for externd_factorize, k = 0 for the step
+ * entry points.  Independent of block and of whether weights are given.
+ * Dominated by one fp32 copy of the residual (4 m n bytes).  0 on invalid
+ * arguments or unsupported shapes.                                       */
+size_t externd_workspace_bytes(int64_t m, int64_t n, int64_t k);
+
+/*
+ * externd_factorize -- full greedy block-ALS factorization (Sec. 2.3-2.5).
+ *
+ *  A          device, fp32 m x n, read only.
+ *  m, n       1 <= m <= 2^26, 1 <= n <= 2^20, and with both rounded up to
+ *             multiples of 32 their product below 2^31 (else
+ *             EXTERND_EUNSUPPORTED).
+ *  mu         inner-rank multiplier, k = externd_rank(m, n, mu) >= 1.
+ *  tau        threshold scale of T_tau, Eq. (2); finite, >= 0.
+ *  block      requested block width b >= 1 (see externd_effective_block;
+ *             block = 1 is the sequential algorithm of Sec. 2.3).
+ *  iters      ALS iterations per block, >= 1; one iteration is a V-step
+ *             followed by a U-step (Sec. 2.3 order).
+ *  importance device fp32[n] per-column weights h (finite, >= 0, max > 0),
+ *             or NULL for the plain Frobenius objective.  h~ = h / max(h).
+ *  B_packed   device, m rows of ceil(k/4) bytes (packed trits, B[:, i]).
+ *  C_packed   device, k rows of ceil(n/4) bytes (packed trits, C[i, :]).
+ *  D          device fp32[k].
+ *  energy     host, out: E = 1 - ||A - B diag(D) C||^2 / ||A||^2 (Sec. 2.1)
+ *             as tracked on the device residual.
+ *  energy_w   host, out (may be NULL): weighted energy
+ *             1 - sum_j h~_j ||R_:j||^2 / sum_j h~_j ||A_:j||^2;
+ *             equals energy when importance is NULL.
+ *  energy_curve, energy_w_curve
+ *             host, out (may be NULL): E (resp. weighted E) after each
+ *             block, ceil(k / b_eff) doubles.
+ *  workspace  device, >= externd_workspace_bytes(m, n, k) bytes, 256-byte
+ *             aligned.
+ *  stream     hipStream_t or NULL.
+ *
+ * Enqueues all work on `stream` and synchronises that stream before
+ * returning (energies are host outputs).  Deterministic: identical inputs
+ * give bit-identical outputs.
+ */
+int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double tau,
+                      int32_t block, int32_t iters, const float* importance,
+                      uint8_t* B_packed, uint8_t* C_packed, float* D,
+                      double* energy, double* energy_w,
+                      double* energy_curve, double* energy_w_curve,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Step entry points: one step each of the block ALS on caller-given state,
+ * for per-step parity checks.  They share the kernels of
+ * externd_factorize.  Block matrices are row-major with bb columns:
+ * U is m x bb int8 in {-1,0,1}, V is n x bb int8.  1 <= bb <= 64.
+ * Every pointer except `h` / `*_or_null` outputs is required.  These calls
+ * are asynchronous on `stream`.
+ */
+
+/* Initial U of a block (paper silent; reading: the residual columns with
+ * the bb largest h~_j ||R_:j||^2, ties to the smaller index, are
+ * ternarized with T_tau, Eq. (2)).  J_out: device int32[bb], the chosen
+ * column indices in descending order of weighted energy.                 */
+int externd_step_init(const float* R, int64_t m, int64_t n, const float* h, int32_t bb,
+                      double tau, int8_t* U_out, int32_t* J_out,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* V-step of Eq. (3): Y = (U^T U + eps I)^{-1} U^T R, V[:, c] = T_tau(Y[c, :]).
+ * V_out device int8 n x bb; Y_out_or_null device fp64 bb x n.            */
+int externd_step_vstep(const float* R, int64_t m, int64_t n, const int8_t* U, int32_t bb,
+                       double tau, int8_t* V_out, double* Y_out_or_null,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* U-step of Eq. (3) with the weighting of Sec. 2.5:
+ * Q = R diag(h~) V, Z = Q (V^T diag(h~) V + eps I)^{-1}, U[:, c] = T_tau(Z[:, c]).
+ * h may be NULL (h~ = 1).  U_out device int8 m x bb; Q_out_or_null and
+ * Z_out_or_null device fp64 m x bb.                                      */
+int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, int32_t bb,
+                       double tau, const float* h, int8_t* U_out,
+                       double* Q_out_or_null, double* Z_out_or_null,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Joint scale solve, Eq. (4): [(U^T U) o (V^T diag(h~) V) + delta I] d =
+ * diag(U^T Q) with Q = R diag(h~) V (device fp64 m x bb, as returned by
+ * externd_step_ustep).  d_out device fp64[bb].                           */
+int externd_step_scale(const int8_t* U, const int8_t* V, const double* Q, int64_t m,
+                       int64_t n, int32_t bb, const float* h, double* d_out,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Block deflation R <- R - U diag(d) V^T (Sec. 2.4), in place on the
+ * device fp32 m x n matrix R, with d rounded to fp32 (as stored in D).
+ * colnorm2_out device fp64[n] (may be NULL): ||R_:j||^2 after the update;
+ * fro2_out device fp64[1] (may be NULL): ||R||_F^2 after the update.    */
+int externd_step_deflate(float* R, int64_t m, int64_t n, const int8_t* U, const int8_t* V,
+                         const double* d, int32_t bb, double* colnorm2_out, double* fro2_out,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EXTERND_H */

@@ -1,0 +1,333 @@
+// C-ABI entry points of the ExTernD factorizer (declared in include/externd.h).
+//
+// Host orchestration of the greedy block ALS (paper Sec. 2.3-2.5): argument
+// validation, workspace carving, the sequential loop over blocks
+// (deflation across blocks is sequential, Sec. 2.4), and the read-back of
+// the energy history.  All arithmetic runs in the kernels of
+// externd_kernels.hip.
+#include "externd.h"
+#include "externd_internal.hpp"
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <string.h>
+#include <vector>
+
+namespace externd {
+
+static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+static inline int64_t round_up(int64_t x, int64_t q) { return (x + q - 1) / q * q; }
+static inline int clampi(int64_t v, int64_t lo, int64_t hi) { return (int)(v < lo ? lo : (v > hi ? hi : v)); }
+
+struct Layout {
+  int64_t m_pad, n_pad;
+  int gv, gd, nblk_cap;
+  size_t off[32];
+  size_t total;
+};
+
+static Layout make_layout(int64_t m, int64_t n, int64_t k) {
+  Layout L{};
+  L.m_pad = round_up(m, TILE);
+  L.n_pad = round_up(n, TILE);
+  const int64_t nct = L.n_pad / TILE, nrt = L.m_pad / TILE;
+  // V-step: about 320 column-tile x row-group workgroups; deflation and
+  // staging: about 640.
+  L.gv = clampi((320 + nct - 1) / nct, 1, nrt < 16 ? nrt : 16);
+  L.gd = clampi((640 + nct - 1) / nct, 1, nrt < 64 ? nrt : 64);
+  L.nblk_cap = (int)(k + 2);  // fro2 before every block and after the last; one spare
+  const size_t sizes[] = {
+      sizeof(float) * (size_t)(L.m_pad * L.n_pad),     // 0 R
+      (size_t)(BBP * L.m_pad),                         // 1 Ut
+      (size_t)(BBP * L.m_pad),                         // 2 Ur
+      (size_t)(BBP * L.n_pad),                         // 3 Vt
+      (size_t)(BBP * L.n_pad),                         // 4 Vr
+      sizeof(double) * (size_t)(BBP * L.m_pad),        // 5 Q
+      sizeof(double) * (size_t)(BBP * L.m_pad),        // 6 Z
+      sizeof(long long) * (size_t)(L.gv * BBP * L.n_pad),  // 7 Pp
+      sizeof(double) * (size_t)(BBP * L.n_pad),        // 8 Y
+      sizeof(double) * 4096,                           // 9 ginvU
+      sizeof(double) * 4096,                           // 10 ginvV
+      sizeof(double) * 4096,                           // 11 gramV
+      sizeof(double) * 4096 * NSIDE,                   // 12 gpart
+      sizeof(int) * 4096 * NSIDE,                      // 13 gparti
+      sizeof(double) * (size_t)(L.gd * L.n_pad),       // 14 colE_part
+      sizeof(double) * (size_t)L.n_pad,                // 15 hw
+      sizeof(double) * BBP,                            // 16 gvec
+      sizeof(double) * BBP,                            // 17 dvec
+      sizeof(float) * BBP,                             // 18 dF
+      sizeof(int) * BBP,                               // 19 J
+      sizeof(unsigned) * (size_t)L.nblk_cap,           // 20 maxbits
+      sizeof(double) * (size_t)L.nblk_cap,             // 21 fro2_hist
+      sizeof(double) * (size_t)L.nblk_cap,             // 22 fro2w_hist
+      sizeof(unsigned) * CNT_COUNT,                    // 23 counters
+      sizeof(int) * FLAG_COUNT,                        // 24 flags
+      sizeof(unsigned) * (size_t)L.nblk_cap,           // 25 maxbits_w
+  };
+  size_t o = 0;
+  for (size_t i = 0; i < sizeof(sizes) / sizeof(sizes[0]); ++i) {
+    L.off[i] = o;
+    o += align256(sizes[i]);
+  }
+  L.total = o;
+  return L;
+}
+
+size_t workspace_bytes(int64_t m, int64_t n, int64_t k) { return make_layout(m, n, k).total; }
+
+bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
+  const Layout L = make_layout(m, n, k);
+  if (bytes < L.total || base == nullptr || ((uintptr_t)base & 255u) != 0) return false;
+  char* b = (char*)base;
+  w.m = m;
+  w.n = n;
+  w.m_pad = L.m_pad;
+  w.n_pad = L.n_pad;
+  w.nblk_cap = L.nblk_cap;
+  w.gv = L.gv;
+  w.gd = L.gd;
+  w.R = (float*)(b + L.off[0]);
+  w.Ut = (int8_t*)(b + L.off[1]);
+  w.Ur = (int8_t*)(b + L.off[2]);
+  w.Vt = (int8_t*)(b + L.off[3]);
+  w.Vr = (int8_t*)(b + L.off[4]);
+  w.Q = (double*)(b + L.off[5]);
+  w.Z = (double*)(b + L.off[6]);
+  w.Pp = (long long*)(b + L.off[7]);
+  w.Y = (double*)(b + L.off[8]);
+  w.ginvU = (double*)(b + L.off[9]);
+  w.ginvV = (double*)(b + L.off[10]);
+  w.gramV = (double*)(b + L.off[11]);
+  w.gpart = (double*)(b + L.off[12]);
+  w.gparti = (int*)(b + L.off[13]);
+  w.colE_part = (double*)(b + L.off[14]);
+  w.hw = (double*)(b + L.off[15]);
+  w.gvec = (double*)(b + L.off[16]);
+  w.dvec = (double*)(b + L.off[17]);
+  w.dF = (float*)(b + L.off[18]);
+  w.J = (int*)(b + L.off[19]);
+  w.maxbits = (unsigned*)(b + L.off[20]);
+  w.fro2_hist = (double*)(b + L.off[21]);
+  w.fro2w_hist = (double*)(b + L.off[22]);
+  w.counters = (unsigned*)(b + L.off[23]);
+  w.flags = (int*)(b + L.off[24]);
+  w.maxbits_w = (unsigned*)(b + L.off[25]);
+  return true;
+}
+
+}  // namespace externd
+
+using namespace externd;
+
+// ---------------------------------------------------------------------------
+// validation helpers
+// ---------------------------------------------------------------------------
+static const int64_t kMaxDim = (int64_t)1 << 26;
+
+static bool shape_ok(int64_t m, int64_t n) {
+  if (m < 1 || n < 1 || m > kMaxDim || n > ((int64_t)1 << 20)) return false;
+  const int64_t mp = (m + TILE - 1) / TILE * TILE, np = (n + TILE - 1) / TILE * TILE;
+  return mp * np < ((int64_t)1 << 31);
+}
+
+#define HIP_TRY(expr)                               \
+  do {                                              \
+    hipError_t _e = (expr);                         \
+    if (_e != hipSuccess) return EXTERND_EHIP;      \
+  } while (0)
+
+extern "C" {
+
+const char* externd_strerror(int status) {
+  switch (status) {
+    case EXTERND_OK: return "ok";
+    case EXTERND_EINVAL: return "invalid argument";
+    case EXTERND_ENONFINITE: return "non-finite value in the input matrix";
+    case EXTERND_EWORKSPACE: return "workspace too small or misaligned";
+    case EXTERND_EHIP: return "HIP runtime or launch failure";
+    case EXTERND_EUNSUPPORTED: return "unsupported shape";
+    default: return "unknown status";
+  }
+}
+
+int64_t externd_rank(int64_t m, int64_t n, double mu) {
+  if (m < 1 || n < 1 || !(mu > 0.0) || !isfinite(mu)) return -1;
+  const double kk = floor(mu * (double)(m < n ? m : n) + 0.5);
+  if (kk < 1.0 || kk > 9.0e15) return -1;
+  return (int64_t)kk;
+}
+
+int32_t externd_effective_block(int64_t m, int64_t n, int32_t block) {
+  if (m < 1 || n < 1 || block < 1) return -1;
+  int64_t cap = (m < n ? m : n) / 8;
+  if (cap < 1) cap = 1;
+  int64_t b = block;
+  if (b > cap) b = cap;
+  if (b > EXTERND_MAX_BLOCK) b = EXTERND_MAX_BLOCK;
+  return (int32_t)b;
+}
+
+size_t externd_workspace_bytes(int64_t m, int64_t n, int64_t k) {
+  if (!shape_ok(m, n) || k < 0) return 0;
+  return externd::workspace_bytes(m, n, k);
+}
+
+int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
+                      const float* importance, uint8_t* B_packed, uint8_t* C_packed, float* D, double* energy,
+                      double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  if (energy) *energy = NAN;
+  if (energy_w) *energy_w = NAN;
+  if (!A || !B_packed || !C_packed || !D || !energy || !workspace) return EXTERND_EINVAL;
+  if (m < 1 || n < 1 || !isfinite(tau) || tau < 0.0 || block < 1 || iters < 1) return EXTERND_EINVAL;
+  const int64_t k = externd_rank(m, n, mu);
+  if (k < 1) return EXTERND_EINVAL;
+  if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
+  const int b_eff = externd_effective_block(m, n, block);
+  const int64_t nblk = (k + b_eff - 1) / b_eff;
+  Ws w{};
+  if (!carve(w, workspace, workspace_bytes, m, n, k)) return EXTERND_EWORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  const bool weighted = importance != nullptr;
+
+  HIP_TRY(launch_prep(w, importance, s));
+  HIP_TRY(launch_stage(w, A, n, s));
+  int flags[FLAG_COUNT];
+  HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (flags[FLAG_BADWEIGHT]) return EXTERND_EINVAL;
+  if (flags[FLAG_NONFINITE]) return EXTERND_ENONFINITE;
+
+  for (int64_t blk = 0; blk < nblk; ++blk) {
+    const int64_t c0 = blk * b_eff;
+    const int bb = (int)((k - c0) < b_eff ? (k - c0) : b_eff);
+    HIP_TRY(launch_select(w, (int)blk, bb, s));
+    HIP_TRY(launch_init(w, bb, tau, s));
+    for (int it = 0; it < iters; ++it) {
+      HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s));
+      HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, s));
+    }
+    HIP_TRY(launch_scale(w, bb, s));
+    HIP_TRY(launch_deflate(w, (int)blk, s));
+    HIP_TRY(launch_emit(w, c0, bb, k, B_packed, C_packed, D, s));
+  }
+  HIP_TRY(launch_finish(w, (int)nblk, s));
+
+  std::vector<double> f2((size_t)nblk + 1), f2w((size_t)nblk + 1);
+  HIP_TRY(hipMemcpyAsync(f2.data(), w.fro2_hist, sizeof(double) * (nblk + 1), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(f2w.data(), w.fro2w_hist, sizeof(double) * (nblk + 1), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  const double a2 = f2[0], a2w = f2w[0];
+  auto E = [&](int64_t b) { return a2 == 0.0 ? 1.0 : 1.0 - f2[(size_t)b] / a2; };
+  auto Ew = [&](int64_t b) { return a2w == 0.0 ? 1.0 : 1.0 - f2w[(size_t)b] / a2w; };
+  *energy = E(nblk);
+  if (energy_w) *energy_w = Ew(nblk);
+  for (int64_t b = 0; b < nblk; ++b) {
+    if (energy_curve) energy_curve[b] = E(b + 1);
+    if (energy_w_curve) energy_w_curve[b] = Ew(b + 1);
+  }
+  return EXTERND_OK;
+}
+
+// ---------------------------------------------------------------------------
+// step entry points
+// ---------------------------------------------------------------------------
+static int step_prologue(Ws& w, const float* R, int64_t m, int64_t n, int32_t bb, void* ws, size_t ws_bytes) {
+  if (!R || !ws || m < 1 || n < 1 || bb < 1 || bb > BBP) return EXTERND_EINVAL;
+  if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
+  if (!carve(w, ws, ws_bytes, m, n, 0)) return EXTERND_EWORKSPACE;
+  return EXTERND_OK;
+}
+
+int externd_step_init(const float* R, int64_t m, int64_t n, const float* h, int32_t bb, double tau, int8_t* U_out,
+                      int32_t* J_out, void* ws, size_t ws_bytes, void* stream) {
+  Ws w{};
+  int st = step_prologue(w, R, m, n, bb, ws, ws_bytes);
+  if (st) return st;
+  if (!U_out || !J_out || !isfinite(tau) || tau < 0.0 || bb > n) return EXTERND_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(launch_prep(w, h, s));
+  HIP_TRY(launch_stage(w, R, n, s));
+  HIP_TRY(launch_select(w, 0, bb, s));
+  HIP_TRY(launch_init(w, bb, tau, s));
+  HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
+  HIP_TRY(hipMemcpyAsync(J_out, w.J, sizeof(int32_t) * bb, hipMemcpyDeviceToDevice, s));
+  return EXTERND_OK;
+}
+
+int externd_step_vstep(const float* R, int64_t m, int64_t n, const int8_t* U, int32_t bb, double tau, int8_t* V_out,
+                       double* Y_out_or_null, void* ws, size_t ws_bytes, void* stream) {
+  Ws w{};
+  int st = step_prologue(w, R, m, n, bb, ws, ws_bytes);
+  if (st) return st;
+  if (!U || !V_out || !isfinite(tau) || tau < 0.0) return EXTERND_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(launch_prep(w, nullptr, s));
+  HIP_TRY(launch_stage(w, R, n, s));
+  HIP_TRY(launch_load_factor(w.Ut, w.Ur, U, m, w.m_pad, bb, s));
+  HIP_TRY(launch_vstep(w, 0, bb, tau, s));
+  HIP_TRY(launch_store_factor(V_out, w.Vt, n, w.n_pad, bb, s));
+  if (Y_out_or_null) {
+    // Y is bb x n: row c of the component-major buffer, pitch n_pad -> n
+    HIP_TRY(hipMemcpy2DAsync(Y_out_or_null, sizeof(double) * n, w.Y, sizeof(double) * w.n_pad, sizeof(double) * n,
+                             bb, hipMemcpyDeviceToDevice, s));
+  }
+  return EXTERND_OK;
+}
+
+int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, int32_t bb, double tau, const float* h,
+                       int8_t* U_out, double* Q_out_or_null, double* Z_out_or_null, void* ws, size_t ws_bytes,
+                       void* stream) {
+  Ws w{};
+  int st = step_prologue(w, R, m, n, bb, ws, ws_bytes);
+  if (st) return st;
+  if (!V || !U_out || !isfinite(tau) || tau < 0.0) return EXTERND_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(launch_prep(w, h, s));
+  HIP_TRY(launch_stage(w, R, n, s));
+  HIP_TRY(launch_load_factor(w.Vt, w.Vr, V, n, w.n_pad, bb, s));
+  HIP_TRY(launch_ustep(w, 0, bb, tau, h != nullptr, s));
+  HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
+  if (Q_out_or_null) HIP_TRY(launch_store_cm(Q_out_or_null, w.Q, m, w.m_pad, bb, s));
+  if (Z_out_or_null) HIP_TRY(launch_store_cm(Z_out_or_null, w.Z, m, w.m_pad, bb, s));
+  return EXTERND_OK;
+}
+
+int externd_step_scale(const int8_t* U, const int8_t* V, const double* Q, int64_t m, int64_t n, int32_t bb,
+                       const float* h, double* d_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!U || !V || !Q || !d_out || !ws || m < 1 || n < 1 || bb < 1 || bb > BBP) return EXTERND_EINVAL;
+  if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
+  Ws w{};
+  if (!carve(w, ws, ws_bytes, m, n, 0)) return EXTERND_EWORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(launch_prep(w, h, s));
+  HIP_TRY(launch_load_factor(w.Ut, w.Ur, U, m, w.m_pad, bb, s));
+  HIP_TRY(launch_load_factor(w.Vt, w.Vr, V, n, w.n_pad, bb, s));
+  HIP_TRY(launch_load_cm(w.Q, Q, m, w.m_pad, bb, s));
+  HIP_TRY(launch_gram_only(w, bb, h != nullptr, s));
+  HIP_TRY(launch_gvec(w, bb, s));
+  HIP_TRY(launch_scale(w, bb, s));
+  HIP_TRY(hipMemcpyAsync(d_out, w.dvec, sizeof(double) * bb, hipMemcpyDeviceToDevice, s));
+  return EXTERND_OK;
+}
+
+int externd_step_deflate(float* R, int64_t m, int64_t n, const int8_t* U, const int8_t* V, const double* d,
+                         int32_t bb, double* colnorm2_out, double* fro2_out, void* ws, size_t ws_bytes,
+                         void* stream) {
+  Ws w{};
+  int st = step_prologue(w, R, m, n, bb, ws, ws_bytes);
+  if (st) return st;
+  if (!U || !V || !d) return EXTERND_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(launch_prep(w, nullptr, s));
+  HIP_TRY(launch_stage(w, R, n, s));
+  HIP_TRY(launch_load_factor(w.Ut, w.Ur, U, m, w.m_pad, bb, s));
+  HIP_TRY(launch_load_factor(w.Vt, w.Vr, V, n, w.n_pad, bb, s));
+  HIP_TRY(launch_set_scales(w, d, bb, s));
+  HIP_TRY(launch_deflate(w, 0, s));
+  HIP_TRY(launch_unstage(w, R, s));
+  if (colnorm2_out || fro2_out) HIP_TRY(launch_colnorms(w, 0, colnorm2_out, fro2_out, s));
+  return EXTERND_OK;
+}
+
+}  // extern "C"

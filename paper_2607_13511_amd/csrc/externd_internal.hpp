@@ -1,0 +1,91 @@
+// Internal declarations shared by the kernels and the host orchestration.
+// Not part of the public ABI (see include/externd.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace externd {
+
+// Components of a block are padded to BBP; rows and columns of the residual
+// are padded to multiples of TILE (zero padding, never touched by updates).
+constexpr int BBP = 64;
+constexpr int TILE = 32;
+// Side workgroups that build Gram matrices next to a contraction.
+constexpr int NSIDE = 16;
+// Threads per workgroup for all kernels except the selection kernel.
+constexpr int NT = 256;
+constexpr int NT_SELECT = 1024;
+
+// Index of counters in Ws::counters (each used by one kernel family, reset
+// to zero by the workgroup that consumes it).
+enum Counter { CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2, CNT_COUNT = 8 };
+// Flags written by the device, read by the host.
+enum Flag { FLAG_NONFINITE = 0, FLAG_BADWEIGHT = 1, FLAG_COUNT = 4 };
+
+// Device workspace carved out of the caller's buffer.
+struct Ws {
+  int64_t m, n, m_pad, n_pad;
+  int nblk_cap;          // capacity of the per-block arrays (k + 2)
+  int gv;                // row groups of the V-step contraction
+  int gd;                // row groups of the deflation / staging passes
+
+  float* R;              // m_pad x n_pad residual, fp32, row-major
+  int8_t* Ut;            // BBP x m_pad, U transposed (component-major)
+  int8_t* Ur;            // m_pad x BBP, U row-major
+  int8_t* Vt;            // BBP x n_pad
+  int8_t* Vr;            // n_pad x BBP
+  double* Q;             // BBP x m_pad, Q = R diag(h) V  (component-major)
+  double* Z;             // BBP x m_pad, U-step target
+  long long* Pp;         // gv x BBP x n_pad, V-step partial contractions
+  double* Y;             // BBP x n_pad, V-step target
+  double* ginvU;         // BBP x BBP
+  double* ginvV;         // BBP x BBP
+  double* gramV;         // BBP x BBP raw V^T H V (no ridge)
+  double* gpart;         // NSIDE x BBP x BBP partial Gram matrices
+  int* gparti;           // NSIDE x BBP x BBP partial integer Grams
+  double* colE_part;     // gd x n_pad partial column energies
+  double* hw;            // n_pad: h~ (fp64), 1 when unweighted
+  double* gvec;          // BBP: diag(U^T Q)
+  double* dvec;          // BBP: joint scales (fp64)
+  float* dF;             // BBP: joint scales rounded to fp32
+  int* J;                // BBP: init columns
+  unsigned* maxbits;     // nblk_cap: max|R| (fp32 bits) before each block
+  unsigned* maxbits_w;   // nblk_cap: bound on max|R_ij h~_j| (fp32 bits)
+  double* fro2_hist;     // nblk_cap: ||R||^2 before each block, then after the last
+  double* fro2w_hist;    // nblk_cap: weighted ||R||^2
+  unsigned* counters;    // CNT_COUNT
+  int* flags;            // FLAG_COUNT
+};
+
+size_t workspace_bytes(int64_t m, int64_t n, int64_t k);
+bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k);
+
+// ---- launchers (all asynchronous on `s`) ----
+hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s);
+hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s);
+hipError_t launch_select(const Ws& w, int blk, int bb, hipStream_t s);
+hipError_t launch_finish(const Ws& w, int blk, hipStream_t s);
+hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s);
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s);
+hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s);
+hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
+hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s);
+hipError_t launch_emit(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp,
+                       float* D, hipStream_t s);
+// step-entry helpers
+hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, const int8_t* X, int64_t len, int64_t len_pad,
+                              int bb, hipStream_t s);
+hipError_t launch_store_factor(int8_t* X, const int8_t* Xt, int64_t len, int64_t len_pad, int bb, hipStream_t s);
+hipError_t launch_store_cm(double* X, const double* Xcm, int64_t len, int64_t len_pad, int bb,
+                           hipStream_t s);
+hipError_t launch_load_cm(double* Xcm, const double* X, int64_t len, int64_t len_pad, int bb,
+                          hipStream_t s);
+hipError_t launch_unstage(const Ws& w, float* A, hipStream_t s);
+hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2, hipStream_t s);
+hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s);
+hipError_t launch_gvec(const Ws& w, int bb, hipStream_t s);
+hipError_t launch_set_scales(const Ws& w, const double* d, int bb, hipStream_t s);
+
+}  // namespace externd

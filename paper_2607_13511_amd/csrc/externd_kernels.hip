@@ -1,0 +1,1393 @@
+// HIP kernels (gfx950) for the ExTernD greedy block-ALS factorization.
+//
+// Method (paper "ExTernD: Expanded-Rank Ternary Decomposition"):
+//   * T_tau ternarization, Eq. (2), Sec. 2.2;
+//   * block ALS with decorrelated targets, Eq. (3), Sec. 2.4, weighted per
+//     Sec. 2.5 (U-step on R diag(h~), V-step on the plain residual);
+//   * joint exact scale solve, Eq. (4);
+//   * block deflation R <- R - U diag(d) V^T, Sec. 2.4.
+//
+// Arithmetic design:
+//   * The two residual contractions (P = U^T R and Q = R diag(h~) V) run on
+//     int8 MFMA (v_mfma_i32_32x32x32_i8).  Each fp32 residual entry is
+//     scaled by 2^s (|x 2^s| <= 2^30, s from max|R|, or from max|R h~| for
+//     the weighted U-step) and rounded to a 32-bit integer, which is split
+//     into four signed 8-bit digits; the
+//     ternary operand is exact in int8.  The four digit planes accumulate
+//     separately in int32 and are combined in int64, so each contraction is
+//     exact for the fixed-point residual and independent of summation
+//     order.
+//   * Gram matrices of ternary factors are exact integers (int8 MFMA); the
+//     weighted Gram V^T diag(h~) V and all solves are fp64.
+//   * Targets Y, Z and the T_tau thresholds are fp64.
+//   * Deflation runs on bf16 MFMA: the ternary factors are exact in bf16
+//     and each fp32 scale d_c is split exactly into three bf16 parts;
+//     products accumulate in fp32.
+#include "externd.h"
+#include "externd_internal.hpp"
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+namespace externd {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef short v8s __attribute__((ext_vector_type(8)));
+
+// ---------------------------------------------------------------------------
+// small helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+// Fixed-point exponent: max|R| < 2^e  =>  s = 30 - e, so |x 2^s| < 2^30.
+__device__ __forceinline__ int fx_shift(unsigned maxbits) {
+  float mx = __uint_as_float(maxbits);
+  int e = 0;
+  if (mx > 0.0f) frexpf(mx, &e);
+  return 30 - e;
+}
+
+// x 2^s rounded to the nearest int32 (unbiased, so rounding errors do not
+// accumulate along fitted signs), biased so that every byte is a digit + 128
+// (bytes 0..2) or the signed top digit (byte 3).
+__device__ __forceinline__ unsigned fx_biased(float x, int s) {
+  return (unsigned)(int)__builtin_rintf(__builtin_amdgcn_ldexpf(x, s)) + 0x00808080u;
+}
+__device__ __forceinline__ unsigned fx_biased_w(float x, double fw) {
+  return (unsigned)(int)__builtin_rint((double)x * fw) + 0x00808080u;
+}
+
+// Upper bound (fp32) on |v| * hw for the weighted fixed-point scale: the
+// fp64 product rounded to fp32, inflated by 2^-20 so that rounding can never
+// make the bound smaller than the true value.
+__device__ __forceinline__ float weighted_abs_bound(float v, double hw) {
+  return (float)((double)fabsf(v) * hw) * 1.000001f;
+}
+
+// Byte-transpose four biased words into four digit planes:
+// plane p holds byte p of (y0, y1, y2, y3); planes 0..2 are re-centred
+// (xor 0x80 turns an unsigned digit+128 into the signed digit).
+__device__ __forceinline__ void planes4(unsigned y0, unsigned y1, unsigned y2, unsigned y3,
+                                        int& p0, int& p1, int& p2, int& p3) {
+  unsigned t0 = __builtin_amdgcn_perm(y1, y0, 0x05010400u);  // y0b0 y1b0 y0b1 y1b1
+  unsigned t1 = __builtin_amdgcn_perm(y1, y0, 0x07030602u);  // y0b2 y1b2 y0b3 y1b3
+  unsigned t2 = __builtin_amdgcn_perm(y3, y2, 0x05010400u);
+  unsigned t3 = __builtin_amdgcn_perm(y3, y2, 0x07030602u);
+  p0 = (int)(__builtin_amdgcn_perm(t2, t0, 0x05040100u) ^ 0x80808080u);
+  p1 = (int)(__builtin_amdgcn_perm(t2, t0, 0x07060302u) ^ 0x80808080u);
+  p2 = (int)(__builtin_amdgcn_perm(t3, t1, 0x05040100u) ^ 0x80808080u);
+  p3 = (int)__builtin_amdgcn_perm(t3, t1, 0x07060302u);
+}
+
+// 16 biased words (K slots 0..15 of one lane) -> 4 planes of 16 int8.
+__device__ __forceinline__ void make_planes(const unsigned (&y)[16], v4i (&P)[4]) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    int a, b, c, d;
+    planes4(y[4 * g], y[4 * g + 1], y[4 * g + 2], y[4 * g + 3], a, b, c, d);
+    P[0][g] = a;
+    P[1][g] = b;
+    P[2][g] = c;
+    P[3][g] = d;
+  }
+}
+
+__device__ __forceinline__ v16i mfma_i8(v4i a, v4i b, v16i c) {
+  return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+}
+
+// Deterministic reductions: fixed shuffle tree, lane 0 holds the result.
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ long long wave_sum_ll(long long v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, 64);
+  return v;
+}
+// max |x| with the smallest index on ties
+__device__ __forceinline__ void argmax_merge(double& v, long long& i, double v2, long long i2) {
+  if (v2 > v || (v2 == v && i2 < i)) {
+    v = v2;
+    i = i2;
+  }
+}
+__device__ __forceinline__ void wave_argmax(double& v, long long& i) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    double v2 = __shfl_down(v, o, 64);
+    long long i2 = __shfl_down(i, o, 64);
+    argmax_merge(v, i, v2, i2);
+  }
+}
+
+// Block-wide sum over NT threads, result broadcast to all threads.
+__device__ double block_sum_d(double v, double* sh /* >= NT/64 */) {
+  v = wave_sum_d(v);
+  if (lane_id() == 0) sh[wave_id()] = v;
+  __syncthreads();
+  double r = 0.0;
+  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) r += sh[w];
+  __syncthreads();
+  return r;
+}
+__device__ int block_sum_i(int v, int* sh) {
+  v = wave_sum_i(v);
+  if (lane_id() == 0) sh[wave_id()] = v;
+  __syncthreads();
+  int r = 0;
+  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) r += sh[w];
+  __syncthreads();
+  return r;
+}
+__device__ void block_argmax(double& v, long long& i, double* shv, long long* shi) {
+  wave_argmax(v, i);
+  if (lane_id() == 0) {
+    shv[wave_id()] = v;
+    shi[wave_id()] = i;
+  }
+  __syncthreads();
+  double bv = shv[0];
+  long long bi = shi[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) argmax_merge(bv, bi, shv[w], shi[w]);
+  __syncthreads();
+  v = bv;
+  i = bi;
+}
+
+// ---------------------------------------------------------------------------
+// 64x64 SPD inverse by the symmetric sweep operator (Gauss-Jordan without
+// pivoting, stable for SPD).  A: LDS 64x64 row-major, in: matrix, out:
+// inverse.  colbuf: LDS 2x64.  Requires blockDim.x == 256.  Each thread
+// keeps 16 entries (column j = tid % 64, rows tid / 64 + 4q) in registers;
+// the pivot column is published through LDS, one barrier per pivot.
+// ---------------------------------------------------------------------------
+__device__ void spd_inverse64(double* A, double* colbuf) {
+  const int t = threadIdx.x;
+  const int j = t & 63;
+  const int r0 = t >> 6;
+  double a[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) a[q] = A[(r0 + 4 * q) * 64 + j];
+  if (j == 0) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) colbuf[r0 + 4 * q] = a[q];
+  }
+  __syncthreads();
+  for (int k = 0; k < 64; ++k) {
+    const double* ck = colbuf + (k & 1) * 64;
+    const double inv = 1.0 / ck[k];
+    const double akj = ck[j];  // a_kj = a_jk (symmetric)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int i = r0 + 4 * q;
+      const double aik = ck[i];
+      double v;
+      if (i == k && j == k) v = -inv;
+      else if (i == k) v = akj * inv;
+      else if (j == k) v = aik * inv;
+      else v = a[q] - aik * akj * inv;
+      a[q] = v;
+    }
+    if (k + 1 < 64 && j == k + 1) {
+      double* cn = colbuf + ((k + 1) & 1) * 64;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) cn[r0 + 4 * q] = a[q];
+    }
+    __syncthreads();
+  }
+  // the sweep of every pivot leaves -A^{-1}
+#pragma unroll
+  for (int q = 0; q < 16; ++q) A[(r0 + 4 * q) * 64 + j] = -a[q];
+  __syncthreads();
+}
+
+// Turn the raw Gram (LDS, 64x64) of a block with bb real components into
+// (G + eps I) on the real block and the identity on the padding, invert,
+// and write the inverse.  Zero trace -> zero inverse on the real block
+// (every component is zero, Eq. (3) target is zero).
+__device__ void ridge_invert_store(double* G, double* colbuf, int bb, double* ginv_out) {
+  __shared__ double s_tr;
+  const int t = threadIdx.x;
+  if (t == 0) {
+    double tr = 0.0;
+    for (int c = 0; c < bb; ++c) tr += G[c * 64 + c];
+    s_tr = tr;
+  }
+  __syncthreads();
+  const double tr = s_tr;
+  const double eps = EXTERND_RIDGE_REL * tr / (double)bb;
+  for (int e = t; e < 4096; e += blockDim.x) {
+    const int r = e >> 6, c = e & 63;
+    if (r >= bb || c >= bb) G[e] = (r == c) ? 1.0 : 0.0;
+    else if (r == c) G[e] += eps;
+  }
+  __syncthreads();
+  if (tr == 0.0) {
+    for (int e = t; e < 4096; e += blockDim.x) {
+      const int r = e >> 6, c = e & 63;
+      ginv_out[e] = (r >= bb || c >= bb) ? ((r == c) ? 1.0 : 0.0) : 0.0;
+    }
+    return;
+  }
+  spd_inverse64(G, colbuf);
+  for (int e = t; e < 4096; e += blockDim.x) ginv_out[e] = G[e];
+}
+
+// ---------------------------------------------------------------------------
+// Gram matrices of a ternary factor, built by NSIDE workgroups
+// ---------------------------------------------------------------------------
+// Partial integer Gram of Tt (BBP x L int8, component-major) over this
+// workgroup's share of K steps, on int8 MFMA; all four wave results are
+// summed in LDS (integer adds, order-free) and written to gparti[side].
+// Returns true in the last of the NSIDE workgroups to finish, with the
+// complete Gram in G (LDS, fp64).
+__device__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side, int* gparti,
+                              unsigned* counter, double* G, int* ired /* LDS 4096 */) {
+  const int lane = lane_id(), wave = wave_id();
+  const int h = lane >> 5, l32 = lane & 31;
+  const int nks = (int)(L / TILE);
+  const int ks0 = (int)((long long)side * nks / NSIDE), ks1 = (int)((long long)(side + 1) * nks / NSIDE);
+  v16i acc00 = {}, acc01 = {}, acc10 = {}, acc11 = {};
+  for (int ks = ks0 + wave; ks < ks1; ks += 4) {
+    const int64_t i0 = (int64_t)ks * TILE + 16 * h;
+    const v4i a0 = *(const v4i*)(Tt + (int64_t)l32 * L + i0);
+    const v4i a1 = *(const v4i*)(Tt + (int64_t)(32 + l32) * L + i0);
+    acc00 = mfma_i8(a0, a0, acc00);
+    acc01 = mfma_i8(a0, a1, acc01);
+    acc10 = mfma_i8(a1, a0, acc10);
+    acc11 = mfma_i8(a1, a1, acc11);
+  }
+  for (int e = threadIdx.x; e < 4096; e += blockDim.x) ired[e] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int M = 8 * (r >> 2) + 4 * h + (r & 3);
+    const int N = l32;
+    atomicAdd(&ired[M * 64 + N], acc00[r]);
+    atomicAdd(&ired[M * 64 + 32 + N], acc01[r]);
+    atomicAdd(&ired[(32 + M) * 64 + N], acc10[r]);
+    atomicAdd(&ired[(32 + M) * 64 + 32 + N], acc11[r]);
+  }
+  __syncthreads();
+  int* mine = gparti + (size_t)side * 4096;
+  for (int e = threadIdx.x; e < 4096; e += blockDim.x) mine[e] = ired[e];
+  __threadfence();
+  __syncthreads();
+  __shared__ int s_last;
+  if (threadIdx.x == 0) {
+    const unsigned old = atomicAdd(counter, 1u);
+    s_last = (old == (unsigned)(NSIDE - 1));
+  }
+  __syncthreads();
+  if (!s_last) return false;
+  __threadfence();
+  for (int e = threadIdx.x; e < 4096; e += blockDim.x) {
+    long long s = 0;
+    for (int q = 0; q < NSIDE; ++q) s += __builtin_nontemporal_load(gparti + (size_t)q * 4096 + e);
+    G[e] = (double)s;
+  }
+  if (threadIdx.x == 0) *counter = 0u;
+  __syncthreads();
+  return true;
+}
+
+// Partial weighted Gram V^T diag(hw) V over this workgroup's share of rows
+// of Vr (n_pad x BBP int8, row-major), fp64 VALU.  Thread t owns the 4x4
+// block (4*(t/16)+a, 4*(t%16)+b).  Same last-workgroup protocol.
+__device__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restrict__ hw, int64_t L,
+                            int side, double* gpart, unsigned* counter, double* G) {
+  const int t = threadIdx.x;
+  const int cb = t >> 4, cc = t & 15;
+  const int64_t j0 = (int64_t)side * L / NSIDE, j1 = (int64_t)(side + 1) * L / NSIDE;
+  double acc[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) acc[q] = 0.0;
+  for (int64_t j = j0; j < j1; ++j) {
+    const unsigned ua = *(const unsigned*)(Vr + j * BBP + 4 * cb);
+    const unsigned ub = *(const unsigned*)(Vr + j * BBP + 4 * cc);
+    const double w = hw[j];
+    double va[4], vb[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      va[e] = w * (double)(signed char)((ua >> (8 * e)) & 0xff);
+      vb[e] = (double)(signed char)((ub >> (8 * e)) & 0xff);
+    }
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a * 4 + b] += va[a] * vb[b];
+  }
+  double* mine = gpart + (size_t)side * 4096;
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) mine[(4 * cb + a) * 64 + 4 * cc + b] = acc[a * 4 + b];
+  __threadfence();
+  __syncthreads();
+  __shared__ int s_last;
+  if (t == 0) {
+    const unsigned old = atomicAdd(counter, 1u);
+    s_last = (old == (unsigned)(NSIDE - 1));
+  }
+  __syncthreads();
+  if (!s_last) return false;
+  __threadfence();
+  for (int e = t; e < 4096; e += blockDim.x) {
+    double s = 0.0;
+    for (int q = 0; q < NSIDE; ++q) s += __builtin_nontemporal_load(gpart + (size_t)q * 4096 + e);
+    G[e] = s;
+  }
+  if (t == 0) *counter = 0u;
+  __syncthreads();
+  return true;
+}
+
+// Integer-plane reduction of the 4 waves' MFMA accumulators into LDS.
+// red layout: [plane][tile][M * 33 + N] int32 (33-word row pitch).
+constexpr int RED_TILE = 32 * 33;
+__device__ __forceinline__ void reduce_planes(int* red, const v16i (&acc)[2][4]) {
+  const int lane = lane_id();
+  const int h = lane >> 5, l32 = lane & 31;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int M = 8 * (r >> 2) + 4 * h + (r & 3);
+        atomicAdd(&red[(p * 2 + t) * RED_TILE + M * 33 + l32], acc[t][p][r]);
+      }
+}
+__device__ __forceinline__ long long combine_planes(const int* red, int t, int M, int N) {
+  const int o = M * 33 + N;
+  return (long long)red[(0 * 2 + t) * RED_TILE + o] + ((long long)red[(1 * 2 + t) * RED_TILE + o] << 8) +
+         ((long long)red[(2 * 2 + t) * RED_TILE + o] << 16) + ((long long)red[(3 * 2 + t) * RED_TILE + o] << 24);
+}
+
+// ---------------------------------------------------------------------------
+// V-step contraction P = U^T R  (Eq. (3), first half)
+// grid: NSIDE side WGs (Gram U^T U + ridge + inverse) followed by
+//       (n_pad/32 column tiles) x gv row groups.
+// Each WG owns 32 columns and a contiguous range of 32-row K steps, split
+// over its 4 waves; A = Ut (components x rows), B = R digit planes.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void k_vstep(const float* __restrict__ R, const int8_t* __restrict__ Ut,
+                                              long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
+                                              int64_t m_pad, int64_t n_pad, int gv, int bb, int* gparti,
+                                              unsigned* counter, double* ginvU) {
+  __shared__ int red[8 * RED_TILE];
+  __shared__ double Gs[4096];
+  __shared__ double colbuf[128];
+  if (blockIdx.x < NSIDE) {
+    if (side_gram_int(Ut, m_pad, blockIdx.x, gparti, counter, Gs, red)) ridge_invert_store(Gs, colbuf, bb, ginvU);
+    return;
+  }
+  const int b = blockIdx.x - NSIDE;
+  const int nct = (int)(n_pad / TILE);
+  const int ct = b % nct, g = b / nct;
+  const int nks = (int)(m_pad / TILE);
+  const int ks0 = (int)((long long)g * nks / gv), ks1 = (int)((long long)(g + 1) * nks / gv);
+  const int lane = lane_id(), wave = wave_id();
+  const int h = lane >> 5, l32 = lane & 31;
+  const int s = fx_shift(*maxbits);
+  v16i acc[2][4];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) acc[t][p] = v16i{};
+  const float* Rc = R + (int64_t)ct * TILE + l32;
+  for (int ks = ks0 + wave; ks < ks1; ks += 4) {
+    const int64_t i0 = (int64_t)ks * TILE + 16 * h;
+    const v4i a0 = *(const v4i*)(Ut + (int64_t)l32 * m_pad + i0);
+    const v4i a1 = *(const v4i*)(Ut + (int64_t)(32 + l32) * m_pad + i0);
+    unsigned y[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) y[q] = fx_biased(Rc[(i0 + q) * n_pad], s);
+    v4i P[4];
+    make_planes(y, P);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      acc[0][p] = mfma_i8(a0, P[p], acc[0][p]);
+      acc[1][p] = mfma_i8(a1, P[p], acc[1][p]);
+    }
+  }
+  for (int e = threadIdx.x; e < 8 * RED_TILE; e += NT) red[e] = 0;
+  __syncthreads();
+  reduce_planes(red, acc);
+  __syncthreads();
+  // out[t][M = component][N = column]
+  for (int e = threadIdx.x; e < 2048; e += NT) {
+    const int t = e >> 10, rem = e & 1023, M = rem >> 5, N = rem & 31;
+    Pp[((int64_t)g * BBP + 32 * t + M) * n_pad + (int64_t)ct * TILE + N] = combine_planes(red, t, M, N);
+  }
+  (void)bb;
+}
+
+// ---------------------------------------------------------------------------
+// U-step contraction Q = R diag(h~) V  (Eq. (3) second half, Sec. 2.5)
+// grid: NSIDE side WGs (Gram V^T H V + ridge + inverse, raw Gram kept for
+//       the scale solve) followed by m_pad/32 row tiles.
+// Each WG owns 32 full rows; its 4 waves interleave 32-column K steps.
+// A = R digit planes (rows x columns), B = Vt (columns x components).
+// ---------------------------------------------------------------------------
+template <bool WEIGHTED>
+__global__ __launch_bounds__(NT) void k_ustep(const float* __restrict__ R, const int8_t* __restrict__ Vt,
+                                              const int8_t* __restrict__ Vr, const double* __restrict__ hw,
+                                              double* __restrict__ Q, const unsigned* __restrict__ maxbits,
+                                              int64_t m_pad, int64_t n_pad, int bb, int* gparti, double* gpart,
+                                              unsigned* counter, double* ginvV, double* gramV) {
+  __shared__ int red[8 * RED_TILE];
+  __shared__ double Gs[4096];
+  __shared__ double colbuf[128];
+  if (blockIdx.x < NSIDE) {
+    bool last;
+    if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, gpart, counter, Gs);
+    else last = side_gram_int(Vt, n_pad, blockIdx.x, gparti, counter, Gs, red);
+    if (last) {
+      for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
+      __syncthreads();
+      ridge_invert_store(Gs, colbuf, bb, ginvV);
+    }
+    return;
+  }
+  const int rt = blockIdx.x - NSIDE;
+  const int lane = lane_id(), wave = wave_id();
+  const int h = lane >> 5, l32 = lane & 31;
+  const int s = fx_shift(*maxbits);
+  v16i acc[2][4];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) acc[t][p] = v16i{};
+  const float* Rrow = R + ((int64_t)rt * TILE + l32) * n_pad;
+  const int nks = (int)(n_pad / TILE);
+  for (int ks = wave; ks < nks; ks += 4) {
+    const int64_t j0 = (int64_t)ks * TILE + 16 * h;
+    const float4* src = (const float4*)(Rrow + j0);
+    float x[16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = src[q];
+      x[4 * q] = v.x;
+      x[4 * q + 1] = v.y;
+      x[4 * q + 2] = v.z;
+      x[4 * q + 3] = v.w;
+    }
+    unsigned y[16];
+    if (WEIGHTED) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) y[q] = fx_biased_w(x[q], ldexp(hw[j0 + q], s));
+    } else {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) y[q] = fx_biased(x[q], s);
+    }
+    v4i P[4];
+    make_planes(y, P);
+    const v4i b0 = *(const v4i*)(Vt + (int64_t)l32 * n_pad + j0);
+    const v4i b1 = *(const v4i*)(Vt + (int64_t)(32 + l32) * n_pad + j0);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      acc[0][p] = mfma_i8(P[p], b0, acc[0][p]);
+      acc[1][p] = mfma_i8(P[p], b1, acc[1][p]);
+    }
+  }
+  for (int e = threadIdx.x; e < 8 * RED_TILE; e += NT) red[e] = 0;
+  __syncthreads();
+  reduce_planes(red, acc);
+  __syncthreads();
+  // out[t][M = row][N = component] -> Q[32t + N][row]
+  for (int e = threadIdx.x; e < 2048; e += NT) {
+    const int t = e >> 10, rem = e & 1023, N = rem >> 5, M = rem & 31;
+    const long long v = combine_planes(red, t, M, N);
+    Q[(int64_t)(32 * t + N) * m_pad + (int64_t)rt * TILE + M] = ldexp((double)v, -s);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// V-step target Y = G_U^{-1} P (fp64); P summed over the gv row groups
+// (int64, exact) and scaled back by 2^-s.  grid: n_pad/32 column tiles.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void k_vepi(const long long* __restrict__ Pp, int gv,
+                                             const double* __restrict__ ginv, double* __restrict__ Y,
+                                             const unsigned* __restrict__ maxbits, int64_t n_pad) {
+  __shared__ double Ps[64][33];
+  __shared__ double Gi[64][65];
+  const int64_t j0 = (int64_t)blockIdx.x * TILE;
+  const int s = fx_shift(*maxbits);
+  for (int e = threadIdx.x; e < 64 * 32; e += NT) {
+    const int c = e >> 5, jj = e & 31;
+    long long acc = 0;
+    for (int g = 0; g < gv; ++g) acc += Pp[((int64_t)g * BBP + c) * n_pad + j0 + jj];
+    Ps[c][jj] = ldexp((double)acc, -s);
+  }
+  for (int e = threadIdx.x; e < 4096; e += NT) Gi[e >> 6][e & 63] = ginv[e];
+  __syncthreads();
+  const int jj = threadIdx.x & 31, cg = threadIdx.x >> 5;
+  double y[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) y[q] = 0.0;
+  for (int c2 = 0; c2 < 64; ++c2) {
+    const double p = Ps[c2][jj];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) y[q] += Gi[8 * cg + q][c2] * p;
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) Y[(int64_t)(8 * cg + q) * n_pad + j0 + jj] = y[q];
+}
+
+// U-step target Z = Q G_V^{-1} (fp64).  grid: m_pad/32 row tiles.
+__global__ __launch_bounds__(NT) void k_uepi(const double* __restrict__ Q, const double* __restrict__ ginv,
+                                             double* __restrict__ Z, int64_t m_pad) {
+  __shared__ double Qs[64][33];
+  __shared__ double Gi[64][65];
+  const int64_t i0 = (int64_t)blockIdx.x * TILE;
+  for (int e = threadIdx.x; e < 64 * 32; e += NT) {
+    const int c = e >> 5, ii = e & 31;
+    Qs[c][ii] = Q[(int64_t)c * m_pad + i0 + ii];
+  }
+  for (int e = threadIdx.x; e < 4096; e += NT) Gi[e >> 6][e & 63] = ginv[e];
+  __syncthreads();
+  const int ii = threadIdx.x & 31, cg = threadIdx.x >> 5;
+  double z[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) z[q] = 0.0;
+  for (int c2 = 0; c2 < 64; ++c2) {
+    const double qv = Qs[c2][ii];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) z[q] += qv * Gi[c2][8 * cg + q];
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) Z[(int64_t)(8 * cg + q) * m_pad + i0 + ii] = z[q];
+}
+
+// ---------------------------------------------------------------------------
+// T_tau of one component per workgroup (Eq. (2)): theta = tau * mean|x|
+// over the true length L (fp64), strict ">", keep the largest |x| (smallest
+// index) when nothing passes.  Writes the trits component-major
+// (dst[0 .. L_pad)), zero beyond L.
+// ---------------------------------------------------------------------------
+template <typename Load>
+__device__ void ternarize_wg(Load load, int64_t L, int64_t L_pad, double tau, int8_t* dst, int* nnz_out) {
+  __shared__ double shd[16];
+  __shared__ long long shl[16];
+  __shared__ int shi[16];
+  double sabs = 0.0, mx = -1.0;
+  long long imx = 0;
+  for (int64_t i = threadIdx.x; i < L; i += blockDim.x) {
+    const double x = load(i);
+    const double a = fabs(x);
+    sabs += a;
+    argmax_merge(mx, imx, a, i);
+  }
+  const double S = block_sum_d(sabs, shd);
+  block_argmax(mx, imx, shd, shl);
+  const double theta = tau * (S / (double)L);
+  int nnz = 0;
+  for (int64_t i = threadIdx.x; i < L_pad; i += blockDim.x) {
+    int8_t t = 0;
+    if (i < L) {
+      const double x = load(i);
+      if (fabs(x) > theta) t = (x > 0.0) ? 1 : -1;
+    }
+    nnz += (t != 0);
+    dst[i] = t;
+  }
+  nnz = block_sum_i(nnz, shi);
+  if (nnz == 0 && threadIdx.x == 0 && L > 0) {
+    const double x = load(imx);
+    const int8_t t = (x > 0.0) ? 1 : ((x < 0.0) ? -1 : 0);
+    dst[imx] = t;
+    nnz = (t != 0);
+  }
+  if (nnz_out && threadIdx.x == 0) *nnz_out = nnz;
+  __syncthreads();
+}
+
+// V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.  grid: BBP.
+__global__ __launch_bounds__(NT) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb,
+                                               double tau, int8_t* __restrict__ Vt) {
+  const int c = blockIdx.x;
+  int8_t* dst = Vt + (int64_t)c * n_pad;
+  if (c >= bb) {
+    for (int64_t j = threadIdx.x; j < n_pad; j += NT) dst[j] = 0;
+    return;
+  }
+  const double* y = Y + (int64_t)c * n_pad;
+  ternarize_wg([=](int64_t j) { return y[j]; }, n, n_pad, tau, dst, nullptr);
+}
+
+// U <- T_tau(Z[:, c]); also g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for
+// the joint scale solve (Eq. (4)).  grid: BBP.
+__global__ __launch_bounds__(NT) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q,
+                                               int64_t m, int64_t m_pad, int bb, double tau,
+                                               int8_t* __restrict__ Ut, double* __restrict__ gvec) {
+  __shared__ double shd[16];
+  const int c = blockIdx.x;
+  int8_t* dst = Ut + (int64_t)c * m_pad;
+  if (c >= bb) {
+    for (int64_t i = threadIdx.x; i < m_pad; i += NT) dst[i] = 0;
+    if (threadIdx.x == 0) gvec[c] = 0.0;
+    return;
+  }
+  const double* z = Z + (int64_t)c * m_pad;
+  ternarize_wg([=](int64_t i) { return z[i]; }, m, m_pad, tau, dst, nullptr);
+  const double* q = Q + (int64_t)c * m_pad;
+  double acc = 0.0;
+  for (int64_t i = threadIdx.x; i < m; i += NT) acc += (double)dst[i] * q[i];
+  acc = block_sum_d(acc, shd);
+  if (threadIdx.x == 0) gvec[c] = acc;
+}
+
+// Block initialisation (paper silent; reading: U[:, c] = T_tau(R[:, J_c])).
+// grid: BBP.
+__global__ __launch_bounds__(NT) void k_init(const float* __restrict__ R, const int* __restrict__ J, int64_t m,
+                                             int64_t m_pad, int64_t n_pad, int bb, double tau,
+                                             int8_t* __restrict__ Ut) {
+  const int c = blockIdx.x;
+  int8_t* dst = Ut + (int64_t)c * m_pad;
+  if (c >= bb) {
+    for (int64_t i = threadIdx.x; i < m_pad; i += NT) dst[i] = 0;
+    return;
+  }
+  int jc = J[c];
+  jc = jc < 0 ? 0 : (jc >= n_pad ? (int)(n_pad - 1) : jc);  // J comes from k_select; keep reads in bounds
+  const float* col = R + jc;
+  ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, m, m_pad, tau, dst, nullptr);
+}
+
+// Xt (BBP x L int8, component-major) -> Xr (L x BBP, row-major).
+// grid: L/32 chunks.
+__global__ __launch_bounds__(NT) void k_transpose8(const int8_t* __restrict__ Xt, int8_t* __restrict__ Xr,
+                                                   int64_t L) {
+  __shared__ int8_t tile[32][BBP + 4];
+  const int64_t j0 = (int64_t)blockIdx.x * 32;
+  for (int e = threadIdx.x; e < BBP * 32; e += NT) {
+    const int c = e >> 5, jj = e & 31;
+    tile[jj][c] = Xt[(int64_t)c * L + j0 + jj];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < BBP * 32; e += NT) {
+    const int jj = e >> 6, c = e & 63;
+    Xr[(j0 + jj) * BBP + c] = tile[jj][c];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Joint scale solve, Eq. (4): M = (U^T U) o (V^T H V) (+ delta I),
+// d = M^{-1} g.  grid: NSIDE (partial U^T U on int8 MFMA, last WG solves).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void k_scale(const int8_t* __restrict__ Ut, int64_t m_pad, int bb,
+                                              const double* __restrict__ gramV, const double* __restrict__ gvec,
+                                              int* gparti, unsigned* counter, double* dvec, float* dF,
+                                              float* Dout) {
+  __shared__ int red[4096];
+  __shared__ double Gs[4096];
+  __shared__ double colbuf[128];
+  __shared__ double s_tr;
+  if (!side_gram_int(Ut, m_pad, blockIdx.x, gparti, counter, Gs, red)) return;
+  const int t = threadIdx.x;
+  for (int e = t; e < 4096; e += NT) {
+    const int r = e >> 6, c = e & 63;
+    Gs[e] = (r < bb && c < bb) ? Gs[e] * gramV[e] : ((r == c) ? 1.0 : 0.0);
+  }
+  __syncthreads();
+  if (t == 0) {
+    double tr = 0.0;
+    for (int c = 0; c < bb; ++c) tr += Gs[c * 64 + c];
+    s_tr = tr;
+  }
+  __syncthreads();
+  const double tr = s_tr;
+  if (tr == 0.0) {
+    if (t < BBP) {
+      dvec[t] = 0.0;
+      dF[t] = 0.0f;
+      if (Dout && t < bb) Dout[t] = 0.0f;
+    }
+    return;
+  }
+  const double delta = EXTERND_SCALE_GUARD_REL * tr / (double)bb;
+  if (t < bb) Gs[t * 64 + t] += delta;
+  __syncthreads();
+  spd_inverse64(Gs, colbuf);
+  if (t < BBP) {
+    double d = 0.0;
+    if (t < bb)
+      for (int c = 0; c < bb; ++c) d += Gs[t * 64 + c] * gvec[c];
+    dvec[t] = d;
+    dF[t] = (float)d;
+    if (Dout && t < bb) Dout[t] = (float)d;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Deflation R <- R - U diag(d) V^T on bf16 MFMA (Sec. 2.4), fused with the
+// column energies ||R_:j||^2 (fp64 partials per row group) and max|R|.
+// grid: (n_pad/32 column strips) x gd row groups; each wave takes 32-row
+// tiles of its WG's group.  B = d-weighted V (3 exact bf16 parts of d),
+// A = U (exact bf16).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ unsigned short bf16_bits_trunc(float x) { return (unsigned short)(__float_as_uint(x) >> 16); }
+__device__ __forceinline__ float bf16_to_f(unsigned short b) { return __uint_as_float((unsigned)b << 16); }
+__device__ __forceinline__ short tern_bf16(int8_t t, unsigned short mag) {
+  // t in {-1, 0, 1}: 0 -> +0, 1 -> mag, -1 -> mag with the sign bit flipped
+  return (short)(t == 0 ? 0 : (t > 0 ? mag : (unsigned short)(mag ^ 0x8000u)));
+}
+
+__global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const int8_t* __restrict__ Ur,
+                                                const int8_t* __restrict__ Vr, const float* __restrict__ dF,
+                                                double* __restrict__ colE_part, unsigned* __restrict__ maxbits_next,
+                                                unsigned* __restrict__ maxbits_w_next, const double* __restrict__ hw,
+                                                int64_t m_pad, int64_t n_pad, int gd) {
+  __shared__ double colsum[4][32];
+  __shared__ float wmax[4];
+  __shared__ float wmaxw[4];
+  const int nct = (int)(n_pad / TILE);
+  const int ct = blockIdx.x % nct, g = blockIdx.x / nct;
+  const int nrt = (int)(m_pad / TILE);
+  const int rt0 = (int)((long long)g * nrt / gd), rt1 = (int)((long long)(g + 1) * nrt / gd);
+  const int lane = lane_id(), wave = wave_id();
+  const int h = lane >> 5, l32 = lane & 31;
+  const int64_t col = (int64_t)ct * TILE + l32;
+  // B fragments: lane (h, col) holds components 16 ks + 8 h + e.
+  v8s Bf[3][4];
+  {
+    const int8_t* vrow = Vr + col * BBP;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int c = 16 * ks + 8 * h + e;
+        const float d = dF[c];
+        const unsigned short hi = bf16_bits_trunc(d);
+        const float r1 = d - bf16_to_f(hi);
+        const unsigned short mi = bf16_bits_trunc(r1);
+        const float r2 = r1 - bf16_to_f(mi);
+        const unsigned short lo = bf16_bits_trunc(r2);
+        const int8_t v = vrow[c];
+        Bf[0][ks][e] = tern_bf16(v, hi);
+        Bf[1][ks][e] = tern_bf16(v, mi);
+        Bf[2][ks][e] = tern_bf16(v, lo);
+      }
+    }
+  }
+  double csum = 0.0;
+  float vmax = 0.0f;
+  for (int rt = rt0 + wave; rt < rt1; rt += 4) {
+    const int64_t i0 = (int64_t)rt * TILE;
+    const int8_t* urow = Ur + (i0 + l32) * BBP;
+    v16f acc = {};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint2 uu = *(const uint2*)(urow + 16 * ks + 8 * h);
+      v8s Af;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const unsigned word = (e < 4) ? uu.x : uu.y;
+        const int8_t t = (int8_t)((word >> (8 * (e & 3))) & 0xff);
+        Af[e] = tern_bf16(t, (unsigned short)0x3F80u);
+      }
+#pragma unroll
+      for (int p = 0; p < 3; ++p)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, Af), __builtin_bit_cast(v8bf, Bf[p][ks]),
+                                                      acc, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 8 * (r >> 2) + 4 * h + (r & 3);
+      float* p = R + (i0 + row) * n_pad + col;
+      const float v = *p - acc[r];
+      *p = v;
+      csum += (double)v * (double)v;
+      vmax = fmaxf(vmax, fabsf(v));
+    }
+  }
+  // combine the two half-waves (same column), then the 4 waves in order
+  csum += __shfl_down(csum, 32, 64);
+  float vmaxw = weighted_abs_bound(vmax, hw[col]);
+  for (int o = 32; o > 0; o >>= 1) {
+    vmax = fmaxf(vmax, __shfl_down(vmax, o, 64));
+    vmaxw = fmaxf(vmaxw, __shfl_down(vmaxw, o, 64));
+  }
+  if (h == 0) colsum[wave][l32] = csum;
+  if (lane == 0) {
+    wmax[wave] = vmax;
+    wmaxw[wave] = vmaxw;
+  }
+  __syncthreads();
+  if (threadIdx.x < 32) {
+    const double s = ((colsum[0][threadIdx.x] + colsum[1][threadIdx.x]) + colsum[2][threadIdx.x]) + colsum[3][threadIdx.x];
+    colE_part[(int64_t)g * n_pad + (int64_t)ct * TILE + threadIdx.x] = s;
+  }
+  if (threadIdx.x == 0) {
+    const float mx = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+    const float mxw = fmaxf(fmaxf(wmaxw[0], wmaxw[1]), fmaxf(wmaxw[2], wmaxw[3]));
+    atomicMax(maxbits_next, __float_as_uint(mx));
+    atomicMax(maxbits_w_next, __float_as_uint(mxw));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Staging: R <- A (zero padded), column energies (fp64 partials), max|A|,
+// non-finite detection.  grid: (n_pad/32) x gd; thread (row lane, column).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64_t lda, int64_t m, int64_t n,
+                                              float* __restrict__ R, double* __restrict__ colE_part,
+                                              unsigned* __restrict__ maxbits0, unsigned* __restrict__ maxbits_w0,
+                                              const double* __restrict__ hw, int* flags, int64_t m_pad,
+                                              int64_t n_pad, int gd) {
+  __shared__ double colsum[8][32];
+  __shared__ float smax[NT / 64];
+  __shared__ float smaxw[NT / 64];
+  const int nct = (int)(n_pad / TILE);
+  const int ct = blockIdx.x % nct, g = blockIdx.x / nct;
+  const int64_t r0 = (int64_t)g * m_pad / gd, r1 = (int64_t)(g + 1) * m_pad / gd;
+  const int cl = threadIdx.x & 31, rl = threadIdx.x >> 5;
+  const int64_t j = (int64_t)ct * TILE + cl;
+  double cs = 0.0;
+  float vmax = 0.0f;
+  int bad = 0;
+  const double hwj = hw[j];
+  for (int64_t i = r0 + rl; i < r1; i += 8) {
+    float v = 0.0f;
+    if (i < m && j < n) v = A[i * lda + j];
+    if (!isfinite(v)) {
+      bad = 1;
+      v = 0.0f;
+    }
+    R[i * n_pad + j] = v;
+    cs += (double)v * (double)v;
+    vmax = fmaxf(vmax, fabsf(v));
+  }
+  colsum[rl][cl] = cs;
+  float vmaxw = weighted_abs_bound(vmax, hwj);
+  for (int o = 32; o > 0; o >>= 1) {
+    vmax = fmaxf(vmax, __shfl_down(vmax, o, 64));
+    vmaxw = fmaxf(vmaxw, __shfl_down(vmaxw, o, 64));
+  }
+  if (lane_id() == 0) {
+    smax[wave_id()] = vmax;
+    smaxw[wave_id()] = vmaxw;
+  }
+  if (bad) flags[FLAG_NONFINITE] = 1;
+  __syncthreads();
+  if (threadIdx.x < 32) {
+    double s = 0.0;
+    for (int q = 0; q < 8; ++q) s += colsum[q][threadIdx.x];
+    colE_part[(int64_t)g * n_pad + j] = s;
+  }
+  if (threadIdx.x == 0) {
+    float mx = 0.0f, mxw = 0.0f;
+    for (int w = 0; w < NT / 64; ++w) {
+      mx = fmaxf(mx, smax[w]);
+      mxw = fmaxf(mxw, smaxw[w]);
+    }
+    atomicMax(maxbits0, __float_as_uint(mx));
+    atomicMax(maxbits_w0, __float_as_uint(mxw));
+  }
+}
+
+// R (padded) -> A (m x n, row-major)
+__global__ __launch_bounds__(NT) void k_unstage(const float* __restrict__ R, float* __restrict__ A, int64_t m,
+                                                int64_t n, int64_t n_pad) {
+  const int64_t total = m * n;
+  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
+    const int64_t i = e / n, j = e % n;
+    A[e] = R[i * n_pad + j];
+  }
+}
+
+// Weights and bookkeeping (1 WG): h~ = h / max(h) in fp64 (ones when no
+// weights), zero padding; clear counters, flags and the per-block arrays.
+__global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_t n, int64_t n_pad,
+                                             double* __restrict__ hw, unsigned* maxbits, unsigned* maxbits_w,
+                                             double* fro2_hist, double* fro2w_hist, int nblk_cap,
+                                             unsigned* counters, int* flags) {
+  __shared__ float smax[NT / 64];
+  __shared__ int sbad[NT / 64];
+  for (int e = threadIdx.x; e < nblk_cap; e += NT) {
+    maxbits[e] = 0u;
+    maxbits_w[e] = 0u;
+    fro2_hist[e] = 0.0;
+    fro2w_hist[e] = 0.0;
+  }
+  if (threadIdx.x < CNT_COUNT) counters[threadIdx.x] = 0u;
+  if (threadIdx.x < FLAG_COUNT) flags[threadIdx.x] = 0;
+  if (!h) {
+    for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? 1.0 : 0.0;
+    return;
+  }
+  float mx = 0.0f;
+  int bad = 0;
+  for (int64_t j = threadIdx.x; j < n; j += NT) {
+    const float v = h[j];
+    if (!isfinite(v) || v < 0.0f) bad = 1;
+    else mx = fmaxf(mx, v);
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    mx = fmaxf(mx, __shfl_down(mx, o, 64));
+    bad |= __shfl_down(bad, o, 64);
+  }
+  if (lane_id() == 0) {
+    smax[wave_id()] = mx;
+    sbad[wave_id()] = bad;
+  }
+  __syncthreads();
+  float gmx = 0.0f;
+  int gbad = 0;
+  for (int w = 0; w < NT / 64; ++w) {
+    gmx = fmaxf(gmx, smax[w]);
+    gbad |= sbad[w];
+  }
+  if (!(gmx > 0.0f)) gbad = 1;
+  if (gbad) {
+    if (threadIdx.x == 0) flags[FLAG_BADWEIGHT] = 1;
+    for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? 1.0 : 0.0;
+    return;
+  }
+  const double dm = (double)gmx;
+  for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? (double)h[j] / dm : 0.0;
+}
+
+// ---------------------------------------------------------------------------
+// Column energies -> ||R||^2 history and the top-bb selection (1 WG,
+// NT_SELECT threads).  key_j = h~_j ||R_:j||^2 (fp64, >= 0, so its bit
+// pattern orders like the value); exact radix select of the bb-th largest
+// key, ties broken towards the smaller column index.
+// ---------------------------------------------------------------------------
+__device__ void reduce_colE(const double* __restrict__ colE_part, int gd, int64_t n, int64_t n_pad,
+                            const double* __restrict__ hw, double* colE, double* out_fro2, double* out_fro2w,
+                            double* shd) {
+  double s = 0.0, sw = 0.0;
+  for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
+    double c = 0.0;
+    for (int g = 0; g < gd; ++g) c += colE_part[(int64_t)g * n_pad + j];
+    if (j >= n) c = 0.0;
+    if (colE && j < n) colE[j] = c;
+    s += c;
+    sw += hw[j] * c;
+  }
+  s = block_sum_d(s, shd);
+  sw = block_sum_d(sw, shd);
+  if (threadIdx.x == 0) {
+    *out_fro2 = s;
+    if (out_fro2w) *out_fro2w = sw;
+  }
+}
+
+__global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__ colE_part, int gd, int64_t n,
+                                                      int64_t n_pad, const double* __restrict__ hw,
+                                                      double* keys /* n_pad scratch */, double* fro2_out,
+                                                      double* fro2w_out, int bb, int* __restrict__ J) {
+  __shared__ double shd[16];
+  __shared__ unsigned hist[256];
+  __shared__ unsigned long long s_prefix;
+  __shared__ int s_need;
+  __shared__ int s_cnt;
+  __shared__ unsigned long long cand_key[BBP];
+  __shared__ int cand_idx[BBP];
+  __shared__ int s_scan[NT_SELECT / 64];
+  if (threadIdx.x < BBP) {
+    cand_key[threadIdx.x] = 0ull;
+    cand_idx[threadIdx.x] = 0;
+  }
+  reduce_colE(colE_part, gd, n, n_pad, hw, keys, fro2_out, fro2w_out, shd);
+  __syncthreads();
+  for (int64_t j = threadIdx.x; j < n; j += blockDim.x) keys[j] = hw[j] * keys[j];
+  __syncthreads();
+  // radix select over the 64-bit patterns, 8 bits at a time from the top
+  if (threadIdx.x == 0) {
+    s_prefix = 0ull;
+    s_need = bb;
+  }
+  __syncthreads();
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+    for (int e = threadIdx.x; e < 256; e += blockDim.x) hist[e] = 0u;
+    __syncthreads();
+    const unsigned long long prefix = s_prefix;
+    const unsigned long long hmask = (pass == 0) ? 0ull : (~0ull << (shift + 8));
+    for (int64_t j = threadIdx.x; j < n; j += blockDim.x) {
+      const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
+      if ((kb & hmask) == prefix) atomicAdd(&hist[(kb >> shift) & 0xff], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int need = s_need;
+      int d = 255;
+      for (; d > 0; --d) {
+        if ((int)hist[d] >= need) break;
+        need -= (int)hist[d];
+      }
+      s_need = need;
+      s_prefix = prefix | ((unsigned long long)d << shift);
+    }
+    __syncthreads();
+  }
+  // T = s_prefix (exact key of the bb-th largest); keys > T all selected,
+  // then the s_need smallest indices with key == T.
+  const unsigned long long T = s_prefix;
+  const int need_eq = s_need;
+  if (threadIdx.x == 0) s_cnt = 0;
+  __syncthreads();
+  for (int64_t j = threadIdx.x; j < n; j += blockDim.x) {
+    const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
+    if (kb > T) {
+      const int slot = atomicAdd(&s_cnt, 1);
+      if (slot < BBP) {
+        cand_key[slot] = kb;
+        cand_idx[slot] = (int)j;
+      }
+    }
+  }
+  __syncthreads();
+  int carry = 0;
+  const int base = s_cnt;
+  for (int64_t j0 = 0; j0 < n; j0 += blockDim.x) {
+    const int64_t j = j0 + threadIdx.x;
+    int f = 0;
+    if (j < n) f = ((unsigned long long)__double_as_longlong(keys[j]) == T);
+    // exclusive scan of f over the block, in index order
+    int v = f;
+    const int lane = lane_id();
+    for (int o = 1; o < 64; o <<= 1) {
+      const int u = __shfl_up(v, o, 64);
+      if (lane >= o) v += u;
+    }
+    if (lane == 63) s_scan[wave_id()] = v;
+    __syncthreads();
+    int woff = 0, tot = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+      if (w < wave_id()) woff += s_scan[w];
+      tot += s_scan[w];
+    }
+    const int pos = carry + woff + v - f;
+    if (f && pos < need_eq && base + pos < BBP) {
+      cand_key[base + pos] = T;
+      cand_idx[base + pos] = (int)j;
+    }
+    carry += tot;
+    __syncthreads();
+  }
+  __syncthreads();
+  // order the bb winners by (key desc, index asc)
+  if (threadIdx.x < bb) {
+    const unsigned long long k0 = cand_key[threadIdx.x];
+    const int i0 = cand_idx[threadIdx.x];
+    int rank = 0;
+    for (int q = 0; q < bb; ++q) {
+      const unsigned long long k1 = cand_key[q];
+      const int i1 = cand_idx[q];
+      rank += (k1 > k0) || (k1 == k0 && i1 < i0);
+    }
+    J[rank] = i0;
+  }
+}
+
+// ||R||^2 after the last block (1 WG).
+__global__ __launch_bounds__(NT_SELECT) void k_finish(const double* __restrict__ colE_part, int gd, int64_t n,
+                                                      int64_t n_pad, const double* __restrict__ hw,
+                                                      double* colE_out, double* fro2_out, double* fro2w_out) {
+  __shared__ double shd[16];
+  reduce_colE(colE_part, gd, n, n_pad, hw, colE_out, fro2_out, fro2w_out, shd);
+}
+
+// ---------------------------------------------------------------------------
+// Emit a block into the packed outputs (2-bit trits: 00 = 0, 01 = +1,
+// 11 = -1; element j of a row at byte j>>2, bits 2(j&3)).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ unsigned trit_code(int8_t t) { return t == 0 ? 0u : (t > 0 ? 1u : 3u); }
+
+// B rows: byte range covering columns [c0, c0 + bb) of B (read-modify-write
+// of shared bytes; padding bits beyond k cleared).
+__global__ __launch_bounds__(NT) void k_emit_b(const int8_t* __restrict__ Ur, int64_t m, int64_t c0, int bb,
+                                               int64_t k, uint8_t* __restrict__ Bp) {
+  const int64_t pitch = (k + 3) >> 2;
+  const int64_t q0 = c0 >> 2, q1 = (c0 + bb - 1) >> 2;
+  const int64_t nq = q1 - q0 + 1;
+  const int64_t total = m * nq;
+  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
+    const int64_t i = e / nq, q = q0 + e % nq;
+    uint8_t* dst = Bp + i * pitch + q;
+    unsigned byte = *dst;
+    for (int s = 0; s < 4; ++s) {
+      const int64_t p = 4 * q + s;
+      if (p >= k) byte &= ~(3u << (2 * s));
+      else if (p >= c0 && p < c0 + bb) {
+        byte &= ~(3u << (2 * s));
+        byte |= trit_code(Ur[i * BBP + (p - c0)]) << (2 * s);
+      }
+    }
+    *dst = (uint8_t)byte;
+  }
+}
+
+// C rows c0 .. c0 + bb - 1 from Vt.
+__global__ __launch_bounds__(NT) void k_emit_c(const int8_t* __restrict__ Vt, int64_t n, int64_t n_pad,
+                                               int64_t c0, int bb, uint8_t* __restrict__ Cp) {
+  const int64_t pitch = (n + 3) >> 2;
+  const int64_t total = (int64_t)bb * pitch;
+  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
+    const int64_t c = e / pitch, q = e % pitch;
+    unsigned byte = 0;
+    for (int s = 0; s < 4; ++s) {
+      const int64_t j = 4 * q + s;
+      if (j < n) byte |= trit_code(Vt[c * n_pad + j]) << (2 * s);
+    }
+    Cp[(c0 + c) * pitch + q] = (uint8_t)byte;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// step-entry helpers: caller layouts <-> workspace layouts
+// ---------------------------------------------------------------------------
+// X: len x bb row-major int8 -> Xt (BBP x len_pad) and Xr (len_pad x BBP), zero padded.
+__global__ __launch_bounds__(NT) void k_load_factor(int8_t* Xt, int8_t* Xr, const int8_t* X, int64_t len,
+                                                    int64_t len_pad, int bb) {
+  const int64_t total = len_pad * BBP;
+  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
+    const int64_t i = e / BBP;
+    const int c = (int)(e % BBP);
+    const int8_t v = (i < len && c < bb) ? X[i * bb + c] : (int8_t)0;
+    Xr[e] = v;
+    Xt[(int64_t)c * len_pad + i] = v;
+  }
+}
+__global__ __launch_bounds__(NT) void k_store_factor(int8_t* X, const int8_t* Xt, int64_t len, int64_t len_pad,
+                                                     int bb) {
+  const int64_t total = len * bb;
+  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
+    const int64_t i = e / bb;
+    const int c = (int)(e % bb);
+    X[e] = Xt[(int64_t)c * len_pad + i];
+  }
+}
+// component-major (BBP x len_pad) <-> row-major (len x bb)
+__global__ __launch_bounds__(NT) void k_store_cm(double* X, const double* Xcm, int64_t len, int64_t len_pad,
+                                                 int bb) {
+  const int64_t total = len * bb;
+  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
+    const int64_t i = e / bb;
+    const int c = (int)(e % bb);
+    X[e] = Xcm[(int64_t)c * len_pad + i];
+  }
+}
+__global__ __launch_bounds__(NT) void k_load_cm(double* Xcm, const double* X, int64_t len, int64_t len_pad,
+                                                int bb) {
+  const int64_t total = len_pad * BBP;
+  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
+    const int c = (int)(e / len_pad);
+    const int64_t i = e % len_pad;
+    Xcm[e] = (i < len && c < bb) ? X[i * bb + c] : 0.0;
+  }
+}
+
+
+// Gram of V alone (raw V^T H V and its ridge inverse), for the scale step
+// entry point.  grid: NSIDE.
+template <bool WEIGHTED>
+__global__ __launch_bounds__(NT) void k_gram_v(const int8_t* __restrict__ Vt, const int8_t* __restrict__ Vr,
+                                               const double* __restrict__ hw, int64_t n_pad, int bb, int* gparti,
+                                               double* gpart, unsigned* counter, double* ginvV, double* gramV) {
+  __shared__ int red[4096];
+  __shared__ double Gs[4096];
+  __shared__ double colbuf[128];
+  bool last;
+  if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, gpart, counter, Gs);
+  else last = side_gram_int(Vt, n_pad, blockIdx.x, gparti, counter, Gs, red);
+  if (!last) return;
+  for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
+  __syncthreads();
+  ridge_invert_store(Gs, colbuf, bb, ginvV);
+}
+
+// g_c = sum_i U_ic Q_ic (fp64).  grid: BBP.
+__global__ __launch_bounds__(NT) void k_gvec(const int8_t* __restrict__ Ut, const double* __restrict__ Q, int64_t m,
+                                             int64_t m_pad, int bb, double* __restrict__ gvec) {
+  __shared__ double shd[16];
+  const int c = blockIdx.x;
+  double acc = 0.0;
+  if (c < bb)
+    for (int64_t i = threadIdx.x; i < m; i += NT) acc += (double)Ut[(int64_t)c * m_pad + i] * Q[(int64_t)c * m_pad + i];
+  acc = block_sum_d(acc, shd);
+  if (threadIdx.x == 0) gvec[c] = acc;
+}
+
+// Scales given by the caller: dvec = d, dF = fp32(d), zero beyond bb.
+__global__ void k_set_scales(const double* __restrict__ d, int bb, double* dvec, float* dF) {
+  const int c = threadIdx.x;
+  if (c < BBP) {
+    const double v = (c < bb) ? d[c] : 0.0;
+    dvec[c] = v;
+    dF[c] = (float)v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host launchers
+// ---------------------------------------------------------------------------
+static inline unsigned grid_for(int64_t total) {
+  int64_t g = (total + NT - 1) / NT;
+  if (g < 1) g = 1;
+  if (g > 8192) g = 8192;
+  return (unsigned)g;
+}
+
+hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s) {
+  hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.maxbits, w.maxbits_w, w.fro2_hist,
+                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags);
+  return hipGetLastError();
+}
+
+hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s) {
+  const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
+  hipLaunchKernelGGL(k_stage, dim3(grid), dim3(NT), 0, s, A, lda, w.m, w.n, w.R, w.colE_part, w.maxbits,
+                     w.maxbits_w, w.hw, w.flags, w.m_pad, w.n_pad, w.gd);
+  return hipGetLastError();
+}
+
+hipError_t launch_unstage(const Ws& w, float* A, hipStream_t s) {
+  hipLaunchKernelGGL(k_unstage, dim3(grid_for(w.m * w.n)), dim3(NT), 0, s, w.R, A, w.m, w.n, w.n_pad);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(const Ws& w, int blk, int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_select, dim3(1), dim3(NT_SELECT), 0, s, w.colE_part, w.gd, w.n, w.n_pad, w.hw, w.Y,
+                     w.fro2_hist + blk, w.fro2w_hist + blk, bb, w.J);
+  return hipGetLastError();
+}
+
+hipError_t launch_finish(const Ws& w, int blk, hipStream_t s) {
+  hipLaunchKernelGGL(k_finish, dim3(1), dim3(NT_SELECT), 0, s, w.colE_part, w.gd, w.n, w.n_pad, w.hw,
+                     (double*)nullptr, w.fro2_hist + blk, w.fro2w_hist + blk);
+  return hipGetLastError();
+}
+
+hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2, hipStream_t s) {
+  hipLaunchKernelGGL(k_finish, dim3(1), dim3(NT_SELECT), 0, s, w.colE_part, w.gd, w.n, w.n_pad, w.hw, colnorm2,
+                     fro2 ? fro2 : (w.fro2_hist + blk), w.fro2w_hist + blk);
+  return hipGetLastError();
+}
+
+hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
+  hipLaunchKernelGGL(k_init, dim3(BBP), dim3(NT), 0, s, w.R, w.J, w.m, w.m_pad, w.n_pad, bb, tau, w.Ut);
+  return hipGetLastError();
+}
+
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s) {
+  const unsigned grid = (unsigned)(NSIDE + (w.n_pad / TILE) * w.gv);
+  hipLaunchKernelGGL(k_vstep, dim3(grid), dim3(NT), 0, s, w.R, w.Ut, w.Pp, w.maxbits + blk, w.m_pad, w.n_pad, w.gv,
+                     bb, w.gparti, w.counters + CNT_GRAM_U, w.ginvU);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_vepi, dim3((unsigned)(w.n_pad / TILE)), dim3(NT), 0, s, w.Pp, w.gv, w.ginvU, w.Y,
+                     w.maxbits + blk, w.n_pad);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.Vt);
+  return hipGetLastError();
+}
+
+hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s) {
+  hipError_t e;
+  const unsigned grid = (unsigned)(NSIDE + w.m_pad / TILE);
+  if (weighted) {
+    hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_ustep<true>, dim3(grid), dim3(NT), 0, s, w.R, w.Vt, w.Vr, w.hw, w.Q, w.maxbits_w + blk,
+                       w.m_pad, w.n_pad, bb, w.gparti, w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
+  } else {
+    hipLaunchKernelGGL(k_ustep<false>, dim3(grid), dim3(NT), 0, s, w.R, w.Vt, w.Vr, w.hw, w.Q, w.maxbits + blk,
+                       w.m_pad, w.n_pad, bb, w.gparti, w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_uepi, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0, s, w.Q, w.ginvV, w.Z, w.m_pad);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.Ut, w.gvec);
+  return hipGetLastError();
+}
+
+hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_scale, dim3(NSIDE), dim3(NT), 0, s, w.Ut, w.m_pad, bb, w.gramV, w.gvec, w.gparti,
+                     w.counters + CNT_SCALE, w.dvec, w.dF, (float*)nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s) {
+  hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.m_pad / 32)), dim3(NT), 0, s, w.Ut, w.Ur, w.m_pad);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
+  hipLaunchKernelGGL(k_deflate, dim3(grid), dim3(NT), 0, s, w.R, w.Ur, w.Vr, w.dF, w.colE_part,
+                     w.maxbits + blk + 1, w.maxbits_w + blk + 1, w.hw, w.m_pad, w.n_pad, w.gd);
+  return hipGetLastError();
+}
+
+hipError_t launch_emit(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
+                       hipStream_t s) {
+  const int64_t nq = ((c0 + bb - 1) >> 2) - (c0 >> 2) + 1;
+  hipLaunchKernelGGL(k_emit_b, dim3(grid_for(w.m * nq)), dim3(NT), 0, s, w.Ur, w.m, c0, bb, k, Bp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_emit_c, dim3(grid_for((int64_t)bb * ((w.n + 3) >> 2))), dim3(NT), 0, s, w.Vt, w.n, w.n_pad,
+                     c0, bb, Cp);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return hipMemcpyAsync(D + c0, w.dF, sizeof(float) * bb, hipMemcpyDeviceToDevice, s);
+}
+
+hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, const int8_t* X, int64_t len, int64_t len_pad, int bb,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(k_load_factor, dim3(grid_for(len_pad * BBP)), dim3(NT), 0, s, Xt, Xr, X, len, len_pad, bb);
+  return hipGetLastError();
+}
+hipError_t launch_store_factor(int8_t* X, const int8_t* Xt, int64_t len, int64_t len_pad, int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_store_factor, dim3(grid_for(len * bb)), dim3(NT), 0, s, X, Xt, len, len_pad, bb);
+  return hipGetLastError();
+}
+hipError_t launch_store_cm(double* X, const double* Xcm, int64_t len, int64_t len_pad, int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_store_cm, dim3(grid_for(len * bb)), dim3(NT), 0, s, X, Xcm, len, len_pad, bb);
+  return hipGetLastError();
+}
+hipError_t launch_load_cm(double* Xcm, const double* X, int64_t len, int64_t len_pad, int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_load_cm, dim3(grid_for(len_pad * BBP)), dim3(NT), 0, s, Xcm, X, len, len_pad, bb);
+  return hipGetLastError();
+}
+
+hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s) {
+  if (weighted)
+    hipLaunchKernelGGL(k_gram_v<true>, dim3(NSIDE), dim3(NT), 0, s, w.Vt, w.Vr, w.hw, w.n_pad, bb, w.gparti, w.gpart,
+                       w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
+  else
+    hipLaunchKernelGGL(k_gram_v<false>, dim3(NSIDE), dim3(NT), 0, s, w.Vt, w.Vr, w.hw, w.n_pad, bb, w.gparti,
+                       w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
+  return hipGetLastError();
+}
+hipError_t launch_gvec(const Ws& w, int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_gvec, dim3(BBP), dim3(NT), 0, s, w.Ut, w.Q, w.m, w.m_pad, bb, w.gvec);
+  return hipGetLastError();
+}
+hipError_t launch_set_scales(const Ws& w, const double* d, int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_set_scales, dim3(1), dim3(BBP), 0, s, d, bb, w.dvec, w.dF);
+  return hipGetLastError();
+}
+
+}  // namespace externd

@@ -1,0 +1,91 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function declared in include/externd.h, and rejects bad arguments
+before any device work."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_13511_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "externd.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(externd_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = binding.lib()
+    declared = _declared_functions()
+    assert len(declared) >= 10
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(binding.EXPORTED) == declared
+
+
+def test_rank_block_and_workspace_rules():
+    for m, n, mu in [(256, 256, 2.0), (2048, 2048, 2.0), (9728, 2560, 3.0), (2560, 1024, 2.5), (10, 10, 0.25),
+                     (37, 11, 1.3)]:
+        assert binding.rank(m, n, mu) == oracle.rank_of(m, n, mu)
+    for m, n, b in [(256, 256, 1), (9728, 2560, 64), (64, 64, 256), (5, 7, 4), (2048, 2048, 32)]:
+        assert binding.effective_block(m, n, b) == min(oracle.effective_block(m, n, b), binding.MAX_BLOCK)
+    assert binding.effective_block(4096, 4096, 256) == 64
+    assert binding.rank(0, 5, 1.0) == -1 and binding.rank(5, 5, 0.0) == -1 and binding.rank(5, 5, float("nan")) == -1
+    ws = binding.workspace_bytes(9728, 2560, 7680)
+    assert 4 * 9728 * 2560 < ws < 2 * 4 * 9728 * 2560
+    assert binding.workspace_bytes(0, 10, 0) == 0
+    assert binding.workspace_bytes(1 << 16, 1 << 16, 0) == 0        # beyond the supported size
+    assert binding.workspace_bytes(100, 70, 10000) > binding.workspace_bytes(100, 70, 0)  # per-block history
+
+
+def test_argument_errors_before_device_work():
+    L = binding.lib()
+    dummy = ctypes.c_void_p(256)          # never dereferenced: validation fails first
+    E = ctypes.c_double(0.0)
+    f = L.externd_factorize
+    # null A
+    assert f(None, 10, 10, 1.0, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             dummy, 1 << 30, None) == binding.EINVAL
+    assert np.isnan(E.value)
+    # bad scalars
+    for (m, n, mu, tau, block, iters) in [(0, 10, 1.0, 0.7, 1, 1), (10, 10, 0.0, 0.7, 1, 1),
+                                          (10, 10, 1.0, -1.0, 1, 1), (10, 10, 1.0, float("inf"), 1, 1),
+                                          (10, 10, 1.0, 0.7, 0, 1), (10, 10, 1.0, 0.7, 1, 0)]:
+        assert f(dummy, m, n, mu, tau, block, iters, None, dummy, dummy, dummy, ctypes.byref(E), None, None,
+                 None, dummy, 1 << 30, None) == binding.EINVAL
+    # workspace too small / misaligned
+    assert f(dummy, 10, 10, 1.0, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             dummy, 16, None) == binding.EWORKSPACE
+    assert f(dummy, 10, 10, 1.0, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             ctypes.c_void_p(257), 1 << 30, None) == binding.EWORKSPACE
+    # unsupported shape
+    assert f(dummy, 1 << 16, 1 << 16, 1.0, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None,
+             None, dummy, 1 << 40, None) == binding.EUNSUPPORTED
+    # step entry points
+    assert L.externd_step_vstep(None, 10, 10, dummy, 4, 0.7, dummy, None, dummy, 1 << 30, None) == binding.EINVAL
+    assert L.externd_step_vstep(dummy, 10, 10, dummy, 65, 0.7, dummy, None, dummy, 1 << 30, None) == binding.EINVAL
+    assert L.externd_step_ustep(dummy, 10, 10, dummy, 0, 0.7, None, dummy, None, None, dummy, 1 << 30,
+                                None) == binding.EINVAL
+    assert L.externd_step_scale(dummy, dummy, None, 10, 10, 4, None, dummy, dummy, 1 << 30, None) == binding.EINVAL
+    assert L.externd_step_deflate(dummy, 10, 10, dummy, dummy, None, 4, None, None, dummy, 1 << 30,
+                                  None) == binding.EINVAL
+    assert L.externd_step_init(dummy, 10, 10, None, 11, 0.7, dummy, dummy, dummy, 1 << 30, None) == binding.EINVAL
+    assert L.externd_strerror(binding.EHIP).decode().startswith("HIP")
+
+
+def test_unpack_trits_format():
+    # row: [+1, -1, 0, +1, -1] -> codes 01 11 00 01 | 11 (pad 00 00 00)
+    b0 = 0b01_00_11_01
+    b1 = 0b00_00_00_11
+    out = binding.unpack_trits(np.array([[b0, b1]], dtype=np.uint8), 5)
+    assert out.tolist() == [[1, -1, 0, 1, -1]]
+    with pytest.raises(ValueError):
+        binding.unpack_trits(np.array([[0b10, 0]], dtype=np.uint8), 5)       # code 10
+    with pytest.raises(ValueError):
+        binding.unpack_trits(np.array([[0, 0b0100]], dtype=np.uint8), 5)     # padding bit set

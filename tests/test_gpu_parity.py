@@ -1,0 +1,248 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle.
+
+Per-step checks inject identical state (R, partner factor, weights) into
+both sides.  Tolerances:
+* ternarizations bit-exact, except entries whose oracle target is within
+  1e-5 (relative) of the oracle threshold; in a keep-largest fallback the
+  chosen index may differ only if the two largest |x| are within 1e-5;
+* joint scales D within 1e-4 relative (observed ~1e-12);
+* energies within 1e-3 absolute of the oracle at every checkpoint.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_13511_amd import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+BAND = 1e-5
+
+
+@pytest.fixture(scope="module")
+def ext():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_13511_amd import binding
+    binding.lib()
+    return binding
+
+
+def cuda(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def assert_tern_parity(t_gpu, x, tau, what=""):
+    """t_gpu must equal T_tau(x) except within the threshold band."""
+    x = np.asarray(x, dtype=np.float64)
+    t_ref = oracle.ternarize(x, tau)
+    diff = np.flatnonzero(t_gpu != t_ref)
+    if diff.size == 0:
+        return 0
+    a = np.abs(x)
+    theta = tau * np.sum(a) / x.size
+    near = np.abs(a - theta) <= BAND * theta
+    excused = near[diff]
+    if not np.all(a <= theta):
+        assert np.all(excused), f"{what}: {np.count_nonzero(~excused)} trits differ outside the band"
+        return diff.size
+    # the oracle took the keep-largest fallback
+    top = np.sort(a)[::-1]
+    tie = top.size > 1 and top[0] - top[1] <= BAND * top[0]
+    for i in diff[~excused]:
+        assert tie and a[i] >= top[0] * (1 - BAND), f"{what}: fallback index differs at {i}"
+    return diff.size
+
+
+def cols_parity(T_gpu, X, tau, what):
+    n = 0
+    for c in range(X.shape[1]):
+        n += assert_tern_parity(T_gpu[:, c], X[:, c], tau, f"{what} column {c}")
+    return n
+
+
+SHAPES = [
+    ("t4_rowscale", 100, 70, 4),
+    ("t4", 256, 96, 12),
+    ("t4_outliers", 333, 130, 32),
+    ("gauss", 1000, 257, 64),
+    ("t4", 64, 2000, 8),
+    ("t4_rowscale", 31, 17, 1),
+]
+
+
+@pytest.mark.parametrize("kind,m,n,bb", SHAPES)
+def test_vstep_parity(ext, kind, m, n, bb):
+    R = synth.small(kind, m, n, 1)
+    tau = 0.7
+    U, _ = oracle.init_block(R.astype(np.float64), np.ones(n), bb, tau)
+    V_ref, Y_ref = oracle.vstep(R.astype(np.float64), U, tau)
+    V, Y = ext.step_vstep(cuda(R), cuda(U), tau)
+    V, Y = host(V), host(Y)
+    assert np.max(np.abs(Y - Y_ref)) <= 1e-7 * np.max(np.abs(Y_ref))
+    cols_parity(V, Y_ref.T, tau, "V")
+
+
+@pytest.mark.parametrize("weighted", [False, True])
+@pytest.mark.parametrize("kind,m,n,bb", SHAPES)
+def test_ustep_parity(ext, kind, m, n, bb, weighted):
+    R = synth.small(kind, m, n, 2)
+    h = synth.small_importance(n, 2) if weighted else None
+    w = oracle.normalized_weights(h, n)
+    tau = 1.0
+    U0, _ = oracle.init_block(R.astype(np.float64), w, bb, tau)
+    V, _ = oracle.vstep(R.astype(np.float64), U0, tau)
+    U_ref, Q_ref, Z_ref = oracle.ustep(R.astype(np.float64), V, w, tau)
+    U, Q, Z = ext.step_ustep(cuda(R), cuda(V), tau, h=cuda(h) if weighted else None)
+    U, Q, Z = host(U), host(Q), host(Z)
+    # the contraction is exact for the fixed-point residual (2^-30 max|R h~|)
+    assert np.max(np.abs(Q - Q_ref)) <= 1e-7 * np.max(np.abs(Q_ref))
+    # the fp64 solve, isolated from the contraction's rounding
+    G = V.astype(np.float64).T @ (w[:, None] * V.astype(np.float64))
+    G = G + oracle.RIDGE_REL * np.trace(G) / bb * np.eye(bb)
+    Z_chk = np.linalg.solve(G, Q.T).T
+    assert np.max(np.abs(Z - Z_chk)) <= 1e-10 * np.max(np.abs(Z_chk))
+    cols_parity(U, Z_ref, tau, "U")
+
+
+@pytest.mark.parametrize("weighted", [False, True])
+@pytest.mark.parametrize("kind,m,n,bb", SHAPES)
+def test_scale_parity(ext, kind, m, n, bb, weighted):
+    R = synth.small(kind, m, n, 3).astype(np.float64)
+    h = synth.small_importance(n, 3) if weighted else None
+    w = oracle.normalized_weights(h, n)
+    U, _ = oracle.init_block(R, w, bb, 1.0)
+    for _ in range(2):
+        V, _ = oracle.vstep(R, U, 1.0)
+        U, Q, _ = oracle.ustep(R, V, w, 1.0)
+    d_ref = oracle.scale_solve(U, V, Q, w)
+    d = host(ext.step_scale(cuda(U), cuda(V), cuda(Q), h=cuda(h) if weighted else None))
+    np.testing.assert_allclose(d, d_ref, rtol=1e-8, atol=1e-12 * np.max(np.abs(d_ref)))
+
+
+@pytest.mark.parametrize("kind,m,n,bb", SHAPES)
+def test_deflate_parity(ext, kind, m, n, bb):
+    R = synth.small(kind, m, n, 4)
+    R64 = R.astype(np.float64)
+    U, _ = oracle.init_block(R64, np.ones(n), bb, 0.7)
+    V, _ = oracle.vstep(R64, U, 0.7)
+    U, Q, _ = oracle.ustep(R64, V, np.ones(n), 0.7)
+    d = oracle.scale_solve(U, V, Q, np.ones(n))
+    ref = oracle.deflate(R64, U, V, d.astype(np.float32).astype(np.float64))
+    Rt = cuda(R)
+    col, fro = ext.step_deflate(Rt, cuda(U), cuda(V), cuda(d))
+    Rg = host(Rt).astype(np.float64)
+    # fp32 bound: one rounding of R - dR plus the fp32 accumulation of the
+    # 64 terms of dR, measured by sum_c |U_ic d_c V_jc|
+    absterm = (np.abs(U).astype(np.float64) * np.abs(d)[None, :]) @ np.abs(V).astype(np.float64).T
+    scale = np.abs(ref) + absterm
+    assert np.all(np.abs(Rg - ref) <= 2e-6 * scale + 1e-30)
+    np.testing.assert_allclose(host(col), np.sum(Rg * Rg, axis=0), rtol=1e-12, atol=1e-300)
+    np.testing.assert_allclose(host(fro)[0], np.sum(Rg * Rg), rtol=1e-12)
+
+
+@pytest.mark.parametrize("weighted", [False, True])
+@pytest.mark.parametrize("kind,m,n,bb", SHAPES)
+def test_init_parity(ext, kind, m, n, bb, weighted):
+    R = synth.small(kind, m, n, 5)
+    h = synth.small_importance(n, 5) if weighted else None
+    w = oracle.normalized_weights(h, n)
+    U_ref, J_ref = oracle.init_block(R.astype(np.float64), w, bb, 0.7)
+    U, J = ext.step_init(cuda(R), bb, 0.7, h=cuda(h) if weighted else None)
+    U, J = host(U), host(J)
+    key = w * np.sum(R.astype(np.float64) ** 2, axis=0)
+    # the chosen set must carry the same keys (ties may pick other indices)
+    np.testing.assert_allclose(key[J], key[J_ref], rtol=1e-12)
+    for c in range(bb):
+        assert_tern_parity(U[:, c], R[:, J[c]].astype(np.float64), 0.7, f"init column {c}")
+
+
+# ---------------------------------------------------------------------------
+# end-to-end
+# ---------------------------------------------------------------------------
+def decode(res, m, n):
+    from paper_2607_13511_amd import binding
+    B = binding.unpack_trits(host(res.B_packed), res.k)
+    C = binding.unpack_trits(host(res.C_packed), n)
+    D = host(res.D).astype(np.float64)
+    return B, C, D
+
+
+E2E = [
+    # kind, m, n, mu, tau, block, iters, weighted
+    ("t4_rowscale", 96, 80, 1.0, 0.7, 8, 4, False),
+    ("t4_outliers", 100, 70, 1.5, 1.0, 8, 3, False),
+    ("gauss", 64, 64, 1.0, 0.7, 1, 3, False),
+    ("t4", 200, 150, 1.0, 2.0, 16, 5, False),
+    ("t4_rowscale", 128, 96, 1.5, 1.0, 8, 4, True),
+    ("t4", 300, 45, 2.0, 1.0, 5, 3, True),
+]
+
+
+@pytest.mark.parametrize("kind,m,n,mu,tau,block,iters,weighted", E2E)
+def test_factorize_parity(ext, kind, m, n, mu, tau, block, iters, weighted):
+    A = synth.small(kind, m, n, 6)
+    h = synth.small_importance(n, 6) if weighted else None
+    res = ext.factorize(cuda(A), mu, tau, block, iters, h=cuda(h) if weighted else None)
+    ref = oracle.factorize_block(A, mu, tau, min(block, 64), iters, h=h)
+    assert res.k == ref.k and res.block == ref.block
+    np.testing.assert_allclose(res.curve, ref.curve, rtol=0, atol=1e-3)
+    if weighted:
+        np.testing.assert_allclose(res.curve_w, ref.curve_w, rtol=0, atol=1e-3)
+        assert np.all(np.diff(res.curve_w) >= -1e-6)
+    else:
+        assert np.all(np.diff(res.curve) >= -1e-6)
+    # the packed factors reproduce the reported energy
+    B, C, D = decode(res, m, n)
+    A64 = A.astype(np.float64)
+    Rr = A64 - oracle.reconstruct(B, D, C)
+    assert abs((1 - np.sum(Rr * Rr) / np.sum(A64 * A64)) - res.E) < 1e-5
+    zf = 0.5 * (np.mean(B == 0) + np.mean(C == 0))
+    zf_ref = 0.5 * (np.mean(ref.B == 0) + np.mean(ref.C == 0))
+    assert abs(zf - zf_ref) < 0.02
+
+
+def test_factorize_deterministic(ext):
+    A = cuda(synth.small("t4_outliers", 160, 120, 7))
+    r1 = ext.factorize(A, 1.0, 1.0, 8, 3)
+    r2 = ext.factorize(A, 1.0, 1.0, 8, 3)
+    assert torch.equal(r1.B_packed, r2.B_packed) and torch.equal(r1.C_packed, r2.C_packed)
+    assert torch.equal(r1.D, r2.D) and r1.E == r2.E
+
+
+def test_gauss256_sequential_checkpoints(ext):
+    # 256 x 256 N(0, 0.02^2) seed 0, mu = 2 (k = 512), tau = 0.7, block = 1,
+    # 8 iterations: the GPU runs Sec. 2.3 exactly; E at k = 64, 128, 256, 512.
+    w = synth.gauss256()
+    res = ext.factorize(cuda(w.A), w.mu, w.tau, w.block, w.iters)
+    ref = oracle.factorize_sequential(w.A, w.mu, w.tau, w.iters)
+    ks = np.array(w.checkpoints_k) - 1
+    np.testing.assert_allclose(res.curve[ks], ref.curve[ks], rtol=0, atol=1e-3)
+
+
+def test_zero_matrix(ext):
+    res = ext.factorize(torch.zeros((40, 24), dtype=torch.float32, device="cuda"), 1.0, 0.7, 2, 2)
+    assert res.E == 1.0
+    assert not host(res.D).any()
+    B, C, _ = decode(res, 40, 24)
+    assert not B.any() and not C.any()
+
+
+def test_nonfinite_and_bad_weights(ext):
+    A = synth.small("gauss", 40, 24, 8)
+    A[3, 5] = np.nan
+    with pytest.raises(ext.ExterndError) as e:
+        ext.factorize(cuda(A), 1.0, 0.7, 2, 2)
+    assert e.value.status == ext.ENONFINITE
+    A = synth.small("gauss", 40, 24, 8)
+    h = np.ones(24, dtype=np.float32)
+    h[2] = -1.0
+    with pytest.raises(ext.ExterndError) as e:
+        ext.factorize(cuda(A), 1.0, 0.7, 2, 2, h=cuda(h))
+    assert e.value.status == ext.EINVAL
