@@ -119,6 +119,29 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
                       double* energy_curve, double* energy_w_curve,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* Kernel classes timed by externd_factorize_timed. */
+#define EXTERND_KCLASS_VSTEP   0  /* V-step contraction P = U^T R (+ Gram of U)          */
+#define EXTERND_KCLASS_USTEP   1  /* U-step contraction Q = R diag(h~) V (+ Gram of V)  */
+#define EXTERND_KCLASS_DEFLATE 2  /* deflation R -= U diag(d) V^T (+ column energies)   */
+#define EXTERND_KCLASS_COUNT   3
+
+typedef struct {
+  double total_ms[EXTERND_KCLASS_COUNT];  /* summed kernel durations            */
+  int64_t launches[EXTERND_KCLASS_COUNT]; /* number of launches of each class   */
+} externd_kernel_times;
+
+/* externd_factorize with HIP events recorded on `stream` around every
+ * launch of the kernel classes above (profiling; the events add a small
+ * per-launch cost).  `times` (host, required) receives the summed
+ * durations.  Same outputs and status codes as externd_factorize.        */
+int externd_factorize_timed(const float* A, int64_t m, int64_t n, double mu, double tau,
+                            int32_t block, int32_t iters, const float* importance,
+                            uint8_t* B_packed, uint8_t* C_packed, float* D,
+                            double* energy, double* energy_w,
+                            double* energy_curve, double* energy_w_curve,
+                            void* workspace, size_t workspace_bytes, void* stream,
+                            externd_kernel_times* times);
+
 /*
  * Step entry points: one step each of the block ALS on caller-given state,
  * for per-step parity checks.  They share the kernels of

@@ -37,6 +37,9 @@ _SIGNATURES = {
     "externd_factorize": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_ptr,
                                          _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                          _c_ptr, _c_size, _c_ptr]),
+    "externd_factorize_timed": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_ptr,
+                                               _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
+                                               _c_ptr, _c_size, _c_ptr, _c_ptr]),
     "externd_step_init": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_ptr, _c_i32, _c_dbl, _c_ptr, _c_ptr,
                                          _c_ptr, _c_size, _c_ptr]),
     "externd_step_vstep": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_ptr, _c_i32, _c_dbl, _c_ptr, _c_ptr,
@@ -49,6 +52,13 @@ _SIGNATURES = {
                                             _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr]),
 }
 EXPORTED = tuple(_SIGNATURES)
+
+
+KCLASS_NAMES = ("vstep_contraction", "ustep_contraction", "deflate")
+
+
+class KernelTimes(ctypes.Structure):
+    _fields_ = [("total_ms", ctypes.c_double * 3), ("launches", ctypes.c_int64 * 3)]
 
 
 class ExterndError(RuntimeError):
@@ -133,11 +143,16 @@ class Factorization:
     curve_w: np.ndarray
     k: int
     block: int
+    kernel_times: Optional[dict] = None   # class -> (total_ms, launches) when timed
 
 
 def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=None,
-              workspace=None) -> Factorization:
-    """Factorize the fp32 CUDA tensor A (m x n) as B diag(D) C on the GPU."""
+              workspace=None, timed: bool = False) -> Factorization:
+    """Factorize the fp32 CUDA tensor A (m x n) as B diag(D) C on the GPU.
+
+    With ``timed`` the library records HIP events around every contraction
+    and deflation launch and returns their summed durations.
+    """
     torch = _torch()
     m, n = A.shape
     _req(A, torch, torch.float32, (m, n), "A")
@@ -157,12 +172,17 @@ def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=N
     Ew = ctypes.c_double(0.0)
     curve = np.zeros(nblk, dtype=np.float64)
     curve_w = np.zeros(nblk, dtype=np.float64)
-    st = lib().externd_factorize(
-        _dev_ptr(A), m, n, mu, tau, block, iters, _dev_ptr(h) if h is not None else None,
-        _dev_ptr(Bp), _dev_ptr(Cp), _dev_ptr(D), ctypes.byref(E), ctypes.byref(Ew),
-        curve.ctypes.data, curve_w.ctypes.data, _dev_ptr(ws), ws.numel(), _stream_ptr(torch, stream))
-    _check(st, "externd_factorize")
-    return Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b)
+    args = (_dev_ptr(A), m, n, mu, tau, block, iters, _dev_ptr(h) if h is not None else None,
+            _dev_ptr(Bp), _dev_ptr(Cp), _dev_ptr(D), ctypes.byref(E), ctypes.byref(Ew),
+            curve.ctypes.data, curve_w.ctypes.data, _dev_ptr(ws), ws.numel(), _stream_ptr(torch, stream))
+    kt = None
+    if timed:
+        times = KernelTimes()
+        _check(lib().externd_factorize_timed(*args, ctypes.byref(times)), "externd_factorize_timed")
+        kt = {name: (times.total_ms[i], int(times.launches[i])) for i, name in enumerate(KCLASS_NAMES)}
+    else:
+        _check(lib().externd_factorize(*args), "externd_factorize")
+    return Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b, kt)
 
 
 def step_init(R, bb: int, tau: float, h=None, stream=None):

@@ -49,8 +49,8 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(double) * 4096,                           // 9 ginvU
       sizeof(double) * 4096,                           // 10 ginvV
       sizeof(double) * 4096,                           // 11 gramV
-      sizeof(double) * 4096 * NSIDE,                   // 12 gpart
-      sizeof(int) * 4096 * NSIDE,                      // 13 gparti
+      sizeof(double) * 4096 * NSIDE_MAX,               // 12 gpart
+      sizeof(int) * 4096 * NSIDE_MAX,                  // 13 gparti
       sizeof(double) * (size_t)(L.gd * L.n_pad),       // 14 colE_part
       sizeof(double) * (size_t)L.n_pad,                // 15 hw
       sizeof(double) * BBP,                            // 16 gvec
@@ -115,6 +115,61 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   return true;
 }
 
+hipError_t Timer::begin(int cls) {
+  if (n == cap) {
+    const int ncap = cap ? 2 * cap : 1024;
+    Mark* nm = new Mark[ncap];
+    for (int i = 0; i < n; ++i) nm[i] = marks[i];
+    delete[] marks;
+    marks = nm;
+    for (int i = cap; i < ncap; ++i) {
+      marks[i].a = nullptr;
+      marks[i].b = nullptr;
+    }
+    cap = ncap;
+  }
+  Mark& mk = marks[n];
+  if (!mk.a) {
+    hipError_t e = hipEventCreate(&mk.a);
+    if (e != hipSuccess) return e;
+    e = hipEventCreate(&mk.b);
+    if (e != hipSuccess) return e;
+  }
+  mk.cls = cls;
+  return hipEventRecord(mk.a, stream);
+}
+
+hipError_t Timer::end() {
+  hipError_t e = hipEventRecord(marks[n].b, stream);
+  ++n;
+  return e;
+}
+
+hipError_t Timer::collect(double* total_ms, int64_t* launches, int ncls) {
+  for (int c = 0; c < ncls; ++c) {
+    total_ms[c] = 0.0;
+    launches[c] = 0;
+  }
+  for (int i = 0; i < n; ++i) {
+    float ms = 0.0f;
+    hipError_t e = hipEventElapsedTime(&ms, marks[i].a, marks[i].b);
+    if (e != hipSuccess) return e;
+    if (marks[i].cls >= 0 && marks[i].cls < ncls) {
+      total_ms[marks[i].cls] += ms;
+      launches[marks[i].cls] += 1;
+    }
+  }
+  return hipSuccess;
+}
+
+Timer::~Timer() {
+  for (int i = 0; i < cap; ++i) {
+    if (marks[i].a) (void)hipEventDestroy(marks[i].a);
+    if (marks[i].b) (void)hipEventDestroy(marks[i].b);
+  }
+  delete[] marks;
+}
+
 }  // namespace externd
 
 using namespace externd;
@@ -172,10 +227,10 @@ size_t externd_workspace_bytes(int64_t m, int64_t n, int64_t k) {
   return externd::workspace_bytes(m, n, k);
 }
 
-int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
-                      const float* importance, uint8_t* B_packed, uint8_t* C_packed, float* D, double* energy,
-                      double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
-                      size_t workspace_bytes, void* stream) {
+static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
+                          const float* importance, uint8_t* B_packed, uint8_t* C_packed, float* D, double* energy,
+                          double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
+                          size_t workspace_bytes, void* stream, externd_kernel_times* times) {
   if (energy) *energy = NAN;
   if (energy_w) *energy_w = NAN;
   if (!A || !B_packed || !C_packed || !D || !energy || !workspace) return EXTERND_EINVAL;
@@ -189,6 +244,9 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
   if (!carve(w, workspace, workspace_bytes, m, n, k)) return EXTERND_EWORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   const bool weighted = importance != nullptr;
+  Timer timer;
+  timer.stream = s;
+  Timer* tm = times ? &timer : nullptr;
 
   HIP_TRY(launch_prep(w, importance, s));
   HIP_TRY(launch_stage(w, A, n, s));
@@ -204,11 +262,11 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
     HIP_TRY(launch_select(w, (int)blk, bb, s));
     HIP_TRY(launch_init(w, bb, tau, s));
     for (int it = 0; it < iters; ++it) {
-      HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s));
-      HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, s));
+      HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm));
+      HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, s, tm));
     }
     HIP_TRY(launch_scale(w, bb, s));
-    HIP_TRY(launch_deflate(w, (int)blk, s));
+    HIP_TRY(launch_deflate(w, (int)blk, s, tm));
     HIP_TRY(launch_emit(w, c0, bb, k, B_packed, C_packed, D, s));
   }
   HIP_TRY(launch_finish(w, (int)nblk, s));
@@ -217,6 +275,7 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
   HIP_TRY(hipMemcpyAsync(f2.data(), w.fro2_hist, sizeof(double) * (nblk + 1), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipMemcpyAsync(f2w.data(), w.fro2w_hist, sizeof(double) * (nblk + 1), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
+  if (tm) HIP_TRY(tm->collect(times->total_ms, times->launches, EXTERND_KCLASS_COUNT));
   const double a2 = f2[0], a2w = f2w[0];
   auto E = [&](int64_t b) { return a2 == 0.0 ? 1.0 : 1.0 - f2[(size_t)b] / a2; };
   auto Ew = [&](int64_t b) { return a2w == 0.0 ? 1.0 : 1.0 - f2w[(size_t)b] / a2w; };
@@ -227,6 +286,26 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
     if (energy_w_curve) energy_w_curve[b] = Ew(b + 1);
   }
   return EXTERND_OK;
+}
+
+int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
+                      const float* importance, uint8_t* B_packed, uint8_t* C_packed, float* D, double* energy,
+                      double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  return factorize_impl(A, m, n, mu, tau, block, iters, importance, B_packed, C_packed, D, energy, energy_w,
+                        energy_curve, energy_w_curve, workspace, workspace_bytes, stream, nullptr);
+}
+
+int externd_factorize_timed(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block,
+                            int32_t iters, const float* importance, uint8_t* B_packed, uint8_t* C_packed, float* D,
+                            double* energy, double* energy_w, double* energy_curve, double* energy_w_curve,
+                            void* workspace, size_t workspace_bytes, void* stream, externd_kernel_times* times) {
+  if (!times) {
+    if (energy) *energy = NAN;
+    return EXTERND_EINVAL;
+  }
+  return factorize_impl(A, m, n, mu, tau, block, iters, importance, B_packed, C_packed, D, energy, energy_w,
+                        energy_curve, energy_w_curve, workspace, workspace_bytes, stream, times);
 }
 
 // ---------------------------------------------------------------------------

@@ -12,11 +12,15 @@ namespace externd {
 // are padded to multiples of TILE (zero padding, never touched by updates).
 constexpr int BBP = 64;
 constexpr int TILE = 32;
-// Side workgroups that build Gram matrices next to a contraction.
-constexpr int NSIDE = 16;
+// Side workgroups that build Gram matrices next to a contraction: integer
+// Grams (int8 MFMA) and the weighted fp64 Gram (fp64 MFMA).
+constexpr int NSIDE_INT = 8;
+constexpr int NSIDE_W = 16;
+constexpr int NSIDE_MAX = 16;
 // Threads per workgroup for all kernels except the selection kernel.
 constexpr int NT = 256;
 constexpr int NT_SELECT = 1024;
+constexpr int NT_TERN = 1024;   // per-component ternarization kernels
 
 // Index of counters in Ws::counters (each used by one kernel family, reset
 // to zero by the workgroup that consumes it).
@@ -43,8 +47,8 @@ struct Ws {
   double* ginvU;         // BBP x BBP
   double* ginvV;         // BBP x BBP
   double* gramV;         // BBP x BBP raw V^T H V (no ridge)
-  double* gpart;         // NSIDE x BBP x BBP partial Gram matrices
-  int* gparti;           // NSIDE x BBP x BBP partial integer Grams
+  double* gpart;         // NSIDE_MAX x BBP x BBP partial Gram matrices
+  int* gparti;           // NSIDE_MAX x BBP x BBP partial integer Grams
   double* colE_part;     // gd x n_pad partial column energies
   double* hw;            // n_pad: h~ (fp64), 1 when unweighted
   double* gvec;          // BBP: diag(U^T Q)
@@ -59,6 +63,27 @@ struct Ws {
   int* flags;            // FLAG_COUNT
 };
 
+// Optional per-kernel-class event timing (host side).  begin/end record a
+// pair of events on the stream around one launch; collect() sums the
+// elapsed times after the stream has been synchronised.
+struct Timer {
+  hipStream_t stream = nullptr;
+  struct Mark { hipEvent_t a, b; int cls; };
+  Mark* marks = nullptr;
+  int n = 0, cap = 0;
+  hipError_t begin(int cls);
+  hipError_t end();
+  hipError_t collect(double* total_ms, int64_t* launches, int ncls);
+  ~Timer();
+};
+// Record an event pair around `launch` when `t` is non-null.
+#define EXTERND_TIMED(t, cls, launch)                      \
+  do {                                                     \
+    if (t) { hipError_t _e = (t)->begin(cls); if (_e != hipSuccess) return _e; } \
+    launch;                                                \
+    if (t) { hipError_t _e = (t)->end(); if (_e != hipSuccess) return _e; } \
+  } while (0)
+
 size_t workspace_bytes(int64_t m, int64_t n, int64_t k);
 bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k);
 
@@ -68,10 +93,11 @@ hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s)
 hipError_t launch_select(const Ws& w, int blk, int bb, hipStream_t s);
 hipError_t launch_finish(const Ws& w, int blk, hipStream_t s);
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s);
-hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s);
-hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s);
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr);
+hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s,
+                        Timer* t = nullptr);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
-hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s);
+hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s, Timer* t = nullptr);
 hipError_t launch_emit(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp,
                        float* D, hipStream_t s);
 // step-entry helpers

@@ -36,6 +36,7 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef short v8s __attribute__((ext_vector_type(8)));
+typedef double v4d __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // small helpers
@@ -167,49 +168,102 @@ __device__ void block_argmax(double& v, long long& i, double* shv, long long* sh
 }
 
 // ---------------------------------------------------------------------------
-// 64x64 SPD inverse by the symmetric sweep operator (Gauss-Jordan without
-// pivoting, stable for SPD).  A: LDS 64x64 row-major, in: matrix, out:
-// inverse.  colbuf: LDS 2x64.  Requires blockDim.x == 256.  Each thread
-// keeps 16 entries (column j = tid % 64, rows tid / 64 + 4q) in registers;
-// the pivot column is published through LDS, one barrier per pivot.
+// 64x64 SPD inverse by the symmetric sweep operator with 2x2 pivot blocks
+// (block Gauss-Jordan without pivoting, stable for SPD).  A: LDS 64x64
+// row-major, in: matrix, out: inverse.  colbuf: LDS 2 x 2 x 64 doubles.
+// Requires blockDim.x == 256.
+//
+// The matrix is first scaled exactly by powers of two, A~ = S A S with
+// S = diag(2^-e_i), so that every diagonal entry lies in [0.5, 2); then
+// A^{-1} = S A~^{-1} S.  Sweeping the pivot block K = {k, k+1} with
+// P = A~_KK maps A_ij -> A_ij - A_iK P^{-1} A_Kj (i, j not in K),
+// A_iK -> A_iK P^{-1}, A_Kj -> P^{-1} A_Kj, A_KK -> -P^{-1}; after all
+// blocks the matrix is -A~^{-1}.  With C = A~[:, K] - E_K (published
+// through LDS) all cases are the single update A -= (C P^{-1}) C^T, except
+// the diagonal of the pivot block, which needs a further -2.  Thread t keeps
+// the 4x4 block (rows 4 (t/16) + r, columns 4 (t%16) + c) in registers; one
+// barrier per pivot block.
 // ---------------------------------------------------------------------------
 __device__ void spd_inverse64(double* A, double* colbuf) {
+  __shared__ int sexp[64];
   const int t = threadIdx.x;
-  const int j = t & 63;
-  const int r0 = t >> 6;
-  double a[16];
-#pragma unroll
-  for (int q = 0; q < 16; ++q) a[q] = A[(r0 + 4 * q) * 64 + j];
-  if (j == 0) {
-#pragma unroll
-    for (int q = 0; q < 16; ++q) colbuf[r0 + 4 * q] = a[q];
+  const int rb = t >> 4, cb = t & 15;
+  if (t < 64) {
+    int E = 0;
+    frexp(A[t * 65], &E);
+    sexp[t] = E >> 1;  // floor(E / 2)
   }
   __syncthreads();
-  for (int k = 0; k < 64; ++k) {
-    const double* ck = colbuf + (k & 1) * 64;
-    const double inv = 1.0 / ck[k];
-    const double akj = ck[j];  // a_kj = a_jk (symmetric)
+  int er[4], ec[4];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int i = r0 + 4 * q;
-      const double aik = ck[i];
-      double v;
-      if (i == k && j == k) v = -inv;
-      else if (i == k) v = akj * inv;
-      else if (j == k) v = aik * inv;
-      else v = a[q] - aik * akj * inv;
-      a[q] = v;
+  for (int q = 0; q < 4; ++q) {
+    er[q] = sexp[4 * rb + q];
+    ec[q] = sexp[4 * cb + q];
+  }
+  double a[4][4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) a[r][c] = ldexp(A[(4 * rb + r) * 64 + 4 * cb + c], -(er[r] + ec[c]));
+  // publish pivot columns 0, 1 minus the identity
+  if (cb == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 4 * rb + r;
+      colbuf[i] = a[r][0] - (i == 0 ? 1.0 : 0.0);
+      colbuf[64 + i] = a[r][1] - (i == 1 ? 1.0 : 0.0);
     }
-    if (k + 1 < 64 && j == k + 1) {
-      double* cn = colbuf + ((k + 1) & 1) * 64;
+  }
+  __syncthreads();
+  for (int kp = 0; kp < 32; ++kp) {
+    const int k = 2 * kp;
+    const double* c0 = colbuf + (kp & 1) * 128;
+    const double* c1 = c0 + 64;
+    double u0[4], u1[4], v0[4], v1[4];
 #pragma unroll
-      for (int q = 0; q < 16; ++q) cn[r0 + 4 * q] = a[q];
+    for (int r = 0; r < 4; ++r) {
+      u0[r] = c0[4 * rb + r];
+      u1[r] = c1[4 * rb + r];
+      v0[r] = c0[4 * cb + r];
+      v1[r] = c1[4 * cb + r];
+    }
+    const double p00 = c0[k] + 1.0, p01 = c1[k], p11 = c1[k + 1] + 1.0;
+    const double idet = 1.0 / (p00 * p11 - p01 * p01);
+    const double q00 = p11 * idet, q01 = -p01 * idet, q11 = p00 * idet;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const double w0 = u0[r] * q00 + u1[r] * q01;
+      const double w1 = u0[r] * q01 + u1[r] * q11;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) a[r][c] = fma(-w0, v0[c], fma(-w1, v1[c], a[r][c]));
+    }
+    if (rb == (k >> 2) && cb == (k >> 2)) {
+      if ((k & 3) == 0) {
+        a[0][0] -= 2.0;
+        a[1][1] -= 2.0;
+      } else {
+        a[2][2] -= 2.0;
+        a[3][3] -= 2.0;
+      }
+    }
+    const int k2 = k + 2;
+    if (k2 < 64 && cb == (k2 >> 2)) {
+      double* n0 = colbuf + ((kp + 1) & 1) * 128;
+      double* n1 = n0 + 64;
+      const bool lo = (k2 & 3) == 0;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 4 * rb + r;
+        n0[i] = (lo ? a[r][0] : a[r][2]) - (i == k2 ? 1.0 : 0.0);
+        n1[i] = (lo ? a[r][1] : a[r][3]) - (i == k2 + 1 ? 1.0 : 0.0);
+      }
     }
     __syncthreads();
   }
-  // the sweep of every pivot leaves -A^{-1}
 #pragma unroll
-  for (int q = 0; q < 16; ++q) A[(r0 + 4 * q) * 64 + j] = -a[q];
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) A[(4 * rb + r) * 64 + 4 * cb + c] = -ldexp(a[r][c], -(er[r] + ec[c]));
   __syncthreads();
 }
 
@@ -218,15 +272,9 @@ __device__ void spd_inverse64(double* A, double* colbuf) {
 // and write the inverse.  Zero trace -> zero inverse on the real block
 // (every component is zero, Eq. (3) target is zero).
 __device__ void ridge_invert_store(double* G, double* colbuf, int bb, double* ginv_out) {
-  __shared__ double s_tr;
+  __shared__ double shd[16];
   const int t = threadIdx.x;
-  if (t == 0) {
-    double tr = 0.0;
-    for (int c = 0; c < bb; ++c) tr += G[c * 64 + c];
-    s_tr = tr;
-  }
-  __syncthreads();
-  const double tr = s_tr;
+  const double tr = block_sum_d((t < bb) ? G[t * 64 + t] : 0.0, shd);
   const double eps = EXTERND_RIDGE_REL * tr / (double)bb;
   for (int e = t; e < 4096; e += blockDim.x) {
     const int r = e >> 6, c = e & 63;
@@ -246,19 +294,19 @@ __device__ void ridge_invert_store(double* G, double* colbuf, int bb, double* gi
 }
 
 // ---------------------------------------------------------------------------
-// Gram matrices of a ternary factor, built by NSIDE workgroups
+// Gram matrices of a ternary factor, built by `nside` workgroups
 // ---------------------------------------------------------------------------
 // Partial integer Gram of Tt (BBP x L int8, component-major) over this
 // workgroup's share of K steps, on int8 MFMA; all four wave results are
 // summed in LDS (integer adds, order-free) and written to gparti[side].
-// Returns true in the last of the NSIDE workgroups to finish, with the
+// Returns true in the last of the nside workgroups to finish, with the
 // complete Gram in G (LDS, fp64).
-__device__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side, int* gparti,
+__device__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side, int nside, int* gparti,
                               unsigned* counter, double* G, int* ired /* LDS 4096 */) {
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
   const int nks = (int)(L / TILE);
-  const int ks0 = (int)((long long)side * nks / NSIDE), ks1 = (int)((long long)(side + 1) * nks / NSIDE);
+  const int ks0 = (int)((long long)side * nks / nside), ks1 = (int)((long long)(side + 1) * nks / nside);
   v16i acc00 = {}, acc01 = {}, acc10 = {}, acc11 = {};
   for (int ks = ks0 + wave; ks < ks1; ks += 4) {
     const int64_t i0 = (int64_t)ks * TILE + 16 * h;
@@ -288,15 +336,25 @@ __device__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side
   __shared__ int s_last;
   if (threadIdx.x == 0) {
     const unsigned old = atomicAdd(counter, 1u);
-    s_last = (old == (unsigned)(NSIDE - 1));
+    s_last = (old == (unsigned)(nside - 1));
   }
   __syncthreads();
   if (!s_last) return false;
   __threadfence();
-  for (int e = threadIdx.x; e < 4096; e += blockDim.x) {
-    long long s = 0;
-    for (int q = 0; q < NSIDE; ++q) s += __builtin_nontemporal_load(gparti + (size_t)q * 4096 + e);
-    G[e] = (double)s;
+  for (int e4 = threadIdx.x; e4 < 1024; e4 += blockDim.x) {
+    int4 acc = make_int4(0, 0, 0, 0);
+#pragma unroll 8
+    for (int q = 0; q < nside; ++q) {
+      const int4 v = ((const int4*)(gparti + (size_t)q * 4096))[e4];
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    G[4 * e4] = (double)acc.x;
+    G[4 * e4 + 1] = (double)acc.y;
+    G[4 * e4 + 2] = (double)acc.z;
+    G[4 * e4 + 3] = (double)acc.w;
   }
   if (threadIdx.x == 0) *counter = 0u;
   __syncthreads();
@@ -304,52 +362,74 @@ __device__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side
 }
 
 // Partial weighted Gram V^T diag(hw) V over this workgroup's share of rows
-// of Vr (n_pad x BBP int8, row-major), fp64 VALU.  Thread t owns the 4x4
-// block (4*(t/16)+a, 4*(t%16)+b).  Same last-workgroup protocol.
-__device__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restrict__ hw, int64_t L,
-                            int side, double* gpart, unsigned* counter, double* G) {
-  const int t = threadIdx.x;
-  const int cb = t >> 4, cc = t & 15;
-  const int64_t j0 = (int64_t)side * L / NSIDE, j1 = (int64_t)(side + 1) * L / NSIDE;
-  double acc[16];
-#pragma unroll
-  for (int q = 0; q < 16; ++q) acc[q] = 0.0;
-  for (int64_t j = j0; j < j1; ++j) {
-    const unsigned ua = *(const unsigned*)(Vr + j * BBP + 4 * cb);
-    const unsigned ub = *(const unsigned*)(Vr + j * BBP + 4 * cc);
+// of Vr (n_pad x BBP int8, row-major) on fp64 MFMA (v_mfma_f64_16x16x4):
+// products h~_j v_jc v_jc' are exact and the sums are fp64.  The 10
+// 16x16 tiles of the upper triangle are dealt to the 4 waves; each wave
+// covers all of the workgroup's rows for its tiles.  Same last-workgroup
+// protocol as side_gram_int.
+__device__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restrict__ hw, int64_t L, int side,
+                            int nside, double* gpart, unsigned* counter, double* G) {
+  const int lane = lane_id(), wave = wave_id();
+  const int i16 = lane & 15, kq = lane >> 4;
+  const int64_t nks = L / 4;
+  const int64_t ks0 = side * nks / nside, ks1 = (side + 1) * nks / nside;
+  // tile t in 0..9 -> (mt, nt), mt <= nt, row-major over the upper triangle
+  const int TM[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
+  const int TN[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
+  v4d acc[3] = {v4d{}, v4d{}, v4d{}};
+  const int ntile = (wave < 2) ? 3 : 2;
+  for (int64_t ks = ks0; ks < ks1; ++ks) {
+    const int64_t j = ks * 4 + kq;
+    const int8_t* row = Vr + j * BBP;
     const double w = hw[j];
-    double va[4], vb[4];
+    double v[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      va[e] = w * (double)(signed char)((ua >> (8 * e)) & 0xff);
-      vb[e] = (double)(signed char)((ub >> (8 * e)) & 0xff);
+    for (int q = 0; q < 4; ++q) v[q] = (double)row[16 * q + i16];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      if (q < ntile) {
+        const int tt = wave + 4 * q;
+        acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(w * v[TM[tt]], v[TN[tt]], acc[q], 0, 0, 0);
+      }
     }
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a * 4 + b] += va[a] * vb[b];
   }
   double* mine = gpart + (size_t)side * 4096;
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int q = 0; q < 3; ++q) {
+    if (q < ntile) {
+      const int tt = wave + 4 * q;
+      const int mt = TM[tt], nt = TN[tt];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) mine[(4 * cb + a) * 64 + 4 * cc + b] = acc[a * 4 + b];
+      for (int r = 0; r < 4; ++r) {
+        // v_mfma_f64_16x16x4f64 result: lane l, register r holds row l/16 + 4 r, column l%16
+        const int gi = 16 * mt + kq + 4 * r, gj = 16 * nt + i16;
+        mine[gi * 64 + gj] = acc[q][r];
+        if (mt != nt) mine[gj * 64 + gi] = acc[q][r];
+      }
+    }
+  }
   __threadfence();
   __syncthreads();
   __shared__ int s_last;
-  if (t == 0) {
+  if (threadIdx.x == 0) {
     const unsigned old = atomicAdd(counter, 1u);
-    s_last = (old == (unsigned)(NSIDE - 1));
+    s_last = (old == (unsigned)(nside - 1));
   }
   __syncthreads();
   if (!s_last) return false;
   __threadfence();
-  for (int e = t; e < 4096; e += blockDim.x) {
-    double s = 0.0;
-    for (int q = 0; q < NSIDE; ++q) s += __builtin_nontemporal_load(gpart + (size_t)q * 4096 + e);
-    G[e] = s;
+  for (int e2 = threadIdx.x; e2 < 2048; e2 += blockDim.x) {
+    double2 acc2 = make_double2(0.0, 0.0);
+#pragma unroll 8
+    for (int q = 0; q < nside; ++q) {
+      const double2 v = ((const double2*)(gpart + (size_t)q * 4096))[e2];
+      acc2.x += v.x;
+      acc2.y += v.y;
+    }
+    G[2 * e2] = acc2.x;
+    G[2 * e2 + 1] = acc2.y;
   }
-  if (t == 0) *counter = 0u;
+  if (threadIdx.x == 0) *counter = 0u;
   __syncthreads();
   return true;
 }
@@ -378,23 +458,23 @@ __device__ __forceinline__ long long combine_planes(const int* red, int t, int M
 
 // ---------------------------------------------------------------------------
 // V-step contraction P = U^T R  (Eq. (3), first half)
-// grid: NSIDE side WGs (Gram U^T U + ridge + inverse) followed by
+// grid: nside side WGs (Gram U^T U + ridge + inverse) followed by
 //       (n_pad/32 column tiles) x gv row groups.
 // Each WG owns 32 columns and a contiguous range of 32-row K steps, split
 // over its 4 waves; A = Ut (components x rows), B = R digit planes.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) void k_vstep(const float* __restrict__ R, const int8_t* __restrict__ Ut,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vstep(const float* __restrict__ R, const int8_t* __restrict__ Ut,
                                               long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
                                               int64_t m_pad, int64_t n_pad, int gv, int bb, int* gparti,
-                                              unsigned* counter, double* ginvU) {
+                                              unsigned* counter, double* ginvU, int nside) {
   __shared__ int red[8 * RED_TILE];
   __shared__ double Gs[4096];
-  __shared__ double colbuf[128];
-  if (blockIdx.x < NSIDE) {
-    if (side_gram_int(Ut, m_pad, blockIdx.x, gparti, counter, Gs, red)) ridge_invert_store(Gs, colbuf, bb, ginvU);
+  __shared__ double colbuf[256];
+  if ((int)blockIdx.x < nside) {
+    if (side_gram_int(Ut, m_pad, blockIdx.x, nside, gparti, counter, Gs, red)) ridge_invert_store(Gs, colbuf, bb, ginvU);
     return;
   }
-  const int b = blockIdx.x - NSIDE;
+  const int b = blockIdx.x - nside;
   const int nct = (int)(n_pad / TILE);
   const int ct = b % nct, g = b / nct;
   const int nks = (int)(m_pad / TILE);
@@ -408,13 +488,33 @@ __global__ __launch_bounds__(NT) void k_vstep(const float* __restrict__ R, const
 #pragma unroll
     for (int p = 0; p < 4; ++p) acc[t][p] = v16i{};
   const float* Rc = R + (int64_t)ct * TILE + l32;
-  for (int ks = ks0 + wave; ks < ks1; ks += 4) {
+  const int8_t* U0 = Ut + (int64_t)l32 * m_pad + 16 * h;
+  const int8_t* U1 = Ut + (int64_t)(32 + l32) * m_pad + 16 * h;
+  // software pipeline: the loads of K step ks + 4 are in flight while
+  // step ks is converted and multiplied
+  float xn[16];
+  v4i an0 = {}, an1 = {};
+  int ks = ks0 + wave;
+  if (ks < ks1) {
     const int64_t i0 = (int64_t)ks * TILE + 16 * h;
-    const v4i a0 = *(const v4i*)(Ut + (int64_t)l32 * m_pad + i0);
-    const v4i a1 = *(const v4i*)(Ut + (int64_t)(32 + l32) * m_pad + i0);
+    an0 = *(const v4i*)(U0 + (int64_t)ks * TILE);
+    an1 = *(const v4i*)(U1 + (int64_t)ks * TILE);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) xn[q] = Rc[(i0 + q) * n_pad];
+  }
+  for (; ks < ks1; ks += 4) {
     unsigned y[16];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) y[q] = fx_biased(Rc[(i0 + q) * n_pad], s);
+    for (int q = 0; q < 16; ++q) y[q] = fx_biased(xn[q], s);
+    const v4i a0 = an0, a1 = an1;
+    const int ksn = ks + 4;
+    if (ksn < ks1) {
+      const int64_t i0 = (int64_t)ksn * TILE + 16 * h;
+      an0 = *(const v4i*)(U0 + (int64_t)ksn * TILE);
+      an1 = *(const v4i*)(U1 + (int64_t)ksn * TILE);
+#pragma unroll
+      for (int q = 0; q < 16; ++q) xn[q] = Rc[(i0 + q) * n_pad];
+    }
     v4i P[4];
     make_planes(y, P);
 #pragma unroll
@@ -437,24 +537,24 @@ __global__ __launch_bounds__(NT) void k_vstep(const float* __restrict__ R, const
 
 // ---------------------------------------------------------------------------
 // U-step contraction Q = R diag(h~) V  (Eq. (3) second half, Sec. 2.5)
-// grid: NSIDE side WGs (Gram V^T H V + ridge + inverse, raw Gram kept for
+// grid: nside side WGs (Gram V^T H V + ridge + inverse, raw Gram kept for
 //       the scale solve) followed by m_pad/32 row tiles.
 // Each WG owns 32 full rows; its 4 waves interleave 32-column K steps.
 // A = R digit planes (rows x columns), B = Vt (columns x components).
 // ---------------------------------------------------------------------------
 template <bool WEIGHTED>
-__global__ __launch_bounds__(NT) void k_ustep(const float* __restrict__ R, const int8_t* __restrict__ Vt,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_ustep(const float* __restrict__ R, const int8_t* __restrict__ Vt,
                                               const int8_t* __restrict__ Vr, const double* __restrict__ hw,
                                               double* __restrict__ Q, const unsigned* __restrict__ maxbits,
                                               int64_t m_pad, int64_t n_pad, int bb, int* gparti, double* gpart,
-                                              unsigned* counter, double* ginvV, double* gramV) {
+                                              unsigned* counter, double* ginvV, double* gramV, int nside) {
   __shared__ int red[8 * RED_TILE];
   __shared__ double Gs[4096];
-  __shared__ double colbuf[128];
-  if (blockIdx.x < NSIDE) {
+  __shared__ double colbuf[256];
+  if ((int)blockIdx.x < nside) {
     bool last;
-    if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, gpart, counter, Gs);
-    else last = side_gram_int(Vt, n_pad, blockIdx.x, gparti, counter, Gs, red);
+    if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, nside, gpart, counter, Gs);
+    else last = side_gram_int(Vt, n_pad, blockIdx.x, nside, gparti, counter, Gs, red);
     if (last) {
       for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
       __syncthreads();
@@ -462,7 +562,7 @@ __global__ __launch_bounds__(NT) void k_ustep(const float* __restrict__ R, const
     }
     return;
   }
-  const int rt = blockIdx.x - NSIDE;
+  const int rt = blockIdx.x - nside;
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
   const int s = fx_shift(*maxbits);
@@ -471,32 +571,44 @@ __global__ __launch_bounds__(NT) void k_ustep(const float* __restrict__ R, const
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int p = 0; p < 4; ++p) acc[t][p] = v16i{};
-  const float* Rrow = R + ((int64_t)rt * TILE + l32) * n_pad;
+  const float* Rrow = R + ((int64_t)rt * TILE + l32) * n_pad + 16 * h;
+  const int8_t* V0 = Vt + (int64_t)l32 * n_pad + 16 * h;
+  const int8_t* V1 = Vt + (int64_t)(32 + l32) * n_pad + 16 * h;
   const int nks = (int)(n_pad / TILE);
-  for (int ks = wave; ks < nks; ks += 4) {
+  // software pipeline: loads of K step ks + 4 in flight during step ks
+  float4 xn[4];
+  v4i bn0 = {}, bn1 = {};
+  int ks = wave;
+  if (ks < nks) {
+    const float4* src = (const float4*)(Rrow + (int64_t)ks * TILE);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) xn[q] = src[q];
+    bn0 = *(const v4i*)(V0 + (int64_t)ks * TILE);
+    bn1 = *(const v4i*)(V1 + (int64_t)ks * TILE);
+  }
+  for (; ks < nks; ks += 4) {
     const int64_t j0 = (int64_t)ks * TILE + 16 * h;
-    const float4* src = (const float4*)(Rrow + j0);
-    float x[16];
+    unsigned y[16];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float4 v = src[q];
-      x[4 * q] = v.x;
-      x[4 * q + 1] = v.y;
-      x[4 * q + 2] = v.z;
-      x[4 * q + 3] = v.w;
+      const float xs[4] = {xn[q].x, xn[q].y, xn[q].z, xn[q].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (WEIGHTED) y[4 * q + e] = fx_biased_w(xs[e], ldexp(hw[j0 + 4 * q + e], s));
+        else y[4 * q + e] = fx_biased(xs[e], s);
+      }
     }
-    unsigned y[16];
-    if (WEIGHTED) {
+    const v4i b0 = bn0, b1 = bn1;
+    const int ksn = ks + 4;
+    if (ksn < nks) {
+      const float4* src = (const float4*)(Rrow + (int64_t)ksn * TILE);
 #pragma unroll
-      for (int q = 0; q < 16; ++q) y[q] = fx_biased_w(x[q], ldexp(hw[j0 + q], s));
-    } else {
-#pragma unroll
-      for (int q = 0; q < 16; ++q) y[q] = fx_biased(x[q], s);
+      for (int q = 0; q < 4; ++q) xn[q] = src[q];
+      bn0 = *(const v4i*)(V0 + (int64_t)ksn * TILE);
+      bn1 = *(const v4i*)(V1 + (int64_t)ksn * TILE);
     }
     v4i P[4];
     make_planes(y, P);
-    const v4i b0 = *(const v4i*)(Vt + (int64_t)l32 * n_pad + j0);
-    const v4i b1 = *(const v4i*)(Vt + (int64_t)(32 + l32) * n_pad + j0);
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       acc[0][p] = mfma_i8(P[p], b0, acc[0][p]);
@@ -526,13 +638,31 @@ __global__ __launch_bounds__(NT) void k_vepi(const long long* __restrict__ Pp, i
   __shared__ double Gi[64][65];
   const int64_t j0 = (int64_t)blockIdx.x * TILE;
   const int s = fx_shift(*maxbits);
-  for (int e = threadIdx.x; e < 64 * 32; e += NT) {
-    const int c = e >> 5, jj = e & 31;
-    long long acc = 0;
-    for (int g = 0; g < gv; ++g) acc += Pp[((int64_t)g * BBP + c) * n_pad + j0 + jj];
-    Ps[c][jj] = ldexp((double)acc, -s);
+  // all loads of a round are issued before any LDS store (independent
+  // iterations, compile-time trip counts)
+  long long acc[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) acc[q] = 0;
+  for (int g = 0; g < gv; ++g) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = threadIdx.x + q * NT, c = e >> 5, jj = e & 31;
+      acc[q] += Pp[((int64_t)g * BBP + c) * n_pad + j0 + jj];
+    }
   }
-  for (int e = threadIdx.x; e < 4096; e += NT) Gi[e >> 6][e & 63] = ginv[e];
+  double gv_[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) gv_[q] = ginv[threadIdx.x + q * NT];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int e = threadIdx.x + q * NT;
+    Ps[e >> 5][e & 31] = ldexp((double)acc[q], -s);
+  }
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int e = threadIdx.x + q * NT;
+    Gi[e >> 6][e & 63] = gv_[q];
+  }
   __syncthreads();
   const int jj = threadIdx.x & 31, cg = threadIdx.x >> 5;
   double y[8];
@@ -553,11 +683,24 @@ __global__ __launch_bounds__(NT) void k_uepi(const double* __restrict__ Q, const
   __shared__ double Qs[64][33];
   __shared__ double Gi[64][65];
   const int64_t i0 = (int64_t)blockIdx.x * TILE;
-  for (int e = threadIdx.x; e < 64 * 32; e += NT) {
-    const int c = e >> 5, ii = e & 31;
-    Qs[c][ii] = Q[(int64_t)c * m_pad + i0 + ii];
+  double qv_[8], gv_[16];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int e = threadIdx.x + q * NT;
+    qv_[q] = Q[(int64_t)(e >> 5) * m_pad + i0 + (e & 31)];
   }
-  for (int e = threadIdx.x; e < 4096; e += NT) Gi[e >> 6][e & 63] = ginv[e];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) gv_[q] = ginv[threadIdx.x + q * NT];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int e = threadIdx.x + q * NT;
+    Qs[e >> 5][e & 31] = qv_[q];
+  }
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int e = threadIdx.x + q * NT;
+    Gi[e >> 6][e & 63] = gv_[q];
+  }
   __syncthreads();
   const int ii = threadIdx.x & 31, cg = threadIdx.x >> 5;
   double z[8];
@@ -576,18 +719,40 @@ __global__ __launch_bounds__(NT) void k_uepi(const double* __restrict__ Q, const
 // T_tau of one component per workgroup (Eq. (2)): theta = tau * mean|x|
 // over the true length L (fp64), strict ">", keep the largest |x| (smallest
 // index) when nothing passes.  Writes the trits component-major
-// (dst[0 .. L_pad)), zero beyond L.
+// (dst[0 .. L_pad)), zero beyond L.  The first TERN_CACHE * blockDim values
+// are loaded once and kept in registers for the threshold pass.  With an
+// auxiliary vector q (may be null) it also returns sum_i t_i q_i (fp64).
 // ---------------------------------------------------------------------------
+constexpr int TERN_CACHE = 16;
+
 template <typename Load>
-__device__ void ternarize_wg(Load load, int64_t L, int64_t L_pad, double tau, int8_t* dst, int* nnz_out) {
+__device__ double ternarize_wg(Load load, const double* __restrict__ q, int64_t L, int64_t L_pad, double tau,
+                               int8_t* dst) {
   __shared__ double shd[16];
   __shared__ long long shl[16];
   __shared__ int shi[16];
+  const int64_t st = blockDim.x;
+  const int64_t tid = threadIdx.x;
+  double xc[TERN_CACHE], qc[TERN_CACHE];
+#pragma unroll
+  for (int c = 0; c < TERN_CACHE; ++c) {
+    const int64_t i = tid + c * st;
+    xc[c] = (i < L) ? load(i) : 0.0;
+    qc[c] = (q && i < L) ? q[i] : 0.0;
+  }
   double sabs = 0.0, mx = -1.0;
   long long imx = 0;
-  for (int64_t i = threadIdx.x; i < L; i += blockDim.x) {
-    const double x = load(i);
-    const double a = fabs(x);
+#pragma unroll
+  for (int c = 0; c < TERN_CACHE; ++c) {
+    const int64_t i = tid + c * st;
+    if (i < L) {
+      const double a = fabs(xc[c]);
+      sabs += a;
+      argmax_merge(mx, imx, a, i);
+    }
+  }
+  for (int64_t i = tid + TERN_CACHE * st; i < L; i += st) {
+    const double a = fabs(load(i));
     sabs += a;
     argmax_merge(mx, imx, a, i);
   }
@@ -595,76 +760,89 @@ __device__ void ternarize_wg(Load load, int64_t L, int64_t L_pad, double tau, in
   block_argmax(mx, imx, shd, shl);
   const double theta = tau * (S / (double)L);
   int nnz = 0;
-  for (int64_t i = threadIdx.x; i < L_pad; i += blockDim.x) {
+  double g = 0.0;
+#pragma unroll
+  for (int c = 0; c < TERN_CACHE; ++c) {
+    const int64_t i = tid + c * st;
+    if (i < L_pad) {
+      int8_t t = 0;
+      if (i < L && fabs(xc[c]) > theta) t = (xc[c] > 0.0) ? 1 : -1;
+      nnz += (t != 0);
+      g += (double)t * qc[c];
+      dst[i] = t;
+    }
+  }
+  for (int64_t i = tid + TERN_CACHE * st; i < L_pad; i += st) {
     int8_t t = 0;
     if (i < L) {
       const double x = load(i);
       if (fabs(x) > theta) t = (x > 0.0) ? 1 : -1;
+      if (q) g += (double)t * q[i];
     }
     nnz += (t != 0);
     dst[i] = t;
   }
   nnz = block_sum_i(nnz, shi);
-  if (nnz == 0 && threadIdx.x == 0 && L > 0) {
-    const double x = load(imx);
-    const int8_t t = (x > 0.0) ? 1 : ((x < 0.0) ? -1 : 0);
-    dst[imx] = t;
-    nnz = (t != 0);
+  if (nnz == 0 && L > 0) {
+    // keep-largest fallback: only the argmax entry is nonzero
+    if (tid == 0) {
+      const double x = load(imx);
+      const int8_t t = (x > 0.0) ? 1 : ((x < 0.0) ? -1 : 0);
+      dst[imx] = t;
+      g = q ? (double)t * q[imx] : 0.0;
+    } else {
+      g = 0.0;
+    }
   }
-  if (nnz_out && threadIdx.x == 0) *nnz_out = nnz;
-  __syncthreads();
+  g = block_sum_d(g, shd);
+  return g;
 }
 
 // V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.  grid: BBP.
-__global__ __launch_bounds__(NT) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb,
-                                               double tau, int8_t* __restrict__ Vt) {
+__global__ __launch_bounds__(NT_TERN) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb,
+                                                    double tau, int8_t* __restrict__ Vt) {
   const int c = blockIdx.x;
   int8_t* dst = Vt + (int64_t)c * n_pad;
   if (c >= bb) {
-    for (int64_t j = threadIdx.x; j < n_pad; j += NT) dst[j] = 0;
+    for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) dst[j] = 0;
     return;
   }
   const double* y = Y + (int64_t)c * n_pad;
-  ternarize_wg([=](int64_t j) { return y[j]; }, n, n_pad, tau, dst, nullptr);
+  ternarize_wg([=](int64_t j) { return y[j]; }, nullptr, n, n_pad, tau, dst);
 }
 
 // U <- T_tau(Z[:, c]); also g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for
 // the joint scale solve (Eq. (4)).  grid: BBP.
-__global__ __launch_bounds__(NT) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q,
-                                               int64_t m, int64_t m_pad, int bb, double tau,
-                                               int8_t* __restrict__ Ut, double* __restrict__ gvec) {
-  __shared__ double shd[16];
+__global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q,
+                                                    int64_t m, int64_t m_pad, int bb, double tau,
+                                                    int8_t* __restrict__ Ut, double* __restrict__ gvec) {
   const int c = blockIdx.x;
   int8_t* dst = Ut + (int64_t)c * m_pad;
   if (c >= bb) {
-    for (int64_t i = threadIdx.x; i < m_pad; i += NT) dst[i] = 0;
+    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) dst[i] = 0;
     if (threadIdx.x == 0) gvec[c] = 0.0;
     return;
   }
   const double* z = Z + (int64_t)c * m_pad;
-  ternarize_wg([=](int64_t i) { return z[i]; }, m, m_pad, tau, dst, nullptr);
-  const double* q = Q + (int64_t)c * m_pad;
-  double acc = 0.0;
-  for (int64_t i = threadIdx.x; i < m; i += NT) acc += (double)dst[i] * q[i];
-  acc = block_sum_d(acc, shd);
-  if (threadIdx.x == 0) gvec[c] = acc;
+  const double g = ternarize_wg([=](int64_t i) { return z[i]; }, Q + (int64_t)c * m_pad, m, m_pad, tau, dst);
+  if (threadIdx.x == 0) gvec[c] = g;
 }
 
 // Block initialisation (paper silent; reading: U[:, c] = T_tau(R[:, J_c])).
 // grid: BBP.
-__global__ __launch_bounds__(NT) void k_init(const float* __restrict__ R, const int* __restrict__ J, int64_t m,
+__global__ __launch_bounds__(NT_TERN) void k_init(const float* __restrict__ R, const int* __restrict__ J, int64_t m,
                                              int64_t m_pad, int64_t n_pad, int bb, double tau,
                                              int8_t* __restrict__ Ut) {
   const int c = blockIdx.x;
   int8_t* dst = Ut + (int64_t)c * m_pad;
   if (c >= bb) {
-    for (int64_t i = threadIdx.x; i < m_pad; i += NT) dst[i] = 0;
+    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) dst[i] = 0;
     return;
   }
   int jc = J[c];
   jc = jc < 0 ? 0 : (jc >= n_pad ? (int)(n_pad - 1) : jc);  // J comes from k_select; keep reads in bounds
   const float* col = R + jc;
-  ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, m, m_pad, tau, dst, nullptr);
+  ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, nullptr, m, m_pad, tau, dst);
 }
 
 // Xt (BBP x L int8, component-major) -> Xr (L x BBP, row-major).
@@ -686,7 +864,7 @@ __global__ __launch_bounds__(NT) void k_transpose8(const int8_t* __restrict__ Xt
 
 // ---------------------------------------------------------------------------
 // Joint scale solve, Eq. (4): M = (U^T U) o (V^T H V) (+ delta I),
-// d = M^{-1} g.  grid: NSIDE (partial U^T U on int8 MFMA, last WG solves).
+// d = M^{-1} g.  grid: NSIDE_INT (partial U^T U on int8 MFMA, last WG solves).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NT) void k_scale(const int8_t* __restrict__ Ut, int64_t m_pad, int bb,
                                               const double* __restrict__ gramV, const double* __restrict__ gvec,
@@ -694,22 +872,16 @@ __global__ __launch_bounds__(NT) void k_scale(const int8_t* __restrict__ Ut, int
                                               float* Dout) {
   __shared__ int red[4096];
   __shared__ double Gs[4096];
-  __shared__ double colbuf[128];
-  __shared__ double s_tr;
-  if (!side_gram_int(Ut, m_pad, blockIdx.x, gparti, counter, Gs, red)) return;
+  __shared__ double colbuf[256];
+  __shared__ double s_trb[16];
+  if (!side_gram_int(Ut, m_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red)) return;
   const int t = threadIdx.x;
   for (int e = t; e < 4096; e += NT) {
     const int r = e >> 6, c = e & 63;
     Gs[e] = (r < bb && c < bb) ? Gs[e] * gramV[e] : ((r == c) ? 1.0 : 0.0);
   }
   __syncthreads();
-  if (t == 0) {
-    double tr = 0.0;
-    for (int c = 0; c < bb; ++c) tr += Gs[c * 64 + c];
-    s_tr = tr;
-  }
-  __syncthreads();
-  const double tr = s_tr;
+  const double tr = block_sum_d((t < bb) ? Gs[t * 64 + t] : 0.0, s_trb);
   if (tr == 0.0) {
     if (t < BBP) {
       dvec[t] = 0.0;
@@ -973,6 +1145,7 @@ __device__ void reduce_colE(const double* __restrict__ colE_part, int gd, int64_
   double s = 0.0, sw = 0.0;
   for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
     double c = 0.0;
+#pragma unroll 8
     for (int g = 0; g < gd; ++g) c += colE_part[(int64_t)g * n_pad + j];
     if (j >= n) c = 0.0;
     if (colE && j < n) colE[j] = c;
@@ -1024,15 +1197,43 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
       if ((kb & hmask) == prefix) atomicAdd(&hist[(kb >> shift) & 0xff], 1u);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      int need = s_need;
-      int d = 255;
-      for (; d > 0; --d) {
-        if ((int)hist[d] >= need) break;
-        need -= (int)hist[d];
+    if (threadIdx.x < 64) {
+      // wave 0: lane l holds digits 255-4l .. 252-4l (descending); the
+      // first lane whose inclusive count reaches `need` holds the digit.
+      const int lane = threadIdx.x;
+      const int need = s_need;
+      int c[4], tot = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        c[q] = (int)hist[255 - 4 * lane - q];
+        tot += c[q];
       }
-      s_need = need;
-      s_prefix = prefix | ((unsigned long long)d << shift);
+      int incl = tot;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int u = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += u;
+      }
+      const unsigned long long hit = __ballot(incl >= need);
+      const int first = hit ? (__ffsll((long long)hit) - 1) : 63;
+      if (lane == first) {
+        int run = incl - tot, d = 0, nn = need;
+        bool found = false;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (!found && run + c[q] >= need) {
+            d = 255 - 4 * lane - q;
+            nn = need - run;
+            found = true;
+          }
+          if (!found) run += c[q];
+        }
+        if (!found) {
+          d = 0;
+          nn = need - run;
+        }
+        s_need = nn;
+        s_prefix = prefix | ((unsigned long long)d << shift);
+      }
     }
     __syncthreads();
   }
@@ -1196,17 +1397,17 @@ __global__ __launch_bounds__(NT) void k_load_cm(double* Xcm, const double* X, in
 
 
 // Gram of V alone (raw V^T H V and its ridge inverse), for the scale step
-// entry point.  grid: NSIDE.
+// entry point.  grid: NSIDE_INT or NSIDE_W.
 template <bool WEIGHTED>
 __global__ __launch_bounds__(NT) void k_gram_v(const int8_t* __restrict__ Vt, const int8_t* __restrict__ Vr,
                                                const double* __restrict__ hw, int64_t n_pad, int bb, int* gparti,
                                                double* gpart, unsigned* counter, double* ginvV, double* gramV) {
   __shared__ int red[4096];
   __shared__ double Gs[4096];
-  __shared__ double colbuf[128];
+  __shared__ double colbuf[256];
   bool last;
-  if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, gpart, counter, Gs);
-  else last = side_gram_int(Vt, n_pad, blockIdx.x, gparti, counter, Gs, red);
+  if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, (int)gridDim.x, gpart, counter, Gs);
+  else last = side_gram_int(Vt, n_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red);
   if (!last) return;
   for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
   __syncthreads();
@@ -1282,53 +1483,59 @@ hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2,
 }
 
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
-  hipLaunchKernelGGL(k_init, dim3(BBP), dim3(NT), 0, s, w.R, w.J, w.m, w.m_pad, w.n_pad, bb, tau, w.Ut);
+  hipLaunchKernelGGL(k_init, dim3(BBP), dim3(NT_TERN), 0, s, w.R, w.J, w.m, w.m_pad, w.n_pad, bb, tau, w.Ut);
   return hipGetLastError();
 }
 
-hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s) {
-  const unsigned grid = (unsigned)(NSIDE + (w.n_pad / TILE) * w.gv);
-  hipLaunchKernelGGL(k_vstep, dim3(grid), dim3(NT), 0, s, w.R, w.Ut, w.Pp, w.maxbits + blk, w.m_pad, w.n_pad, w.gv,
-                     bb, w.gparti, w.counters + CNT_GRAM_U, w.ginvU);
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
+  const unsigned grid = (unsigned)(NSIDE_INT + (w.n_pad / TILE) * w.gv);
+  EXTERND_TIMED(tm, EXTERND_KCLASS_VSTEP,
+                hipLaunchKernelGGL(k_vstep, dim3(grid), dim3(NT), 0, s, w.R, w.Ut, w.Pp, w.maxbits + blk, w.m_pad,
+                                   w.n_pad, w.gv, bb, w.gparti, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_INT));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_vepi, dim3((unsigned)(w.n_pad / TILE)), dim3(NT), 0, s, w.Pp, w.gv, w.ginvU, w.Y,
                      w.maxbits + blk, w.n_pad);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.Vt);
+  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.Vt);
   return hipGetLastError();
 }
 
-hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s) {
+hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* tm) {
   hipError_t e;
-  const unsigned grid = (unsigned)(NSIDE + w.m_pad / TILE);
+  const unsigned nside = weighted ? NSIDE_W : NSIDE_INT;
+  const unsigned grid = (unsigned)(nside + w.m_pad / TILE);
   if (weighted) {
     hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_ustep<true>, dim3(grid), dim3(NT), 0, s, w.R, w.Vt, w.Vr, w.hw, w.Q, w.maxbits_w + blk,
-                       w.m_pad, w.n_pad, bb, w.gparti, w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
+    EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
+                  hipLaunchKernelGGL(k_ustep<true>, dim3(grid), dim3(NT), 0, s, w.R, w.Vt, w.Vr, w.hw, w.Q,
+                                     w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gparti, w.gpart,
+                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside));
   } else {
-    hipLaunchKernelGGL(k_ustep<false>, dim3(grid), dim3(NT), 0, s, w.R, w.Vt, w.Vr, w.hw, w.Q, w.maxbits + blk,
-                       w.m_pad, w.n_pad, bb, w.gparti, w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
+    EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
+                  hipLaunchKernelGGL(k_ustep<false>, dim3(grid), dim3(NT), 0, s, w.R, w.Vt, w.Vr, w.hw, w.Q,
+                                     w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gparti, w.gpart,
+                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside));
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_uepi, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0, s, w.Q, w.ginvV, w.Z, w.m_pad);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.Ut, w.gvec);
+  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.Ut, w.gvec);
   return hipGetLastError();
 }
 
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
-  hipLaunchKernelGGL(k_scale, dim3(NSIDE), dim3(NT), 0, s, w.Ut, w.m_pad, bb, w.gramV, w.gvec, w.gparti,
+  hipLaunchKernelGGL(k_scale, dim3(NSIDE_INT), dim3(NT), 0, s, w.Ut, w.m_pad, bb, w.gramV, w.gvec, w.gparti,
                      w.counters + CNT_SCALE, w.dvec, w.dF, (float*)nullptr);
   return hipGetLastError();
 }
 
-hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s) {
+hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s, Timer* tm) {
   hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.m_pad / 32)), dim3(NT), 0, s, w.Ut, w.Ur, w.m_pad);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1336,8 +1543,9 @@ hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s) {
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
-  hipLaunchKernelGGL(k_deflate, dim3(grid), dim3(NT), 0, s, w.R, w.Ur, w.Vr, w.dF, w.colE_part,
-                     w.maxbits + blk + 1, w.maxbits_w + blk + 1, w.hw, w.m_pad, w.n_pad, w.gd);
+  EXTERND_TIMED(tm, EXTERND_KCLASS_DEFLATE,
+                hipLaunchKernelGGL(k_deflate, dim3(grid), dim3(NT), 0, s, w.R, w.Ur, w.Vr, w.dF, w.colE_part,
+                                   w.maxbits + blk + 1, w.maxbits_w + blk + 1, w.hw, w.m_pad, w.n_pad, w.gd));
   return hipGetLastError();
 }
 
@@ -1374,10 +1582,10 @@ hipError_t launch_load_cm(double* Xcm, const double* X, int64_t len, int64_t len
 
 hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s) {
   if (weighted)
-    hipLaunchKernelGGL(k_gram_v<true>, dim3(NSIDE), dim3(NT), 0, s, w.Vt, w.Vr, w.hw, w.n_pad, bb, w.gparti, w.gpart,
+    hipLaunchKernelGGL(k_gram_v<true>, dim3(NSIDE_W), dim3(NT), 0, s, w.Vt, w.Vr, w.hw, w.n_pad, bb, w.gparti, w.gpart,
                        w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
   else
-    hipLaunchKernelGGL(k_gram_v<false>, dim3(NSIDE), dim3(NT), 0, s, w.Vt, w.Vr, w.hw, w.n_pad, bb, w.gparti,
+    hipLaunchKernelGGL(k_gram_v<false>, dim3(NSIDE_INT), dim3(NT), 0, s, w.Vt, w.Vr, w.hw, w.n_pad, bb, w.gparti,
                        w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
   return hipGetLastError();
 }
