@@ -115,7 +115,7 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="down9728")
-    ap.add_argument("--cpu-blocks", type=int, default=6, help="oracle sample size in blocks (0 = skip)")
+    ap.add_argument("--cpu-blocks", type=int, default=40, help="oracle sample size in blocks (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0, help="run only a copy of this many bytes")
     args = ap.parse_args()
 
