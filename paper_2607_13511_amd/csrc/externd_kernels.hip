@@ -134,7 +134,7 @@ __device__ __forceinline__ void wave_argmax(double& v, long long& i) {
 }
 
 // Block-wide sum over NT threads, result broadcast to all threads.
-__device__ double block_sum_d(double v, double* sh /* >= NT/64 */) {
+__device__ __forceinline__ double block_sum_d(double v, double* sh /* >= NT/64 */) {
   v = wave_sum_d(v);
   if (lane_id() == 0) sh[wave_id()] = v;
   __syncthreads();
@@ -143,7 +143,7 @@ __device__ double block_sum_d(double v, double* sh /* >= NT/64 */) {
   __syncthreads();
   return r;
 }
-__device__ int block_sum_i(int v, int* sh) {
+__device__ __forceinline__ int block_sum_i(int v, int* sh) {
   v = wave_sum_i(v);
   if (lane_id() == 0) sh[wave_id()] = v;
   __syncthreads();
@@ -152,7 +152,7 @@ __device__ int block_sum_i(int v, int* sh) {
   __syncthreads();
   return r;
 }
-__device__ void block_argmax(double& v, long long& i, double* shv, long long* shi) {
+__device__ __forceinline__ void block_argmax(double& v, long long& i, double* shv, long long* shi) {
   wave_argmax(v, i);
   if (lane_id() == 0) {
     shv[wave_id()] = v;
@@ -168,26 +168,64 @@ __device__ void block_argmax(double& v, long long& i, double* shv, long long* sh
 }
 
 // ---------------------------------------------------------------------------
-// 64x64 SPD inverse by the symmetric sweep operator with 2x2 pivot blocks
-// (block Gauss-Jordan without pivoting, stable for SPD).  A: LDS 64x64
-// row-major, in: matrix, out: inverse.  colbuf: LDS 2 x 2 x 64 doubles.
+// 64x64 SPD inverse: block sweep operator (block Gauss-Jordan without
+// pivoting, stable for SPD) with 4x4 pivot blocks and fp64 MFMA updates.
+// A: LDS 64x64 row-major, in: matrix, out: inverse.  pbuf: LDS 1024 doubles.
 // Requires blockDim.x == 256.
 //
 // The matrix is first scaled exactly by powers of two, A~ = S A S with
 // S = diag(2^-e_i), so that every diagonal entry lies in [0.5, 2); then
-// A^{-1} = S A~^{-1} S.  Sweeping the pivot block K = {k, k+1} with
-// P = A~_KK maps A_ij -> A_ij - A_iK P^{-1} A_Kj (i, j not in K),
-// A_iK -> A_iK P^{-1}, A_Kj -> P^{-1} A_Kj, A_KK -> -P^{-1}; after all
-// blocks the matrix is -A~^{-1}.  With C = A~[:, K] - E_K (published
-// through LDS) all cases are the single update A -= (C P^{-1}) C^T, except
-// the diagonal of the pivot block, which needs a further -2.  Thread t keeps
-// the 4x4 block (rows 4 (t/16) + r, columns 4 (t%16) + c) in registers; one
-// barrier per pivot block.
+// A^{-1} = S A~^{-1} S.  Sweeping the pivot block K (4 indices) with
+// P = A~_KK maps A_ij -> A_ij - A_iK P^{-1} A_Kj (i, j outside K),
+// A_iK -> A_iK P^{-1}, A_Kj -> P^{-1} A_Kj, A_KK -> -P^{-1}; after all 16
+// blocks the matrix is -A~^{-1}.  With C = A~[:, K] - E_K all four cases
+// are the single rank-4 update A -= (C P^{-1}) C^T, except the diagonal of
+// the pivot block, which needs a further -2.
+//
+// Wave w holds tile row w of A in v_mfma_f64_16x16x4f64 accumulators
+// (lane l, register r, tile nt <-> A[16 w + l/16 + 4 r][16 nt + l%16]);
+// each step publishes C through LDS, every thread forms P^{-1} (closed
+// form by 2x2 Schur blocks) and one row of W = -C P^{-1}, and each wave
+// applies W C^T to its four tiles with four MFMAs.  Two barriers per step.
 // ---------------------------------------------------------------------------
-__device__ void spd_inverse64(double* A, double* colbuf) {
+__device__ __forceinline__ v4d mfma_f64(double a, double b, v4d c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+// Inverse of the symmetric 4x4 block [[A, B], [B^T, D]] (2x2 blocks) by the
+// Schur complement S = D - B^T A^{-1} B; uses the upper triangle of P.
+__device__ __forceinline__ void spd_inverse4(const double (&P)[4][4], double (&Pi)[4][4]) {
+  const double ra = 1.0 / (P[0][0] * P[1][1] - P[0][1] * P[0][1]);
+  const double a00 = P[1][1] * ra, a01 = -P[0][1] * ra, a11 = P[0][0] * ra;
+  // X = A^{-1} B
+  const double x00 = a00 * P[0][2] + a01 * P[1][2], x01 = a00 * P[0][3] + a01 * P[1][3];
+  const double x10 = a01 * P[0][2] + a11 * P[1][2], x11 = a01 * P[0][3] + a11 * P[1][3];
+  // S = D - B^T X
+  const double s00 = P[2][2] - (P[0][2] * x00 + P[1][2] * x10);
+  const double s01 = P[2][3] - (P[0][2] * x01 + P[1][2] * x11);
+  const double s11 = P[3][3] - (P[0][3] * x01 + P[1][3] * x11);
+  const double rs = 1.0 / (s00 * s11 - s01 * s01);
+  const double t00 = s11 * rs, t01 = -s01 * rs, t11 = s00 * rs;
+  // Y = X S^{-1}
+  const double y00 = x00 * t00 + x01 * t01, y01 = x00 * t01 + x01 * t11;
+  const double y10 = x10 * t00 + x11 * t01, y11 = x10 * t01 + x11 * t11;
+  Pi[0][0] = a00 + (y00 * x00 + y01 * x01);
+  Pi[0][1] = a01 + (y00 * x10 + y01 * x11);
+  Pi[1][0] = Pi[0][1];
+  Pi[1][1] = a11 + (y10 * x10 + y11 * x11);
+  Pi[0][2] = -y00; Pi[0][3] = -y01;
+  Pi[1][2] = -y10; Pi[1][3] = -y11;
+  Pi[2][0] = -y00; Pi[3][0] = -y01;
+  Pi[2][1] = -y10; Pi[3][1] = -y11;
+  Pi[2][2] = t00; Pi[2][3] = t01;
+  Pi[3][2] = t01; Pi[3][3] = t11;
+}
+
+__device__ __forceinline__ void spd_inverse64(double* A, double* pbuf) {
   __shared__ int sexp[64];
   const int t = threadIdx.x;
-  const int rb = t >> 4, cb = t & 15;
+  const int lane = t & 63, w = t >> 6;
+  const int lr = lane >> 4, lc = lane & 15;
   if (t < 64) {
     int E = 0;
     frexp(A[t * 65], &E);
@@ -197,73 +235,61 @@ __device__ void spd_inverse64(double* A, double* colbuf) {
   int er[4], ec[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    er[q] = sexp[4 * rb + q];
-    ec[q] = sexp[4 * cb + q];
+    er[q] = sexp[16 * w + lr + 4 * q];
+    ec[q] = sexp[16 * q + lc];
   }
-  double a[4][4];
+  v4d acc[4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) a[r][c] = ldexp(A[(4 * rb + r) * 64 + 4 * cb + c], -(er[r] + ec[c]));
-  // publish pivot columns 0, 1 minus the identity
-  if (cb == 0) {
+    for (int r = 0; r < 4; ++r)
+      acc[nt][r] = ldexp(A[(16 * w + lr + 4 * r) * 64 + 16 * nt + lc], -(er[r] + ec[nt]));
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int i = 4 * rb + r;
-      colbuf[i] = a[r][0] - (i == 0 ? 1.0 : 0.0);
-      colbuf[64 + i] = a[r][1] - (i == 1 ? 1.0 : 0.0);
-    }
-  }
-  __syncthreads();
-  for (int kp = 0; kp < 32; ++kp) {
-    const int k = 2 * kp;
-    const double* c0 = colbuf + (kp & 1) * 128;
-    const double* c1 = c0 + 64;
-    double u0[4], u1[4], v0[4], v1[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      u0[r] = c0[4 * rb + r];
-      u1[r] = c1[4 * rb + r];
-      v0[r] = c0[4 * cb + r];
-      v1[r] = c1[4 * cb + r];
-    }
-    const double p00 = c0[k] + 1.0, p01 = c1[k], p11 = c1[k + 1] + 1.0;
-    const double idet = 1.0 / (p00 * p11 - p01 * p01);
-    const double q00 = p11 * idet, q01 = -p01 * idet, q11 = p00 * idet;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const double w0 = u0[r] * q00 + u1[r] * q01;
-      const double w1 = u0[r] * q01 + u1[r] * q11;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) a[r][c] = fma(-w0, v0[c], fma(-w1, v1[c], a[r][c]));
-    }
-    if (rb == (k >> 2) && cb == (k >> 2)) {
-      if ((k & 3) == 0) {
-        a[0][0] -= 2.0;
-        a[1][1] -= 2.0;
-      } else {
-        a[2][2] -= 2.0;
-        a[3][3] -= 2.0;
-      }
-    }
-    const int k2 = k + 2;
-    if (k2 < 64 && cb == (k2 >> 2)) {
-      double* n0 = colbuf + ((kp + 1) & 1) * 128;
-      double* n1 = n0 + 64;
-      const bool lo = (k2 & 3) == 0;
+  for (int K = 0; K < 16; ++K) {
+    double* Cb = pbuf + (K & 1) * 512;  // C[i][c] at Cb[c * 64 + i]
+    double* Wb = Cb + 256;              // -W[i][b] at Wb[b * 64 + i]
+    const int ntK = K >> 2, jK = 4 * (K & 3);
+    // (1) publish the pivot columns 4K .. 4K+3 minus the identity
+    if (lc >= jK && lc < jK + 4) {
+      const int cp = lc - jK;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int i = 4 * rb + r;
-        n0[i] = (lo ? a[r][0] : a[r][2]) - (i == k2 ? 1.0 : 0.0);
-        n1[i] = (lo ? a[r][1] : a[r][3]) - (i == k2 + 1 ? 1.0 : 0.0);
+        const int row = 16 * w + lr + 4 * r;
+        Cb[cp * 64 + row] = acc[ntK][r] - (row == 4 * K + cp ? 1.0 : 0.0);
       }
     }
     __syncthreads();
+    // (2) P^{-1} (every thread, same inputs) and one entry of -W = -C P^{-1}
+    double P[4][4], Pi[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = a; b < 4; ++b) {
+        P[a][b] = Cb[b * 64 + 4 * K + a] + (a == b ? 1.0 : 0.0);
+        P[b][a] = P[a][b];
+      }
+    spd_inverse4(P, Pi);
+    {
+      const int i = t & 63, b = t >> 6;
+      double sacc = 0.0;
+#pragma unroll
+      for (int a = 0; a < 4; ++a) sacc = fma(Cb[a * 64 + i], Pi[a][b], sacc);
+      Wb[b * 64 + i] = -sacc;
+    }
+    __syncthreads();
+    // (3) rank-4 update of the wave's tile row on fp64 MFMA
+    const double aop = Wb[lr * 64 + 16 * w + lc];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma_f64(aop, Cb[lr * 64 + 16 * nt + lc], acc[nt]);
+    // (4) the pivot block's diagonal
+    if (w == ntK && lc == jK + lr) acc[ntK][K & 3] -= 2.0;
   }
+  __syncthreads();
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) A[(4 * rb + r) * 64 + 4 * cb + c] = -ldexp(a[r][c], -(er[r] + ec[c]));
+    for (int r = 0; r < 4; ++r)
+      A[(16 * w + lr + 4 * r) * 64 + 16 * nt + lc] = -ldexp(acc[nt][r], -(er[r] + ec[nt]));
   __syncthreads();
 }
 
@@ -271,7 +297,7 @@ __device__ void spd_inverse64(double* A, double* colbuf) {
 // (G + eps I) on the real block and the identity on the padding, invert,
 // and write the inverse.  Zero trace -> zero inverse on the real block
 // (every component is zero, Eq. (3) target is zero).
-__device__ void ridge_invert_store(double* G, double* colbuf, int bb, double* ginv_out) {
+__device__ __forceinline__ void ridge_invert_store(double* G, double* colbuf, int bb, double* ginv_out) {
   __shared__ double shd[16];
   const int t = threadIdx.x;
   const double tr = block_sum_d((t < bb) ? G[t * 64 + t] : 0.0, shd);
@@ -301,7 +327,7 @@ __device__ void ridge_invert_store(double* G, double* colbuf, int bb, double* gi
 // summed in LDS (integer adds, order-free) and written to gparti[side].
 // Returns true in the last of the nside workgroups to finish, with the
 // complete Gram in G (LDS, fp64).
-__device__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side, int nside, int* gparti,
+__device__ __forceinline__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side, int nside, int* gparti,
                               unsigned* counter, double* G, int* ired /* LDS 4096 */) {
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
@@ -367,15 +393,23 @@ __device__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side
 // 16x16 tiles of the upper triangle are dealt to the 4 waves; each wave
 // covers all of the workgroup's rows for its tiles.  Same last-workgroup
 // protocol as side_gram_int.
-__device__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restrict__ hw, int64_t L, int side,
+__device__ __forceinline__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restrict__ hw, int64_t L, int side,
                             int nside, double* gpart, unsigned* counter, double* G) {
   const int lane = lane_id(), wave = wave_id();
   const int i16 = lane & 15, kq = lane >> 4;
   const int64_t nks = L / 4;
   const int64_t ks0 = side * nks / nside, ks1 = (side + 1) * nks / nside;
-  // tile t in 0..9 -> (mt, nt), mt <= nt, row-major over the upper triangle
-  const int TM[10] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
-  const int TN[10] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
+  // tile tt in 0..9 -> (mt, nt), mt <= nt, row-major over the upper
+  // triangle (rows start at 0, 4, 7, 9); wave w takes tt = w, w + 4, w + 8
+  int TMq[3], TNq[3];
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    const int tt = wave + 4 * q;
+    const int mt = (tt >= 4) + (tt >= 7) + (tt >= 9);
+    const int start = (mt == 0) ? 0 : (mt == 1) ? 4 : (mt == 2) ? 7 : 9;
+    TMq[q] = mt;
+    TNq[q] = mt + (tt - start);
+  }
   v4d acc[3] = {v4d{}, v4d{}, v4d{}};
   const int ntile = (wave < 2) ? 3 : 2;
   for (int64_t ks = ks0; ks < ks1; ++ks) {
@@ -388,8 +422,10 @@ __device__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restr
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
       if (q < ntile) {
-        const int tt = wave + 4 * q;
-        acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(w * v[TM[tt]], v[TN[tt]], acc[q], 0, 0, 0);
+        const int mt = TMq[q], nt = TNq[q];
+        const double va = (mt == 0) ? v[0] : (mt == 1) ? v[1] : (mt == 2) ? v[2] : v[3];
+        const double vb = (nt == 0) ? v[0] : (nt == 1) ? v[1] : (nt == 2) ? v[2] : v[3];
+        acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(w * va, vb, acc[q], 0, 0, 0);
       }
     }
   }
@@ -397,8 +433,7 @@ __device__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restr
 #pragma unroll
   for (int q = 0; q < 3; ++q) {
     if (q < ntile) {
-      const int tt = wave + 4 * q;
-      const int mt = TM[tt], nt = TN[tt];
+      const int mt = TMq[q], nt = TNq[q];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         // v_mfma_f64_16x16x4f64 result: lane l, register r holds row l/16 + 4 r, column l%16
@@ -469,7 +504,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                               unsigned* counter, double* ginvU, int nside) {
   __shared__ int red[8 * RED_TILE];
   __shared__ double Gs[4096];
-  __shared__ double colbuf[256];
+  __shared__ double colbuf[1024];
   if ((int)blockIdx.x < nside) {
     if (side_gram_int(Ut, m_pad, blockIdx.x, nside, gparti, counter, Gs, red)) ridge_invert_store(Gs, colbuf, bb, ginvU);
     return;
@@ -550,7 +585,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                               unsigned* counter, double* ginvV, double* gramV, int nside) {
   __shared__ int red[8 * RED_TILE];
   __shared__ double Gs[4096];
-  __shared__ double colbuf[256];
+  __shared__ double colbuf[1024];
   if ((int)blockIdx.x < nside) {
     bool last;
     if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, nside, gpart, counter, Gs);
@@ -723,10 +758,10 @@ __global__ __launch_bounds__(NT) void k_uepi(const double* __restrict__ Q, const
 // are loaded once and kept in registers for the threshold pass.  With an
 // auxiliary vector q (may be null) it also returns sum_i t_i q_i (fp64).
 // ---------------------------------------------------------------------------
-constexpr int TERN_CACHE = 16;
+constexpr int TERN_CACHE = 12;
 
 template <typename Load>
-__device__ double ternarize_wg(Load load, const double* __restrict__ q, int64_t L, int64_t L_pad, double tau,
+__device__ __forceinline__ double ternarize_wg(Load load, const double* __restrict__ q, int64_t L, int64_t L_pad, double tau,
                                int8_t* dst) {
   __shared__ double shd[16];
   __shared__ long long shl[16];
@@ -872,7 +907,7 @@ __global__ __launch_bounds__(NT) void k_scale(const int8_t* __restrict__ Ut, int
                                               float* Dout) {
   __shared__ int red[4096];
   __shared__ double Gs[4096];
-  __shared__ double colbuf[256];
+  __shared__ double colbuf[1024];
   __shared__ double s_trb[16];
   if (!side_gram_int(Ut, m_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red)) return;
   const int t = threadIdx.x;
@@ -1139,7 +1174,7 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
 // pattern orders like the value); exact radix select of the bb-th largest
 // key, ties broken towards the smaller column index.
 // ---------------------------------------------------------------------------
-__device__ void reduce_colE(const double* __restrict__ colE_part, int gd, int64_t n, int64_t n_pad,
+__device__ __forceinline__ void reduce_colE(const double* __restrict__ colE_part, int gd, int64_t n, int64_t n_pad,
                             const double* __restrict__ hw, double* colE, double* out_fro2, double* out_fro2w,
                             double* shd) {
   double s = 0.0, sw = 0.0;
@@ -1404,7 +1439,7 @@ __global__ __launch_bounds__(NT) void k_gram_v(const int8_t* __restrict__ Vt, co
                                                double* gpart, unsigned* counter, double* ginvV, double* gramV) {
   __shared__ int red[4096];
   __shared__ double Gs[4096];
-  __shared__ double colbuf[256];
+  __shared__ double colbuf[1024];
   bool last;
   if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, (int)gridDim.x, gpart, counter, Gs);
   else last = side_gram_int(Vt, n_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red);
