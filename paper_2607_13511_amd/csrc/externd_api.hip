@@ -31,9 +31,9 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   L.m_pad = round_up(m, TILE);
   L.n_pad = round_up(n, TILE);
   const int64_t nct = L.n_pad / TILE, nrt = L.m_pad / TILE;
-  // V-step: about 320 column-tile x row-group workgroups; deflation and
+  // V-step: about 480 column-tile x row-group workgroups; deflation and
   // staging: about 640.
-  L.gv = clampi((320 + nct - 1) / nct, 1, nrt < 16 ? nrt : 16);
+  L.gv = clampi((480 + nct - 1) / nct, 1, nrt < 16 ? nrt : 16);
   L.gd = clampi((640 + nct - 1) / nct, 1, nrt < 64 ? nrt : 64);
   L.nblk_cap = (int)(k + 2);  // fro2 before every block and after the last; one spare
   const size_t sizes[] = {
@@ -63,6 +63,8 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(unsigned) * CNT_COUNT,                    // 23 counters
       sizeof(int) * FLAG_COUNT,                        // 24 flags
       sizeof(unsigned) * (size_t)L.nblk_cap,           // 25 maxbits_w
+      (size_t)(BBP * L.m_pad),                         // 26 Umf
+      (size_t)(BBP * L.n_pad),                         // 27 Vmf
   };
   size_t o = 0;
   for (size_t i = 0; i < sizeof(sizes) / sizeof(sizes[0]); ++i) {
@@ -112,6 +114,8 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.counters = (unsigned*)(b + L.off[23]);
   w.flags = (int*)(b + L.off[24]);
   w.maxbits_w = (unsigned*)(b + L.off[25]);
+  w.Umf = (int8_t*)(b + L.off[26]);
+  w.Vmf = (int8_t*)(b + L.off[27]);
   return true;
 }
 
@@ -343,7 +347,7 @@ int externd_step_vstep(const float* R, int64_t m, int64_t n, const int8_t* U, in
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(launch_prep(w, nullptr, s));
   HIP_TRY(launch_stage(w, R, n, s));
-  HIP_TRY(launch_load_factor(w.Ut, w.Ur, U, m, w.m_pad, bb, s));
+  HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
   HIP_TRY(launch_vstep(w, 0, bb, tau, s));
   HIP_TRY(launch_store_factor(V_out, w.Vt, n, w.n_pad, bb, s));
   if (Y_out_or_null) {
@@ -364,7 +368,7 @@ int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, in
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(launch_prep(w, h, s));
   HIP_TRY(launch_stage(w, R, n, s));
-  HIP_TRY(launch_load_factor(w.Vt, w.Vr, V, n, w.n_pad, bb, s));
+  HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
   HIP_TRY(launch_ustep(w, 0, bb, tau, h != nullptr, s));
   HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
   if (Q_out_or_null) HIP_TRY(launch_store_cm(Q_out_or_null, w.Q, m, w.m_pad, bb, s));
@@ -380,8 +384,8 @@ int externd_step_scale(const int8_t* U, const int8_t* V, const double* Q, int64_
   if (!carve(w, ws, ws_bytes, m, n, 0)) return EXTERND_EWORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(launch_prep(w, h, s));
-  HIP_TRY(launch_load_factor(w.Ut, w.Ur, U, m, w.m_pad, bb, s));
-  HIP_TRY(launch_load_factor(w.Vt, w.Vr, V, n, w.n_pad, bb, s));
+  HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
+  HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
   HIP_TRY(launch_load_cm(w.Q, Q, m, w.m_pad, bb, s));
   HIP_TRY(launch_gram_only(w, bb, h != nullptr, s));
   HIP_TRY(launch_gvec(w, bb, s));
@@ -400,8 +404,8 @@ int externd_step_deflate(float* R, int64_t m, int64_t n, const int8_t* U, const 
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(launch_prep(w, nullptr, s));
   HIP_TRY(launch_stage(w, R, n, s));
-  HIP_TRY(launch_load_factor(w.Ut, w.Ur, U, m, w.m_pad, bb, s));
-  HIP_TRY(launch_load_factor(w.Vt, w.Vr, V, n, w.n_pad, bb, s));
+  HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
+  HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
   HIP_TRY(launch_set_scales(w, d, bb, s));
   HIP_TRY(launch_deflate(w, 0, s));
   HIP_TRY(launch_unstage(w, R, s));

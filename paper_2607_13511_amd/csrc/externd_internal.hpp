@@ -40,6 +40,8 @@ struct Ws {
   int8_t* Ur;            // m_pad x BBP, U row-major
   int8_t* Vt;            // BBP x n_pad
   int8_t* Vr;            // n_pad x BBP
+  int8_t* Umf;           // BBP x m_pad bytes, U in the MFMA-ready operand layout
+  int8_t* Vmf;           // BBP x n_pad bytes, V in the MFMA-ready operand layout
   double* Q;             // BBP x m_pad, Q = R diag(h) V  (component-major)
   double* Z;             // BBP x m_pad, U-step target
   long long* Pp;         // gv x BBP x n_pad, V-step partial contractions
@@ -101,7 +103,7 @@ hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s, Timer* t = nullpt
 hipError_t launch_emit(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp,
                        float* D, hipStream_t s);
 // step-entry helpers
-hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, const int8_t* X, int64_t len, int64_t len_pad,
+hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len, int64_t len_pad,
                               int bb, hipStream_t s);
 hipError_t launch_store_factor(int8_t* X, const int8_t* Xt, int64_t len, int64_t len_pad, int bb, hipStream_t s);
 hipError_t launch_store_cm(double* X, const double* Xcm, int64_t len, int64_t len_pad, int bb,

@@ -37,6 +37,8 @@ typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef short v8s __attribute__((ext_vector_type(8)));
 typedef double v4d __attribute__((ext_vector_type(4)));
+typedef double v2d __attribute__((ext_vector_type(2)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // small helpers
@@ -99,6 +101,82 @@ __device__ __forceinline__ void make_planes(const unsigned (&y)[16], v4i (&P)[4]
 
 __device__ __forceinline__ v16i mfma_i8(v4i a, v4i b, v16i c) {
   return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+}
+
+// MFMA-ready layout of a ternary factor X (BBP components x L): for K step
+// ks (32 indices) and component half t, the 64 lanes' 16-byte operands of
+// v_mfma_i32_32x32x32_i8 are contiguous, lane l holding
+// X[32 t + l % 32][32 ks + 16 (l / 32) .. + 16).  Both operands of the
+// integer Gram and the ternary operand of either contraction load from it
+// with one fully coalesced 1 KB read per wave.
+__device__ __forceinline__ int64_t mf_offset(int c, int64_t i) {
+  return ((i >> 5) * 2 + (c >> 5)) * 1024 + ((c & 31) + 32 * ((i >> 4) & 1)) * 16 + (i & 15);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ unsigned lds_addr(const void* p) { return (unsigned)(uintptr_t)(const lds_void*)p; }
+
+// Four 16-byte LDS reads after waiting until at most VM vector-memory
+// operations of this wave are outstanding.  Direct-to-LDS loads
+// (global_load_lds) complete in issue order with the other vector loads,
+// so VM = the number of direct loads issued after the ones being read
+// makes their data visible.  Written as one asm block because the
+// compiler otherwise waits for every outstanding direct load before any
+// LDS read.
+template <int VM>
+__device__ __forceinline__ void lds_read4_after(unsigned a0, unsigned a1, unsigned a2, unsigned a3, v4f& x0, v4f& x1,
+                                                v4f& x2, v4f& x3) {
+  asm volatile(
+      "s_waitcnt vmcnt(%8)\n\tds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\t"
+      "ds_read_b128 %3, %7\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3)
+      : "v"(a0), "v"(a1), "v"(a2), "v"(a3), "n"(VM)
+      : "memory");
+}
+// Eight 16-byte LDS reads (no vector-memory wait: issue after
+// lds_read4_after on the same stage).
+__device__ __forceinline__ void lds_read8(unsigned a, v2d (&x)[8]) {
+  asm volatile(
+      "ds_read_b128 %0, %8\n\tds_read_b128 %1, %8 offset:16\n\tds_read_b128 %2, %8 offset:32\n\t"
+      "ds_read_b128 %3, %8 offset:48\n\tds_read_b128 %4, %8 offset:64\n\tds_read_b128 %5, %8 offset:80\n\t"
+      "ds_read_b128 %6, %8 offset:96\n\tds_read_b128 %7, %8 offset:112\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(x[4]), "=&v"(x[5]), "=&v"(x[6]), "=&v"(x[7])
+      : "v"(a)
+      : "memory");
+}
+
+// Planes of one wave's accumulators combined exactly into int64.
+__device__ __forceinline__ long long combine_acc(const v16i (&acc)[2][4], int t, int r) {
+  return (long long)acc[t][0][r] + ((long long)acc[t][1][r] << 8) + ((long long)acc[t][2][r] << 16) +
+         ((long long)acc[t][3][r] << 24);
+}
+
+// Sum of the 4 waves' contraction tiles (2 tiles of 32x32, MFMA output
+// layout) through LDS (red: 8192 int64 = 64 KB).  Wave w finishes slots
+// 8w .. 8w + 7; out(t, M, N, v) receives every entry once, M the tile row
+// and N the tile column.  Integer sums: exact and order-free.
+template <typename Out>
+__device__ __forceinline__ void reduce_waves(long long* red, const v16i (&acc)[2][4], Out out) {
+  const int lane = lane_id(), wave = wave_id();
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) red[(wave * 32 + t * 16 + r) * 64 + lane] = combine_acc(acc, t, r);
+  __syncthreads();
+  long long v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int slot = wave * 8 + i;
+    v[i] = red[slot * 64 + lane] + red[(32 + slot) * 64 + lane] + red[(64 + slot) * 64 + lane] +
+           red[(96 + slot) * 64 + lane];
+  }
+  __syncthreads();  // red may be reused by out()
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int slot = wave * 8 + i;
+    const int t = slot >> 4, r = slot & 15;
+    out(t, 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3), lane & 31, v[i]);
+  }
 }
 
 // Deterministic reductions: fixed shuffle tree, lane 0 holds the result.
@@ -184,9 +262,11 @@ __device__ __forceinline__ void block_argmax(double& v, long long& i, double* sh
 //
 // Wave w holds tile row w of A in v_mfma_f64_16x16x4f64 accumulators
 // (lane l, register r, tile nt <-> A[16 w + l/16 + 4 r][16 nt + l%16]);
-// each step publishes C through LDS, every thread forms P^{-1} (closed
-// form by 2x2 Schur blocks) and one row of W = -C P^{-1}, and each wave
-// applies W C^T to its four tiles with four MFMAs.  Two barriers per step.
+// the sweep keeps A symmetric, so C^T is the pivot rows minus E_K^T, held
+// by one wave: it publishes them through LDS, every lane forms P^{-1}
+// (closed form by 2x2 Schur blocks) and its entry of W = -C P^{-1}, and
+// each wave applies W C^T to its four tiles with four MFMAs.  One barrier
+// per step (the published rows are double-buffered).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ v4d mfma_f64(double a, double b, v4d c) {
   return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
@@ -244,47 +324,48 @@ __device__ __forceinline__ void spd_inverse64(double* A, double* pbuf) {
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       acc[nt][r] = ldexp(A[(16 * w + lr + 4 * r) * 64 + 16 * nt + lc], -(er[r] + ec[nt]));
+  const double m0 = lr == 0, m1 = lr == 1, m2 = lr == 2, m3 = lr == 3;
 #pragma unroll
   for (int K = 0; K < 16; ++K) {
-    double* Cb = pbuf + (K & 1) * 512;  // C[i][c] at Cb[c * 64 + i]
-    double* Wb = Cb + 256;              // -W[i][b] at Wb[b * 64 + i]
-    const int ntK = K >> 2, jK = 4 * (K & 3);
-    // (1) publish the pivot columns 4K .. 4K+3 minus the identity
-    if (lc >= jK && lc < jK + 4) {
-      const int cp = lc - jK;
+    // The sweep keeps A symmetric, so the pivot column block equals the
+    // pivot rows: their owner (wave K / 4, register K % 4) publishes
+    // C^T[c][j] = A[4K + c][j] - delta(j, 4K + c) and every wave builds
+    // its own operands from it.  Double-buffered: one barrier per step.
+    double* Rb = pbuf + (K & 1) * 256;
+    const int ntK = K >> 2, rK = K & 3;
+    if (w == ntK) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 16 * w + lr + 4 * r;
-        Cb[cp * 64 + row] = acc[ntK][r] - (row == 4 * K + cp ? 1.0 : 0.0);
+      for (int nt = 0; nt < 4; ++nt) {
+        const int col = 16 * nt + lc;
+        Rb[lr * 64 + col] = acc[nt][rK] - (col == 4 * K + lr ? 1.0 : 0.0);
       }
     }
     __syncthreads();
-    // (2) P^{-1} (every thread, same inputs) and one entry of -W = -C P^{-1}
     double P[4][4], Pi[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
       for (int b = a; b < 4; ++b) {
-        P[a][b] = Cb[b * 64 + 4 * K + a] + (a == b ? 1.0 : 0.0);
+        P[a][b] = Rb[a * 64 + 4 * K + b] + (a == b ? 1.0 : 0.0);
         P[b][a] = P[a][b];
       }
+    double cw[4], bop[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) cw[c] = Rb[c * 64 + 16 * w + lc];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) bop[nt] = Rb[lr * 64 + 16 * nt + lc];
     spd_inverse4(P, Pi);
-    {
-      const int i = t & 63, b = t >> 6;
-      double sacc = 0.0;
+    // A operand: W[16 w + lc][lr] = -(C P^{-1})[16 w + lc][lr]; column lr
+    // of P^{-1} picked by exact 0/1 weights (no divergent selects)
+    double wc[4];
 #pragma unroll
-      for (int a = 0; a < 4; ++a) sacc = fma(Cb[a * 64 + i], Pi[a][b], sacc);
-      Wb[b * 64 + i] = -sacc;
-    }
-    __syncthreads();
-    // (3) rank-4 update of the wave's tile row on fp64 MFMA
-    const double aop = Wb[lr * 64 + 16 * w + lc];
+    for (int b = 0; b < 4; ++b) wc[b] = cw[0] * Pi[0][b] + cw[1] * Pi[1][b] + cw[2] * Pi[2][b] + cw[3] * Pi[3][b];
+    const double aop = -(wc[0] * m0 + wc[1] * m1 + wc[2] * m2 + wc[3] * m3);
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma_f64(aop, Cb[lr * 64 + 16 * nt + lc], acc[nt]);
-    // (4) the pivot block's diagonal
-    if (w == ntK && lc == jK + lr) acc[ntK][K & 3] -= 2.0;
+    for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma_f64(aop, bop[nt], acc[nt]);
+    // the pivot block's diagonal
+    if (w == ntK && lc == 4 * rK + lr) acc[ntK][rK] -= 2.0;
   }
-  __syncthreads();
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
@@ -322,12 +403,12 @@ __device__ __forceinline__ void ridge_invert_store(double* G, double* colbuf, in
 // ---------------------------------------------------------------------------
 // Gram matrices of a ternary factor, built by `nside` workgroups
 // ---------------------------------------------------------------------------
-// Partial integer Gram of Tt (BBP x L int8, component-major) over this
+// Partial integer Gram of X (BBP x L int8, MFMA-ready layout) over this
 // workgroup's share of K steps, on int8 MFMA; all four wave results are
 // summed in LDS (integer adds, order-free) and written to gparti[side].
 // Returns true in the last of the nside workgroups to finish, with the
 // complete Gram in G (LDS, fp64).
-__device__ __forceinline__ bool side_gram_int(const int8_t* __restrict__ Tt, int64_t L, int side, int nside, int* gparti,
+__device__ __forceinline__ bool side_gram_int(const v4i* __restrict__ Xmf, int64_t L, int side, int nside, int* gparti,
                               unsigned* counter, double* G, int* ired /* LDS 4096 */) {
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
@@ -335,9 +416,8 @@ __device__ __forceinline__ bool side_gram_int(const int8_t* __restrict__ Tt, int
   const int ks0 = (int)((long long)side * nks / nside), ks1 = (int)((long long)(side + 1) * nks / nside);
   v16i acc00 = {}, acc01 = {}, acc10 = {}, acc11 = {};
   for (int ks = ks0 + wave; ks < ks1; ks += 4) {
-    const int64_t i0 = (int64_t)ks * TILE + 16 * h;
-    const v4i a0 = *(const v4i*)(Tt + (int64_t)l32 * L + i0);
-    const v4i a1 = *(const v4i*)(Tt + (int64_t)(32 + l32) * L + i0);
+    const v4i a0 = Xmf[(int64_t)ks * 128 + lane];
+    const v4i a1 = Xmf[(int64_t)ks * 128 + 64 + lane];
     acc00 = mfma_i8(a0, a0, acc00);
     acc01 = mfma_i8(a0, a1, acc01);
     acc10 = mfma_i8(a1, a0, acc10);
@@ -469,44 +549,27 @@ __device__ __forceinline__ bool side_gram_w(const int8_t* __restrict__ Vr, const
   return true;
 }
 
-// Integer-plane reduction of the 4 waves' MFMA accumulators into LDS.
-// red layout: [plane][tile][M * 33 + N] int32 (33-word row pitch).
-constexpr int RED_TILE = 32 * 33;
-__device__ __forceinline__ void reduce_planes(int* red, const v16i (&acc)[2][4]) {
-  const int lane = lane_id();
-  const int h = lane >> 5, l32 = lane & 31;
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int p = 0; p < 4; ++p)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int M = 8 * (r >> 2) + 4 * h + (r & 3);
-        atomicAdd(&red[(p * 2 + t) * RED_TILE + M * 33 + l32], acc[t][p][r]);
-      }
-}
-__device__ __forceinline__ long long combine_planes(const int* red, int t, int M, int N) {
-  const int o = M * 33 + N;
-  return (long long)red[(0 * 2 + t) * RED_TILE + o] + ((long long)red[(1 * 2 + t) * RED_TILE + o] << 8) +
-         ((long long)red[(2 * 2 + t) * RED_TILE + o] << 16) + ((long long)red[(3 * 2 + t) * RED_TILE + o] << 24);
-}
-
 // ---------------------------------------------------------------------------
 // V-step contraction P = U^T R  (Eq. (3), first half)
 // grid: nside side WGs (Gram U^T U + ridge + inverse) followed by
 //       (n_pad/32 column tiles) x gv row groups.
 // Each WG owns 32 columns and a contiguous range of 32-row K steps, split
-// over its 4 waves; A = Ut (components x rows), B = R digit planes.
+// over its 4 waves; A = U (MFMA-ready layout), B = R digit planes.  Lane
+// (j, h) loads column j, rows 16h .. 16h+15 of the K step: every load
+// instruction reads two full 128-byte row segments.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vstep(const float* __restrict__ R, const int8_t* __restrict__ Ut,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vstep(const float* __restrict__ R, const v4i* __restrict__ Umf,
                                               long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
                                               int64_t m_pad, int64_t n_pad, int gv, int bb, int* gparti,
                                               unsigned* counter, double* ginvU, int nside) {
-  __shared__ int red[8 * RED_TILE];
-  __shared__ double Gs[4096];
-  __shared__ double colbuf[1024];
+  // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
+  // 64 KB wave reduction
+  __shared__ __attribute__((aligned(16))) long long smem[8192];
   if ((int)blockIdx.x < nside) {
-    if (side_gram_int(Ut, m_pad, blockIdx.x, nside, gparti, counter, Gs, red)) ridge_invert_store(Gs, colbuf, bb, ginvU);
+    int* ired = (int*)smem;
+    double* Gs = (double*)(smem + 2048);
+    double* pbuf = Gs + 4096;
+    if (side_gram_int(Umf, m_pad, blockIdx.x, nside, gparti, counter, Gs, ired)) ridge_invert_store(Gs, pbuf, bb, ginvU);
     return;
   }
   const int b = blockIdx.x - nside;
@@ -523,8 +586,6 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 #pragma unroll
     for (int p = 0; p < 4; ++p) acc[t][p] = v16i{};
   const float* Rc = R + (int64_t)ct * TILE + l32;
-  const int8_t* U0 = Ut + (int64_t)l32 * m_pad + 16 * h;
-  const int8_t* U1 = Ut + (int64_t)(32 + l32) * m_pad + 16 * h;
   // software pipeline: the loads of K step ks + 4 are in flight while
   // step ks is converted and multiplied
   float xn[16];
@@ -532,8 +593,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   int ks = ks0 + wave;
   if (ks < ks1) {
     const int64_t i0 = (int64_t)ks * TILE + 16 * h;
-    an0 = *(const v4i*)(U0 + (int64_t)ks * TILE);
-    an1 = *(const v4i*)(U1 + (int64_t)ks * TILE);
+    an0 = Umf[(int64_t)ks * 128 + lane];
+    an1 = Umf[(int64_t)ks * 128 + 64 + lane];
 #pragma unroll
     for (int q = 0; q < 16; ++q) xn[q] = Rc[(i0 + q) * n_pad];
   }
@@ -545,8 +606,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     const int ksn = ks + 4;
     if (ksn < ks1) {
       const int64_t i0 = (int64_t)ksn * TILE + 16 * h;
-      an0 = *(const v4i*)(U0 + (int64_t)ksn * TILE);
-      an1 = *(const v4i*)(U1 + (int64_t)ksn * TILE);
+      an0 = Umf[(int64_t)ksn * 128 + lane];
+      an1 = Umf[(int64_t)ksn * 128 + 64 + lane];
 #pragma unroll
       for (int q = 0; q < 16; ++q) xn[q] = Rc[(i0 + q) * n_pad];
     }
@@ -558,16 +619,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
       acc[1][p] = mfma_i8(a1, P[p], acc[1][p]);
     }
   }
-  for (int e = threadIdx.x; e < 8 * RED_TILE; e += NT) red[e] = 0;
-  __syncthreads();
-  reduce_planes(red, acc);
-  __syncthreads();
   // out[t][M = component][N = column]
-  for (int e = threadIdx.x; e < 2048; e += NT) {
-    const int t = e >> 10, rem = e & 1023, M = rem >> 5, N = rem & 31;
-    Pp[((int64_t)g * BBP + 32 * t + M) * n_pad + (int64_t)ct * TILE + N] = combine_planes(red, t, M, N);
-  }
-  (void)bb;
+  long long* Pg = Pp + ((int64_t)g * BBP) * n_pad + (int64_t)ct * TILE;
+  reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { Pg[(int64_t)(32 * t + M) * n_pad + N] = v; });
 }
 
 // ---------------------------------------------------------------------------
@@ -575,25 +629,36 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // grid: nside side WGs (Gram V^T H V + ridge + inverse, raw Gram kept for
 //       the scale solve) followed by m_pad/32 row tiles.
 // Each WG owns 32 full rows; its 4 waves interleave 32-column K steps.
-// A = R digit planes (rows x columns), B = Vt (columns x components).
+// A = R digit planes (rows x columns), B = V (MFMA-ready layout).  Each
+// wave streams its 32 x 32 residual tiles into LDS with direct loads
+// (8 lanes per 128-byte row segment, 16-byte chunks XOR-swizzled by row)
+// NST_U tiles ahead, then reads them back in operand order (lane (i, h):
+// row i, columns 16h .. 16h+15).  The weighted variant stages the 32
+// weights of the K step beside each tile.
 // ---------------------------------------------------------------------------
+constexpr int NST_U = 3;
+constexpr int USTAGE_B = 4096 + 256;  // bytes per staged K step: tile + weights
+
 template <bool WEIGHTED>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_ustep(const float* __restrict__ R, const int8_t* __restrict__ Vt,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_ustep(const float* __restrict__ R, const v4i* __restrict__ Vmf,
                                               const int8_t* __restrict__ Vr, const double* __restrict__ hw,
                                               double* __restrict__ Q, const unsigned* __restrict__ maxbits,
                                               int64_t m_pad, int64_t n_pad, int bb, int* gparti, double* gpart,
                                               unsigned* counter, double* ginvV, double* gramV, int nside) {
-  __shared__ int red[8 * RED_TILE];
-  __shared__ double Gs[4096];
-  __shared__ double colbuf[1024];
+  // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
+  // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
+  __shared__ __attribute__((aligned(16))) long long smem[8192];
   if ((int)blockIdx.x < nside) {
+    int* ired = (int*)smem;
+    double* Gs = (double*)(smem + 2048);
+    double* pbuf = Gs + 4096;
     bool last;
     if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, nside, gpart, counter, Gs);
-    else last = side_gram_int(Vt, n_pad, blockIdx.x, nside, gparti, counter, Gs, red);
+    else last = side_gram_int(Vmf, n_pad, blockIdx.x, nside, gparti, counter, Gs, ired);
     if (last) {
       for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
       __syncthreads();
-      ridge_invert_store(Gs, colbuf, bb, ginvV);
+      ridge_invert_store(Gs, pbuf, bb, ginvV);
     }
     return;
   }
@@ -606,60 +671,77 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int p = 0; p < 4; ++p) acc[t][p] = v16i{};
-  const float* Rrow = R + ((int64_t)rt * TILE + l32) * n_pad + 16 * h;
-  const int8_t* V0 = Vt + (int64_t)l32 * n_pad + 16 * h;
-  const int8_t* V1 = Vt + (int64_t)(32 + l32) * n_pad + 16 * h;
   const int nks = (int)(n_pad / TILE);
-  // software pipeline: loads of K step ks + 4 in flight during step ks
-  float4 xn[4];
-  v4i bn0 = {}, bn1 = {};
-  int ks = wave;
-  if (ks < nks) {
-    const float4* src = (const float4*)(Rrow + (int64_t)ks * TILE);
+  char* wst = (char*)smem + wave * (NST_U * USTAGE_B);
+  // loader mapping: lane -> row 8 q + lane / 8, 16-byte chunk lane % 8,
+  // stored at chunk position (lane % 8) ^ (row % 8)
+  const int lrow = lane >> 3;
+  const float* Rld = R + ((int64_t)rt * TILE + lrow) * n_pad + (((lane & 7) ^ lrow) * 4);
+  constexpr int NLD = WEIGHTED ? 5 : 4;  // direct loads per staged K step
+  v4i bn[NST_U][2];
+  auto issue = [&](int kk, int st) {
+    kk = kk < nks ? kk : nks - 1;
+    char* dst = wst + st * USTAGE_B;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) xn[q] = src[q];
-    bn0 = *(const v4i*)(V0 + (int64_t)ks * TILE);
-    bn1 = *(const v4i*)(V1 + (int64_t)ks * TILE);
-  }
-  for (; ks < nks; ks += 4) {
-    const int64_t j0 = (int64_t)ks * TILE + 16 * h;
-    unsigned y[16];
+    for (int q = 0; q < 4; ++q)
+      __builtin_amdgcn_global_load_lds(Rld + (int64_t)8 * q * n_pad + (int64_t)kk * TILE, (lds_void*)(dst + q * 1024),
+                                       16, 0, 0);
+    if (WEIGHTED)
+      __builtin_amdgcn_global_load_lds((const float*)(hw + (int64_t)kk * TILE) + lane, (lds_void*)(dst + 4096), 4, 0,
+                                       0);
+    bn[st][0] = Vmf[(int64_t)kk * 128 + lane];
+    bn[st][1] = Vmf[(int64_t)kk * 128 + 64 + lane];
+  };
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float xs[4] = {xn[q].x, xn[q].y, xn[q].z, xn[q].w};
+  for (int d = 0; d < NST_U - 1; ++d) issue(wave + 4 * d, d);
+  // operand read: row l32, logical chunks 4h .. 4h+3
+  const unsigned sw = (unsigned)(l32 & 7);
+  const unsigned o0 = l32 * 128 + ((4 * h + 0) ^ sw) * 16, o1 = l32 * 128 + ((4 * h + 1) ^ sw) * 16;
+  const unsigned o2 = l32 * 128 + ((4 * h + 2) ^ sw) * 16, o3 = l32 * 128 + ((4 * h + 3) ^ sw) * 16;
+  const unsigned wbase = lds_addr(wst);
+  for (int ks = wave; ks < nks; ks += 4 * NST_U) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (WEIGHTED) y[4 * q + e] = fx_biased_w(xs[e], ldexp(hw[j0 + 4 * q + e], s));
-        else y[4 * q + e] = fx_biased(xs[e], s);
+    for (int u = 0; u < NST_U; ++u) {
+      const int kk = ks + 4 * u;
+      issue(kk + 4 * (NST_U - 1), (u + NST_U - 1) % NST_U);
+      if (kk < nks) {
+        const unsigned b = wbase + u * USTAGE_B;
+        v4f x[4];
+        lds_read4_after<NLD * (NST_U - 1)>(b + o0, b + o1, b + o2, b + o3, x[0], x[1], x[2], x[3]);
+        unsigned y[16];
+        if (WEIGHTED) {
+          v2d wv[8];
+          lds_read8(b + 4096 + 128 * h, wv);
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) y[4 * q + e] = fx_biased_w(x[q][e], ldexp(wv[(4 * q + e) >> 1][e & 1], s));
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) y[4 * q + e] = fx_biased(x[q][e], s);
+        }
+        v4i P[4];
+        make_planes(y, P);
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          acc[0][p] = mfma_i8(P[p], bn[u][0], acc[0][p]);
+          acc[1][p] = mfma_i8(P[p], bn[u][1], acc[1][p]);
+        }
       }
     }
-    const v4i b0 = bn0, b1 = bn1;
-    const int ksn = ks + 4;
-    if (ksn < nks) {
-      const float4* src = (const float4*)(Rrow + (int64_t)ksn * TILE);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) xn[q] = src[q];
-      bn0 = *(const v4i*)(V0 + (int64_t)ksn * TILE);
-      bn1 = *(const v4i*)(V1 + (int64_t)ksn * TILE);
-    }
-    v4i P[4];
-    make_planes(y, P);
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      acc[0][p] = mfma_i8(P[p], b0, acc[0][p]);
-      acc[1][p] = mfma_i8(P[p], b1, acc[1][p]);
-    }
   }
-  for (int e = threadIdx.x; e < 8 * RED_TILE; e += NT) red[e] = 0;
+  // every direct load (including the clamped ones past the end) has landed
+  // before the staging area is reused
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  reduce_planes(red, acc);
+  // out[t][M = row][N = component] -> Q[32 t + N][row], via a transposed
+  // LDS tile for coalesced stores
+  double* tq = (double*)smem;
+  reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { tq[(32 * t + N) * 32 + M] = ldexp((double)v, -s); });
   __syncthreads();
-  // out[t][M = row][N = component] -> Q[32t + N][row]
-  for (int e = threadIdx.x; e < 2048; e += NT) {
-    const int t = e >> 10, rem = e & 1023, N = rem >> 5, M = rem & 31;
-    const long long v = combine_planes(red, t, M, N);
-    Q[(int64_t)(32 * t + N) * m_pad + (int64_t)rt * TILE + M] = ldexp((double)v, -s);
-  }
+  for (int e = threadIdx.x; e < 2048; e += NT) Q[(int64_t)(e >> 5) * m_pad + (int64_t)rt * TILE + (e & 31)] = tq[e];
 }
 
 // ---------------------------------------------------------------------------
@@ -753,8 +835,9 @@ __global__ __launch_bounds__(NT) void k_uepi(const double* __restrict__ Q, const
 // ---------------------------------------------------------------------------
 // T_tau of one component per workgroup (Eq. (2)): theta = tau * mean|x|
 // over the true length L (fp64), strict ">", keep the largest |x| (smallest
-// index) when nothing passes.  Writes the trits component-major
-// (dst[0 .. L_pad)), zero beyond L.  The first TERN_CACHE * blockDim values
+// index) when nothing passes.  Writes the trits of component c
+// component-major (dst[0 .. L_pad)) and into the MFMA-ready layout mf,
+// zero beyond L.  The first TERN_CACHE * blockDim values
 // are loaded once and kept in registers for the threshold pass.  With an
 // auxiliary vector q (may be null) it also returns sum_i t_i q_i (fp64).
 // ---------------------------------------------------------------------------
@@ -762,7 +845,7 @@ constexpr int TERN_CACHE = 12;
 
 template <typename Load>
 __device__ __forceinline__ double ternarize_wg(Load load, const double* __restrict__ q, int64_t L, int64_t L_pad, double tau,
-                               int8_t* dst) {
+                               int8_t* dst, int8_t* mf, int c) {
   __shared__ double shd[16];
   __shared__ long long shl[16];
   __shared__ int shi[16];
@@ -770,18 +853,18 @@ __device__ __forceinline__ double ternarize_wg(Load load, const double* __restri
   const int64_t tid = threadIdx.x;
   double xc[TERN_CACHE], qc[TERN_CACHE];
 #pragma unroll
-  for (int c = 0; c < TERN_CACHE; ++c) {
-    const int64_t i = tid + c * st;
-    xc[c] = (i < L) ? load(i) : 0.0;
-    qc[c] = (q && i < L) ? q[i] : 0.0;
+  for (int cc = 0; cc < TERN_CACHE; ++cc) {
+    const int64_t i = tid + cc * st;
+    xc[cc] = (i < L) ? load(i) : 0.0;
+    qc[cc] = (q && i < L) ? q[i] : 0.0;
   }
   double sabs = 0.0, mx = -1.0;
   long long imx = 0;
 #pragma unroll
-  for (int c = 0; c < TERN_CACHE; ++c) {
-    const int64_t i = tid + c * st;
+  for (int cc = 0; cc < TERN_CACHE; ++cc) {
+    const int64_t i = tid + cc * st;
     if (i < L) {
-      const double a = fabs(xc[c]);
+      const double a = fabs(xc[cc]);
       sabs += a;
       argmax_merge(mx, imx, a, i);
     }
@@ -797,14 +880,15 @@ __device__ __forceinline__ double ternarize_wg(Load load, const double* __restri
   int nnz = 0;
   double g = 0.0;
 #pragma unroll
-  for (int c = 0; c < TERN_CACHE; ++c) {
-    const int64_t i = tid + c * st;
+  for (int cc = 0; cc < TERN_CACHE; ++cc) {
+    const int64_t i = tid + cc * st;
     if (i < L_pad) {
       int8_t t = 0;
-      if (i < L && fabs(xc[c]) > theta) t = (xc[c] > 0.0) ? 1 : -1;
+      if (i < L && fabs(xc[cc]) > theta) t = (xc[cc] > 0.0) ? 1 : -1;
       nnz += (t != 0);
-      g += (double)t * qc[c];
+      g += (double)t * qc[cc];
       dst[i] = t;
+      mf[mf_offset(c, i)] = t;
     }
   }
   for (int64_t i = tid + TERN_CACHE * st; i < L_pad; i += st) {
@@ -816,6 +900,7 @@ __device__ __forceinline__ double ternarize_wg(Load load, const double* __restri
     }
     nnz += (t != 0);
     dst[i] = t;
+    mf[mf_offset(c, i)] = t;
   }
   nnz = block_sum_i(nnz, shi);
   if (nnz == 0 && L > 0) {
@@ -824,6 +909,7 @@ __device__ __forceinline__ double ternarize_wg(Load load, const double* __restri
       const double x = load(imx);
       const int8_t t = (x > 0.0) ? 1 : ((x < 0.0) ? -1 : 0);
       dst[imx] = t;
+      mf[mf_offset(c, imx)] = t;
       g = q ? (double)t * q[imx] : 0.0;
     } else {
       g = 0.0;
@@ -835,31 +921,38 @@ __device__ __forceinline__ double ternarize_wg(Load load, const double* __restri
 
 // V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.  grid: BBP.
 __global__ __launch_bounds__(NT_TERN) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb,
-                                                    double tau, int8_t* __restrict__ Vt) {
+                                                    double tau, int8_t* __restrict__ Vt, int8_t* __restrict__ Vmf) {
   const int c = blockIdx.x;
   int8_t* dst = Vt + (int64_t)c * n_pad;
   if (c >= bb) {
-    for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) dst[j] = 0;
+    for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
+      dst[j] = 0;
+      Vmf[mf_offset(c, j)] = 0;
+    }
     return;
   }
   const double* y = Y + (int64_t)c * n_pad;
-  ternarize_wg([=](int64_t j) { return y[j]; }, nullptr, n, n_pad, tau, dst);
+  ternarize_wg([=](int64_t j) { return y[j]; }, nullptr, n, n_pad, tau, dst, Vmf, c);
 }
 
 // U <- T_tau(Z[:, c]); also g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for
 // the joint scale solve (Eq. (4)).  grid: BBP.
 __global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q,
                                                     int64_t m, int64_t m_pad, int bb, double tau,
-                                                    int8_t* __restrict__ Ut, double* __restrict__ gvec) {
+                                                    int8_t* __restrict__ Ut, int8_t* __restrict__ Umf,
+                                                    double* __restrict__ gvec) {
   const int c = blockIdx.x;
   int8_t* dst = Ut + (int64_t)c * m_pad;
   if (c >= bb) {
-    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) dst[i] = 0;
+    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) {
+      dst[i] = 0;
+      Umf[mf_offset(c, i)] = 0;
+    }
     if (threadIdx.x == 0) gvec[c] = 0.0;
     return;
   }
   const double* z = Z + (int64_t)c * m_pad;
-  const double g = ternarize_wg([=](int64_t i) { return z[i]; }, Q + (int64_t)c * m_pad, m, m_pad, tau, dst);
+  const double g = ternarize_wg([=](int64_t i) { return z[i]; }, Q + (int64_t)c * m_pad, m, m_pad, tau, dst, Umf, c);
   if (threadIdx.x == 0) gvec[c] = g;
 }
 
@@ -867,17 +960,20 @@ __global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z
 // grid: BBP.
 __global__ __launch_bounds__(NT_TERN) void k_init(const float* __restrict__ R, const int* __restrict__ J, int64_t m,
                                              int64_t m_pad, int64_t n_pad, int bb, double tau,
-                                             int8_t* __restrict__ Ut) {
+                                             int8_t* __restrict__ Ut, int8_t* __restrict__ Umf) {
   const int c = blockIdx.x;
   int8_t* dst = Ut + (int64_t)c * m_pad;
   if (c >= bb) {
-    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) dst[i] = 0;
+    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) {
+      dst[i] = 0;
+      Umf[mf_offset(c, i)] = 0;
+    }
     return;
   }
   int jc = J[c];
   jc = jc < 0 ? 0 : (jc >= n_pad ? (int)(n_pad - 1) : jc);  // J comes from k_select; keep reads in bounds
   const float* col = R + jc;
-  ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, nullptr, m, m_pad, tau, dst);
+  ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, nullptr, m, m_pad, tau, dst, Umf, c);
 }
 
 // Xt (BBP x L int8, component-major) -> Xr (L x BBP, row-major).
@@ -901,7 +997,7 @@ __global__ __launch_bounds__(NT) void k_transpose8(const int8_t* __restrict__ Xt
 // Joint scale solve, Eq. (4): M = (U^T U) o (V^T H V) (+ delta I),
 // d = M^{-1} g.  grid: NSIDE_INT (partial U^T U on int8 MFMA, last WG solves).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) void k_scale(const int8_t* __restrict__ Ut, int64_t m_pad, int bb,
+__global__ __launch_bounds__(NT) void k_scale(const v4i* __restrict__ Umf, int64_t m_pad, int bb,
                                               const double* __restrict__ gramV, const double* __restrict__ gvec,
                                               int* gparti, unsigned* counter, double* dvec, float* dF,
                                               float* Dout) {
@@ -909,7 +1005,7 @@ __global__ __launch_bounds__(NT) void k_scale(const int8_t* __restrict__ Ut, int
   __shared__ double Gs[4096];
   __shared__ double colbuf[1024];
   __shared__ double s_trb[16];
-  if (!side_gram_int(Ut, m_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red)) return;
+  if (!side_gram_int(Umf, m_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red)) return;
   const int t = threadIdx.x;
   for (int e = t; e < 4096; e += NT) {
     const int r = e >> 6, c = e & 63;
@@ -1390,7 +1486,7 @@ __global__ __launch_bounds__(NT) void k_emit_c(const int8_t* __restrict__ Vt, in
 // step-entry helpers: caller layouts <-> workspace layouts
 // ---------------------------------------------------------------------------
 // X: len x bb row-major int8 -> Xt (BBP x len_pad) and Xr (len_pad x BBP), zero padded.
-__global__ __launch_bounds__(NT) void k_load_factor(int8_t* Xt, int8_t* Xr, const int8_t* X, int64_t len,
+__global__ __launch_bounds__(NT) void k_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len,
                                                     int64_t len_pad, int bb) {
   const int64_t total = len_pad * BBP;
   for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
@@ -1399,6 +1495,7 @@ __global__ __launch_bounds__(NT) void k_load_factor(int8_t* Xt, int8_t* Xr, cons
     const int8_t v = (i < len && c < bb) ? X[i * bb + c] : (int8_t)0;
     Xr[e] = v;
     Xt[(int64_t)c * len_pad + i] = v;
+    Xmf[mf_offset(c, i)] = v;
   }
 }
 __global__ __launch_bounds__(NT) void k_store_factor(int8_t* X, const int8_t* Xt, int64_t len, int64_t len_pad,
@@ -1434,7 +1531,7 @@ __global__ __launch_bounds__(NT) void k_load_cm(double* Xcm, const double* X, in
 // Gram of V alone (raw V^T H V and its ridge inverse), for the scale step
 // entry point.  grid: NSIDE_INT or NSIDE_W.
 template <bool WEIGHTED>
-__global__ __launch_bounds__(NT) void k_gram_v(const int8_t* __restrict__ Vt, const int8_t* __restrict__ Vr,
+__global__ __launch_bounds__(NT) void k_gram_v(const v4i* __restrict__ Vmf, const int8_t* __restrict__ Vr,
                                                const double* __restrict__ hw, int64_t n_pad, int bb, int* gparti,
                                                double* gpart, unsigned* counter, double* ginvV, double* gramV) {
   __shared__ int red[4096];
@@ -1442,7 +1539,7 @@ __global__ __launch_bounds__(NT) void k_gram_v(const int8_t* __restrict__ Vt, co
   __shared__ double colbuf[1024];
   bool last;
   if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, (int)gridDim.x, gpart, counter, Gs);
-  else last = side_gram_int(Vt, n_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red);
+  else last = side_gram_int(Vmf, n_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red);
   if (!last) return;
   for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
   __syncthreads();
@@ -1518,14 +1615,14 @@ hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2,
 }
 
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
-  hipLaunchKernelGGL(k_init, dim3(BBP), dim3(NT_TERN), 0, s, w.R, w.J, w.m, w.m_pad, w.n_pad, bb, tau, w.Ut);
+  hipLaunchKernelGGL(k_init, dim3(BBP), dim3(NT_TERN), 0, s, w.R, w.J, w.m, w.m_pad, w.n_pad, bb, tau, w.Ut, w.Umf);
   return hipGetLastError();
 }
 
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
   const unsigned grid = (unsigned)(NSIDE_INT + (w.n_pad / TILE) * w.gv);
   EXTERND_TIMED(tm, EXTERND_KCLASS_VSTEP,
-                hipLaunchKernelGGL(k_vstep, dim3(grid), dim3(NT), 0, s, w.R, w.Ut, w.Pp, w.maxbits + blk, w.m_pad,
+                hipLaunchKernelGGL(k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, w.maxbits + blk, w.m_pad,
                                    w.n_pad, w.gv, bb, w.gparti, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_INT));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1533,7 +1630,7 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
                      w.maxbits + blk, w.n_pad);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.Vt);
+  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.Vt, w.Vmf);
   return hipGetLastError();
 }
 
@@ -1546,12 +1643,12 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
-                  hipLaunchKernelGGL(k_ustep<true>, dim3(grid), dim3(NT), 0, s, w.R, w.Vt, w.Vr, w.hw, w.Q,
+                  hipLaunchKernelGGL(k_ustep<true>, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gparti, w.gpart,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside));
   } else {
     EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
-                  hipLaunchKernelGGL(k_ustep<false>, dim3(grid), dim3(NT), 0, s, w.R, w.Vt, w.Vr, w.hw, w.Q,
+                  hipLaunchKernelGGL(k_ustep<false>, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gparti, w.gpart,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside));
   }
@@ -1560,12 +1657,12 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
   hipLaunchKernelGGL(k_uepi, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0, s, w.Q, w.ginvV, w.Z, w.m_pad);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.Ut, w.gvec);
+  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.Ut, w.Umf, w.gvec);
   return hipGetLastError();
 }
 
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
-  hipLaunchKernelGGL(k_scale, dim3(NSIDE_INT), dim3(NT), 0, s, w.Ut, w.m_pad, bb, w.gramV, w.gvec, w.gparti,
+  hipLaunchKernelGGL(k_scale, dim3(NSIDE_INT), dim3(NT), 0, s, (const v4i*)w.Umf, w.m_pad, bb, w.gramV, w.gvec, w.gparti,
                      w.counters + CNT_SCALE, w.dvec, w.dF, (float*)nullptr);
   return hipGetLastError();
 }
@@ -1597,9 +1694,9 @@ hipError_t launch_emit(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, 
   return hipMemcpyAsync(D + c0, w.dF, sizeof(float) * bb, hipMemcpyDeviceToDevice, s);
 }
 
-hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, const int8_t* X, int64_t len, int64_t len_pad, int bb,
-                              hipStream_t s) {
-  hipLaunchKernelGGL(k_load_factor, dim3(grid_for(len_pad * BBP)), dim3(NT), 0, s, Xt, Xr, X, len, len_pad, bb);
+hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len, int64_t len_pad,
+                              int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_load_factor, dim3(grid_for(len_pad * BBP)), dim3(NT), 0, s, Xt, Xr, Xmf, X, len, len_pad, bb);
   return hipGetLastError();
 }
 hipError_t launch_store_factor(int8_t* X, const int8_t* Xt, int64_t len, int64_t len_pad, int bb, hipStream_t s) {
@@ -1617,10 +1714,10 @@ hipError_t launch_load_cm(double* Xcm, const double* X, int64_t len, int64_t len
 
 hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s) {
   if (weighted)
-    hipLaunchKernelGGL(k_gram_v<true>, dim3(NSIDE_W), dim3(NT), 0, s, w.Vt, w.Vr, w.hw, w.n_pad, bb, w.gparti, w.gpart,
+    hipLaunchKernelGGL(k_gram_v<true>, dim3(NSIDE_W), dim3(NT), 0, s, (const v4i*)w.Vmf, w.Vr, w.hw, w.n_pad, bb, w.gparti, w.gpart,
                        w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
   else
-    hipLaunchKernelGGL(k_gram_v<false>, dim3(NSIDE_INT), dim3(NT), 0, s, w.Vt, w.Vr, w.hw, w.n_pad, bb, w.gparti,
+    hipLaunchKernelGGL(k_gram_v<false>, dim3(NSIDE_INT), dim3(NT), 0, s, (const v4i*)w.Vmf, w.Vr, w.hw, w.n_pad, bb, w.gparti,
                        w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
   return hipGetLastError();
 }
