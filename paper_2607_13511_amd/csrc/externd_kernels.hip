@@ -301,7 +301,7 @@ __device__ __forceinline__ void spd_inverse4(const double (&P)[4][4], double (&P
   Pi[3][2] = t01; Pi[3][3] = t11;
 }
 
-__device__ __forceinline__ void spd_inverse64(double* A, double* pbuf) {
+__device__ __forceinline__ void spd_inverse64(double* A, double* pbuf, double* out = nullptr) {
   __shared__ int sexp[64];
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
@@ -366,11 +366,13 @@ __device__ __forceinline__ void spd_inverse64(double* A, double* pbuf) {
     // the pivot block's diagonal
     if (w == ntK && lc == 4 * rK + lr) acc[ntK][rK] -= 2.0;
   }
+  // the inverse goes to out (global) when given, else back to A
+  double* dst = out ? out : A;
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      A[(16 * w + lr + 4 * r) * 64 + 16 * nt + lc] = -ldexp(acc[nt][r], -(er[r] + ec[nt]));
+      dst[(16 * w + lr + 4 * r) * 64 + 16 * nt + lc] = -ldexp(acc[nt][r], -(er[r] + ec[nt]));
   __syncthreads();
 }
 
@@ -379,25 +381,26 @@ __device__ __forceinline__ void spd_inverse64(double* A, double* pbuf) {
 // and write the inverse.  Zero trace -> zero inverse on the real block
 // (every component is zero, Eq. (3) target is zero).
 __device__ __forceinline__ void ridge_invert_store(double* G, double* colbuf, int bb, double* ginv_out) {
-  __shared__ double shd[16];
+  // The raw Gram of the zero padding components is exactly zero, so only
+  // the diagonal changes: + eps on the real block, 1 on the padding.
+  __shared__ double s_tr;
   const int t = threadIdx.x;
-  const double tr = block_sum_d((t < bb) ? G[t * 64 + t] : 0.0, shd);
-  const double eps = EXTERND_RIDGE_REL * tr / (double)bb;
-  for (int e = t; e < 4096; e += blockDim.x) {
-    const int r = e >> 6, c = e & 63;
-    if (r >= bb || c >= bb) G[e] = (r == c) ? 1.0 : 0.0;
-    else if (r == c) G[e] += eps;
+  if (t < 64) {
+    const double tr = wave_sum_d(t < bb ? G[t * 65] : 0.0);
+    const double trb = __shfl(tr, 0);
+    if (t == 0) s_tr = trb;
+    const double eps = EXTERND_RIDGE_REL * trb / (double)bb;
+    G[t * 65] = (t < bb) ? G[t * 65] + eps : 1.0;
   }
   __syncthreads();
-  if (tr == 0.0) {
+  if (s_tr == 0.0) {
     for (int e = t; e < 4096; e += blockDim.x) {
       const int r = e >> 6, c = e & 63;
       ginv_out[e] = (r >= bb || c >= bb) ? ((r == c) ? 1.0 : 0.0) : 0.0;
     }
     return;
   }
-  spd_inverse64(G, colbuf);
-  for (int e = t; e < 4096; e += blockDim.x) ginv_out[e] = G[e];
+  spd_inverse64(G, colbuf, ginv_out);
 }
 
 // ---------------------------------------------------------------------------
@@ -415,7 +418,24 @@ __device__ __forceinline__ bool side_gram_int(const v4i* __restrict__ Xmf, int64
   const int nks = (int)(L / TILE);
   const int ks0 = (int)((long long)side * nks / nside), ks1 = (int)((long long)(side + 1) * nks / nside);
   v16i acc00 = {}, acc01 = {}, acc10 = {}, acc11 = {};
-  for (int ks = ks0 + wave; ks < ks1; ks += 4) {
+  int ks = ks0 + wave;
+  // four K steps per round, loads issued before the MFMAs
+  for (; ks + 12 < ks1; ks += 16) {
+    v4i a[4][2];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      a[u][0] = Xmf[(int64_t)(ks + 4 * u) * 128 + lane];
+      a[u][1] = Xmf[(int64_t)(ks + 4 * u) * 128 + 64 + lane];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc00 = mfma_i8(a[u][0], a[u][0], acc00);
+      acc01 = mfma_i8(a[u][0], a[u][1], acc01);
+      acc10 = mfma_i8(a[u][1], a[u][0], acc10);
+      acc11 = mfma_i8(a[u][1], a[u][1], acc11);
+    }
+  }
+  for (; ks < ks1; ks += 4) {
     const v4i a0 = Xmf[(int64_t)ks * 128 + lane];
     const v4i a1 = Xmf[(int64_t)ks * 128 + 64 + lane];
     acc00 = mfma_i8(a0, a0, acc00);
@@ -447,20 +467,31 @@ __device__ __forceinline__ bool side_gram_int(const v4i* __restrict__ Xmf, int64
   __syncthreads();
   if (!s_last) return false;
   __threadfence();
-  for (int e4 = threadIdx.x; e4 < 1024; e4 += blockDim.x) {
-    int4 acc = make_int4(0, 0, 0, 0);
-#pragma unroll 8
-    for (int q = 0; q < nside; ++q) {
-      const int4 v = ((const int4*)(gparti + (size_t)q * 4096))[e4];
-      acc.x += v.x;
-      acc.y += v.y;
-      acc.z += v.z;
-      acc.w += v.w;
+  // all nside x 4 loads of a thread are independent and issued together
+  // (nside <= NSIDE_INT, blockDim == NT): one round of memory latency
+  int4 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = make_int4(0, 0, 0, 0);
+#pragma unroll
+  for (int q = 0; q < NSIDE_INT; ++q) {
+    const int qq = q < nside ? q : nside - 1;
+    const int keep = q < nside;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int4 v = ((const int4*)(gparti + (size_t)qq * 4096))[threadIdx.x + NT * j];
+      acc[j].x += keep * v.x;
+      acc[j].y += keep * v.y;
+      acc[j].z += keep * v.z;
+      acc[j].w += keep * v.w;
     }
-    G[4 * e4] = (double)acc.x;
-    G[4 * e4 + 1] = (double)acc.y;
-    G[4 * e4 + 2] = (double)acc.z;
-    G[4 * e4 + 3] = (double)acc.w;
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e4 = threadIdx.x + NT * j;
+    G[4 * e4] = (double)acc[j].x;
+    G[4 * e4 + 1] = (double)acc[j].y;
+    G[4 * e4 + 2] = (double)acc[j].z;
+    G[4 * e4 + 3] = (double)acc[j].w;
   }
   if (threadIdx.x == 0) *counter = 0u;
   __syncthreads();
