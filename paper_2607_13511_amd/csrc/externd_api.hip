@@ -22,7 +22,7 @@ static inline int clampi(int64_t v, int64_t lo, int64_t hi) { return (int)(v < l
 struct Layout {
   int64_t m_pad, n_pad;
   int gv, gd, nblk_cap;
-  size_t off[32];
+  size_t off[40];
   size_t total;
 };
 
@@ -33,9 +33,10 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   const int64_t nct = L.n_pad / TILE, nrt = L.m_pad / TILE;
   // V-step: about 480 column-tile x row-group workgroups; deflation and
   // staging: about 640.
-  L.gv = clampi((480 + nct - 1) / nct, 1, nrt < 16 ? nrt : 16);
+  L.gv = clampi((480 + nct - 1) / nct, 1, nrt < GV_MAX ? nrt : GV_MAX);
   L.gd = clampi((640 + nct - 1) / nct, 1, nrt < 64 ? nrt : 64);
   L.nblk_cap = (int)(k + 2);  // fro2 before every block and after the last; one spare
+  const int64_t ntmax = nrt > nct ? nrt : nct;  // 32-index tiles of the longer side
   const size_t sizes[] = {
       sizeof(float) * (size_t)(L.m_pad * L.n_pad),     // 0 R
       (size_t)(BBP * L.m_pad),                         // 1 Ut
@@ -65,6 +66,10 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(unsigned) * (size_t)L.nblk_cap,           // 25 maxbits_w
       (size_t)(BBP * L.m_pad),                         // 26 Umf
       (size_t)(BBP * L.n_pad),                         // 27 Vmf
+      sizeof(double) * (size_t)(BBP * ntmax),          // 28 tps
+      sizeof(double) * (size_t)(BBP * ntmax),          // 29 tpm
+      sizeof(int) * (size_t)(BBP * ntmax),             // 30 tpi
+      sizeof(unsigned short) * (size_t)(BBP * L.m_pad),  // 31 Ub
   };
   size_t o = 0;
   for (size_t i = 0; i < sizeof(sizes) / sizeof(sizes[0]); ++i) {
@@ -116,6 +121,10 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.maxbits_w = (unsigned*)(b + L.off[25]);
   w.Umf = (int8_t*)(b + L.off[26]);
   w.Vmf = (int8_t*)(b + L.off[27]);
+  w.tps = (double*)(b + L.off[28]);
+  w.tpm = (double*)(b + L.off[29]);
+  w.tpi = (int*)(b + L.off[30]);
+  w.Ub = (unsigned short*)(b + L.off[31]);
   return true;
 }
 

@@ -17,6 +17,7 @@ constexpr int TILE = 32;
 constexpr int NSIDE_INT = 8;
 constexpr int NSIDE_W = 16;
 constexpr int NSIDE_MAX = 16;
+constexpr int GV_MAX = 8;      // row groups of the V-step contraction
 // Threads per workgroup for all kernels except the selection kernel.
 constexpr int NT = 256;
 constexpr int NT_SELECT = 1024;
@@ -38,10 +39,14 @@ struct Ws {
   float* R;              // m_pad x n_pad residual, fp32, row-major
   int8_t* Ut;            // BBP x m_pad, U transposed (component-major)
   int8_t* Ur;            // m_pad x BBP, U row-major
+  unsigned short* Ub;    // m_pad x BBP, U row-major as bf16 bits (deflation operand)
   int8_t* Vt;            // BBP x n_pad
   int8_t* Vr;            // n_pad x BBP
   int8_t* Umf;           // BBP x m_pad bytes, U in the MFMA-ready operand layout
   int8_t* Vmf;           // BBP x n_pad bytes, V in the MFMA-ready operand layout
+  double* tps;           // BBP x tiles: per-32-index-tile sum |x| of a target component
+  double* tpm;           // BBP x tiles: per-tile max |x|
+  int* tpi;              // BBP x tiles: per-tile smallest index attaining the max
   double* Q;             // BBP x m_pad, Q = R diag(h) V  (component-major)
   double* Z;             // BBP x m_pad, U-step target
   long long* Pp;         // gv x BBP x n_pad, V-step partial contractions

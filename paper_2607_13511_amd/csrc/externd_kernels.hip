@@ -776,91 +776,232 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 }
 
 // ---------------------------------------------------------------------------
-// V-step target Y = G_U^{-1} P (fp64); P summed over the gv row groups
-// (int64, exact) and scaled back by 2^-s.  grid: n_pad/32 column tiles.
+// Targets on fp64 MFMA (v_mfma_f64_16x16x4f64), one 32-index tile per WG,
+// plus the per-tile statistics of |x| that T_tau needs (Eq. (2)): the sum,
+// the max and the smallest index attaining it (indices < L only), written
+// component-major as ps/pm/pi[c * ntile + tile].
+// Wave w computes components 16 w .. 16 w + 15 of both 16-index halves:
+// lane l, register r <-> component 16 w + l/16 + 4 r, index 16 h + l%16.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ void tile_stats(const v4d (&x)[2], int w, int64_t i0, int64_t L, int ntile, int tile,
+                                           double* __restrict__ ps, double* __restrict__ pm, int* __restrict__ pi) {
+  const int lane = lane_id();
+  const int li = lane & 15, lk = lane >> 4;
+  const int64_t ia = i0 + li, ib = i0 + 16 + li;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const double a0 = ia < L ? fabs(x[0][r]) : 0.0, a1 = ib < L ? fabs(x[1][r]) : 0.0;
+    double s = a0 + a1;
+    // invalid indices never win the max
+    double mv = ia < L ? a0 : -1.0;
+    long long mi = ia;
+    argmax_merge(mv, mi, ib < L ? a1 : -1.0, ib);
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) {
+      s += __shfl_xor(s, o, 16);
+      const double mv2 = __shfl_xor(mv, o, 16);
+      const long long mi2 = __shfl_xor(mi, o, 16);
+      argmax_merge(mv, mi, mv2, mi2);
+    }
+    if (li == 0) {
+      const int c = 16 * w + lk + 4 * r;
+      ps[(int64_t)c * ntile + tile] = s;
+      pm[(int64_t)c * ntile + tile] = mv;
+      pi[(int64_t)c * ntile + tile] = (int)mi;
+    }
+  }
+}
+
+// V-step target Y = G_U^{-1} P (Eq. (3)); P summed over the gv row groups
+// (int64, exact) and scaled back by 2^-s.  grid: n_pad/32 column tiles.
 __global__ __launch_bounds__(NT) void k_vepi(const long long* __restrict__ Pp, int gv,
                                              const double* __restrict__ ginv, double* __restrict__ Y,
-                                             const unsigned* __restrict__ maxbits, int64_t n_pad) {
-  __shared__ double Ps[64][33];
-  __shared__ double Gi[64][65];
-  const int64_t j0 = (int64_t)blockIdx.x * TILE;
+                                             const unsigned* __restrict__ maxbits, int64_t n, int64_t n_pad,
+                                             double* __restrict__ ps, double* __restrict__ pm, int* __restrict__ pi) {
+  __shared__ double Ps[64 * 33];
+  const int ct = blockIdx.x;
+  const int64_t j0 = (int64_t)ct * TILE;
   const int s = fx_shift(*maxbits);
-  // all loads of a round are issued before any LDS store (independent
-  // iterations, compile-time trip counts)
+  // every partial of every group is loaded in one round (gv <= GV_MAX,
+  // compile-time trip counts; groups past gv re-read group 0, weight 0)
   long long acc[8];
 #pragma unroll
   for (int q = 0; q < 8; ++q) acc[q] = 0;
-  for (int g = 0; g < gv; ++g) {
+#pragma unroll
+  for (int g = 0; g < GV_MAX; ++g) {
+    const int gg = g < gv ? g : 0;
+    const long long keep = g < gv;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       const int e = threadIdx.x + q * NT, c = e >> 5, jj = e & 31;
-      acc[q] += Pp[((int64_t)g * BBP + c) * n_pad + j0 + jj];
+      acc[q] += keep * Pp[((int64_t)gg * BBP + c) * n_pad + j0 + jj];
     }
   }
-  double gv_[16];
-#pragma unroll
-  for (int q = 0; q < 16; ++q) gv_[q] = ginv[threadIdx.x + q * NT];
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
     const int e = threadIdx.x + q * NT;
-    Ps[e >> 5][e & 31] = ldexp((double)acc[q], -s);
+    Ps[(e >> 5) * 33 + (e & 31)] = ldexp((double)acc[q], -s);
   }
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+  // A = G^{-1}[16 w + li][4 ks + lk] (register, L2), B = P[4 ks + lk][16 h + li] (LDS)
+  double a[16];
 #pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    const int e = threadIdx.x + q * NT;
-    Gi[e >> 6][e & 63] = gv_[q];
-  }
+  for (int ks = 0; ks < 16; ++ks) a[ks] = ginv[(16 * w + li) * 64 + 4 * ks + lk];
   __syncthreads();
-  const int jj = threadIdx.x & 31, cg = threadIdx.x >> 5;
-  double y[8];
+  v4d y[2] = {v4d{}, v4d{}};
 #pragma unroll
-  for (int q = 0; q < 8; ++q) y[q] = 0.0;
-  for (int c2 = 0; c2 < 64; ++c2) {
-    const double p = Ps[c2][jj];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) y[q] += Gi[8 * cg + q][c2] * p;
+  for (int ks = 0; ks < 16; ++ks) {
+    y[0] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + li], y[0]);
+    y[1] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + 16 + li], y[1]);
   }
 #pragma unroll
-  for (int q = 0; q < 8; ++q) Y[(int64_t)(8 * cg + q) * n_pad + j0 + jj] = y[q];
+  for (int r = 0; r < 4; ++r) {
+    double* row = Y + (int64_t)(16 * w + lk + 4 * r) * n_pad + j0;
+    row[li] = y[0][r];
+    row[16 + li] = y[1][r];
+  }
+  tile_stats(y, w, j0, n, (int)gridDim.x, ct, ps, pm, pi);
 }
 
-// U-step target Z = Q G_V^{-1} (fp64).  grid: m_pad/32 row tiles.
+// U-step target Z = Q G_V^{-1} (Eq. (3)), computed as Z^T = G_V^{-T} Q^T so
+// that rows of Z^T (component-major) are written coalesced.
+// grid: m_pad/32 row tiles.
 __global__ __launch_bounds__(NT) void k_uepi(const double* __restrict__ Q, const double* __restrict__ ginv,
-                                             double* __restrict__ Z, int64_t m_pad) {
-  __shared__ double Qs[64][33];
-  __shared__ double Gi[64][65];
-  const int64_t i0 = (int64_t)blockIdx.x * TILE;
-  double qv_[8], gv_[16];
+                                             double* __restrict__ Z, int64_t m, int64_t m_pad,
+                                             double* __restrict__ ps, double* __restrict__ pm, int* __restrict__ pi) {
+  const int rt = blockIdx.x;
+  const int64_t i0 = (int64_t)rt * TILE;
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+  // A = G^{-1}[4 ks + lk][16 w + li] (transposed read), B = Q[4 ks + lk][i0 + 16 h + li]
+  double a[16], b0[16], b1[16];
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int e = threadIdx.x + q * NT;
-    qv_[q] = Q[(int64_t)(e >> 5) * m_pad + i0 + (e & 31)];
+  for (int ks = 0; ks < 16; ++ks) {
+    a[ks] = ginv[(4 * ks + lk) * 64 + 16 * w + li];
+    const double* qrow = Q + (int64_t)(4 * ks + lk) * m_pad + i0;
+    b0[ks] = qrow[li];
+    b1[ks] = qrow[16 + li];
+  }
+  v4d z[2] = {v4d{}, v4d{}};
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) {
+    z[0] = mfma_f64(a[ks], b0[ks], z[0]);
+    z[1] = mfma_f64(a[ks], b1[ks], z[1]);
   }
 #pragma unroll
-  for (int q = 0; q < 16; ++q) gv_[q] = ginv[threadIdx.x + q * NT];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int e = threadIdx.x + q * NT;
-    Qs[e >> 5][e & 31] = qv_[q];
+  for (int r = 0; r < 4; ++r) {
+    double* row = Z + (int64_t)(16 * w + lk + 4 * r) * m_pad + i0;
+    row[li] = z[0][r];
+    row[16 + li] = z[1][r];
   }
+  tile_stats(z, w, i0, m, (int)gridDim.x, rt, ps, pm, pi);
+}
+
+// ---------------------------------------------------------------------------
+// T_tau of one target component from its per-tile statistics (Eq. (2)):
+// theta = tau * (sum |x|) / L, strict ">", and when no entry exceeds theta
+// (max |x| <= theta) only the largest |x| (smallest index) is kept.  One
+// pass over x writes the trits component-major (dst[0 .. L_pad)) and into
+// the MFMA-ready layout mf, zero beyond L; with q it also returns
+// sum_i t_i q_i (fp64, fixed reduction order).  blockDim.x = NT_TERN.
+// ---------------------------------------------------------------------------
+constexpr int TERN_SPAN = 12;  // entries per thread kept in registers (L <= TERN_SPAN * NT_TERN in one pass)
+
+__device__ __forceinline__ double tern_from_stats(const double* __restrict__ x, const double* __restrict__ q, int64_t L,
+                                                  int64_t L_pad, int ntile, const double* __restrict__ ps,
+                                                  const double* __restrict__ pm, const int* __restrict__ pi,
+                                                  double tau, int8_t* __restrict__ dst, int8_t* __restrict__ mf,
+                                                  int c) {
+  __shared__ double shd[16];
+  __shared__ long long shl[16];
+  const int tid = threadIdx.x, st = blockDim.x;
+  // the target loads go out first; their latency overlaps the reduction
+  double xc[TERN_SPAN], qc[TERN_SPAN];
 #pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    const int e = threadIdx.x + q * NT;
-    Gi[e >> 6][e & 63] = gv_[q];
+  for (int cc = 0; cc < TERN_SPAN; ++cc) {
+    const int64_t i = tid + (int64_t)cc * st;
+    xc[cc] = i < L ? x[i] : 0.0;
+    qc[cc] = (q && i < L) ? q[i] : 0.0;
   }
-  __syncthreads();
-  const int ii = threadIdx.x & 31, cg = threadIdx.x >> 5;
-  double z[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) z[q] = 0.0;
-  for (int c2 = 0; c2 < 64; ++c2) {
-    const double qv = Qs[c2][ii];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) z[q] += qv * Gi[c2][8 * cg + q];
+  // statistics over the tiles, fixed order: thread-strided partials, then the block tree
+  double s = 0.0, mv = -1.0;
+  long long mi = 0;
+  for (int t = tid; t < ntile; t += st) {
+    s += ps[t];
+    argmax_merge(mv, mi, pm[t], pi[t]);
   }
+  const double S = block_sum_d(s, shd);
+  block_argmax(mv, mi, shd, shl);
+  const double theta = tau * (S / (double)L);
+  const bool keep_max = !(mv > theta);
+  double g = 0.0;
+  auto decide = [&](int64_t i, double xv) -> int8_t {
+    if (i >= L) return 0;
+    const bool on = keep_max ? (i == mi) : (fabs(xv) > theta);
+    return on ? ((xv > 0.0) ? 1 : ((xv < 0.0) ? -1 : 0)) : 0;
+  };
 #pragma unroll
-  for (int q = 0; q < 8; ++q) Z[(int64_t)(8 * cg + q) * m_pad + i0 + ii] = z[q];
+  for (int cc = 0; cc < TERN_SPAN; ++cc) {
+    const int64_t i = tid + (int64_t)cc * st;
+    if (i < L_pad) {
+      const int8_t t = decide(i, xc[cc]);
+      g += (double)t * qc[cc];
+      dst[i] = t;
+      mf[mf_offset(c, i)] = t;
+    }
+  }
+  for (int64_t i = tid + (int64_t)TERN_SPAN * st; i < L_pad; i += st) {
+    const double xv = i < L ? x[i] : 0.0;
+    const int8_t t = decide(i, xv);
+    if (q && i < L) g += (double)t * q[i];
+    dst[i] = t;
+    mf[mf_offset(c, i)] = t;
+  }
+  return block_sum_d(g, shd);
+}
+
+// V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.  grid: BBP.
+__global__ __launch_bounds__(NT_TERN) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb,
+                                                    double tau, const double* __restrict__ ps,
+                                                    const double* __restrict__ pm, const int* __restrict__ pi,
+                                                    int8_t* __restrict__ Vt, int8_t* __restrict__ Vmf) {
+  const int c = blockIdx.x;
+  const int ntile = (int)(n_pad / TILE);
+  int8_t* dst = Vt + (int64_t)c * n_pad;
+  if (c >= bb) {
+    for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
+      dst[j] = 0;
+      Vmf[mf_offset(c, j)] = 0;
+    }
+    return;
+  }
+  const int64_t o = (int64_t)c * ntile;
+  tern_from_stats(Y + (int64_t)c * n_pad, nullptr, n, n_pad, ntile, ps + o, pm + o, pi + o, tau, dst, Vmf, c);
+}
+
+// U <- T_tau(Z[:, c]); also g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for
+// the joint scale solve (Eq. (4)).  grid: BBP.
+__global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q,
+                                                    int64_t m, int64_t m_pad, int bb, double tau,
+                                                    const double* __restrict__ ps, const double* __restrict__ pm,
+                                                    const int* __restrict__ pi, int8_t* __restrict__ Ut,
+                                                    int8_t* __restrict__ Umf, double* __restrict__ gvec) {
+  const int c = blockIdx.x;
+  const int ntile = (int)(m_pad / TILE);
+  int8_t* dst = Ut + (int64_t)c * m_pad;
+  if (c >= bb) {
+    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) {
+      dst[i] = 0;
+      Umf[mf_offset(c, i)] = 0;
+    }
+    if (threadIdx.x == 0) gvec[c] = 0.0;
+    return;
+  }
+  const int64_t o = (int64_t)c * ntile;
+  const double g = tern_from_stats(Z + (int64_t)c * m_pad, Q + (int64_t)c * m_pad, m, m_pad, ntile, ps + o, pm + o,
+                                   pi + o, tau, dst, Umf, c);
+  if (threadIdx.x == 0) gvec[c] = g;
 }
 
 // ---------------------------------------------------------------------------
@@ -950,43 +1091,6 @@ __device__ __forceinline__ double ternarize_wg(Load load, const double* __restri
   return g;
 }
 
-// V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.  grid: BBP.
-__global__ __launch_bounds__(NT_TERN) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb,
-                                                    double tau, int8_t* __restrict__ Vt, int8_t* __restrict__ Vmf) {
-  const int c = blockIdx.x;
-  int8_t* dst = Vt + (int64_t)c * n_pad;
-  if (c >= bb) {
-    for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
-      dst[j] = 0;
-      Vmf[mf_offset(c, j)] = 0;
-    }
-    return;
-  }
-  const double* y = Y + (int64_t)c * n_pad;
-  ternarize_wg([=](int64_t j) { return y[j]; }, nullptr, n, n_pad, tau, dst, Vmf, c);
-}
-
-// U <- T_tau(Z[:, c]); also g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for
-// the joint scale solve (Eq. (4)).  grid: BBP.
-__global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q,
-                                                    int64_t m, int64_t m_pad, int bb, double tau,
-                                                    int8_t* __restrict__ Ut, int8_t* __restrict__ Umf,
-                                                    double* __restrict__ gvec) {
-  const int c = blockIdx.x;
-  int8_t* dst = Ut + (int64_t)c * m_pad;
-  if (c >= bb) {
-    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) {
-      dst[i] = 0;
-      Umf[mf_offset(c, i)] = 0;
-    }
-    if (threadIdx.x == 0) gvec[c] = 0.0;
-    return;
-  }
-  const double* z = Z + (int64_t)c * m_pad;
-  const double g = ternarize_wg([=](int64_t i) { return z[i]; }, Q + (int64_t)c * m_pad, m, m_pad, tau, dst, Umf, c);
-  if (threadIdx.x == 0) gvec[c] = g;
-}
-
 // Block initialisation (paper silent; reading: U[:, c] = T_tau(R[:, J_c])).
 // grid: BBP.
 __global__ __launch_bounds__(NT_TERN) void k_init(const float* __restrict__ R, const int* __restrict__ J, int64_t m,
@@ -1007,10 +1111,11 @@ __global__ __launch_bounds__(NT_TERN) void k_init(const float* __restrict__ R, c
   ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, nullptr, m, m_pad, tau, dst, Umf, c);
 }
 
-// Xt (BBP x L int8, component-major) -> Xr (L x BBP, row-major).
+// Xt (BBP x L int8, component-major) -> Xr (L x BBP, row-major) and, when
+// Xb is given, the same trits as bf16 (0, +-1.0; L x BBP).
 // grid: L/32 chunks.
 __global__ __launch_bounds__(NT) void k_transpose8(const int8_t* __restrict__ Xt, int8_t* __restrict__ Xr,
-                                                   int64_t L) {
+                                                   int64_t L, unsigned short* __restrict__ Xb) {
   __shared__ int8_t tile[32][BBP + 4];
   const int64_t j0 = (int64_t)blockIdx.x * 32;
   for (int e = threadIdx.x; e < BBP * 32; e += NT) {
@@ -1020,7 +1125,9 @@ __global__ __launch_bounds__(NT) void k_transpose8(const int8_t* __restrict__ Xt
   __syncthreads();
   for (int e = threadIdx.x; e < BBP * 32; e += NT) {
     const int jj = e >> 6, c = e & 63;
-    Xr[(j0 + jj) * BBP + c] = tile[jj][c];
+    const int8_t t = tile[jj][c];
+    Xr[(j0 + jj) * BBP + c] = t;
+    if (Xb) Xb[(j0 + jj) * BBP + c] = t == 0 ? 0 : (t > 0 ? 0x3F80u : 0xBF80u);
   }
 }
 
@@ -1080,7 +1187,7 @@ __device__ __forceinline__ short tern_bf16(int8_t t, unsigned short mag) {
   return (short)(t == 0 ? 0 : (t > 0 ? mag : (unsigned short)(mag ^ 0x8000u)));
 }
 
-__global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const int8_t* __restrict__ Ur,
+__global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s* __restrict__ Ub,
                                                 const int8_t* __restrict__ Vr, const float* __restrict__ dF,
                                                 double* __restrict__ colE_part, unsigned* __restrict__ maxbits_next,
                                                 unsigned* __restrict__ maxbits_w_next, const double* __restrict__ hw,
@@ -1119,31 +1226,42 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const int
   }
   double csum = 0.0;
   float vmax = 0.0f;
+  // software pipeline: the residual values and U fragments of the wave's
+  // next row tile (rt + 4, other rows) are loaded before this tile is
+  // updated and stored
+  float xn[16];
+  v8s un[4];
+  auto load_tile = [&](int rt) {
+    const int64_t i0 = (int64_t)rt * TILE;
+    // A fragments: row i0 + l32, components 16 ks + 8 h .. + 8 (bf16)
+    const v8s* urow = Ub + (i0 + l32) * (BBP / 8);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) un[ks] = urow[2 * ks + h];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) xn[r] = R[(i0 + 8 * (r >> 2) + 4 * h + (r & 3)) * n_pad + col];
+  };
+  if (rt0 + wave < rt1) load_tile(rt0 + wave);
   for (int rt = rt0 + wave; rt < rt1; rt += 4) {
     const int64_t i0 = (int64_t)rt * TILE;
-    const int8_t* urow = Ur + (i0 + l32) * BBP;
+    float x[16];
+    v8s uu[4];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) x[r] = xn[r];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) uu[ks] = un[ks];
+    if (rt + 4 < rt1) load_tile(rt + 4);
     v16f acc = {};
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const uint2 uu = *(const uint2*)(urow + 16 * ks + 8 * h);
-      v8s Af;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const unsigned word = (e < 4) ? uu.x : uu.y;
-        const int8_t t = (int8_t)((word >> (8 * (e & 3))) & 0xff);
-        Af[e] = tern_bf16(t, (unsigned short)0x3F80u);
-      }
+    for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
       for (int p = 0; p < 3; ++p)
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, Af), __builtin_bit_cast(v8bf, Bf[p][ks]),
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, uu[ks]), __builtin_bit_cast(v8bf, Bf[p][ks]),
                                                       acc, 0, 0, 0);
-    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = 8 * (r >> 2) + 4 * h + (r & 3);
-      float* p = R + (i0 + row) * n_pad + col;
-      const float v = *p - acc[r];
-      *p = v;
+      const float v = x[r] - acc[r];
+      R[(i0 + row) * n_pad + col] = v;
       csum += (double)v * (double)v;
       vmax = fmaxf(vmax, fabsf(v));
     }
@@ -1658,10 +1776,11 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_vepi, dim3((unsigned)(w.n_pad / TILE)), dim3(NT), 0, s, w.Pp, w.gv, w.ginvU, w.Y,
-                     w.maxbits + blk, w.n_pad);
+                     w.maxbits + blk, w.n, w.n_pad, w.tps, w.tpm, w.tpi);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.Vt, w.Vmf);
+  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi, w.Vt,
+                     w.Vmf);
   return hipGetLastError();
 }
 
@@ -1670,7 +1789,8 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
   const unsigned nside = weighted ? NSIDE_W : NSIDE_INT;
   const unsigned grid = (unsigned)(nside + w.m_pad / TILE);
   if (weighted) {
-    hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad);
+    hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad,
+                       (unsigned short*)nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
@@ -1685,10 +1805,12 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_uepi, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0, s, w.Q, w.ginvV, w.Z, w.m_pad);
+  hipLaunchKernelGGL(k_uepi, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0, s, w.Q, w.ginvV, w.Z, w.m, w.m_pad, w.tps,
+                     w.tpm, w.tpi);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.Ut, w.Umf, w.gvec);
+  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.tps, w.tpm, w.tpi,
+                     w.Ut, w.Umf, w.gvec);
   return hipGetLastError();
 }
 
@@ -1699,15 +1821,16 @@ hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
 }
 
 hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s, Timer* tm) {
-  hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.m_pad / 32)), dim3(NT), 0, s, w.Ut, w.Ur, w.m_pad);
+  hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.m_pad / 32)), dim3(NT), 0, s, w.Ut, w.Ur, w.m_pad, w.Ub);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad);
+  hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad,
+                     (unsigned short*)nullptr);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
   EXTERND_TIMED(tm, EXTERND_KCLASS_DEFLATE,
-                hipLaunchKernelGGL(k_deflate, dim3(grid), dim3(NT), 0, s, w.R, w.Ur, w.Vr, w.dF, w.colE_part,
+                hipLaunchKernelGGL(k_deflate, dim3(grid), dim3(NT), 0, s, w.R, (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part,
                                    w.maxbits + blk + 1, w.maxbits_w + blk + 1, w.hw, w.m_pad, w.n_pad, w.gd));
   return hipGetLastError();
 }
