@@ -48,6 +48,9 @@ extern "C" {
 #define EXTERND_EWORKSPACE   -3  /* workspace smaller than externd_workspace_bytes()    */
 #define EXTERND_EHIP         -4  /* HIP runtime or launch failure                       */
 #define EXTERND_EUNSUPPORTED -5  /* shape outside the supported range                   */
+#define EXTERND_ESYNC        -6  /* a bounded wait between the workgroups of one kernel
+                                    launch ran out; the call's results are unusable
+                                    (reported instead of hanging; not expected)          */
 
 /* Largest block width the kernels handle; larger requests are clamped. */
 #define EXTERND_MAX_BLOCK 64

@@ -70,6 +70,8 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(double) * (size_t)(BBP * ntmax),          // 29 tpm
       sizeof(int) * (size_t)(BBP * ntmax),             // 30 tpi
       sizeof(unsigned short) * (size_t)(BBP * L.m_pad),  // 31 Ub
+      sizeof(unsigned) * (size_t)nct,                  // 32 tilecnt
+      sizeof(int) * 2 * 4096,                          // 33 gacc
   };
   size_t o = 0;
   for (size_t i = 0; i < sizeof(sizes) / sizeof(sizes[0]); ++i) {
@@ -125,6 +127,8 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.tpm = (double*)(b + L.off[29]);
   w.tpi = (int*)(b + L.off[30]);
   w.Ub = (unsigned short*)(b + L.off[31]);
+  w.tilecnt = (unsigned*)(b + L.off[32]);
+  w.gacc = (int*)(b + L.off[33]);
   return true;
 }
 
@@ -214,6 +218,7 @@ const char* externd_strerror(int status) {
     case EXTERND_EWORKSPACE: return "workspace too small or misaligned";
     case EXTERND_EHIP: return "HIP runtime or launch failure";
     case EXTERND_EUNSUPPORTED: return "unsupported shape";
+    case EXTERND_ESYNC: return "device-side synchronisation between workgroups timed out";
     default: return "unknown status";
   }
 }
@@ -275,7 +280,7 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
     HIP_TRY(launch_select(w, (int)blk, bb, s));
     HIP_TRY(launch_init(w, bb, tau, s));
     for (int it = 0; it < iters; ++it) {
-      HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm));
+      HIP_TRY(launch_vstep(w, (int)blk, bb, tau, weighted, s, tm));
       HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, s, tm));
     }
     HIP_TRY(launch_scale(w, bb, s));
@@ -287,7 +292,9 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   std::vector<double> f2((size_t)nblk + 1), f2w((size_t)nblk + 1);
   HIP_TRY(hipMemcpyAsync(f2.data(), w.fro2_hist, sizeof(double) * (nblk + 1), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipMemcpyAsync(f2w.data(), w.fro2w_hist, sizeof(double) * (nblk + 1), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
+  if (flags[FLAG_SYNC]) return EXTERND_ESYNC;
   if (tm) HIP_TRY(tm->collect(times->total_ms, times->launches, EXTERND_KCLASS_COUNT));
   const double a2 = f2[0], a2w = f2w[0];
   auto E = [&](int64_t b) { return a2 == 0.0 ? 1.0 : 1.0 - f2[(size_t)b] / a2; };
@@ -357,7 +364,8 @@ int externd_step_vstep(const float* R, int64_t m, int64_t n, const int8_t* U, in
   HIP_TRY(launch_prep(w, nullptr, s));
   HIP_TRY(launch_stage(w, R, n, s));
   HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
-  HIP_TRY(launch_vstep(w, 0, bb, tau, s));
+  HIP_TRY(launch_gram_acc(w, 0, s));
+  HIP_TRY(launch_vstep(w, 0, bb, tau, true, s));
   HIP_TRY(launch_store_factor(V_out, w.Vt, n, w.n_pad, bb, s));
   if (Y_out_or_null) {
     // Y is bb x n: row c of the component-major buffer, pitch n_pad -> n
@@ -378,6 +386,7 @@ int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, in
   HIP_TRY(launch_prep(w, h, s));
   HIP_TRY(launch_stage(w, R, n, s));
   HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
+  if (!h) HIP_TRY(launch_gram_acc(w, 1, s));
   HIP_TRY(launch_ustep(w, 0, bb, tau, h != nullptr, s));
   HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
   if (Q_out_or_null) HIP_TRY(launch_store_cm(Q_out_or_null, w.Q, m, w.m_pad, bb, s));
@@ -397,6 +406,7 @@ int externd_step_scale(const int8_t* U, const int8_t* V, const double* Q, int64_
   HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
   HIP_TRY(launch_load_cm(w.Q, Q, m, w.m_pad, bb, s));
   HIP_TRY(launch_gram_only(w, bb, h != nullptr, s));
+  HIP_TRY(launch_gram_acc(w, 0, s));
   HIP_TRY(launch_gvec(w, bb, s));
   HIP_TRY(launch_scale(w, bb, s));
   HIP_TRY(hipMemcpyAsync(d_out, w.dvec, sizeof(double) * bb, hipMemcpyDeviceToDevice, s));

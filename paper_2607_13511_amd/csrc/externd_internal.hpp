@@ -14,7 +14,8 @@ constexpr int BBP = 64;
 constexpr int TILE = 32;
 // Side workgroups that build Gram matrices next to a contraction: integer
 // Grams (int8 MFMA) and the weighted fp64 Gram (fp64 MFMA).
-constexpr int NSIDE_INT = 8;
+constexpr int NSIDE_INT = 8;   // integer-Gram workgroups of the scale solve
+constexpr int NSIDE_GRAM = 16; // workgroups of the integer Gram launch
 constexpr int NSIDE_W = 16;
 constexpr int NSIDE_MAX = 16;
 constexpr int GV_MAX = 8;      // row groups of the V-step contraction
@@ -25,9 +26,10 @@ constexpr int NT_TERN = 1024;   // per-component ternarization kernels
 
 // Index of counters in Ws::counters (each used by one kernel family, reset
 // to zero by the workgroup that consumes it).
-enum Counter { CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2, CNT_COUNT = 8 };
+// CNT_READY_*: G^{-1} of the V-step (U Gram) / U-step (V Gram) is stored.
+enum Counter { CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2, CNT_READY_U = 3, CNT_READY_V = 4, CNT_COUNT = 8 };
 // Flags written by the device, read by the host.
-enum Flag { FLAG_NONFINITE = 0, FLAG_BADWEIGHT = 1, FLAG_COUNT = 4 };
+enum Flag { FLAG_NONFINITE = 0, FLAG_BADWEIGHT = 1, FLAG_SYNC = 2, FLAG_COUNT = 4 };
 
 // Device workspace carved out of the caller's buffer.
 struct Ws {
@@ -47,6 +49,8 @@ struct Ws {
   double* tps;           // BBP x tiles: per-32-index-tile sum |x| of a target component
   double* tpm;           // BBP x tiles: per-tile max |x|
   int* tpi;              // BBP x tiles: per-tile smallest index attaining the max
+  unsigned* tilecnt;     // n_pad/32: arrivals per V-step column tile (0 between launches)
+  int* gacc;             // 2 x 4096: integer Gram accumulators of the V-step (U) and U-step (V)
   double* Q;             // BBP x m_pad, Q = R diag(h) V  (component-major)
   double* Z;             // BBP x m_pad, U-step target
   long long* Pp;         // gv x BBP x n_pad, V-step partial contractions
@@ -100,7 +104,9 @@ hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s)
 hipError_t launch_select(const Ws& w, int blk, int bb, hipStream_t s);
 hipError_t launch_finish(const Ws& w, int blk, hipStream_t s);
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s);
-hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr);
+// weighted: the U-step builds V^T H V itself, so the V-step's ternarization
+// skips the integer V Gram.
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* t = nullptr);
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s,
                         Timer* t = nullptr);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
@@ -119,6 +125,8 @@ hipError_t launch_unstage(const Ws& w, float* A, hipStream_t s);
 hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2, hipStream_t s);
 hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s);
 hipError_t launch_gvec(const Ws& w, int bb, hipStream_t s);
+// X^T X of the factor in Umf (which = 0) or Vmf (which = 1) into its Gram accumulator.
+hipError_t launch_gram_acc(const Ws& w, int which, hipStream_t s);
 hipError_t launch_set_scales(const Ws& w, const double* d, int bb, hipStream_t s);
 
 }  // namespace externd

@@ -404,6 +404,55 @@ __device__ __forceinline__ void ridge_invert_store(double* G, double* colbuf, in
 }
 
 // ---------------------------------------------------------------------------
+// Ready flag between the side workgroups (which store G^{-1}) and the
+// contraction workgroups of the same launch (which apply it).  Workgroups
+// are dispatched in index order and the side workgroups come first and
+// wait on nothing, so a waiting contraction workgroup never blocks them.
+// The flag is 0 before the launch (cleared by the next kernel in the
+// stream and at set-up); the wait is bounded and reports a timeout through
+// FLAG_SYNC instead of hanging.
+// Data that crosses workgroups inside one launch is read with device-scope
+// (coherent) atomic loads, so the waiting side needs no cache-invalidating
+// fence: with one L2 per XCD an acquire fence in hundreds of workgroups
+// would discard the L2 contents the streaming workgroups rely on.
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ T load_coherent(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ void store_coherent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+constexpr unsigned SPIN_LIMIT = 1u << 24;
+
+// The barrier completes every wave's stores into the XCD's L2; one
+// device-scope release (L2 write-back) by the signalling thread then
+// covers them all.
+__device__ __forceinline__ void signal_ready(unsigned* ready) {
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have completed
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __hip_atomic_store(ready, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+__device__ __forceinline__ void wait_ready(unsigned* ready, int* flags) {
+  if (threadIdx.x == 0) {
+    unsigned spins = 0;
+    while (load_coherent(ready) == 0u) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > SPIN_LIMIT) {
+        atomicOr(flags + FLAG_SYNC, 1);
+        break;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
 // Gram matrices of a ternary factor, built by `nside` workgroups
 // ---------------------------------------------------------------------------
 // Partial integer Gram of X (BBP x L int8, MFMA-ready layout) over this
@@ -498,6 +547,83 @@ __device__ __forceinline__ bool side_gram_int(const v4i* __restrict__ Xmf, int64
   return true;
 }
 
+// ---------------------------------------------------------------------------
+// Integer Gram of a ternary factor, computed by a small launch right after
+// the factor is made (no residual stream to compete with): NSIDE_GRAM
+// workgroups add X^T X (MFMA-ready layout) into the accumulator gacc
+// (4096 int32) with integer atomics, exact and independent of order.  The
+// launch that needs G^{-1} takes the accumulated Gram and clears gacc.
+// ---------------------------------------------------------------------------
+// Partial Gram over the K steps [ks0, ks1) of X, added into gacc.  Waves
+// 0..3 compute (any blockDim that is a multiple of 256), each keeping KR K
+// steps of loads in flight, and store their tiles to their own LDS region;
+// all threads then sum the four regions and add the nonzero entries into
+// gacc.  red: LDS, 4 x 4096 int32.
+__device__ __forceinline__ void gram_accumulate(const v4i* __restrict__ Xmf, int ks0, int ks1, int* gacc, int* red) {
+  constexpr int KR = 8;
+  const int lane = lane_id(), wave = wave_id();
+  const int h = lane >> 5, l32 = lane & 31;
+  if (wave < 4) {
+    v16i acc00 = {}, acc01 = {}, acc10 = {}, acc11 = {};
+    for (int ks = ks0 + wave; ks < ks1; ks += 4 * KR) {
+      v4i a[KR][2];
+#pragma unroll
+      for (int u = 0; u < KR; ++u) {
+        const int kk = ks + 4 * u;
+        if (kk < ks1) {
+          a[u][0] = Xmf[(int64_t)kk * 128 + lane];
+          a[u][1] = Xmf[(int64_t)kk * 128 + 64 + lane];
+        } else {
+          a[u][0] = v4i{};
+          a[u][1] = v4i{};
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < KR; ++u) {
+        acc00 = mfma_i8(a[u][0], a[u][0], acc00);
+        acc01 = mfma_i8(a[u][0], a[u][1], acc01);
+        acc10 = mfma_i8(a[u][1], a[u][0], acc10);
+        acc11 = mfma_i8(a[u][1], a[u][1], acc11);
+      }
+    }
+    int* mine = red + wave * 4096;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int M = 8 * (r >> 2) + 4 * h + (r & 3);
+      const int N = l32;
+      mine[M * 64 + N] = acc00[r];
+      mine[M * 64 + 32 + N] = acc01[r];
+      mine[(32 + M) * 64 + N] = acc10[r];
+      mine[(32 + M) * 64 + 32 + N] = acc11[r];
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 4096; e += blockDim.x) {
+    const int v = red[e] + red[4096 + e] + red[8192 + e] + red[12288 + e];
+    if (v) __hip_atomic_fetch_add(gacc + e, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Consumer (a later launch than the producer, so plain accesses suffice):
+// the accumulated Gram into G (LDS, fp64); gacc is cleared for the next
+// accumulation.  blockDim == NT: 16 entries per thread, loaded in one round.
+__device__ __forceinline__ void take_gram(int* gacc, double* G) {
+  int4 v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] = ((const int4*)gacc)[threadIdx.x + NT * j];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = 4 * (threadIdx.x + NT * j);
+    G[e] = (double)v[j].x;
+    G[e + 1] = (double)v[j].y;
+    G[e + 2] = (double)v[j].z;
+    G[e + 3] = (double)v[j].w;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) ((int4*)gacc)[threadIdx.x + NT * j] = make_int4(0, 0, 0, 0);
+}
+
 // Partial weighted Gram V^T diag(hw) V over this workgroup's share of rows
 // of Vr (n_pad x BBP int8, row-major) on fp64 MFMA (v_mfma_f64_16x16x4):
 // products h~_j v_jc v_jc' are exact and the sums are fp64.  The 10
@@ -581,9 +707,129 @@ __device__ __forceinline__ bool side_gram_w(const int8_t* __restrict__ Vr, const
 }
 
 // ---------------------------------------------------------------------------
-// V-step contraction P = U^T R  (Eq. (3), first half)
-// grid: nside side WGs (Gram U^T U + ridge + inverse) followed by
-//       (n_pad/32 column tiles) x gv row groups.
+// Targets on fp64 MFMA (v_mfma_f64_16x16x4f64), one 32-index tile at a
+// time, plus the per-tile statistics of |x| that T_tau needs (Eq. (2)):
+// the sum, the max and the smallest index attaining it (indices < L only),
+// written component-major as ps/pm/pi[c * ntile + tile].
+// Wave w computes components 16 w .. 16 w + 15 of both 16-index halves:
+// lane l, register r <-> component 16 w + l/16 + 4 r, index 16 h + l%16.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void tile_stats(const v4d (&x)[2], int w, int64_t i0, int64_t L, int ntile, int tile,
+                                           double* __restrict__ ps, double* __restrict__ pm, int* __restrict__ pi) {
+  const int lane = lane_id();
+  const int li = lane & 15, lk = lane >> 4;
+  const int64_t ia = i0 + li, ib = i0 + 16 + li;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const double a0 = ia < L ? fabs(x[0][r]) : 0.0, a1 = ib < L ? fabs(x[1][r]) : 0.0;
+    double s = a0 + a1;
+    // invalid indices never win the max
+    double mv = ia < L ? a0 : -1.0;
+    long long mi = ia;
+    argmax_merge(mv, mi, ib < L ? a1 : -1.0, ib);
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) {
+      s += __shfl_xor(s, o, 16);
+      const double mv2 = __shfl_xor(mv, o, 16);
+      const long long mi2 = __shfl_xor(mi, o, 16);
+      argmax_merge(mv, mi, mv2, mi2);
+    }
+    if (li == 0) {
+      const int c = 16 * w + lk + 4 * r;
+      ps[(int64_t)c * ntile + tile] = s;
+      pm[(int64_t)c * ntile + tile] = mv;
+      pi[(int64_t)c * ntile + tile] = (int)mi;
+    }
+  }
+}
+
+// V-step target tile Y[:, j0 .. j0+32) = G_U^{-1} P (Eq. (3)).
+// vtarget_sum: P summed over the gv row-group partials (int64, exact) and
+// scaled back by 2^-s into Ps (LDS, 64 x 33 doubles); vtarget_apply: the
+// product with G_U^{-1}, the stores and the T_tau statistics.
+__device__ __forceinline__ void vtarget_sum(const long long* __restrict__ Pp, int gv, int s, int64_t n_pad, int ct,
+                                            double* Ps) {
+  const int64_t j0 = (int64_t)ct * TILE;
+  // every partial of every group is loaded in one round (gv <= GV_MAX,
+  // compile-time trip counts; groups past gv re-read group 0, weight 0)
+  long long acc[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) acc[q] = 0;
+#pragma unroll
+  for (int g = 0; g < GV_MAX; ++g) {
+    const int gg = g < gv ? g : 0;
+    const long long keep = g < gv;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = threadIdx.x + q * NT, c = e >> 5, jj = e & 31;
+      acc[q] += keep * load_coherent(Pp + ((int64_t)gg * BBP + c) * n_pad + j0 + jj);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int e = threadIdx.x + q * NT;
+    Ps[(e >> 5) * 33 + (e & 31)] = ldexp((double)acc[q], -s);
+  }
+}
+__device__ __forceinline__ void vtarget_apply(const double* __restrict__ ginv, double* __restrict__ Y, int64_t n,
+                                              int64_t n_pad, int ct, int ntile, double* ps, double* pm, int* pi,
+                                              const double* Ps) {
+  const int64_t j0 = (int64_t)ct * TILE;
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+  // A = G^{-1}[16 w + li][4 ks + lk], B = P[4 ks + lk][16 h + li] (LDS)
+  double a[16];
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(ginv + (16 * w + li) * 64 + 4 * ks + lk);
+  __syncthreads();
+  v4d y[2] = {v4d{}, v4d{}};
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) {
+    y[0] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + li], y[0]);
+    y[1] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + 16 + li], y[1]);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    double* row = Y + (int64_t)(16 * w + lk + 4 * r) * n_pad + j0;
+    row[li] = y[0][r];
+    row[16 + li] = y[1][r];
+  }
+  tile_stats(y, w, j0, n, ntile, ct, ps, pm, pi);
+}
+
+// U-step target tile Z[i0 .. i0+32, :] = Q G_V^{-1} (Eq. (3)), computed as
+// Z^T = G_V^{-T} Q^T so that rows of Z^T (component-major) are written
+// coalesced.  Qs: LDS tile Q^T, Qs[c * 32 + i].
+__device__ __forceinline__ void utarget_tile(const double* Qs, const double* __restrict__ ginv, double* __restrict__ Z,
+                                             int64_t m, int64_t m_pad, int rt, int ntile, double* ps, double* pm,
+                                             int* pi) {
+  const int64_t i0 = (int64_t)rt * TILE;
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+  double a[16];
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(ginv + (4 * ks + lk) * 64 + 16 * w + li);
+  v4d z[2] = {v4d{}, v4d{}};
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) {
+    z[0] = mfma_f64(a[ks], Qs[(4 * ks + lk) * 32 + li], z[0]);
+    z[1] = mfma_f64(a[ks], Qs[(4 * ks + lk) * 32 + 16 + li], z[1]);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    double* row = Z + (int64_t)(16 * w + lk + 4 * r) * m_pad + i0;
+    row[li] = z[0][r];
+    row[16 + li] = z[1][r];
+  }
+  tile_stats(z, w, i0, m, ntile, rt, ps, pm, pi);
+}
+
+// ---------------------------------------------------------------------------
+// V-step P = U^T R and target Y = G_U^{-1} P  (Eq. (3), first half)
+// grid: one side WG (the accumulated U Gram, ridge, inverse) followed by
+//       (n_pad/32 column tiles) x gv row groups; the last of the gv WGs of a
+//       column tile (per-tile counter) sums the int64 partials, waits for
+//       G_U^{-1} and writes the Y tile and its T_tau statistics.
 // Each WG owns 32 columns and a contiguous range of 32-row K steps, split
 // over its 4 waves; A = U (MFMA-ready layout), B = R digit planes.  Lane
 // (j, h) loads column j, rows 16h .. 16h+15 of the K step: every load
@@ -591,16 +837,22 @@ __device__ __forceinline__ bool side_gram_w(const int8_t* __restrict__ Vr, const
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vstep(const float* __restrict__ R, const v4i* __restrict__ Umf,
                                               long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
-                                              int64_t m_pad, int64_t n_pad, int gv, int bb, int* gparti,
-                                              unsigned* counter, double* ginvU, int nside) {
+                                              int64_t m_pad, int64_t n_pad, int gv, int bb, int* gacc,
+                                              double* ginvU, int nside, double* __restrict__ Y,
+                                              int64_t n, double* ps, double* pm, int* pi, unsigned* tilecnt,
+                                              unsigned* ready, int* flags) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[8192];
   if ((int)blockIdx.x < nside) {
-    int* ired = (int*)smem;
+    // the side path is the launch's critical path: its waves win issue
+    // arbitration against the streaming waves sharing their SIMDs
+    __builtin_amdgcn_s_setprio(3);
     double* Gs = (double*)(smem + 2048);
     double* pbuf = Gs + 4096;
-    if (side_gram_int(Umf, m_pad, blockIdx.x, nside, gparti, counter, Gs, ired)) ridge_invert_store(Gs, pbuf, bb, ginvU);
+    take_gram(gacc, Gs);
+    ridge_invert_store(Gs, pbuf, bb, ginvU);
+    signal_ready(ready);
     return;
   }
   const int b = blockIdx.x - nside;
@@ -652,13 +904,33 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   }
   // out[t][M = component][N = column]
   long long* Pg = Pp + ((int64_t)g * BBP) * n_pad + (int64_t)ct * TILE;
-  reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { Pg[(int64_t)(32 * t + M) * n_pad + N] = v; });
+  // partials go out with coherent stores; each wave waits for its own
+  // stores to complete before the arrival is counted
+  reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { store_coherent(Pg + (int64_t)(32 * t + M) * n_pad + N, v); });
+  __builtin_amdgcn_s_waitcnt(0);
+  // the last of the tile's gv workgroups forms the target tile
+  __shared__ int s_last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned old = __hip_atomic_fetch_add(tilecnt + ct, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (old == (unsigned)(gv - 1));
+  }
+  __syncthreads();
+  if (!s_last) return;
+  if (threadIdx.x == 0) store_coherent(tilecnt + ct, 0u);  // every group has arrived: ready for the next launch
+  vtarget_sum(Pp, gv, s, n_pad, ct, (double*)smem);
+  wait_ready(ready, flags);
+  vtarget_apply(ginvU, Y, n, n_pad, ct, nct, ps, pm, pi, (double*)smem);
 }
 
 // ---------------------------------------------------------------------------
-// U-step contraction Q = R diag(h~) V  (Eq. (3) second half, Sec. 2.5)
-// grid: nside side WGs (Gram V^T H V + ridge + inverse, raw Gram kept for
-//       the scale solve) followed by m_pad/32 row tiles.
+// U-step Q = R diag(h~) V and target Z = Q G_V^{-1}  (Eq. (3) second half,
+// Sec. 2.5)
+// grid: side WGs (the accumulated V Gram, or, weighted, NSIDE_W WGs
+//       building V^T H V; ridge, inverse; the raw Gram is kept for the scale
+//       solve) followed by m_pad/32 row tiles; each row tile
+//       stores Q, waits for G_V^{-1} and writes its Z tile and T_tau
+//       statistics.
 // Each WG owns 32 full rows; its 4 waves interleave 32-column K steps.
 // A = R digit planes (rows x columns), B = V (MFMA-ready layout).  Each
 // wave streams its 32 x 32 residual tiles into LDS with direct loads
@@ -674,22 +946,26 @@ template <bool WEIGHTED>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_ustep(const float* __restrict__ R, const v4i* __restrict__ Vmf,
                                               const int8_t* __restrict__ Vr, const double* __restrict__ hw,
                                               double* __restrict__ Q, const unsigned* __restrict__ maxbits,
-                                              int64_t m_pad, int64_t n_pad, int bb, int* gparti, double* gpart,
-                                              unsigned* counter, double* ginvV, double* gramV, int nside) {
+                                              int64_t m_pad, int64_t n_pad, int bb, int* gacc, double* gpart,
+                                              unsigned* counter, double* ginvV, double* gramV, int nside,
+                                              double* __restrict__ Z, int64_t m, double* ps, double* pm, int* pi,
+                                              unsigned* ready, int* flags) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[8192];
   if ((int)blockIdx.x < nside) {
-    int* ired = (int*)smem;
+    // critical path of the launch (see k_vstep)
+    __builtin_amdgcn_s_setprio(3);
     double* Gs = (double*)(smem + 2048);
     double* pbuf = Gs + 4096;
-    bool last;
+    bool last = true;
     if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, nside, gpart, counter, Gs);
-    else last = side_gram_int(Vmf, n_pad, blockIdx.x, nside, gparti, counter, Gs, ired);
+    else take_gram(gacc, Gs);
     if (last) {
       for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
       __syncthreads();
       ridge_invert_store(Gs, pbuf, bb, ginvV);
+      signal_ready(ready);
     }
     return;
   }
@@ -773,129 +1049,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { tq[(32 * t + N) * 32 + M] = ldexp((double)v, -s); });
   __syncthreads();
   for (int e = threadIdx.x; e < 2048; e += NT) Q[(int64_t)(e >> 5) * m_pad + (int64_t)rt * TILE + (e & 31)] = tq[e];
-}
-
-// ---------------------------------------------------------------------------
-// Targets on fp64 MFMA (v_mfma_f64_16x16x4f64), one 32-index tile per WG,
-// plus the per-tile statistics of |x| that T_tau needs (Eq. (2)): the sum,
-// the max and the smallest index attaining it (indices < L only), written
-// component-major as ps/pm/pi[c * ntile + tile].
-// Wave w computes components 16 w .. 16 w + 15 of both 16-index halves:
-// lane l, register r <-> component 16 w + l/16 + 4 r, index 16 h + l%16.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void tile_stats(const v4d (&x)[2], int w, int64_t i0, int64_t L, int ntile, int tile,
-                                           double* __restrict__ ps, double* __restrict__ pm, int* __restrict__ pi) {
-  const int lane = lane_id();
-  const int li = lane & 15, lk = lane >> 4;
-  const int64_t ia = i0 + li, ib = i0 + 16 + li;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const double a0 = ia < L ? fabs(x[0][r]) : 0.0, a1 = ib < L ? fabs(x[1][r]) : 0.0;
-    double s = a0 + a1;
-    // invalid indices never win the max
-    double mv = ia < L ? a0 : -1.0;
-    long long mi = ia;
-    argmax_merge(mv, mi, ib < L ? a1 : -1.0, ib);
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) {
-      s += __shfl_xor(s, o, 16);
-      const double mv2 = __shfl_xor(mv, o, 16);
-      const long long mi2 = __shfl_xor(mi, o, 16);
-      argmax_merge(mv, mi, mv2, mi2);
-    }
-    if (li == 0) {
-      const int c = 16 * w + lk + 4 * r;
-      ps[(int64_t)c * ntile + tile] = s;
-      pm[(int64_t)c * ntile + tile] = mv;
-      pi[(int64_t)c * ntile + tile] = (int)mi;
-    }
-  }
-}
-
-// V-step target Y = G_U^{-1} P (Eq. (3)); P summed over the gv row groups
-// (int64, exact) and scaled back by 2^-s.  grid: n_pad/32 column tiles.
-__global__ __launch_bounds__(NT) void k_vepi(const long long* __restrict__ Pp, int gv,
-                                             const double* __restrict__ ginv, double* __restrict__ Y,
-                                             const unsigned* __restrict__ maxbits, int64_t n, int64_t n_pad,
-                                             double* __restrict__ ps, double* __restrict__ pm, int* __restrict__ pi) {
-  __shared__ double Ps[64 * 33];
-  const int ct = blockIdx.x;
-  const int64_t j0 = (int64_t)ct * TILE;
-  const int s = fx_shift(*maxbits);
-  // every partial of every group is loaded in one round (gv <= GV_MAX,
-  // compile-time trip counts; groups past gv re-read group 0, weight 0)
-  long long acc[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) acc[q] = 0;
-#pragma unroll
-  for (int g = 0; g < GV_MAX; ++g) {
-    const int gg = g < gv ? g : 0;
-    const long long keep = g < gv;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = threadIdx.x + q * NT, c = e >> 5, jj = e & 31;
-      acc[q] += keep * Pp[((int64_t)gg * BBP + c) * n_pad + j0 + jj];
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int e = threadIdx.x + q * NT;
-    Ps[(e >> 5) * 33 + (e & 31)] = ldexp((double)acc[q], -s);
-  }
-  const int lane = lane_id(), w = wave_id();
-  const int li = lane & 15, lk = lane >> 4;
-  // A = G^{-1}[16 w + li][4 ks + lk] (register, L2), B = P[4 ks + lk][16 h + li] (LDS)
-  double a[16];
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) a[ks] = ginv[(16 * w + li) * 64 + 4 * ks + lk];
-  __syncthreads();
-  v4d y[2] = {v4d{}, v4d{}};
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) {
-    y[0] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + li], y[0]);
-    y[1] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + 16 + li], y[1]);
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    double* row = Y + (int64_t)(16 * w + lk + 4 * r) * n_pad + j0;
-    row[li] = y[0][r];
-    row[16 + li] = y[1][r];
-  }
-  tile_stats(y, w, j0, n, (int)gridDim.x, ct, ps, pm, pi);
-}
-
-// U-step target Z = Q G_V^{-1} (Eq. (3)), computed as Z^T = G_V^{-T} Q^T so
-// that rows of Z^T (component-major) are written coalesced.
-// grid: m_pad/32 row tiles.
-__global__ __launch_bounds__(NT) void k_uepi(const double* __restrict__ Q, const double* __restrict__ ginv,
-                                             double* __restrict__ Z, int64_t m, int64_t m_pad,
-                                             double* __restrict__ ps, double* __restrict__ pm, int* __restrict__ pi) {
-  const int rt = blockIdx.x;
-  const int64_t i0 = (int64_t)rt * TILE;
-  const int lane = lane_id(), w = wave_id();
-  const int li = lane & 15, lk = lane >> 4;
-  // A = G^{-1}[4 ks + lk][16 w + li] (transposed read), B = Q[4 ks + lk][i0 + 16 h + li]
-  double a[16], b0[16], b1[16];
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) {
-    a[ks] = ginv[(4 * ks + lk) * 64 + 16 * w + li];
-    const double* qrow = Q + (int64_t)(4 * ks + lk) * m_pad + i0;
-    b0[ks] = qrow[li];
-    b1[ks] = qrow[16 + li];
-  }
-  v4d z[2] = {v4d{}, v4d{}};
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) {
-    z[0] = mfma_f64(a[ks], b0[ks], z[0]);
-    z[1] = mfma_f64(a[ks], b1[ks], z[1]);
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    double* row = Z + (int64_t)(16 * w + lk + 4 * r) * m_pad + i0;
-    row[li] = z[0][r];
-    row[16 + li] = z[1][r];
-  }
-  tile_stats(z, w, i0, m, (int)gridDim.x, rt, ps, pm, pi);
+  wait_ready(ready, flags);
+  utarget_tile(tq, ginvV, Z, m, m_pad, rt, (int)(m_pad / TILE), ps, pm, pi);
 }
 
 // ---------------------------------------------------------------------------
@@ -965,8 +1120,10 @@ __device__ __forceinline__ double tern_from_stats(const double* __restrict__ x, 
 __global__ __launch_bounds__(NT_TERN) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb,
                                                     double tau, const double* __restrict__ ps,
                                                     const double* __restrict__ pm, const int* __restrict__ pi,
-                                                    int8_t* __restrict__ Vt, int8_t* __restrict__ Vmf) {
+                                                    int8_t* __restrict__ Vt, int8_t* __restrict__ Vmf,
+                                                    unsigned* ready_clear) {
   const int c = blockIdx.x;
+  if (c == 0 && threadIdx.x == 0) *ready_clear = 0u;
   const int ntile = (int)(n_pad / TILE);
   int8_t* dst = Vt + (int64_t)c * n_pad;
   if (c >= bb) {
@@ -974,10 +1131,10 @@ __global__ __launch_bounds__(NT_TERN) void k_tern_v(const double* __restrict__ Y
       dst[j] = 0;
       Vmf[mf_offset(c, j)] = 0;
     }
-    return;
+  } else {
+    const int64_t o = (int64_t)c * ntile;
+    tern_from_stats(Y + (int64_t)c * n_pad, nullptr, n, n_pad, ntile, ps + o, pm + o, pi + o, tau, dst, Vmf, c);
   }
-  const int64_t o = (int64_t)c * ntile;
-  tern_from_stats(Y + (int64_t)c * n_pad, nullptr, n, n_pad, ntile, ps + o, pm + o, pi + o, tau, dst, Vmf, c);
 }
 
 // U <- T_tau(Z[:, c]); also g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for
@@ -986,8 +1143,10 @@ __global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z
                                                     int64_t m, int64_t m_pad, int bb, double tau,
                                                     const double* __restrict__ ps, const double* __restrict__ pm,
                                                     const int* __restrict__ pi, int8_t* __restrict__ Ut,
-                                                    int8_t* __restrict__ Umf, double* __restrict__ gvec) {
+                                                    int8_t* __restrict__ Umf, double* __restrict__ gvec,
+                                                    unsigned* ready_clear) {
   const int c = blockIdx.x;
+  if (c == 0 && threadIdx.x == 0) *ready_clear = 0u;
   const int ntile = (int)(m_pad / TILE);
   int8_t* dst = Ut + (int64_t)c * m_pad;
   if (c >= bb) {
@@ -996,12 +1155,12 @@ __global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z
       Umf[mf_offset(c, i)] = 0;
     }
     if (threadIdx.x == 0) gvec[c] = 0.0;
-    return;
+  } else {
+    const int64_t o = (int64_t)c * ntile;
+    const double g = tern_from_stats(Z + (int64_t)c * m_pad, Q + (int64_t)c * m_pad, m, m_pad, ntile, ps + o, pm + o,
+                                     pi + o, tau, dst, Umf, c);
+    if (threadIdx.x == 0) gvec[c] = g;
   }
-  const int64_t o = (int64_t)c * ntile;
-  const double g = tern_from_stats(Z + (int64_t)c * m_pad, Q + (int64_t)c * m_pad, m, m_pad, ntile, ps + o, pm + o,
-                                   pi + o, tau, dst, Umf, c);
-  if (threadIdx.x == 0) gvec[c] = g;
 }
 
 // ---------------------------------------------------------------------------
@@ -1093,6 +1252,7 @@ __device__ __forceinline__ double ternarize_wg(Load load, const double* __restri
 
 // Block initialisation (paper silent; reading: U[:, c] = T_tau(R[:, J_c])).
 // grid: BBP.
+// grid: BBP.
 __global__ __launch_bounds__(NT_TERN) void k_init(const float* __restrict__ R, const int* __restrict__ J, int64_t m,
                                              int64_t m_pad, int64_t n_pad, int bb, double tau,
                                              int8_t* __restrict__ Ut, int8_t* __restrict__ Umf) {
@@ -1103,12 +1263,12 @@ __global__ __launch_bounds__(NT_TERN) void k_init(const float* __restrict__ R, c
       dst[i] = 0;
       Umf[mf_offset(c, i)] = 0;
     }
-    return;
+  } else {
+    int jc = J[c];
+    jc = jc < 0 ? 0 : (jc >= n_pad ? (int)(n_pad - 1) : jc);  // J comes from k_select; keep reads in bounds
+    const float* col = R + jc;
+    ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, nullptr, m, m_pad, tau, dst, Umf, c);
   }
-  int jc = J[c];
-  jc = jc < 0 ? 0 : (jc >= n_pad ? (int)(n_pad - 1) : jc);  // J comes from k_select; keep reads in bounds
-  const float* col = R + jc;
-  ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, nullptr, m, m_pad, tau, dst, Umf, c);
 }
 
 // Xt (BBP x L int8, component-major) -> Xr (L x BBP, row-major) and, when
@@ -1133,17 +1293,16 @@ __global__ __launch_bounds__(NT) void k_transpose8(const int8_t* __restrict__ Xt
 
 // ---------------------------------------------------------------------------
 // Joint scale solve, Eq. (4): M = (U^T U) o (V^T H V) (+ delta I),
-// d = M^{-1} g.  grid: NSIDE_INT (partial U^T U on int8 MFMA, last WG solves).
+// d = M^{-1} g.  grid: one WG; U^T U is the accumulated Gram of the block's
+// final U.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) void k_scale(const v4i* __restrict__ Umf, int64_t m_pad, int bb,
+__global__ __launch_bounds__(NT) void k_scale(int* gacc, int bb,
                                               const double* __restrict__ gramV, const double* __restrict__ gvec,
-                                              int* gparti, unsigned* counter, double* dvec, float* dF,
-                                              float* Dout) {
-  __shared__ int red[4096];
+                                              double* dvec, float* dF, float* Dout) {
   __shared__ double Gs[4096];
   __shared__ double colbuf[1024];
   __shared__ double s_trb[16];
-  if (!side_gram_int(Umf, m_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red)) return;
+  take_gram(gacc, Gs);
   const int t = threadIdx.x;
   for (int e = t; e < 4096; e += NT) {
     const int r = e >> 6, c = e & 63;
@@ -1366,7 +1525,7 @@ __global__ __launch_bounds__(NT) void k_unstage(const float* __restrict__ R, flo
 __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_t n, int64_t n_pad,
                                              double* __restrict__ hw, unsigned* maxbits, unsigned* maxbits_w,
                                              double* fro2_hist, double* fro2w_hist, int nblk_cap,
-                                             unsigned* counters, int* flags) {
+                                             unsigned* counters, int* flags, unsigned* tilecnt, int* gacc) {
   __shared__ float smax[NT / 64];
   __shared__ int sbad[NT / 64];
   for (int e = threadIdx.x; e < nblk_cap; e += NT) {
@@ -1376,6 +1535,8 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
     fro2w_hist[e] = 0.0;
   }
   if (threadIdx.x < CNT_COUNT) counters[threadIdx.x] = 0u;
+  for (int64_t e = threadIdx.x; e < n_pad / TILE; e += NT) tilecnt[e] = 0u;
+  for (int e = threadIdx.x; e < 2 * 4096; e += NT) gacc[e] = 0;
   if (threadIdx.x < FLAG_COUNT) flags[threadIdx.x] = 0;
   if (!h) {
     for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? 1.0 : 0.0;
@@ -1695,6 +1856,15 @@ __global__ __launch_bounds__(NT) void k_gram_v(const v4i* __restrict__ Vmf, cons
   ridge_invert_store(Gs, colbuf, bb, ginvV);
 }
 
+// Integer Gram of a factor given by the caller (step entry points): adds
+// X^T X into gacc.  grid: NSIDE_GRAM WGs over the K steps.
+__global__ __launch_bounds__(NT) void k_gram_acc(const v4i* __restrict__ Xmf, int64_t L_pad, int* gacc) {
+  __shared__ int red[4 * 4096];
+  const int nks = (int)(L_pad / TILE);
+  gram_accumulate(Xmf, (int)((long long)blockIdx.x * nks / gridDim.x), (int)((long long)(blockIdx.x + 1) * nks / gridDim.x),
+                  gacc, red);
+}
+
 // g_c = sum_i U_ic Q_ic (fp64).  grid: BBP.
 __global__ __launch_bounds__(NT) void k_gvec(const int8_t* __restrict__ Ut, const double* __restrict__ Q, int64_t m,
                                              int64_t m_pad, int bb, double* __restrict__ gvec) {
@@ -1729,7 +1899,7 @@ static inline unsigned grid_for(int64_t total) {
 
 hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s) {
   hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.maxbits, w.maxbits_w, w.fro2_hist,
-                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags);
+                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.tilecnt, w.gacc);
   return hipGetLastError();
 }
 
@@ -1765,28 +1935,29 @@ hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2,
 
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
   hipLaunchKernelGGL(k_init, dim3(BBP), dim3(NT_TERN), 0, s, w.R, w.J, w.m, w.m_pad, w.n_pad, bb, tau, w.Ut, w.Umf);
-  return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_gram_acc(w, 0, s);
 }
 
-hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
-  const unsigned grid = (unsigned)(NSIDE_INT + (w.n_pad / TILE) * w.gv);
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* tm) {
+  const unsigned grid = (unsigned)(1 + (w.n_pad / TILE) * w.gv);
   EXTERND_TIMED(tm, EXTERND_KCLASS_VSTEP,
                 hipLaunchKernelGGL(k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, w.maxbits + blk, w.m_pad,
-                                   w.n_pad, w.gv, bb, w.gparti, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_INT));
+                                   w.n_pad, w.gv, bb, w.gacc, w.ginvU, 1, w.Y, w.n,
+                                   w.tps, w.tpm, w.tpi, w.tilecnt, w.counters + CNT_READY_U, w.flags));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_vepi, dim3((unsigned)(w.n_pad / TILE)), dim3(NT), 0, s, w.Pp, w.gv, w.ginvU, w.Y,
-                     w.maxbits + blk, w.n, w.n_pad, w.tps, w.tpm, w.tpi);
+  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi, w.Vt,
+                     w.Vmf, w.counters + CNT_READY_U);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi, w.Vt,
-                     w.Vmf);
-  return hipGetLastError();
+  return weighted ? hipSuccess : launch_gram_acc(w, 1, s);
 }
 
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* tm) {
   hipError_t e;
-  const unsigned nside = weighted ? NSIDE_W : NSIDE_INT;
+  const unsigned nside = weighted ? NSIDE_W : 1;
   const unsigned grid = (unsigned)(nside + w.m_pad / TILE);
   if (weighted) {
     hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad,
@@ -1795,28 +1966,29 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
     if (e != hipSuccess) return e;
     EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
                   hipLaunchKernelGGL(k_ustep<true>, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
-                                     w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gparti, w.gpart,
-                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside));
+                                     w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
+                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside,
+                                     w.Z, w.m, w.tps,
+                                     w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags));
   } else {
     EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
                   hipLaunchKernelGGL(k_ustep<false>, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
-                                     w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gparti, w.gpart,
-                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside));
+                                     w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
+                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside,
+                                     w.Z, w.m, w.tps,
+                                     w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags));
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_uepi, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0, s, w.Q, w.ginvV, w.Z, w.m, w.m_pad, w.tps,
-                     w.tpm, w.tpi);
+  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.tps, w.tpm, w.tpi,
+                     w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.tps, w.tpm, w.tpi,
-                     w.Ut, w.Umf, w.gvec);
-  return hipGetLastError();
+  return launch_gram_acc(w, 0, s);
 }
 
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
-  hipLaunchKernelGGL(k_scale, dim3(NSIDE_INT), dim3(NT), 0, s, (const v4i*)w.Umf, w.m_pad, bb, w.gramV, w.gvec, w.gparti,
-                     w.counters + CNT_SCALE, w.dvec, w.dF, (float*)nullptr);
+  hipLaunchKernelGGL(k_scale, dim3(1), dim3(NT), 0, s, w.gacc, bb, w.gramV, w.gvec, w.dvec, w.dF, (float*)nullptr);
   return hipGetLastError();
 }
 
@@ -1875,6 +2047,12 @@ hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s) {
                        w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
   return hipGetLastError();
 }
+hipError_t launch_gram_acc(const Ws& w, int which, hipStream_t s) {
+  const v4i* X = (const v4i*)(which ? w.Vmf : w.Umf);
+  hipLaunchKernelGGL(k_gram_acc, dim3(NSIDE_GRAM), dim3(NT), 0, s, X, which ? w.n_pad : w.m_pad, w.gacc + 4096 * which);
+  return hipGetLastError();
+}
+
 hipError_t launch_gvec(const Ws& w, int bb, hipStream_t s) {
   hipLaunchKernelGGL(k_gvec, dim3(BBP), dim3(NT), 0, s, w.Ut, w.Q, w.m, w.m_pad, bb, w.gvec);
   return hipGetLastError();
