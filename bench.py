@@ -109,6 +109,61 @@ def calibrate_copy(nbytes: int, reps: int):
     print(json.dumps({"copy_bytes": nbytes, "reps": reps}))
 
 
+def collect_traffic(dbs, copy_bytes: int):
+    """Per-launch HBM bytes of the timed kernel classes from rocprofv3 --pmc
+    databases (FETCH_SIZE run, WRITE_SIZE run, and the same two counters on
+    a plain device copy of copy_bytes), each counter scaled by copy-bytes /
+    the counter's reading for the copy.  Writes profiles/traffic_counters.json
+    and a short markdown summary beside it."""
+    import re
+    import sqlite3
+
+    def per_kernel(path, counter):
+        con = sqlite3.connect(path)
+        rows = con.execute("select kernel_name, count(*), avg(value) from counters_collection "
+                           "where counter_name=? group by kernel_name", (counter,)).fetchall()
+        return {re.sub(r"\(.*", "", k).replace("void ", "").replace("externd::", ""): (int(c), float(a) * 1024.0)
+                for k, c, a in rows}
+
+    fetch, write = per_kernel(dbs[0], "FETCH_SIZE"), per_kernel(dbs[1], "WRITE_SIZE")
+    cfetch, cwrite = per_kernel(dbs[2], "FETCH_SIZE"), per_kernel(dbs[3], "WRITE_SIZE")
+    copy_f = max(v[1] for k, v in cfetch.items() if "copyBuffer" in k)
+    copy_w = max(v[1] for k, v in cwrite.items() if "copyBuffer" in k)
+    ff, fw = copy_bytes / copy_f, copy_bytes / copy_w
+    classes = {"vstep_contraction": "k_vstep", "ustep_contraction": "k_ustep<false>", "deflate": "k_deflate"}
+    out = {"kernel_source_sha256": kernel_source_hash(), "copy_bytes": copy_bytes,
+           "fetch_scale": ff, "write_scale": fw, "kernels": {}}
+    lines = ["# HBM traffic per launch (rocprofv3 --pmc), 9728x2560 workload", "",
+             "Commands (repository root, one MI355X):", "", "```",
+             "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o pmc -- python bench.py --steps 1 --warmup 0 --cpu-blocks 0",
+             "rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o pmc -- python bench.py --steps 1 --warmup 0 --cpu-blocks 0",
+             f"rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_copy_fetch -o pmc -- python bench.py --calibrate-copy {copy_bytes}",
+             f"rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_copy_write -o pmc -- python bench.py --calibrate-copy {copy_bytes}",
+             "python bench.py --collect-traffic gpurun_out/pmc_fetch/pmc_results.db gpurun_out/pmc_write/pmc_results.db "
+             f"gpurun_out/pmc_copy_fetch/pmc_results.db gpurun_out/pmc_copy_write/pmc_results.db --copy-bytes {copy_bytes}",
+             "```", "",
+             f"Copy calibration: a {copy_bytes} B device copy reads FETCH_SIZE = {copy_f:.0f} B and WRITE_SIZE = "
+             f"{copy_w:.0f} B, so fetch counts are scaled by {ff:.4f} and write counts by {fw:.4f}.", "",
+             "| kernel | launches | fetch MB/launch | write MB/launch | algorithmic MB/launch |", "|---|---:|---:|---:|---:|"]
+    m, n = 9728, 2560
+    for cls, kname in classes.items():
+        if kname not in fetch:
+            continue
+        fb, wb = fetch[kname][1] * ff, write.get(kname, (0, 0.0))[1] * fw
+        out["kernels"][cls] = {"kernel": kname, "launches": fetch[kname][0], "fetch_bytes": fb, "write_bytes": wb}
+        lines.append(f"| {kname} | {fetch[kname][0]} | {fb / 1e6:.1f} | {wb / 1e6:.1f} | "
+                     f"{algorithmic_bytes(cls, m, n) / 1e6:.1f} |")
+    lines += ["", "All kernels (unscaled counter averages, MiB per launch):", "",
+              "| kernel | launches | FETCH_SIZE | WRITE_SIZE |", "|---|---:|---:|---:|"]
+    for k in sorted(fetch, key=lambda k: -fetch[k][0] * fetch[k][1]):
+        lines.append(f"| {k} | {fetch[k][0]} | {fetch[k][1] / 2**20:.2f} | {write.get(k, (0, 0.0))[1] / 2**20:.2f} |")
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    with open(os.path.join(ROOT, "profiles", "traffic_down9728x2560.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,7 +172,13 @@ def main():
     ap.add_argument("--workload", default="down9728")
     ap.add_argument("--cpu-blocks", type=int, default=40, help="oracle sample size in blocks (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0, help="run only a copy of this many bytes")
+    ap.add_argument("--collect-traffic", nargs=4, metavar="DB",
+                    help="rocprofv3 --pmc databases: FETCH_SIZE, WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE")
+    ap.add_argument("--copy-bytes", type=int, default=268435456)
     args = ap.parse_args()
+    if args.collect_traffic:
+        collect_traffic(args.collect_traffic, args.copy_bytes)
+        return
 
     if args.gpus != 1:
         print(json.dumps({"error": f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "

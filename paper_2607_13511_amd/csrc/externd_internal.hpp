@@ -2,6 +2,7 @@
 // Not part of the public ABI (see include/externd.h).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <stddef.h>
@@ -82,17 +83,24 @@ struct Timer {
   struct Mark { hipEvent_t a, b; int cls; };
   Mark* marks = nullptr;
   int n = 0, cap = 0;
-  hipError_t begin(int cls);
-  hipError_t end();
+  // The event pair of the next timed launch (created on first use).
+  hipError_t take(int cls, hipEvent_t* a, hipEvent_t* b);
   hipError_t collect(double* total_ms, int64_t* launches, int ncls);
   ~Timer();
 };
-// Record an event pair around `launch` when `t` is non-null.
-#define EXTERND_TIMED(t, cls, launch)                      \
-  do {                                                     \
-    if (t) { hipError_t _e = (t)->begin(cls); if (_e != hipSuccess) return _e; } \
-    launch;                                                \
-    if (t) { hipError_t _e = (t)->end(); if (_e != hipSuccess) return _e; } \
+// Launch `kernel`; when `t` is non-null the launch carries start/stop
+// events that the runtime stamps at the kernel's own start and end
+// (hipExtLaunchKernelGGL), so the measured time excludes dispatch gaps.
+#define EXTERND_LAUNCH_TIMED(t, cls, kernel, grid, block, shm, s, ...)          \
+  do {                                                                        \
+    if (t) {                                                                  \
+      hipEvent_t _a, _b;                                                      \
+      hipError_t _e = (t)->take(cls, &_a, &_b);                               \
+      if (_e != hipSuccess) return _e;                                        \
+      hipExtLaunchKernelGGL(kernel, grid, block, shm, s, _a, _b, 0, __VA_ARGS__); \
+    } else {                                                                  \
+      hipLaunchKernelGGL(kernel, grid, block, shm, s, __VA_ARGS__);           \
+    }                                                                         \
   } while (0)
 
 size_t workspace_bytes(int64_t m, int64_t n, int64_t k);

@@ -1942,10 +1942,9 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
 
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* tm) {
   const unsigned grid = (unsigned)(1 + (w.n_pad / TILE) * w.gv);
-  EXTERND_TIMED(tm, EXTERND_KCLASS_VSTEP,
-                hipLaunchKernelGGL(k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, w.maxbits + blk, w.m_pad,
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, w.maxbits + blk, w.m_pad,
                                    w.n_pad, w.gv, bb, w.gacc, w.ginvU, 1, w.Y, w.n,
-                                   w.tps, w.tpm, w.tpi, w.tilecnt, w.counters + CNT_READY_U, w.flags));
+                                   w.tps, w.tpm, w.tpi, w.tilecnt, w.counters + CNT_READY_U, w.flags);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi, w.Vt,
@@ -1964,19 +1963,17 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
                        (unsigned short*)nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
-                  hipLaunchKernelGGL(k_ustep<true>, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside,
                                      w.Z, w.m, w.tps,
-                                     w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags));
+                                     w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags);
   } else {
-    EXTERND_TIMED(tm, EXTERND_KCLASS_USTEP,
-                  hipLaunchKernelGGL(k_ustep<false>, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside,
                                      w.Z, w.m, w.tps,
-                                     w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags));
+                                     w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -2001,9 +1998,8 @@ hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s, Timer* tm) {
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
-  EXTERND_TIMED(tm, EXTERND_KCLASS_DEFLATE,
-                hipLaunchKernelGGL(k_deflate, dim3(grid), dim3(NT), 0, s, w.R, (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part,
-                                   w.maxbits + blk + 1, w.maxbits_w + blk + 1, w.hw, w.m_pad, w.n_pad, w.gd));
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_DEFLATE, k_deflate, dim3(grid), dim3(NT), 0, s, w.R, (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part,
+                                   w.maxbits + blk + 1, w.maxbits_w + blk + 1, w.hw, w.m_pad, w.n_pad, w.gd);
   return hipGetLastError();
 }
 
