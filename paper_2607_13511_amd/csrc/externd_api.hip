@@ -280,9 +280,8 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
       HIP_TRY(launch_vstep(w, (int)blk, bb, tau, weighted, s, tm));
       HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, s, tm));
     }
-    HIP_TRY(launch_scale(w, bb, s));
-    HIP_TRY(launch_deflate(w, (int)blk, s, tm));
-    HIP_TRY(launch_emit(w, c0, bb, k, B_packed, C_packed, D, s));
+    HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s));
+    HIP_TRY(launch_deflate(w, (int)blk, false, s, tm));
   }
   HIP_TRY(launch_finish(w, (int)nblk, s));
 
@@ -423,7 +422,7 @@ int externd_step_deflate(float* R, int64_t m, int64_t n, const int8_t* U, const 
   HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
   HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
   HIP_TRY(launch_set_scales(w, d, bb, s));
-  HIP_TRY(launch_deflate(w, 0, s));
+  HIP_TRY(launch_deflate(w, 0, true, s));
   HIP_TRY(launch_unstage(w, R, s));
   if (colnorm2_out || fro2_out) HIP_TRY(launch_colnorms(w, 0, colnorm2_out, fro2_out, s));
   return EXTERND_OK;

@@ -118,9 +118,11 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, bool weighted,
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s,
                         Timer* t = nullptr);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
-hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s, Timer* t = nullptr);
-hipError_t launch_emit(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp,
-                       float* D, hipStream_t s);
+// The end of a block: scale solve, row-major factor copies, packed B and C, D.
+hipError_t launch_block_out(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
+                            hipStream_t s);
+// transposes: rebuild the row-major factor copies from Ut/Vt first (step entry point).
+hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, Timer* t = nullptr);
 // step-entry helpers
 hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len, int64_t len_pad,
                               int bb, hipStream_t s);

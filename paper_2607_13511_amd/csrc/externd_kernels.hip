@@ -1157,117 +1157,61 @@ __global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z
     if (threadIdx.x == 0) gvec[c] = 0.0;
   } else {
     const int64_t o = (int64_t)c * ntile;
-    const double g = tern_from_stats(Z + (int64_t)c * m_pad, Q + (int64_t)c * m_pad, m, m_pad, ntile, ps + o, pm + o,
-                                     pi + o, tau, dst, Umf, c);
+    const double* qrow = Q ? Q + (int64_t)c * m_pad : nullptr;  // no Q: initialisation, g unused
+    const double g = tern_from_stats(Z + (int64_t)c * m_pad, qrow, m, m_pad, ntile, ps + o, pm + o, pi + o, tau, dst,
+                                     Umf, c);
     if (threadIdx.x == 0) gvec[c] = g;
   }
 }
 
-// ---------------------------------------------------------------------------
-// T_tau of one component per workgroup (Eq. (2)): theta = tau * mean|x|
-// over the true length L (fp64), strict ">", keep the largest |x| (smallest
-// index) when nothing passes.  Writes the trits of component c
-// component-major (dst[0 .. L_pad)) and into the MFMA-ready layout mf,
-// zero beyond L.  The first TERN_CACHE * blockDim values
-// are loaded once and kept in registers for the threshold pass.  With an
-// auxiliary vector q (may be null) it also returns sum_i t_i q_i (fp64).
-// ---------------------------------------------------------------------------
-constexpr int TERN_CACHE = 12;
-
-template <typename Load>
-__device__ __forceinline__ double ternarize_wg(Load load, const double* __restrict__ q, int64_t L, int64_t L_pad, double tau,
-                               int8_t* dst, int8_t* mf, int c) {
-  __shared__ double shd[16];
-  __shared__ long long shl[16];
-  __shared__ int shi[16];
-  const int64_t st = blockDim.x;
-  const int64_t tid = threadIdx.x;
-  double xc[TERN_CACHE], qc[TERN_CACHE];
-#pragma unroll
-  for (int cc = 0; cc < TERN_CACHE; ++cc) {
-    const int64_t i = tid + cc * st;
-    xc[cc] = (i < L) ? load(i) : 0.0;
-    qc[cc] = (q && i < L) ? q[i] : 0.0;
-  }
-  double sabs = 0.0, mx = -1.0;
-  long long imx = 0;
-#pragma unroll
-  for (int cc = 0; cc < TERN_CACHE; ++cc) {
-    const int64_t i = tid + cc * st;
-    if (i < L) {
-      const double a = fabs(xc[cc]);
-      sabs += a;
-      argmax_merge(mx, imx, a, i);
-    }
-  }
-  for (int64_t i = tid + TERN_CACHE * st; i < L; i += st) {
-    const double a = fabs(load(i));
-    sabs += a;
-    argmax_merge(mx, imx, a, i);
-  }
-  const double S = block_sum_d(sabs, shd);
-  block_argmax(mx, imx, shd, shl);
-  const double theta = tau * (S / (double)L);
-  int nnz = 0;
-  double g = 0.0;
-#pragma unroll
-  for (int cc = 0; cc < TERN_CACHE; ++cc) {
-    const int64_t i = tid + cc * st;
-    if (i < L_pad) {
-      int8_t t = 0;
-      if (i < L && fabs(xc[cc]) > theta) t = (xc[cc] > 0.0) ? 1 : -1;
-      nnz += (t != 0);
-      g += (double)t * qc[cc];
-      dst[i] = t;
-      mf[mf_offset(c, i)] = t;
-    }
-  }
-  for (int64_t i = tid + TERN_CACHE * st; i < L_pad; i += st) {
-    int8_t t = 0;
-    if (i < L) {
-      const double x = load(i);
-      if (fabs(x) > theta) t = (x > 0.0) ? 1 : -1;
-      if (q) g += (double)t * q[i];
-    }
-    nnz += (t != 0);
-    dst[i] = t;
-    mf[mf_offset(c, i)] = t;
-  }
-  nnz = block_sum_i(nnz, shi);
-  if (nnz == 0 && L > 0) {
-    // keep-largest fallback: only the argmax entry is nonzero
-    if (tid == 0) {
-      const double x = load(imx);
-      const int8_t t = (x > 0.0) ? 1 : ((x < 0.0) ? -1 : 0);
-      dst[imx] = t;
-      mf[mf_offset(c, imx)] = t;
-      g = q ? (double)t * q[imx] : 0.0;
-    } else {
-      g = 0.0;
-    }
-  }
-  g = block_sum_d(g, shd);
-  return g;
-}
-
 // Block initialisation (paper silent; reading: U[:, c] = T_tau(R[:, J_c])).
-// grid: BBP.
-// grid: BBP.
-__global__ __launch_bounds__(NT_TERN) void k_init(const float* __restrict__ R, const int* __restrict__ J, int64_t m,
-                                             int64_t m_pad, int64_t n_pad, int bb, double tau,
-                                             int8_t* __restrict__ Ut, int8_t* __restrict__ Umf) {
-  const int c = blockIdx.x;
-  int8_t* dst = Ut + (int64_t)c * m_pad;
-  if (c >= bb) {
-    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) {
-      dst[i] = 0;
-      Umf[mf_offset(c, i)] = 0;
+// Gathers the bb selected residual columns into X (component-major fp64,
+// 64 x m_pad; zero for c >= bb) with the per-32-row-tile statistics of
+// |x| that T_tau needs; k_tern_u then thresholds them like a U target.
+// grid: m_pad/32 row tiles; thread (c = tid % 64, g = tid / 64) takes rows
+// 8 g .. 8 g + 7 of the tile for component c.
+__global__ __launch_bounds__(NT) void k_init_gather(const float* __restrict__ R, const int* __restrict__ J, int64_t m,
+                                                    int64_t m_pad, int64_t n_pad, int bb, double* __restrict__ X,
+                                                    double* __restrict__ ps, double* __restrict__ pm,
+                                                    int* __restrict__ pi) {
+  __shared__ double s_sum[4][BBP], s_max[4][BBP];
+  __shared__ int s_idx[4][BBP];
+  const int rt = blockIdx.x, ntile = (int)gridDim.x;
+  const int c = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int64_t i0 = (int64_t)rt * TILE + 8 * g;
+  int jc = c < bb ? J[c] : 0;
+  jc = jc < 0 ? 0 : (jc >= n_pad ? (int)(n_pad - 1) : jc);  // J comes from k_select; keep reads in bounds
+  double v[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int64_t i = i0 + r;
+    v[r] = (c < bb && i < m) ? (double)R[i * n_pad + jc] : 0.0;
+  }
+  double s = 0.0, mv = -1.0;
+  long long mi = i0;
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    X[(int64_t)c * m_pad + i0 + r] = v[r];
+    if (i0 + r < m) {
+      s += fabs(v[r]);
+      argmax_merge(mv, mi, fabs(v[r]), i0 + r);
     }
-  } else {
-    int jc = J[c];
-    jc = jc < 0 ? 0 : (jc >= n_pad ? (int)(n_pad - 1) : jc);  // J comes from k_select; keep reads in bounds
-    const float* col = R + jc;
-    ternarize_wg([=](int64_t i) { return (double)col[i * n_pad]; }, nullptr, m, m_pad, tau, dst, Umf, c);
+  }
+  s_sum[g][c] = s;
+  s_max[g][c] = mv;
+  s_idx[g][c] = (int)mi;
+  __syncthreads();
+  if (g == 0) {
+    double S = s_sum[0][c], M = s_max[0][c];
+    long long I = s_idx[0][c];
+#pragma unroll
+    for (int q = 1; q < 4; ++q) {
+      S += s_sum[q][c];
+      argmax_merge(M, I, s_max[q][c], s_idx[q][c]);
+    }
+    ps[(int64_t)c * ntile + rt] = S;
+    pm[(int64_t)c * ntile + rt] = M;
+    pi[(int64_t)c * ntile + rt] = (int)I;
   }
 }
 
@@ -1296,11 +1240,9 @@ __global__ __launch_bounds__(NT) void k_transpose8(const int8_t* __restrict__ Xt
 // d = M^{-1} g.  grid: one WG; U^T U is the accumulated Gram of the block's
 // final U.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) void k_scale(int* gacc, int bb,
-                                              const double* __restrict__ gramV, const double* __restrict__ gvec,
-                                              double* dvec, float* dF, float* Dout) {
-  __shared__ double Gs[4096];
-  __shared__ double colbuf[1024];
+__device__ __forceinline__ void scale_solve(int* gacc, int bb, const double* __restrict__ gramV,
+                                            const double* __restrict__ gvec, double* dvec, float* dF, float* Dout,
+                                            double* Gs /* LDS 4096 */, double* colbuf /* LDS 1024 */) {
   __shared__ double s_trb[16];
   take_gram(gacc, Gs);
   const int t = threadIdx.x;
@@ -1330,6 +1272,13 @@ __global__ __launch_bounds__(NT) void k_scale(int* gacc, int bb,
     dF[t] = (float)d;
     if (Dout && t < bb) Dout[t] = (float)d;
   }
+}
+
+__global__ __launch_bounds__(NT) void k_scale(int* gacc, int bb, const double* __restrict__ gramV,
+                                              const double* __restrict__ gvec, double* dvec, float* dF, float* Dout) {
+  __shared__ double Gs[4096];
+  __shared__ double colbuf[1024];
+  scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf);
 }
 
 // ---------------------------------------------------------------------------
@@ -1601,6 +1550,8 @@ __device__ __forceinline__ void reduce_colE(const double* __restrict__ colE_part
   }
 }
 
+constexpr int SELECT_CACHE = 8;  // keys per thread kept in registers (n <= SELECT_CACHE * NT_SELECT without memory passes)
+
 __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__ colE_part, int gd, int64_t n,
                                                       int64_t n_pad, const double* __restrict__ hw,
                                                       double* keys /* n_pad scratch */, double* fro2_out,
@@ -1619,8 +1570,17 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
   }
   reduce_colE(colE_part, gd, n, n_pad, hw, keys, fro2_out, fro2w_out, shd);
   __syncthreads();
-  for (int64_t j = threadIdx.x; j < n; j += blockDim.x) keys[j] = hw[j] * keys[j];
-  __syncthreads();
+  // key_j = h~_j ||R_:j||^2 as a 64-bit pattern (non-negative doubles order
+  // like their bit patterns); the first SELECT_CACHE keys of each thread
+  // stay in registers, the rest (large n only) are re-read from `keys`
+  const int64_t st = blockDim.x;
+  unsigned long long kc[SELECT_CACHE];
+#pragma unroll
+  for (int q = 0; q < SELECT_CACHE; ++q) {
+    const int64_t j = threadIdx.x + q * st;
+    kc[q] = j < n ? (unsigned long long)__double_as_longlong(hw[j] * keys[j]) : 0ull;
+  }
+  for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) keys[j] = hw[j] * keys[j];
   // radix select over the 64-bit patterns, 8 bits at a time from the top
   if (threadIdx.x == 0) {
     s_prefix = 0ull;
@@ -1633,7 +1593,12 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
     __syncthreads();
     const unsigned long long prefix = s_prefix;
     const unsigned long long hmask = (pass == 0) ? 0ull : (~0ull << (shift + 8));
-    for (int64_t j = threadIdx.x; j < n; j += blockDim.x) {
+#pragma unroll
+    for (int q = 0; q < SELECT_CACHE; ++q) {
+      const int64_t j = threadIdx.x + q * st;
+      if (j < n && (kc[q] & hmask) == prefix) atomicAdd(&hist[(kc[q] >> shift) & 0xff], 1u);
+    }
+    for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) {
       const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
       if ((kb & hmask) == prefix) atomicAdd(&hist[(kb >> shift) & 0xff], 1u);
     }
@@ -1684,7 +1649,18 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
   const int need_eq = s_need;
   if (threadIdx.x == 0) s_cnt = 0;
   __syncthreads();
-  for (int64_t j = threadIdx.x; j < n; j += blockDim.x) {
+#pragma unroll
+  for (int q = 0; q < SELECT_CACHE; ++q) {
+    const int64_t j = threadIdx.x + q * st;
+    if (j < n && kc[q] > T) {
+      const int slot = atomicAdd(&s_cnt, 1);
+      if (slot < BBP) {
+        cand_key[slot] = kc[q];
+        cand_idx[slot] = (int)j;
+      }
+    }
+  }
+  for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) {
     const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
     if (kb > T) {
       const int slot = atomicAdd(&s_cnt, 1);
@@ -1695,13 +1671,15 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
     }
   }
   __syncthreads();
+  // keys equal to T, in index order: block-wide exclusive scans over
+  // consecutive rounds of blockDim indices (the round count and the stop
+  // condition are uniform across the block)
   int carry = 0;
   const int base = s_cnt;
-  for (int64_t j0 = 0; j0 < n; j0 += blockDim.x) {
-    const int64_t j = j0 + threadIdx.x;
-    int f = 0;
-    if (j < n) f = ((unsigned long long)__double_as_longlong(keys[j]) == T);
-    // exclusive scan of f over the block, in index order
+  const int rounds = (int)((n + st - 1) / st);
+  bool done = false;
+  auto scan_round = [&](int64_t j, unsigned long long kb) {
+    const int f = (j < n && kb == T) ? 1 : 0;
     int v = f;
     const int lane = lane_id();
     for (int o = 1; o < 64; o <<= 1) {
@@ -1722,6 +1700,14 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
     }
     carry += tot;
     __syncthreads();
+    done = carry >= need_eq;
+  };
+#pragma unroll
+  for (int q = 0; q < SELECT_CACHE; ++q)
+    if (!done && q < rounds) scan_round(threadIdx.x + q * st, kc[q]);
+  for (int q = SELECT_CACHE; !done && q < rounds; ++q) {
+    const int64_t j = threadIdx.x + q * st;
+    scan_round(j, j < n ? (unsigned long long)__double_as_longlong(keys[j]) : 0ull);
   }
   __syncthreads();
   // order the bb winners by (key desc, index asc)
@@ -1752,43 +1738,81 @@ __global__ __launch_bounds__(NT_SELECT) void k_finish(const double* __restrict__
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ unsigned trit_code(int8_t t) { return t == 0 ? 0u : (t > 0 ? 1u : 3u); }
 
-// B rows: byte range covering columns [c0, c0 + bb) of B (read-modify-write
-// of shared bytes; padding bits beyond k cleared).
-__global__ __launch_bounds__(NT) void k_emit_b(const int8_t* __restrict__ Ur, int64_t m, int64_t c0, int bb,
-                                               int64_t k, uint8_t* __restrict__ Bp) {
-  const int64_t pitch = (k + 3) >> 2;
-  const int64_t q0 = c0 >> 2, q1 = (c0 + bb - 1) >> 2;
-  const int64_t nq = q1 - q0 + 1;
-  const int64_t total = m * nq;
-  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
-    const int64_t i = e / nq, q = q0 + e % nq;
-    uint8_t* dst = Bp + i * pitch + q;
-    unsigned byte = *dst;
-    for (int s = 0; s < 4; ++s) {
-      const int64_t p = 4 * q + s;
-      if (p >= k) byte &= ~(3u << (2 * s));
-      else if (p >= c0 && p < c0 + bb) {
-        byte &= ~(3u << (2 * s));
-        byte |= trit_code(Ur[i * BBP + (p - c0)]) << (2 * s);
-      }
-    }
-    *dst = (uint8_t)byte;
+// ---------------------------------------------------------------------------
+// End of a block, one launch: the joint scale solve (Eq. (4)) in WG 0,
+// writing d to the output D; then 32-index tiles of U and V: their
+// row-major copies for the deflation (U also as bf16) and the block's trits
+// packed into the rows of B and C (Eq. (1); 2-bit codes, element j at byte
+// j>>2, bits 2(j&3); B bytes shared with neighbouring blocks are
+// read-modified-written, padding bits beyond k cleared).
+// grid: 1 + m_pad/32 (U tiles) + n_pad/32 (V tiles).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const double* __restrict__ gramV,
+                                                  const double* __restrict__ gvec, double* dvec, float* dF,
+                                                  float* Dout, const int8_t* __restrict__ Ut, int8_t* __restrict__ Ur,
+                                                  unsigned short* __restrict__ Ub, int64_t m, int64_t m_pad,
+                                                  int64_t c0, int64_t k, uint8_t* __restrict__ Bp,
+                                                  const int8_t* __restrict__ Vt, int8_t* __restrict__ Vr, int64_t n,
+                                                  int64_t n_pad, uint8_t* __restrict__ Cp) {
+  __shared__ double Gs[4096];
+  __shared__ double colbuf[1024];
+  if (blockIdx.x == 0) {
+    scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf);
+    return;
   }
-}
-
-// C rows c0 .. c0 + bb - 1 from Vt.
-__global__ __launch_bounds__(NT) void k_emit_c(const int8_t* __restrict__ Vt, int64_t n, int64_t n_pad,
-                                               int64_t c0, int bb, uint8_t* __restrict__ Cp) {
-  const int64_t pitch = (n + 3) >> 2;
-  const int64_t total = (int64_t)bb * pitch;
-  for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
-    const int64_t c = e / pitch, q = e % pitch;
-    unsigned byte = 0;
-    for (int s = 0; s < 4; ++s) {
-      const int64_t j = 4 * q + s;
-      if (j < n) byte |= trit_code(Vt[c * n_pad + j]) << (2 * s);
+  int8_t (*tile)[BBP + 4] = (int8_t (*)[BBP + 4])Gs;  // 32 x 68 bytes
+  const int nut = (int)(m_pad / TILE);
+  const bool isU = (int)blockIdx.x <= nut;
+  const int64_t L = isU ? m_pad : n_pad;
+  const int8_t* Xt = isU ? Ut : Vt;
+  const int64_t j0 = (int64_t)(isU ? blockIdx.x - 1 : blockIdx.x - 1 - nut) * 32;
+  for (int e = threadIdx.x; e < BBP * 32; e += NT) {
+    const int c = e >> 5, jj = e & 31;
+    tile[jj][c] = Xt[(int64_t)c * L + j0 + jj];
+  }
+  __syncthreads();
+  int8_t* Xr = isU ? Ur : Vr;
+  for (int e = threadIdx.x; e < BBP * 32; e += NT) {
+    const int jj = e >> 6, c = e & 63;
+    const int8_t t = tile[jj][c];
+    Xr[(j0 + jj) * BBP + c] = t;
+    if (isU) Ub[(j0 + jj) * BBP + c] = t == 0 ? 0 : (t > 0 ? 0x3F80u : 0xBF80u);
+  }
+  if (isU) {
+    // rows j0 .. j0+31 of B, byte range covering columns [c0, c0 + bb)
+    const int64_t pitch = (k + 3) >> 2;
+    const int64_t q0 = c0 >> 2, q1 = (c0 + bb - 1) >> 2;
+    const int nq = (int)(q1 - q0 + 1);
+    for (int e = threadIdx.x; e < 32 * nq; e += NT) {
+      const int jj = e / nq;
+      const int64_t i = j0 + jj, q = q0 + e % nq;
+      if (i >= m) continue;
+      uint8_t* dst = Bp + i * pitch + q;
+      unsigned byte = *dst;
+      for (int s = 0; s < 4; ++s) {
+        const int64_t p = 4 * q + s;
+        if (p >= k) byte &= ~(3u << (2 * s));
+        else if (p >= c0 && p < c0 + bb) {
+          byte &= ~(3u << (2 * s));
+          byte |= trit_code(tile[jj][p - c0]) << (2 * s);
+        }
+      }
+      *dst = (uint8_t)byte;
     }
-    Cp[(c0 + c) * pitch + q] = (uint8_t)byte;
+  } else {
+    // columns j0 .. j0+31 of C rows c0 .. c0+bb-1: 8 whole bytes per row
+    const int64_t pitch = (n + 3) >> 2;
+    for (int e = threadIdx.x; e < bb * 8; e += NT) {
+      const int c = e >> 3, qq = e & 7;
+      const int64_t q = (j0 >> 2) + qq;
+      if (q >= pitch) continue;
+      unsigned byte = 0;
+      for (int s = 0; s < 4; ++s) {
+        const int64_t j = 4 * q + s;
+        if (j < n) byte |= trit_code(tile[4 * qq + s][c]) << (2 * s);
+      }
+      Cp[(c0 + c) * pitch + q] = (uint8_t)byte;
+    }
   }
 }
 
@@ -1934,8 +1958,13 @@ hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2,
 }
 
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
-  hipLaunchKernelGGL(k_init, dim3(BBP), dim3(NT_TERN), 0, s, w.R, w.J, w.m, w.m_pad, w.n_pad, bb, tau, w.Ut, w.Umf);
-  const hipError_t e = hipGetLastError();
+  hipLaunchKernelGGL(k_init_gather, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0, s, w.R, w.J, w.m, w.m_pad, w.n_pad,
+                     bb, w.Z, w.tps, w.tpm, w.tpi);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, (const double*)nullptr, w.m, w.m_pad, bb, tau,
+                     w.tps, w.tpm, w.tpi, w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_gram_acc(w, 0, s);
 }
@@ -1989,31 +2018,29 @@ hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_deflate(const Ws& w, int blk, hipStream_t s, Timer* tm) {
-  hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.m_pad / 32)), dim3(NT), 0, s, w.Ut, w.Ur, w.m_pad, w.Ub);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad,
-                     (unsigned short*)nullptr);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
+hipError_t launch_block_out(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
+                           hipStream_t s) {
+  const unsigned grid = (unsigned)(1 + w.m_pad / TILE + w.n_pad / TILE);
+  hipLaunchKernelGGL(k_block_out, dim3(grid), dim3(NT), 0, s, w.gacc, bb, w.gramV, w.gvec, w.dvec, w.dF, D + c0,
+                     w.Ut, w.Ur, w.Ub, w.m, w.m_pad, c0, k, Bp, w.Vt, w.Vr, w.n, w.n_pad, Cp);
+  return hipGetLastError();
+}
+
+hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, Timer* tm) {
+  hipError_t e;
+  if (transposes) {
+    hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.m_pad / 32)), dim3(NT), 0, s, w.Ut, w.Ur, w.m_pad, w.Ub);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad,
+                       (unsigned short*)nullptr);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_DEFLATE, k_deflate, dim3(grid), dim3(NT), 0, s, w.R, (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part,
                                    w.maxbits + blk + 1, w.maxbits_w + blk + 1, w.hw, w.m_pad, w.n_pad, w.gd);
   return hipGetLastError();
-}
-
-hipError_t launch_emit(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
-                       hipStream_t s) {
-  const int64_t nq = ((c0 + bb - 1) >> 2) - (c0 >> 2) + 1;
-  hipLaunchKernelGGL(k_emit_b, dim3(grid_for(w.m * nq)), dim3(NT), 0, s, w.Ur, w.m, c0, bb, k, Bp);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_emit_c, dim3(grid_for((int64_t)bb * ((w.n + 3) >> 2))), dim3(NT), 0, s, w.Vt, w.n, w.n_pad,
-                     c0, bb, Cp);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return hipMemcpyAsync(D + c0, w.dF, sizeof(float) * bb, hipMemcpyDeviceToDevice, s);
 }
 
 hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len, int64_t len_pad,
