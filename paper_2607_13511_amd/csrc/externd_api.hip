@@ -22,6 +22,7 @@ static inline int clampi(int64_t v, int64_t lo, int64_t hi) { return (int)(v < l
 struct Layout {
   int64_t m_pad, n_pad;
   int gv, gd, nblk_cap;
+  int urows, ntu;
   size_t off[40];
   size_t total;
 };
@@ -35,8 +36,14 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   // staging: about 640.
   L.gv = clampi((480 + nct - 1) / nct, 1, nrt < GV_MAX ? nrt : GV_MAX);
   L.gd = clampi((640 + nct - 1) / nct, 1, nrt < 64 ? nrt : 64);
+  // U-step: equal row groups of at most 32 rows, as many as fit beside the
+  // side workgroups in one pass of USTEP_SLOTS resident workgroups, so
+  // that every CU streams the same share of R.
+  L.urows = clampi((L.m_pad + (USTEP_SLOTS - NSIDE_MAX) - 1) / (USTEP_SLOTS - NSIDE_MAX), 1, TILE);
+  L.ntu = (int)((L.m_pad + L.urows - 1) / L.urows);
   L.nblk_cap = (int)(k + 2);  // fro2 before every block and after the last; one spare
-  const int64_t ntmax = nrt > nct ? nrt : nct;  // 32-index tiles of the longer side
+  int64_t ntmax = nrt > nct ? nrt : nct;  // statistics tiles: 32-index tiles of either side,
+  if (L.ntu > ntmax) ntmax = L.ntu;       // or the U-step's row groups
   const size_t sizes[] = {
       sizeof(float) * (size_t)(L.m_pad * L.n_pad),     // 0 R
       (size_t)(BBP * L.m_pad),                         // 1 Ut
@@ -95,6 +102,8 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.nblk_cap = L.nblk_cap;
   w.gv = L.gv;
   w.gd = L.gd;
+  w.urows = L.urows;
+  w.ntu = L.ntu;
   w.R = (float*)(b + L.off[0]);
   w.Ut = (int8_t*)(b + L.off[1]);
   w.Ur = (int8_t*)(b + L.off[2]);

@@ -20,6 +20,9 @@ constexpr int NSIDE_GRAM = 16; // workgroups of the integer Gram launch
 constexpr int NSIDE_W = 16;
 constexpr int NSIDE_MAX = 16;
 constexpr int GV_MAX = 8;      // row groups of the V-step contraction
+// Workgroups of the contraction kernels resident at once: two per CU on
+// 256 CUs (LDS and register budgets of k_vstep / k_ustep).
+constexpr int USTEP_SLOTS = 512;
 // Threads per workgroup for all kernels except the selection kernel.
 constexpr int NT = 256;
 constexpr int NT_SELECT = 1024;
@@ -38,6 +41,7 @@ struct Ws {
   int nblk_cap;          // capacity of the per-block arrays (k + 2)
   int gv;                // row groups of the V-step contraction
   int gd;                // row groups of the deflation / staging passes
+  int urows, ntu;        // U-step: rows per workgroup (<= 32) and number of row groups
 
   float* R;              // m_pad x n_pad residual, fp32, row-major
   int8_t* Ut;            // BBP x m_pad, U transposed (component-major)

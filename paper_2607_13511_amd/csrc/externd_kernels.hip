@@ -272,10 +272,21 @@ __device__ __forceinline__ v4d mfma_f64(double a, double b, v4d c) {
   return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
 }
 
+// 1 / x for the pivots of the sweep below: the hardware estimate refined by
+// two Newton steps r <- r (2 - x r) (error ~ 1 ulp).  The sweep works on a
+// matrix scaled to a unit-order diagonal, so x is far from the denormal and
+// overflow ranges that the full IEEE division sequence guards against.
+__device__ __forceinline__ double recip_nr(double x) {
+  double r = __builtin_amdgcn_rcp(x);
+  r = r * fma(-x, r, 2.0);
+  r = r * fma(-x, r, 2.0);
+  return r;
+}
+
 // Inverse of the symmetric 4x4 block [[A, B], [B^T, D]] (2x2 blocks) by the
 // Schur complement S = D - B^T A^{-1} B; uses the upper triangle of P.
 __device__ __forceinline__ void spd_inverse4(const double (&P)[4][4], double (&Pi)[4][4]) {
-  const double ra = 1.0 / (P[0][0] * P[1][1] - P[0][1] * P[0][1]);
+  const double ra = recip_nr(P[0][0] * P[1][1] - P[0][1] * P[0][1]);
   const double a00 = P[1][1] * ra, a01 = -P[0][1] * ra, a11 = P[0][0] * ra;
   // X = A^{-1} B
   const double x00 = a00 * P[0][2] + a01 * P[1][2], x01 = a00 * P[0][3] + a01 * P[1][3];
@@ -284,7 +295,7 @@ __device__ __forceinline__ void spd_inverse4(const double (&P)[4][4], double (&P
   const double s00 = P[2][2] - (P[0][2] * x00 + P[1][2] * x10);
   const double s01 = P[2][3] - (P[0][2] * x01 + P[1][2] * x11);
   const double s11 = P[3][3] - (P[0][3] * x01 + P[1][3] * x11);
-  const double rs = 1.0 / (s00 * s11 - s01 * s01);
+  const double rs = recip_nr(s00 * s11 - s01 * s01);
   const double t00 = s11 * rs, t01 = -s01 * rs, t11 = s00 * rs;
   // Y = X S^{-1}
   const double y00 = x00 * t00 + x01 * t01, y01 = x00 * t01 + x01 * t11;
@@ -299,6 +310,30 @@ __device__ __forceinline__ void spd_inverse4(const double (&P)[4][4], double (&P
   Pi[2][1] = -y10; Pi[3][1] = -y11;
   Pi[2][2] = t00; Pi[2][3] = t01;
   Pi[3][2] = t01; Pi[3][3] = t11;
+}
+
+template <typename T>
+__device__ __forceinline__ T load_coherent(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ void store_coherent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// A 64 x 64 inverse shared between workgroups is stored in the operand
+// order of the fp64 MFMA (A operand, 16x16x4): wave w, K step ks and lane
+// (li = lane % 16, lk = lane / 16) read element [16 w + li][4 ks + lk] at
+// (16 w + ks) * 64 + lane, so each load instruction of a wave reads 512
+// contiguous bytes.  The inverses are symmetric, so the same array serves
+// the transposed operand (Z^T = G^{-1} Q^T).
+__device__ __forceinline__ int ginv_index(int row, int col) {
+  return (((row >> 4) * 16 + (col >> 2)) << 6) + (col & 3) * 16 + (row & 15);
+}
+__device__ __forceinline__ void load_ginv(const double* ginv, double (&a)[16]) {
+  const double* p = ginv + wave_id() * 1024 + lane_id();
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(p + ks * 64);
 }
 
 __device__ __forceinline__ void spd_inverse64(double* A, double* pbuf, double* out = nullptr) {
@@ -325,14 +360,19 @@ __device__ __forceinline__ void spd_inverse64(double* A, double* pbuf, double* o
     for (int r = 0; r < 4; ++r)
       acc[nt][r] = ldexp(A[(16 * w + lr + 4 * r) * 64 + 16 * nt + lc], -(er[r] + ec[nt]));
   const double m0 = lr == 0, m1 = lr == 1, m2 = lr == 2, m3 = lr == 3;
+  // The loop over the owner waves stays rolled: the sweep runs once per
+  // launch, and its code is fetched cold while the streaming workgroups
+  // load the memory system, so a 4x smaller body is faster.
+#pragma unroll 1
+  for (int ntK = 0; ntK < 4; ++ntK)
 #pragma unroll
-  for (int K = 0; K < 16; ++K) {
+  for (int rK = 0; rK < 4; ++rK) {
+    const int K = 4 * ntK + rK;
     // The sweep keeps A symmetric, so the pivot column block equals the
     // pivot rows: their owner (wave K / 4, register K % 4) publishes
     // C^T[c][j] = A[4K + c][j] - delta(j, 4K + c) and every wave builds
     // its own operands from it.  Double-buffered: one barrier per step.
-    double* Rb = pbuf + (K & 1) * 256;
-    const int ntK = K >> 2, rK = K & 3;
+    double* Rb = pbuf + (rK & 1) * 256;
     if (w == ntK) {
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
@@ -363,16 +403,28 @@ __device__ __forceinline__ void spd_inverse64(double* A, double* pbuf, double* o
     const double aop = -(wc[0] * m0 + wc[1] * m1 + wc[2] * m2 + wc[3] * m3);
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma_f64(aop, bop[nt], acc[nt]);
-    // the pivot block's diagonal
-    if (w == ntK && lc == 4 * rK + lr) acc[ntK][rK] -= 2.0;
   }
-  // the inverse goes to out (global) when given, else back to A
-  double* dst = out ? out : A;
+  // Each step also takes 2 off its pivot block's diagonal.  A pivot row is
+  // published only in its own step and no later step reads the diagonal
+  // entry, so all these corrections are applied here at once (the
+  // accumulators stay in the MFMA registers during the sweep).
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      dst[(16 * w + lr + 4 * r) * 64 + 16 * nt + lc] = -ldexp(acc[nt][r], -(er[r] + ec[nt]));
+      if (16 * w + lr + 4 * r == 16 * nt + lc) acc[nt][r] -= 2.0;
+  // the inverse goes back to A (LDS, row-major), or to out (global, in the
+  // fp64 MFMA operand order of ginv_index, written through for consumers
+  // in other workgroups of the same launch)
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 16 * w + lr + 4 * r, col = 16 * nt + lc;
+      const double v = -ldexp(acc[nt][r], -(er[r] + ec[nt]));
+      if (out) store_coherent(out + ginv_index(row, col), v);
+      else A[row * 64 + col] = v;
+    }
   __syncthreads();
 }
 
@@ -396,7 +448,7 @@ __device__ __forceinline__ void ridge_invert_store(double* G, double* colbuf, in
   if (s_tr == 0.0) {
     for (int e = t; e < 4096; e += blockDim.x) {
       const int r = e >> 6, c = e & 63;
-      ginv_out[e] = (r >= bb || c >= bb) ? ((r == c) ? 1.0 : 0.0) : 0.0;
+      store_coherent(ginv_out + ginv_index(r, c), (r >= bb || c >= bb) ? ((r == c) ? 1.0 : 0.0) : 0.0);
     }
     return;
   }
@@ -416,26 +468,16 @@ __device__ __forceinline__ void ridge_invert_store(double* G, double* colbuf, in
 // fence: with one L2 per XCD an acquire fence in hundreds of workgroups
 // would discard the L2 contents the streaming workgroups rely on.
 // ---------------------------------------------------------------------------
-template <typename T>
-__device__ __forceinline__ T load_coherent(const T* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-template <typename T>
-__device__ __forceinline__ void store_coherent(T* p, T v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 constexpr unsigned SPIN_LIMIT = 1u << 24;
 
-// The barrier completes every wave's stores into the XCD's L2; one
-// device-scope release (L2 write-back) by the signalling thread then
-// covers them all.
+// Everything the waiting workgroups read (G^{-1}) is written with
+// device-coherent (write-through) stores, so no L2 write-back is needed:
+// each wave waits for its own stores to complete, and after the barrier
+// one thread raises the flag.
 __device__ __forceinline__ void signal_ready(unsigned* ready) {
   __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have completed
   __syncthreads();
-  if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    __hip_atomic_store(ready, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  if (threadIdx.x == 0) __hip_atomic_store(ready, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void wait_ready(unsigned* ready, int* flags) {
@@ -747,41 +789,51 @@ __device__ __forceinline__ void tile_stats(const v4d (&x)[2], int w, int64_t i0,
 // vtarget_sum: P summed over the gv row-group partials (int64, exact) and
 // scaled back by 2^-s into Ps (LDS, 64 x 33 doubles); vtarget_apply: the
 // product with G_U^{-1}, the stores and the T_tau statistics.
-__device__ __forceinline__ void vtarget_sum(const long long* __restrict__ Pp, int gv, int s, int64_t n_pad, int ct,
-                                            double* Ps) {
+template <int GV>
+__device__ __forceinline__ void vtarget_sum_g(const long long* __restrict__ Pp, int s, int64_t n_pad, int ct,
+                                              double* Ps) {
   const int64_t j0 = (int64_t)ct * TILE;
-  // every partial of every group is loaded in one round (gv <= GV_MAX,
-  // compile-time trip counts; groups past gv re-read group 0, weight 0)
-  long long acc[8];
+  // every partial of every group is loaded in one round (straight-line
+  // loads, then the sums)
+  long long v[GV][8];
 #pragma unroll
-  for (int q = 0; q < 8; ++q) acc[q] = 0;
-#pragma unroll
-  for (int g = 0; g < GV_MAX; ++g) {
-    const int gg = g < gv ? g : 0;
-    const long long keep = g < gv;
+  for (int g = 0; g < GV; ++g)
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       const int e = threadIdx.x + q * NT, c = e >> 5, jj = e & 31;
-      acc[q] += keep * load_coherent(Pp + ((int64_t)gg * BBP + c) * n_pad + j0 + jj);
+      v[g][q] = load_coherent(Pp + ((int64_t)g * BBP + c) * n_pad + j0 + jj);
     }
-  }
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
+    long long acc = 0;
+#pragma unroll
+    for (int g = 0; g < GV; ++g) acc += v[g][q];
     const int e = threadIdx.x + q * NT;
-    Ps[(e >> 5) * 33 + (e & 31)] = ldexp((double)acc[q], -s);
+    Ps[(e >> 5) * 33 + (e & 31)] = ldexp((double)acc, -s);
+  }
+  __syncthreads();
+}
+__device__ __forceinline__ void vtarget_sum(const long long* __restrict__ Pp, int gv, int s, int64_t n_pad, int ct,
+                                            double* Ps) {
+  static_assert(GV_MAX == 8, "one case per group count");
+  switch (gv) {
+    case 1: vtarget_sum_g<1>(Pp, s, n_pad, ct, Ps); break;
+    case 2: vtarget_sum_g<2>(Pp, s, n_pad, ct, Ps); break;
+    case 3: vtarget_sum_g<3>(Pp, s, n_pad, ct, Ps); break;
+    case 4: vtarget_sum_g<4>(Pp, s, n_pad, ct, Ps); break;
+    case 5: vtarget_sum_g<5>(Pp, s, n_pad, ct, Ps); break;
+    case 6: vtarget_sum_g<6>(Pp, s, n_pad, ct, Ps); break;
+    case 7: vtarget_sum_g<7>(Pp, s, n_pad, ct, Ps); break;
+    default: vtarget_sum_g<8>(Pp, s, n_pad, ct, Ps); break;
   }
 }
-__device__ __forceinline__ void vtarget_apply(const double* __restrict__ ginv, double* __restrict__ Y, int64_t n,
+__device__ __forceinline__ void vtarget_apply(const double (&a)[16], double* __restrict__ Y, int64_t n,
                                               int64_t n_pad, int ct, int ntile, double* ps, double* pm, int* pi,
                                               const double* Ps) {
   const int64_t j0 = (int64_t)ct * TILE;
   const int lane = lane_id(), w = wave_id();
   const int li = lane & 15, lk = lane >> 4;
-  // A = G^{-1}[16 w + li][4 ks + lk], B = P[4 ks + lk][16 h + li] (LDS)
-  double a[16];
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(ginv + (16 * w + li) * 64 + 4 * ks + lk);
-  __syncthreads();
+  // A = G^{-1}[16 w + li][4 ks + lk] (a, from load_ginv), B = P[4 ks + lk][16 h + li] (LDS)
   v4d y[2] = {v4d{}, v4d{}};
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
@@ -797,18 +849,15 @@ __device__ __forceinline__ void vtarget_apply(const double* __restrict__ ginv, d
   tile_stats(y, w, j0, n, ntile, ct, ps, pm, pi);
 }
 
-// U-step target tile Z[i0 .. i0+32, :] = Q G_V^{-1} (Eq. (3)), computed as
-// Z^T = G_V^{-T} Q^T so that rows of Z^T (component-major) are written
-// coalesced.  Qs: LDS tile Q^T, Qs[c * 32 + i].
-__device__ __forceinline__ void utarget_tile(const double* Qs, const double* __restrict__ ginv, double* __restrict__ Z,
-                                             int64_t m, int64_t m_pad, int rt, int ntile, double* ps, double* pm,
-                                             int* pi) {
-  const int64_t i0 = (int64_t)rt * TILE;
+// U-step target tile Z[i0 .. i0+rows, :] = Q G_V^{-1} (Eq. (3)), rows <= 32,
+// computed as Z^T = G_V^{-1} Q^T (G_V^{-1} symmetric) so that rows of Z^T
+// (component-major) are written coalesced.  Qs: LDS tile Q^T,
+// Qs[c * 32 + r] (entries r >= rows are ignored).  a: G_V^{-1} from load_ginv.
+__device__ __forceinline__ void utarget_tile(const double* Qs, const double (&a)[16], double* __restrict__ Z,
+                                             int64_t m, int64_t m_pad, int64_t i0, int rows, int tile, int ntile,
+                                             double* ps, double* pm, int* pi) {
   const int lane = lane_id(), w = wave_id();
   const int li = lane & 15, lk = lane >> 4;
-  double a[16];
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(ginv + (4 * ks + lk) * 64 + 16 * w + li);
   v4d z[2] = {v4d{}, v4d{}};
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
@@ -818,10 +867,11 @@ __device__ __forceinline__ void utarget_tile(const double* Qs, const double* __r
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     double* row = Z + (int64_t)(16 * w + lk + 4 * r) * m_pad + i0;
-    row[li] = z[0][r];
-    row[16 + li] = z[1][r];
+    if (li < rows) row[li] = z[0][r];
+    if (16 + li < rows) row[16 + li] = z[1][r];
   }
-  tile_stats(z, w, i0, m, ntile, rt, ps, pm, pi);
+  const int64_t lim = i0 + rows < m ? i0 + rows : m;
+  tile_stats(z, w, i0, lim, ntile, tile, ps, pm, pi);
 }
 
 // ---------------------------------------------------------------------------
@@ -918,9 +968,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   __syncthreads();
   if (!s_last) return;
   if (threadIdx.x == 0) store_coherent(tilecnt + ct, 0u);  // every group has arrived: ready for the next launch
-  vtarget_sum(Pp, gv, s, n_pad, ct, (double*)smem);
+  // G^{-1} (stored long before) and the partials are loaded in one round
   wait_ready(ready, flags);
-  vtarget_apply(ginvU, Y, n, n_pad, ct, nct, ps, pm, pi, (double*)smem);
+  double a[16];
+  load_ginv(ginvU, a);
+  vtarget_sum(Pp, gv, s, n_pad, ct, (double*)smem);
+  vtarget_apply(a, Y, n, n_pad, ct, nct, ps, pm, pi, (double*)smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -928,10 +981,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // Sec. 2.5)
 // grid: side WGs (the accumulated V Gram, or, weighted, NSIDE_W WGs
 //       building V^T H V; ridge, inverse; the raw Gram is kept for the scale
-//       solve) followed by m_pad/32 row tiles; each row tile
-//       stores Q, waits for G_V^{-1} and writes its Z tile and T_tau
-//       statistics.
-// Each WG owns 32 full rows; its 4 waves interleave 32-column K steps.
+//       solve) followed by ntile row groups of `rows` <= 32 rows, sized so
+//       that the whole grid is resident at two workgroups per CU and every
+//       CU streams the same share of R; each row group stores Q, waits for
+//       G_V^{-1} and writes its Z rows and T_tau statistics.
+// Each WG owns `rows` full rows (one 32-row MFMA tile; rows past `rows`
+// are neither loaded nor stored); its 4 waves interleave 32-column K steps.
 // A = R digit planes (rows x columns), B = V (MFMA-ready layout).  Each
 // wave streams its 32 x 32 residual tiles into LDS with direct loads
 // (8 lanes per 128-byte row segment, 16-byte chunks XOR-swizzled by row)
@@ -948,8 +1003,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                               double* __restrict__ Q, const unsigned* __restrict__ maxbits,
                                               int64_t m_pad, int64_t n_pad, int bb, int* gacc, double* gpart,
                                               unsigned* counter, double* ginvV, double* gramV, int nside,
-                                              double* __restrict__ Z, int64_t m, double* ps, double* pm, int* pi,
-                                              unsigned* ready, int* flags) {
+                                              double* __restrict__ Z, int64_t m, int rows, int ntile, double* ps,
+                                              double* pm, int* pi, unsigned* ready, int* flags) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[8192];
@@ -970,6 +1025,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     return;
   }
   const int rt = blockIdx.x - nside;
+  const int64_t i0 = (int64_t)rt * rows;
+  const int valid = (int)(m_pad - i0 < rows ? m_pad - i0 : rows);  // >= 1: ntile = ceil(m_pad / rows)
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
   const int s = fx_shift(*maxbits);
@@ -981,18 +1038,23 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const int nks = (int)(n_pad / TILE);
   char* wst = (char*)smem + wave * (NST_U * USTAGE_B);
   // loader mapping: lane -> row 8 q + lane / 8, 16-byte chunk lane % 8,
-  // stored at chunk position (lane % 8) ^ (row % 8)
+  // stored at chunk position (lane % 8) ^ (row % 8); rows >= valid are
+  // not loaded (their staging rows hold stale values; the MFMA output rows
+  // they feed are discarded).  Row 0 is always valid, so every stage
+  // issues at least one direct load and the vmcnt bounds of the operand
+  // reads (which count one stage's loads plus the two factor loads) hold.
   const int lrow = lane >> 3;
-  const float* Rld = R + ((int64_t)rt * TILE + lrow) * n_pad + (((lane & 7) ^ lrow) * 4);
+  const float* Rld = R + (i0 + lrow) * n_pad + (((lane & 7) ^ lrow) * 4);
   constexpr int NLD = WEIGHTED ? 5 : 4;  // direct loads per staged K step
   v4i bn[NST_U][2];
+  // stage st <- K step kk (< nks); nothing is loaded past the last K step
   auto issue = [&](int kk, int st) {
-    kk = kk < nks ? kk : nks - 1;
     char* dst = wst + st * USTAGE_B;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      __builtin_amdgcn_global_load_lds(Rld + (int64_t)8 * q * n_pad + (int64_t)kk * TILE, (lds_void*)(dst + q * 1024),
-                                       16, 0, 0);
+      if (8 * q + lrow < valid)
+        __builtin_amdgcn_global_load_lds(Rld + (int64_t)8 * q * n_pad + (int64_t)kk * TILE,
+                                         (lds_void*)(dst + q * 1024), 16, 0, 0);
     if (WEIGHTED)
       __builtin_amdgcn_global_load_lds((const float*)(hw + (int64_t)kk * TILE) + lane, (lds_void*)(dst + 4096), 4, 0,
                                        0);
@@ -1000,7 +1062,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     bn[st][1] = Vmf[(int64_t)kk * 128 + 64 + lane];
   };
 #pragma unroll
-  for (int d = 0; d < NST_U - 1; ++d) issue(wave + 4 * d, d);
+  for (int d = 0; d < NST_U - 1; ++d)
+    if (wave + 4 * d < nks) issue(wave + 4 * d, d);
   // operand read: row l32, logical chunks 4h .. 4h+3
   const unsigned sw = (unsigned)(l32 & 7);
   const unsigned o0 = l32 * 128 + ((4 * h + 0) ^ sw) * 16, o1 = l32 * 128 + ((4 * h + 1) ^ sw) * 16;
@@ -1009,12 +1072,15 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   for (int ks = wave; ks < nks; ks += 4 * NST_U) {
 #pragma unroll
     for (int u = 0; u < NST_U; ++u) {
-      const int kk = ks + 4 * u;
-      issue(kk + 4 * (NST_U - 1), (u + NST_U - 1) % NST_U);
+      const int kk = ks + 4 * u, kn = kk + 4 * (NST_U - 1);
+      if (kn < nks) issue(kn, (u + NST_U - 1) % NST_U);
       if (kk < nks) {
         const unsigned b = wbase + u * USTAGE_B;
         v4f x[4];
-        lds_read4_after<NLD * (NST_U - 1)>(b + o0, b + o1, b + o2, b + o3, x[0], x[1], x[2], x[3]);
+        // with the following stages issued, at least NLD * (NST_U - 1)
+        // loads follow this stage's; near the end the wait drains
+        if (kn < nks) lds_read4_after<NLD * (NST_U - 1)>(b + o0, b + o1, b + o2, b + o3, x[0], x[1], x[2], x[3]);
+        else lds_read4_after<0>(b + o0, b + o1, b + o2, b + o3, x[0], x[1], x[2], x[3]);
         unsigned y[16];
         if (WEIGHTED) {
           v2d wv[8];
@@ -1039,8 +1105,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
       }
     }
   }
-  // every direct load (including the clamped ones past the end) has landed
-  // before the staging area is reused
+  // every direct load has landed before the staging area is reused
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   // out[t][M = row][N = component] -> Q[32 t + N][row], via a transposed
@@ -1048,9 +1113,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   double* tq = (double*)smem;
   reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { tq[(32 * t + N) * 32 + M] = ldexp((double)v, -s); });
   __syncthreads();
-  for (int e = threadIdx.x; e < 2048; e += NT) Q[(int64_t)(e >> 5) * m_pad + (int64_t)rt * TILE + (e & 31)] = tq[e];
   wait_ready(ready, flags);
-  utarget_tile(tq, ginvV, Z, m, m_pad, rt, (int)(m_pad / TILE), ps, pm, pi);
+  double a[16];
+  load_ginv(ginvV, a);
+  for (int e = threadIdx.x; e < 2048; e += NT)
+    if ((e & 31) < valid) Q[(int64_t)(e >> 5) * m_pad + i0 + (e & 31)] = tq[e];
+  utarget_tile(tq, a, Z, m, m_pad, i0, valid, rt, ntile, ps, pm, pi);
 }
 
 // ---------------------------------------------------------------------------
@@ -1138,16 +1206,17 @@ __global__ __launch_bounds__(NT_TERN) void k_tern_v(const double* __restrict__ Y
 }
 
 // U <- T_tau(Z[:, c]); also g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for
-// the joint scale solve (Eq. (4)).  grid: BBP.
+// the joint scale solve (Eq. (4)).  ps/pm/pi: statistics of ntile row
+// groups (the U-step's groups, or 32-row tiles after the initial gather).
+// grid: BBP.
 __global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q,
                                                     int64_t m, int64_t m_pad, int bb, double tau,
                                                     const double* __restrict__ ps, const double* __restrict__ pm,
-                                                    const int* __restrict__ pi, int8_t* __restrict__ Ut,
+                                                    const int* __restrict__ pi, int ntile, int8_t* __restrict__ Ut,
                                                     int8_t* __restrict__ Umf, double* __restrict__ gvec,
                                                     unsigned* ready_clear) {
   const int c = blockIdx.x;
   if (c == 0 && threadIdx.x == 0) *ready_clear = 0u;
-  const int ntile = (int)(m_pad / TILE);
   int8_t* dst = Ut + (int64_t)c * m_pad;
   if (c >= bb) {
     for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) {
@@ -1963,7 +2032,7 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, (const double*)nullptr, w.m, w.m_pad, bb, tau,
-                     w.tps, w.tpm, w.tpi, w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
+                     w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_gram_acc(w, 0, s);
@@ -1986,7 +2055,7 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, bool weighted,
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* tm) {
   hipError_t e;
   const unsigned nside = weighted ? NSIDE_W : 1;
-  const unsigned grid = (unsigned)(nside + w.m_pad / TILE);
+  const unsigned grid = (unsigned)(nside + w.ntu);
   if (weighted) {
     hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad,
                        (unsigned short*)nullptr);
@@ -1995,19 +2064,19 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside,
-                                     w.Z, w.m, w.tps,
+                                     w.Z, w.m, w.urows, w.ntu, w.tps,
                                      w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags);
   } else {
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside,
-                                     w.Z, w.m, w.tps,
+                                     w.Z, w.m, w.urows, w.ntu, w.tps,
                                      w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.tps, w.tpm, w.tpi,
-                     w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
+                     w.ntu, w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_gram_acc(w, 0, s);
