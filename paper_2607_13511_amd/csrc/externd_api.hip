@@ -286,9 +286,10 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
     HIP_TRY(launch_select(w, (int)blk, bb, s));
     HIP_TRY(launch_init(w, bb, tau, s));
     for (int it = 0; it < iters; ++it) {
-      HIP_TRY(launch_vstep(w, (int)blk, bb, tau, weighted, s, tm));
+      HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm));
       HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, s, tm));
     }
+    HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
     HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s));
     HIP_TRY(launch_deflate(w, (int)blk, false, s, tm));
   }
@@ -369,8 +370,7 @@ int externd_step_vstep(const float* R, int64_t m, int64_t n, const int8_t* U, in
   HIP_TRY(launch_prep(w, nullptr, s));
   HIP_TRY(launch_stage(w, R, n, s));
   HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
-  HIP_TRY(launch_gram_acc(w, 0, s));
-  HIP_TRY(launch_vstep(w, 0, bb, tau, true, s));
+  HIP_TRY(launch_vstep(w, 0, bb, tau, s));
   HIP_TRY(launch_store_factor(V_out, w.Vt, n, w.n_pad, bb, s));
   if (Y_out_or_null) {
     // Y is bb x n: row c of the component-major buffer, pitch n_pad -> n
@@ -391,7 +391,6 @@ int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, in
   HIP_TRY(launch_prep(w, h, s));
   HIP_TRY(launch_stage(w, R, n, s));
   HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
-  if (!h) HIP_TRY(launch_gram_acc(w, 1, s));
   HIP_TRY(launch_ustep(w, 0, bb, tau, h != nullptr, s));
   HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
   if (Q_out_or_null) HIP_TRY(launch_store_cm(Q_out_or_null, w.Q, m, w.m_pad, bb, s));

@@ -116,9 +116,9 @@ hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s)
 hipError_t launch_select(const Ws& w, int blk, int bb, hipStream_t s);
 hipError_t launch_finish(const Ws& w, int blk, hipStream_t s);
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s);
-// weighted: the U-step builds V^T H V itself, so the V-step's ternarization
-// skips the integer V Gram.
-hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* t = nullptr);
+// The contraction launches build the Gram of their factor themselves (side
+// workgroups); launch_gram_acc serves the scale solve.
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr);
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s,
                         Timer* t = nullptr);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);

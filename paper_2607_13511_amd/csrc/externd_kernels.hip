@@ -646,6 +646,36 @@ __device__ __forceinline__ void gram_accumulate(const v4i* __restrict__ Xmf, int
   }
 }
 
+// Side workgroup `side` of `nside` adds its share of the K steps of X^T X
+// into gacc; the last to arrive (arrival counter, reset by it) takes the
+// accumulated Gram into G (LDS, fp64) with coherent loads, as the atomics
+// of the other side workgroups belong to the same launch, and clears gacc
+// for the next accumulation.  red: LDS, 4 x 4096 int32 (may alias G).
+__device__ __forceinline__ bool side_gram_acc(const v4i* __restrict__ Xmf, int64_t L_pad, int side, int nside,
+                                              int* gacc, unsigned* counter, double* G, int* red) {
+  const int nks = (int)(L_pad / TILE);
+  gram_accumulate(Xmf, (int)((long long)side * nks / nside), (int)((long long)(side + 1) * nks / nside), gacc, red);
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's atomics have been performed
+  __shared__ int s_last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (old == (unsigned)(nside - 1));
+  }
+  __syncthreads();
+  if (!s_last) return false;
+  if (threadIdx.x == 0) store_coherent(counter, 0u);
+  int v[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) v[j] = load_coherent(gacc + threadIdx.x + NT * j);
+#pragma unroll
+  for (int j = 0; j < 16; ++j) G[threadIdx.x + NT * j] = (double)v[j];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) gacc[threadIdx.x + NT * j] = 0;
+  __syncthreads();
+  return true;
+}
+
 // Consumer (a later launch than the producer, so plain accesses suffice):
 // the accumulated Gram into G (LDS, fp64); gacc is cleared for the next
 // accumulation.  blockDim == NT: 16 entries per thread, loaded in one round.
@@ -876,7 +906,8 @@ __device__ __forceinline__ void utarget_tile(const double* Qs, const double (&a)
 
 // ---------------------------------------------------------------------------
 // V-step P = U^T R and target Y = G_U^{-1} P  (Eq. (3), first half)
-// grid: one side WG (the accumulated U Gram, ridge, inverse) followed by
+// grid: nside side WGs (the U Gram U^T U on int8 MFMA over K slices, then
+//       in the last of them the ridge and inverse) followed by
 //       (n_pad/32 column tiles) x gv row groups; the last of the gv WGs of a
 //       column tile (per-tile counter) sums the int64 partials, waits for
 //       G_U^{-1} and writes the Y tile and its T_tau statistics.
@@ -888,7 +919,7 @@ __device__ __forceinline__ void utarget_tile(const double* Qs, const double (&a)
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vstep(const float* __restrict__ R, const v4i* __restrict__ Umf,
                                               long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
                                               int64_t m_pad, int64_t n_pad, int gv, int bb, int* gacc,
-                                              double* ginvU, int nside, double* __restrict__ Y,
+                                              unsigned* gcounter, double* ginvU, int nside, double* __restrict__ Y,
                                               int64_t n, double* ps, double* pm, int* pi, unsigned* tilecnt,
                                               unsigned* ready, int* flags) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
@@ -900,7 +931,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     __builtin_amdgcn_s_setprio(3);
     double* Gs = (double*)(smem + 2048);
     double* pbuf = Gs + 4096;
-    take_gram(gacc, Gs);
+    if (!side_gram_acc(Umf, m_pad, blockIdx.x, nside, gacc, gcounter, Gs, (int*)smem)) return;
     ridge_invert_store(Gs, pbuf, bb, ginvU);
     signal_ready(ready);
     return;
@@ -979,9 +1010,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // ---------------------------------------------------------------------------
 // U-step Q = R diag(h~) V and target Z = Q G_V^{-1}  (Eq. (3) second half,
 // Sec. 2.5)
-// grid: side WGs (the accumulated V Gram, or, weighted, NSIDE_W WGs
-//       building V^T H V; ridge, inverse; the raw Gram is kept for the scale
-//       solve) followed by ntile row groups of `rows` <= 32 rows, sized so
+// grid: nside side WGs (V^T V on int8 MFMA or, weighted, V^T H V on fp64
+//       MFMA, over K slices; the last of them adds the ridge and inverts;
+//       the raw Gram is kept for the scale solve) followed by ntile row groups of `rows` <= 32 rows, sized so
 //       that the whole grid is resident at two workgroups per CU and every
 //       CU streams the same share of R; each row group stores Q, waits for
 //       G_V^{-1} and writes its Z rows and T_tau statistics.
@@ -1015,7 +1046,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     double* pbuf = Gs + 4096;
     bool last = true;
     if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, nside, gpart, counter, Gs);
-    else take_gram(gacc, Gs);
+    else last = side_gram_acc(Vmf, n_pad, blockIdx.x, nside, gacc, counter, Gs, (int*)smem);
     if (last) {
       for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
       __syncthreads();
@@ -2033,28 +2064,24 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, (const double*)nullptr, w.m, w.m_pad, bb, tau,
                      w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_gram_acc(w, 0, s);
+  return hipGetLastError();
 }
 
-hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* tm) {
-  const unsigned grid = (unsigned)(1 + (w.n_pad / TILE) * w.gv);
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
+  const unsigned grid = (unsigned)(NSIDE_GRAM + (w.n_pad / TILE) * w.gv);
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, w.maxbits + blk, w.m_pad,
-                                   w.n_pad, w.gv, bb, w.gacc, w.ginvU, 1, w.Y, w.n,
+                                   w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM, w.Y, w.n,
                                    w.tps, w.tpm, w.tpi, w.tilecnt, w.counters + CNT_READY_U, w.flags);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi, w.Vt,
                      w.Vmf, w.counters + CNT_READY_U);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return weighted ? hipSuccess : launch_gram_acc(w, 1, s);
+  return hipGetLastError();
 }
 
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* tm) {
   hipError_t e;
-  const unsigned nside = weighted ? NSIDE_W : 1;
+  const unsigned nside = weighted ? NSIDE_W : NSIDE_GRAM;
   const unsigned grid = (unsigned)(nside + w.ntu);
   if (weighted) {
     hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad,
@@ -2077,9 +2104,7 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.tps, w.tpm, w.tpi,
                      w.ntu, w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_gram_acc(w, 0, s);
+  return hipGetLastError();
 }
 
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
