@@ -55,6 +55,9 @@ EXPORTED = tuple(_SIGNATURES)
 
 
 KCLASS_NAMES = ("vstep_contraction", "ustep_contraction", "deflate")
+# externd_factorize_timed times one launch in TIMING_STRIDE of each class
+# (EXTERND_TIMING_STRIDE in include/externd.h).
+TIMING_STRIDE = 16
 
 
 class KernelTimes(ctypes.Structure):

@@ -7,6 +7,8 @@
 #include <stdint.h>
 #include <stddef.h>
 
+#include "externd.h"
+
 namespace externd {
 
 // Components of a block are padded to BBP; rows and columns of the residual
@@ -87,17 +89,23 @@ struct Timer {
   struct Mark { hipEvent_t a, b; int cls; };
   Mark* marks = nullptr;
   int n = 0, cap = 0;
+  int64_t seen[EXTERND_KCLASS_COUNT] = {};
+  // Whether this launch of class cls is one of the sampled ones (every
+  // EXTERND_TIMING_STRIDE-th, from the middle of the first stride on).
+  bool sample(int cls) { return (seen[cls]++ % EXTERND_TIMING_STRIDE) == EXTERND_TIMING_STRIDE / 2; }
   // The event pair of the next timed launch (created on first use).
   hipError_t take(int cls, hipEvent_t* a, hipEvent_t* b);
   hipError_t collect(double* total_ms, int64_t* launches, int ncls);
   ~Timer();
 };
-// Launch `kernel`; when `t` is non-null the launch carries start/stop
-// events that the runtime stamps at the kernel's own start and end
-// (hipExtLaunchKernelGGL), so the measured time excludes dispatch gaps.
+// Launch `kernel`; when `t` is non-null, every EXTERND_TIMING_STRIDE-th
+// launch of the class carries start/stop events that the runtime stamps at
+// the kernel's own start and end (hipExtLaunchKernelGGL), so the measured
+// time excludes dispatch gaps; sampling keeps the host-side cost of the
+// events from slowing the launch stream it measures.
 #define EXTERND_LAUNCH_TIMED(t, cls, kernel, grid, block, shm, s, ...)          \
   do {                                                                        \
-    if (t) {                                                                  \
+    if ((t) && (t)->sample(cls)) {                                            \
       hipEvent_t _a, _b;                                                      \
       hipError_t _e = (t)->take(cls, &_a, &_b);                               \
       if (_e != hipSuccess) return _e;                                        \
