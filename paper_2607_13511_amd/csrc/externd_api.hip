@@ -22,7 +22,7 @@ static inline int clampi(int64_t v, int64_t lo, int64_t hi) { return (int)(v < l
 struct Layout {
   int64_t m_pad, n_pad;
   int gv, gd, nblk_cap;
-  int urows, ntu;
+  int urows, ntu, nsu, nsv;
   size_t off[40];
   size_t total;
 };
@@ -41,6 +41,8 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   // that every CU streams the same share of R.
   L.urows = clampi((L.m_pad + (USTEP_SLOTS - NSIDE_MAX) - 1) / (USTEP_SLOTS - NSIDE_MAX), 1, TILE);
   L.ntu = (int)((L.m_pad + L.urows - 1) / L.urows);
+  L.nsu = clampi((L.m_pad + TERN_CHUNK - 1) / TERN_CHUNK, 1, TERN_SPLIT_MAX);
+  L.nsv = clampi((L.n_pad + TERN_CHUNK - 1) / TERN_CHUNK, 1, TERN_SPLIT_MAX);
   L.nblk_cap = (int)(k + 2);  // fro2 before every block and after the last; one spare
   int64_t ntmax = nrt > nct ? nrt : nct;  // statistics tiles: 32-index tiles of either side,
   if (L.ntu > ntmax) ntmax = L.ntu;       // or the U-step's row groups
@@ -61,7 +63,7 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(int) * 4096 * NSIDE_MAX,                  // 13 gparti
       sizeof(double) * (size_t)(L.gd * L.n_pad),       // 14 colE_part
       sizeof(double) * (size_t)L.n_pad,                // 15 hw
-      sizeof(double) * BBP,                            // 16 gvec
+      sizeof(double) * BBP * TERN_SPLIT_MAX,           // 16 gvec
       sizeof(double) * BBP,                            // 17 dvec
       sizeof(float) * BBP,                             // 18 dF
       sizeof(int) * BBP,                               // 19 J
@@ -104,6 +106,8 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.gd = L.gd;
   w.urows = L.urows;
   w.ntu = L.ntu;
+  w.nsu = L.nsu;
+  w.nsv = L.nsv;
   w.R = (float*)(b + L.off[0]);
   w.Ut = (int8_t*)(b + L.off[1]);
   w.Ur = (int8_t*)(b + L.off[2]);
@@ -287,7 +291,7 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
     HIP_TRY(launch_init(w, bb, tau, s));
     for (int it = 0; it < iters; ++it) {
       HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm));
-      HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, s, tm));
+      HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm));
     }
     HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
     HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s));
@@ -391,7 +395,7 @@ int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, in
   HIP_TRY(launch_prep(w, h, s));
   HIP_TRY(launch_stage(w, R, n, s));
   HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
-  HIP_TRY(launch_ustep(w, 0, bb, tau, h != nullptr, s));
+  HIP_TRY(launch_ustep(w, 0, bb, tau, h != nullptr, false, s));
   HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
   if (Q_out_or_null) HIP_TRY(launch_store_cm(Q_out_or_null, w.Q, m, w.m_pad, bb, s));
   if (Z_out_or_null) HIP_TRY(launch_store_cm(Z_out_or_null, w.Z, m, w.m_pad, bb, s));

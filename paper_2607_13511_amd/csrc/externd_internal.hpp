@@ -28,7 +28,10 @@ constexpr int USTEP_SLOTS = 512;
 // Threads per workgroup for all kernels except the selection kernel.
 constexpr int NT = 256;
 constexpr int NT_SELECT = 1024;
-constexpr int NT_TERN = 1024;   // per-component ternarization kernels
+// Ternarization: workgroups per component (each takes a 32-aligned chunk
+// of about TERN_CHUNK entries; at most TERN_SPLIT_MAX per component).
+constexpr int TERN_SPLIT_MAX = 8;
+constexpr int TERN_CHUNK = 640;
 
 // Index of counters in Ws::counters (each used by one kernel family, reset
 // to zero by the workgroup that consumes it).
@@ -44,6 +47,7 @@ struct Ws {
   int gv;                // row groups of the V-step contraction
   int gd;                // row groups of the deflation / staging passes
   int urows, ntu;        // U-step: rows per workgroup (<= 32) and number of row groups
+  int nsu, nsv;          // ternarization workgroups per U / V component
 
   float* R;              // m_pad x n_pad residual, fp32, row-major
   int8_t* Ut;            // BBP x m_pad, U transposed (component-major)
@@ -69,7 +73,7 @@ struct Ws {
   int* gparti;           // NSIDE_MAX x BBP x BBP partial integer Grams
   double* colE_part;     // gd x n_pad partial column energies
   double* hw;            // n_pad: h~ (fp64), 1 when unweighted
-  double* gvec;          // BBP: diag(U^T Q)
+  double* gvec;          // BBP x TERN_SPLIT_MAX: diag(U^T Q) in per-split partial sums
   double* dvec;          // BBP: joint scales (fp64)
   float* dF;             // BBP: joint scales rounded to fp32
   int* J;                // BBP: init columns
@@ -127,7 +131,9 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s);
 // The contraction launches build the Gram of their factor themselves (side
 // workgroups); launch_gram_acc serves the scale solve.
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr);
-hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s,
+// final: the last U-step of a block, which also forms g = diag(U^T Q) for
+// the scale solve.
+hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
                         Timer* t = nullptr);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
 // The end of a block: scale solve, row-major factor copies, packed B and C, D.

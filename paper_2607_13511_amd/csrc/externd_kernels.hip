@@ -1153,114 +1153,174 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 }
 
 // ---------------------------------------------------------------------------
-// T_tau of one target component from its per-tile statistics (Eq. (2)):
+// T_tau of target components from their per-tile statistics (Eq. (2)):
 // theta = tau * (sum |x|) / L, strict ">", and when no entry exceeds theta
-// (max |x| <= theta) only the largest |x| (smallest index) is kept.  One
-// pass over x writes the trits component-major (dst[0 .. L_pad)) and into
-// the MFMA-ready layout mf, zero beyond L; with q it also returns
-// sum_i t_i q_i (fp64, fixed reduction order).  blockDim.x = NT_TERN.
+// (max |x| <= theta) only the largest |x| (smallest index) is kept.
+// Workgroup (c, split) handles entries [i0, i1) of component c: every split
+// reduces the same statistics with the same arithmetic, so all splits of a
+// component apply the identical threshold.  The statistics loads are
+// issued before the chunk's targets so that the reduction overlaps them.
+// Writes the trits component-major (dst) and into the MFMA-ready layout
+// mf, zero beyond L; with q it returns this chunk's sum_i t_i q_i (fp64,
+// fixed reduction order).  blockDim.x = NT.
 // ---------------------------------------------------------------------------
-constexpr int TERN_SPAN = 12;  // entries per thread kept in registers (L <= TERN_SPAN * NT_TERN in one pass)
+constexpr int TERN_SP = 2;  // statistics tiles per thread loaded up front
+constexpr int TERN_XS = 8;  // chunk entries per thread kept in registers
 
-__device__ __forceinline__ double tern_from_stats(const double* __restrict__ x, const double* __restrict__ q, int64_t L,
-                                                  int64_t L_pad, int ntile, const double* __restrict__ ps,
-                                                  const double* __restrict__ pm, const int* __restrict__ pi,
-                                                  double tau, int8_t* __restrict__ dst, int8_t* __restrict__ mf,
-                                                  int c) {
-  __shared__ double shd[16];
-  __shared__ long long shl[16];
-  const int tid = threadIdx.x, st = blockDim.x;
-  // the target loads go out first; their latency overlaps the reduction
-  double xc[TERN_SPAN], qc[TERN_SPAN];
+// Sum (fixed butterfly and wave order) and max over the workgroup; every
+// thread receives both.
+__device__ __forceinline__ void block_sum_max(double& s, double& m, double* sh /* >= 8 */) {
 #pragma unroll
-  for (int cc = 0; cc < TERN_SPAN; ++cc) {
-    const int64_t i = tid + (int64_t)cc * st;
-    xc[cc] = i < L ? x[i] : 0.0;
-    qc[cc] = (q && i < L) ? q[i] : 0.0;
+  for (int o = 32; o > 0; o >>= 1) {
+    s += __shfl_xor(s, o, 64);
+    m = fmax(m, __shfl_xor(m, o, 64));
   }
-  // statistics over the tiles, fixed order: thread-strided partials, then the block tree
-  double s = 0.0, mv = -1.0;
-  long long mi = 0;
-  for (int t = tid; t < ntile; t += st) {
-    s += ps[t];
-    argmax_merge(mv, mi, pm[t], pi[t]);
+  const int w = wave_id();
+  if (lane_id() == 0) {
+    sh[w] = s;
+    sh[4 + w] = m;
   }
-  const double S = block_sum_d(s, shd);
-  block_argmax(mv, mi, shd, shl);
+  __syncthreads();
+  s = ((sh[0] + sh[1]) + sh[2]) + sh[3];
+  m = fmax(fmax(sh[4], sh[5]), fmax(sh[6], sh[7]));
+}
+
+__device__ __forceinline__ double tern_chunk(const double* __restrict__ x, const double* __restrict__ q, int64_t L,
+                                             int64_t i0, int64_t i1, int ntile, const double* __restrict__ ps,
+                                             const double* __restrict__ pm, const int* __restrict__ pi, double tau,
+                                             int8_t* __restrict__ dst, int8_t* __restrict__ mf, int c) {
+  __shared__ double shd[8];
+  __shared__ int shi[4];
+  const int tid = threadIdx.x;
+  double psr[TERN_SP], pmr[TERN_SP];
+#pragma unroll
+  for (int k = 0; k < TERN_SP; ++k) {
+    const int t = tid + k * NT;
+    psr[k] = t < ntile ? ps[t] : 0.0;
+    pmr[k] = t < ntile ? pm[t] : -1.0;
+  }
+  double xc[TERN_XS], qc[TERN_XS];
+#pragma unroll
+  for (int k = 0; k < TERN_XS; ++k) {
+    const int64_t i = i0 + tid + (int64_t)k * NT;
+    xc[k] = (i < i1 && i < L) ? x[i] : 0.0;
+    qc[k] = (q && i < i1 && i < L) ? q[i] : 0.0;
+  }
+  double S = 0.0, M = -1.0;
+#pragma unroll
+  for (int k = 0; k < TERN_SP; ++k) {
+    S += psr[k];
+    M = fmax(M, pmr[k]);
+  }
+  for (int t = tid + TERN_SP * NT; t < ntile; t += NT) {
+    S += ps[t];
+    M = fmax(M, pm[t]);
+  }
+  block_sum_max(S, M, shd);
   const double theta = tau * (S / (double)L);
-  const bool keep_max = !(mv > theta);
-  double g = 0.0;
+  const bool keep_max = !(M > theta);  // uniform over the workgroup
+  int mi = 0;
+  if (keep_max) {
+    // the smallest index attaining the maximum: the smallest tile argmax
+    // among the tiles whose maximum is M
+    int best = 0x7fffffff;
+    for (int t = tid; t < ntile; t += NT)
+      if (pm[t] == M) best = min(best, pi[t]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) best = min(best, __shfl_xor(best, o, 64));
+    if (lane_id() == 0) shi[wave_id()] = best;
+    __syncthreads();
+    mi = min(min(shi[0], shi[1]), min(shi[2], shi[3]));
+  }
   auto decide = [&](int64_t i, double xv) -> int8_t {
     if (i >= L) return 0;
     const bool on = keep_max ? (i == mi) : (fabs(xv) > theta);
     return on ? ((xv > 0.0) ? 1 : ((xv < 0.0) ? -1 : 0)) : 0;
   };
+  double g = 0.0;
 #pragma unroll
-  for (int cc = 0; cc < TERN_SPAN; ++cc) {
-    const int64_t i = tid + (int64_t)cc * st;
-    if (i < L_pad) {
-      const int8_t t = decide(i, xc[cc]);
-      g += (double)t * qc[cc];
+  for (int k = 0; k < TERN_XS; ++k) {
+    const int64_t i = i0 + tid + (int64_t)k * NT;
+    if (i < i1) {
+      const int8_t t = decide(i, xc[k]);
+      g += (double)t * qc[k];
       dst[i] = t;
       mf[mf_offset(c, i)] = t;
     }
   }
-  for (int64_t i = tid + (int64_t)TERN_SPAN * st; i < L_pad; i += st) {
+  for (int64_t i = i0 + tid + (int64_t)TERN_XS * NT; i < i1; i += NT) {
     const double xv = i < L ? x[i] : 0.0;
     const int8_t t = decide(i, xv);
     if (q && i < L) g += (double)t * q[i];
     dst[i] = t;
     mf[mf_offset(c, i)] = t;
   }
-  return block_sum_d(g, shd);
+  if (!q) return 0.0;
+  double dummy = 0.0;
+  __syncthreads();  // shd reuse
+  block_sum_max(g, dummy, shd);
+  return g;
 }
 
-// V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.  grid: BBP.
-__global__ __launch_bounds__(NT_TERN) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb,
-                                                    double tau, const double* __restrict__ ps,
-                                                    const double* __restrict__ pm, const int* __restrict__ pi,
-                                                    int8_t* __restrict__ Vt, int8_t* __restrict__ Vmf,
-                                                    unsigned* ready_clear) {
-  const int c = blockIdx.x;
-  if (c == 0 && threadIdx.x == 0) *ready_clear = 0u;
-  const int ntile = (int)(n_pad / TILE);
+// Split `sp` of `ns` of a length-L_pad component: [i0, i1), 32-aligned.
+__device__ __forceinline__ void tern_range(int64_t L_pad, int sp, int ns, int64_t& i0, int64_t& i1) {
+  const int64_t chunk = ((L_pad + ns - 1) / ns + TILE - 1) / TILE * TILE;
+  i0 = (int64_t)sp * chunk;
+  i1 = i0 + chunk < L_pad ? i0 + chunk : L_pad;
+}
+
+// V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.
+// grid: BBP x ns (component c = blockIdx.x / ns, split blockIdx.x % ns).
+__global__ __launch_bounds__(NT) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb, double tau,
+                                               const double* __restrict__ ps, const double* __restrict__ pm,
+                                               const int* __restrict__ pi, int ntile, int ns, int8_t* __restrict__ Vt,
+                                               int8_t* __restrict__ Vmf, unsigned* ready_clear) {
+  const int c = blockIdx.x / ns, sp = blockIdx.x % ns;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *ready_clear = 0u;
+  int64_t i0, i1;
+  tern_range(n_pad, sp, ns, i0, i1);
   int8_t* dst = Vt + (int64_t)c * n_pad;
   if (c >= bb) {
-    for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
+    for (int64_t j = i0 + threadIdx.x; j < i1; j += NT) {
       dst[j] = 0;
       Vmf[mf_offset(c, j)] = 0;
     }
-  } else {
-    const int64_t o = (int64_t)c * ntile;
-    tern_from_stats(Y + (int64_t)c * n_pad, nullptr, n, n_pad, ntile, ps + o, pm + o, pi + o, tau, dst, Vmf, c);
+    return;
   }
+  const int64_t o = (int64_t)c * ntile;
+  tern_chunk(Y + (int64_t)c * n_pad, nullptr, n, i0, i1, ntile, ps + o, pm + o, pi + o, tau, dst, Vmf, c);
 }
 
-// U <- T_tau(Z[:, c]); also g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for
-// the joint scale solve (Eq. (4)).  ps/pm/pi: statistics of ntile row
-// groups (the U-step's groups, or 32-row tiles after the initial gather).
-// grid: BBP.
-__global__ __launch_bounds__(NT_TERN) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q,
-                                                    int64_t m, int64_t m_pad, int bb, double tau,
-                                                    const double* __restrict__ ps, const double* __restrict__ pm,
-                                                    const int* __restrict__ pi, int ntile, int8_t* __restrict__ Ut,
-                                                    int8_t* __restrict__ Umf, double* __restrict__ gvec,
-                                                    unsigned* ready_clear) {
-  const int c = blockIdx.x;
-  if (c == 0 && threadIdx.x == 0) *ready_clear = 0u;
+// U <- T_tau(Z[:, c]).  With Q (the last U-step of a block), also the
+// split's share of g_c = sum_i U_ic Q_ic = diag(U^T R H V)_c for the joint
+// scale solve (Eq. (4)): gpart[c * TERN_SPLIT_MAX + sp], unused slots 0.
+// ps/pm/pi: statistics of ntile row groups (the U-step's groups, or 32-row
+// tiles after the initial gather).  grid: BBP x ns as k_tern_v.
+__global__ __launch_bounds__(NT) void k_tern_u(const double* __restrict__ Z, const double* __restrict__ Q, int64_t m,
+                                               int64_t m_pad, int bb, double tau, const double* __restrict__ ps,
+                                               const double* __restrict__ pm, const int* __restrict__ pi, int ntile,
+                                               int ns, int8_t* __restrict__ Ut, int8_t* __restrict__ Umf,
+                                               double* __restrict__ gpart, unsigned* ready_clear) {
+  const int c = blockIdx.x / ns, sp = blockIdx.x % ns;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *ready_clear = 0u;
+  int64_t i0, i1;
+  tern_range(m_pad, sp, ns, i0, i1);
   int8_t* dst = Ut + (int64_t)c * m_pad;
+  double g = 0.0;
   if (c >= bb) {
-    for (int64_t i = threadIdx.x; i < m_pad; i += blockDim.x) {
+    for (int64_t i = i0 + threadIdx.x; i < i1; i += NT) {
       dst[i] = 0;
       Umf[mf_offset(c, i)] = 0;
     }
-    if (threadIdx.x == 0) gvec[c] = 0.0;
   } else {
     const int64_t o = (int64_t)c * ntile;
-    const double* qrow = Q ? Q + (int64_t)c * m_pad : nullptr;  // no Q: initialisation, g unused
-    const double g = tern_from_stats(Z + (int64_t)c * m_pad, qrow, m, m_pad, ntile, ps + o, pm + o, pi + o, tau, dst,
-                                     Umf, c);
-    if (threadIdx.x == 0) gvec[c] = g;
+    const double* qrow = Q ? Q + (int64_t)c * m_pad : nullptr;
+    g = tern_chunk(Z + (int64_t)c * m_pad, qrow, m, i0, i1, ntile, ps + o, pm + o, pi + o, tau, dst, Umf, c);
+  }
+  if (Q && threadIdx.x == 0) {
+    gpart[c * TERN_SPLIT_MAX + sp] = g;
+    if (sp == 0)
+      for (int k = ns; k < TERN_SPLIT_MAX; ++k) gpart[c * TERN_SPLIT_MAX + k] = 0.0;
   }
 }
 
@@ -1364,10 +1424,19 @@ __device__ __forceinline__ void scale_solve(int* gacc, int bb, const double* __r
   if (t < bb) Gs[t * 64 + t] += delta;
   __syncthreads();
   spd_inverse64(Gs, colbuf);
+  // g_c: the per-split partial sums in split order
+  __shared__ double s_g[BBP];
+  if (t < BBP) {
+    double g = 0.0;
+#pragma unroll
+    for (int k = 0; k < TERN_SPLIT_MAX; ++k) g += gvec[t * TERN_SPLIT_MAX + k];
+    s_g[t] = g;
+  }
+  __syncthreads();
   if (t < BBP) {
     double d = 0.0;
     if (t < bb)
-      for (int c = 0; c < bb; ++c) d += Gs[t * 64 + c] * gvec[c];
+      for (int c = 0; c < bb; ++c) d += Gs[t * 64 + c] * s_g[c];
     dvec[t] = d;
     dF[t] = (float)d;
     if (Dout && t < bb) Dout[t] = (float)d;
@@ -1989,7 +2058,8 @@ __global__ __launch_bounds__(NT) void k_gram_acc(const v4i* __restrict__ Xmf, in
                   gacc, red);
 }
 
-// g_c = sum_i U_ic Q_ic (fp64).  grid: BBP.
+// g_c = sum_i U_ic Q_ic (fp64), in slot 0 of the per-split partial sums.
+// grid: BBP.
 __global__ __launch_bounds__(NT) void k_gvec(const int8_t* __restrict__ Ut, const double* __restrict__ Q, int64_t m,
                                              int64_t m_pad, int bb, double* __restrict__ gvec) {
   __shared__ double shd[16];
@@ -1998,7 +2068,7 @@ __global__ __launch_bounds__(NT) void k_gvec(const int8_t* __restrict__ Ut, cons
   if (c < bb)
     for (int64_t i = threadIdx.x; i < m; i += NT) acc += (double)Ut[(int64_t)c * m_pad + i] * Q[(int64_t)c * m_pad + i];
   acc = block_sum_d(acc, shd);
-  if (threadIdx.x == 0) gvec[c] = acc;
+  if (threadIdx.x < TERN_SPLIT_MAX) gvec[c * TERN_SPLIT_MAX + threadIdx.x] = threadIdx.x == 0 ? acc : 0.0;
 }
 
 // Scales given by the caller: dvec = d, dF = fp32(d), zero beyond bb.
@@ -2062,8 +2132,9 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
                      bb, w.Z, w.tps, w.tpm, w.tpi);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, (const double*)nullptr, w.m, w.m_pad, bb, tau,
-                     w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
+  hipLaunchKernelGGL(k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, w.Z, (const double*)nullptr, w.m, w.m_pad, bb, tau,
+                     w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec,
+                     w.counters + CNT_READY_V);
   return hipGetLastError();
 }
 
@@ -2074,12 +2145,13 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
                                    w.tps, w.tpm, w.tpi, w.tilecnt, w.counters + CNT_READY_U, w.flags);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_v, dim3(BBP), dim3(NT_TERN), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi, w.Vt,
-                     w.Vmf, w.counters + CNT_READY_U);
+  hipLaunchKernelGGL(k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi,
+                     (int)(w.n_pad / TILE), w.nsv, w.Vt, w.Vmf, w.counters + CNT_READY_U);
   return hipGetLastError();
 }
 
-hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, hipStream_t s, Timer* tm) {
+hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
+                        Timer* tm) {
   hipError_t e;
   const unsigned nside = weighted ? NSIDE_W : NSIDE_GRAM;
   const unsigned grid = (unsigned)(nside + w.ntu);
@@ -2102,8 +2174,9 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_u, dim3(BBP), dim3(NT_TERN), 0, s, w.Z, w.Q, w.m, w.m_pad, bb, tau, w.tps, w.tpm, w.tpi,
-                     w.ntu, w.Ut, w.Umf, w.gvec, w.counters + CNT_READY_V);
+  hipLaunchKernelGGL(k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, w.Z, final ? (const double*)w.Q : nullptr, w.m,
+                     w.m_pad, bb, tau, w.tps, w.tpm, w.tpi, w.ntu, w.nsu, w.Ut, w.Umf, w.gvec,
+                     w.counters + CNT_READY_V);
   return hipGetLastError();
 }
 
