@@ -1027,6 +1027,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // ---------------------------------------------------------------------------
 constexpr int NST_U = 3;
 constexpr int USTAGE_B = 4096 + 256;  // bytes per staged K step: tile + weights
+// LDS of k_ustep: the staging area (4 waves x NST_U K steps), which the
+// 64 KB wave reduction reuses afterwards
+constexpr int USTEP_SMEM_LL = (4 * NST_U * USTAGE_B + 7) / 8 > 8192 ? (4 * NST_U * USTAGE_B + 7) / 8 : 8192;
 
 template <bool WEIGHTED>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_ustep(const float* __restrict__ R, const v4i* __restrict__ Vmf,
@@ -1038,7 +1041,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                               double* pm, int* pi, unsigned* ready, int* flags) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
-  __shared__ __attribute__((aligned(16))) long long smem[8192];
+  __shared__ __attribute__((aligned(16))) long long smem[USTEP_SMEM_LL];
   if ((int)blockIdx.x < nside) {
     // critical path of the launch (see k_vstep)
     __builtin_amdgcn_s_setprio(3);
@@ -1071,9 +1074,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   // loader mapping: lane -> row 8 q + lane / 8, 16-byte chunk lane % 8,
   // stored at chunk position (lane % 8) ^ (row % 8); rows >= valid are
   // not loaded (their staging rows hold stale values; the MFMA output rows
-  // they feed are discarded).  Row 0 is always valid, so every stage
-  // issues at least one direct load and the vmcnt bounds of the operand
-  // reads (which count one stage's loads plus the two factor loads) hold.
+  // they feed are discarded), so a stage issues between 1 and 4 direct
+  // loads.  The operand reads wait until at most NLD * (NST_U - 1) loads are
+  // outstanding; even with one direct load per stage at least that many
+  // follow the stage read (its two factor loads, then NST_U - 1 stages of
+  // >= 3 loads each; weighted >= 4), so the bound holds for NST_U = 3.
+  static_assert(NST_U == 3, "vmcnt bound of the operand reads assumes three stages");
   const int lrow = lane >> 3;
   const float* Rld = R + (i0 + lrow) * n_pad + (((lane & 7) ^ lrow) * 4);
   constexpr int NLD = WEIGHTED ? 5 : 4;  // direct loads per staged K step
@@ -1726,9 +1732,10 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
                                                       double* keys /* n_pad scratch */, double* fro2_out,
                                                       double* fro2w_out, int bb, int* __restrict__ J) {
   __shared__ double shd[16];
-  __shared__ unsigned hist[256];
+  __shared__ unsigned hist[NT_SELECT / 64][256];  // one histogram per wave
+  __shared__ unsigned htot[256];
   __shared__ unsigned long long s_prefix;
-  __shared__ int s_need;
+  __shared__ int s_need, s_exact;
   __shared__ int s_cnt;
   __shared__ unsigned long long cand_key[BBP];
   __shared__ int cand_idx[BBP];
@@ -1750,26 +1757,39 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
     kc[q] = j < n ? (unsigned long long)__double_as_longlong(hw[j] * keys[j]) : 0ull;
   }
   for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) keys[j] = hw[j] * keys[j];
-  // radix select over the 64-bit patterns, 8 bits at a time from the top
+  // radix select over the 64-bit patterns, 8 bits at a time from the top.
+  // Energies share their leading bits, so each wave counts into its own
+  // histogram (no block-wide contention on one bin).  The passes stop early
+  // once the bin holding the bb-th largest key holds exactly the keys still
+  // needed: then the selection is every key >= that bin's lower bound.
   if (threadIdx.x == 0) {
     s_prefix = 0ull;
     s_need = bb;
+    s_exact = 0;
   }
   __syncthreads();
+  unsigned* whist = hist[wave_id()];
   for (int pass = 0; pass < 8; ++pass) {
     const int shift = 56 - 8 * pass;
-    for (int e = threadIdx.x; e < 256; e += blockDim.x) hist[e] = 0u;
+    for (int e = threadIdx.x; e < (NT_SELECT / 64) * 256; e += blockDim.x) (&hist[0][0])[e] = 0u;
     __syncthreads();
     const unsigned long long prefix = s_prefix;
     const unsigned long long hmask = (pass == 0) ? 0ull : (~0ull << (shift + 8));
 #pragma unroll
     for (int q = 0; q < SELECT_CACHE; ++q) {
       const int64_t j = threadIdx.x + q * st;
-      if (j < n && (kc[q] & hmask) == prefix) atomicAdd(&hist[(kc[q] >> shift) & 0xff], 1u);
+      if (j < n && (kc[q] & hmask) == prefix) atomicAdd(&whist[(kc[q] >> shift) & 0xff], 1u);
     }
     for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) {
       const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
-      if ((kb & hmask) == prefix) atomicAdd(&hist[(kb >> shift) & 0xff], 1u);
+      if ((kb & hmask) == prefix) atomicAdd(&whist[(kb >> shift) & 0xff], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x < 256) {
+      unsigned c = 0;
+#pragma unroll
+      for (int w = 0; w < NT_SELECT / 64; ++w) c += hist[w][threadIdx.x];
+      htot[threadIdx.x] = c;
     }
     __syncthreads();
     if (threadIdx.x < 64) {
@@ -1780,7 +1800,7 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
       int c[4], tot = 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        c[q] = (int)hist[255 - 4 * lane - q];
+        c[q] = (int)htot[255 - 4 * lane - q];
         tot += c[q];
       }
       int incl = tot;
@@ -1793,11 +1813,13 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
       if (lane == first) {
         int run = incl - tot, d = 0, nn = need;
         bool found = false;
+        int cd = 0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if (!found && run + c[q] >= need) {
             d = 255 - 4 * lane - q;
             nn = need - run;
+            cd = c[q];
             found = true;
           }
           if (!found) run += c[q];
@@ -1808,20 +1830,26 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
         }
         s_need = nn;
         s_prefix = prefix | ((unsigned long long)d << shift);
+        s_exact = found && cd == nn;
       }
     }
     __syncthreads();
+    if (s_exact) break;
   }
-  // T = s_prefix (exact key of the bb-th largest); keys > T all selected,
-  // then the s_need smallest indices with key == T.
+  // T = s_prefix: either the exact key of the bb-th largest (keys > T all
+  // selected, then the s_need smallest indices with key == T), or, after an
+  // early stop, the lower bound of a bin whose keys are all selected (keys
+  // >= T, nothing left to tie-break).
+  const bool ge = s_exact != 0;
   const unsigned long long T = s_prefix;
-  const int need_eq = s_need;
+  const int need_eq = ge ? 0 : s_need;
+  auto above = [&](unsigned long long kb) { return ge ? kb >= T : kb > T; };
   if (threadIdx.x == 0) s_cnt = 0;
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < SELECT_CACHE; ++q) {
     const int64_t j = threadIdx.x + q * st;
-    if (j < n && kc[q] > T) {
+    if (j < n && above(kc[q])) {
       const int slot = atomicAdd(&s_cnt, 1);
       if (slot < BBP) {
         cand_key[slot] = kc[q];
@@ -1831,7 +1859,7 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
   }
   for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) {
     const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
-    if (kb > T) {
+    if (above(kb)) {
       const int slot = atomicAdd(&s_cnt, 1);
       if (slot < BBP) {
         cand_key[slot] = kb;
@@ -1846,7 +1874,7 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
   int carry = 0;
   const int base = s_cnt;
   const int rounds = (int)((n + st - 1) / st);
-  bool done = false;
+  bool done = need_eq == 0;
   auto scan_round = [&](int64_t j, unsigned long long kb) {
     const int f = (j < n && kb == T) ? 1 : 0;
     int v = f;

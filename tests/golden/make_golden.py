@@ -1,0 +1,68 @@
+"""Write the full-size expected energy curves used by tests/test_gpu_fullsize.py.
+
+Every stored value comes from the fp64 CPU oracle (oracle/) run on the same
+seeded synthetic inputs the GPU tests build (paper_2607_13511_amd/synth.py):
+the block-ALS energy curve E after each block (and E_w for weighted runs),
+the final energies, the factor zero fractions and a SHA-256 of the input
+matrix so that a drifting generator is caught.  Run from the repository
+root:  python tests/golden/make_golden.py [name ...]
+"""
+from __future__ import annotations
+
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import oracle  # noqa: E402
+from paper_2607_13511_amd import synth  # noqa: E402
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+# one (mu, tau) point per matrix of the transformer block: the diagonal of
+# the mu in {2, 2.5, 3.5} x tau in {0.7, 1.0, 2.0} sweep
+BLOCK_POINTS = ((2.0, 0.7), (2.5, 1.0), (3.5, 2.0))
+
+
+def cases():
+    w = synth.attn2048()
+    yield w.name, w.A, w.h, w.mu, w.tau, w.block, w.iters
+    for weighted in (False, True):
+        w = synth.down9728(weighted=weighted)
+        yield w.name, w.A, w.h, w.mu, w.tau, w.block, w.iters
+    for idx, (mname, m, n) in enumerate(synth.BLOCK_SHAPES):
+        _, A, h = synth.transformer_block(idx)
+        for mu, tau in BLOCK_POINTS:
+            yield f"block_{mname}_{m}x{n}_mu{mu}_tau{tau}_b64_imatrix", A, h, mu, tau, 64, 8
+
+
+def main(names):
+    for name, A, h, mu, tau, block, iters in cases():
+        if names and name not in names:
+            continue
+        path = os.path.join(HERE, name + ".json")
+        t0 = time.time()
+        f = oracle.factorize_block(A, mu, tau, block, iters, h=h)
+        rec = {
+            "source": "oracle.factorize_block on synth inputs (tests/golden/make_golden.py)",
+            "name": name, "m": int(A.shape[0]), "n": int(A.shape[1]), "mu": mu, "tau": tau, "block": block,
+            "iters": iters, "weighted": h is not None, "k": int(f.k), "block_eff": int(f.block),
+            "a_sha256": hashlib.sha256(np.ascontiguousarray(A, dtype=np.float32).tobytes()).hexdigest(),
+            "curve": [float(x) for x in f.curve], "E": float(f.E),
+            "curve_w": [float(x) for x in f.curve_w] if f.curve_w is not None else None,
+            "E_w": float(f.E_w) if f.E_w is not None else None,
+            "zero_fraction_B": float(np.mean(f.B == 0)), "zero_fraction_C": float(np.mean(f.C == 0)),
+        }
+        with open(path, "w") as fh:
+            json.dump(rec, fh, indent=0)
+        print(f"{name}: k={f.k} E={f.E:.6f} ({time.time() - t0:.1f} s)", flush=True)
+
+
+if __name__ == "__main__":
+    main(set(sys.argv[1:]))

@@ -1,0 +1,37 @@
+"""The stored full-size expectations (tests/golden/*.json) still describe
+the inputs the tests build: each record's SHA-256 of its input matrix is
+recomputed from the seeded generator, and the record is self-consistent
+(k and block follow the rank and block rules; the curve ends at E and
+never decreases)."""
+import glob
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+GOLDEN = sorted(glob.glob(os.path.join(HERE, "golden", "*.json")))
+
+
+def test_golden_present():
+    assert len(GOLDEN) >= 3
+
+
+@pytest.mark.parametrize("path", GOLDEN, ids=lambda p: os.path.basename(p)[:-5])
+def test_golden_record(path):
+    from test_gpu_fullsize import inputs, load
+    rec = load(path)
+    A, h = inputs(rec)
+    assert A.shape == (rec["m"], rec["n"])
+    assert (h is not None) == rec["weighted"]
+    assert hashlib.sha256(np.ascontiguousarray(A, dtype=np.float32).tobytes()).hexdigest() == rec["a_sha256"]
+    assert rec["k"] == oracle.rank_of(rec["m"], rec["n"], rec["mu"])
+    assert rec["block_eff"] == oracle.effective_block(rec["m"], rec["n"], rec["block"])
+    curve = np.asarray(rec["curve"])
+    assert len(curve) == -(-rec["k"] // rec["block_eff"])
+    assert curve[-1] == rec["E"]
+    assert np.all(np.diff(curve) >= -1e-12)
