@@ -131,6 +131,7 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
 typedef struct {
   double total_ms[EXTERND_KCLASS_COUNT];  /* summed durations of the timed launches */
   int64_t launches[EXTERND_KCLASS_COUNT]; /* number of timed launches of each class */
+  int64_t issued[EXTERND_KCLASS_COUNT];   /* number of launches of each class       */
 } externd_kernel_times;
 
 /* Launches of each class timed by externd_factorize_timed: one in every
@@ -139,10 +140,12 @@ typedef struct {
 
 /* externd_factorize with HIP events recorded on `stream` around a sample
  * of the launches of the kernel classes above (every
- * EXTERND_TIMING_STRIDE-th launch of a class; the events add a small
- * host-side cost per timed launch).  `times` (host, required) receives the
- * summed durations and the number of timed launches of each class.  Same
- * outputs and status codes as externd_factorize.                         */
+ * EXTERND_TIMING_STRIDE-th launch of a class; the events are created
+ * without system-scope fences, so a timed launch ends without an L2
+ * write-back, and add a small host-side cost per timed launch).  `times`
+ * (host, required) receives the summed durations, the number of timed
+ * launches and the number of all launches of each class.  Same outputs and
+ * status codes as externd_factorize.                                     */
 int externd_factorize_timed(const float* A, int64_t m, int64_t n, double mu, double tau,
                             int32_t block, int32_t iters, const float* importance,
                             uint8_t* B_packed, uint8_t* C_packed, float* D,

@@ -61,7 +61,7 @@ TIMING_STRIDE = 16
 
 
 class KernelTimes(ctypes.Structure):
-    _fields_ = [("total_ms", ctypes.c_double * 3), ("launches", ctypes.c_int64 * 3)]
+    _fields_ = [("total_ms", ctypes.c_double * 3), ("launches", ctypes.c_int64 * 3), ("issued", ctypes.c_int64 * 3)]
 
 
 class ExterndError(RuntimeError):
@@ -146,7 +146,7 @@ class Factorization:
     curve_w: np.ndarray
     k: int
     block: int
-    kernel_times: Optional[dict] = None   # class -> (total_ms, launches) when timed
+    kernel_times: Optional[dict] = None   # class -> (total_ms, timed launches, all launches) when timed
 
 
 def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=None,
@@ -182,7 +182,8 @@ def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=N
     if timed:
         times = KernelTimes()
         _check(lib().externd_factorize_timed(*args, ctypes.byref(times)), "externd_factorize_timed")
-        kt = {name: (times.total_ms[i], int(times.launches[i])) for i, name in enumerate(KCLASS_NAMES)}
+        kt = {name: (times.total_ms[i], int(times.launches[i]), int(times.issued[i]))
+              for i, name in enumerate(KCLASS_NAMES)}
     else:
         _check(lib().externd_factorize(*args), "externd_factorize")
     return Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b, kt)

@@ -160,9 +160,11 @@ hipError_t Timer::take(int cls, hipEvent_t* a, hipEvent_t* b) {
   }
   Mark& mk = marks[n];
   if (!mk.a) {
-    hipError_t e = hipEventCreate(&mk.a);
+    // timing only: no system-scope fence (no L2 write-back at the timed
+    // kernel's end, which would lengthen the very launch being measured)
+    hipError_t e = hipEventCreateWithFlags(&mk.a, hipEventDisableSystemFence);
     if (e != hipSuccess) return e;
-    e = hipEventCreate(&mk.b);
+    e = hipEventCreateWithFlags(&mk.b, hipEventDisableSystemFence);
     if (e != hipSuccess) return e;
   }
   mk.cls = cls;
@@ -305,7 +307,10 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (flags[FLAG_SYNC]) return EXTERND_ESYNC;
-  if (tm) HIP_TRY(tm->collect(times->total_ms, times->launches, EXTERND_KCLASS_COUNT));
+  if (tm) {
+    HIP_TRY(tm->collect(times->total_ms, times->launches, EXTERND_KCLASS_COUNT));
+    for (int c = 0; c < EXTERND_KCLASS_COUNT; ++c) times->issued[c] = tm->seen[c];
+  }
   const double a2 = f2[0], a2w = f2w[0];
   auto E = [&](int64_t b) { return a2 == 0.0 ? 1.0 : 1.0 - f2[(size_t)b] / a2; };
   auto Ew = [&](int64_t b) { return a2w == 0.0 ? 1.0 : 1.0 - f2w[(size_t)b] / a2w; };
