@@ -175,6 +175,9 @@ def main():
     ap.add_argument("--collect-traffic", nargs=4, metavar="DB",
                     help="rocprofv3 --pmc databases: FETCH_SIZE, WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE")
     ap.add_argument("--copy-bytes", type=int, default=268435456)
+    ap.add_argument("--target-energy", type=float, default=None,
+                    help="time the energy-target run instead (stop at the first block with E >= target, "
+                         "mu of the workload as the maximum)")
     args = ap.parse_args()
     if args.collect_traffic:
         collect_traffic(args.collect_traffic, args.copy_bytes)
@@ -198,6 +201,9 @@ def main():
     w = workload(args.workload)
     m, n = w.A.shape
     dev = torch.device("cuda:0")
+    if args.target_energy is not None:
+        bench_target(binding, torch, w, args)
+        return
     A = torch.from_numpy(w.A).to(dev)
     h = torch.from_numpy(w.h).to(dev) if w.h is not None else None
     k = binding.rank(m, n, w.mu)
@@ -283,6 +289,33 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def bench_target(binding, torch, w, args):
+    """Time externd_factorize_to_energy on the workload: the components needed
+    to reach the target (effective mu) and the time per matrix."""
+    m, n = w.A.shape
+    dev = torch.device("cuda:0")
+    A = torch.from_numpy(w.A).to(dev)
+    h = torch.from_numpy(w.h).to(dev) if w.h is not None else None
+    k = binding.rank(m, n, w.mu)
+    ws = torch.empty(binding.workspace_bytes(m, n, k), dtype=torch.uint8, device=dev)
+    for _ in range(args.warmup):
+        binding.factorize_to_energy(A, w.mu, args.target_energy, w.tau, w.block, w.iters, h=h, workspace=ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        res = binding.factorize_to_energy(A, w.mu, args.target_energy, w.tau, w.block, w.iters, h=h, workspace=ws)
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.steps
+    print(json.dumps({
+        "metric": "sec/matrix to reach the energy target", "value": sec, "unit": "s", "higher_is_better": False,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "data": "synthetic",
+        "config": {"workload": w.name, "target_energy": args.target_energy, "mu_max": w.mu, "tau": w.tau,
+                   "block": res.block, "iters": w.iters, "importance": w.h is not None},
+        "k_used": res.k_used, "mu_effective": res.k_used / min(m, n), "energy": res.E, "energy_w": res.E_w,
+        "components_per_s": res.k_used / sec,
+    }), flush=True)
 
 
 if __name__ == "__main__":

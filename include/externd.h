@@ -122,6 +122,33 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
                       double* energy_curve, double* energy_w_curve,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * externd_factorize_to_energy -- the factorization stopped at an energy
+ * target (the paper chooses mu per matrix so that a target accuracy is met
+ * exactly, Sec. 1 and Sec. 3; greedy deflation makes every prefix of the
+ * components the same as in a longer run, Sec. 2.1).
+ *
+ *  mu_max         k_max = externd_rank(m, n, mu_max) components at most.
+ *  target_energy  finite; after each block the energy E (or, with
+ *                 importance, the weighted energy E_w) is compared with
+ *                 it, and extraction stops at the first block that
+ *                 reaches it (or at k_max).
+ *  k_used         host, out: components extracted, a multiple of the
+ *                 effective block width, or k_max.
+ *  B_packed, C_packed, D, workspace: sized for k_max as in
+ *                 externd_factorize; components past k_used are zero.
+ *  energy, energy_w: after k_used components.  energy_curve,
+ *                 energy_w_curve (may be NULL): room for ceil(k_max / b)
+ *                 entries, the first ceil(k_used / b) are written.
+ * Other arguments, status codes and synchronisation as externd_factorize.
+ * Each block adds one small device-to-host read of the energy history.
+ */
+int externd_factorize_to_energy(const float* A, int64_t m, int64_t n, double mu_max, double target_energy,
+                                double tau, int32_t block, int32_t iters, const float* importance,
+                                uint8_t* B_packed, uint8_t* C_packed, float* D, int64_t* k_used, double* energy,
+                                double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
 /* Kernel classes timed by externd_factorize_timed. */
 #define EXTERND_KCLASS_VSTEP   0  /* V-step contraction P = U^T R (+ Gram of U)          */
 #define EXTERND_KCLASS_USTEP   1  /* U-step contraction Q = R diag(h~) V (+ Gram of V)  */

@@ -59,6 +59,12 @@ Readings taken where the paper is silent (each also listed in the design doc):
 * R9 (energies): E = 1 - ||R||_F^2 / ||A||_F^2 (Sec. 2.1); the weighted
   energy is E_w = 1 - sum_j h~_j ||R_:j||^2 / sum_j h~_j ||A_:j||^2.  A zero
   matrix has E = 1.
+* R10 (energy target, Sec. 1 and Sec. 3: mu chosen per matrix so that a
+  target accuracy is met exactly): the run stops after the first block
+  whose energy reaches the target (E, or E_w when weights are given, the
+  objective that run minimizes), or at k = rank_of(m, n, mu_max).  Greedy
+  deflation makes the result the prefix of the full mu_max run, so this is
+  the smallest block-multiple k that meets the target.
 """
 from __future__ import annotations
 
@@ -240,6 +246,7 @@ class Factorization:
     safeguard_fired: int = 0      # Prop. 2 single-entry step taken (S)
     safeguard_would_fire: int = 0 # single entry would beat ALS (S)
     fro2_curve: np.ndarray = field(default_factory=lambda: np.zeros(0))
+    k_used: int = -1              # components extracted (R10 stop), else k
 
 
 def factorize_sequential(A: np.ndarray, mu: float, tau: float, iters: int,
@@ -312,14 +319,16 @@ def factorize_sequential(A: np.ndarray, mu: float, tau: float, iters: int,
 
 def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int,
                     h: Optional[np.ndarray] = None, k: Optional[int] = None,
-                    max_blocks: Optional[int] = None) -> Factorization:
+                    max_blocks: Optional[int] = None, target: Optional[float] = None) -> Factorization:
     """Batched block ALS with decorrelated targets, Sec. 2.4 (mode B).
 
     For each block of bb = min(b_eff, k - c0) components: U from reading R1,
     then ``iters`` times the V-step and U-step of Eq. (3); joint scales
     from Eq. (4); R <- R - U diag(d) V^T.  Deflation across blocks is
     sequential.  Weighted per Sec. 2.5 (reading R8).  ``max_blocks`` stops
-    early (used only to time a bounded sample).
+    early (used only to time a bounded sample).  ``target``: stop after the
+    first block whose energy reaches it (reading R10); the components past
+    ``k_used`` stay zero and ``curve`` holds the blocks done.
     """
     A = np.asarray(A, dtype=np.float64)
     m, n = A.shape
@@ -359,8 +368,15 @@ def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int
         fro2[blk] = float(np.sum(R * R))
         if weighted:
             curve_w[blk] = Ew
+        if target is not None and (Ew if weighted else E) >= target:
+            nblk = blk + 1
+            curve, fro2 = curve[:nblk], fro2[:nblk]
+            if weighted:
+                curve_w = curve_w[:nblk]
+            break
     E, Ew = energy(R, A_fro2, w if weighted else None, A_col2)
-    return Factorization(B, C, D, E, Ew, curve, curve_w, k, b_eff, 0, 0, fro2)
+    k_used = min(nblk * b_eff, k)
+    return Factorization(B, C, D, E, Ew, curve, curve_w, k, b_eff, 0, 0, fro2, k_used)
 
 
 def reconstruct(B: np.ndarray, D: np.ndarray, C: np.ndarray) -> np.ndarray:

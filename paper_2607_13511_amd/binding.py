@@ -37,6 +37,9 @@ _SIGNATURES = {
     "externd_factorize": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_ptr,
                                          _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                          _c_ptr, _c_size, _c_ptr]),
+    "externd_factorize_to_energy": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_dbl, _c_i32, _c_i32,
+                                                   _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
+                                                   _c_ptr, _c_ptr, _c_size, _c_ptr]),
     "externd_factorize_timed": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_ptr,
                                                _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                                _c_ptr, _c_size, _c_ptr, _c_ptr]),
@@ -147,6 +150,7 @@ class Factorization:
     k: int
     block: int
     kernel_times: Optional[dict] = None   # class -> (total_ms, timed launches, all launches) when timed
+    k_used: int = -1                      # components extracted (factorize_to_energy), else k
 
 
 def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=None,
@@ -186,7 +190,42 @@ def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=N
               for i, name in enumerate(KCLASS_NAMES)}
     else:
         _check(lib().externd_factorize(*args), "externd_factorize")
-    return Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b, kt)
+    return Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b, kt, k)
+
+
+def factorize_to_energy(A, mu_max: float, target: float, tau: float, block: int, iters: int, h=None,
+                        stream=None, workspace=None) -> Factorization:
+    """Factorize A until the energy (E, or E_w with h) reaches ``target``,
+    with at most rank(m, n, mu_max) components (externd_factorize_to_energy).
+    The result is sized for the maximum; components past ``k_used`` are
+    zero and ``curve`` holds the blocks extracted."""
+    torch = _torch()
+    m, n = A.shape
+    _req(A, torch, torch.float32, (m, n), "A")
+    if h is not None:
+        _req(h, torch, torch.float32, (n,), "h")
+    k = rank(m, n, mu_max)
+    if k < 1:
+        raise ExterndError(EINVAL, "rank")
+    b = effective_block(m, n, block)
+    nblk = -(-k // b)
+    dev = A.device
+    Bp = torch.empty((m, (k + 3) // 4), dtype=torch.uint8, device=dev)
+    Cp = torch.empty((k, (n + 3) // 4), dtype=torch.uint8, device=dev)
+    D = torch.empty((k,), dtype=torch.float32, device=dev)
+    ws = workspace if workspace is not None else _workspace(torch, m, n, k, dev)
+    E = ctypes.c_double(0.0)
+    Ew = ctypes.c_double(0.0)
+    ku = ctypes.c_int64(0)
+    curve = np.zeros(nblk, dtype=np.float64)
+    curve_w = np.zeros(nblk, dtype=np.float64)
+    _check(lib().externd_factorize_to_energy(
+        _dev_ptr(A), m, n, mu_max, target, tau, block, iters, _dev_ptr(h) if h is not None else None,
+        _dev_ptr(Bp), _dev_ptr(Cp), _dev_ptr(D), ctypes.byref(ku), ctypes.byref(E), ctypes.byref(Ew),
+        curve.ctypes.data, curve_w.ctypes.data, _dev_ptr(ws), ws.numel(), _stream_ptr(torch, stream)),
+        "externd_factorize_to_energy")
+    nb = -(-ku.value // b)
+    return Factorization(Bp, Cp, D, E.value, Ew.value, curve[:nb], curve_w[:nb], k, b, None, int(ku.value))
 
 
 def step_init(R, bb: int, tau: float, h=None, stream=None):

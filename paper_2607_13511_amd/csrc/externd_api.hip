@@ -257,14 +257,19 @@ size_t externd_workspace_bytes(int64_t m, int64_t n, int64_t k) {
   return externd::workspace_bytes(m, n, k);
 }
 
+// target: NaN for the full run; else stop after the first block whose
+// energy (E, or E_w with weights) reaches it, reporting *k_used.
 static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
                           const float* importance, uint8_t* B_packed, uint8_t* C_packed, float* D, double* energy,
                           double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
-                          size_t workspace_bytes, void* stream, externd_kernel_times* times) {
+                          size_t workspace_bytes, void* stream, externd_kernel_times* times,
+                          double target = NAN, int64_t* k_used = nullptr) {
   if (energy) *energy = NAN;
   if (energy_w) *energy_w = NAN;
   if (!A || !B_packed || !C_packed || !D || !energy || !workspace) return EXTERND_EINVAL;
   if (m < 1 || n < 1 || !isfinite(tau) || tau < 0.0 || block < 1 || iters < 1) return EXTERND_EINVAL;
+  const bool stop_at_target = !isnan(target);
+  if (stop_at_target && (!isfinite(target) || !k_used)) return EXTERND_EINVAL;
   const int64_t k = externd_rank(m, n, mu);
   if (k < 1) return EXTERND_EINVAL;
   if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
@@ -285,7 +290,14 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   HIP_TRY(hipStreamSynchronize(s));
   if (flags[FLAG_BADWEIGHT]) return EXTERND_EINVAL;
   if (flags[FLAG_NONFINITE]) return EXTERND_ENONFINITE;
+  if (stop_at_target) {
+    // components past the stop stay zero
+    HIP_TRY(hipMemsetAsync(B_packed, 0, (size_t)m * (size_t)((k + 3) / 4), s));
+    HIP_TRY(hipMemsetAsync(C_packed, 0, (size_t)k * (size_t)((n + 3) / 4), s));
+    HIP_TRY(hipMemsetAsync(D, 0, sizeof(float) * (size_t)k, s));
+  }
 
+  int64_t nblk_done = nblk;
   for (int64_t blk = 0; blk < nblk; ++blk) {
     const int64_t c0 = blk * b_eff;
     const int bb = (int)((k - c0) < b_eff ? (k - c0) : b_eff);
@@ -298,12 +310,28 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
     HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
     HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s));
     HIP_TRY(launch_deflate(w, (int)blk, false, s, tm));
+    if (stop_at_target && blk + 1 < nblk) {
+      // energy after this block (||R||^2 history entries 0 and blk + 1)
+      HIP_TRY(launch_finish(w, (int)blk + 1, s));
+      double h2[2][2];
+      HIP_TRY(hipMemcpyAsync(&h2[0][0], w.fro2_hist, sizeof(double), hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipMemcpyAsync(&h2[0][1], w.fro2_hist + blk + 1, sizeof(double), hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipMemcpyAsync(&h2[1][0], w.fro2w_hist, sizeof(double), hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipMemcpyAsync(&h2[1][1], w.fro2w_hist + blk + 1, sizeof(double), hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipStreamSynchronize(s));
+      const double* hv = weighted ? h2[1] : h2[0];
+      const double e = hv[0] == 0.0 ? 1.0 : 1.0 - hv[1] / hv[0];
+      if (e >= target) {
+        nblk_done = blk + 1;
+        break;
+      }
+    }
   }
-  HIP_TRY(launch_finish(w, (int)nblk, s));
+  if (nblk_done == nblk) HIP_TRY(launch_finish(w, (int)nblk, s));
 
-  std::vector<double> f2((size_t)nblk + 1), f2w((size_t)nblk + 1);
-  HIP_TRY(hipMemcpyAsync(f2.data(), w.fro2_hist, sizeof(double) * (nblk + 1), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipMemcpyAsync(f2w.data(), w.fro2w_hist, sizeof(double) * (nblk + 1), hipMemcpyDeviceToHost, s));
+  std::vector<double> f2((size_t)nblk_done + 1), f2w((size_t)nblk_done + 1);
+  HIP_TRY(hipMemcpyAsync(f2.data(), w.fro2_hist, sizeof(double) * (nblk_done + 1), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(f2w.data(), w.fro2w_hist, sizeof(double) * (nblk_done + 1), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (flags[FLAG_SYNC]) return EXTERND_ESYNC;
@@ -314,12 +342,13 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   const double a2 = f2[0], a2w = f2w[0];
   auto E = [&](int64_t b) { return a2 == 0.0 ? 1.0 : 1.0 - f2[(size_t)b] / a2; };
   auto Ew = [&](int64_t b) { return a2w == 0.0 ? 1.0 : 1.0 - f2w[(size_t)b] / a2w; };
-  *energy = E(nblk);
-  if (energy_w) *energy_w = Ew(nblk);
-  for (int64_t b = 0; b < nblk; ++b) {
+  *energy = E(nblk_done);
+  if (energy_w) *energy_w = Ew(nblk_done);
+  for (int64_t b = 0; b < nblk_done; ++b) {
     if (energy_curve) energy_curve[b] = E(b + 1);
     if (energy_w_curve) energy_w_curve[b] = Ew(b + 1);
   }
+  if (k_used) *k_used = nblk_done * b_eff < k ? nblk_done * b_eff : k;
   return EXTERND_OK;
 }
 
@@ -329,6 +358,21 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
                       size_t workspace_bytes, void* stream) {
   return factorize_impl(A, m, n, mu, tau, block, iters, importance, B_packed, C_packed, D, energy, energy_w,
                         energy_curve, energy_w_curve, workspace, workspace_bytes, stream, nullptr);
+}
+
+int externd_factorize_to_energy(const float* A, int64_t m, int64_t n, double mu_max, double target_energy,
+                                double tau, int32_t block, int32_t iters, const float* importance,
+                                uint8_t* B_packed, uint8_t* C_packed, float* D, int64_t* k_used, double* energy,
+                                double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  if (k_used) *k_used = 0;
+  if (isnan(target_energy)) {
+    if (energy) *energy = NAN;
+    return EXTERND_EINVAL;
+  }
+  return factorize_impl(A, m, n, mu_max, tau, block, iters, importance, B_packed, C_packed, D, energy, energy_w,
+                        energy_curve, energy_w_curve, workspace, workspace_bytes, stream, nullptr, target_energy,
+                        k_used);
 }
 
 int externd_factorize_timed(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block,

@@ -76,6 +76,15 @@ def test_argument_errors_before_device_work():
     assert L.externd_step_deflate(dummy, 10, 10, dummy, dummy, None, 4, None, None, dummy, 1 << 30,
                                   None) == binding.EINVAL
     assert L.externd_step_init(dummy, 10, 10, None, 11, 0.7, dummy, dummy, dummy, 1 << 30, None) == binding.EINVAL
+    # energy-target run: the target must be finite and k_used given
+    ku = ctypes.c_int64(7)
+    g = L.externd_factorize_to_energy
+    for target, kptr in [(float("nan"), ctypes.byref(ku)), (float("inf"), ctypes.byref(ku)), (0.9, None)]:
+        assert g(dummy, 10, 10, 1.0, target, 0.7, 1, 1, None, dummy, dummy, dummy, kptr, ctypes.byref(E), None,
+                 None, None, dummy, 1 << 30, None) == binding.EINVAL
+        assert np.isnan(E.value)
+    assert g(None, 10, 10, 1.0, 0.9, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(ku), ctypes.byref(E), None,
+             None, None, dummy, 1 << 30, None) == binding.EINVAL
     assert L.externd_strerror(binding.EHIP).decode().startswith("HIP")
 
 
