@@ -175,6 +175,8 @@ def main():
     ap.add_argument("--collect-traffic", nargs=4, metavar="DB",
                     help="rocprofv3 --pmc databases: FETCH_SIZE, WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE")
     ap.add_argument("--copy-bytes", type=int, default=268435456)
+    ap.add_argument("--apply", action="store_true",
+                    help="time inference with the workload's factorization (externd_apply, nb = 1 and 8)")
     ap.add_argument("--target-energy", type=float, default=None,
                     help="time the energy-target run instead (stop at the first block with E >= target, "
                          "mu of the workload as the maximum)")
@@ -203,6 +205,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.target_energy is not None:
         bench_target(binding, torch, w, args)
+        return
+    if args.apply:
+        bench_apply(binding, torch, w, args)
         return
     A = torch.from_numpy(w.A).to(dev)
     h = torch.from_numpy(w.h).to(dev) if w.h is not None else None
@@ -288,6 +293,40 @@ def main():
         "kernels": per_kernel,
         "cpu_baseline": cpu,
     }
+    print(json.dumps(out), flush=True)
+
+
+def bench_apply(binding, torch, w, args):
+    """Time y = B (diag(D) (C x)) on the packed factors of the workload's
+    factorization (HIP events on the current stream, 50 launches per batch
+    size).  Bytes per call: the packed B and C, D, the inputs and outputs and
+    the k x nb intermediate (written and read)."""
+    m, n = w.A.shape
+    dev = torch.device("cuda:0")
+    A = torch.from_numpy(w.A).to(dev)
+    res = binding.factorize(A, w.mu, w.tau, w.block, w.iters)
+    k = res.k
+    out = {"metric": "inference y = B(diag(D)(C x)) time per call", "unit": "us", "higher_is_better": False,
+           "n_gpus": 1, "data": "synthetic", "config": {"workload": w.name, "m": m, "n": n, "k": k}, "batches": {}}
+    for nb in (1, 8):
+        X = torch.randn((nb, n), dtype=torch.float32, device=dev)
+        ws = torch.empty(binding.lib().externd_apply_workspace_bytes(k, nb), dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            binding.apply(res.B_packed, res.C_packed, res.D, m, n, X, workspace=ws)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 50
+        a.record()
+        for _ in range(reps):
+            binding.apply(res.B_packed, res.C_packed, res.D, m, n, X, workspace=ws)
+        b.record()
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1e3 / reps
+        slots = 1 if nb == 1 else 8
+        nbytes = m * ((k + 3) // 4) + k * ((n + 3) // 4) + 4 * k + 4 * nb * (n + m) + 2 * 4 * k * slots
+        out["batches"][str(nb)] = {"us_per_call": us, "bytes_per_call": nbytes, "GB_s": nbytes / us / 1e3,
+                                   "frac_of_8TBs": nbytes / us / 1e3 / HBM_PEAK_GBS,
+                                   "trit_macs_per_s": nb * k * (m + n) / us / 1e-6}
     print(json.dumps(out), flush=True)
 
 

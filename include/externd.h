@@ -149,6 +149,28 @@ int externd_factorize_to_energy(const float* A, int64_t m, int64_t n, double mu_
                                 double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
+/*
+ * Inference with a factorization (Sec. 2.6 cost model): for each of nb
+ * input vectors x (rows of X), y = B (diag(D) (C x)), computed on the packed
+ * trits with fp32 arithmetic and fp32 accumulation (deterministic order).
+ *
+ *  B_packed   device, m rows of ceil(k/4) bytes; C_packed device, k rows of
+ *             ceil(n/4) bytes; D device fp32[k] -- as written by
+ *             externd_factorize (or _to_energy, whose zero components
+ *             contribute nothing).
+ *  X          device fp32, nb x n row-major.  Y device fp32, nb x m
+ *             row-major (out).
+ *  nb         1 <= nb <= EXTERND_APPLY_MAX_BATCH.
+ *  workspace  device, >= externd_apply_workspace_bytes(k, nb) bytes,
+ *             16-byte aligned (the k x nb intermediate diag(D) C X^T).
+ * Asynchronous on `stream`.  m, n, k <= 2^31 (else EXTERND_EUNSUPPORTED).
+ */
+#define EXTERND_APPLY_MAX_BATCH 8
+size_t externd_apply_workspace_bytes(int64_t k, int32_t nb);  /* 0 on invalid arguments */
+int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n,
+                  int64_t k, const float* X, int32_t nb, float* Y, void* workspace, size_t workspace_bytes,
+                  void* stream);
+
 /* Kernel classes timed by externd_factorize_timed. */
 #define EXTERND_KCLASS_VSTEP   0  /* V-step contraction P = U^T R (+ Gram of U)          */
 #define EXTERND_KCLASS_USTEP   1  /* U-step contraction Q = R diag(h~) V (+ Gram of V)  */

@@ -26,6 +26,8 @@ Sec. 2):
                               mentioned in Sec. 2.2 (test aid only).
 * ``bruteforce_rank1``     -- exhaustive best ternary rank-one fit on tiny
                               matrices (test aid only).
+* ``apply``                -- inference y = B (diag(D) (C x)), the cost
+                              model of Sec. 2.6, written as its definition.
 
 Everything is float64.  Library primitives (matmul, linear solve, stable
 sort) serve as single steps; there is no blocking, fusion or reordering
@@ -80,7 +82,7 @@ __all__ = [
     "ternarize", "ternarize_columns",
     "init_block", "vstep", "ustep", "scale_solve", "deflate",
     "energy", "Factorization",
-    "factorize_sequential", "factorize_block",
+    "factorize_sequential", "factorize_block", "apply",
     "optimal_projection", "bruteforce_rank1", "reconstruct",
 ]
 
@@ -377,6 +379,14 @@ def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int
     E, Ew = energy(R, A_fro2, w if weighted else None, A_col2)
     k_used = min(nblk * b_eff, k)
     return Factorization(B, C, D, E, Ew, curve, curve_w, k, b_eff, 0, 0, fro2, k_used)
+
+
+def apply(B: np.ndarray, C: np.ndarray, D: np.ndarray, X: np.ndarray) -> np.ndarray:
+    """Inference with a factorization, Sec. 2.6: y = B (diag(D) (C x)) for
+    each row x of X (nb x n); returns Y (nb x m).  fp64."""
+    T = np.asarray(C, dtype=np.float64) @ np.asarray(X, dtype=np.float64).T      # k x nb
+    T = np.asarray(D, dtype=np.float64)[:, None] * T
+    return (np.asarray(B, dtype=np.float64) @ T).T
 
 
 def reconstruct(B: np.ndarray, D: np.ndarray, C: np.ndarray) -> np.ndarray:

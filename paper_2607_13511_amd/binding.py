@@ -40,6 +40,9 @@ _SIGNATURES = {
     "externd_factorize_to_energy": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_dbl, _c_i32, _c_i32,
                                                    _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                                    _c_ptr, _c_ptr, _c_size, _c_ptr]),
+    "externd_apply_workspace_bytes": (_c_size, [_c_i64, _c_i32]),
+    "externd_apply": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i64, _c_i64, _c_ptr, _c_i32, _c_ptr,
+                                     _c_ptr, _c_size, _c_ptr]),
     "externd_factorize_timed": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_ptr,
                                                _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                                _c_ptr, _c_size, _c_ptr, _c_ptr]),
@@ -191,6 +194,29 @@ def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=N
     else:
         _check(lib().externd_factorize(*args), "externd_factorize")
     return Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b, kt, k)
+
+
+APPLY_MAX_BATCH = 8   # EXTERND_APPLY_MAX_BATCH
+
+
+def apply(B_packed, C_packed, D, m: int, n: int, X, stream=None, workspace=None):
+    """Y = X (B diag(D) C)^T on the GPU for the nb <= 8 rows of the fp32 CUDA
+    tensor X (nb x n), from packed factors (externd_apply).  Returns Y (nb x m)."""
+    torch = _torch()
+    k = D.shape[0]
+    nb = X.shape[0]
+    _req(X, torch, torch.float32, (nb, n), "X")
+    _req(D, torch, torch.float32, (k,), "D")
+    _req(B_packed, torch, torch.uint8, (m, (k + 3) // 4), "B_packed")
+    _req(C_packed, torch, torch.uint8, (k, (n + 3) // 4), "C_packed")
+    Y = torch.empty((nb, m), dtype=torch.float32, device=X.device)
+    nbytes = lib().externd_apply_workspace_bytes(k, nb)
+    if nbytes == 0:
+        raise ExterndError(EINVAL, "externd_apply_workspace_bytes")
+    ws = workspace if workspace is not None else torch.empty(nbytes, dtype=torch.uint8, device=X.device)
+    _check(lib().externd_apply(_dev_ptr(B_packed), _dev_ptr(C_packed), _dev_ptr(D), m, n, k, _dev_ptr(X), nb,
+                               _dev_ptr(Y), _dev_ptr(ws), ws.numel(), _stream_ptr(torch, stream)), "externd_apply")
+    return Y
 
 
 def factorize_to_energy(A, mu_max: float, target: float, tau: float, block: int, iters: int, h=None,

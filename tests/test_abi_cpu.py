@@ -85,6 +85,15 @@ def test_argument_errors_before_device_work():
         assert np.isnan(E.value)
     assert g(None, 10, 10, 1.0, 0.9, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(ku), ctypes.byref(E), None,
              None, None, dummy, 1 << 30, None) == binding.EINVAL
+    # inference: batch limits, workspace size and alignment
+    ap = L.externd_apply
+    assert L.externd_apply_workspace_bytes(100, 1) == 400 and L.externd_apply_workspace_bytes(100, 3) == 1600
+    assert L.externd_apply_workspace_bytes(100, 9) == 0 and L.externd_apply_workspace_bytes(0, 1) == 0
+    assert ap(dummy, dummy, dummy, 10, 10, 5, dummy, 0, dummy, dummy, 1 << 20, None) == binding.EINVAL
+    assert ap(dummy, dummy, dummy, 10, 10, 5, dummy, 9, dummy, dummy, 1 << 20, None) == binding.EINVAL
+    assert ap(None, dummy, dummy, 10, 10, 5, dummy, 1, dummy, dummy, 1 << 20, None) == binding.EINVAL
+    assert ap(dummy, dummy, dummy, 10, 10, 5, dummy, 1, dummy, dummy, 4, None) == binding.EWORKSPACE
+    assert ap(dummy, dummy, dummy, 10, 10, 5, dummy, 1, dummy, ctypes.c_void_p(260), 1 << 20, None) == binding.EWORKSPACE
     assert L.externd_strerror(binding.EHIP).decode().startswith("HIP")
 
 

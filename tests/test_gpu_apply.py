@@ -1,0 +1,109 @@
+"""GPU parity of inference with a factorization, y = B (diag(D) (C x))
+(externd_apply, Sec. 2.6), against the oracle's fp64 evaluation.
+
+Tolerance, from the arithmetic: the GPU forms t_c = D_c sum_j C_cj x_j and
+y_i = sum_c B_ic t_c in fp32 with fp32 accumulation over n and k terms, so
+|y_gpu - y| <= (n + k + 2) u (|B| (|D| (|C| |x|)))_i with u = 2^-24.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_13511_amd import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+U = 2.0 ** -24
+
+
+def pack_trits(X: np.ndarray) -> np.ndarray:
+    """Rows of trits -> the packed 2-bit format of include/externd.h."""
+    X = np.asarray(X, dtype=np.int8)
+    rows, cols = X.shape
+    code = np.where(X == 0, 0, np.where(X > 0, 1, 3)).astype(np.uint8)
+    pad = (-cols) % 4
+    code = np.concatenate([code, np.zeros((rows, pad), np.uint8)], axis=1).reshape(rows, -1, 4)
+    return (code[:, :, 0] | (code[:, :, 1] << 2) | (code[:, :, 2] << 4) | (code[:, :, 3] << 6)).astype(np.uint8)
+
+
+def bound(B, C, D, X):
+    n, k = C.shape[1], C.shape[0]
+    a = np.abs(B).astype(np.float64) @ (np.abs(D)[:, None] * (np.abs(C).astype(np.float64) @ np.abs(X).T))
+    return (n + k + 2) * U * a.T
+
+
+@pytest.fixture(scope="module")
+def ext():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_13511_amd import binding
+    binding.lib()
+    return binding
+
+
+def run(ext, B, C, D, X):
+    m, k = B.shape
+    n = C.shape[1]
+    Bp = torch.from_numpy(pack_trits(B)).cuda()
+    Cp = torch.from_numpy(pack_trits(C)).cuda()
+    Y = ext.apply(Bp, Cp, torch.from_numpy(D.astype(np.float32)).cuda(), m, n,
+                  torch.from_numpy(X.astype(np.float32)).cuda())
+    torch.cuda.synchronize()
+    return Y.cpu().numpy().astype(np.float64)
+
+
+def test_pack_roundtrip(ext):
+    rng = np.random.default_rng(3)
+    X = rng.integers(-1, 2, size=(7, 23)).astype(np.int8)
+    np.testing.assert_array_equal(ext.unpack_trits(pack_trits(X), 23), X)
+
+
+@pytest.mark.parametrize("m,n,k,nb", [(37, 29, 53, 1), (37, 29, 53, 3), (64, 64, 64, 8), (1000, 777, 1500, 1),
+                                      (1000, 777, 1500, 5), (9, 3, 2, 2)])
+def test_apply_random_factors(ext, m, n, k, nb):
+    print(f"[apply] random m={m} n={n} k={k} nb={nb}", flush=True)
+    rng = np.random.default_rng(m + n + k + nb)
+    B = rng.integers(-1, 2, size=(m, k)).astype(np.int8)
+    C = rng.integers(-1, 2, size=(k, n)).astype(np.int8)
+    D = rng.standard_normal(k).astype(np.float32).astype(np.float64)
+    X = rng.standard_normal((nb, n)).astype(np.float32).astype(np.float64)
+    Y = run(ext, B, C, D, X)
+    ref = oracle.apply(B, C, D, X)
+    assert np.all(np.abs(Y - ref) <= bound(B, C, D, X))
+
+
+def test_apply_factorization(ext):
+    A = synth.small("t4_rowscale", 384, 320, 21)
+    res = ext.factorize(torch.from_numpy(A).cuda(), 2.0, 1.0, 16, 8)
+    torch.cuda.synchronize()
+    B = ext.unpack_trits(res.B_packed.cpu().numpy(), res.k)
+    C = ext.unpack_trits(res.C_packed.cpu().numpy(), 320)
+    D = res.D.cpu().numpy().astype(np.float64)
+    X = np.random.default_rng(5).standard_normal((4, 320)).astype(np.float32).astype(np.float64)
+    Y = ext.apply(res.B_packed, res.C_packed, res.D, 384, 320, torch.from_numpy(X.astype(np.float32)).cuda())
+    torch.cuda.synchronize()
+    Y = Y.cpu().numpy().astype(np.float64)
+    ref = oracle.apply(B, C, D, X)
+    assert np.all(np.abs(Y - ref) <= bound(B, C, D, X))
+    # and the product approximates A x as well as the factorization approximates A
+    err = np.linalg.norm(Y - X @ A.T.astype(np.float64)) / np.linalg.norm(X @ A.T.astype(np.float64))
+    assert err < 2.0 * np.sqrt(1.0 - res.E) + 1e-3
+
+
+def test_apply_fullsize(ext):
+    w = synth.down9728()
+    m, n = w.A.shape
+    print("[apply] down9728 full size", flush=True)
+    res = ext.factorize(torch.from_numpy(w.A).cuda(), w.mu, w.tau, w.block, w.iters)
+    torch.cuda.synchronize()
+    B = ext.unpack_trits(res.B_packed.cpu().numpy(), res.k)
+    C = ext.unpack_trits(res.C_packed.cpu().numpy(), n)
+    D = res.D.cpu().numpy().astype(np.float64)
+    for nb in (1, 8):
+        X = np.random.default_rng(nb).standard_normal((nb, n)).astype(np.float32).astype(np.float64)
+        Y = ext.apply(res.B_packed, res.C_packed, res.D, m, n, torch.from_numpy(X.astype(np.float32)).cuda())
+        torch.cuda.synchronize()
+        Y = Y.cpu().numpy().astype(np.float64)
+        ref = oracle.apply(B, C, D, X)
+        assert np.all(np.abs(Y - ref) <= bound(B, C, D, X))
