@@ -26,6 +26,9 @@ Sec. 2):
                               mentioned in Sec. 2.2 (test aid only).
 * ``bruteforce_rank1``     -- exhaustive best ternary rank-one fit on tiny
                               matrices (test aid only).
+* ``refine``, ``refine_block`` -- refinement sweeps of Sec. 2.4: each
+                              block in turn is added back to the residual,
+                              fitted again and deflated again.
 * ``apply``                -- inference y = B (diag(D) (C x)), the cost
                               model of Sec. 2.6, written as its definition.
 
@@ -83,6 +86,7 @@ __all__ = [
     "init_block", "vstep", "ustep", "scale_solve", "deflate",
     "energy", "Factorization",
     "factorize_sequential", "factorize_block", "apply",
+    "refine_block", "refine", "Refinement",
     "optimal_projection", "bruteforce_rank1", "reconstruct",
 ]
 
@@ -379,6 +383,99 @@ def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int
     E, Ew = energy(R, A_fro2, w if weighted else None, A_col2)
     k_used = min(nblk * b_eff, k)
     return Factorization(B, C, D, E, Ew, curve, curve_w, k, b_eff, 0, 0, fro2, k_used)
+
+
+def _weighted_fro2(R: np.ndarray, w: np.ndarray) -> float:
+    """sum_j h~_j ||R[:, j]||^2 (w = ones gives ||R||_F^2)."""
+    return float(np.dot(w, np.sum(R * R, axis=0)))
+
+
+def refine_block(R: np.ndarray, U: np.ndarray, V: np.ndarray, d: np.ndarray, w: np.ndarray,
+                 tau: float, iters: int):
+    """One revisit of a refinement sweep (Sec. 2.4; reading R11).
+
+    R is the residual with the block (U m x bb, V n x bb, scales d) already
+    deflated.  R' = R + U diag(d) V^T; the block ALS of Eq. (3) runs
+    ``iters`` times from the current U; scales from Eq. (4).  The new block
+    is kept when it removes strictly more of the objective from R' than the
+    old one.  Returns (R_new, U, V, d, accepted, old_gain, new_gain).
+    """
+    Rp = R + (U.astype(np.float64) * d[None, :]) @ V.astype(np.float64).T
+    old_gain = _weighted_fro2(Rp, w) - _weighted_fro2(R, w)
+    Un = U
+    Vn = V
+    Q = np.zeros((R.shape[0], U.shape[1]))
+    for _ in range(iters):
+        Vn, _ = vstep(Rp, Un, tau)
+        Un, Q, _ = ustep(Rp, Vn, w, tau)
+    dn = scale_solve(Un, Vn, Q, w)
+    # energy the new block removes from R': 2 d^T g - d^T M d, with
+    # g = diag(U^T R' H V) and M = (U^T U) o (V^T H V) as in Eq. (4)
+    Uf = Un.astype(np.float64)
+    Vf = Vn.astype(np.float64)
+    M = (Uf.T @ Uf) * (Vf.T @ (w[:, None] * Vf))
+    g = np.sum(Uf * Q, axis=0)
+    new_gain = float(2.0 * (dn @ g) - dn @ M @ dn)
+    if new_gain > old_gain:
+        return deflate(Rp, Un, Vn, dn), Un, Vn, dn, True, old_gain, new_gain
+    return R, U, V, d, False, old_gain, new_gain
+
+
+@dataclass
+class Refinement:
+    B: np.ndarray
+    C: np.ndarray
+    D: np.ndarray
+    E: float
+    E_w: Optional[float]
+    sweep_curve: np.ndarray            # E after each sweep
+    sweep_curve_w: Optional[np.ndarray]
+    accepted: int                      # revisits that replaced their block
+    revisits: int
+
+
+def refine(A: np.ndarray, F: Factorization, tau: float, iters: int, sweeps: int,
+           h: Optional[np.ndarray] = None) -> Refinement:
+    """Refinement sweeps after a block factorization F of A (Sec. 2.4; R11).
+
+    Each sweep revisits the blocks of F (width F.block, the last one
+    partial) in order with ``refine_block``; R starts as A - B diag(D) C.
+    """
+    A = np.asarray(A, dtype=np.float64)
+    m, n = A.shape
+    w = normalized_weights(h, n)
+    weighted = h is not None
+    B = F.B.copy()
+    C = F.C.copy()
+    D = np.asarray(F.D, dtype=np.float64).copy()
+    k, b = F.k, F.block
+    A_col2 = np.sum(A * A, axis=0)
+    A_fro2 = float(np.sum(A_col2))
+    R = A - reconstruct(B, D, C)
+    nblk = (k + b - 1) // b
+    curve = np.zeros(sweeps)
+    curve_w = np.zeros(sweeps) if weighted else None
+    accepted = 0
+    for sw in range(sweeps):
+        for blk in range(nblk):
+            c0 = blk * b
+            bb = min(b, k - c0)
+            R, U, V, d, acc, _, _ = refine_block(R, B[:, c0:c0 + bb], C[c0:c0 + bb, :].T, D[c0:c0 + bb], w,
+                                                 tau, iters)
+            if acc:
+                accepted += 1
+                B[:, c0:c0 + bb] = U
+                C[c0:c0 + bb, :] = V.T
+                D[c0:c0 + bb] = d
+        E, Ew = energy(R, A_fro2, w if weighted else None, A_col2)
+        curve[sw] = E
+        if weighted:
+            curve_w[sw] = Ew
+    if sweeps:
+        E, Ew = curve[-1], (curve_w[-1] if weighted else None)
+    else:
+        E, Ew = energy(R, A_fro2, w if weighted else None, A_col2)
+    return Refinement(B, C, D, E, Ew, curve, curve_w, accepted, sweeps * nblk)
 
 
 def apply(B: np.ndarray, C: np.ndarray, D: np.ndarray, X: np.ndarray) -> np.ndarray:
