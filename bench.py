@@ -177,6 +177,8 @@ def main():
     ap.add_argument("--copy-bytes", type=int, default=268435456)
     ap.add_argument("--apply", action="store_true",
                     help="time inference with the workload's factorization (externd_apply, nb = 1 and 8)")
+    ap.add_argument("--sweeps", type=int, default=None,
+                    help="time externd_factorize_refined with this many refinement sweeps instead")
     ap.add_argument("--target-energy", type=float, default=None,
                     help="time the energy-target run instead (stop at the first block with E >= target, "
                          "mu of the workload as the maximum)")
@@ -203,6 +205,8 @@ def main():
     w = workload(args.workload)
     m, n = w.A.shape
     dev = torch.device("cuda:0")
+    if args.sweeps is not None:
+        return bench_sweeps(binding, torch, w, args)
     if args.target_energy is not None:
         bench_target(binding, torch, w, args)
         return
@@ -354,6 +358,36 @@ def bench_target(binding, torch, w, args):
                    "block": res.block, "iters": w.iters, "importance": w.h is not None},
         "k_used": res.k_used, "mu_effective": res.k_used / min(m, n), "energy": res.E, "energy_w": res.E_w,
         "components_per_s": res.k_used / sec,
+    }), flush=True)
+
+
+def bench_sweeps(binding, torch, w, args):
+    """Time externd_factorize_refined on the workload: extraction plus
+    ``--sweeps`` refinement sweeps, with the energy before and after."""
+    m, n = w.A.shape
+    dev = torch.device("cuda:0")
+    A = torch.from_numpy(w.A).to(dev)
+    h = torch.from_numpy(w.h).to(dev) if w.h is not None else None
+    k = binding.rank(m, n, w.mu)
+    ws = torch.empty(binding.workspace_bytes(m, n, k), dtype=torch.uint8, device=dev)
+    for _ in range(args.warmup):
+        binding.factorize_refined(A, w.mu, w.tau, w.block, w.iters, args.sweeps, h=h, workspace=ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        res = binding.factorize_refined(A, w.mu, w.tau, w.block, w.iters, args.sweeps, h=h, workspace=ws)
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.steps
+    F = res.factorization
+    print(json.dumps({
+        "metric": "sec/matrix with refinement sweeps", "value": sec, "unit": "s", "higher_is_better": False,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "data": "synthetic",
+        "config": {"workload": w.name, "mu": w.mu, "tau": w.tau, "block": F.block, "iters": w.iters,
+                   "sweeps": args.sweeps, "importance": w.h is not None},
+        "energy_extraction": float(F.curve[-1]), "energy_w_extraction": float(F.curve_w[-1]),
+        "sweep_energy": [float(x) for x in res.sweep_curve],
+        "sweep_energy_w": [float(x) for x in res.sweep_curve_w],
+        "accepted": res.accepted, "revisits": res.revisits,
     }), flush=True)
 
 

@@ -150,6 +150,39 @@ int externd_factorize_to_energy(const float* A, int64_t m, int64_t n, double mu_
                                 size_t workspace_bytes, void* stream);
 
 /*
+ * externd_factorize_refined -- externd_factorize followed by refinement
+ * sweeps (Sec. 2.4: after extraction each block is added back to the
+ * residual, fitted again and deflated again, which raises energy
+ * monotonically).
+ *
+ * A sweep revisits the blocks in extraction order.  A revisit forms
+ * R' = R + U diag(d) V^T, runs `iters` V-step/U-step iterations of Eq. (3)
+ * warm-started from the block's current U, and solves Eq. (4) for the new
+ * scales d'.  The new block replaces the old one (in B_packed, C_packed
+ * and D) only when the objective it removes from R', 2 d'^T g' - d'^T M' d'
+ * (weighted when importance is given), exceeds what the old block removes,
+ * ||R'||^2 - ||R||^2; otherwise the old block is deflated again and the
+ * outputs keep it.  No revisit therefore increases the objective beyond the
+ * rounding of the fp32 residual.
+ *
+ *  sweeps          >= 0 (0 gives the result of externd_factorize).
+ *  energy, energy_w  host, out: after the last sweep.
+ *  energy_curve, energy_w_curve  host, out (may be NULL): the extraction's
+ *                  per-block curve, as in externd_factorize.
+ *  sweep_energy, sweep_energy_w  host, out (may be NULL): E and weighted E
+ *                  after each sweep (`sweeps` doubles each).
+ *  accepted        host, out (may be NULL): revisits that replaced their
+ *                  block, out of sweeps * ceil(k / b_eff).
+ * Other arguments, workspace size, status codes and synchronisation as
+ * externd_factorize.  Each sweep adds one small device-to-host read.
+ */
+int externd_factorize_refined(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block,
+                              int32_t iters, int32_t sweeps, const float* importance, uint8_t* B_packed,
+                              uint8_t* C_packed, float* D, double* energy, double* energy_w, double* energy_curve,
+                              double* energy_w_curve, double* sweep_energy, double* sweep_energy_w,
+                              int64_t* accepted, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Inference with a factorization (Sec. 2.6 cost model): for each of nb
  * input vectors x (rows of X), y = B (diag(D) (C x)), computed on the packed
  * trits with fp32 arithmetic and fp32 accumulation (deterministic order).

@@ -40,6 +40,9 @@ _SIGNATURES = {
     "externd_factorize_to_energy": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_dbl, _c_i32, _c_i32,
                                                    _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                                    _c_ptr, _c_ptr, _c_size, _c_ptr]),
+    "externd_factorize_refined": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_i32,
+                                                 _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
+                                                 _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr]),
     "externd_apply_workspace_bytes": (_c_size, [_c_i64, _c_i32]),
     "externd_apply": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i64, _c_i64, _c_ptr, _c_i32, _c_ptr,
                                      _c_ptr, _c_size, _c_ptr]),
@@ -252,6 +255,50 @@ def factorize_to_energy(A, mu_max: float, target: float, tau: float, block: int,
         "externd_factorize_to_energy")
     nb = -(-ku.value // b)
     return Factorization(Bp, Cp, D, E.value, Ew.value, curve[:nb], curve_w[:nb], k, b, None, int(ku.value))
+
+
+@dataclass
+class Refined:
+    factorization: Factorization       # final factors; E, E_w after the last sweep; extraction curve
+    sweep_curve: np.ndarray            # E after each sweep
+    sweep_curve_w: np.ndarray          # weighted E after each sweep
+    accepted: int                      # revisits that replaced their block
+    revisits: int
+
+
+def factorize_refined(A, mu: float, tau: float, block: int, iters: int, sweeps: int, h=None, stream=None,
+                      workspace=None) -> Refined:
+    """Factorize A, then run ``sweeps`` refinement sweeps over its blocks
+    (externd_factorize_refined)."""
+    torch = _torch()
+    m, n = A.shape
+    _req(A, torch, torch.float32, (m, n), "A")
+    if h is not None:
+        _req(h, torch, torch.float32, (n,), "h")
+    k = rank(m, n, mu)
+    if k < 1:
+        raise ExterndError(EINVAL, "rank")
+    b = effective_block(m, n, block)
+    nblk = -(-k // b)
+    dev = A.device
+    Bp = torch.empty((m, (k + 3) // 4), dtype=torch.uint8, device=dev)
+    Cp = torch.empty((k, (n + 3) // 4), dtype=torch.uint8, device=dev)
+    D = torch.empty((k,), dtype=torch.float32, device=dev)
+    ws = workspace if workspace is not None else _workspace(torch, m, n, k, dev)
+    E = ctypes.c_double(0.0)
+    Ew = ctypes.c_double(0.0)
+    acc = ctypes.c_int64(0)
+    curve = np.zeros(nblk, dtype=np.float64)
+    curve_w = np.zeros(nblk, dtype=np.float64)
+    sc = np.zeros(max(sweeps, 1), dtype=np.float64)
+    scw = np.zeros(max(sweeps, 1), dtype=np.float64)
+    _check(lib().externd_factorize_refined(
+        _dev_ptr(A), m, n, mu, tau, block, iters, sweeps, _dev_ptr(h) if h is not None else None,
+        _dev_ptr(Bp), _dev_ptr(Cp), _dev_ptr(D), ctypes.byref(E), ctypes.byref(Ew),
+        curve.ctypes.data, curve_w.ctypes.data, sc.ctypes.data, scw.ctypes.data, ctypes.byref(acc),
+        _dev_ptr(ws), ws.numel(), _stream_ptr(torch, stream)), "externd_factorize_refined")
+    F = Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b, None, k)
+    return Refined(F, sc[:sweeps], scw[:sweeps], int(acc.value), sweeps * nblk)
 
 
 def step_init(R, bb: int, tau: float, h=None, stream=None):

@@ -257,19 +257,76 @@ size_t externd_workspace_bytes(int64_t m, int64_t n, int64_t k) {
   return externd::workspace_bytes(m, n, k);
 }
 
+// Refinement sweeps after extraction (Sec. 2.4): every block in turn is
+// added back to R, fitted again from its current U, and the better of the
+// old and the new block (by the objective removed from R + U diag(d) V^T)
+// is deflated.  The per-pass history slots (residual bound, ||R||^2) are
+// used as a ring of nblk_cap >= 3 entries from slot S on; the extraction's
+// energy curve has been read before.
+struct SweepOut {
+  double* energy;     // host, sweeps entries (may be null)
+  double* energy_w;   // host, sweeps entries (may be null)
+  double fro2_last, fro2w_last;
+};
+static hipError_t run_sweeps(const Ws& w, int64_t k, int b_eff, double tau, int32_t iters, int32_t sweeps,
+                             bool weighted, uint8_t* B_packed, uint8_t* C_packed, float* D, int S, double a2,
+                             double a2w, SweepOut& out, hipStream_t s, Timer* tm) {
+  const int64_t nblk = (k + b_eff - 1) / b_eff;
+  const int cap = w.nblk_cap;
+  hipError_t e;
+#define SWEEP_TRY(expr)          \
+  do {                           \
+    e = (expr);                  \
+    if (e != hipSuccess) return e; \
+  } while (0)
+  for (int sw = 0; sw < sweeps; ++sw) {
+    for (int64_t blk = 0; blk < nblk; ++blk) {
+      const int64_t c0 = blk * b_eff;
+      const int bb = (int)((k - c0) < b_eff ? (k - c0) : b_eff);
+      const int S1 = (S + 1) % cap, S2 = (S + 2) % cap;
+      SWEEP_TRY(launch_revisit_load(w, B_packed, C_packed, D, c0, bb, k, S1, S2, s));
+      SWEEP_TRY(launch_deflate_slot(w, S1, s, tm));  // R' = R + U diag(d) V^T
+      SWEEP_TRY(launch_finish(w, S1, s));
+      for (int it = 0; it < iters; ++it) {
+        SWEEP_TRY(launch_vstep(w, S1, bb, tau, s, tm));
+        SWEEP_TRY(launch_ustep(w, S1, bb, tau, weighted, it == iters - 1, s, tm));
+      }
+      SWEEP_TRY(launch_gram_acc(w, 0, s));
+      SWEEP_TRY(launch_revisit_decide(w, bb, D + c0, weighted, S, S1, s));
+      SWEEP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s, true));
+      SWEEP_TRY(launch_deflate_slot(w, S2, s, tm));
+      SWEEP_TRY(launch_finish(w, S2, s));
+      S = S2;
+    }
+    double f[2];
+    SWEEP_TRY(hipMemcpyAsync(&f[0], w.fro2_hist + S, sizeof(double), hipMemcpyDeviceToHost, s));
+    SWEEP_TRY(hipMemcpyAsync(&f[1], w.fro2w_hist + S, sizeof(double), hipMemcpyDeviceToHost, s));
+    SWEEP_TRY(hipStreamSynchronize(s));
+    out.fro2_last = f[0];
+    out.fro2w_last = f[1];
+    if (out.energy) out.energy[sw] = a2 == 0.0 ? 1.0 : 1.0 - f[0] / a2;
+    if (out.energy_w) out.energy_w[sw] = a2w == 0.0 ? 1.0 : 1.0 - f[1] / a2w;
+  }
+#undef SWEEP_TRY
+  return hipSuccess;
+}
+
 // target: NaN for the full run; else stop after the first block whose
 // energy (E, or E_w with weights) reaches it, reporting *k_used.
+// sweeps: refinement sweeps after a full run (0 = none).
 static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
                           const float* importance, uint8_t* B_packed, uint8_t* C_packed, float* D, double* energy,
                           double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
                           size_t workspace_bytes, void* stream, externd_kernel_times* times,
-                          double target = NAN, int64_t* k_used = nullptr) {
+                          double target = NAN, int64_t* k_used = nullptr, int32_t sweeps = 0,
+                          double* sweep_energy = nullptr, double* sweep_energy_w = nullptr,
+                          int64_t* accepted = nullptr) {
   if (energy) *energy = NAN;
   if (energy_w) *energy_w = NAN;
   if (!A || !B_packed || !C_packed || !D || !energy || !workspace) return EXTERND_EINVAL;
-  if (m < 1 || n < 1 || !isfinite(tau) || tau < 0.0 || block < 1 || iters < 1) return EXTERND_EINVAL;
+  if (m < 1 || n < 1 || !isfinite(tau) || tau < 0.0 || block < 1 || iters < 1 || sweeps < 0) return EXTERND_EINVAL;
   const bool stop_at_target = !isnan(target);
-  if (stop_at_target && (!isfinite(target) || !k_used)) return EXTERND_EINVAL;
+  if (stop_at_target && (!isfinite(target) || !k_used || sweeps > 0)) return EXTERND_EINVAL;
   const int64_t k = externd_rank(m, n, mu);
   if (k < 1) return EXTERND_EINVAL;
   if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
@@ -332,9 +389,17 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   std::vector<double> f2((size_t)nblk_done + 1), f2w((size_t)nblk_done + 1);
   HIP_TRY(hipMemcpyAsync(f2.data(), w.fro2_hist, sizeof(double) * (nblk_done + 1), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipMemcpyAsync(f2w.data(), w.fro2w_hist, sizeof(double) * (nblk_done + 1), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  SweepOut so{sweep_energy, sweep_energy_w, f2[(size_t)nblk_done], f2w[(size_t)nblk_done]};
+  if (sweeps > 0)
+    HIP_TRY(run_sweeps(w, k, b_eff, tau, iters, sweeps, weighted, B_packed, C_packed, D, (int)nblk, f2[0], f2w[0], so,
+                       s, tm));
+  unsigned n_acc = 0;
+  HIP_TRY(hipMemcpyAsync(&n_acc, w.counters + CNT_ACCEPTED, sizeof(unsigned), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (flags[FLAG_SYNC]) return EXTERND_ESYNC;
+  if (accepted) *accepted = (int64_t)n_acc;
   if (tm) {
     HIP_TRY(tm->collect(times->total_ms, times->launches, EXTERND_KCLASS_COUNT));
     for (int c = 0; c < EXTERND_KCLASS_COUNT; ++c) times->issued[c] = tm->seen[c];
@@ -342,8 +407,8 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   const double a2 = f2[0], a2w = f2w[0];
   auto E = [&](int64_t b) { return a2 == 0.0 ? 1.0 : 1.0 - f2[(size_t)b] / a2; };
   auto Ew = [&](int64_t b) { return a2w == 0.0 ? 1.0 : 1.0 - f2w[(size_t)b] / a2w; };
-  *energy = E(nblk_done);
-  if (energy_w) *energy_w = Ew(nblk_done);
+  *energy = a2 == 0.0 ? 1.0 : 1.0 - so.fro2_last / a2;
+  if (energy_w) *energy_w = a2w == 0.0 ? 1.0 : 1.0 - so.fro2w_last / a2w;
   for (int64_t b = 0; b < nblk_done; ++b) {
     if (energy_curve) energy_curve[b] = E(b + 1);
     if (energy_w_curve) energy_w_curve[b] = Ew(b + 1);
@@ -373,6 +438,16 @@ int externd_factorize_to_energy(const float* A, int64_t m, int64_t n, double mu_
   return factorize_impl(A, m, n, mu_max, tau, block, iters, importance, B_packed, C_packed, D, energy, energy_w,
                         energy_curve, energy_w_curve, workspace, workspace_bytes, stream, nullptr, target_energy,
                         k_used);
+}
+
+int externd_factorize_refined(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block,
+                              int32_t iters, int32_t sweeps, const float* importance, uint8_t* B_packed,
+                              uint8_t* C_packed, float* D, double* energy, double* energy_w, double* energy_curve,
+                              double* energy_w_curve, double* sweep_energy, double* sweep_energy_w,
+                              int64_t* accepted, void* workspace, size_t workspace_bytes, void* stream) {
+  return factorize_impl(A, m, n, mu, tau, block, iters, importance, B_packed, C_packed, D, energy, energy_w,
+                        energy_curve, energy_w_curve, workspace, workspace_bytes, stream, nullptr, NAN, nullptr,
+                        sweeps, sweep_energy, sweep_energy_w, accepted);
 }
 
 int externd_factorize_timed(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block,

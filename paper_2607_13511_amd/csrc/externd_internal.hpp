@@ -36,7 +36,12 @@ constexpr int TERN_CHUNK = 640;
 // Index of counters in Ws::counters (each used by one kernel family, reset
 // to zero by the workgroup that consumes it).
 // CNT_READY_*: G^{-1} of the V-step (U Gram) / U-step (V Gram) is stored.
-enum Counter { CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2, CNT_READY_U = 3, CNT_READY_V = 4, CNT_COUNT = 8 };
+// CNT_DECISION: the last refinement revisit kept its new block (1) or not;
+// CNT_ACCEPTED: revisits of the call that kept the new block.
+enum Counter {
+  CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2, CNT_READY_U = 3, CNT_READY_V = 4,
+  CNT_DECISION = 5, CNT_ACCEPTED = 6, CNT_COUNT = 8
+};
 // Flags written by the device, read by the host.
 enum Flag { FLAG_NONFINITE = 0, FLAG_BADWEIGHT = 1, FLAG_SYNC = 2, FLAG_COUNT = 4 };
 
@@ -137,10 +142,24 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
                         Timer* t = nullptr);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
 // The end of a block: scale solve, row-major factor copies, packed B and C, D.
+// revisit: the scales were settled by launch_revisit_decide, whose decision
+// selects the new block (written out) or the old one (operands rebuilt from
+// the packed outputs).
 hipError_t launch_block_out(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
-                            hipStream_t s);
-// transposes: rebuild the row-major factor copies from Ut/Vt first (step entry point).
+                            hipStream_t s, bool revisit = false);
+// transposes: rebuild the row-major factor copies from Ut/Vt first (step
+// entry point).  Writes max|R| of the result into slot blk + 1.
 hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, Timer* t = nullptr);
+hipError_t launch_deflate_slot(const Ws& w, int out_slot, hipStream_t s, Timer* t = nullptr);
+// Refinement revisit of the block at columns c0 .. c0+bb-1: decode it from
+// the packed outputs (clearing residual-bound slots slot1 and slot2), and
+// after the fit choose between the new and the old block by the objective
+// each removes (history slots slot_prev: before the add-back, slot_added:
+// after it).
+hipError_t launch_revisit_load(const Ws& w, const uint8_t* Bp, const uint8_t* Cp, const float* D, int64_t c0, int bb,
+                               int64_t k, int slot1, int slot2, hipStream_t s);
+hipError_t launch_revisit_decide(const Ws& w, int bb, float* D_block, bool weighted, int slot_prev, int slot_added,
+                                 hipStream_t s);
 // step-entry helpers
 hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len, int64_t len_pad,
                               int bb, hipStream_t s);

@@ -1406,9 +1406,13 @@ __global__ __launch_bounds__(NT) void k_transpose8(const int8_t* __restrict__ Xt
 // d = M^{-1} g.  grid: one WG; U^T U is the accumulated Gram of the block's
 // final U.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void scale_solve(int* gacc, int bb, const double* __restrict__ gramV,
-                                            const double* __restrict__ gvec, double* dvec, float* dF, float* Dout,
-                                            double* Gs /* LDS 4096 */, double* colbuf /* LDS 1024 */) {
+// Returns (want_gain, all threads) the objective the block removes from
+// the residual, 2 d^T g - d^T M d, which equals d^T g + delta ||d||^2 when
+// (M + delta I) d = g.
+__device__ __forceinline__ double scale_solve(int* gacc, int bb, const double* __restrict__ gramV,
+                                              const double* __restrict__ gvec, double* dvec, float* dF, float* Dout,
+                                              double* Gs /* LDS 4096 */, double* colbuf /* LDS 1024 */,
+                                              bool want_gain = false) {
   __shared__ double s_trb[16];
   take_gram(gacc, Gs);
   const int t = threadIdx.x;
@@ -1424,7 +1428,7 @@ __device__ __forceinline__ void scale_solve(int* gacc, int bb, const double* __r
       dF[t] = 0.0f;
       if (Dout && t < bb) Dout[t] = 0.0f;
     }
-    return;
+    return 0.0;
   }
   const double delta = EXTERND_SCALE_GUARD_REL * tr / (double)bb;
   if (t < bb) Gs[t * 64 + t] += delta;
@@ -1439,6 +1443,7 @@ __device__ __forceinline__ void scale_solve(int* gacc, int bb, const double* __r
     s_g[t] = g;
   }
   __syncthreads();
+  double gain = 0.0;
   if (t < BBP) {
     double d = 0.0;
     if (t < bb)
@@ -1446,7 +1451,9 @@ __device__ __forceinline__ void scale_solve(int* gacc, int bb, const double* __r
     dvec[t] = d;
     dF[t] = (float)d;
     if (Dout && t < bb) Dout[t] = (float)d;
+    gain = d * s_g[t] + delta * d * d;
   }
+  return want_gain ? block_sum_d(gain, s_trb) : 0.0;
 }
 
 __global__ __launch_bounds__(NT) void k_scale(int* gacc, int bb, const double* __restrict__ gramV,
@@ -1944,17 +1951,28 @@ __device__ __forceinline__ unsigned trit_code(int8_t t) { return t == 0 ? 0u : (
 // read-modified-written, padding bits beyond k cleared).
 // grid: 1 + m_pad/32 (U tiles) + n_pad/32 (V tiles).
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ int8_t trit_decode(unsigned byte, int64_t pos) {
+  const unsigned code = (byte >> (2 * (int)(pos & 3))) & 3u;
+  return (int8_t)(code == 1u ? 1 : (code == 3u ? -1 : 0));
+}
+
+// decision: null during extraction.  In a refinement revisit it is the
+// device word set by k_revisit_decide: WG 0 then does nothing (the scales
+// are settled), and when the old block is kept (decision 0) the tiles
+// rebuild the deflation operands from the packed B and C, which stay as
+// they are.
 __global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const double* __restrict__ gramV,
                                                   const double* __restrict__ gvec, double* dvec, float* dF,
                                                   float* Dout, const int8_t* __restrict__ Ut, int8_t* __restrict__ Ur,
                                                   unsigned short* __restrict__ Ub, int64_t m, int64_t m_pad,
                                                   int64_t c0, int64_t k, uint8_t* __restrict__ Bp,
                                                   const int8_t* __restrict__ Vt, int8_t* __restrict__ Vr, int64_t n,
-                                                  int64_t n_pad, uint8_t* __restrict__ Cp) {
+                                                  int64_t n_pad, uint8_t* __restrict__ Cp,
+                                                  const unsigned* __restrict__ decision) {
   __shared__ double Gs[4096];
   __shared__ double colbuf[1024];
   if (blockIdx.x == 0) {
-    scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf);
+    if (!decision) scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf);
     return;
   }
   int8_t (*tile)[BBP + 4] = (int8_t (*)[BBP + 4])Gs;  // 32 x 68 bytes
@@ -1963,9 +1981,27 @@ __global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const doubl
   const int64_t L = isU ? m_pad : n_pad;
   const int8_t* Xt = isU ? Ut : Vt;
   const int64_t j0 = (int64_t)(isU ? blockIdx.x - 1 : blockIdx.x - 1 - nut) * 32;
-  for (int e = threadIdx.x; e < BBP * 32; e += NT) {
-    const int c = e >> 5, jj = e & 31;
-    tile[jj][c] = Xt[(int64_t)c * L + j0 + jj];
+  const bool keep_old = decision && *decision == 0u;
+  if (keep_old) {
+    const int64_t pitchB = (k + 3) >> 2, pitchC = (n + 3) >> 2;
+    for (int e = threadIdx.x; e < BBP * 32; e += NT) {
+      const int c = e >> 5, jj = e & 31;
+      const int64_t j = j0 + jj;
+      int8_t t = 0;
+      if (c < bb) {
+        if (isU) {
+          if (j < m) t = trit_decode(Bp[j * pitchB + ((c0 + c) >> 2)], c0 + c);
+        } else if (j < n) {
+          t = trit_decode(Cp[(c0 + c) * pitchC + (j >> 2)], j);
+        }
+      }
+      tile[jj][c] = t;
+    }
+  } else {
+    for (int e = threadIdx.x; e < BBP * 32; e += NT) {
+      const int c = e >> 5, jj = e & 31;
+      tile[jj][c] = Xt[(int64_t)c * L + j0 + jj];
+    }
   }
   __syncthreads();
   int8_t* Xr = isU ? Ur : Vr;
@@ -1975,6 +2011,7 @@ __global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const doubl
     Xr[(j0 + jj) * BBP + c] = t;
     if (isU) Ub[(j0 + jj) * BBP + c] = t == 0 ? 0 : (t > 0 ? 0x3F80u : 0xBF80u);
   }
+  if (keep_old) return;
   if (isU) {
     // rows j0 .. j0+31 of B, byte range covering columns [c0, c0 + bb)
     const int64_t pitch = (k + 3) >> 2;
@@ -2010,6 +2047,95 @@ __global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const doubl
       }
       Cp[(c0 + c) * pitch + q] = (uint8_t)byte;
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Refinement sweeps (Sec. 2.4): a revisit adds the block back to R, fits it
+// again from its current U and deflates the better of the old and the new
+// block.
+// ---------------------------------------------------------------------------
+// Start of a revisit: the block's factors decoded from the packed B and C
+// into the workspace layouts (U as the warm start and, with V, as the
+// add-back operands), add-back scales -D, and the residual-bound slots the
+// revisit's two deflations write cleared.
+// grid: 1 + m_pad/32 (U tiles) + n_pad/32 (V tiles).
+__global__ __launch_bounds__(NT) void k_revisit_load(const uint8_t* __restrict__ Bp, const uint8_t* __restrict__ Cp,
+                                                     const float* __restrict__ D, int64_t c0, int bb, int64_t k,
+                                                     int64_t m, int64_t m_pad, int64_t n, int64_t n_pad,
+                                                     int8_t* __restrict__ Ut, int8_t* __restrict__ Ur,
+                                                     unsigned short* __restrict__ Ub, int8_t* __restrict__ Umf,
+                                                     int8_t* __restrict__ Vt, int8_t* __restrict__ Vr,
+                                                     int8_t* __restrict__ Vmf, float* __restrict__ dF,
+                                                     unsigned* maxbits, unsigned* maxbits_w, int slot1, int slot2) {
+  if (blockIdx.x == 0) {
+    if (threadIdx.x < BBP) dF[threadIdx.x] = (int)threadIdx.x < bb ? -D[c0 + threadIdx.x] : 0.0f;
+    if (threadIdx.x == 0) {
+      maxbits[slot1] = 0u;
+      maxbits[slot2] = 0u;
+      maxbits_w[slot1] = 0u;
+      maxbits_w[slot2] = 0u;
+    }
+    return;
+  }
+  const int nut = (int)(m_pad / TILE);
+  const bool isU = (int)blockIdx.x <= nut;
+  const int64_t j0 = (int64_t)(isU ? blockIdx.x - 1 : blockIdx.x - 1 - nut) * 32;
+  const int64_t pitchB = (k + 3) >> 2, pitchC = (n + 3) >> 2;
+  for (int e = threadIdx.x; e < 32 * BBP; e += NT) {
+    const int jj = e >> 6, c = e & 63;
+    const int64_t j = j0 + jj;
+    int8_t t = 0;
+    if (c < bb) {
+      if (isU) {
+        if (j < m) t = trit_decode(Bp[j * pitchB + ((c0 + c) >> 2)], c0 + c);
+      } else if (j < n) {
+        t = trit_decode(Cp[(c0 + c) * pitchC + (j >> 2)], j);
+      }
+    }
+    if (isU) {
+      Ut[(int64_t)c * m_pad + j] = t;
+      Ur[j * BBP + c] = t;
+      Ub[j * BBP + c] = t == 0 ? 0 : (t > 0 ? 0x3F80u : 0xBF80u);
+      Umf[mf_offset(c, j)] = t;
+    } else {
+      Vt[(int64_t)c * n_pad + j] = t;
+      Vr[j * BBP + c] = t;
+      Vmf[mf_offset(c, j)] = t;
+    }
+  }
+}
+
+// After the fit: the joint scale solve of the new block (Eq. (4)) and the
+// choice between it and the old block.  The new block is kept when the
+// objective it removes from R' exceeds what the old block removes,
+// fro2_added - fro2_prev (both from the fused column energies: R before the
+// add-back and R' after it).  Kept: D <- fp32(d) and the new scales go to
+// the deflation.  Otherwise the deflation takes the old scales D and the
+// outputs stay.  *decision = 1 / 0; *accepted counts the kept new blocks.
+// grid: one WG.
+__global__ __launch_bounds__(NT) void k_revisit_decide(int* gacc, int bb, const double* __restrict__ gramV,
+                                                       const double* __restrict__ gvec, double* dvec, float* dF,
+                                                       float* D, const double* fro2_prev,
+                                                       const double* fro2_added, unsigned* decision,
+                                                       unsigned* accepted) {
+  __shared__ double Gs[4096];
+  __shared__ double colbuf[1024];
+  const double gain = scale_solve(gacc, bb, gramV, gvec, dvec, dF, nullptr, Gs, colbuf, true);
+  const double old_gain = *fro2_added - *fro2_prev;
+  const bool take_new = gain > old_gain;
+  const int t = threadIdx.x;
+  // thread t wrote dF[t] in the solve
+  if (t < BBP) {
+    if (take_new) {
+      if (t < bb) D[t] = dF[t];
+    } else {
+      dF[t] = t < bb ? D[t] : 0.0f;
+    }
+  }
+  if (t == 0) {
+    *decision = take_new ? 1u : 0u;
+    if (take_new) *accepted += 1u;
   }
 }
 
@@ -2214,10 +2340,25 @@ hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
 }
 
 hipError_t launch_block_out(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
-                           hipStream_t s) {
+                           hipStream_t s, bool revisit) {
   const unsigned grid = (unsigned)(1 + w.m_pad / TILE + w.n_pad / TILE);
   hipLaunchKernelGGL(k_block_out, dim3(grid), dim3(NT), 0, s, w.gacc, bb, w.gramV, w.gvec, w.dvec, w.dF, D + c0,
-                     w.Ut, w.Ur, w.Ub, w.m, w.m_pad, c0, k, Bp, w.Vt, w.Vr, w.n, w.n_pad, Cp);
+                     w.Ut, w.Ur, w.Ub, w.m, w.m_pad, c0, k, Bp, w.Vt, w.Vr, w.n, w.n_pad, Cp,
+                     revisit ? (const unsigned*)(w.counters + CNT_DECISION) : nullptr);
+  return hipGetLastError();
+}
+hipError_t launch_revisit_load(const Ws& w, const uint8_t* Bp, const uint8_t* Cp, const float* D, int64_t c0, int bb,
+                               int64_t k, int slot1, int slot2, hipStream_t s) {
+  const unsigned grid = (unsigned)(1 + w.m_pad / TILE + w.n_pad / TILE);
+  hipLaunchKernelGGL(k_revisit_load, dim3(grid), dim3(NT), 0, s, Bp, Cp, D, c0, bb, k, w.m, w.m_pad, w.n, w.n_pad,
+                     w.Ut, w.Ur, w.Ub, w.Umf, w.Vt, w.Vr, w.Vmf, w.dF, w.maxbits, w.maxbits_w, slot1, slot2);
+  return hipGetLastError();
+}
+hipError_t launch_revisit_decide(const Ws& w, int bb, float* D_block, bool weighted, int slot_prev, int slot_added,
+                                 hipStream_t s) {
+  const double* hist = weighted ? w.fro2w_hist : w.fro2_hist;
+  hipLaunchKernelGGL(k_revisit_decide, dim3(1), dim3(NT), 0, s, w.gacc, bb, w.gramV, w.gvec, w.dvec, w.dF, D_block,
+                     hist + slot_prev, hist + slot_added, w.counters + CNT_DECISION, w.counters + CNT_ACCEPTED);
   return hipGetLastError();
 }
 
@@ -2232,9 +2373,12 @@ hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, 
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  return launch_deflate_slot(w, blk + 1, s, tm);
+}
+hipError_t launch_deflate_slot(const Ws& w, int out_slot, hipStream_t s, Timer* tm) {
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_DEFLATE, k_deflate, dim3(grid), dim3(NT), 0, s, w.R, (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part,
-                                   w.maxbits + blk + 1, w.maxbits_w + blk + 1, w.hw, w.m_pad, w.n_pad, w.gd);
+                                   w.maxbits + out_slot, w.maxbits_w + out_slot, w.hw, w.m_pad, w.n_pad, w.gd);
   return hipGetLastError();
 }
 

@@ -1,4 +1,5 @@
-"""Write the full-size expected energy curves used by tests/test_gpu_fullsize.py.
+"""Write the full-size expected energy curves used by tests/test_gpu_fullsize.py
+and tests/test_gpu_refine_fullsize.py (records under tests/golden/refine/).
 
 Every stored value comes from the fp64 CPU oracle (oracle/) run on the same
 seeded synthetic inputs the GPU tests build (paper_2607_13511_amd/synth.py):
@@ -6,6 +7,7 @@ the block-ALS energy curve E after each block (and E_w for weighted runs),
 the final energies, the factor zero fractions and a SHA-256 of the input
 matrix so that a drifting generator is caught.  Run from the repository
 root:  python tests/golden/make_golden.py [name ...]
+       python tests/golden/make_golden.py --refine [name ...]
 """
 from __future__ import annotations
 
@@ -42,6 +44,44 @@ def cases():
             yield f"block_{mname}_{m}x{n}_mu{mu}_tau{tau}_b64_imatrix", A, h, mu, tau, 64, 8
 
 
+# refinement sweeps (Sec. 2.4) on the 9728x2560 down projection at mu = 1
+REFINE_POINTS = ((1.0, 1.0, 64, 8, 1),)
+
+
+def refine_cases():
+    for weighted in (False, True):
+        w = synth.down9728(weighted=weighted)
+        for mu, tau, block, iters, sweeps in REFINE_POINTS:
+            name = f"refine_down9728x2560_mu{mu:g}_tau{tau}_b{block}_s{sweeps}" + ("_imatrix" if weighted else "")
+            yield name, w.A, w.h, mu, tau, block, iters, sweeps
+
+
+def main_refine(names):
+    os.makedirs(os.path.join(HERE, "refine"), exist_ok=True)
+    for name, A, h, mu, tau, block, iters, sweeps in refine_cases():
+        if names and name not in names:
+            continue
+        t0 = time.time()
+        f = oracle.factorize_block(A, mu, tau, block, iters, h=h)
+        r = oracle.refine(A, f, tau, iters, sweeps, h=h)
+        rec = {
+            "source": "oracle.factorize_block + oracle.refine on synth inputs (tests/golden/make_golden.py)",
+            "name": name, "m": int(A.shape[0]), "n": int(A.shape[1]), "mu": mu, "tau": tau, "block": block,
+            "iters": iters, "sweeps": sweeps, "weighted": h is not None, "k": int(f.k), "block_eff": int(f.block),
+            "a_sha256": hashlib.sha256(np.ascontiguousarray(A, dtype=np.float32).tobytes()).hexdigest(),
+            "curve": [float(x) for x in f.curve],
+            "curve_w": [float(x) for x in f.curve_w] if f.curve_w is not None else None,
+            "sweep_curve": [float(x) for x in r.sweep_curve],
+            "sweep_curve_w": [float(x) for x in r.sweep_curve_w] if r.sweep_curve_w is not None else None,
+            "E": float(r.E), "E_w": float(r.E_w) if r.E_w is not None else None,
+            "accepted": int(r.accepted), "revisits": int(r.revisits),
+        }
+        with open(os.path.join(HERE, "refine", name + ".json"), "w") as fh:
+            json.dump(rec, fh, indent=0)
+        print(f"{name}: E {f.E:.6f} -> {r.E:.6f}, accepted {r.accepted}/{r.revisits} ({time.time() - t0:.1f} s)",
+              flush=True)
+
+
 def main(names):
     for name, A, h, mu, tau, block, iters in cases():
         if names and name not in names:
@@ -65,4 +105,8 @@ def main(names):
 
 
 if __name__ == "__main__":
-    main(set(sys.argv[1:]))
+    args = sys.argv[1:]
+    if args[:1] == ["--refine"]:
+        main_refine(set(args[1:]))
+    else:
+        main(set(args))

@@ -85,6 +85,15 @@ def test_argument_errors_before_device_work():
         assert np.isnan(E.value)
     assert g(None, 10, 10, 1.0, 0.9, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(ku), ctypes.byref(E), None,
              None, None, dummy, 1 << 30, None) == binding.EINVAL
+    # refinement sweeps: sweeps >= 0, same argument rules as externd_factorize
+    r = L.externd_factorize_refined
+    assert r(dummy, 10, 10, 1.0, 0.7, 1, 1, -1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             None, None, None, dummy, 1 << 30, None) == binding.EINVAL
+    assert np.isnan(E.value)
+    assert r(None, 10, 10, 1.0, 0.7, 1, 1, 2, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             None, None, None, dummy, 1 << 30, None) == binding.EINVAL
+    assert r(dummy, 10, 10, 1.0, 0.7, 1, 1, 2, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             None, None, None, dummy, 16, None) == binding.EWORKSPACE
     # inference: batch limits, workspace size and alignment
     ap = L.externd_apply
     assert L.externd_apply_workspace_bytes(100, 1) == 400 and L.externd_apply_workspace_bytes(100, 3) == 1600

@@ -15,6 +15,7 @@ import oracle
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 GOLDEN = sorted(glob.glob(os.path.join(HERE, "golden", "*.json")))
+REFINE = sorted(glob.glob(os.path.join(HERE, "golden", "refine", "*.json")))
 
 
 def test_golden_present():
@@ -35,3 +36,29 @@ def test_golden_record(path):
     assert len(curve) == -(-rec["k"] // rec["block_eff"])
     assert curve[-1] == rec["E"]
     assert np.all(np.diff(curve) >= -1e-12)
+
+
+def test_refine_records_present():
+    assert len(REFINE) >= 2
+
+
+@pytest.mark.parametrize("path", REFINE, ids=lambda p: os.path.basename(p)[:-5])
+def test_refine_record(path):
+    from paper_2607_13511_amd import synth
+    rec = load_json(path)
+    w = synth.down9728(weighted=rec["weighted"])
+    assert hashlib.sha256(np.ascontiguousarray(w.A, dtype=np.float32).tobytes()).hexdigest() == rec["a_sha256"]
+    assert rec["k"] == oracle.rank_of(rec["m"], rec["n"], rec["mu"])
+    nblk = -(-rec["k"] // rec["block_eff"])
+    assert len(rec["curve"]) == nblk and len(rec["sweep_curve"]) == rec["sweeps"]
+    assert rec["revisits"] == rec["sweeps"] * nblk and 0 <= rec["accepted"] <= rec["revisits"]
+    # sweeps never lower the objective the run minimizes (Sec. 2.4)
+    key = "_w" if rec["weighted"] else ""
+    obj = [rec["curve" + key][-1]] + rec["sweep_curve" + key]
+    assert np.all(np.diff(obj) >= -1e-12)
+    assert rec["sweep_curve"][-1] == rec["E"]
+
+
+def load_json(path):
+    with open(path) as f:
+        return json.load(f)
