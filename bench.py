@@ -55,11 +55,27 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
+def vstep_row_groups(m: int, n: int) -> int:
+    """Row groups of the V-step contraction (the library's layout rule:
+    about 480 column-tile x row-group workgroups, at most 8)."""
+    nct, nrt = -(-n // 32), -(-m // 32)
+    return max(1, min(-(-480 // nct), min(nrt, 8)))
+
+
 def algorithmic_bytes(kclass: str, m: int, n: int) -> float:
     """Algorithmic HBM bytes per launch: the residual is read once by each
     contraction (4 m n) and read and written once by the deflation (8 m n);
-    the ternary operands and outputs add < 2 % and are not counted."""
-    return (8.0 if kclass == "deflate" else 4.0) * m * n
+    the ternary operands and outputs add < 2 % and are not counted.  The
+    target kernels read the contraction's output (V: the row groups' int64
+    partials of P, 64 x n each; U: Q, 64 x m fp64) and write the fp64
+    target (64 x n or 64 x m)."""
+    if kclass == "deflate":
+        return 8.0 * m * n
+    if kclass == "vstep_target":
+        return (vstep_row_groups(m, n) + 1) * 64 * 8.0 * n
+    if kclass == "ustep_target":
+        return 2 * 64 * 8.0 * m
+    return 4.0 * m * n
 
 
 def traffic_from_counters(kclass: str):
@@ -130,7 +146,8 @@ def collect_traffic(dbs, copy_bytes: int):
     copy_f = max(v[1] for k, v in cfetch.items() if "copyBuffer" in k)
     copy_w = max(v[1] for k, v in cwrite.items() if "copyBuffer" in k)
     ff, fw = copy_bytes / copy_f, copy_bytes / copy_w
-    classes = {"vstep_contraction": "k_vstep", "ustep_contraction": "k_ustep<false>", "deflate": "k_deflate"}
+    classes = {"vstep_contraction": "k_vstep", "ustep_contraction": "k_ustep<false>", "deflate": "k_deflate",
+               "vstep_target": "k_vtarget", "ustep_target": "k_utarget"}
     out = {"kernel_source_sha256": kernel_source_hash(), "copy_bytes": copy_bytes,
            "fetch_scale": ff, "write_scale": fw, "kernels": {}}
     lines = ["# HBM traffic per launch (rocprofv3 --pmc), 9728x2560 workload", "",
@@ -256,7 +273,7 @@ def main():
                           "launches_per_matrix": issued // args.steps,
                           "avg_us": avg * 1e6, "GB_s": gbs,
                           "share_of_step": avg * issued / dt}
-        if kc != "deflate":
+        if kc in ("vstep_contraction", "ustep_contraction"):
             # int8 MFMA work issued: 4 digit planes x 2 m n (block padded to 64)
             tops = 4 * 2.0 * m * n * 64 / avg / 1e12
             per_kernel[kc]["mfma_int8_tops"] = tops

@@ -49,8 +49,8 @@ extern "C" {
 #define EXTERND_EHIP         -4  /* HIP runtime or launch failure                       */
 #define EXTERND_EUNSUPPORTED -5  /* shape outside the supported range                   */
 #define EXTERND_ESYNC        -6  /* a bounded wait between the workgroups of one kernel
-                                    launch ran out; the call's results are unusable
-                                    (reported instead of hanging; not expected)          */
+                                    launch ran out (reserved: no kernel of this version
+                                    waits on another workgroup)                          */
 
 /* Largest block width the kernels handle; larger requests are clamped. */
 #define EXTERND_MAX_BLOCK 64
@@ -205,10 +205,12 @@ int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float*
                   void* stream);
 
 /* Kernel classes timed by externd_factorize_timed. */
-#define EXTERND_KCLASS_VSTEP   0  /* V-step contraction P = U^T R (+ Gram of U)          */
+#define EXTERND_KCLASS_VSTEP   0  /* V-step contraction P = U^T R (+ Gram of U, inverse) */
 #define EXTERND_KCLASS_USTEP   1  /* U-step contraction Q = R diag(h~) V (+ Gram of V)  */
 #define EXTERND_KCLASS_DEFLATE 2  /* deflation R -= U diag(d) V^T (+ column energies)   */
-#define EXTERND_KCLASS_COUNT   3
+#define EXTERND_KCLASS_VTARGET 3  /* V-step target Y = G_U^{-1} P and its statistics    */
+#define EXTERND_KCLASS_UTARGET 4  /* U-step target Z = Q G_V^{-1} and its statistics    */
+#define EXTERND_KCLASS_COUNT   5
 
 typedef struct {
   double total_ms[EXTERND_KCLASS_COUNT];  /* summed durations of the timed launches */

@@ -63,14 +63,15 @@ _SIGNATURES = {
 EXPORTED = tuple(_SIGNATURES)
 
 
-KCLASS_NAMES = ("vstep_contraction", "ustep_contraction", "deflate")
+KCLASS_NAMES = ("vstep_contraction", "ustep_contraction", "deflate", "vstep_target", "ustep_target")
 # externd_factorize_timed times one launch in TIMING_STRIDE of each class
 # (EXTERND_TIMING_STRIDE in include/externd.h).
 TIMING_STRIDE = 16
 
 
 class KernelTimes(ctypes.Structure):
-    _fields_ = [("total_ms", ctypes.c_double * 3), ("launches", ctypes.c_int64 * 3), ("issued", ctypes.c_int64 * 3)]
+    _fields_ = [("total_ms", ctypes.c_double * len(KCLASS_NAMES)), ("launches", ctypes.c_int64 * len(KCLASS_NAMES)),
+                ("issued", ctypes.c_int64 * len(KCLASS_NAMES))]
 
 
 class ExterndError(RuntimeError):

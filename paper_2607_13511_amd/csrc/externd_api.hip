@@ -44,8 +44,8 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   L.nsu = clampi((L.m_pad + TERN_CHUNK - 1) / TERN_CHUNK, 1, TERN_SPLIT_MAX);
   L.nsv = clampi((L.n_pad + TERN_CHUNK - 1) / TERN_CHUNK, 1, TERN_SPLIT_MAX);
   L.nblk_cap = (int)(k + 2);  // fro2 before every block and after the last; one spare
-  int64_t ntmax = nrt > nct ? nrt : nct;  // statistics tiles: 32-index tiles of either side,
-  if (L.ntu > ntmax) ntmax = L.ntu;       // or the U-step's row groups
+  // statistics tiles: 32-row tiles of the U side, 16-column tiles of the V side
+  const int64_t ntmax = nrt > 2 * nct ? nrt : 2 * nct;
   const size_t sizes[] = {
       sizeof(float) * (size_t)(L.m_pad * L.n_pad),     // 0 R
       (size_t)(BBP * L.m_pad),                         // 1 Ut
@@ -79,7 +79,7 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(double) * (size_t)(BBP * ntmax),          // 29 tpm
       sizeof(int) * (size_t)(BBP * ntmax),             // 30 tpi
       sizeof(unsigned short) * (size_t)(BBP * L.m_pad),  // 31 Ub
-      sizeof(unsigned) * (size_t)nct,                  // 32 tilecnt
+      0,                                               // 32 (unused)
       sizeof(int) * 2 * 4096,                          // 33 gacc
   };
   size_t o = 0;
@@ -140,7 +140,6 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.tpm = (double*)(b + L.off[29]);
   w.tpi = (int*)(b + L.off[30]);
   w.Ub = (unsigned short*)(b + L.off[31]);
-  w.tilecnt = (unsigned*)(b + L.off[32]);
   w.gacc = (int*)(b + L.off[33]);
   return true;
 }

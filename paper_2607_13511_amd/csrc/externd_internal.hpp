@@ -35,11 +35,10 @@ constexpr int TERN_CHUNK = 640;
 
 // Index of counters in Ws::counters (each used by one kernel family, reset
 // to zero by the workgroup that consumes it).
-// CNT_READY_*: G^{-1} of the V-step (U Gram) / U-step (V Gram) is stored.
 // CNT_DECISION: the last refinement revisit kept its new block (1) or not;
 // CNT_ACCEPTED: revisits of the call that kept the new block.
 enum Counter {
-  CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2, CNT_READY_U = 3, CNT_READY_V = 4,
+  CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2,
   CNT_DECISION = 5, CNT_ACCEPTED = 6, CNT_COUNT = 8
 };
 // Flags written by the device, read by the host.
@@ -65,7 +64,6 @@ struct Ws {
   double* tps;           // BBP x tiles: per-32-index-tile sum |x| of a target component
   double* tpm;           // BBP x tiles: per-tile max |x|
   int* tpi;              // BBP x tiles: per-tile smallest index attaining the max
-  unsigned* tilecnt;     // n_pad/32: arrivals per V-step column tile (0 between launches)
   int* gacc;             // 2 x 4096: integer Gram accumulators of the V-step (U) and U-step (V)
   double* Q;             // BBP x m_pad, Q = R diag(h) V  (component-major)
   double* Z;             // BBP x m_pad, U-step target

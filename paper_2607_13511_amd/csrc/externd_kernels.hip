@@ -456,45 +456,6 @@ __device__ __forceinline__ void ridge_invert_store(double* G, double* colbuf, in
 }
 
 // ---------------------------------------------------------------------------
-// Ready flag between the side workgroups (which store G^{-1}) and the
-// contraction workgroups of the same launch (which apply it).  Workgroups
-// are dispatched in index order and the side workgroups come first and
-// wait on nothing, so a waiting contraction workgroup never blocks them.
-// The flag is 0 before the launch (cleared by the next kernel in the
-// stream and at set-up); the wait is bounded and reports a timeout through
-// FLAG_SYNC instead of hanging.
-// Data that crosses workgroups inside one launch is read with device-scope
-// (coherent) atomic loads, so the waiting side needs no cache-invalidating
-// fence: with one L2 per XCD an acquire fence in hundreds of workgroups
-// would discard the L2 contents the streaming workgroups rely on.
-// ---------------------------------------------------------------------------
-constexpr unsigned SPIN_LIMIT = 1u << 24;
-
-// Everything the waiting workgroups read (G^{-1}) is written with
-// device-coherent (write-through) stores, so no L2 write-back is needed:
-// each wave waits for its own stores to complete, and after the barrier
-// one thread raises the flag.
-__device__ __forceinline__ void signal_ready(unsigned* ready) {
-  __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have completed
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_store(ready, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ void wait_ready(unsigned* ready, int* flags) {
-  if (threadIdx.x == 0) {
-    unsigned spins = 0;
-    while (load_coherent(ready) == 0u) {
-      __builtin_amdgcn_s_sleep(2);
-      if (++spins > SPIN_LIMIT) {
-        atomicOr(flags + FLAG_SYNC, 1);
-        break;
-      }
-    }
-  }
-  __syncthreads();
-}
-
-// ---------------------------------------------------------------------------
 // Gram matrices of a ternary factor, built by `nside` workgroups
 // ---------------------------------------------------------------------------
 // Partial integer Gram of X (BBP x L int8, MFMA-ready layout) over this
@@ -815,102 +776,13 @@ __device__ __forceinline__ void tile_stats(const v4d (&x)[2], int w, int64_t i0,
   }
 }
 
-// V-step target tile Y[:, j0 .. j0+32) = G_U^{-1} P (Eq. (3)).
-// vtarget_sum: P summed over the gv row-group partials (int64, exact) and
-// scaled back by 2^-s into Ps (LDS, 64 x 33 doubles); vtarget_apply: the
-// product with G_U^{-1}, the stores and the T_tau statistics.
-template <int GV>
-__device__ __forceinline__ void vtarget_sum_g(const long long* __restrict__ Pp, int s, int64_t n_pad, int ct,
-                                              double* Ps) {
-  const int64_t j0 = (int64_t)ct * TILE;
-  // every partial of every group is loaded in one round (straight-line
-  // loads, then the sums)
-  long long v[GV][8];
-#pragma unroll
-  for (int g = 0; g < GV; ++g)
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = threadIdx.x + q * NT, c = e >> 5, jj = e & 31;
-      v[g][q] = load_coherent(Pp + ((int64_t)g * BBP + c) * n_pad + j0 + jj);
-    }
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    long long acc = 0;
-#pragma unroll
-    for (int g = 0; g < GV; ++g) acc += v[g][q];
-    const int e = threadIdx.x + q * NT;
-    Ps[(e >> 5) * 33 + (e & 31)] = ldexp((double)acc, -s);
-  }
-  __syncthreads();
-}
-__device__ __forceinline__ void vtarget_sum(const long long* __restrict__ Pp, int gv, int s, int64_t n_pad, int ct,
-                                            double* Ps) {
-  static_assert(GV_MAX == 8, "one case per group count");
-  switch (gv) {
-    case 1: vtarget_sum_g<1>(Pp, s, n_pad, ct, Ps); break;
-    case 2: vtarget_sum_g<2>(Pp, s, n_pad, ct, Ps); break;
-    case 3: vtarget_sum_g<3>(Pp, s, n_pad, ct, Ps); break;
-    case 4: vtarget_sum_g<4>(Pp, s, n_pad, ct, Ps); break;
-    case 5: vtarget_sum_g<5>(Pp, s, n_pad, ct, Ps); break;
-    case 6: vtarget_sum_g<6>(Pp, s, n_pad, ct, Ps); break;
-    case 7: vtarget_sum_g<7>(Pp, s, n_pad, ct, Ps); break;
-    default: vtarget_sum_g<8>(Pp, s, n_pad, ct, Ps); break;
-  }
-}
-__device__ __forceinline__ void vtarget_apply(const double (&a)[16], double* __restrict__ Y, int64_t n,
-                                              int64_t n_pad, int ct, int ntile, double* ps, double* pm, int* pi,
-                                              const double* Ps) {
-  const int64_t j0 = (int64_t)ct * TILE;
-  const int lane = lane_id(), w = wave_id();
-  const int li = lane & 15, lk = lane >> 4;
-  // A = G^{-1}[16 w + li][4 ks + lk] (a, from load_ginv), B = P[4 ks + lk][16 h + li] (LDS)
-  v4d y[2] = {v4d{}, v4d{}};
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) {
-    y[0] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + li], y[0]);
-    y[1] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + 16 + li], y[1]);
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    double* row = Y + (int64_t)(16 * w + lk + 4 * r) * n_pad + j0;
-    row[li] = y[0][r];
-    row[16 + li] = y[1][r];
-  }
-  tile_stats(y, w, j0, n, ntile, ct, ps, pm, pi);
-}
-
-// U-step target tile Z[i0 .. i0+rows, :] = Q G_V^{-1} (Eq. (3)), rows <= 32,
-// computed as Z^T = G_V^{-1} Q^T (G_V^{-1} symmetric) so that rows of Z^T
-// (component-major) are written coalesced.  Qs: LDS tile Q^T,
-// Qs[c * 32 + r] (entries r >= rows are ignored).  a: G_V^{-1} from load_ginv.
-__device__ __forceinline__ void utarget_tile(const double* Qs, const double (&a)[16], double* __restrict__ Z,
-                                             int64_t m, int64_t m_pad, int64_t i0, int rows, int tile, int ntile,
-                                             double* ps, double* pm, int* pi) {
-  const int lane = lane_id(), w = wave_id();
-  const int li = lane & 15, lk = lane >> 4;
-  v4d z[2] = {v4d{}, v4d{}};
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) {
-    z[0] = mfma_f64(a[ks], Qs[(4 * ks + lk) * 32 + li], z[0]);
-    z[1] = mfma_f64(a[ks], Qs[(4 * ks + lk) * 32 + 16 + li], z[1]);
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    double* row = Z + (int64_t)(16 * w + lk + 4 * r) * m_pad + i0;
-    if (li < rows) row[li] = z[0][r];
-    if (16 + li < rows) row[16 + li] = z[1][r];
-  }
-  const int64_t lim = i0 + rows < m ? i0 + rows : m;
-  tile_stats(z, w, i0, lim, ntile, tile, ps, pm, pi);
-}
-
 // ---------------------------------------------------------------------------
-// V-step P = U^T R and target Y = G_U^{-1} P  (Eq. (3), first half)
+// V-step contraction P = U^T R  (Eq. (3), first half; the target
+// Y = G_U^{-1} P follows in k_vtarget)
 // grid: nside side WGs (the U Gram U^T U on int8 MFMA over K slices, then
-//       in the last of them the ridge and inverse) followed by
-//       (n_pad/32 column tiles) x gv row groups; the last of the gv WGs of a
-//       column tile (per-tile counter) sums the int64 partials, waits for
-//       G_U^{-1} and writes the Y tile and its T_tau statistics.
+//       in the last of them the ridge and inverse G_U^{-1}) followed by
+//       (n_pad/32 column tiles) x gv row groups, each storing its exact
+//       int64 partial of the P tile.
 // Each WG owns 32 columns and a contiguous range of 32-row K steps, split
 // over its 4 waves; A = U (MFMA-ready layout), B = R digit planes.  Lane
 // (j, h) loads column j, rows 16h .. 16h+15 of the K step: every load
@@ -919,9 +791,7 @@ __device__ __forceinline__ void utarget_tile(const double* Qs, const double (&a)
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vstep(const float* __restrict__ R, const v4i* __restrict__ Umf,
                                               long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
                                               int64_t m_pad, int64_t n_pad, int gv, int bb, int* gacc,
-                                              unsigned* gcounter, double* ginvU, int nside, double* __restrict__ Y,
-                                              int64_t n, double* ps, double* pm, int* pi, unsigned* tilecnt,
-                                              unsigned* ready, int* flags) {
+                                              unsigned* gcounter, double* ginvU, int nside) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[8192];
@@ -933,7 +803,6 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     double* pbuf = Gs + 4096;
     if (!side_gram_acc(Umf, m_pad, blockIdx.x, nside, gacc, gcounter, Gs, (int*)smem)) return;
     ridge_invert_store(Gs, pbuf, bb, ginvU);
-    signal_ready(ready);
     return;
   }
   const int b = blockIdx.x - nside;
@@ -983,33 +852,72 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
       acc[1][p] = mfma_i8(a1, P[p], acc[1][p]);
     }
   }
-  // out[t][M = component][N = column]
+  // out[t][M = component][N = column]: this row group's partial P tile
   long long* Pg = Pp + ((int64_t)g * BBP) * n_pad + (int64_t)ct * TILE;
-  // partials go out with coherent stores; each wave waits for its own
-  // stores to complete before the arrival is counted
-  reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { store_coherent(Pg + (int64_t)(32 * t + M) * n_pad + N, v); });
-  __builtin_amdgcn_s_waitcnt(0);
-  // the last of the tile's gv workgroups forms the target tile
-  __shared__ int s_last;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const unsigned old = __hip_atomic_fetch_add(tilecnt + ct, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (old == (unsigned)(gv - 1));
-  }
-  __syncthreads();
-  if (!s_last) return;
-  if (threadIdx.x == 0) store_coherent(tilecnt + ct, 0u);  // every group has arrived: ready for the next launch
-  // G^{-1} (stored long before) and the partials are loaded in one round
-  wait_ready(ready, flags);
-  double a[16];
-  load_ginv(ginvU, a);
-  vtarget_sum(Pp, gv, s, n_pad, ct, (double*)smem);
-  vtarget_apply(a, Y, n, n_pad, ct, nct, ps, pm, pi, (double*)smem);
+  reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { Pg[(int64_t)(32 * t + M) * n_pad + N] = v; });
 }
 
+// V-step target Y = G_U^{-1} P (Eq. (3) first half) and its T_tau
+// statistics, after the contraction launch: P is the sum of the gv row
+// groups' exact partials, G_U^{-1} comes from the contraction's side path.
+// grid: n_pad / 16 tiles of 16 columns (statistics per 16-column tile).
+template <int GV>
+__device__ __forceinline__ void vtarget_sum16(const long long* __restrict__ Pp, int s, int64_t n_pad, int64_t j0,
+                                              double* Ps) {
+  long long v[GV][4];
+#pragma unroll
+  for (int g = 0; g < GV; ++g)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = threadIdx.x + q * NT, c = e >> 4, jj = e & 15;
+      v[g][q] = Pp[((int64_t)g * BBP + c) * n_pad + j0 + jj];
+    }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    long long acc = 0;
+#pragma unroll
+    for (int g = 0; g < GV; ++g) acc += v[g][q];
+    const int e = threadIdx.x + q * NT;
+    Ps[(e >> 4) * 17 + (e & 15)] = ldexp((double)acc, -s);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_vtarget(const long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
+                                                int64_t n_pad, int gv, const double* __restrict__ ginvU,
+                                                double* __restrict__ Y, int64_t n, double* ps, double* pm, int* pi) {
+  __shared__ double Ps[64 * 17];
+  const int tile = blockIdx.x;
+  const int ntile = (int)(n_pad / 16);
+  const int64_t j0 = (int64_t)tile * 16;
+  const int s = fx_shift(*maxbits);
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+  double a[16];
+  load_ginv(ginvU, a);
+  static_assert(GV_MAX == 8, "one case per group count");
+  switch (gv) {
+    case 1: vtarget_sum16<1>(Pp, s, n_pad, j0, Ps); break;
+    case 2: vtarget_sum16<2>(Pp, s, n_pad, j0, Ps); break;
+    case 3: vtarget_sum16<3>(Pp, s, n_pad, j0, Ps); break;
+    case 4: vtarget_sum16<4>(Pp, s, n_pad, j0, Ps); break;
+    case 5: vtarget_sum16<5>(Pp, s, n_pad, j0, Ps); break;
+    case 6: vtarget_sum16<6>(Pp, s, n_pad, j0, Ps); break;
+    case 7: vtarget_sum16<7>(Pp, s, n_pad, j0, Ps); break;
+    default: vtarget_sum16<8>(Pp, s, n_pad, j0, Ps); break;
+  }
+  __syncthreads();
+  // A = G^{-1}[16 w + li][4 ks + lk] (a), B = P[4 ks + lk][li] (LDS)
+  v4d y[2] = {v4d{}, v4d{}};
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) y[0] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 17 + li], y[0]);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) Y[(int64_t)(16 * w + lk + 4 * r) * n_pad + j0 + li] = y[0][r];
+  // the second half of the 32-wide statistics tile lies past the limit
+  tile_stats(y, w, j0, (j0 + 16 < n ? j0 + 16 : n), ntile, tile, ps, pm, pi);
+}
 // ---------------------------------------------------------------------------
-// U-step Q = R diag(h~) V and target Z = Q G_V^{-1}  (Eq. (3) second half,
-// Sec. 2.5)
+// U-step Q = R diag(h~) V  (Eq. (3) second half, Sec. 2.5); the target
+// Z = Q G_V^{-1} follows in k_utarget
 // grid: nside side WGs (V^T V on int8 MFMA or, weighted, V^T H V on fp64
 //       MFMA, over K slices; the last of them adds the ridge and inverts;
 //       the raw Gram is kept for the scale solve) followed by ntile row groups of `rows` <= 32 rows, sized so
@@ -1037,8 +945,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                               double* __restrict__ Q, const unsigned* __restrict__ maxbits,
                                               int64_t m_pad, int64_t n_pad, int bb, int* gacc, double* gpart,
                                               unsigned* counter, double* ginvV, double* gramV, int nside,
-                                              double* __restrict__ Z, int64_t m, int rows, int ntile, double* ps,
-                                              double* pm, int* pi, unsigned* ready, int* flags) {
+                                              int rows) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[USTEP_SMEM_LL];
@@ -1054,7 +961,6 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
       for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
       __syncthreads();
       ridge_invert_store(Gs, pbuf, bb, ginvV);
-      signal_ready(ready);
     }
     return;
   }
@@ -1150,14 +1056,48 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   double* tq = (double*)smem;
   reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { tq[(32 * t + N) * 32 + M] = ldexp((double)v, -s); });
   __syncthreads();
-  wait_ready(ready, flags);
-  double a[16];
-  load_ginv(ginvV, a);
   for (int e = threadIdx.x; e < 2048; e += NT)
     if ((e & 31) < valid) Q[(int64_t)(e >> 5) * m_pad + i0 + (e & 31)] = tq[e];
-  utarget_tile(tq, a, Z, m, m_pad, i0, valid, rt, ntile, ps, pm, pi);
 }
 
+// U-step target rows Z = Q G_V^{-1} (Eq. (3) second half) and their T_tau
+// statistics, after the contraction launch (G_V^{-1} from its side path).
+// grid: m_pad / 32 row tiles (statistics per tile).  Rows past m hold
+// Q = 0 (zero residual padding), so their targets are zero.
+__global__ __launch_bounds__(NT) void k_utarget(const double* __restrict__ Q, const double* __restrict__ ginvV,
+                                                double* __restrict__ Z, int64_t m, int64_t m_pad, double* ps,
+                                                double* pm, int* pi) {
+  const int nrt = (int)(m_pad / TILE);
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+  double a[16];
+  load_ginv(ginvV, a);
+  {
+    const int rt = (int)blockIdx.x;
+    const int64_t i0 = (int64_t)rt * TILE;
+    // B = Q[4 ks + lk][i0 + li (+16)], straight from memory
+    double b0[16], b1[16];
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) {
+      const double* qr = Q + (int64_t)(4 * ks + lk) * m_pad + i0 + li;
+      b0[ks] = qr[0];
+      b1[ks] = qr[16];
+    }
+    v4d z[2] = {v4d{}, v4d{}};
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) {
+      z[0] = mfma_f64(a[ks], b0[ks], z[0]);
+      z[1] = mfma_f64(a[ks], b1[ks], z[1]);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      double* row = Z + (int64_t)(16 * w + lk + 4 * r) * m_pad + i0;
+      row[li] = z[0][r];
+      row[16 + li] = z[1][r];
+    }
+    tile_stats(z, w, i0, m, nrt, rt, ps, pm, pi);
+  }
+}
 // ---------------------------------------------------------------------------
 // T_tau of target components from their per-tile statistics (Eq. (2)):
 // theta = tau * (sum |x|) / L, strict ">", and when no entry exceeds theta
@@ -1280,9 +1220,8 @@ __device__ __forceinline__ void tern_range(int64_t L_pad, int sp, int ns, int64_
 __global__ __launch_bounds__(NT) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb, double tau,
                                                const double* __restrict__ ps, const double* __restrict__ pm,
                                                const int* __restrict__ pi, int ntile, int ns, int8_t* __restrict__ Vt,
-                                               int8_t* __restrict__ Vmf, unsigned* ready_clear) {
+                                               int8_t* __restrict__ Vmf) {
   const int c = blockIdx.x / ns, sp = blockIdx.x % ns;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *ready_clear = 0u;
   int64_t i0, i1;
   tern_range(n_pad, sp, ns, i0, i1);
   int8_t* dst = Vt + (int64_t)c * n_pad;
@@ -1306,9 +1245,8 @@ __global__ __launch_bounds__(NT) void k_tern_u(const double* __restrict__ Z, con
                                                int64_t m_pad, int bb, double tau, const double* __restrict__ ps,
                                                const double* __restrict__ pm, const int* __restrict__ pi, int ntile,
                                                int ns, int8_t* __restrict__ Ut, int8_t* __restrict__ Umf,
-                                               double* __restrict__ gpart, unsigned* ready_clear) {
+                                               double* __restrict__ gpart) {
   const int c = blockIdx.x / ns, sp = blockIdx.x % ns;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *ready_clear = 0u;
   int64_t i0, i1;
   tern_range(m_pad, sp, ns, i0, i1);
   int8_t* dst = Ut + (int64_t)c * m_pad;
@@ -1656,7 +1594,7 @@ __global__ __launch_bounds__(NT) void k_unstage(const float* __restrict__ R, flo
 __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_t n, int64_t n_pad,
                                              double* __restrict__ hw, unsigned* maxbits, unsigned* maxbits_w,
                                              double* fro2_hist, double* fro2w_hist, int nblk_cap,
-                                             unsigned* counters, int* flags, unsigned* tilecnt, int* gacc) {
+                                             unsigned* counters, int* flags, int* gacc) {
   __shared__ float smax[NT / 64];
   __shared__ int sbad[NT / 64];
   for (int e = threadIdx.x; e < nblk_cap; e += NT) {
@@ -1666,7 +1604,6 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
     fro2w_hist[e] = 0.0;
   }
   if (threadIdx.x < CNT_COUNT) counters[threadIdx.x] = 0u;
-  for (int64_t e = threadIdx.x; e < n_pad / TILE; e += NT) tilecnt[e] = 0u;
   for (int e = threadIdx.x; e < 2 * 4096; e += NT) gacc[e] = 0;
   if (threadIdx.x < FLAG_COUNT) flags[threadIdx.x] = 0;
   if (!h) {
@@ -2247,7 +2184,7 @@ static inline unsigned grid_for(int64_t total) {
 
 hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s) {
   hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.maxbits, w.maxbits_w, w.fro2_hist,
-                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.tilecnt, w.gacc);
+                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc);
   return hipGetLastError();
 }
 
@@ -2287,20 +2224,22 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, w.Z, (const double*)nullptr, w.m, w.m_pad, bb, tau,
-                     w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec,
-                     w.counters + CNT_READY_V);
+                     w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec);
   return hipGetLastError();
 }
 
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
   const unsigned grid = (unsigned)(NSIDE_GRAM + (w.n_pad / TILE) * w.gv);
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, w.maxbits + blk, w.m_pad,
-                                   w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM, w.Y, w.n,
-                                   w.tps, w.tpm, w.tpi, w.tilecnt, w.counters + CNT_READY_U, w.flags);
+                                   w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VTARGET, k_vtarget, dim3((unsigned)(w.n_pad / 16)), dim3(NT), 0, s,
+                       (const long long*)w.Pp, w.maxbits + blk, w.n_pad, w.gv, w.ginvU, w.Y, w.n, w.tps, w.tpm, w.tpi);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi,
-                     (int)(w.n_pad / TILE), w.nsv, w.Vt, w.Vmf, w.counters + CNT_READY_U);
+                     (int)(w.n_pad / 16), w.nsv, w.Vt, w.Vmf);
   return hipGetLastError();
 }
 
@@ -2316,21 +2255,20 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
     if (e != hipSuccess) return e;
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
-                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside,
-                                     w.Z, w.m, w.urows, w.ntu, w.tps,
-                                     w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags);
+                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows);
   } else {
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
-                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside,
-                                     w.Z, w.m, w.urows, w.ntu, w.tps,
-                                     w.tpm, w.tpi, w.counters + CNT_READY_V, w.flags);
+                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_UTARGET, k_utarget, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0,
+                       s, (const double*)w.Q, (const double*)w.ginvV, w.Z, w.m, w.m_pad, w.tps, w.tpm, w.tpi);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, w.Z, final ? (const double*)w.Q : nullptr, w.m,
-                     w.m_pad, bb, tau, w.tps, w.tpm, w.tpi, w.ntu, w.nsu, w.Ut, w.Umf, w.gvec,
-                     w.counters + CNT_READY_V);
+                     w.m_pad, bb, tau, w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec);
   return hipGetLastError();
 }
 
