@@ -57,10 +57,11 @@ Readings taken where the paper is silent (each also listed in the design doc):
 * R6 (rank): k = floor(mu * min(m, n) + 0.5).
 * R7 (block cap, Sec. 2.4): b_eff = min(block, max(1, floor(min(m,n)/8)));
   the last block holds k - c0 components.
-* R8 (weights, Sec. 2.5 with lambda = 0): h~ = h / max(h), one weight per
-  column of A.  The U-step target is R diag(h~) V with Gram V^T diag(h~) V;
-  the V-step uses the plain residual R and U^T U; the scale solve uses
-  (U^T U) o (V^T diag(h~) V) and diag(U^T R diag(h~) V).
+* R8 (weights, Sec. 2.5): h~ = h / max(h) + lambda, one weight per column
+  of A; lambda defaults to 0 (the setting the paper uses).  The U-step
+  target is R diag(h~) V with Gram V^T diag(h~) V; the V-step uses the
+  plain residual R and U^T U; the scale solve uses (U^T U) o (V^T diag(h~) V)
+  and diag(U^T R diag(h~) V).
 * R9 (energies): E = 1 - ||R||_F^2 / ||A||_F^2 (Sec. 2.1); the weighted
   energy is E_w = 1 - sum_j h~_j ||R_:j||^2 / sum_j h~_j ||A_:j||^2.  A zero
   matrix has E = 1.
@@ -70,6 +71,25 @@ Readings taken where the paper is silent (each also listed in the design doc):
   objective that run minimizes), or at k = rank_of(m, n, mu_max).  Greedy
   deflation makes the result the prefix of the full mu_max run, so this is
   the smallest block-multiple k that meets the target.
+* R11 (refinement sweeps, Sec. 2.4, which only says a block is added back,
+  fitted again and deflated again, and that energy improves monotonically):
+  blocks are revisited in extraction order.  The fit is warm-started from the
+  block's current U and runs the same ``iters`` V-step/U-step iterations and
+  joint scale solve as extraction.  The new block replaces the old one only
+  when the energy it removes from R' = R + U diag(d) V^T,
+  2 d'^T g' - d'^T M' d' (the weighted objective when weights are given),
+  is strictly larger than what the old block removes, ||R'||^2 - ||R||^2;
+  otherwise the old block stays.  Every revisit therefore leaves the
+  objective no worse, which is the monotone improvement the paper states.
+* R12 (safeguard for blocks; Proposition 2 augments each sequential step
+  with the single residual entry of largest magnitude): after a block's
+  ALS and Eq. (4) scales, the energy the block removes, 2 d^T g - d^T M d,
+  is compared with max_ij R_ij^2; when the entry is strictly larger the
+  block becomes that one component (u = e_i*, v = sign(R_i*j*) e_j*,
+  d = |R_i*j*|, the first index in row-major order on ties) followed by
+  bb - 1 zero components.  Every block then removes at least
+  ||R||^2 / (m n), which gives Proposition 2's geometric bound per block;
+  at bb = 1 it is the sequential augmented step.  Plain objective only.
 """
 from __future__ import annotations
 
@@ -107,14 +127,16 @@ def effective_block(m: int, n: int, block: int) -> int:
     return int(min(block, max(1, min(m, n) // 8)))
 
 
-def normalized_weights(h: Optional[np.ndarray], n: int) -> np.ndarray:
-    """h~ = h / max(h) + lambda with lambda = 0 (Sec. 2.5); ones if no h."""
+def normalized_weights(h: Optional[np.ndarray], n: int, lam: float = 0.0) -> np.ndarray:
+    """h~ = h / max(h) + lambda (Sec. 2.5); ones if no h (lambda unused)."""
     if h is None:
         return np.ones(n, dtype=np.float64)
     h = np.asarray(h, dtype=np.float64)
     if h.shape != (n,) or not np.all(np.isfinite(h)) or np.any(h < 0) or h.max() <= 0:
         raise ValueError("importance weights must be finite, non-negative, not all zero")
-    return h / h.max()
+    if not (math.isfinite(lam) and lam >= 0.0):
+        raise ValueError("lambda must be finite and non-negative")
+    return h / h.max() + lam
 
 
 # --------------------------------------------------------------------------
@@ -257,7 +279,7 @@ class Factorization:
 
 def factorize_sequential(A: np.ndarray, mu: float, tau: float, iters: int,
                          h: Optional[np.ndarray] = None, safeguard: bool = False,
-                         k: Optional[int] = None) -> Factorization:
+                         k: Optional[int] = None, lam: float = 0.0) -> Factorization:
     """Greedy sequential ALS, Sec. 2.3 (mode S), weighted per Sec. 2.5.
 
     R <- A; for each component: u from reading R1, then ``iters`` times
@@ -271,7 +293,7 @@ def factorize_sequential(A: np.ndarray, mu: float, tau: float, iters: int,
     m, n = A.shape
     if k is None:
         k = rank_of(m, n, mu)
-    w = normalized_weights(h, n)
+    w = normalized_weights(h, n, lam)
     weighted = h is not None
     if safeguard and weighted:
         raise ValueError("the safeguard of Proposition 2 is stated for the unweighted objective")
@@ -325,7 +347,8 @@ def factorize_sequential(A: np.ndarray, mu: float, tau: float, iters: int,
 
 def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int,
                     h: Optional[np.ndarray] = None, k: Optional[int] = None,
-                    max_blocks: Optional[int] = None, target: Optional[float] = None) -> Factorization:
+                    max_blocks: Optional[int] = None, target: Optional[float] = None,
+                    lam: float = 0.0, safeguard: bool = False) -> Factorization:
     """Batched block ALS with decorrelated targets, Sec. 2.4 (mode B).
 
     For each block of bb = min(b_eff, k - c0) components: U from reading R1,
@@ -334,15 +357,19 @@ def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int
     sequential.  Weighted per Sec. 2.5 (reading R8).  ``max_blocks`` stops
     early (used only to time a bounded sample).  ``target``: stop after the
     first block whose energy reaches it (reading R10); the components past
-    ``k_used`` stay zero and ``curve`` holds the blocks done.
+    ``k_used`` stay zero and ``curve`` holds the blocks done.  ``safeguard``:
+    the block analog of Proposition 2's augmented step (reading R12; plain
+    objective only); ``safeguard_fired`` counts the blocks it replaced.
     """
     A = np.asarray(A, dtype=np.float64)
     m, n = A.shape
     if k is None:
         k = rank_of(m, n, mu)
     b_eff = effective_block(m, n, block)
-    w = normalized_weights(h, n)
+    w = normalized_weights(h, n, lam)
     weighted = h is not None
+    if safeguard and weighted:
+        raise ValueError("the safeguard of Proposition 2 is stated for the unweighted objective")
     R = A.copy()
     A_col2 = np.sum(A * A, axis=0)
     A_fro2 = float(np.sum(A_col2))
@@ -355,6 +382,7 @@ def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int
     curve = np.zeros(nblk)
     curve_w = np.zeros(nblk) if weighted else None
     fro2 = np.zeros(nblk)
+    fired = 0
     for blk in range(nblk):
         c0 = blk * b_eff
         bb = min(b_eff, k - c0)
@@ -365,6 +393,23 @@ def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int
             V, _ = vstep(R, U, tau)
             U, Q, _ = ustep(R, V, w, tau)
         d = scale_solve(U, V, Q, w)
+        if safeguard:
+            # energy the block removes, 2 d^T g - d^T M d (Eq. (4)), against
+            # the largest residual entry squared (Proposition 2, option (b))
+            Uf, Vf = U.astype(np.float64), V.astype(np.float64)
+            M = (Uf.T @ Uf) * (Vf.T @ Vf)
+            g = np.sum(Uf * Q, axis=0)
+            gain_blk = float(2.0 * (d @ g) - d @ M @ d)
+            flat = int(np.argmax(np.abs(R)))   # first (row-major) index of the maximum
+            ii, jj = divmod(flat, n)
+            if float(R[ii, jj]) ** 2 > gain_blk:
+                fired += 1
+                U = np.zeros((m, bb), dtype=np.int8)
+                V = np.zeros((n, bb), dtype=np.int8)
+                d = np.zeros(bb)
+                U[ii, 0] = 1
+                V[jj, 0] = 1 if R[ii, jj] >= 0 else -1
+                d[0] = abs(float(R[ii, jj]))
         R = deflate(R, U, V, d)
         B[:, c0:c0 + bb] = U
         C[c0:c0 + bb, :] = V.T
@@ -382,7 +427,7 @@ def factorize_block(A: np.ndarray, mu: float, tau: float, block: int, iters: int
             break
     E, Ew = energy(R, A_fro2, w if weighted else None, A_col2)
     k_used = min(nblk * b_eff, k)
-    return Factorization(B, C, D, E, Ew, curve, curve_w, k, b_eff, 0, 0, fro2, k_used)
+    return Factorization(B, C, D, E, Ew, curve, curve_w, k, b_eff, fired, 0, fro2, k_used)
 
 
 def _weighted_fro2(R: np.ndarray, w: np.ndarray) -> float:
@@ -435,7 +480,7 @@ class Refinement:
 
 
 def refine(A: np.ndarray, F: Factorization, tau: float, iters: int, sweeps: int,
-           h: Optional[np.ndarray] = None) -> Refinement:
+           h: Optional[np.ndarray] = None, lam: float = 0.0) -> Refinement:
     """Refinement sweeps after a block factorization F of A (Sec. 2.4; R11).
 
     Each sweep revisits the blocks of F (width F.block, the last one
@@ -443,7 +488,7 @@ def refine(A: np.ndarray, F: Factorization, tau: float, iters: int, sweeps: int,
     """
     A = np.asarray(A, dtype=np.float64)
     m, n = A.shape
-    w = normalized_weights(h, n)
+    w = normalized_weights(h, n, lam)
     weighted = h is not None
     B = F.B.copy()
     C = F.C.copy()
