@@ -8,7 +8,8 @@
  * alternating least squares with sequential deflation (Sec. 2.3), in blocks
  * of b components with decorrelated least-squares targets (Sec. 2.4,
  * Eq. (3)) and a joint exact scale solve (Eq. (4)); optionally with
- * per-column importance weights (Sec. 2.5, lambda = 0).
+ * per-column importance weights (Sec. 2.5; lambda = 0, or any lambda >= 0
+ * through externd_factorize_ex).
  *
  * Conventions for every entry point:
  *  - "device" pointers are HIP device memory on the current device (for
@@ -121,6 +122,35 @@ int externd_factorize(const float* A, int64_t m, int64_t n, double mu, double ta
                       double* energy, double* energy_w,
                       double* energy_curve, double* energy_w_curve,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * externd_factorize_ex -- externd_factorize with the two options of the
+ * method that the plain call fixes: the lambda of the importance weights
+ * and the single-entry safeguard.
+ *
+ *  lambda     finite, >= 0: h~ = h / max(h) + lambda (Sec. 2.5; lambda
+ *             interpolates between the importance-weighted objective at 0
+ *             and the plain one as it grows).  Ignored when importance is
+ *             NULL.  lambda = 0 gives externd_factorize's result bit for bit.
+ *  safeguard  0 or 1.  1: the block form of Proposition 2's augmented step
+ *             (Appendix A).  After each block's Eq. (4) solve, the objective
+ *             the block removes, 2 d^T g - d^T M d, is compared with the
+ *             largest squared residual entry R_ij^2 (the first in row-major
+ *             order on ties); when the entry is strictly larger the block
+ *             becomes u = e_i, v = sign(R_ij) e_j, d = |R_ij| followed by
+ *             zero components, which removes R_ij exactly.  Every block then
+ *             removes at least ||R||^2 / (m n).  Plain objective only:
+ *             safeguard = 1 with importance != NULL is EXTERND_EINVAL.  When
+ *             it never fires the outputs equal those of externd_factorize.
+ *  safeguard_fired  host, out (may be NULL): blocks replaced.
+ * Other arguments, workspace size, status codes and synchronisation as
+ * externd_factorize.
+ */
+int externd_factorize_ex(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
+                         const float* importance, double lambda, int32_t safeguard, uint8_t* B_packed,
+                         uint8_t* C_packed, float* D, double* energy, double* energy_w, double* energy_curve,
+                         double* energy_w_curve, int64_t* safeguard_fired, void* workspace, size_t workspace_bytes,
+                         void* stream);
 
 /*
  * externd_factorize_to_energy -- the factorization stopped at an energy

@@ -37,6 +37,9 @@ _SIGNATURES = {
     "externd_factorize": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_ptr,
                                          _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                          _c_ptr, _c_size, _c_ptr]),
+    "externd_factorize_ex": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_ptr,
+                                            _c_dbl, _c_i32, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
+                                            _c_ptr, _c_ptr, _c_size, _c_ptr]),
     "externd_factorize_to_energy": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_dbl, _c_i32, _c_i32,
                                                    _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                                    _c_ptr, _c_ptr, _c_size, _c_ptr]),
@@ -158,6 +161,7 @@ class Factorization:
     block: int
     kernel_times: Optional[dict] = None   # class -> (total_ms, timed launches, all launches) when timed
     k_used: int = -1                      # components extracted (factorize_to_energy), else k
+    safeguard_fired: int = 0              # blocks replaced by the single-entry step (factorize_ex)
 
 
 def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=None,
@@ -198,6 +202,39 @@ def factorize(A, mu: float, tau: float, block: int, iters: int, h=None, stream=N
     else:
         _check(lib().externd_factorize(*args), "externd_factorize")
     return Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b, kt, k)
+
+
+def factorize_ex(A, mu: float, tau: float, block: int, iters: int, h=None, lam: float = 0.0,
+                 safeguard: bool = False, stream=None, workspace=None) -> Factorization:
+    """externd_factorize with the lambda of the importance weights
+    (h~ = h / max h + lam) and the single-entry safeguard of Proposition 2
+    (plain objective only) (externd_factorize_ex)."""
+    torch = _torch()
+    m, n = A.shape
+    _req(A, torch, torch.float32, (m, n), "A")
+    if h is not None:
+        _req(h, torch, torch.float32, (n,), "h")
+    k = rank(m, n, mu)
+    if k < 1:
+        raise ExterndError(EINVAL, "rank")
+    b = effective_block(m, n, block)
+    nblk = -(-k // b)
+    dev = A.device
+    Bp = torch.empty((m, (k + 3) // 4), dtype=torch.uint8, device=dev)
+    Cp = torch.empty((k, (n + 3) // 4), dtype=torch.uint8, device=dev)
+    D = torch.empty((k,), dtype=torch.float32, device=dev)
+    ws = workspace if workspace is not None else _workspace(torch, m, n, k, dev)
+    E = ctypes.c_double(0.0)
+    Ew = ctypes.c_double(0.0)
+    fired = ctypes.c_int64(0)
+    curve = np.zeros(nblk, dtype=np.float64)
+    curve_w = np.zeros(nblk, dtype=np.float64)
+    _check(lib().externd_factorize_ex(
+        _dev_ptr(A), m, n, mu, tau, block, iters, _dev_ptr(h) if h is not None else None, lam, int(safeguard),
+        _dev_ptr(Bp), _dev_ptr(Cp), _dev_ptr(D), ctypes.byref(E), ctypes.byref(Ew), curve.ctypes.data,
+        curve_w.ctypes.data, ctypes.byref(fired), _dev_ptr(ws), ws.numel(), _stream_ptr(torch, stream)),
+        "externd_factorize_ex")
+    return Factorization(Bp, Cp, D, E.value, Ew.value, curve, curve_w, k, b, None, k, int(fired.value))
 
 
 APPLY_MAX_BATCH = 8   # EXTERND_APPLY_MAX_BATCH

@@ -79,7 +79,7 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(double) * (size_t)(BBP * ntmax),          // 29 tpm
       sizeof(int) * (size_t)(BBP * ntmax),             // 30 tpi
       sizeof(unsigned short) * (size_t)(BBP * L.m_pad),  // 31 Ub
-      0,                                               // 32 (unused)
+      sizeof(unsigned long long) * (size_t)L.nblk_cap, // 32 argkey
       sizeof(int) * 2 * 4096,                          // 33 gacc
   };
   size_t o = 0;
@@ -140,6 +140,7 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.tpm = (double*)(b + L.off[29]);
   w.tpi = (int*)(b + L.off[30]);
   w.Ub = (unsigned short*)(b + L.off[31]);
+  w.argkey = (unsigned long long*)(b + L.off[32]);
   w.gacc = (int*)(b + L.off[33]);
   return true;
 }
@@ -313,17 +314,21 @@ static hipError_t run_sweeps(const Ws& w, int64_t k, int b_eff, double tau, int3
 // target: NaN for the full run; else stop after the first block whose
 // energy (E, or E_w with weights) reaches it, reporting *k_used.
 // sweeps: refinement sweeps after a full run (0 = none).
+// lam: h~ = h / max(h) + lam (Sec. 2.5).  safeguard: the single-entry
+// option of Proposition 2 per block (plain objective), counted in *fired.
 static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
                           const float* importance, uint8_t* B_packed, uint8_t* C_packed, float* D, double* energy,
                           double* energy_w, double* energy_curve, double* energy_w_curve, void* workspace,
                           size_t workspace_bytes, void* stream, externd_kernel_times* times,
                           double target = NAN, int64_t* k_used = nullptr, int32_t sweeps = 0,
                           double* sweep_energy = nullptr, double* sweep_energy_w = nullptr,
-                          int64_t* accepted = nullptr) {
+                          int64_t* accepted = nullptr, double lam = 0.0, bool safeguard = false,
+                          int64_t* fired = nullptr) {
   if (energy) *energy = NAN;
   if (energy_w) *energy_w = NAN;
   if (!A || !B_packed || !C_packed || !D || !energy || !workspace) return EXTERND_EINVAL;
   if (m < 1 || n < 1 || !isfinite(tau) || tau < 0.0 || block < 1 || iters < 1 || sweeps < 0) return EXTERND_EINVAL;
+  if (!isfinite(lam) || lam < 0.0 || (safeguard && importance)) return EXTERND_EINVAL;
   const bool stop_at_target = !isnan(target);
   if (stop_at_target && (!isfinite(target) || !k_used || sweeps > 0)) return EXTERND_EINVAL;
   const int64_t k = externd_rank(m, n, mu);
@@ -339,8 +344,8 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   timer.stream = s;
   Timer* tm = times ? &timer : nullptr;
 
-  HIP_TRY(launch_prep(w, importance, s));
-  HIP_TRY(launch_stage(w, A, n, s));
+  HIP_TRY(launch_prep(w, importance, s, lam));
+  HIP_TRY(launch_stage(w, A, n, s, safeguard));
   int flags[FLAG_COUNT];
   HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
@@ -364,8 +369,9 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
       HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm));
     }
     HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
-    HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s));
-    HIP_TRY(launch_deflate(w, (int)blk, false, s, tm));
+    if (safeguard) HIP_TRY(launch_safeguard(w, (int)blk, bb, D + c0, s));
+    HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s, false, safeguard));
+    HIP_TRY(launch_deflate(w, (int)blk, false, s, tm, safeguard));
     if (stop_at_target && blk + 1 < nblk) {
       // energy after this block (||R||^2 history entries 0 and blk + 1)
       HIP_TRY(launch_finish(w, (int)blk + 1, s));
@@ -393,12 +399,14 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   if (sweeps > 0)
     HIP_TRY(run_sweeps(w, k, b_eff, tau, iters, sweeps, weighted, B_packed, C_packed, D, (int)nblk, f2[0], f2w[0], so,
                        s, tm));
-  unsigned n_acc = 0;
+  unsigned n_acc = 0, n_fired = 0;
   HIP_TRY(hipMemcpyAsync(&n_acc, w.counters + CNT_ACCEPTED, sizeof(unsigned), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(&n_fired, w.counters + CNT_SAFEGUARD, sizeof(unsigned), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (flags[FLAG_SYNC]) return EXTERND_ESYNC;
   if (accepted) *accepted = (int64_t)n_acc;
+  if (fired) *fired = (int64_t)n_fired;
   if (tm) {
     HIP_TRY(tm->collect(times->total_ms, times->launches, EXTERND_KCLASS_COUNT));
     for (int c = 0; c < EXTERND_KCLASS_COUNT; ++c) times->issued[c] = tm->seen[c];
@@ -447,6 +455,21 @@ int externd_factorize_refined(const float* A, int64_t m, int64_t n, double mu, d
   return factorize_impl(A, m, n, mu, tau, block, iters, importance, B_packed, C_packed, D, energy, energy_w,
                         energy_curve, energy_w_curve, workspace, workspace_bytes, stream, nullptr, NAN, nullptr,
                         sweeps, sweep_energy, sweep_energy_w, accepted);
+}
+
+int externd_factorize_ex(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block, int32_t iters,
+                         const float* importance, double lambda, int32_t safeguard, uint8_t* B_packed,
+                         uint8_t* C_packed, float* D, double* energy, double* energy_w, double* energy_curve,
+                         double* energy_w_curve, int64_t* safeguard_fired, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  if (safeguard_fired) *safeguard_fired = 0;
+  if (safeguard != 0 && safeguard != 1) {
+    if (energy) *energy = NAN;
+    return EXTERND_EINVAL;
+  }
+  return factorize_impl(A, m, n, mu, tau, block, iters, importance, B_packed, C_packed, D, energy, energy_w,
+                        energy_curve, energy_w_curve, workspace, workspace_bytes, stream, nullptr, NAN, nullptr, 0,
+                        nullptr, nullptr, nullptr, lambda, safeguard == 1, safeguard_fired);
 }
 
 int externd_factorize_timed(const float* A, int64_t m, int64_t n, double mu, double tau, int32_t block,

@@ -37,9 +37,12 @@ constexpr int TERN_CHUNK = 640;
 // to zero by the workgroup that consumes it).
 // CNT_DECISION: the last refinement revisit kept its new block (1) or not;
 // CNT_ACCEPTED: revisits of the call that kept the new block.
+// CNT_SAFEGUARD: blocks replaced by the single-entry step; CNT_SG_*: the
+// last block's single-entry decision (fired, row, column, negative sign).
 enum Counter {
   CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2,
-  CNT_DECISION = 5, CNT_ACCEPTED = 6, CNT_COUNT = 8
+  CNT_DECISION = 5, CNT_ACCEPTED = 6, CNT_SAFEGUARD = 7,
+  CNT_SG_FIRE = 8, CNT_SG_ROW = 9, CNT_SG_COL = 10, CNT_SG_NEG = 11, CNT_COUNT = 16
 };
 // Flags written by the device, read by the host.
 enum Flag { FLAG_NONFINITE = 0, FLAG_BADWEIGHT = 1, FLAG_SYNC = 2, FLAG_COUNT = 4 };
@@ -82,6 +85,7 @@ struct Ws {
   int* J;                // BBP: init columns
   unsigned* maxbits;     // nblk_cap: max|R| (fp32 bits) before each block
   unsigned* maxbits_w;   // nblk_cap: bound on max|R_ij h~_j| (fp32 bits)
+  unsigned long long* argkey;  // nblk_cap: (max|R| bits << 32) | (2^32 - 1 - first row-major index), safeguard only
   double* fro2_hist;     // nblk_cap: ||R||^2 before each block, then after the last
   double* fro2w_hist;    // nblk_cap: weighted ||R||^2
   unsigned* counters;    // CNT_COUNT
@@ -126,8 +130,10 @@ size_t workspace_bytes(int64_t m, int64_t n, int64_t k);
 bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k);
 
 // ---- launchers (all asynchronous on `s`) ----
-hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s);
-hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s);
+// lam: h~ = h / max(h) + lam (Sec. 2.5).
+hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s, double lam = 0.0);
+// track: also the position of the largest |R| entry (argkey slot 0).
+hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s, bool track = false);
 hipError_t launch_select(const Ws& w, int blk, int bb, hipStream_t s);
 hipError_t launch_finish(const Ws& w, int blk, hipStream_t s);
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s);
@@ -143,12 +149,19 @@ hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
 // revisit: the scales were settled by launch_revisit_decide, whose decision
 // selects the new block (written out) or the old one (operands rebuilt from
 // the packed outputs).
+// safeguard: the scales were settled by launch_safeguard, and a block it
+// replaced is written out as its single entry.
 hipError_t launch_block_out(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
-                            hipStream_t s, bool revisit = false);
+                            hipStream_t s, bool revisit = false, bool safeguard = false);
+// Joint scale solve of the block before slot blk's residual is deflated,
+// with the single-entry option of Proposition 2 (D_block: D + c0).
+hipError_t launch_safeguard(const Ws& w, int blk, int bb, float* D_block, hipStream_t s);
 // transposes: rebuild the row-major factor copies from Ut/Vt first (step
 // entry point).  Writes max|R| of the result into slot blk + 1.
-hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, Timer* t = nullptr);
-hipError_t launch_deflate_slot(const Ws& w, int out_slot, hipStream_t s, Timer* t = nullptr);
+// track: also the position of the largest |R| entry (argkey of the slot).
+hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, Timer* t = nullptr,
+                          bool track = false);
+hipError_t launch_deflate_slot(const Ws& w, int out_slot, hipStream_t s, Timer* t = nullptr, bool track = false);
 // Refinement revisit of the block at columns c0 .. c0+bb-1: decode it from
 // the packed outputs (clearing residual-bound slots slot1 and slot2), and
 // after the fit choose between the new and the old block by the objective

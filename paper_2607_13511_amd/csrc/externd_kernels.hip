@@ -1407,7 +1407,28 @@ __global__ __launch_bounds__(NT) void k_scale(int* gacc, int bb, const double* _
 // grid: (n_pad/32 column strips) x gd row groups; each wave takes 32-row
 // tiles of its WG's group.  B = d-weighted V (3 exact bf16 parts of d),
 // A = U (exact bf16).
+// TRACK: also the largest |R| entry with its first row-major position, as
+// one 64-bit key per slot (see argmax_key), for the single-entry option of
+// Proposition 2.
 // ---------------------------------------------------------------------------
+// Key ordering the entries of R by |R| (fp32 bits, monotone for values
+// >= 0), then by the smaller row-major index i * n + j.
+__device__ __forceinline__ unsigned long long argmax_key(float absval, unsigned flat) {
+  return ((unsigned long long)__float_as_uint(absval) << 32) | (unsigned long long)(0xFFFFFFFFu - flat);
+}
+// (value, index) pairs of a wave combined towards lane 0: larger value,
+// then smaller index.
+__device__ __forceinline__ void wave_argmax(float& v, unsigned& idx) {
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_down(v, o, 64);
+    const unsigned oi = __shfl_down(idx, o, 64);
+    if (ov > v || (ov == v && oi < idx)) {
+      v = ov;
+      idx = oi;
+    }
+  }
+}
+
 __device__ __forceinline__ unsigned short bf16_bits_trunc(float x) { return (unsigned short)(__float_as_uint(x) >> 16); }
 __device__ __forceinline__ float bf16_to_f(unsigned short b) { return __uint_as_float((unsigned)b << 16); }
 __device__ __forceinline__ short tern_bf16(int8_t t, unsigned short mag) {
@@ -1415,14 +1436,18 @@ __device__ __forceinline__ short tern_bf16(int8_t t, unsigned short mag) {
   return (short)(t == 0 ? 0 : (t > 0 ? mag : (unsigned short)(mag ^ 0x8000u)));
 }
 
+template <bool TRACK>
 __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s* __restrict__ Ub,
                                                 const int8_t* __restrict__ Vr, const float* __restrict__ dF,
                                                 double* __restrict__ colE_part, unsigned* __restrict__ maxbits_next,
                                                 unsigned* __restrict__ maxbits_w_next, const double* __restrict__ hw,
-                                                int64_t m_pad, int64_t n_pad, int gd) {
+                                                int64_t m_pad, int64_t n_pad, int gd,
+                                                unsigned long long* __restrict__ argkey_next, int64_t n) {
   __shared__ double colsum[4][32];
   __shared__ float wmax[4];
   __shared__ float wmaxw[4];
+  __shared__ float amax[4];
+  __shared__ unsigned aidx[4];
   const int nct = (int)(n_pad / TILE);
   const int ct = blockIdx.x % nct, g = blockIdx.x / nct;
   const int nrt = (int)(m_pad / TILE);
@@ -1454,6 +1479,10 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
   }
   double csum = 0.0;
   float vmax = 0.0f;
+  // TRACK: this lane's first (smallest row) largest |R|; zero entries
+  // (including the padding) never replace the start value
+  float tmax = 0.0f;
+  unsigned tidx = 0xFFFFFFFFu;
   // software pipeline: the residual values and U fragments of the wave's
   // next row tile (rt + 4, other rows) are loaded before this tile is
   // updated and stored
@@ -1492,6 +1521,10 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
       R[(i0 + row) * n_pad + col] = v;
       csum += (double)v * (double)v;
       vmax = fmaxf(vmax, fabsf(v));
+      if (TRACK && fabsf(v) > tmax) {
+        tmax = fabsf(v);
+        tidx = (unsigned)((i0 + row) * n + col);
+      }
     }
   }
   // combine the two half-waves (same column), then the 4 waves in order
@@ -1501,10 +1534,15 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
     vmax = fmaxf(vmax, __shfl_down(vmax, o, 64));
     vmaxw = fmaxf(vmaxw, __shfl_down(vmaxw, o, 64));
   }
+  if (TRACK) wave_argmax(tmax, tidx);
   if (h == 0) colsum[wave][l32] = csum;
   if (lane == 0) {
     wmax[wave] = vmax;
     wmaxw[wave] = vmaxw;
+    if (TRACK) {
+      amax[wave] = tmax;
+      aidx[wave] = tidx;
+    }
   }
   __syncthreads();
   if (threadIdx.x < 32) {
@@ -1516,6 +1554,14 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
     const float mxw = fmaxf(fmaxf(wmaxw[0], wmaxw[1]), fmaxf(wmaxw[2], wmaxw[3]));
     atomicMax(maxbits_next, __float_as_uint(mx));
     atomicMax(maxbits_w_next, __float_as_uint(mxw));
+    if (TRACK) {
+      unsigned long long key = 0ull;
+      for (int q = 0; q < 4; ++q) {
+        const unsigned long long kq = argmax_key(amax[q], aidx[q]);
+        key = kq > key ? kq : key;
+      }
+      atomicMax(argkey_next, key);
+    }
   }
 }
 
@@ -1523,14 +1569,17 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
 // Staging: R <- A (zero padded), column energies (fp64 partials), max|A|,
 // non-finite detection.  grid: (n_pad/32) x gd; thread (row lane, column).
 // ---------------------------------------------------------------------------
+template <bool TRACK>
 __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64_t lda, int64_t m, int64_t n,
                                               float* __restrict__ R, double* __restrict__ colE_part,
                                               unsigned* __restrict__ maxbits0, unsigned* __restrict__ maxbits_w0,
                                               const double* __restrict__ hw, int* flags, int64_t m_pad,
-                                              int64_t n_pad, int gd) {
+                                              int64_t n_pad, int gd, unsigned long long* __restrict__ argkey0) {
   __shared__ double colsum[8][32];
   __shared__ float smax[NT / 64];
   __shared__ float smaxw[NT / 64];
+  __shared__ float amax[NT / 64];
+  __shared__ unsigned aidx[NT / 64];
   const int nct = (int)(n_pad / TILE);
   const int ct = blockIdx.x % nct, g = blockIdx.x / nct;
   const int64_t r0 = (int64_t)g * m_pad / gd, r1 = (int64_t)(g + 1) * m_pad / gd;
@@ -1538,6 +1587,8 @@ __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64
   const int64_t j = (int64_t)ct * TILE + cl;
   double cs = 0.0;
   float vmax = 0.0f;
+  float tmax = 0.0f;            // TRACK: first (smallest row) largest |A| of this thread
+  unsigned tidx = 0xFFFFFFFFu;
   int bad = 0;
   const double hwj = hw[j];
   for (int64_t i = r0 + rl; i < r1; i += 8) {
@@ -1550,6 +1601,10 @@ __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64
     R[i * n_pad + j] = v;
     cs += (double)v * (double)v;
     vmax = fmaxf(vmax, fabsf(v));
+    if (TRACK && fabsf(v) > tmax) {
+      tmax = fabsf(v);
+      tidx = (unsigned)(i * n + j);
+    }
   }
   colsum[rl][cl] = cs;
   float vmaxw = weighted_abs_bound(vmax, hwj);
@@ -1557,9 +1612,14 @@ __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64
     vmax = fmaxf(vmax, __shfl_down(vmax, o, 64));
     vmaxw = fmaxf(vmaxw, __shfl_down(vmaxw, o, 64));
   }
+  if (TRACK) wave_argmax(tmax, tidx);
   if (lane_id() == 0) {
     smax[wave_id()] = vmax;
     smaxw[wave_id()] = vmaxw;
+    if (TRACK) {
+      amax[wave_id()] = tmax;
+      aidx[wave_id()] = tidx;
+    }
   }
   if (bad) flags[FLAG_NONFINITE] = 1;
   __syncthreads();
@@ -1576,6 +1636,14 @@ __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64
     }
     atomicMax(maxbits0, __float_as_uint(mx));
     atomicMax(maxbits_w0, __float_as_uint(mxw));
+    if (TRACK) {
+      unsigned long long key = 0ull;
+      for (int w = 0; w < NT / 64; ++w) {
+        const unsigned long long kw = argmax_key(amax[w], aidx[w]);
+        key = kw > key ? kw : key;
+      }
+      atomicMax(argkey0, key);
+    }
   }
 }
 
@@ -1589,12 +1657,14 @@ __global__ __launch_bounds__(NT) void k_unstage(const float* __restrict__ R, flo
   }
 }
 
-// Weights and bookkeeping (1 WG): h~ = h / max(h) in fp64 (ones when no
-// weights), zero padding; clear counters, flags and the per-block arrays.
+// Weights and bookkeeping (1 WG): h~ = h / max(h) + lam in fp64 (Sec. 2.5;
+// ones when no weights), zero padding; clear counters, flags and the
+// per-block arrays.
 __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_t n, int64_t n_pad,
                                              double* __restrict__ hw, unsigned* maxbits, unsigned* maxbits_w,
                                              double* fro2_hist, double* fro2w_hist, int nblk_cap,
-                                             unsigned* counters, int* flags, int* gacc) {
+                                             unsigned* counters, int* flags, int* gacc, double lam,
+                                             unsigned long long* argkey) {
   __shared__ float smax[NT / 64];
   __shared__ int sbad[NT / 64];
   for (int e = threadIdx.x; e < nblk_cap; e += NT) {
@@ -1602,6 +1672,7 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
     maxbits_w[e] = 0u;
     fro2_hist[e] = 0.0;
     fro2w_hist[e] = 0.0;
+    argkey[e] = 0ull;
   }
   if (threadIdx.x < CNT_COUNT) counters[threadIdx.x] = 0u;
   for (int e = threadIdx.x; e < 2 * 4096; e += NT) gacc[e] = 0;
@@ -1639,7 +1710,7 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
     return;
   }
   const double dm = (double)gmx;
-  for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? (double)h[j] / dm : 0.0;
+  for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? (double)h[j] / dm + lam : 0.0;
 }
 
 // ---------------------------------------------------------------------------
@@ -1898,6 +1969,9 @@ __device__ __forceinline__ int8_t trit_decode(unsigned byte, int64_t pos) {
 // are settled), and when the old block is kept (decision 0) the tiles
 // rebuild the deflation operands from the packed B and C, which stay as
 // they are.
+// sg: null unless the single-entry option is on; then the scales were
+// settled by k_safeguard, and when it fired (sg[0]) the block written out
+// is u = e_row, v = (+-1) e_col in component 0 and zero components after.
 __global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const double* __restrict__ gramV,
                                                   const double* __restrict__ gvec, double* dvec, float* dF,
                                                   float* Dout, const int8_t* __restrict__ Ut, int8_t* __restrict__ Ur,
@@ -1905,11 +1979,12 @@ __global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const doubl
                                                   int64_t c0, int64_t k, uint8_t* __restrict__ Bp,
                                                   const int8_t* __restrict__ Vt, int8_t* __restrict__ Vr, int64_t n,
                                                   int64_t n_pad, uint8_t* __restrict__ Cp,
-                                                  const unsigned* __restrict__ decision) {
+                                                  const unsigned* __restrict__ decision,
+                                                  const unsigned* __restrict__ sg) {
   __shared__ double Gs[4096];
   __shared__ double colbuf[1024];
   if (blockIdx.x == 0) {
-    if (!decision) scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf);
+    if (!decision && !sg) scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf);
     return;
   }
   int8_t (*tile)[BBP + 4] = (int8_t (*)[BBP + 4])Gs;  // 32 x 68 bytes
@@ -1919,7 +1994,15 @@ __global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const doubl
   const int8_t* Xt = isU ? Ut : Vt;
   const int64_t j0 = (int64_t)(isU ? blockIdx.x - 1 : blockIdx.x - 1 - nut) * 32;
   const bool keep_old = decision && *decision == 0u;
-  if (keep_old) {
+  const bool single = sg && sg[0] != 0u;
+  if (single) {
+    const int64_t at = isU ? (int64_t)sg[1] : (int64_t)sg[2];
+    const int8_t one = (!isU && sg[3]) ? (int8_t)-1 : (int8_t)1;
+    for (int e = threadIdx.x; e < BBP * 32; e += NT) {
+      const int c = e >> 5, jj = e & 31;
+      tile[jj][c] = (c == 0 && j0 + jj == at) ? one : (int8_t)0;
+    }
+  } else if (keep_old) {
     const int64_t pitchB = (k + 3) >> 2, pitchC = (n + 3) >> 2;
     for (int e = threadIdx.x; e < BBP * 32; e += NT) {
       const int c = e >> 5, jj = e & 31;
@@ -2077,6 +2160,52 @@ __global__ __launch_bounds__(NT) void k_revisit_decide(int* gacc, int bb, const 
 }
 
 // ---------------------------------------------------------------------------
+// Single-entry option of Proposition 2 for a block (plain objective): after
+// the Eq. (4) solve, the objective the block removes, 2 d^T g - d^T M d
+// (= d^T g + delta ||d||^2 for the guarded solve), is compared with the
+// largest squared residual entry R_ij^2 (first in row-major order on
+// ties).  When the entry is strictly larger the block becomes the single
+// component u = e_i, v = sign(R_ij) e_j, d = |R_ij| followed by zero
+// components; k_block_out writes it out and the deflation removes R_ij
+// exactly.  sg receives (fired, i, j, R_ij < 0); *fired counts the blocks.
+// grid: one WG.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NT) void k_safeguard(int* gacc, int bb, const double* __restrict__ gramV,
+                                                  const double* __restrict__ gvec, double* dvec, float* dF,
+                                                  float* Dout, const float* __restrict__ R, int64_t n, int64_t n_pad,
+                                                  const unsigned long long* __restrict__ argkey, unsigned* sg,
+                                                  unsigned* fired) {
+  __shared__ double Gs[4096];
+  __shared__ double colbuf[1024];
+  const double gain = scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf, true);
+  const unsigned long long key = *argkey;
+  const float rmax = __uint_as_float((unsigned)(key >> 32));
+  const bool fire = rmax > 0.0f && (double)rmax * (double)rmax > gain;
+  const int t = threadIdx.x;
+  // thread t wrote dvec[t], dF[t] and Dout[t] in the solve
+  if (fire && t < BBP) {
+    const float dv = t == 0 ? rmax : 0.0f;
+    dvec[t] = (double)dv;
+    dF[t] = dv;
+    if (t < bb) Dout[t] = dv;
+  }
+  if (t == 0) {
+    unsigned i = 0u, j = 0u, neg = 0u;
+    if (fire) {
+      const unsigned flat = 0xFFFFFFFFu - (unsigned)(key & 0xFFFFFFFFull);
+      i = (unsigned)(flat / (unsigned long long)n);
+      j = (unsigned)(flat % (unsigned long long)n);
+      neg = R[(int64_t)i * n_pad + j] < 0.0f ? 1u : 0u;
+      *fired += 1u;
+    }
+    sg[0] = fire ? 1u : 0u;
+    sg[1] = i;
+    sg[2] = j;
+    sg[3] = neg;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // step-entry helpers: caller layouts <-> workspace layouts
 // ---------------------------------------------------------------------------
 // X: len x bb row-major int8 -> Xt (BBP x len_pad) and Xr (len_pad x BBP), zero padded.
@@ -2182,16 +2311,20 @@ static inline unsigned grid_for(int64_t total) {
   return (unsigned)g;
 }
 
-hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s) {
+hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s, double lam) {
   hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.maxbits, w.maxbits_w, w.fro2_hist,
-                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc);
+                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc, lam, w.argkey);
   return hipGetLastError();
 }
 
-hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s) {
+hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s, bool track) {
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
-  hipLaunchKernelGGL(k_stage, dim3(grid), dim3(NT), 0, s, A, lda, w.m, w.n, w.R, w.colE_part, w.maxbits,
-                     w.maxbits_w, w.hw, w.flags, w.m_pad, w.n_pad, w.gd);
+  if (track)
+    hipLaunchKernelGGL(k_stage<true>, dim3(grid), dim3(NT), 0, s, A, lda, w.m, w.n, w.R, w.colE_part, w.maxbits,
+                       w.maxbits_w, w.hw, w.flags, w.m_pad, w.n_pad, w.gd, w.argkey);
+  else
+    hipLaunchKernelGGL(k_stage<false>, dim3(grid), dim3(NT), 0, s, A, lda, w.m, w.n, w.R, w.colE_part, w.maxbits,
+                       w.maxbits_w, w.hw, w.flags, w.m_pad, w.n_pad, w.gd, (unsigned long long*)nullptr);
   return hipGetLastError();
 }
 
@@ -2278,11 +2411,18 @@ hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
 }
 
 hipError_t launch_block_out(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
-                           hipStream_t s, bool revisit) {
+                           hipStream_t s, bool revisit, bool safeguard) {
   const unsigned grid = (unsigned)(1 + w.m_pad / TILE + w.n_pad / TILE);
   hipLaunchKernelGGL(k_block_out, dim3(grid), dim3(NT), 0, s, w.gacc, bb, w.gramV, w.gvec, w.dvec, w.dF, D + c0,
                      w.Ut, w.Ur, w.Ub, w.m, w.m_pad, c0, k, Bp, w.Vt, w.Vr, w.n, w.n_pad, Cp,
-                     revisit ? (const unsigned*)(w.counters + CNT_DECISION) : nullptr);
+                     revisit ? (const unsigned*)(w.counters + CNT_DECISION) : nullptr,
+                     safeguard ? (const unsigned*)(w.counters + CNT_SG_FIRE) : nullptr);
+  return hipGetLastError();
+}
+hipError_t launch_safeguard(const Ws& w, int blk, int bb, float* D_block, hipStream_t s) {
+  hipLaunchKernelGGL(k_safeguard, dim3(1), dim3(NT), 0, s, w.gacc, bb, w.gramV, w.gvec, w.dvec, w.dF, D_block,
+                     (const float*)w.R, w.n, w.n_pad, (const unsigned long long*)(w.argkey + blk),
+                     w.counters + CNT_SG_FIRE, w.counters + CNT_SAFEGUARD);
   return hipGetLastError();
 }
 hipError_t launch_revisit_load(const Ws& w, const uint8_t* Bp, const uint8_t* Cp, const float* D, int64_t c0, int bb,
@@ -2300,7 +2440,7 @@ hipError_t launch_revisit_decide(const Ws& w, int bb, float* D_block, bool weigh
   return hipGetLastError();
 }
 
-hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, Timer* tm) {
+hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, Timer* tm, bool track) {
   hipError_t e;
   if (transposes) {
     hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.m_pad / 32)), dim3(NT), 0, s, w.Ut, w.Ur, w.m_pad, w.Ub);
@@ -2311,12 +2451,18 @@ hipError_t launch_deflate(const Ws& w, int blk, bool transposes, hipStream_t s, 
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  return launch_deflate_slot(w, blk + 1, s, tm);
+  return launch_deflate_slot(w, blk + 1, s, tm, track);
 }
-hipError_t launch_deflate_slot(const Ws& w, int out_slot, hipStream_t s, Timer* tm) {
+hipError_t launch_deflate_slot(const Ws& w, int out_slot, hipStream_t s, Timer* tm, bool track) {
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
-  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_DEFLATE, k_deflate, dim3(grid), dim3(NT), 0, s, w.R, (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part,
-                                   w.maxbits + out_slot, w.maxbits_w + out_slot, w.hw, w.m_pad, w.n_pad, w.gd);
+  if (track)
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_DEFLATE, k_deflate<true>, dim3(grid), dim3(NT), 0, s, w.R, (const v8s*)w.Ub,
+                         w.Vr, w.dF, w.colE_part, w.maxbits + out_slot, w.maxbits_w + out_slot, w.hw, w.m_pad, w.n_pad,
+                         w.gd, w.argkey + out_slot, w.n);
+  else
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_DEFLATE, k_deflate<false>, dim3(grid), dim3(NT), 0, s, w.R,
+                         (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part, w.maxbits + out_slot, w.maxbits_w + out_slot, w.hw,
+                         w.m_pad, w.n_pad, w.gd, (unsigned long long*)nullptr, w.n);
   return hipGetLastError();
 }
 

@@ -13,6 +13,8 @@ recipes below stand in for them:
                    (Var t_4 = 2, so the draw is multiplied by std / sqrt(2))
 * ``t4_outliers``  t4 plus ``n_outlier_cols`` columns scaled by 10
 * ``t4_rowscale``  t4 with row i multiplied by exp(N(0, 0.3^2))
+* ``spiky``        N(0, 0.05^2) with a few isolated entries of magnitude 1-3
+                   (test input for the single-entry safeguard)
 * importance       h_j = exp(N(0, 1)), with 1% of columns boosted x50
 
 All draws use numpy's PCG64.  Named workloads use
@@ -126,7 +128,20 @@ def small(kind: str, m: int, n: int, seed: int, std: float = 0.02) -> np.ndarray
         return t4_outliers(m, n, std, max(1, n // 256), rng, np.random.default_rng(np.random.SeedSequence([2, seed, m, n])))
     if kind == "t4_rowscale":
         return t4_rowscale(m, n, std, 0.3, rng, np.random.default_rng(np.random.SeedSequence([3, seed, m, n])))
+    if kind == "spiky":
+        return spiky(m, n, seed)
     raise ValueError(kind)
+
+
+def spiky(m: int, n: int, seed: int, spikes: int = 3, std: float = 0.05) -> np.ndarray:
+    """N(0, std^2) background with ``spikes`` isolated entries of magnitude
+    U(1, 3) and random sign: a residual whose single largest entry is worth
+    more than a dense ternary component (exercises the single-entry step)."""
+    rng = np.random.default_rng(np.random.SeedSequence([6, seed, m, n]))
+    A = rng.standard_normal((m, n)) * std
+    for _ in range(spikes):
+        A[rng.integers(m), rng.integers(n)] = rng.choice([-1.0, 1.0]) * rng.uniform(1.0, 3.0)
+    return A.astype(np.float32)
 
 
 def small_importance(n: int, seed: int) -> np.ndarray:

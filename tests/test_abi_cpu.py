@@ -94,6 +94,19 @@ def test_argument_errors_before_device_work():
              None, None, None, dummy, 1 << 30, None) == binding.EINVAL
     assert r(dummy, 10, 10, 1.0, 0.7, 1, 1, 2, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
              None, None, None, dummy, 16, None) == binding.EWORKSPACE
+    # lambda and safeguard options: lambda finite and >= 0, safeguard 0 or 1
+    # and only for the plain objective
+    x = L.externd_factorize_ex
+    fired = ctypes.c_int64(5)
+    for lam, sg, imp in [(-0.5, 0, dummy), (float("nan"), 0, dummy), (float("inf"), 0, None), (0.0, 2, None),
+                         (0.0, -1, None), (0.0, 1, dummy), (1.0, 1, dummy)]:
+        assert x(dummy, 10, 10, 1.0, 0.7, 1, 1, imp, lam, sg, dummy, dummy, dummy, ctypes.byref(E), None, None,
+                 None, ctypes.byref(fired), dummy, 1 << 30, None) == binding.EINVAL
+        assert np.isnan(E.value) and fired.value == 0
+    assert x(None, 10, 10, 1.0, 0.7, 1, 1, None, 0.0, 1, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             None, dummy, 1 << 30, None) == binding.EINVAL
+    assert x(dummy, 10, 10, 1.0, 0.7, 1, 1, None, 0.0, 1, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             None, dummy, 16, None) == binding.EWORKSPACE
     # inference: batch limits, workspace size and alignment
     ap = L.externd_apply
     assert L.externd_apply_workspace_bytes(100, 1) == 400 and L.externd_apply_workspace_bytes(100, 3) == 1600
