@@ -30,6 +30,10 @@ import numpy as np  # noqa: E402
 METRIC = "sec/matrix + ALS components/sec at 9728×2560 μ=3 τ=1.0; energy preserved E"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, published
+# The one-launch sequential path runs in a single workgroup, i.e. on one of
+# the 256 compute units: its ceiling is one CU's share of the published fp32
+# vector rate (157.3 TFLOP/s / 256).
+CU_FP32_PEAK_GFLOPS = 157.3e3 / 256
 KERNEL_SOURCES = ["paper_2607_13511_amd/csrc/externd_kernels.hip"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
 
@@ -60,6 +64,15 @@ def vstep_row_groups(m: int, n: int) -> int:
     about 480 column-tile x row-group workgroups, at most 8)."""
     nct, nrt = -(-n // 32), -(-m // 32)
     return max(1, min(-(-480 // nct), min(nrt, 8)))
+
+
+def seq_flops(m: int, n: int, k: int, iters: int) -> float:
+    """Algorithmic flops of one factorization on the one-launch sequential
+    path: per component, each ALS iteration contracts the residual twice
+    (R^T u and R diag(h~) v: a multiply-add per entry, 2 m n flops each),
+    and the deflation and the column energies take one more multiply-add
+    per entry each (2 m n flops each)."""
+    return float(k) * (4.0 * iters + 4.0) * m * n
 
 
 def algorithmic_bytes(kclass: str, m: int, n: int) -> float:
@@ -146,7 +159,7 @@ def collect_traffic(dbs, copy_bytes: int):
     copy_f = max(v[1] for k, v in cfetch.items() if "copyBuffer" in k)
     copy_w = max(v[1] for k, v in cwrite.items() if "copyBuffer" in k)
     ff, fw = copy_bytes / copy_f, copy_bytes / copy_w
-    classes = {"vstep_contraction": "k_vstep", "ustep_contraction": "k_ustep<false>", "deflate": "k_deflate",
+    classes = {"vstep_contraction": "k_vstep", "ustep_contraction": "k_ustep<false>", "deflate": "k_deflate<false>",
                "vstep_target": "k_vtarget", "ustep_target": "k_utarget"}
     out = {"kernel_source_sha256": kernel_source_hash(), "copy_bytes": copy_bytes,
            "fetch_scale": ff, "write_scale": fw, "kernels": {}}
@@ -255,18 +268,31 @@ def main():
     print(f"bench: timed {args.steps} steps, {sec_per_matrix * 1e3:.2f} ms/matrix E={res.E:.6f}",
           file=sys.stderr, flush=True)
 
+    ktot = {kc: v for kc, v in ktot.items() if v[1] > 0}      # classes this workload launches
     # dominant kernel class by summed duration
     dom = max(ktot, key=lambda kc: ktot[kc][0] / max(1, ktot[kc][1]) * ktot[kc][2])
     dom_ms, dom_cnt, _ = ktot[dom]
     avg_s = dom_ms / dom_cnt / 1e3
-    abytes = algorithmic_bytes(dom, m, n)
-    achieved = abytes / avg_s / 1e9
-    roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_from_counters(dom),
-                "kernel": dom, "avg_launch_us": avg_s * 1e6, "algorithmic_bytes_per_launch": abytes}
+    if dom == "sequential_one_launch":
+        flops = seq_flops(m, n, k, w.iters)
+        achieved = flops / avg_s / 1e9
+        roofline = {"bound": "alu", "achieved": achieved, "peak": CU_FP32_PEAK_GFLOPS, "unit": "GFLOP/s",
+                    "frac": achieved / CU_FP32_PEAK_GFLOPS, "traffic": None, "kernel": dom,
+                    "avg_launch_us": avg_s * 1e6, "algorithmic_flops_per_launch": flops,
+                    "note": "one workgroup on one compute unit; peak = 157.3 TFLOP/s fp32 vector / 256 CUs"}
+    else:
+        abytes = algorithmic_bytes(dom, m, n)
+        achieved = abytes / avg_s / 1e9
+        roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_from_counters(dom),
+                    "kernel": dom, "avg_launch_us": avg_s * 1e6, "algorithmic_bytes_per_launch": abytes}
     per_kernel = {}
     for kc, (ms, cnt, issued) in ktot.items():
         avg = ms / cnt / 1e3
+        if kc == "sequential_one_launch":
+            per_kernel[kc] = {"launches_per_matrix": issued // args.steps, "avg_us": avg * 1e6,
+                              "GFLOP_s": seq_flops(m, n, k, w.iters) / avg / 1e9, "share_of_step": avg * issued / dt}
+            continue
         gbs = algorithmic_bytes(kc, m, n) / avg / 1e9
         # one launch in binding.TIMING_STRIDE is timed (events on the library's stream)
         per_kernel[kc] = {"timed_launches_per_matrix": cnt / args.steps,
@@ -308,8 +334,10 @@ def main():
         "energy": res.E,
         "energy_w": res.E_w,
         "energy_checkpoints": checkpoints,
-        "arithmetic": "fp32 residual; exact int8-MFMA contractions of 32-bit fixed point; fp64 targets/solves; "
-                      "bf16-MFMA deflation with fp32 accumulation",
+        "arithmetic": ("fp32 residual in registers of one workgroup; fp32 per-thread partial sums combined in "
+                       "fp64; fp64 thresholds, scales and energies") if dom == "sequential_one_launch" else
+                      ("fp32 residual; exact int8-MFMA contractions of 32-bit fixed point; fp64 targets/solves; "
+                       "bf16-MFMA deflation with fp32 accumulation"),
         "roofline": roofline,
         "kernels": per_kernel,
         "cpu_baseline": cpu,

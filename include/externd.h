@@ -240,7 +240,9 @@ int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float*
 #define EXTERND_KCLASS_DEFLATE 2  /* deflation R -= U diag(d) V^T (+ column energies)   */
 #define EXTERND_KCLASS_VTARGET 3  /* V-step target Y = G_U^{-1} P and its statistics    */
 #define EXTERND_KCLASS_UTARGET 4  /* U-step target Z = Q G_V^{-1} and its statistics    */
-#define EXTERND_KCLASS_COUNT   5
+#define EXTERND_KCLASS_SEQ     5  /* the one-launch sequential path (block width 1 on a
+                                     small matrix: every launch is timed)              */
+#define EXTERND_KCLASS_COUNT   6
 
 typedef struct {
   double total_ms[EXTERND_KCLASS_COUNT];  /* summed durations of the timed launches */

@@ -344,52 +344,65 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   timer.stream = s;
   Timer* tm = times ? &timer : nullptr;
 
-  HIP_TRY(launch_prep(w, importance, s, lam));
-  HIP_TRY(launch_stage(w, A, n, s, safeguard));
+  // Block width 1 on a small matrix: the whole extraction in one launch.
+  const bool one_launch = b_eff == 1 && sweeps == 0 && seq_supported(m, n);
   int flags[FLAG_COUNT];
-  HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
-  if (flags[FLAG_BADWEIGHT]) return EXTERND_EINVAL;
-  if (flags[FLAG_NONFINITE]) return EXTERND_ENONFINITE;
+  HIP_TRY(launch_prep(w, importance, s, lam));
   if (stop_at_target) {
     // components past the stop stay zero
     HIP_TRY(hipMemsetAsync(B_packed, 0, (size_t)m * (size_t)((k + 3) / 4), s));
     HIP_TRY(hipMemsetAsync(C_packed, 0, (size_t)k * (size_t)((n + 3) / 4), s));
     HIP_TRY(hipMemsetAsync(D, 0, sizeof(float) * (size_t)k, s));
   }
-
   int64_t nblk_done = nblk;
-  for (int64_t blk = 0; blk < nblk; ++blk) {
-    const int64_t c0 = blk * b_eff;
-    const int bb = (int)((k - c0) < b_eff ? (k - c0) : b_eff);
-    HIP_TRY(launch_select(w, (int)blk, bb, s));
-    HIP_TRY(launch_init(w, bb, tau, s));
-    for (int it = 0; it < iters; ++it) {
-      HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm));
-      HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm));
-    }
-    HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
-    if (safeguard) HIP_TRY(launch_safeguard(w, (int)blk, bb, D + c0, s));
-    HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s, false, safeguard));
-    HIP_TRY(launch_deflate(w, (int)blk, false, s, tm, safeguard));
-    if (stop_at_target && blk + 1 < nblk) {
-      // energy after this block (||R||^2 history entries 0 and blk + 1)
-      HIP_TRY(launch_finish(w, (int)blk + 1, s));
-      double h2[2][2];
-      HIP_TRY(hipMemcpyAsync(&h2[0][0], w.fro2_hist, sizeof(double), hipMemcpyDeviceToHost, s));
-      HIP_TRY(hipMemcpyAsync(&h2[0][1], w.fro2_hist + blk + 1, sizeof(double), hipMemcpyDeviceToHost, s));
-      HIP_TRY(hipMemcpyAsync(&h2[1][0], w.fro2w_hist, sizeof(double), hipMemcpyDeviceToHost, s));
-      HIP_TRY(hipMemcpyAsync(&h2[1][1], w.fro2w_hist + blk + 1, sizeof(double), hipMemcpyDeviceToHost, s));
-      HIP_TRY(hipStreamSynchronize(s));
-      const double* hv = weighted ? h2[1] : h2[0];
-      const double e = hv[0] == 0.0 ? 1.0 : 1.0 - hv[1] / hv[0];
-      if (e >= target) {
-        nblk_done = blk + 1;
-        break;
+  if (one_launch) {
+    HIP_TRY(launch_seq(w, A, k, tau, iters, weighted, safeguard, stop_at_target ? target : NAN, B_packed, C_packed,
+                       D, s, tm));
+    unsigned used = 0;
+    HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(&used, w.counters + CNT_SEQ_USED, sizeof(unsigned), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (flags[FLAG_BADWEIGHT]) return EXTERND_EINVAL;
+    if (flags[FLAG_NONFINITE]) return EXTERND_ENONFINITE;
+    nblk_done = (int64_t)used;
+  } else {
+    HIP_TRY(launch_stage(w, A, n, s, safeguard));
+    HIP_TRY(hipMemcpyAsync(flags, w.flags, sizeof(flags), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (flags[FLAG_BADWEIGHT]) return EXTERND_EINVAL;
+    if (flags[FLAG_NONFINITE]) return EXTERND_ENONFINITE;
+    for (int64_t blk = 0; blk < nblk; ++blk) {
+      const int64_t c0 = blk * b_eff;
+      const int bb = (int)((k - c0) < b_eff ? (k - c0) : b_eff);
+      HIP_TRY(launch_select(w, (int)blk, bb, s));
+      HIP_TRY(launch_init(w, bb, tau, s));
+      for (int it = 0; it < iters; ++it) {
+        HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm));
+        HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm));
+      }
+      HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
+      if (safeguard) HIP_TRY(launch_safeguard(w, (int)blk, bb, D + c0, s));
+      HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s, false, safeguard));
+      HIP_TRY(launch_deflate(w, (int)blk, false, s, tm, safeguard));
+      if (stop_at_target && blk + 1 < nblk) {
+        // energy after this block (||R||^2 history entries 0 and blk + 1)
+        HIP_TRY(launch_finish(w, (int)blk + 1, s));
+        double h2[2][2];
+        HIP_TRY(hipMemcpyAsync(&h2[0][0], w.fro2_hist, sizeof(double), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(&h2[0][1], w.fro2_hist + blk + 1, sizeof(double), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(&h2[1][0], w.fro2w_hist, sizeof(double), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(&h2[1][1], w.fro2w_hist + blk + 1, sizeof(double), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        const double* hv = weighted ? h2[1] : h2[0];
+        const double e = hv[0] == 0.0 ? 1.0 : 1.0 - hv[1] / hv[0];
+        if (e >= target) {
+          nblk_done = blk + 1;
+          break;
+        }
       }
     }
+    if (nblk_done == nblk) HIP_TRY(launch_finish(w, (int)nblk, s));
   }
-  if (nblk_done == nblk) HIP_TRY(launch_finish(w, (int)nblk, s));
 
   std::vector<double> f2((size_t)nblk_done + 1), f2w((size_t)nblk_done + 1);
   HIP_TRY(hipMemcpyAsync(f2.data(), w.fro2_hist, sizeof(double) * (nblk_done + 1), hipMemcpyDeviceToHost, s));

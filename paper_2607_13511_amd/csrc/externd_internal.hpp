@@ -38,11 +38,12 @@ constexpr int TERN_CHUNK = 640;
 // CNT_DECISION: the last refinement revisit kept its new block (1) or not;
 // CNT_ACCEPTED: revisits of the call that kept the new block.
 // CNT_SAFEGUARD: blocks replaced by the single-entry step; CNT_SG_*: the
-// last block's single-entry decision (fired, row, column, negative sign).
+// last block's single-entry decision (fired, row, column, negative sign);
+// CNT_SEQ_USED: components extracted by the persistent sequential path.
 enum Counter {
   CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2,
   CNT_DECISION = 5, CNT_ACCEPTED = 6, CNT_SAFEGUARD = 7,
-  CNT_SG_FIRE = 8, CNT_SG_ROW = 9, CNT_SG_COL = 10, CNT_SG_NEG = 11, CNT_COUNT = 16
+  CNT_SG_FIRE = 8, CNT_SG_ROW = 9, CNT_SG_COL = 10, CNT_SG_NEG = 11, CNT_SEQ_USED = 12, CNT_COUNT = 16
 };
 // Flags written by the device, read by the host.
 enum Flag { FLAG_NONFINITE = 0, FLAG_BADWEIGHT = 1, FLAG_SYNC = 2, FLAG_COUNT = 4 };
@@ -103,7 +104,10 @@ struct Timer {
   int64_t seen[EXTERND_KCLASS_COUNT] = {};
   // Whether this launch of class cls is one of the sampled ones (every
   // EXTERND_TIMING_STRIDE-th, from the middle of the first stride on).
-  bool sample(int cls) { return (seen[cls]++ % EXTERND_TIMING_STRIDE) == EXTERND_TIMING_STRIDE / 2; }
+  // The one-launch sequential path is always timed.
+  bool sample(int cls) {
+    return (seen[cls]++ % EXTERND_TIMING_STRIDE) == EXTERND_TIMING_STRIDE / 2 || cls == EXTERND_KCLASS_SEQ;
+  }
   // The event pair of the next timed launch (created on first use).
   hipError_t take(int cls, hipEvent_t* a, hipEvent_t* b);
   hipError_t collect(double* total_ms, int64_t* launches, int ncls);
@@ -186,5 +190,12 @@ hipError_t launch_gvec(const Ws& w, int bb, hipStream_t s);
 // X^T X of the factor in Umf (which = 0) or Vmf (which = 1) into its Gram accumulator.
 hipError_t launch_gram_acc(const Ws& w, int which, hipStream_t s);
 hipError_t launch_set_scales(const Ws& w, const double* d, int bb, hipStream_t s);
+// Persistent single-workgroup sequential path (block width 1) for small
+// shapes: the whole extraction in one launch (staging included; weights
+// from launch_prep).  target: NaN, or stop after the first component whose
+// energy reaches it (components extracted in counters[CNT_SEQ_USED]).
+bool seq_supported(int64_t m, int64_t n);
+hipError_t launch_seq(const Ws& w, const float* A, int64_t k, double tau, int iters, bool weighted, bool safeguard,
+                      double target, uint8_t* Bp, uint8_t* Cp, float* D, hipStream_t s, Timer* t = nullptr);
 
 }  // namespace externd
