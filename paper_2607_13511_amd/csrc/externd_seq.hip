@@ -4,24 +4,51 @@
 //
 // Thread (wave w of 8, lane l) holds R[w + 8 r][l + 64 c] for r < NR,
 // c < NC (NR * NC = 128 fp32 values, zero outside m x n), so m <= 8 NR and
-// n <= 64 NC: up to 256 x 256, or 128 x 512.  Per component (Sec. 2.3, with the readings of the block
-// path at b = 1):
-//   init   j* = argmax_j h~_j ||R_:j||^2 (smaller j on ties), u = T(R[:, j*])
-//   iters  v = T(R^T u); u = T(R diag(h~) v)       (Eq. (3) at b = 1: the
-//          ridge and Gram factors are positive scalars, which T ignores)
-//   scale  d = g / (M + delta), g = u^T R diag(h~) v, M = ||u||^2 v^T diag(h~) v,
-//          delta = 1e-12 M (Eq. (4) at b = 1); optionally the single-entry
-//          option of Proposition 2
+// n <= 64 NC: up to 256 x 256, or 128 x 512.  Vectors over the rows or the
+// columns are distributed one entry per thread (entry t in thread t).
+// Per component (Sec. 2.3, with the readings of the block path at b = 1):
+//   init    j* = argmax_j h~_j ||R_:j||^2 (smaller j on ties), u = T(R[:, j*])
+//   iters   v = T(R^T u); u = T(R diag(h~) v)       (Eq. (3) at b = 1: the
+//           ridge and Gram factors are positive scalars, which T ignores)
+//   scale   d = g / (M + delta), g = u^T R diag(h~) v, M = ||u||^2 v^T diag(h~) v,
+//           delta = 1e-12 M (Eq. (4) at b = 1); optionally the single-entry
+//           option of Proposition 2
 //   deflate R -= fp32(d) u v^T, column energies, ||R||^2, weighted ||R||^2
-// Contractions: each thread sums its own terms in fp32 (at most 64), the
-// partial sums are combined across threads in fp64 in a fixed order.
-// Thresholds, scales and energies are fp64.  Deterministic.
+// Contractions: each thread sums its own terms in fp32 (NR rows, or NC
+// columns), and the partial sums are combined across threads in fp64 in a
+// fixed order: through LDS across the waves for R^T u, through an LDS
+// transpose inside each wave for R v.  Block reductions: DPP within a wave
+// (result in lane 63), then the 8 wave results in wave order, read by every
+// thread, so every thread holds bit-identical values and every branch is
+// uniform.  Thresholds, scales and energies are fp64.  Deterministic.
 #include "externd_internal.hpp"
+
+#include <limits.h>
 
 namespace externd {
 
 constexpr int SEQ_NT = 512;
 constexpr int SEQ_WAVES = SEQ_NT / 64;
+constexpr int SEQ_P2_PITCH = 68;  // floats per row of the R v transpose (16-byte rows, banks spread)
+
+// DPP controls (row = 16 lanes): shift right by 1, 2, 4, 8 within a row;
+// broadcast lane 15 of each row to the next row; broadcast lane 31 to the
+// upper half; quad permutations swapping neighbours / pairs.
+constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114, DPP_ROW_SHR8 = 0x118;
+constexpr int DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143;
+constexpr int DPP_QUAD_XOR1 = 0xB1, DPP_QUAD_XOR2 = 0x4E;
+
+// One DPP move of a 64-bit value; lanes whose source lies outside the
+// pattern, or whose row ROWMASK excludes, receive `old`.
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ double dpp_f64(double old, double src) {
+  const unsigned long long o = (unsigned long long)__double_as_longlong(old);
+  const unsigned long long v = (unsigned long long)__double_as_longlong(src);
+  const int lo = __builtin_amdgcn_update_dpp((int)(unsigned)o, (int)(unsigned)v, CTRL, ROWMASK, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(unsigned)(o >> 32), (int)(unsigned)(v >> 32), CTRL, ROWMASK, 0xF,
+                                             false);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
 
 // (value, index) pairs: larger value first, then smaller index.
 __device__ __forceinline__ void seq_argmax_combine(double& v, int& i, double ov, int oi) {
@@ -31,92 +58,166 @@ __device__ __forceinline__ void seq_argmax_combine(double& v, int& i, double ov,
   }
 }
 
-// Block-wide sum of three fp64 values and (max, first index) of one more;
-// every thread receives the same results (xor butterflies are symmetric,
-// the 16 wave results are combined in wave order by every thread).
-struct SeqShared {
-  double s[SEQ_WAVES][4];
-  int i[SEQ_WAVES];
-};
-__device__ __forceinline__ void seq_reduce(double& a, double& b, double& c, double& mx, int& ix, SeqShared& sh) {
-  for (int o = 32; o > 0; o >>= 1) {
-    a += __shfl_xor(a, o, 64);
-    b += __shfl_xor(b, o, 64);
-    c += __shfl_xor(c, o, 64);
-    const double om = __shfl_xor(mx, o, 64);
-    const int oi = __shfl_xor(ix, o, 64);
-    seq_argmax_combine(mx, ix, om, oi);
-  }
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    sh.s[w][0] = a;
-    sh.s[w][1] = b;
-    sh.s[w][2] = c;
-    sh.s[w][3] = mx;
-    sh.i[w] = ix;
-  }
-  __syncthreads();
-  a = sh.s[0][0];
-  b = sh.s[0][1];
-  c = sh.s[0][2];
-  mx = sh.s[0][3];
-  ix = sh.i[0];
-  for (int q = 1; q < SEQ_WAVES; ++q) {
-    a += sh.s[q][0];
-    b += sh.s[q][1];
-    c += sh.s[q][2];
-    seq_argmax_combine(mx, ix, sh.s[q][3], sh.i[q]);
-  }
-  __syncthreads();
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ void dpp_sum_step(double& x) {
+  x += dpp_f64<CTRL, ROWMASK>(0.0, x);
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ void dpp_argmax_step(double& v, int& i) {
+  const double ov = dpp_f64<CTRL, ROWMASK>(-1.0, v);
+  const int oi = __builtin_amdgcn_update_dpp(INT_MAX, i, CTRL, ROWMASK, 0xF, false);
+  seq_argmax_combine(v, i, ov, oi);
+}
+// Wave sum; lane 63 receives the total (rows by shifts, then across rows).
+__device__ __forceinline__ void wave_sum63(double& x) {
+  dpp_sum_step<DPP_ROW_SHR1, 0xF>(x);
+  dpp_sum_step<DPP_ROW_SHR2, 0xF>(x);
+  dpp_sum_step<DPP_ROW_SHR4, 0xF>(x);
+  dpp_sum_step<DPP_ROW_SHR8, 0xF>(x);
+  dpp_sum_step<DPP_ROW_BCAST15, 0xA>(x);
+  dpp_sum_step<DPP_ROW_BCAST31, 0xC>(x);
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ void dpp_max_step(double& x) {
+  x = fmax(x, dpp_f64<CTRL, ROWMASK>(-1.0, x));
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ void dpp_imin_step(int& x) {
+  x = min(x, __builtin_amdgcn_update_dpp(INT_MAX, x, CTRL, ROWMASK, 0xF, false));
+}
+// Wave max of values >= 0 (identity -1); lane 63.
+__device__ __forceinline__ void wave_max63(double& x) {
+  dpp_max_step<DPP_ROW_SHR1, 0xF>(x);
+  dpp_max_step<DPP_ROW_SHR2, 0xF>(x);
+  dpp_max_step<DPP_ROW_SHR4, 0xF>(x);
+  dpp_max_step<DPP_ROW_SHR8, 0xF>(x);
+  dpp_max_step<DPP_ROW_BCAST15, 0xA>(x);
+  dpp_max_step<DPP_ROW_BCAST31, 0xC>(x);
+}
+// Wave minimum of ints (identity INT_MAX); lane 63.
+__device__ __forceinline__ void wave_imin63(int& x) {
+  dpp_imin_step<DPP_ROW_SHR1, 0xF>(x);
+  dpp_imin_step<DPP_ROW_SHR2, 0xF>(x);
+  dpp_imin_step<DPP_ROW_SHR4, 0xF>(x);
+  dpp_imin_step<DPP_ROW_SHR8, 0xF>(x);
+  dpp_imin_step<DPP_ROW_BCAST15, 0xA>(x);
+  dpp_imin_step<DPP_ROW_BCAST31, 0xC>(x);
+}
+// Wave (max, first index); values >= 0, identity (-1, INT_MAX); lane 63.
+__device__ __forceinline__ void wave_argmax63(double& v, int& i) {
+  dpp_argmax_step<DPP_ROW_SHR1, 0xF>(v, i);
+  dpp_argmax_step<DPP_ROW_SHR2, 0xF>(v, i);
+  dpp_argmax_step<DPP_ROW_SHR4, 0xF>(v, i);
+  dpp_argmax_step<DPP_ROW_SHR8, 0xF>(v, i);
+  dpp_argmax_step<DPP_ROW_BCAST15, 0xA>(v, i);
+  dpp_argmax_step<DPP_ROW_BCAST31, 0xC>(v, i);
 }
 
-// T_tau (Eq. (2)) of x[0 .. L) into out[0 .. Lpad) as floats in {-1, 0, 1}:
-// theta = tau * sum|x| / L, strict ">", and when no entry passes the
-// largest |x_i| (smallest i) keeps its sign; zero stays zero.  L <= SEQ_NT.
-__device__ __forceinline__ void seq_ternarize(const double* x, int L, int Lpad, double tau, float* out,
-                                              SeqShared& sh) {
-  const int t = threadIdx.x;
-  const double xv = t < L ? x[t] : 0.0;
-  double s = fabs(xv), z0 = 0.0, z1 = 0.0, mx = t < L ? fabs(xv) : -1.0;
-  int ix = t;
-  seq_reduce(s, z0, z1, mx, ix, sh);
-  const double theta = tau * (s / (double)L);
-  if (t < Lpad) {
-    float o = 0.0f;
-    if (t < L) {
-      const bool keep = mx > theta ? fabs(xv) > theta : (t == ix && mx > 0.0);
-      if (keep) o = xv > 0.0 ? 1.0f : -1.0f;
+// Wave results of the block reductions, double-buffered: a reduction writes
+// one buffer and the next the other, so a buffer is rewritten only after
+// every thread has passed the barrier of the reduction in between.
+struct SeqRed {
+  double v[2][SEQ_WAVES][4];
+  int i[2][SEQ_WAVES];
+};
+
+// Sum of the 8 wave results of slot q as a fixed tree.
+__device__ __forceinline__ double tree8(const double (&v)[SEQ_WAVES][4], int q) {
+  return ((v[0][q] + v[1][q]) + (v[2][q] + v[3][q])) + ((v[4][q] + v[5][q]) + (v[6][q] + v[7][q]));
+}
+
+// Block reduction of NSUM (<= 3) fp64 sums s[0 .. NSUM) and, with ARG, one
+// (max, first index) pair; every thread receives the same results.
+template <int NSUM, bool ARG>
+__device__ __forceinline__ void block_reduce(double* s, double& mv, int& mi, SeqRed& R, int& buf) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+#pragma unroll
+  for (int q = 0; q < NSUM; ++q) wave_sum63(s[q]);
+  if (ARG) wave_argmax63(mv, mi);
+  if (l == 63) {
+#pragma unroll
+    for (int q = 0; q < NSUM; ++q) R.v[buf][w][q] = s[q];
+    if (ARG) {
+      R.v[buf][w][3] = mv;
+      R.i[buf][w] = mi;
     }
-    out[t] = o;
   }
   __syncthreads();
+#pragma unroll
+  for (int q = 0; q < NSUM; ++q) s[q] = tree8(R.v[buf], q);
+  if (ARG) {
+    mv = R.v[buf][0][3];
+    mi = R.i[buf][0];
+#pragma unroll
+    for (int x = 1; x < SEQ_WAVES; ++x) seq_argmax_combine(mv, mi, R.v[buf][x][3], R.i[buf][x]);
+  }
+  buf ^= 1;
+}
+
+// T_tau (Eq. (2)) of a vector of length L held one entry per thread (entry
+// t in thread t, `valid` = t < L): theta = tau * sum|x| / L, strict ">",
+// and when no entry passes, the largest |x_t| (smallest t) keeps its sign;
+// zero stays zero.  Returns this thread's trit as a float.
+__device__ __forceinline__ float seq_ternarize(double xv, bool valid, int L, double tau, SeqRed& R, int& buf) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const double a = valid ? fabs(xv) : 0.0;
+  double s = a, mx = valid ? a : -1.0;
+  wave_sum63(s);
+  wave_max63(mx);
+  if (l == 63) {
+    R.v[buf][w][0] = s;
+    R.v[buf][w][1] = mx;
+  }
+  __syncthreads();
+  s = tree8(R.v[buf], 0);
+  {
+    const double(&v)[SEQ_WAVES][4] = R.v[buf];
+    mx = fmax(fmax(fmax(v[0][1], v[1][1]), fmax(v[2][1], v[3][1])), fmax(fmax(v[4][1], v[5][1]), fmax(v[6][1], v[7][1])));
+  }
+  buf ^= 1;
+  const double theta = tau * (s / (double)L);
+  if (mx > theta) return (valid && a > theta) ? (xv > 0.0 ? 1.0f : -1.0f) : 0.0f;
+  if (!(mx > 0.0)) return 0.0f;
+  // no entry passes: the first entry of largest magnitude keeps its sign
+  int first = (valid && a == mx) ? (int)threadIdx.x : INT_MAX;
+  wave_imin63(first);
+  if (l == 63) R.i[buf][w] = first;
+  __syncthreads();
+  int f = R.i[buf][0];
+#pragma unroll
+  for (int x = 1; x < SEQ_WAVES; ++x) f = min(f, R.i[buf][x]);
+  buf ^= 1;
+  return (int)threadIdx.x == f ? (xv > 0.0 ? 1.0f : -1.0f) : 0.0f;
 }
 
 template <int NR, int NC>
 struct SeqLds {
   static constexpr int MP = SEQ_WAVES * NR, NP = 64 * NC, XL = MP > NP ? MP : NP;
-  double part[SEQ_WAVES][NP];   // per-wave column partial sums
-  double x[XL];                 // the vector being ternarized (targets), then q of the last U-step
-  double colE[NP];              // ||R_:j||^2
-  double hw[NP];                // h~_j (zero past n)
-  float uf[MP];                 // current u
-  float vf[NP];                 // current v
-  int8_t uh[4][MP];             // the last four u's (one packed byte of B per row)
-  SeqShared red;
+  union {
+    double part[SEQ_WAVES][NP];             // per-wave column partial sums
+    float p2[SEQ_WAVES][NR][SEQ_P2_PITCH];  // per-lane row partial sums (R v)
+  } u;
+  double x[XL];      // a gathered column, or q = R diag(h~) v by row
+  double colE[NP];   // ||R_:j||^2
+  double hw[NP];     // h~_j (zero past n)
+  float uf[MP];      // current u
+  float vf[NP];      // current v
+  int8_t uh[4][MP];  // the last four u's (one packed byte of B per row)
+  SeqRed red;
 };
 
-// Column energies of the residual in registers (and, with track, its largest
-// |R_ij|: value, first row-major index i * n + j, sign), the plain and the
-// weighted ||R||^2.
+// Column energies of the residual in registers, ||R||^2, the weighted
+// ||R||^2 and, with track, the largest |R_ij| with key 2 (i n + j) + [R_ij < 0]
+// (the first in row-major order on ties).
 template <int NR, int NC>
-__device__ __forceinline__ void seq_energies(const float (&Rr)[NR][NC], int64_t n, bool track, SeqLds<NR, NC>& S,
-                                             double& fro2, double& fro2w, double& gmax, int& gidx, float& gval) {
+__device__ __forceinline__ void seq_energies(const float (&Rr)[NR][NC], int n, bool track, SeqLds<NR, NC>& S,
+                                             int& buf, double& fro2, double& fro2w, double& gmax, int& gkey) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   double ce[NC];
 #pragma unroll
   for (int c = 0; c < NC; ++c) ce[c] = 0.0;
-  float tmax = 0.0f, tval = 0.0f;
-  int tidx = 0x7FFFFFFF;
+  float tmax = 0.0f;
+  int tkey = INT_MAX;
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
 #pragma unroll
@@ -125,73 +226,32 @@ __device__ __forceinline__ void seq_energies(const float (&Rr)[NR][NC], int64_t 
       ce[c] = fma((double)v, (double)v, ce[c]);
       if (track && fabsf(v) > tmax) {
         tmax = fabsf(v);
-        tval = v;
-        tidx = (int)((int64_t)(w + SEQ_WAVES * r) * n + (l + 64 * c));
+        tkey = 2 * ((w + SEQ_WAVES * r) * n + (l + 64 * c)) + (v < 0.0f ? 1 : 0);
       }
     }
   }
 #pragma unroll
-  for (int c = 0; c < NC; ++c) S.part[w][l + 64 * c] = ce[c];
+  for (int c = 0; c < NC; ++c) S.u.part[w][l + 64 * c] = ce[c];
   __syncthreads();
   double cj = 0.0;
   if (t < SeqLds<NR, NC>::NP) {
-    for (int q = 0; q < SEQ_WAVES; ++q) cj += S.part[q][t];
+#pragma unroll
+    for (int q = 0; q < SEQ_WAVES; ++q) cj += S.u.part[q][t];
     if (t >= n) cj = 0.0;
     S.colE[t] = cj;
   }
-  double a = cj, b = t < SeqLds<NR, NC>::NP ? S.hw[t] * cj : 0.0, z = 0.0;
-  double mx = track ? (double)tmax : 0.0;
-  int ix = tidx;
-  // the signed value travels with the index: recover it from the owner
-  seq_reduce(a, b, z, mx, ix, S.red);
-  fro2 = a;
-  fro2w = b;
-  if (track) {
-    gmax = mx;
-    gidx = ix;
-    // the thread that holds the winning entry publishes its sign
-    if (tidx == ix && (double)tmax == mx && mx > 0.0) S.red.s[0][0] = (double)tval;
-    __syncthreads();
-    gval = mx > 0.0 ? (float)S.red.s[0][0] : 0.0f;
-    __syncthreads();
-  }
+  double s[2] = {cj, t < SeqLds<NR, NC>::NP ? S.hw[t] * cj : 0.0};
+  double mv = tmax > 0.0f ? (double)tmax : -1.0;
+  int mi = tmax > 0.0f ? tkey : INT_MAX;
+  if (track)
+    block_reduce<2, true>(s, mv, mi, S.red, buf);
+  else
+    block_reduce<2, false>(s, mv, mi, S.red, buf);
+  fro2 = s[0];
+  fro2w = s[1];
+  gmax = track && mv > 0.0 ? mv : 0.0;
+  gkey = mi;
 }
-
-// Sum over the 64 lanes of a wave of each of p[0 .. NR): recursive halving
-// (a lane keeps one half of its values and adds its partner's copy of that
-// half), after which lane l holds the sum of p[l >> (6 - log2 NR)].
-template <int K, int MASK, int NR>
-struct SeqHalve {
-  static __device__ __forceinline__ void run(double (&p)[NR], int l) {
-    if constexpr (K > 1) {
-      const bool hi = (l & MASK) != 0;
-#pragma unroll
-      for (int i = 0; i < K / 2; ++i) {
-        const double keep = hi ? p[i + K / 2] : p[i];
-        const double send = hi ? p[i] : p[i + K / 2];
-        p[i] = keep + __shfl_xor(send, MASK, 64);
-      }
-      SeqHalve<K / 2, MASK / 2, NR>::run(p, l);
-    } else if constexpr (MASK > 0) {
-      p[0] += __shfl_xor(p[0], MASK, 64);
-      SeqHalve<1, MASK / 2, NR>::run(p, l);
-    }
-  }
-};
-template <int NR>
-__device__ __forceinline__ double seq_lane_reduce_scatter(double (&p)[NR]) {
-  SeqHalve<NR, 32, NR>::run(p, threadIdx.x & 63);
-  return p[0];
-}
-
-template <int NR>
-struct Log2 {
-  static constexpr int v = NR <= 1 ? 0 : 1 + Log2<NR / 2>::v;
-};
-template <>
-struct Log2<1> {
-  static constexpr int v = 0;
-};
 
 __device__ __forceinline__ unsigned seq_trit_code(float t) { return t == 0.0f ? 0u : (t > 0.0f ? 1u : 3u); }
 
@@ -204,26 +264,31 @@ static bool seq_fits(int64_t m, int64_t n) {
 template <int NR, int NC>
 __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int64_t m, int64_t n, int64_t k,
                                                 double tau, int iters, const double* __restrict__ hw, int weighted,
-                                                int safeguard, double target, uint8_t* __restrict__ Bp, uint8_t* __restrict__ Cp,
-                                                float* __restrict__ D, double* __restrict__ fro2_hist,
-                                                double* __restrict__ fro2w_hist, unsigned* counters, int* flags) {
+                                                int safeguard, double target, uint8_t* __restrict__ Bp,
+                                                uint8_t* __restrict__ Cp, float* __restrict__ D,
+                                                double* __restrict__ fro2_hist, double* __restrict__ fro2w_hist,
+                                                unsigned* counters, int* flags) {
   constexpr int MP = SeqLds<NR, NC>::MP, NP = SeqLds<NR, NC>::NP;
-  constexpr int RC = NR < 4 ? NR : 4;  // rows per lane reduction (bounds the registers it holds)
-  constexpr int LG = Log2<RC>::v;
+  constexpr int LPR = 64 / NR;  // lanes per row in the R v transpose
+  constexpr int PER = 64 / LPR; // partials each of them sums
+  static_assert(NR * NC == 128 && (LPR == 2 || LPR == 4), "register layouts of 128 values, 2 or 4 lanes per row");
   __shared__ SeqLds<NR, NC> S;
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   if (flags[FLAG_BADWEIGHT]) return;  // invalid weights: the host reports it
   const bool track = safeguard != 0;
   const bool has_target = !isnan(target);
   const int64_t pitchB = (k + 3) >> 2, pitchC = (n + 3) >> 2;
+  const int mi = (int)m, ni = (int)n;
+  int buf = 0;
 
   float hwf[NC];
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const int j = l + 64 * c;
-    hwf[c] = j < n ? (float)hw[j] : 0.0f;
+    hwf[c] = j < ni ? (float)hw[j] : 0.0f;
   }
-  if (t < NP) S.hw[t] = t < n ? hw[t] : 0.0;
+  const double hw_t = t < ni ? hw[t] : 0.0;
+  if (t < NP) S.hw[t] = hw_t;
 
   // stage: R <- A (zero outside m x n), non-finite check
   float Rr[NR][NC];
@@ -235,7 +300,7 @@ __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int
     for (int c = 0; c < NC; ++c) {
       const int j = l + 64 * c;
       float v = 0.0f;
-      if (i < m && j < n) v = A[(int64_t)i * n + j];
+      if (i < mi && j < ni) v = A[(int64_t)i * n + j];
       if (!isfinite(v)) {
         bad = 1;
         v = 0.0f;
@@ -244,18 +309,17 @@ __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int
     }
   }
   {
-    double a = (double)bad, z0 = 0.0, z1 = 0.0, mx = 0.0;
-    int ix = 0;
-    seq_reduce(a, z0, z1, mx, ix, S.red);
-    if (a != 0.0) {
+    double s[1] = {(double)bad}, mv = 0.0;
+    int mx = 0;
+    block_reduce<1, false>(s, mv, mx, S.red, buf);
+    if (s[0] != 0.0) {
       if (t == 0) flags[FLAG_NONFINITE] = 1;
       return;
     }
   }
-  double fro2, fro2w, gmax = 0.0;
-  int gidx = 0;
-  float gval = 0.0f;
-  seq_energies<NR, NC>(Rr, n, track, S, fro2, fro2w, gmax, gidx, gval);
+  double fro2, fro2w, gmax;
+  int gkey;
+  seq_energies<NR, NC>(Rr, ni, track, S, buf, fro2, fro2w, gmax, gkey);
   const double a2 = fro2, a2w = fro2w;
   if (t == 0) {
     fro2_hist[0] = fro2;
@@ -264,13 +328,12 @@ __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int
   int64_t used = k;
   unsigned fired = 0;
   for (int64_t comp = 0; comp < k; ++comp) {
-    // init (reading R1): column with the largest weighted energy
+    // init (reading R1): the column with the largest weighted energy
     int js;
     {
-      double z0 = 0.0, z1 = 0.0, z2 = 0.0;
-      double kv = (t < n) ? S.hw[t] * S.colE[t] : -1.0;
-      int ki = t;
-      seq_reduce(z0, z1, z2, kv, ki, S.red);
+      double kv = t < ni ? S.hw[t] * S.colE[t] : -1.0;
+      int ki = t < ni ? t : INT_MAX;
+      block_reduce<0, true>(nullptr, kv, ki, S.red, buf);
       js = ki;
     }
     if (l == (js & 63)) {
@@ -285,62 +348,86 @@ __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int
       }
     }
     __syncthreads();
-    seq_ternarize(S.x, (int)m, MP, tau, S.uf, S.red);
+    float u_t = seq_ternarize(t < mi ? S.x[t] : 0.0, t < mi, mi, tau, S.red, buf);
+    if (t < MP) S.uf[t] = u_t;
+    __syncthreads();
+    float v_t = 0.0f;
+    double q_t = 0.0;
     for (int it = 0; it < iters; ++it) {
       // V-step: y = R^T u, v = T(y)
       {
-        float p[NC];
+        // two independent accumulation chains per column (rows r < NR/2, r >= NR/2)
+        float p[2][NC];
 #pragma unroll
-        for (int c = 0; c < NC; ++c) p[c] = 0.0f;
+        for (int c = 0; c < NC; ++c) p[0][c] = p[1][c] = 0.0f;
 #pragma unroll
-        for (int r = 0; r < NR; ++r) {
-          const float u = S.uf[w + SEQ_WAVES * r];
+        for (int r = 0; r < NR / 2; ++r) {
+          const float u0 = S.uf[w + SEQ_WAVES * r], u1 = S.uf[w + SEQ_WAVES * (r + NR / 2)];
 #pragma unroll
-          for (int c = 0; c < NC; ++c) p[c] = fmaf(Rr[r][c], u, p[c]);
+          for (int c = 0; c < NC; ++c) {
+            p[0][c] = fmaf(Rr[r][c], u0, p[0][c]);
+            p[1][c] = fmaf(Rr[r + NR / 2][c], u1, p[1][c]);
+          }
         }
 #pragma unroll
-        for (int c = 0; c < NC; ++c) S.part[w][l + 64 * c] = (double)p[c];
+        for (int c = 0; c < NC; ++c) S.u.part[w][l + 64 * c] = (double)p[0][c] + (double)p[1][c];
       }
       __syncthreads();
+      double y = 0.0;
       if (t < NP) {
-        double y = 0.0;
-        for (int q = 0; q < SEQ_WAVES; ++q) y += S.part[q][t];
-        S.x[t] = y;
+        const double(&pp)[SEQ_WAVES][NP] = S.u.part;
+        y = ((pp[0][t] + pp[1][t]) + (pp[2][t] + pp[3][t])) + ((pp[4][t] + pp[5][t]) + (pp[6][t] + pp[7][t]));
       }
+      v_t = seq_ternarize(y, t < ni, ni, tau, S.red, buf);
+      if (t < NP) S.vf[t] = v_t;
       __syncthreads();
-      seq_ternarize(S.x, (int)n, NP, tau, S.vf, S.red);
       // U-step: q = R diag(h~) v, u = T(q)
       {
         float hv[NC];
 #pragma unroll
         for (int c = 0; c < NC; ++c) hv[c] = hwf[c] * S.vf[l + 64 * c];
 #pragma unroll
-        for (int ch = 0; ch < NR / RC; ++ch) {
-          double p[RC];
+        for (int r = 0; r < NR; ++r) {
+          float s = 0.0f;
 #pragma unroll
-          for (int r = 0; r < RC; ++r) {
-            float s = 0.0f;
-#pragma unroll
-            for (int c = 0; c < NC; ++c) s = fmaf(Rr[ch * RC + r][c], hv[c], s);
-            p[r] = (double)s;
-          }
-          const double q = seq_lane_reduce_scatter<RC>(p);
-          if ((l & ((64 >> LG) - 1)) == 0) S.x[w + SEQ_WAVES * (ch * RC + (l >> (6 - LG)))] = q;
+          for (int c = 0; c < NC; ++c) s = fmaf(Rr[r][c], hv[c], s);
+          S.u.p2[w][r][l] = s;
         }
+        // each wave reads back only what it wrote itself
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // lane l sums PER partials of row l / LPR, then the LPR lanes of a row combine
+        const int rr = l / LPR, pp = l % LPR;
+        const float4* src = (const float4*)&S.u.p2[w][rr][pp * PER];
+        double a4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int e = 0; e < PER / 4; ++e) {
+          const float4 f = src[e];
+          a4[0] += (double)f.x;
+          a4[1] += (double)f.y;
+          a4[2] += (double)f.z;
+          a4[3] += (double)f.w;
+        }
+        double acc = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+        acc += dpp_f64<DPP_QUAD_XOR1, 0xF>(0.0, acc);
+        if (LPR == 4) acc += dpp_f64<DPP_QUAD_XOR2, 0xF>(0.0, acc);
+        if (pp == 0) S.x[w + SEQ_WAVES * rr] = acc;
       }
       __syncthreads();
-      seq_ternarize(S.x, (int)m, MP, tau, S.uf, S.red);
+      q_t = t < mi ? S.x[t] : 0.0;
+      u_t = seq_ternarize(q_t, t < mi, mi, tau, S.red, buf);
+      if (t < MP) S.uf[t] = u_t;
+      __syncthreads();
     }
     // joint scale (Eq. (4) at b = 1) from the last U-step's q
     double d, delta;
     {
-      double g = t < m ? (double)S.uf[t] * S.x[t] : 0.0;
-      double nu = t < m ? (double)(S.uf[t] * S.uf[t]) : 0.0;
-      double vh = t < n ? S.hw[t] * (double)(S.vf[t] * S.vf[t]) : 0.0;
-      double z = 0.0;
-      int zi = 0;
-      seq_reduce(g, nu, vh, z, zi, S.red);
-      const double M = nu * vh;
+      double s[3] = {(double)u_t * q_t, (double)(u_t * u_t), hw_t * (double)(v_t * v_t)};
+      double mv = 0.0;
+      int mx = 0;
+      block_reduce<3, false>(s, mv, mx, S.red, buf);
+      const double g = s[0], M = s[1] * s[2];
       d = 0.0;
       delta = 0.0;
       if (M != 0.0) {
@@ -349,10 +436,11 @@ __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int
       }
       // single-entry option of Proposition 2: removed objective d g + delta d^2
       if (track && gmax > 0.0 && gmax * gmax > d * g + delta * d * d) {
-        const int gi = (int)(gidx / n), gj = (int)(gidx % n);
+        const int flat = gkey >> 1;
+        const int gi = flat / ni, gj = flat % ni;
         d = gmax;
         if (t < MP) S.uf[t] = t == gi ? 1.0f : 0.0f;
-        if (t < NP) S.vf[t] = t == gj ? (gval < 0.0f ? -1.0f : 1.0f) : 0.0f;
+        if (t < NP) S.vf[t] = t == gj ? ((gkey & 1) ? -1.0f : 1.0f) : 0.0f;
         ++fired;
         __syncthreads();
       }
@@ -365,20 +453,25 @@ __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         const int j = 4 * t + s;
-        if (j < n) byte |= seq_trit_code(S.vf[j]) << (2 * s);
+        if (j < ni) byte |= seq_trit_code(S.vf[j]) << (2 * s);
       }
       Cp[comp * pitchC + t] = (uint8_t)byte;
     }
     if (t < MP) S.uh[comp & 3][t] = (int8_t)S.uf[t];
-    // deflation R -= fp32(d) u v^T (the ternary product is exact)
+    // deflation R -= fp32(d) u v^T (u v is an exact ternary product)
+    {
+      float vv[NC];
 #pragma unroll
-    for (int r = 0; r < NR; ++r) {
-      const float u = S.uf[w + SEQ_WAVES * r];
+      for (int c = 0; c < NC; ++c) vv[c] = S.vf[l + 64 * c];
 #pragma unroll
-      for (int c = 0; c < NC; ++c) Rr[r][c] -= (u * S.vf[l + 64 * c]) * dF;
+      for (int r = 0; r < NR; ++r) {
+        const float u = S.uf[w + SEQ_WAVES * r];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) Rr[r][c] -= (u * vv[c]) * dF;
+      }
     }
-    __syncthreads();  // uh written, uf / vf read
-    seq_energies<NR, NC>(Rr, n, track, S, fro2, fro2w, gmax, gidx, gval);
+    // (the barrier in seq_energies also orders the uh writes before the B write)
+    seq_energies<NR, NC>(Rr, ni, track, S, buf, fro2, fro2w, gmax, gkey);
     if (t == 0) {
       fro2_hist[comp + 1] = fro2;
       fro2w_hist[comp + 1] = fro2w;
@@ -390,7 +483,7 @@ __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int
       stop = e >= target;
     }
     if ((comp & 3) == 3 || comp == k - 1 || stop) {
-      if (t < m) {
+      if (t < mi) {
         unsigned byte = 0;
         const int top = (int)(comp & 3);
         for (int s = 0; s <= top; ++s) byte |= seq_trit_code((float)S.uh[s][t]) << (2 * s);
@@ -408,13 +501,7 @@ __global__ __launch_bounds__(SEQ_NT) void k_seq(const float* __restrict__ A, int
   }
 }
 
-}  // namespace externd
-
-namespace externd {
-
-bool seq_supported(int64_t m, int64_t n) {
-  return seq_fits<32, 4>(m, n) || seq_fits<16, 8>(m, n);
-}
+bool seq_supported(int64_t m, int64_t n) { return seq_fits<32, 4>(m, n) || seq_fits<16, 8>(m, n); }
 
 hipError_t launch_seq(const Ws& w, const float* A, int64_t k, double tau, int iters, bool weighted, bool safeguard,
                       double target, uint8_t* Bp, uint8_t* Cp, float* D, hipStream_t s, Timer* tm) {
