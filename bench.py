@@ -81,13 +81,19 @@ def algorithmic_bytes(kclass: str, m: int, n: int) -> float:
     the ternary operands and outputs add < 2 % and are not counted.  The
     target kernels read the contraction's output (V: the row groups' int64
     partials of P, 64 x n each; U: Q, 64 x m fp64) and write the fp64
-    target (64 x n or 64 x m)."""
+    target (64 x n or 64 x m).  The ternarizations read the fp64 target
+    and write the factor in two int8 forms (component-major and MFMA-ready);
+    the last U-step of a block also reads Q, which is not counted."""
     if kclass == "deflate":
         return 8.0 * m * n
     if kclass == "vstep_target":
         return (vstep_row_groups(m, n) + 1) * 64 * 8.0 * n
     if kclass == "ustep_target":
         return 2 * 64 * 8.0 * m
+    if kclass == "ternarize_v":
+        return 64 * (8.0 + 2.0) * n
+    if kclass == "ternarize_u":
+        return 64 * (8.0 + 2.0) * m
     return 4.0 * m * n
 
 
@@ -160,7 +166,8 @@ def collect_traffic(dbs, copy_bytes: int):
     copy_w = max(v[1] for k, v in cwrite.items() if "copyBuffer" in k)
     ff, fw = copy_bytes / copy_f, copy_bytes / copy_w
     classes = {"vstep_contraction": "k_vstep", "ustep_contraction": "k_ustep<false>", "deflate": "k_deflate<false>",
-               "vstep_target": "k_vtarget", "ustep_target": "k_utarget"}
+               "vstep_target": "k_vtarget", "ustep_target": "k_utarget", "ternarize_v": "k_tern_v",
+               "ternarize_u": "k_tern_u"}
     out = {"kernel_source_sha256": kernel_source_hash(), "copy_bytes": copy_bytes,
            "fetch_scale": ff, "write_scale": fw, "kernels": {}}
     lines = ["# HBM traffic per launch (rocprofv3 --pmc), 9728x2560 workload", "",

@@ -242,7 +242,10 @@ int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float*
 #define EXTERND_KCLASS_UTARGET 4  /* U-step target Z = Q G_V^{-1} and its statistics    */
 #define EXTERND_KCLASS_SEQ     5  /* the one-launch sequential path (block width 1 on a
                                      small matrix: every launch is timed)              */
-#define EXTERND_KCLASS_COUNT   6
+#define EXTERND_KCLASS_TERNV   6  /* V = T_tau(Y^T) per component, Eq. (2)            */
+#define EXTERND_KCLASS_TERNU   7  /* U = T_tau(Z) per component, Eq. (2) (+ g = diag(U^T Q)
+                                     in the last U-step of a block)                     */
+#define EXTERND_KCLASS_COUNT   8
 
 typedef struct {
   double total_ms[EXTERND_KCLASS_COUNT];  /* summed durations of the timed launches */

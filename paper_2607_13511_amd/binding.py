@@ -67,7 +67,7 @@ EXPORTED = tuple(_SIGNATURES)
 
 
 KCLASS_NAMES = ("vstep_contraction", "ustep_contraction", "deflate", "vstep_target", "ustep_target",
-                "sequential_one_launch")
+                "sequential_one_launch", "ternarize_v", "ternarize_u")
 # externd_factorize_timed times one launch in TIMING_STRIDE of each class
 # (EXTERND_TIMING_STRIDE in include/externd.h).
 TIMING_STRIDE = 16

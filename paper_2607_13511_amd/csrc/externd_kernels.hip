@@ -2371,8 +2371,9 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
                        (const long long*)w.Pp, w.maxbits + blk, w.n_pad, w.gv, w.ginvU, w.Y, w.n, w.tps, w.tpm, w.tpi);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, w.Y, w.n, w.n_pad, bb, tau, w.tps, w.tpm, w.tpi,
-                     (int)(w.n_pad / 16), w.nsv, w.Vt, w.Vmf);
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, (const double*)w.Y, w.n,
+                       w.n_pad, bb, tau, (const double*)w.tps, (const double*)w.tpm, (const int*)w.tpi,
+                       (int)(w.n_pad / 16), w.nsv, w.Vt, w.Vmf);
   return hipGetLastError();
 }
 
@@ -2400,8 +2401,9 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
                        s, (const double*)w.Q, (const double*)w.ginvV, w.Z, w.m, w.m_pad, w.tps, w.tpm, w.tpi);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, w.Z, final ? (const double*)w.Q : nullptr, w.m,
-                     w.m_pad, bb, tau, w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec);
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNU, k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, (const double*)w.Z,
+                       final ? (const double*)w.Q : nullptr, w.m, w.m_pad, bb, tau, (const double*)w.tps,
+                       (const double*)w.tpm, (const int*)w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec);
   return hipGetLastError();
 }
 
