@@ -48,6 +48,8 @@ def workload(name: str):
         return synth.attn2048()
     if name == "gauss256":
         return synth.gauss256()
+    if name == "block4b":
+        return None      # the seven matrices of a transformer block: bench_block
     raise SystemExit(f"unknown workload {name}")
 
 
@@ -240,6 +242,8 @@ def main():
     binding.lib()      # fails loudly when the HIP library is missing
 
     w = workload(args.workload)
+    if w is None:
+        return bench_block(binding, torch, args)
     m, n = w.A.shape
     dev = torch.device("cuda:0")
     if args.sweeps is not None:
@@ -350,6 +354,63 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def bench_block(binding, torch, args):
+    """The seven matrices of one synthetic ~4B transformer block (q 2560x4096,
+    k and v 2560x1024, o 4096x2560, gate and up 2560x9728, down 9728x2560;
+    Student-t(4) at std 0.02, importance weights exp(N(0, 1))), factorized
+    matrix by matrix to mu = 3.5 at each tau in (0.7, 1.0, 2.0), block 64,
+    8 ALS iterations, importance-weighted: the whole sweep is one step.
+    Energies at mu = 2, 2.5 and 3.5 come from the per-block curve (every
+    prefix of a greedy run is the run to that rank)."""
+    from paper_2607_13511_amd import synth
+    dev = torch.device("cuda:0")
+    mats = []
+    for idx in range(len(synth.BLOCK_SHAPES)):
+        name, A, h = synth.transformer_block(idx)
+        mats.append((name, torch.from_numpy(A).to(dev), torch.from_numpy(h).to(dev)))
+    taus, mu, block, iters = (0.7, 1.0, 2.0), 3.5, 64, 8
+    # one workspace sized for the largest matrix and rank
+    ws = torch.empty(max(binding.workspace_bytes(A.shape[0], A.shape[1], binding.rank(A.shape[0], A.shape[1], mu))
+                         for _, A, _ in mats), dtype=torch.uint8, device=dev)
+
+    def one_step(record):
+        per = {}
+        for tau in taus:
+            for name, A, h in mats:
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                r = binding.factorize(A, mu, tau, block, iters, h=h, workspace=ws)
+                torch.cuda.synchronize()
+                dt = time.perf_counter() - t0
+                if record:
+                    m, n = A.shape
+                    pts = {}
+                    for mu_c in (2.0, 2.5, 3.5):
+                        b = binding.rank(m, n, mu_c) // r.block - 1
+                        pts[str(mu_c)] = {"E": float(r.curve[b]), "E_w": float(r.curve_w[b])}
+                    per[f"{name}@tau{tau}"] = {"m": m, "n": n, "k": r.k, "sec": dt, "components_per_s": r.k / dt,
+                                               "checkpoints": pts}
+        return per
+
+    for _ in range(args.warmup):
+        one_step(False)
+    t0 = time.perf_counter()
+    per = {}
+    for _ in range(args.steps):
+        per = one_step(True)
+    sec = (time.perf_counter() - t0) / args.steps
+    comps = sum(v["k"] for v in per.values())
+    print(json.dumps({
+        "metric": "sec per transformer block (7 matrices x 3 tau) + ALS components/sec", "value": comps / sec,
+        "unit": "components/s", "higher_is_better": True, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "sec_per_step": sec, "data": "synthetic",
+        "config": {"workload": "transformer_block_4b_7mat_mu3.5_tau0.7-1.0-2.0_b64_imatrix", "mu": mu,
+                   "taus": list(taus), "block": block, "iters": iters, "importance": True},
+        "sec_per_tau": {str(t): sum(v["sec"] for k2, v in per.items() if k2.endswith(f"tau{t}")) for t in taus},
+        "matrices": per,
+    }), flush=True)
 
 
 def bench_apply(binding, torch, w, args):

@@ -81,6 +81,7 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(unsigned short) * (size_t)(BBP * L.m_pad),  // 31 Ub
       sizeof(unsigned long long) * (size_t)L.nblk_cap, // 32 argkey
       sizeof(int) * 2 * 4096,                          // 33 gacc
+      sizeof(double) * 4096 * VPREP_MAX_WG,            // 34 partw
   };
   size_t o = 0;
   for (size_t i = 0; i < sizeof(sizes) / sizeof(sizes[0]); ++i) {
@@ -142,6 +143,7 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.Ub = (unsigned short*)(b + L.off[31]);
   w.argkey = (unsigned long long*)(b + L.off[32]);
   w.gacc = (int*)(b + L.off[33]);
+  w.partw = (double*)(b + L.off[34]);
   return true;
 }
 

@@ -87,6 +87,7 @@ struct Ws {
   unsigned* maxbits;     // nblk_cap: max|R| (fp32 bits) before each block
   unsigned* maxbits_w;   // nblk_cap: bound on max|R_ij h~_j| (fp32 bits)
   unsigned long long* argkey;  // nblk_cap: (max|R| bits << 32) | (2^32 - 1 - first row-major index), safeguard only
+  double* partw;               // VPREP_MAX_WG x 64 x 64: partial weighted Grams V^T diag(h~) V
   double* fro2_hist;     // nblk_cap: ||R||^2 before each block, then after the last
   double* fro2w_hist;    // nblk_cap: weighted ||R||^2
   unsigned* counters;    // CNT_COUNT
@@ -131,6 +132,8 @@ struct Timer {
   } while (0)
 
 size_t workspace_bytes(int64_t m, int64_t n, int64_t k);
+// Workgroups of the weighted-Gram preparation (each covers >= 32 rows of V).
+constexpr int VPREP_MAX_WG = 128;
 bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k);
 
 // ---- launchers (all asynchronous on `s`) ----

@@ -60,8 +60,13 @@ __device__ __forceinline__ int fx_shift(unsigned maxbits) {
 __device__ __forceinline__ unsigned fx_biased(float x, int s) {
   return (unsigned)(int)__builtin_rintf(__builtin_amdgcn_ldexpf(x, s)) + 0x00808080u;
 }
+// Weighted: x fw rounded to the nearest integer (ties to even) in one
+// step.  Adding 1.5 2^52 inside the fma rounds the exact product at unit
+// spacing, so for |x fw| < 2^31 the low word of the result is that integer
+// in two's complement.
 __device__ __forceinline__ unsigned fx_biased_w(float x, double fw) {
-  return (unsigned)(int)__builtin_rint((double)x * fw) + 0x00808080u;
+  const double t = __builtin_fma((double)x, fw, 6755399441055744.0);
+  return (unsigned)__double2loint(t) + 0x00808080u;
 }
 
 // Upper bound (fp32) on |v| * hw for the weighted fixed-point scale: the
@@ -661,10 +666,13 @@ __device__ __forceinline__ void take_gram(int* gacc, double* G) {
 // of Vr (n_pad x BBP int8, row-major) on fp64 MFMA (v_mfma_f64_16x16x4):
 // products h~_j v_jc v_jc' are exact and the sums are fp64.  The 10
 // 16x16 tiles of the upper triangle are dealt to the 4 waves; each wave
-// covers all of the workgroup's rows for its tiles.  Same last-workgroup
-// protocol as side_gram_int.
+// covers all of the workgroup's rows for its tiles.  The rows and their
+// weights are staged through LDS in chunks of SIDE_W_CHUNK K steps (one
+// round of coalesced loads per chunk instead of a dependent load per K
+// step).  Same last-workgroup protocol as side_gram_int.
+constexpr int SIDE_W_CHUNK = 56;  // K steps of 4 rows per staged chunk: 56 x 4 x (64 + 8) bytes <= 16 KB
 __device__ __forceinline__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restrict__ hw, int64_t L, int side,
-                            int nside, double* gpart, unsigned* counter, double* G) {
+                            int nside, double* gpart, unsigned* counter, double* G, char* stage /* LDS, 16 KB */) {
   const int lane = lane_id(), wave = wave_id();
   const int i16 = lane & 15, kq = lane >> 4;
   const int64_t nks = L / 4;
@@ -682,20 +690,30 @@ __device__ __forceinline__ bool side_gram_w(const int8_t* __restrict__ Vr, const
   }
   v4d acc[3] = {v4d{}, v4d{}, v4d{}};
   const int ntile = (wave < 2) ? 3 : 2;
-  for (int64_t ks = ks0; ks < ks1; ++ks) {
-    const int64_t j = ks * 4 + kq;
-    const int8_t* row = Vr + j * BBP;
-    const double w = hw[j];
-    double v[4];
+  int8_t* sv = (int8_t*)stage;                                         // rows x 64 bytes
+  double* sw = (double*)(stage + SIDE_W_CHUNK * 4 * BBP);              // their weights
+  for (int64_t c0 = ks0; c0 < ks1; c0 += SIDE_W_CHUNK) {
+    const int nk = (int)(ks1 - c0 < SIDE_W_CHUNK ? ks1 - c0 : SIDE_W_CHUNK);
+    __syncthreads();  // the previous chunk has been consumed
+    const int4* src = (const int4*)(Vr + 4 * c0 * BBP);
+    for (int e = threadIdx.x; e < nk * 4 * (BBP / 16); e += blockDim.x) ((int4*)sv)[e] = src[e];
+    for (int e = threadIdx.x; e < nk * 4; e += blockDim.x) sw[e] = hw[4 * c0 + e];
+    __syncthreads();
+    for (int k = 0; k < nk; ++k) {
+      const int r = 4 * k + kq;
+      const int8_t* row = sv + r * BBP;
+      const double w = sw[r];
+      double v[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = (double)row[16 * q + i16];
+      for (int q = 0; q < 4; ++q) v[q] = (double)row[16 * q + i16];
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      if (q < ntile) {
-        const int mt = TMq[q], nt = TNq[q];
-        const double va = (mt == 0) ? v[0] : (mt == 1) ? v[1] : (mt == 2) ? v[2] : v[3];
-        const double vb = (nt == 0) ? v[0] : (nt == 1) ? v[1] : (nt == 2) ? v[2] : v[3];
-        acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(w * va, vb, acc[q], 0, 0, 0);
+      for (int q = 0; q < 3; ++q) {
+        if (q < ntile) {
+          const int mt = TMq[q], nt = TNq[q];
+          const double va = (mt == 0) ? v[0] : (mt == 1) ? v[1] : (mt == 2) ? v[2] : v[3];
+          const double vb = (nt == 0) ? v[0] : (nt == 1) ? v[1] : (nt == 2) ? v[2] : v[3];
+          acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(w * va, vb, acc[q], 0, 0, 0);
+        }
       }
     }
   }
@@ -916,11 +934,138 @@ __global__ __launch_bounds__(NT) void k_vtarget(const long long* __restrict__ Pp
   tile_stats(y, w, j0, (j0 + 16 < n ? j0 + 16 : n), ntile, tile, ps, pm, pi);
 }
 // ---------------------------------------------------------------------------
+// Weighted U-step preparation (Sec. 2.5): V row-major (Vr) from the
+// component-major Vt, and this workgroup's partial of the weighted Gram
+// V^T diag(h~) V on fp64 MFMA (v_mfma_f64_16x16x4; the products
+// h~_j v_jc v_jc' are exact, the sums fp64 in a fixed order), 16x16 tiles of
+// the upper triangle dealt to the 4 waves as in side_gram_w.  Workgroup g
+// covers rows [g rows_wg, (g + 1) rows_wg), staged in LDS in chunks of
+// VPREP_CHUNK, and writes its partial to partw[g]; k_gramw_sum adds the
+// partials in workgroup order.  Running before the U-step launch, the Gram
+// does not compete with the residual stream.
+// grid: ceil(n_pad / rows_wg) <= VPREP_MAX_WG.
+// ---------------------------------------------------------------------------
+constexpr int VPREP_CHUNK = 128;
+constexpr int VPREP_MIN_ROWS = 32;
+__global__ __launch_bounds__(NT) void k_vprep_w(const int8_t* __restrict__ Vt, int8_t* __restrict__ Vr, int64_t n_pad,
+                                                const double* __restrict__ hw, int rows_wg,
+                                                double* __restrict__ partw) {
+  __shared__ int8_t tile[VPREP_CHUNK][BBP + 4];
+  __shared__ double hws[VPREP_CHUNK];
+  const int lane = lane_id(), wave = wave_id();
+  const int i16 = lane & 15, kq = lane >> 4;
+  // tile tt in 0..9 -> (mt, nt), mt <= nt (rows of the triangle start at 0, 4, 7, 9); wave w takes w, w + 4, w + 8
+  int TMq[3], TNq[3];
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    const int tt = wave + 4 * q;
+    const int mt = (tt >= 4) + (tt >= 7) + (tt >= 9);
+    const int start = (mt == 0) ? 0 : (mt == 1) ? 4 : (mt == 2) ? 7 : 9;
+    TMq[q] = mt;
+    TNq[q] = mt + (tt - start);
+  }
+  const int ntile = (wave < 2) ? 3 : 2;
+  v4d acc[3] = {v4d{}, v4d{}, v4d{}};
+  const int64_t r0 = (int64_t)blockIdx.x * rows_wg;
+  const int64_t r1 = r0 + rows_wg < n_pad ? r0 + rows_wg : n_pad;
+  for (int64_t j0 = r0; j0 < r1; j0 += VPREP_CHUNK) {
+    const int nr = (int)(r1 - j0 < VPREP_CHUNK ? r1 - j0 : VPREP_CHUNK);  // a multiple of 32
+    __syncthreads();  // the previous chunk has been consumed
+    // 16-byte pieces: piece p of component c holds rows j0 + 16 p .. + 15
+    const int npc = nr / 16;
+    int4 piece[2];
+    double hwv = 0.0;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int e = threadIdx.x + NT * u, c = e / npc, p = e % npc;
+      if (e < BBP * npc) piece[u] = *(const int4*)(Vt + (int64_t)c * n_pad + j0 + 16 * p);
+    }
+    if (threadIdx.x < nr) hwv = hw[j0 + threadIdx.x];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int e = threadIdx.x + NT * u, c = e / npc, p = e % npc;
+      if (e < BBP * npc) {
+        const int8_t* b = (const int8_t*)&piece[u];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) tile[16 * p + q][c] = b[q];
+      }
+    }
+    if (threadIdx.x < nr) hws[threadIdx.x] = hwv;
+    __syncthreads();
+    // row-major copy: 16-byte pieces of 64-byte rows
+    for (int e = threadIdx.x; e < nr * (BBP / 16); e += NT) {
+      const int jj = e >> 2, p = e & 3;
+      int4 v;
+      int8_t* vb = (int8_t*)&v;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) vb[q] = tile[jj][16 * p + q];
+      *(int4*)(Vr + (j0 + jj) * BBP + 16 * p) = v;
+    }
+    for (int k = 0; k < nr / 4; ++k) {
+      const int r = 4 * k + kq;
+      double v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = (double)tile[r][16 * q + i16];
+      const double wr = hws[r];
+#pragma unroll
+      for (int q = 0; q < 3; ++q) {
+        if (q < ntile) {
+          const int mt = TMq[q], nt = TNq[q];
+          const double va = (mt == 0) ? v[0] : (mt == 1) ? v[1] : (mt == 2) ? v[2] : v[3];
+          const double vb = (nt == 0) ? v[0] : (nt == 1) ? v[1] : (nt == 2) ? v[2] : v[3];
+          acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(wr * va, vb, acc[q], 0, 0, 0);
+        }
+      }
+    }
+  }
+  double* mine = partw + (int64_t)blockIdx.x * (BBP * BBP);
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    if (q < ntile) {
+      const int mt = TMq[q], nt = TNq[q];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        // v_mfma_f64_16x16x4f64 result: lane l, register r holds row l/16 + 4 r, column l%16
+        mine[(16 * mt + kq + 4 * r) * BBP + 16 * nt + i16] = acc[q][r];
+      }
+    }
+  }
+}
+
+// The weighted Gram from the partials of k_vprep_w, added in a fixed order
+// (workgroups q, q + 4, ... per quarter q, then the quarters in order), both
+// triangles into gramV.  Workgroup b takes the 64 entries [64 b, 64 b + 64).
+// grid: BBP * BBP / 64.
+__global__ __launch_bounds__(NT) void k_gramw_sum(const double* __restrict__ partw, int nwg,
+                                                  double* __restrict__ gramV) {
+  __shared__ double q4[4][64];
+  const int el = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int e = blockIdx.x * 64 + el, c = e >> 6, c2 = e & 63;
+  double v[VPREP_MAX_WG / 4];
+#pragma unroll
+  for (int k = 0; k < VPREP_MAX_WG / 4; ++k) {
+    const int g = q + 4 * k;
+    v[k] = (c <= c2 && g < nwg) ? partw[(int64_t)g * (BBP * BBP) + e] : 0.0;
+  }
+  double sum = 0.0;
+#pragma unroll
+  for (int k = 0; k < VPREP_MAX_WG / 4; ++k) sum += v[k];
+  q4[q][el] = sum;
+  __syncthreads();
+  if (q == 0 && c <= c2) {
+    const double d = ((q4[0][el] + q4[1][el]) + q4[2][el]) + q4[3][el];
+    gramV[e] = d;
+    gramV[c2 * BBP + c] = d;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // U-step Q = R diag(h~) V  (Eq. (3) second half, Sec. 2.5); the target
 // Z = Q G_V^{-1} follows in k_utarget
-// grid: nside side WGs (V^T V on int8 MFMA or, weighted, V^T H V on fp64
-//       MFMA, over K slices; the last of them adds the ridge and inverts;
-//       the raw Gram is kept for the scale solve) followed by ntile row groups of `rows` <= 32 rows, sized so
+// grid: nside side WGs (V^T V on int8 MFMA over K slices, the last of them
+//       adds the ridge and inverts; weighted: one side WG takes V^T H V,
+//       formed by k_vprep_w before the launch, and inverts it; the raw Gram
+//       is kept for the scale solve) followed by ntile row groups of `rows` <= 32 rows, sized so
 //       that the whole grid is resident at two workgroups per CU and every
 //       CU streams the same share of R; each row group stores Q, waits for
 //       G_V^{-1} and writes its Z rows and T_tau statistics.
@@ -943,9 +1088,8 @@ template <bool WEIGHTED>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_ustep(const float* __restrict__ R, const v4i* __restrict__ Vmf,
                                               const int8_t* __restrict__ Vr, const double* __restrict__ hw,
                                               double* __restrict__ Q, const unsigned* __restrict__ maxbits,
-                                              int64_t m_pad, int64_t n_pad, int bb, int* gacc, double* gpart,
-                                              unsigned* counter, double* ginvV, double* gramV, int nside,
-                                              int rows) {
+                                              int64_t m_pad, int64_t n_pad, int bb, int* gacc, unsigned* counter,
+                                              double* ginvV, double* gramV, int nside, int rows) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[USTEP_SMEM_LL];
@@ -954,10 +1098,14 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     __builtin_amdgcn_s_setprio(3);
     double* Gs = (double*)(smem + 2048);
     double* pbuf = Gs + 4096;
-    bool last = true;
-    if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, nside, gpart, counter, Gs);
-    else last = side_gram_acc(Vmf, n_pad, blockIdx.x, nside, gacc, counter, Gs, (int*)smem);
-    if (last) {
+    if (WEIGHTED) {
+      // one side workgroup: V^T H V was formed by k_vprep_w / k_gramw_sum
+      for (int e = threadIdx.x; e < 4096; e += NT) Gs[e] = gramV[e];
+      __syncthreads();
+      ridge_invert_store(Gs, pbuf, bb, ginvV);
+      return;
+    }
+    if (side_gram_acc(Vmf, n_pad, blockIdx.x, nside, gacc, counter, Gs, (int*)smem)) {
       for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
       __syncthreads();
       ridge_invert_store(Gs, pbuf, bb, ginvV);
@@ -2257,11 +2405,11 @@ template <bool WEIGHTED>
 __global__ __launch_bounds__(NT) void k_gram_v(const v4i* __restrict__ Vmf, const int8_t* __restrict__ Vr,
                                                const double* __restrict__ hw, int64_t n_pad, int bb, int* gparti,
                                                double* gpart, unsigned* counter, double* ginvV, double* gramV) {
-  __shared__ int red[4096];
+  __shared__ __attribute__((aligned(16))) int red[4096];
   __shared__ double Gs[4096];
   __shared__ double colbuf[1024];
   bool last;
-  if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, (int)gridDim.x, gpart, counter, Gs);
+  if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, (int)gridDim.x, gpart, counter, Gs, (char*)red);
   else last = side_gram_int(Vmf, n_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red);
   if (!last) return;
   for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
@@ -2380,19 +2528,26 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
                         Timer* tm) {
   hipError_t e;
-  const unsigned nside = weighted ? NSIDE_W : NSIDE_GRAM;
+  const unsigned nside = weighted ? 1 : NSIDE_GRAM;
   const unsigned grid = (unsigned)(nside + w.ntu);
   if (weighted) {
-    hipLaunchKernelGGL(k_transpose8, dim3((unsigned)(w.n_pad / 32)), dim3(NT), 0, s, w.Vt, w.Vr, w.n_pad,
-                       (unsigned short*)nullptr);
+    // rows per preparation workgroup: a multiple of 32, at least 32, at most VPREP_MAX_WG workgroups
+    int64_t rows_wg = (w.n_pad + VPREP_MAX_WG - 1) / VPREP_MAX_WG;
+    rows_wg = rows_wg < VPREP_MIN_ROWS ? VPREP_MIN_ROWS : (rows_wg + TILE - 1) / TILE * TILE;
+    const int nwg = (int)((w.n_pad + rows_wg - 1) / rows_wg);
+    hipLaunchKernelGGL(k_vprep_w, dim3((unsigned)nwg), dim3(NT), 0, s, (const int8_t*)w.Vt, w.Vr, w.n_pad,
+                       (const double*)w.hw, (int)rows_wg, w.partw);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_gramw_sum, dim3(BBP * BBP / 64), dim3(NT), 0, s, (const double*)w.partw, nwg, w.gramV);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
-                                     w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
+                                     w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows);
   } else {
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
-                                     w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096, w.gpart,
+                                     w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows);
   }
   e = hipGetLastError();
