@@ -341,7 +341,13 @@ __device__ __forceinline__ void load_ginv(const double* ginv, double (&a)[16]) {
   for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(p + ks * 64);
 }
 
-__device__ __forceinline__ void spd_inverse64(double* A, double* pbuf, double* out = nullptr) {
+// nk: pivot blocks to sweep, ceil(bb / 4) for a block of bb real components
+// whose padding is the identity.  A pivot block made only of padding has
+// A - I exactly zero in its rows (the padding diagonal is exactly 1 before
+// and after the power-of-two scaling, and no earlier step touches rows
+// that are zero in every real column), so its step would add exactly zero:
+// stopping after nk blocks gives the same inverse bit for bit.
+__device__ __forceinline__ void spd_inverse64(double* A, double* pbuf, int nk, double* out = nullptr) {
   __shared__ int sexp[64];
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
@@ -369,10 +375,11 @@ __device__ __forceinline__ void spd_inverse64(double* A, double* pbuf, double* o
   // launch, and its code is fetched cold while the streaming workgroups
   // load the memory system, so a 4x smaller body is faster.
 #pragma unroll 1
-  for (int ntK = 0; ntK < 4; ++ntK)
+  for (int ntK = 0; ntK < 4 && 4 * ntK < nk; ++ntK)
 #pragma unroll
   for (int rK = 0; rK < 4; ++rK) {
     const int K = 4 * ntK + rK;
+    if (K >= nk) break;
     // The sweep keeps A symmetric, so the pivot column block equals the
     // pivot rows: their owner (wave K / 4, register K % 4) publishes
     // C^T[c][j] = A[4K + c][j] - delta(j, 4K + c) and every wave builds
@@ -457,7 +464,7 @@ __device__ __forceinline__ void ridge_invert_store(double* G, double* colbuf, in
     }
     return;
   }
-  spd_inverse64(G, colbuf, ginv_out);
+  spd_inverse64(G, colbuf, (bb + 3) >> 2, ginv_out);
 }
 
 // ---------------------------------------------------------------------------
@@ -1519,7 +1526,7 @@ __device__ __forceinline__ double scale_solve(int* gacc, int bb, const double* _
   const double delta = EXTERND_SCALE_GUARD_REL * tr / (double)bb;
   if (t < bb) Gs[t * 64 + t] += delta;
   __syncthreads();
-  spd_inverse64(Gs, colbuf);
+  spd_inverse64(Gs, colbuf, (bb + 3) >> 2);
   // g_c: the per-split partial sums in split order
   __shared__ double s_g[BBP];
   if (t < BBP) {
