@@ -218,6 +218,9 @@ def main():
                     help="time inference with the workload's factorization (externd_apply, nb = 1 and 8)")
     ap.add_argument("--sweeps", type=int, default=None,
                     help="time externd_factorize_refined with this many refinement sweeps instead")
+    ap.add_argument("--concurrency", type=int, default=4,
+                    help="block4b: factorizations in flight at once (one HIP stream, host thread and "
+                         "workspace each; the 21 jobs are dealt longest first)")
     ap.add_argument("--target-energy", type=float, default=None,
                     help="time the energy-target run instead (stop at the first block with E >= target, "
                          "mu of the workload as the maximum)")
@@ -371,28 +374,56 @@ def bench_block(binding, torch, args):
         name, A, h = synth.transformer_block(idx)
         mats.append((name, torch.from_numpy(A).to(dev), torch.from_numpy(h).to(dev)))
     taus, mu, block, iters = (0.7, 1.0, 2.0), 3.5, 64, 8
-    # one workspace sized for the largest matrix and rank
-    ws = torch.empty(max(binding.workspace_bytes(A.shape[0], A.shape[1], binding.rank(A.shape[0], A.shape[1], mu))
-                         for _, A, _ in mats), dtype=torch.uint8, device=dev)
+    jobs = [(name, A, h, tau) for tau in taus for name, A, h in mats]
+    # longest first: cost ~ k m n ~ mu min(m, n) m n
+    jobs.sort(key=lambda j: -min(j[1].shape) * j[1].shape[0] * j[1].shape[1])
+    nconc = max(1, args.concurrency)
+    wsize = max(binding.workspace_bytes(A.shape[0], A.shape[1], binding.rank(A.shape[0], A.shape[1], mu))
+                for _, A, _ in mats)
+    lanes = []
+    for _ in range(nconc):
+        st = torch.cuda.Stream()      # default priority
+        with torch.cuda.stream(st):
+            lanes.append((st, torch.empty(wsize, dtype=torch.uint8, device=dev)))
+    torch.cuda.synchronize()
+
+    def run_job(lane, job):
+        st, ws = lane
+        name, A, h, tau = job
+        with torch.cuda.stream(st):
+            t0 = time.perf_counter()
+            r = binding.factorize(A, mu, tau, block, iters, h=h, workspace=ws, stream=st)
+            dt = time.perf_counter() - t0
+        m, n = A.shape
+        pts = {}
+        for mu_c in (2.0, 2.5, 3.5):
+            b = binding.rank(m, n, mu_c) // r.block - 1
+            pts[str(mu_c)] = {"E": float(r.curve[b]), "E_w": float(r.curve_w[b])}
+        return f"{name}@tau{tau}", {"m": m, "n": n, "k": r.k, "sec": dt, "components_per_s": r.k / dt,
+                                    "checkpoints": pts}
 
     def one_step(record):
-        per = {}
-        for tau in taus:
-            for name, A, h in mats:
-                torch.cuda.synchronize()
-                t0 = time.perf_counter()
-                r = binding.factorize(A, mu, tau, block, iters, h=h, workspace=ws)
-                torch.cuda.synchronize()
-                dt = time.perf_counter() - t0
-                if record:
-                    m, n = A.shape
-                    pts = {}
-                    for mu_c in (2.0, 2.5, 3.5):
-                        b = binding.rank(m, n, mu_c) // r.block - 1
-                        pts[str(mu_c)] = {"E": float(r.curve[b]), "E_w": float(r.curve_w[b])}
-                    per[f"{name}@tau{tau}"] = {"m": m, "n": n, "k": r.k, "sec": dt, "components_per_s": r.k / dt,
-                                               "checkpoints": pts}
-        return per
+        import threading
+        per, lock, nxt = {}, threading.Lock(), [0]
+
+        def worker(i):
+            while True:
+                with lock:
+                    if nxt[0] >= len(jobs):
+                        return
+                    job = jobs[nxt[0]]
+                    nxt[0] += 1
+                key, val = run_job(lanes[i], job)
+                with lock:
+                    per[key] = val
+
+        threads = [threading.Thread(target=worker, args=(i,)) for i in range(nconc)]
+        for th in threads:
+            th.start()
+        for th in threads:
+            th.join()
+        torch.cuda.synchronize()
+        return per if record else {}
 
     for _ in range(args.warmup):
         one_step(False)
@@ -407,8 +438,10 @@ def bench_block(binding, torch, args):
         "unit": "components/s", "higher_is_better": True, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "sec_per_step": sec, "data": "synthetic",
         "config": {"workload": "transformer_block_4b_7mat_mu3.5_tau0.7-1.0-2.0_b64_imatrix", "mu": mu,
-                   "taus": list(taus), "block": block, "iters": iters, "importance": True},
-        "sec_per_tau": {str(t): sum(v["sec"] for k2, v in per.items() if k2.endswith(f"tau{t}")) for t in taus},
+                   "taus": list(taus), "block": block, "iters": iters, "importance": True,
+                   "concurrency": nconc},
+        "job_sec_sum_per_tau": {str(t): sum(v["sec"] for k2, v in per.items() if k2.endswith(f"tau{t}"))
+                                for t in taus},
         "matrices": per,
     }), flush=True)
 
