@@ -59,7 +59,7 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(double) * 4096,                           // 9 ginvU
       sizeof(double) * 4096,                           // 10 ginvV
       sizeof(double) * 4096,                           // 11 gramV
-      sizeof(double) * 4096 * NSIDE_MAX,               // 12 gpart
+      0,                                               // 12 (unused)
       sizeof(int) * 4096 * NSIDE_MAX,                  // 13 gparti
       sizeof(double) * (size_t)(L.gd * L.n_pad),       // 14 colE_part
       sizeof(double) * (size_t)L.n_pad,                // 15 hw
@@ -121,7 +121,6 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.ginvU = (double*)(b + L.off[9]);
   w.ginvV = (double*)(b + L.off[10]);
   w.gramV = (double*)(b + L.off[11]);
-  w.gpart = (double*)(b + L.off[12]);
   w.gparti = (int*)(b + L.off[13]);
   w.colE_part = (double*)(b + L.off[14]);
   w.hw = (double*)(b + L.off[15]);

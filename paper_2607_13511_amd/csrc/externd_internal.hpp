@@ -15,11 +15,10 @@ namespace externd {
 // are padded to multiples of TILE (zero padding, never touched by updates).
 constexpr int BBP = 64;
 constexpr int TILE = 32;
-// Side workgroups that build Gram matrices next to a contraction: integer
-// Grams (int8 MFMA) and the weighted fp64 Gram (fp64 MFMA).
+// Workgroups that build integer Gram matrices (int8 MFMA), beside a
+// contraction or in a launch of their own.
 constexpr int NSIDE_INT = 8;   // integer-Gram workgroups of the scale solve
 constexpr int NSIDE_GRAM = 16; // workgroups of the integer Gram launch
-constexpr int NSIDE_W = 16;
 constexpr int NSIDE_MAX = 16;
 constexpr int GV_MAX = 8;      // row groups of the V-step contraction
 // Workgroups of the contraction kernels resident at once: two per CU on
@@ -76,7 +75,6 @@ struct Ws {
   double* ginvU;         // BBP x BBP
   double* ginvV;         // BBP x BBP
   double* gramV;         // BBP x BBP raw V^T H V (no ridge)
-  double* gpart;         // NSIDE_MAX x BBP x BBP partial Gram matrices
   int* gparti;           // NSIDE_MAX x BBP x BBP partial integer Grams
   double* colE_part;     // gd x n_pad partial column energies
   double* hw;            // n_pad: h~ (fp64), 1 when unweighted
@@ -189,6 +187,7 @@ hipError_t launch_load_cm(double* Xcm, const double* X, int64_t len, int64_t len
 hipError_t launch_unstage(const Ws& w, float* A, hipStream_t s);
 hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2, hipStream_t s);
 hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s);
+hipError_t launch_gram_w(const Ws& w, hipStream_t s);
 hipError_t launch_gvec(const Ws& w, int bb, hipStream_t s);
 // X^T X of the factor in Umf (which = 0) or Vmf (which = 1) into its Gram accumulator.
 hipError_t launch_gram_acc(const Ws& w, int which, hipStream_t s);

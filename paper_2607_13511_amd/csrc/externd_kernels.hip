@@ -669,100 +669,6 @@ __device__ __forceinline__ void take_gram(int* gacc, double* G) {
   for (int j = 0; j < 4; ++j) ((int4*)gacc)[threadIdx.x + NT * j] = make_int4(0, 0, 0, 0);
 }
 
-// Partial weighted Gram V^T diag(hw) V over this workgroup's share of rows
-// of Vr (n_pad x BBP int8, row-major) on fp64 MFMA (v_mfma_f64_16x16x4):
-// products h~_j v_jc v_jc' are exact and the sums are fp64.  The 10
-// 16x16 tiles of the upper triangle are dealt to the 4 waves; each wave
-// covers all of the workgroup's rows for its tiles.  The rows and their
-// weights are staged through LDS in chunks of SIDE_W_CHUNK K steps (one
-// round of coalesced loads per chunk instead of a dependent load per K
-// step).  Same last-workgroup protocol as side_gram_int.
-constexpr int SIDE_W_CHUNK = 56;  // K steps of 4 rows per staged chunk: 56 x 4 x (64 + 8) bytes <= 16 KB
-__device__ __forceinline__ bool side_gram_w(const int8_t* __restrict__ Vr, const double* __restrict__ hw, int64_t L, int side,
-                            int nside, double* gpart, unsigned* counter, double* G, char* stage /* LDS, 16 KB */) {
-  const int lane = lane_id(), wave = wave_id();
-  const int i16 = lane & 15, kq = lane >> 4;
-  const int64_t nks = L / 4;
-  const int64_t ks0 = side * nks / nside, ks1 = (side + 1) * nks / nside;
-  // tile tt in 0..9 -> (mt, nt), mt <= nt, row-major over the upper
-  // triangle (rows start at 0, 4, 7, 9); wave w takes tt = w, w + 4, w + 8
-  int TMq[3], TNq[3];
-#pragma unroll
-  for (int q = 0; q < 3; ++q) {
-    const int tt = wave + 4 * q;
-    const int mt = (tt >= 4) + (tt >= 7) + (tt >= 9);
-    const int start = (mt == 0) ? 0 : (mt == 1) ? 4 : (mt == 2) ? 7 : 9;
-    TMq[q] = mt;
-    TNq[q] = mt + (tt - start);
-  }
-  v4d acc[3] = {v4d{}, v4d{}, v4d{}};
-  const int ntile = (wave < 2) ? 3 : 2;
-  int8_t* sv = (int8_t*)stage;                                         // rows x 64 bytes
-  double* sw = (double*)(stage + SIDE_W_CHUNK * 4 * BBP);              // their weights
-  for (int64_t c0 = ks0; c0 < ks1; c0 += SIDE_W_CHUNK) {
-    const int nk = (int)(ks1 - c0 < SIDE_W_CHUNK ? ks1 - c0 : SIDE_W_CHUNK);
-    __syncthreads();  // the previous chunk has been consumed
-    const int4* src = (const int4*)(Vr + 4 * c0 * BBP);
-    for (int e = threadIdx.x; e < nk * 4 * (BBP / 16); e += blockDim.x) ((int4*)sv)[e] = src[e];
-    for (int e = threadIdx.x; e < nk * 4; e += blockDim.x) sw[e] = hw[4 * c0 + e];
-    __syncthreads();
-    for (int k = 0; k < nk; ++k) {
-      const int r = 4 * k + kq;
-      const int8_t* row = sv + r * BBP;
-      const double w = sw[r];
-      double v[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = (double)row[16 * q + i16];
-#pragma unroll
-      for (int q = 0; q < 3; ++q) {
-        if (q < ntile) {
-          const int mt = TMq[q], nt = TNq[q];
-          const double va = (mt == 0) ? v[0] : (mt == 1) ? v[1] : (mt == 2) ? v[2] : v[3];
-          const double vb = (nt == 0) ? v[0] : (nt == 1) ? v[1] : (nt == 2) ? v[2] : v[3];
-          acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(w * va, vb, acc[q], 0, 0, 0);
-        }
-      }
-    }
-  }
-  double* mine = gpart + (size_t)side * 4096;
-#pragma unroll
-  for (int q = 0; q < 3; ++q) {
-    if (q < ntile) {
-      const int mt = TMq[q], nt = TNq[q];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        // v_mfma_f64_16x16x4f64 result: lane l, register r holds row l/16 + 4 r, column l%16
-        const int gi = 16 * mt + kq + 4 * r, gj = 16 * nt + i16;
-        mine[gi * 64 + gj] = acc[q][r];
-        if (mt != nt) mine[gj * 64 + gi] = acc[q][r];
-      }
-    }
-  }
-  __threadfence();
-  __syncthreads();
-  __shared__ int s_last;
-  if (threadIdx.x == 0) {
-    const unsigned old = atomicAdd(counter, 1u);
-    s_last = (old == (unsigned)(nside - 1));
-  }
-  __syncthreads();
-  if (!s_last) return false;
-  __threadfence();
-  for (int e2 = threadIdx.x; e2 < 2048; e2 += blockDim.x) {
-    double2 acc2 = make_double2(0.0, 0.0);
-#pragma unroll 8
-    for (int q = 0; q < nside; ++q) {
-      const double2 v = ((const double2*)(gpart + (size_t)q * 4096))[e2];
-      acc2.x += v.x;
-      acc2.y += v.y;
-    }
-    G[2 * e2] = acc2.x;
-    G[2 * e2 + 1] = acc2.y;
-  }
-  if (threadIdx.x == 0) *counter = 0u;
-  __syncthreads();
-  return true;
-}
 
 // ---------------------------------------------------------------------------
 // Targets on fp64 MFMA (v_mfma_f64_16x16x4f64), one 32-index tile at a
@@ -944,8 +850,8 @@ __global__ __launch_bounds__(NT) void k_vtarget(const long long* __restrict__ Pp
 // Weighted U-step preparation (Sec. 2.5): V row-major (Vr) from the
 // component-major Vt, and this workgroup's partial of the weighted Gram
 // V^T diag(h~) V on fp64 MFMA (v_mfma_f64_16x16x4; the products
-// h~_j v_jc v_jc' are exact, the sums fp64 in a fixed order), 16x16 tiles of
-// the upper triangle dealt to the 4 waves as in side_gram_w.  Workgroup g
+// h~_j v_jc v_jc' are exact, the sums fp64 in a fixed order), the 10 16x16
+// tiles of the upper triangle dealt to the 4 waves.  Workgroup g
 // covers rows [g rows_wg, (g + 1) rows_wg), staged in LDS in chunks of
 // VPREP_CHUNK, and writes its partial to partw[g]; k_gramw_sum adds the
 // partials in workgroup order.  Running before the U-step launch, the Gram
@@ -2406,19 +2312,15 @@ __global__ __launch_bounds__(NT) void k_load_cm(double* Xcm, const double* X, in
 }
 
 
-// Gram of V alone (raw V^T H V and its ridge inverse), for the scale step
-// entry point.  grid: NSIDE_INT or NSIDE_W.
-template <bool WEIGHTED>
-__global__ __launch_bounds__(NT) void k_gram_v(const v4i* __restrict__ Vmf, const int8_t* __restrict__ Vr,
-                                               const double* __restrict__ hw, int64_t n_pad, int bb, int* gparti,
-                                               double* gpart, unsigned* counter, double* ginvV, double* gramV) {
+// Integer Gram of V alone (raw V^T V and its ridge inverse), for the scale
+// step entry point; the weighted Gram comes from k_vprep_w / k_gramw_sum.
+// grid: NSIDE_INT.
+__global__ __launch_bounds__(NT) void k_gram_v(const v4i* __restrict__ Vmf, int64_t n_pad, int bb, int* gparti,
+                                               unsigned* counter, double* ginvV, double* gramV) {
   __shared__ __attribute__((aligned(16))) int red[4096];
   __shared__ double Gs[4096];
   __shared__ double colbuf[1024];
-  bool last;
-  if (WEIGHTED) last = side_gram_w(Vr, hw, n_pad, blockIdx.x, (int)gridDim.x, gpart, counter, Gs, (char*)red);
-  else last = side_gram_int(Vmf, n_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red);
-  if (!last) return;
+  if (!side_gram_int(Vmf, n_pad, blockIdx.x, (int)gridDim.x, gparti, counter, Gs, red)) return;
   for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
   __syncthreads();
   ridge_invert_store(Gs, colbuf, bb, ginvV);
@@ -2532,22 +2434,28 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
   return hipGetLastError();
 }
 
+// Weighted: V row-major and the raw weighted Gram V^T diag(h~) V into
+// gramV, before the U-step launch.
+hipError_t launch_gram_w(const Ws& w, hipStream_t s) {
+  // rows per preparation workgroup: a multiple of 32, at least 32, at most VPREP_MAX_WG workgroups
+  int64_t rows_wg = (w.n_pad + VPREP_MAX_WG - 1) / VPREP_MAX_WG;
+  rows_wg = rows_wg < VPREP_MIN_ROWS ? VPREP_MIN_ROWS : (rows_wg + TILE - 1) / TILE * TILE;
+  const int nwg = (int)((w.n_pad + rows_wg - 1) / rows_wg);
+  hipLaunchKernelGGL(k_vprep_w, dim3((unsigned)nwg), dim3(NT), 0, s, (const int8_t*)w.Vt, w.Vr, w.n_pad,
+                     (const double*)w.hw, (int)rows_wg, w.partw);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_gramw_sum, dim3(BBP * BBP / 64), dim3(NT), 0, s, (const double*)w.partw, nwg, w.gramV);
+  return hipGetLastError();
+}
+
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
                         Timer* tm) {
   hipError_t e;
   const unsigned nside = weighted ? 1 : NSIDE_GRAM;
   const unsigned grid = (unsigned)(nside + w.ntu);
   if (weighted) {
-    // rows per preparation workgroup: a multiple of 32, at least 32, at most VPREP_MAX_WG workgroups
-    int64_t rows_wg = (w.n_pad + VPREP_MAX_WG - 1) / VPREP_MAX_WG;
-    rows_wg = rows_wg < VPREP_MIN_ROWS ? VPREP_MIN_ROWS : (rows_wg + TILE - 1) / TILE * TILE;
-    const int nwg = (int)((w.n_pad + rows_wg - 1) / rows_wg);
-    hipLaunchKernelGGL(k_vprep_w, dim3((unsigned)nwg), dim3(NT), 0, s, (const int8_t*)w.Vt, w.Vr, w.n_pad,
-                       (const double*)w.hw, (int)rows_wg, w.partw);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_gramw_sum, dim3(BBP * BBP / 64), dim3(NT), 0, s, (const double*)w.partw, nwg, w.gramV);
-    e = hipGetLastError();
+    e = launch_gram_w(w, s);
     if (e != hipSuccess) return e;
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096,
@@ -2649,12 +2557,9 @@ hipError_t launch_load_cm(double* Xcm, const double* X, int64_t len, int64_t len
 }
 
 hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s) {
-  if (weighted)
-    hipLaunchKernelGGL(k_gram_v<true>, dim3(NSIDE_W), dim3(NT), 0, s, (const v4i*)w.Vmf, w.Vr, w.hw, w.n_pad, bb, w.gparti, w.gpart,
-                       w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
-  else
-    hipLaunchKernelGGL(k_gram_v<false>, dim3(NSIDE_INT), dim3(NT), 0, s, (const v4i*)w.Vmf, w.Vr, w.hw, w.n_pad, bb, w.gparti,
-                       w.gpart, w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
+  if (weighted) return launch_gram_w(w, s);
+  hipLaunchKernelGGL(k_gram_v, dim3(NSIDE_INT), dim3(NT), 0, s, (const v4i*)w.Vmf, w.n_pad, bb, w.gparti,
+                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
   return hipGetLastError();
 }
 hipError_t launch_gram_acc(const Ws& w, int which, hipStream_t s) {
