@@ -813,7 +813,7 @@ __device__ __forceinline__ void vtarget_sum16(const long long* __restrict__ Pp, 
   }
 }
 
-__global__ __launch_bounds__(NT) void k_vtarget(const long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vtarget(const long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
                                                 int64_t n_pad, int gv, const double* __restrict__ ginvU,
                                                 double* __restrict__ Y, int64_t n, double* ps, double* pm, int* pi) {
   __shared__ double Ps[64 * 17];
@@ -860,24 +860,53 @@ __global__ __launch_bounds__(NT) void k_vtarget(const long long* __restrict__ Pp
 // ---------------------------------------------------------------------------
 constexpr int VPREP_CHUNK = 128;
 constexpr int VPREP_MIN_ROWS = 32;
-__global__ __launch_bounds__(NT) void k_vprep_w(const int8_t* __restrict__ Vt, int8_t* __restrict__ Vr, int64_t n_pad,
+// tile tt in 0..9 of the upper triangle of 16x16 tiles -> (row tile, column
+// tile); the rows of the triangle start at tiles 0, 4, 7, 9.  Wave w takes
+// tiles w, w + 4 and (waves 0, 1) w + 8.
+__host__ __device__ constexpr int vprep_tm(int tt) { return (tt >= 4) + (tt >= 7) + (tt >= 9); }
+__host__ __device__ constexpr int vprep_tn(int tt) {
+  return vprep_tm(tt) + tt - (vprep_tm(tt) == 0 ? 0 : vprep_tm(tt) == 1 ? 4 : vprep_tm(tt) == 2 ? 7 : 9);
+}
+// One chunk of nr staged rows into wave W's accumulators: the tile indices are
+// compile-time, so the accumulators stay in place and the three chains interleave.
+template <int W>
+__device__ __forceinline__ void vprep_gram_chunk(const int8_t (*tile)[BBP + 4], const double* hws, int nr, int i16,
+                                                 int kq, v4d* acc) {
+  constexpr int NTILE = W < 2 ? 3 : 2;
+  // nr is a multiple of 32: eight 4-row steps per pass, their LDS reads batched
+  for (int k0 = 0; k0 < nr / 4; k0 += 8) {
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      const int r = 4 * (k0 + kk) + kq;
+      double v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = (double)tile[r][16 * q + i16];
+      const double wr = hws[r];
+#pragma unroll
+      for (int q = 0; q < NTILE; ++q)
+        acc[q] = mfma_f64(wr * v[vprep_tm(W + 4 * q)], v[vprep_tn(W + 4 * q)], acc[q]);
+    }
+  }
+}
+template <int W>
+__device__ __forceinline__ void vprep_gram_store(double* mine, int i16, int kq, const v4d* acc) {
+  constexpr int NTILE = W < 2 ? 3 : 2;
+#pragma unroll
+  for (int q = 0; q < NTILE; ++q) {
+    const int mt = vprep_tm(W + 4 * q), nt = vprep_tn(W + 4 * q);
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      // v_mfma_f64_16x16x4f64 result: lane l, register r holds row l/16 + 4 r, column l%16
+      mine[(16 * mt + kq + 4 * r) * BBP + 16 * nt + i16] = acc[q][r];
+  }
+}
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vprep_w(const int8_t* __restrict__ Vt, int8_t* __restrict__ Vr, int64_t n_pad,
                                                 const double* __restrict__ hw, int rows_wg,
                                                 double* __restrict__ partw) {
   __shared__ int8_t tile[VPREP_CHUNK][BBP + 4];
   __shared__ double hws[VPREP_CHUNK];
   const int lane = lane_id(), wave = wave_id();
   const int i16 = lane & 15, kq = lane >> 4;
-  // tile tt in 0..9 -> (mt, nt), mt <= nt (rows of the triangle start at 0, 4, 7, 9); wave w takes w, w + 4, w + 8
-  int TMq[3], TNq[3];
-#pragma unroll
-  for (int q = 0; q < 3; ++q) {
-    const int tt = wave + 4 * q;
-    const int mt = (tt >= 4) + (tt >= 7) + (tt >= 9);
-    const int start = (mt == 0) ? 0 : (mt == 1) ? 4 : (mt == 2) ? 7 : 9;
-    TMq[q] = mt;
-    TNq[q] = mt + (tt - start);
-  }
-  const int ntile = (wave < 2) ? 3 : 2;
   v4d acc[3] = {v4d{}, v4d{}, v4d{}};
   const int64_t r0 = (int64_t)blockIdx.x * rows_wg;
   const int64_t r1 = r0 + rows_wg < n_pad ? r0 + rows_wg : n_pad;
@@ -914,34 +943,20 @@ __global__ __launch_bounds__(NT) void k_vprep_w(const int8_t* __restrict__ Vt, i
       for (int q = 0; q < 16; ++q) vb[q] = tile[jj][16 * p + q];
       *(int4*)(Vr + (j0 + jj) * BBP + 16 * p) = v;
     }
-    for (int k = 0; k < nr / 4; ++k) {
-      const int r = 4 * k + kq;
-      double v[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = (double)tile[r][16 * q + i16];
-      const double wr = hws[r];
-#pragma unroll
-      for (int q = 0; q < 3; ++q) {
-        if (q < ntile) {
-          const int mt = TMq[q], nt = TNq[q];
-          const double va = (mt == 0) ? v[0] : (mt == 1) ? v[1] : (mt == 2) ? v[2] : v[3];
-          const double vb = (nt == 0) ? v[0] : (nt == 1) ? v[1] : (nt == 2) ? v[2] : v[3];
-          acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(wr * va, vb, acc[q], 0, 0, 0);
-        }
-      }
+    // wave is uniform: each branch runs one wave's compile-time tile set
+    switch (wave) {
+      case 0: vprep_gram_chunk<0>(tile, hws, nr, i16, kq, acc); break;
+      case 1: vprep_gram_chunk<1>(tile, hws, nr, i16, kq, acc); break;
+      case 2: vprep_gram_chunk<2>(tile, hws, nr, i16, kq, acc); break;
+      default: vprep_gram_chunk<3>(tile, hws, nr, i16, kq, acc); break;
     }
   }
   double* mine = partw + (int64_t)blockIdx.x * (BBP * BBP);
-#pragma unroll
-  for (int q = 0; q < 3; ++q) {
-    if (q < ntile) {
-      const int mt = TMq[q], nt = TNq[q];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        // v_mfma_f64_16x16x4f64 result: lane l, register r holds row l/16 + 4 r, column l%16
-        mine[(16 * mt + kq + 4 * r) * BBP + 16 * nt + i16] = acc[q][r];
-      }
-    }
+  switch (wave) {
+    case 0: vprep_gram_store<0>(mine, i16, kq, acc); break;
+    case 1: vprep_gram_store<1>(mine, i16, kq, acc); break;
+    case 2: vprep_gram_store<2>(mine, i16, kq, acc); break;
+    default: vprep_gram_store<3>(mine, i16, kq, acc); break;
   }
 }
 
@@ -1125,7 +1140,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // statistics, after the contraction launch (G_V^{-1} from its side path).
 // grid: m_pad / 32 row tiles (statistics per tile).  Rows past m hold
 // Q = 0 (zero residual padding), so their targets are zero.
-__global__ __launch_bounds__(NT) void k_utarget(const double* __restrict__ Q, const double* __restrict__ ginvV,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_utarget(const double* __restrict__ Q, const double* __restrict__ ginvV,
                                                 double* __restrict__ Z, int64_t m, int64_t m_pad, double* ps,
                                                 double* pm, int* pi) {
   const int nrt = (int)(m_pad / TILE);
@@ -1455,7 +1470,7 @@ __device__ __forceinline__ double scale_solve(int* gacc, int bb, const double* _
   return want_gain ? block_sum_d(gain, s_trb) : 0.0;
 }
 
-__global__ __launch_bounds__(NT) void k_scale(int* gacc, int bb, const double* __restrict__ gramV,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_scale(int* gacc, int bb, const double* __restrict__ gramV,
                                               const double* __restrict__ gvec, double* dvec, float* dF, float* Dout) {
   __shared__ double Gs[4096];
   __shared__ double colbuf[1024];
@@ -2033,7 +2048,7 @@ __device__ __forceinline__ int8_t trit_decode(unsigned byte, int64_t pos) {
 // sg: null unless the single-entry option is on; then the scales were
 // settled by k_safeguard, and when it fired (sg[0]) the block written out
 // is u = e_row, v = (+-1) e_col in component 0 and zero components after.
-__global__ __launch_bounds__(NT) void k_block_out(int* gacc, int bb, const double* __restrict__ gramV,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_block_out(int* gacc, int bb, const double* __restrict__ gramV,
                                                   const double* __restrict__ gvec, double* dvec, float* dF,
                                                   float* Dout, const int8_t* __restrict__ Ut, int8_t* __restrict__ Ur,
                                                   unsigned short* __restrict__ Ub, int64_t m, int64_t m_pad,
@@ -2195,7 +2210,7 @@ __global__ __launch_bounds__(NT) void k_revisit_load(const uint8_t* __restrict__
 // the deflation.  Otherwise the deflation takes the old scales D and the
 // outputs stay.  *decision = 1 / 0; *accepted counts the kept new blocks.
 // grid: one WG.
-__global__ __launch_bounds__(NT) void k_revisit_decide(int* gacc, int bb, const double* __restrict__ gramV,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_revisit_decide(int* gacc, int bb, const double* __restrict__ gramV,
                                                        const double* __restrict__ gvec, double* dvec, float* dF,
                                                        float* D, const double* fro2_prev,
                                                        const double* fro2_added, unsigned* decision,
@@ -2231,7 +2246,7 @@ __global__ __launch_bounds__(NT) void k_revisit_decide(int* gacc, int bb, const 
 // exactly.  sg receives (fired, i, j, R_ij < 0); *fired counts the blocks.
 // grid: one WG.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NT) void k_safeguard(int* gacc, int bb, const double* __restrict__ gramV,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_safeguard(int* gacc, int bb, const double* __restrict__ gramV,
                                                   const double* __restrict__ gvec, double* dvec, float* dF,
                                                   float* Dout, const float* __restrict__ R, int64_t n, int64_t n_pad,
                                                   const unsigned long long* __restrict__ argkey, unsigned* sg,
@@ -2315,7 +2330,7 @@ __global__ __launch_bounds__(NT) void k_load_cm(double* Xcm, const double* X, in
 // Integer Gram of V alone (raw V^T V and its ridge inverse), for the scale
 // step entry point; the weighted Gram comes from k_vprep_w / k_gramw_sum.
 // grid: NSIDE_INT.
-__global__ __launch_bounds__(NT) void k_gram_v(const v4i* __restrict__ Vmf, int64_t n_pad, int bb, int* gparti,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gram_v(const v4i* __restrict__ Vmf, int64_t n_pad, int bb, int* gparti,
                                                unsigned* counter, double* ginvV, double* gramV) {
   __shared__ __attribute__((aligned(16))) int red[4096];
   __shared__ double Gs[4096];
@@ -2328,7 +2343,7 @@ __global__ __launch_bounds__(NT) void k_gram_v(const v4i* __restrict__ Vmf, int6
 
 // Integer Gram of a factor given by the caller (step entry points): adds
 // X^T X into gacc.  grid: NSIDE_GRAM WGs over the K steps.
-__global__ __launch_bounds__(NT) void k_gram_acc(const v4i* __restrict__ Xmf, int64_t L_pad, int* gacc) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gram_acc(const v4i* __restrict__ Xmf, int64_t L_pad, int* gacc) {
   __shared__ int red[4 * 4096];
   const int nks = (int)(L_pad / TILE);
   gram_accumulate(Xmf, (int)((long long)blockIdx.x * nks / gridDim.x), (int)((long long)(blockIdx.x + 1) * nks / gridDim.x),
