@@ -1215,11 +1215,19 @@ __device__ __forceinline__ double tern_chunk(const double* __restrict__ x, const
   __shared__ int shi[4];
   const int tid = threadIdx.x;
   double psr[TERN_SP], pmr[TERN_SP];
+  // loads from clamped indices, masked afterwards: a load under a branch
+  // would be waited for at the join before the next one is issued
 #pragma unroll
   for (int k = 0; k < TERN_SP; ++k) {
-    const int t = tid + k * NT;
-    psr[k] = t < ntile ? ps[t] : 0.0;
-    pmr[k] = t < ntile ? pm[t] : -1.0;
+    const int t = tid + k * NT, tc = t < ntile ? t : 0;
+    psr[k] = ps[tc];
+    pmr[k] = pm[tc];
+  }
+#pragma unroll
+  for (int k = 0; k < TERN_SP; ++k) {
+    const bool ok = tid + k * NT < ntile;
+    psr[k] = ok ? psr[k] : 0.0;
+    pmr[k] = ok ? pmr[k] : -1.0;
   }
   double xc[TERN_XS], qc[TERN_XS];
 #pragma unroll
@@ -1361,12 +1369,16 @@ __global__ __launch_bounds__(NT) void k_init_gather(const float* __restrict__ R,
   const int64_t i0 = (int64_t)rt * TILE + 8 * g;
   int jc = c < bb ? J[c] : 0;
   jc = jc < 0 ? 0 : (jc >= n_pad ? (int)(n_pad - 1) : jc);  // J comes from k_select; keep reads in bounds
-  double v[8];
+  // all eight loads in flight together: clamped rows, masked afterwards
+  float f[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
-    const int64_t i = i0 + r;
-    v[r] = (c < bb && i < m) ? (double)R[i * n_pad + jc] : 0.0;
+    const int64_t i = i0 + r < m ? i0 + r : m - 1;
+    f[r] = R[i * n_pad + jc];
   }
+  double v[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) v[r] = (c < bb && i0 + r < m) ? (double)f[r] : 0.0;
   double s = 0.0, mv = -1.0;
   long long mi = i0;
 #pragma unroll
@@ -1428,11 +1440,16 @@ __device__ __forceinline__ double scale_solve(int* gacc, int bb, const double* _
                                               double* Gs /* LDS 4096 */, double* colbuf /* LDS 1024 */,
                                               bool want_gain = false) {
   __shared__ double s_trb[16];
-  take_gram(gacc, Gs);
   const int t = threadIdx.x;
-  for (int e = t; e < 4096; e += NT) {
-    const int r = e >> 6, c = e & 63;
-    Gs[e] = (r < bb && c < bb) ? Gs[e] * gramV[e] : ((r == c) ? 1.0 : 0.0);
+  // V^T H V issued with the U Gram's loads, all in one round
+  double gv[4096 / NT];
+#pragma unroll
+  for (int j = 0; j < 4096 / NT; ++j) gv[j] = gramV[t + NT * j];
+  take_gram(gacc, Gs);
+#pragma unroll
+  for (int j = 0; j < 4096 / NT; ++j) {
+    const int e = t + NT * j, r = e >> 6, c = e & 63;
+    Gs[e] = (r < bb && c < bb) ? Gs[e] * gv[j] : ((r == c) ? 1.0 : 0.0);
   }
   __syncthreads();
   const double tr = block_sum_d((t < bb) ? Gs[t * 64 + t] : 0.0, s_trb);
@@ -1454,14 +1471,24 @@ __device__ __forceinline__ double scale_solve(int* gacc, int bb, const double* _
     double g = 0.0;
 #pragma unroll
     for (int k = 0; k < TERN_SPLIT_MAX; ++k) g += gvec[t * TERN_SPLIT_MAX + k];
-    s_g[t] = g;
+    s_g[t] = t < bb ? g : 0.0;
+  }
+  __syncthreads();
+  // d = M^{-1} g: row t / 4, the quarter t % 4 of its columns in registers,
+  // the quarters added pairwise in a fixed order
+  double dq = 0.0;
+  {
+    const int r = t >> 2, q = t & 3;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) dq += Gs[r * 64 + 16 * q + c] * s_g[16 * q + c];
+    dq += __shfl_xor(dq, 1, 64);
+    dq += __shfl_xor(dq, 2, 64);
+    if (q == 0) colbuf[r] = (r < bb) ? dq : 0.0;
   }
   __syncthreads();
   double gain = 0.0;
   if (t < BBP) {
-    double d = 0.0;
-    if (t < bb)
-      for (int c = 0; c < bb; ++c) d += Gs[t * 64 + c] * s_g[c];
+    const double d = colbuf[t];
     dvec[t] = d;
     dF[t] = (float)d;
     if (Dout && t < bb) Dout[t] = (float)d;
@@ -1799,14 +1826,45 @@ __device__ __forceinline__ void reduce_colE(const double* __restrict__ colE_part
                             const double* __restrict__ hw, double* colE, double* out_fro2, double* out_fro2w,
                             double* shd) {
   double s = 0.0, sw = 0.0;
-  for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
-    double c = 0.0;
-#pragma unroll 8
-    for (int g = 0; g < gd; ++g) c += colE_part[(int64_t)g * n_pad + j];
-    if (j >= n) c = 0.0;
-    if (colE && j < n) colE[j] = c;
-    s += c;
-    sw += hw[j] * c;
+  // four columns per thread per pass, so that the loads of all groups for
+  // them are in flight together; each column adds its groups in order, and
+  // s, sw add the columns in increasing order per thread
+  // (loads from clamped indices, masked afterwards: a load under a branch
+  // would be waited for at the join before the next one is issued)
+  const int64_t st = blockDim.x;
+  for (int64_t jb = threadIdx.x; jb < n_pad; jb += 4 * st) {
+    double c[4] = {0.0, 0.0, 0.0, 0.0};
+    int64_t jc[4];
+    double hv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      jc[u] = jb + u * st < n_pad ? jb + u * st : jb;
+      hv[u] = hw[jc[u]];
+    }
+    for (int g0 = 0; g0 < gd; g0 += 8) {
+      double v[8][4];
+#pragma unroll
+      for (int gg = 0; gg < 8; ++gg) {
+        const int g = g0 + gg < gd ? g0 + gg : gd - 1;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[gg][u] = colE_part[(int64_t)g * n_pad + jc[u]];
+      }
+#pragma unroll
+      for (int gg = 0; gg < 8; ++gg)
+        if (g0 + gg < gd)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) c[u] += v[gg][u];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t j = jb + u * st;
+      if (j < n_pad) {
+        const double cu = j < n ? c[u] : 0.0;
+        if (colE && j < n) colE[j] = cu;
+        s += cu;
+        sw += hv[u] * cu;
+      }
+    }
   }
   s = block_sum_d(s, shd);
   sw = block_sum_d(sw, shd);
