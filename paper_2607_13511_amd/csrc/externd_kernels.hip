@@ -1826,45 +1826,14 @@ __device__ __forceinline__ void reduce_colE(const double* __restrict__ colE_part
                             const double* __restrict__ hw, double* colE, double* out_fro2, double* out_fro2w,
                             double* shd) {
   double s = 0.0, sw = 0.0;
-  // four columns per thread per pass, so that the loads of all groups for
-  // them are in flight together; each column adds its groups in order, and
-  // s, sw add the columns in increasing order per thread
-  // (loads from clamped indices, masked afterwards: a load under a branch
-  // would be waited for at the join before the next one is issued)
-  const int64_t st = blockDim.x;
-  for (int64_t jb = threadIdx.x; jb < n_pad; jb += 4 * st) {
-    double c[4] = {0.0, 0.0, 0.0, 0.0};
-    int64_t jc[4];
-    double hv[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      jc[u] = jb + u * st < n_pad ? jb + u * st : jb;
-      hv[u] = hw[jc[u]];
-    }
-    for (int g0 = 0; g0 < gd; g0 += 8) {
-      double v[8][4];
-#pragma unroll
-      for (int gg = 0; gg < 8; ++gg) {
-        const int g = g0 + gg < gd ? g0 + gg : gd - 1;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) v[gg][u] = colE_part[(int64_t)g * n_pad + jc[u]];
-      }
-#pragma unroll
-      for (int gg = 0; gg < 8; ++gg)
-        if (g0 + gg < gd)
-#pragma unroll
-          for (int u = 0; u < 4; ++u) c[u] += v[gg][u];
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int64_t j = jb + u * st;
-      if (j < n_pad) {
-        const double cu = j < n ? c[u] : 0.0;
-        if (colE && j < n) colE[j] = cu;
-        s += cu;
-        sw += hv[u] * cu;
-      }
-    }
+  for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
+    double c = 0.0;
+#pragma unroll 8
+    for (int g = 0; g < gd; ++g) c += colE_part[(int64_t)g * n_pad + j];
+    if (j >= n) c = 0.0;
+    if (colE && j < n) colE[j] = c;
+    s += c;
+    sw += hw[j] * c;
   }
   s = block_sum_d(s, shd);
   sw = block_sum_d(sw, shd);
