@@ -335,10 +335,13 @@ __device__ __forceinline__ void store_coherent(T* p, T v) {
 __device__ __forceinline__ int ginv_index(int row, int col) {
   return (((row >> 4) * 16 + (col >> 2)) << 6) + (col & 3) * 16 + (row & 15);
 }
+// The consumers run in a later launch than the producer, so plain loads
+// see the inverse, and after the first workgroup of an XCD they hit in its
+// L2 (coherent loads would go past the L2 for every workgroup).
 __device__ __forceinline__ void load_ginv(const double* ginv, double (&a)[16]) {
   const double* p = ginv + wave_id() * 1024 + lane_id();
 #pragma unroll
-  for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(p + ks * 64);
+  for (int ks = 0; ks < 16; ++ks) a[ks] = p[ks * 64];
 }
 
 // nk: pivot blocks to sweep, ceil(bb / 4) for a block of bb real components
@@ -426,8 +429,8 @@ __device__ __forceinline__ void spd_inverse64(double* A, double* pbuf, int nk, d
     for (int r = 0; r < 4; ++r)
       if (16 * w + lr + 4 * r == 16 * nt + lc) acc[nt][r] -= 2.0;
   // the inverse goes back to A (LDS, row-major), or to out (global, in the
-  // fp64 MFMA operand order of ginv_index, written through for consumers
-  // in other workgroups of the same launch)
+  // fp64 MFMA operand order of ginv_index, for the target kernel of the
+  // next launch; written through)
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
