@@ -32,10 +32,12 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   L.m_pad = round_up(m, TILE);
   L.n_pad = round_up(n, TILE);
   const int64_t nct = L.n_pad / TILE, nrt = L.m_pad / TILE;
-  // V-step: about 480 column-tile x row-group workgroups; deflation and
-  // staging: about 640.
+  // V-step: about 480 column-tile x row-group workgroups.  Deflation and
+  // staging: as many row groups as keep the whole deflation grid resident
+  // in one pass (a second, partial pass leaves its CUs moving 1.5 shares of
+  // the residual while the others idle).
   L.gv = clampi((480 + nct - 1) / nct, 1, nrt < GV_MAX ? nrt : GV_MAX);
-  L.gd = clampi((640 + nct - 1) / nct, 1, nrt < 64 ? nrt : 64);
+  L.gd = clampi(DEFLATE_SLOTS / nct, 1, nrt < 64 ? nrt : 64);
   // U-step: equal row groups of at most 32 rows, as many as fit beside the
   // side workgroups in one pass of USTEP_SLOTS resident workgroups, so
   // that every CU streams the same share of R.

@@ -24,6 +24,8 @@ constexpr int GV_MAX = 8;      // row groups of the V-step contraction
 // Workgroups of the contraction kernels resident at once: two per CU on
 // 256 CUs (LDS and register budgets of k_vstep / k_ustep).
 constexpr int USTEP_SLOTS = 512;
+// The same for the deflation kernel (240 VGPRs: two workgroups per CU).
+constexpr int DEFLATE_SLOTS = 512;
 // Threads per workgroup for all kernels except the selection kernel.
 constexpr int NT = 256;
 constexpr int NT_SELECT = 1024;
