@@ -34,7 +34,9 @@ INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, published
 # the 256 compute units: its ceiling is one CU's share of the published fp32
 # vector rate (157.3 TFLOP/s / 256).
 CU_FP32_PEAK_GFLOPS = 157.3e3 / 256
-KERNEL_SOURCES = ["paper_2607_13511_amd/csrc/externd_kernels.hip"]
+# the kernels and the launch geometry (grid sizes and workspace layout)
+KERNEL_SOURCES = ["paper_2607_13511_amd/csrc/externd_kernels.hip", "paper_2607_13511_amd/csrc/externd_api.hip",
+                  "paper_2607_13511_amd/csrc/externd_internal.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
 
 
