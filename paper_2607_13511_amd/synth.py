@@ -103,6 +103,16 @@ def down9728(weighted: bool = False) -> Workload:
     return Workload(name, A, h, 3.0, 1.0, 64, 8, (2560, 5120, 7680))
 
 
+def ragged5003() -> Workload:
+    """5003x3001 (neither side a multiple of 32), t4 std 0.02 with row scales
+    exp(N(0, 0.3^2)) and importance weights; mu=1.5 (k=4502: 70 blocks of 64
+    and a last block of 22), tau=1.0, block=64, 8 iters.
+    """
+    A = t4_rowscale(5003, 3001, 0.02, 0.3, _rng(6, 0, Q_A), _rng(6, 0, Q_ROWSCALE))
+    h = importance(3001, _rng(6, 0, Q_H))
+    return Workload("ragged5003x3001_mu1.5_tau1.0_b64_imatrix", A, h, 1.5, 1.0, 64, 8, (3001, 4502))
+
+
 BLOCK_SHAPES = (
     ("q", 2560, 4096), ("k", 2560, 1024), ("v", 2560, 1024), ("o", 4096, 2560),
     ("gate", 2560, 9728), ("up", 2560, 9728), ("down", 9728, 2560),

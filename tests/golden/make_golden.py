@@ -38,6 +38,8 @@ def cases():
     for weighted in (False, True):
         w = synth.down9728(weighted=weighted)
         yield w.name, w.A, w.h, w.mu, w.tau, w.block, w.iters
+    w = synth.ragged5003()
+    yield w.name, w.A, w.h, w.mu, w.tau, w.block, w.iters
     for idx, (mname, m, n) in enumerate(synth.BLOCK_SHAPES):
         _, A, h = synth.transformer_block(idx)
         for mu, tau in BLOCK_POINTS:

@@ -10,8 +10,9 @@ written by tests/golden/make_golden.py, which calls only oracle/):
 * the factors' zero fractions within 0.02 of the oracle's.
 Workloads: the 2048x2048 attention projection (mu=2, tau=0.7, b=32), the
 9728x2560 down projection with and without importance weights (mu=3,
-tau=1.0, b=64), and the seven matrices of the synthetic transformer block
-at three (mu, tau) points each.
+tau=1.0, b=64), a weighted 5003x3001 matrix whose sides and rank are off
+every tile grid (mu=1.5, tau=1.0, b=64), and the seven matrices of the
+synthetic transformer block at three (mu, tau) points each.
 """
 import glob
 import hashlib
@@ -42,6 +43,9 @@ def inputs(rec):
         return w.A, w.h
     if name.startswith("down9728x2560"):
         w = synth.down9728(weighted=name.endswith("_imatrix"))
+        return w.A, w.h
+    if name.startswith("ragged5003x3001"):
+        w = synth.ragged5003()
         return w.A, w.h
     if name.startswith("block_"):
         mname = name.split("_")[1]
