@@ -184,6 +184,7 @@ E2E = [
     ("t4", 300, 45, 2.0, 1.0, 5, 3, True),
     ("gauss", 300, 64, 0.5, 0.7, 1, 3, False),     # b = 1 beyond the one-launch shapes: the block kernels
     ("t4", 40, 17000, 1.0, 1.0, 8, 3, True),       # > 512 column strips: one deflation and V-step row group
+    ("t4_rowscale", 17000, 40, 1.0, 0.7, 8, 3, False),  # U-step groups of 32 rows beyond one resident pass
 ]
 
 
