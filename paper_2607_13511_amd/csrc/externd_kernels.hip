@@ -24,6 +24,7 @@
 //     and each fp32 scale d_c is split exactly into three bf16 parts;
 //     products accumulate in fp32.
 #include "externd.h"
+#include "externd_dpp.hpp"
 #include "externd_internal.hpp"
 
 #include <hip/hip_runtime.h>
@@ -690,18 +691,16 @@ __device__ __forceinline__ void tile_stats(const v4d (&x)[2], int w, int64_t i0,
   for (int r = 0; r < 4; ++r) {
     const double a0 = ia < L ? fabs(x[0][r]) : 0.0, a1 = ib < L ? fabs(x[1][r]) : 0.0;
     double s = a0 + a1;
-    // invalid indices never win the max
+    // invalid indices never win the max; the 16 lanes of a row (one
+    // component) are reduced on DPP into lane 15 of the row
     double mv = ia < L ? a0 : -1.0;
     long long mi = ia;
     argmax_merge(mv, mi, ib < L ? a1 : -1.0, ib);
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) {
-      s += __shfl_xor(s, o, 16);
-      const double mv2 = __shfl_xor(mv, o, 16);
-      const long long mi2 = __shfl_xor(mi, o, 16);
-      argmax_merge(mv, mi, mv2, mi2);
-    }
-    if (li == 0) {
+    int mi32 = (int)mi;
+    row_sum15(s);
+    row_argmax15(mv, mi32);
+    mi = mi32;
+    if (li == 15) {
       const int c = 16 * w + lk + 4 * r;
       ps[(int64_t)c * ntile + tile] = s;
       pm[(int64_t)c * ntile + tile] = mv;
@@ -1192,16 +1191,13 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 constexpr int TERN_SP = 2;  // statistics tiles per thread loaded up front
 constexpr int TERN_XS = 8;  // chunk entries per thread kept in registers
 
-// Sum (fixed butterfly and wave order) and max over the workgroup; every
-// thread receives both.
+// Sum and max over the workgroup (DPP within each wave, then the waves in
+// order); every thread receives both.  m: values >= -1.
 __device__ __forceinline__ void block_sum_max(double& s, double& m, double* sh /* >= 8 */) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    s += __shfl_xor(s, o, 64);
-    m = fmax(m, __shfl_xor(m, o, 64));
-  }
+  wave_sum63(s);
+  wave_max63(m);
   const int w = wave_id();
-  if (lane_id() == 0) {
+  if (lane_id() == 63) {
     sh[w] = s;
     sh[4 + w] = m;
   }
