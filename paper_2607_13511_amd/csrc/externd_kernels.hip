@@ -186,10 +186,12 @@ __device__ __forceinline__ void reduce_waves(long long* red, const v16i (&acc)[2
 }
 
 // Deterministic reductions: fixed shuffle tree, lane 0 holds the result.
+// Wave sum on DPP (lane 63), read back so that every lane holds it.
 __device__ __forceinline__ double wave_sum_d(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, 64);
-  return v;
+  wave_sum63(v);
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane((int)b, 63), hi = __builtin_amdgcn_readlane((int)(b >> 32), 63);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
 }
 __device__ __forceinline__ long long wave_sum_ll(long long v) {
 #pragma unroll
@@ -1920,11 +1922,14 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
         c[q] = (int)htot[255 - 4 * lane - q];
         tot += c[q];
       }
+      // inclusive scan over the wave on DPP: within rows, then across rows
       int incl = tot;
-      for (int o = 1; o < 64; o <<= 1) {
-        const int u = __shfl_up(incl, o, 64);
-        if (lane >= o) incl += u;
-      }
+      incl += __builtin_amdgcn_update_dpp(0, incl, DPP_ROW_SHR1, 0xF, 0xF, false);
+      incl += __builtin_amdgcn_update_dpp(0, incl, DPP_ROW_SHR2, 0xF, 0xF, false);
+      incl += __builtin_amdgcn_update_dpp(0, incl, DPP_ROW_SHR4, 0xF, 0xF, false);
+      incl += __builtin_amdgcn_update_dpp(0, incl, DPP_ROW_SHR8, 0xF, 0xF, false);
+      incl += __builtin_amdgcn_update_dpp(0, incl, DPP_ROW_BCAST15, 0xA, 0xF, false);
+      incl += __builtin_amdgcn_update_dpp(0, incl, DPP_ROW_BCAST31, 0xC, 0xF, false);
       const unsigned long long hit = __ballot(incl >= need);
       const int first = hit ? (__ffsll((long long)hit) - 1) : 63;
       if (lane == first) {
