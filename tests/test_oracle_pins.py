@@ -12,8 +12,6 @@ import pytest
 import oracle
 from paper_2607_13511_amd import synth
 
-scipy_special = pytest.importorskip("scipy.special")
-
 
 # --------------------------------------------------------------------------
 # T_tau, Eq. (2): hand-worked values and invariants
@@ -53,7 +51,7 @@ def test_zero_fraction_closed_form(tau):
     # P(|x| <= tau E|x|) = erf(tau / sqrt(pi)): 42.35% / 57.51% / 88.95%.
     x = np.random.default_rng(123).standard_normal(1_000_000)
     zf = 1.0 - np.count_nonzero(oracle.ternarize(x, tau)) / x.size
-    assert abs(zf - scipy_special.erf(tau / math.sqrt(math.pi))) < 3e-3
+    assert abs(zf - math.erf(tau / math.sqrt(math.pi))) < 3e-3
 
 
 def test_factor_zero_fraction_matches_paper():
