@@ -8,6 +8,16 @@ the final energies, the factor zero fractions and a SHA-256 of the input
 matrix so that a drifting generator is caught.  Run from the repository
 root:  python tests/golden/make_golden.py [name ...]
        python tests/golden/make_golden.py --refine [name ...]
+       python tests/golden/make_golden.py --sequential [name ...]
+
+``--sequential`` writes records under tests/golden/seq/ that put the greedy
+sequential ALS (Sec. 2.3, oracle.factorize_sequential) beside the block ALS
+(Sec. 2.4, oracle.factorize_block) on the same input: the energy after every
+component of the sequential run (or after every 64th at full size) and after
+every block of the block run.  They measure the block algorithm's distance
+from the sequential one (the paper reports +-0.2 pt at b = 256, Table 1
+caption) and let the b = 1 GPU run be checked against the sequential oracle
+at a size above the one-launch path.
 """
 from __future__ import annotations
 
@@ -27,9 +37,11 @@ from paper_2607_13511_amd import synth  # noqa: E402
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 
-# one (mu, tau) point per matrix of the transformer block: the diagonal of
-# the mu in {2, 2.5, 3.5} x tau in {0.7, 1.0, 2.0} sweep
-BLOCK_POINTS = ((2.0, 0.7), (2.5, 1.0), (3.5, 2.0))
+# every tau of the transformer-block sweep, run to the largest mu (3.5); the
+# checkpoints mu = 2 and 2.5 are prefixes of that curve (greedy deflation,
+# Sec. 2.1), at block multiples k = 2 min(m,n) and 2.5 min(m,n)
+BLOCK_POINTS = ((3.5, 0.7), (3.5, 1.0), (3.5, 2.0))
+BLOCK_CHECKPOINTS = (2.0, 2.5, 3.5)
 
 
 def cases():
@@ -84,6 +96,50 @@ def main_refine(names):
               flush=True)
 
 
+def seq_cases():
+    for weighted in (False, True):
+        yield synth.down_reduced(weighted=weighted), False
+    yield synth.down9728(), True
+
+
+def main_sequential(names):
+    os.makedirs(os.path.join(HERE, "seq"), exist_ok=True)
+    for w, full in seq_cases():
+        name = "seq_" + w.name
+        if names and name not in names:
+            continue
+        t0 = time.time()
+        fs = oracle.factorize_sequential(w.A, w.mu, w.tau, w.iters, h=w.h)
+        ts = time.time() - t0
+        fb = oracle.factorize_block(w.A, w.mu, w.tau, w.block, w.iters, h=w.h)
+        stride = w.block if full else 1
+        sel = np.arange(stride - 1, fs.k, stride)
+        m, n = w.A.shape
+        rec = {
+            "source": "oracle.factorize_sequential and oracle.factorize_block on synth inputs "
+                      "(tests/golden/make_golden.py --sequential)",
+            "name": name, "m": int(m), "n": int(n), "mu": w.mu, "tau": w.tau, "block": w.block,
+            "iters": w.iters, "weighted": w.h is not None, "k": int(fs.k), "block_eff": int(fb.block),
+            "a_sha256": hashlib.sha256(np.ascontiguousarray(w.A, dtype=np.float32).tobytes()).hexdigest(),
+            "seq_stride": int(stride),
+            "seq_curve": [float(fs.curve[i]) for i in sel],
+            "seq_curve_w": [float(fs.curve_w[i]) for i in sel] if fs.curve_w is not None else None,
+            "seq_E": float(fs.E), "seq_E_w": float(fs.E_w) if fs.E_w is not None else None,
+            "seq_zero_fraction_B": float(np.mean(fs.B == 0)), "seq_zero_fraction_C": float(np.mean(fs.C == 0)),
+            "seq_safeguard_would_fire": int(fs.safeguard_would_fire),
+            "seq_seconds": ts,
+            "block_curve": [float(x) for x in fb.curve],
+            "block_curve_w": [float(x) for x in fb.curve_w] if fb.curve_w is not None else None,
+            "block_E": float(fb.E), "block_E_w": float(fb.E_w) if fb.E_w is not None else None,
+            "checkpoints_k": [int(c) for c in w.checkpoints_k],
+        }
+        with open(os.path.join(HERE, "seq", name + ".json"), "w") as fh:
+            json.dump(rec, fh, indent=0)
+        gap = [float(fb.curve[c // fb.block - 1] - fs.curve[c - 1]) for c in w.checkpoints_k]
+        print(f"{name}: E_seq={fs.E:.6f} E_block={fb.E:.6f} block-seq at checkpoints {gap} "
+              f"(sequential {ts:.1f} s, total {time.time() - t0:.1f} s)", flush=True)
+
+
 def main(names):
     for name, A, h, mu, tau, block, iters in cases():
         if names and name not in names:
@@ -110,5 +166,7 @@ if __name__ == "__main__":
     args = sys.argv[1:]
     if args[:1] == ["--refine"]:
         main_refine(set(args[1:]))
+    elif args[:1] == ["--sequential"]:
+        main_sequential(set(args[1:]))
     else:
         main(set(args))

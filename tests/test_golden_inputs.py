@@ -62,3 +62,32 @@ def test_refine_record(path):
 def load_json(path):
     with open(path) as f:
         return json.load(f)
+
+
+SEQ = sorted(glob.glob(os.path.join(HERE, "golden", "seq", "*.json")))
+
+
+def test_seq_records_present():
+    assert len(SEQ) >= 2
+
+
+@pytest.mark.parametrize("path", SEQ, ids=lambda p: os.path.basename(p)[:-5])
+def test_seq_record(path):
+    """A sequential-vs-block record still describes its input; both curves
+    never decrease in the objective their run minimizes (Proposition 1 for
+    mode S; the Eq. (4) decrease d^T g >= 0 per block for mode B); and the
+    sequential run is no worse than the block run at the last checkpoint
+    (the block algorithm trades quality for batching, Sec. 2.4)."""
+    from test_gpu_sequential import inputs
+    rec = load_json(path)
+    A, h = inputs(rec)
+    assert (h is not None) == rec["weighted"]
+    assert hashlib.sha256(np.ascontiguousarray(A, dtype=np.float32).tobytes()).hexdigest() == rec["a_sha256"]
+    assert rec["k"] == oracle.rank_of(rec["m"], rec["n"], rec["mu"])
+    assert rec["block_eff"] == oracle.effective_block(rec["m"], rec["n"], rec["block"])
+    key = "_w" if rec["weighted"] else ""
+    seq, blk = np.asarray(rec["seq_curve" + key]), np.asarray(rec["block_curve" + key])
+    assert len(seq) == rec["k"] // rec["seq_stride"] and len(blk) == -(-rec["k"] // rec["block_eff"])
+    assert np.all(np.diff(seq) >= -1e-12) and np.all(np.diff(blk) >= -1e-12)
+    assert seq[-1] >= blk[-1]
+    assert rec["seq_curve"][-1] == rec["seq_E"] and rec["block_curve"][-1] == rec["block_E"]
