@@ -12,7 +12,9 @@ Workloads: the 2048x2048 attention projection (mu=2, tau=0.7, b=32), the
 9728x2560 down projection with and without importance weights (mu=3,
 tau=1.0, b=64), a weighted 5003x3001 matrix whose sides and rank are off
 every tile grid (mu=1.5, tau=1.0, b=64), and the seven matrices of the
-synthetic transformer block at three (mu, tau) points each.
+synthetic transformer block, each run to mu = 3.5 at tau = 0.7, 1.0 and 2.0
+with the sweep's checkpoints mu = 2, 2.5 and 3.5 asserted explicitly (the
+shorter runs are prefixes of these: greedy deflation, Sec. 2.1).
 """
 import glob
 import hashlib
@@ -81,6 +83,13 @@ def test_fullsize_energy(ext, path):
     if rec["weighted"]:
         np.testing.assert_allclose(res.curve_w, np.asarray(rec["curve_w"]), rtol=0, atol=1e-3)
         assert np.all(np.diff(res.curve_w) >= -1e-6)
+    if rec["name"].startswith("block_"):
+        # the transformer-block sweep's checkpoints: mu = 2, 2.5, 3.5
+        for mu_c in (2.0, 2.5, 3.5):
+            b = ext.rank(rec["m"], rec["n"], mu_c) // rec["block_eff"] - 1
+            for key in ("curve", "curve_w"):
+                e_gpu = (res.curve if key == "curve" else res.curve_w)[b]
+                assert abs(e_gpu - rec[key][b]) <= 1e-3, (mu_c, key, e_gpu, rec[key][b])
     # decode the packed factors and multiply them out on the GPU (fp64)
     torch.cuda.synchronize()
     m, n = rec["m"], rec["n"]
