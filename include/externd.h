@@ -53,7 +53,9 @@ extern "C" {
                                     launch ran out (reserved: no kernel of this version
                                     waits on another workgroup)                          */
 
-/* Largest block width the kernels handle; larger requests are clamped. */
+/* Largest effective block width the kernels handle.  A call whose
+ * effective width (externd_effective_block) exceeds it returns
+ * EXTERND_EUNSUPPORTED before any device work; nothing is clamped.       */
 #define EXTERND_MAX_BLOCK 64
 
 /* Ridge of the decorrelated targets, Eq. (3): eps = EXTERND_RIDGE_REL *
@@ -70,9 +72,10 @@ const char* externd_strerror(int status);
  * the arguments are invalid.                                             */
 int64_t externd_rank(int64_t m, int64_t n, double mu);
 
-/* Block width actually used: min(block, floor(min(m, n) / 8),
- * EXTERND_MAX_BLOCK), at least 1 (Sec. 2.4 caps b at min(m, n) / 8).
- * -1 on invalid arguments.                                               */
+/* Block width actually used: min(block, floor(min(m, n) / 8)), at least
+ * 1 (Sec. 2.4 caps b at min(m, n) / 8).  The factorizing entry points
+ * return EXTERND_EUNSUPPORTED when it exceeds EXTERND_MAX_BLOCK.  -1 on
+ * invalid arguments.                                                     */
 int32_t externd_effective_block(int64_t m, int64_t n, int32_t block);
 
 /* Device workspace, in bytes, for an m x n matrix and inner rank k:
@@ -92,7 +95,11 @@ size_t externd_workspace_bytes(int64_t m, int64_t n, int64_t k);
  *  mu         inner-rank multiplier, k = externd_rank(m, n, mu) >= 1.
  *  tau        threshold scale of T_tau, Eq. (2); finite, >= 0.
  *  block      requested block width b >= 1 (see externd_effective_block;
- *             block = 1 is the sequential algorithm of Sec. 2.3).
+ *             block = 1 is the sequential algorithm of Sec. 2.3).  An
+ *             effective width above EXTERND_MAX_BLOCK is
+ *             EXTERND_EUNSUPPORTED (the paper's default b = 256 runs only
+ *             where its cap floor(min(m, n) / 8) brings it to 64 or less,
+ *             i.e. min(m, n) < 520).
  *  iters      ALS iterations per block, >= 1; one iteration is a V-step
  *             followed by a U-step (Sec. 2.3 order).
  *  importance device fp32[n] per-column weights h (finite, >= 0, max > 0),

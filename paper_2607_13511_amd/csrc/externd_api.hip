@@ -69,12 +69,12 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(double) * BBP,                            // 17 dvec
       sizeof(float) * BBP,                             // 18 dF
       sizeof(int) * BBP,                               // 19 J
-      sizeof(unsigned) * (size_t)L.nblk_cap,           // 20 maxbits
+      sizeof(float) * (size_t)L.m_pad,                 // 20 rowb
       sizeof(double) * (size_t)L.nblk_cap,             // 21 fro2_hist
       sizeof(double) * (size_t)L.nblk_cap,             // 22 fro2w_hist
       sizeof(unsigned) * CNT_COUNT,                    // 23 counters
       sizeof(int) * FLAG_COUNT,                        // 24 flags
-      sizeof(unsigned) * (size_t)L.nblk_cap,           // 25 maxbits_w
+      sizeof(float) * (size_t)(nct * L.m_pad),         // 25 rowb_part
       (size_t)(BBP * L.m_pad),                         // 26 Umf
       (size_t)(BBP * L.n_pad),                         // 27 Vmf
       sizeof(double) * (size_t)(BBP * ntmax),          // 28 tps
@@ -84,6 +84,8 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(unsigned long long) * (size_t)L.nblk_cap, // 32 argkey
       sizeof(int) * 2 * 4096,                          // 33 gacc
       sizeof(double) * 4096 * VPREP_MAX_WG,            // 34 partw
+      sizeof(double),                                  // 35 hwmax
+      sizeof(int) * (size_t)L.n_pad,                   // 36 cshift
   };
   size_t o = 0;
   for (size_t i = 0; i < sizeof(sizes) / sizeof(sizes[0]); ++i) {
@@ -130,12 +132,12 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.dvec = (double*)(b + L.off[17]);
   w.dF = (float*)(b + L.off[18]);
   w.J = (int*)(b + L.off[19]);
-  w.maxbits = (unsigned*)(b + L.off[20]);
+  w.rowb = (float*)(b + L.off[20]);
   w.fro2_hist = (double*)(b + L.off[21]);
   w.fro2w_hist = (double*)(b + L.off[22]);
   w.counters = (unsigned*)(b + L.off[23]);
   w.flags = (int*)(b + L.off[24]);
-  w.maxbits_w = (unsigned*)(b + L.off[25]);
+  w.rowb_part = (float*)(b + L.off[25]);
   w.Umf = (int8_t*)(b + L.off[26]);
   w.Vmf = (int8_t*)(b + L.off[27]);
   w.tps = (double*)(b + L.off[28]);
@@ -145,6 +147,8 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.argkey = (unsigned long long*)(b + L.off[32]);
   w.gacc = (int*)(b + L.off[33]);
   w.partw = (double*)(b + L.off[34]);
+  w.hwmax = (double*)(b + L.off[35]);
+  w.cshift = (int*)(b + L.off[36]);
   return true;
 }
 
@@ -251,7 +255,6 @@ int32_t externd_effective_block(int64_t m, int64_t n, int32_t block) {
   if (cap < 1) cap = 1;
   int64_t b = block;
   if (b > cap) b = cap;
-  if (b > EXTERND_MAX_BLOCK) b = EXTERND_MAX_BLOCK;
   return (int32_t)b;
 }
 
@@ -338,6 +341,8 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   if (k < 1) return EXTERND_EINVAL;
   if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
   const int b_eff = externd_effective_block(m, n, block);
+  // the kernels hold at most EXTERND_MAX_BLOCK components of a block
+  if (b_eff > EXTERND_MAX_BLOCK) return EXTERND_EUNSUPPORTED;
   const int64_t nblk = (k + b_eff - 1) / b_eff;
   Ws w{};
   if (!carve(w, workspace, workspace_bytes, m, n, k)) return EXTERND_EWORKSPACE;
@@ -535,6 +540,7 @@ int externd_step_vstep(const float* R, int64_t m, int64_t n, const int8_t* U, in
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(launch_prep(w, nullptr, s));
   HIP_TRY(launch_stage(w, R, n, s));
+  HIP_TRY(launch_finish(w, 0, s));  // column energies -> the V-step's per-column exponents
   HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
   HIP_TRY(launch_vstep(w, 0, bb, tau, s));
   HIP_TRY(launch_store_factor(V_out, w.Vt, n, w.n_pad, bb, s));

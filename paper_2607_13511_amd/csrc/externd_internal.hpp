@@ -84,8 +84,13 @@ struct Ws {
   double* dvec;          // BBP: joint scales (fp64)
   float* dF;             // BBP: joint scales rounded to fp32
   int* J;                // BBP: init columns
-  unsigned* maxbits;     // nblk_cap: max|R| (fp32 bits) before each block
-  unsigned* maxbits_w;   // nblk_cap: bound on max|R_ij h~_j| (fp32 bits)
+  float* rowb;           // m_pad: upper bound on max_j |R_ij| h~_j per row (h~ = 1 unweighted): the
+                         // U-step's fixed-point exponent of row i; measured by every U-step, raised
+                         // by every deflation
+  float* rowb_part;      // (n_pad/32) x m_pad: per-column-strip row maxima from staging
+  double* hwmax;         // 1: max_j h~_j (1 + lambda with weights, 1 without)
+  int* cshift;           // n_pad: the V-step's fixed-point exponent of column j, from ||R_:j||^2
+                         // (written with the energy reduction after staging and each deflation)
   unsigned long long* argkey;  // nblk_cap: (max|R| bits << 32) | (2^32 - 1 - first row-major index), safeguard only
   double* partw;               // VPREP_MAX_WG x 64 x 64: partial weighted Grams V^T diag(h~) V
   double* fro2_hist;     // nblk_cap: ||R||^2 before each block, then after the last

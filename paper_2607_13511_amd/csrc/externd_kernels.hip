@@ -10,13 +10,17 @@
 // Arithmetic design:
 //   * The two residual contractions (P = U^T R and Q = R diag(h~) V) run on
 //     int8 MFMA (v_mfma_i32_32x32x32_i8).  Each fp32 residual entry is
-//     scaled by 2^s (|x 2^s| <= 2^30, s from max|R|, or from max|R h~| for
-//     the weighted U-step) and rounded to a 32-bit integer, which is split
-//     into four signed 8-bit digits; the
-//     ternary operand is exact in int8.  The four digit planes accumulate
-//     separately in int32 and are combined in int64, so each contraction is
-//     exact for the fixed-point residual and independent of summation
-//     order.
+//     scaled by a power of two and rounded to a 32-bit integer, which is
+//     split into four signed 8-bit digits; the ternary operand is exact in
+//     int8.  The exponent follows the index the contraction keeps: column j
+//     in the V-step (P[:, j] only involves column j of R; 2^s_j bounds
+//     ||R_:j|| / 2^30, from the fused column energies), row i in the U-step
+//     (Q[i, :] only involves row i; 2^s_i bounds max_j |R_ij h~_j| / 2^30,
+//     measured by the previous U-step and raised by each deflation), so a
+//     large entry costs resolution only in its own column or row.  The four
+//     digit planes accumulate separately in int32 and are combined in
+//     int64, so each contraction is exact for the fixed-point residual and
+//     independent of summation order.
 //   * Gram matrices of ternary factors are exact integers (int8 MFMA); the
 //     weighted Gram V^T diag(h~) V and all solves are fp64.
 //   * Targets Y, Z and the T_tau thresholds are fp64.
@@ -47,12 +51,23 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
 
-// Fixed-point exponent: max|R| < 2^e  =>  s = 30 - e, so |x 2^s| < 2^30.
-__device__ __forceinline__ int fx_shift(unsigned maxbits) {
-  float mx = __uint_as_float(maxbits);
+// Fixed-point exponent of a row from its bound b >= max_j |R_ij h~_j|:
+// b < 2^e  =>  s = 30 - e, so |x 2^s| < 2^30.
+__device__ __forceinline__ int fx_shift(float b) {
   int e = 0;
-  if (mx > 0.0f) frexpf(mx, &e);
+  if (b > 0.0f) frexpf(b, &e);
   return 30 - e;
+}
+// Fixed-point exponent of column j from its energy S = sum_i R_ij^2 (the
+// fused column energies, row-group partials added in group order): every
+// |R_ij| <= sqrt(S) (a sum of non-negative terms never rounds below its
+// largest term), and S < 2^E gives |R_ij| < 2^ceil(E/2).  Computed once per
+// residual by the kernel that reduces the energies (cshift), read by the
+// V-step contraction and its target.
+__device__ __forceinline__ int col_shift(double S) {
+  int E = 0;
+  if (S > 0.0) frexp(S, &E);
+  return 30 - ((E + 1) >> 1);
 }
 
 // x 2^s rounded to the nearest int32 (unbiased, so rounding errors do not
@@ -60,6 +75,10 @@ __device__ __forceinline__ int fx_shift(unsigned maxbits) {
 // (bytes 0..2) or the signed top digit (byte 3).
 __device__ __forceinline__ unsigned fx_biased(float x, int s) {
   return (unsigned)(int)__builtin_rintf(__builtin_amdgcn_ldexpf(x, s)) + 0x00808080u;
+}
+// The same with the power of two 2^s given as a factor (x 2^s is exact).
+__device__ __forceinline__ unsigned fx_biased_m(float x, float p2s) {
+  return (unsigned)(int)__builtin_rintf(x * p2s) + 0x00808080u;
 }
 // Weighted: x fw rounded to the nearest integer (ties to even) in one
 // step.  Adding 1.5 2^52 inside the fma rounds the exact product at unit
@@ -138,6 +157,14 @@ __device__ __forceinline__ void lds_read4_after(unsigned a0, unsigned a1, unsign
       : "=&v"(x0), "=&v"(x1), "=&v"(x2), "=&v"(x3)
       : "v"(a0), "v"(a1), "v"(a2), "v"(a3), "n"(VM)
       : "memory");
+}
+// One 4-byte LDS read after waiting until at most VM vector-memory
+// operations of this wave are outstanding (see lds_read4_after).
+template <int VM>
+__device__ __forceinline__ float lds_read1_after(unsigned a) {
+  float x;
+  asm volatile("s_waitcnt vmcnt(%1)\n\tds_read_b32 %0, %2\n\ts_waitcnt lgkmcnt(0)" : "=&v"(x) : "n"(VM), "v"(a) : "memory");
+  return x;
 }
 // Eight 16-byte LDS reads (no vector-memory wait: issue after
 // lds_read4_after on the same stage).
@@ -724,7 +751,7 @@ __device__ __forceinline__ void tile_stats(const v4d (&x)[2], int w, int64_t i0,
 // instruction reads two full 128-byte row segments.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vstep(const float* __restrict__ R, const v4i* __restrict__ Umf,
-                                              long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
+                                              long long* __restrict__ Pp, const int* __restrict__ cshift,
                                               int64_t m_pad, int64_t n_pad, int gv, int bb, int* gacc,
                                               unsigned* gcounter, double* ginvU, int nside) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
@@ -747,7 +774,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const int ks0 = (int)((long long)g * nks / gv), ks1 = (int)((long long)(g + 1) * nks / gv);
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
-  const int s = fx_shift(*maxbits);
+  // lane (j, h) converts column ct * 32 + j only: its own exponent
+  const int s = cshift[(int64_t)ct * TILE + l32];
   v16i acc[2][4];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
@@ -787,7 +815,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
       acc[1][p] = mfma_i8(a1, P[p], acc[1][p]);
     }
   }
-  // out[t][M = component][N = column]: this row group's partial P tile
+  // out[t][M = component][N = column]: this row group's partial P tile, at
+  // the column's fixed-point scale
   long long* Pg = Pp + ((int64_t)g * BBP) * n_pad + (int64_t)ct * TILE;
   reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { Pg[(int64_t)(32 * t + M) * n_pad + N] = v; });
 }
@@ -813,20 +842,21 @@ __device__ __forceinline__ void vtarget_sum16(const long long* __restrict__ Pp, 
 #pragma unroll
     for (int g = 0; g < GV; ++g) acc += v[g][q];
     const int e = threadIdx.x + q * NT;
-    Ps[(e >> 4) * 17 + (e & 15)] = ldexp((double)acc, -s);
+    Ps[(e >> 4) * 17 + (e & 15)] = ldexp((double)acc, -s);  // column j0 + (e & 15) = j0 + (tid & 15)
   }
 }
 
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vtarget(const long long* __restrict__ Pp, const unsigned* __restrict__ maxbits,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vtarget(const long long* __restrict__ Pp, const int* __restrict__ cshift,
                                                 int64_t n_pad, int gv, const double* __restrict__ ginvU,
                                                 double* __restrict__ Y, int64_t n, double* ps, double* pm, int* pi) {
   __shared__ double Ps[64 * 17];
   const int tile = blockIdx.x;
   const int ntile = (int)(n_pad / 16);
   const int64_t j0 = (int64_t)tile * 16;
-  const int s = fx_shift(*maxbits);
   const int lane = lane_id(), w = wave_id();
   const int li = lane & 15, lk = lane >> 4;
+  // the contraction's exponent of the one column this thread sums
+  const int s = cshift[j0 + (threadIdx.x & 15)];
   double a[16];
   load_ginv(ginvU, a);
   static_assert(GV_MAX == 8, "one case per group count");
@@ -1019,7 +1049,7 @@ constexpr int USTEP_SMEM_LL = (4 * NST_U * USTAGE_B + 7) / 8 > 8192 ? (4 * NST_U
 template <bool WEIGHTED>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_ustep(const float* __restrict__ R, const v4i* __restrict__ Vmf,
                                               const int8_t* __restrict__ Vr, const double* __restrict__ hw,
-                                              double* __restrict__ Q, const unsigned* __restrict__ maxbits,
+                                              double* __restrict__ Q, float* __restrict__ rowb,
                                               int64_t m_pad, int64_t n_pad, int bb, int* gacc, unsigned* counter,
                                               double* ginvV, double* gramV, int nside, int rows) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
@@ -1049,7 +1079,16 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const int valid = (int)(m_pad - i0 < rows ? m_pad - i0 : rows);  // >= 1: ntile = ceil(m_pad / rows)
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
-  const int s = fx_shift(*maxbits);
+  // lane (i, h) converts row i0 + i only: its own exponent, from the row's
+  // bound (rows past `valid` read the last valid row's; their results are
+  // discarded)
+  __shared__ int s_row[TILE];
+  __shared__ int s_rmax[4][64];
+
+  // the row's largest |x h~_j| seen by this lane: fp32 |x| unweighted, the
+  // extreme biased fixed-point words weighted (|x h~_j 2^s| <= |q| + 1/2)
+  float rmax = 0.0f;
+  int ymin = 0x00808080, ymax = 0x00808080;  // q = 0: also right for a wave without K steps
   v16i acc[2][4];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
@@ -1084,9 +1123,22 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     bn[st][0] = Vmf[(int64_t)kk * 128 + lane];
     bn[st][1] = Vmf[(int64_t)kk * 128 + 64 + lane];
   };
+  // The rows' bounds go to LDS with a direct load issued before the first
+  // stages and are read back behind an explicit wait: a register-destined
+  // load here makes the compiler drain every stage of the stream loop.
+  // Lane l of each wave stages the bound of row min(l % 32, valid - 1).
+  __shared__ float s_rbw[4][64];
+  __builtin_amdgcn_global_load_lds(rowb + i0 + (l32 < valid ? l32 : valid - 1), (lds_void*)&s_rbw[wave][0], 4, 0, 0);
 #pragma unroll
   for (int d = 0; d < NST_U - 1; ++d)
     if (wave + 4 * d < nks) issue(wave + 4 * d, d);
+  // with both first stages issued (nks >= 8) at least 2 x 3 loads follow
+  // the bound's (one direct residual load and two factor loads per stage)
+  const unsigned rba = lds_addr(&s_rbw[wave][lane]);
+  const float rbound = nks >= 4 * (NST_U - 1) ? lds_read1_after<2 * 3>(rba) : lds_read1_after<0>(rba);
+  const int s = fx_shift(rbound);
+  const float p2s = __builtin_amdgcn_ldexpf(1.0f, s);  // x 2^s = x * p2s exactly
+  const double p2sd = (double)p2s;
   // operand read: row l32, logical chunks 4h .. 4h+3
   const unsigned sw = (unsigned)(l32 & 7);
   const unsigned o0 = l32 * 128 + ((4 * h + 0) ^ sw) * 16, o1 = l32 * 128 + ((4 * h + 1) ^ sw) * 16;
@@ -1111,12 +1163,19 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 #pragma unroll
           for (int q = 0; q < 4; ++q)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) y[4 * q + e] = fx_biased_w(x[q][e], ldexp(wv[(4 * q + e) >> 1][e & 1], s));
+            for (int e = 0; e < 4; ++e) {
+              y[4 * q + e] = fx_biased_w(x[q][e], wv[(4 * q + e) >> 1][e & 1] * p2sd);
+              ymin = min(ymin, (int)y[4 * q + e]);
+              ymax = max(ymax, (int)y[4 * q + e]);
+            }
         } else {
 #pragma unroll
           for (int q = 0; q < 4; ++q)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) y[4 * q + e] = fx_biased(x[q][e], s);
+            for (int e = 0; e < 4; ++e) {
+              y[4 * q + e] = fx_biased_m(x[q][e], p2s);
+              rmax = fmaxf(rmax, fabsf(x[q][e]));
+            }
         }
         v4i P[4];
         make_planes(y, P);
@@ -1128,13 +1187,30 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
       }
     }
   }
+  // the row's measured bound replaces the one it was converted with (R does
+  // not change until the next deflation, which raises it again)
+  if (threadIdx.x < TILE) s_row[threadIdx.x] = s;
+  if (WEIGHTED) {
+    constexpr int BIAS = 0x00808080;
+    s_rmax[wave][lane] = max(ymax - BIAS, BIAS - ymin);  // max |q| over this lane's words
+  } else {
+    s_rmax[wave][lane] = __float_as_int(rmax);            // non-negative floats order like ints
+  }
   // every direct load has landed before the staging area is reused
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  if (threadIdx.x < valid) {
+    const int i = threadIdx.x;
+    int r = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r = max(r, max(s_rmax[q][i], s_rmax[q][i + 32]));
+    rowb[i0 + i] = WEIGHTED ? __int2float_ru(r + 1) * __builtin_amdgcn_ldexpf(1.0f, -s_row[i]) : __int_as_float(r);
+  }
   // out[t][M = row][N = component] -> Q[32 t + N][row], via a transposed
   // LDS tile for coalesced stores
   double* tq = (double*)smem;
-  reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { tq[(32 * t + N) * 32 + M] = ldexp((double)v, -s); });
+  reduce_waves(smem, acc,
+               [&](int t, int M, int N, long long v) { tq[(32 * t + N) * 32 + M] = ldexp((double)v, -s_row[M]); });
   __syncthreads();
   for (int e = threadIdx.x; e < 2048; e += NT)
     if ((e & 31) < valid) Q[(int64_t)(e >> 5) * m_pad + i0 + (e & 31)] = tq[e];
@@ -1543,13 +1619,11 @@ __device__ __forceinline__ short tern_bf16(int8_t t, unsigned short mag) {
 template <bool TRACK>
 __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s* __restrict__ Ub,
                                                 const int8_t* __restrict__ Vr, const float* __restrict__ dF,
-                                                double* __restrict__ colE_part, unsigned* __restrict__ maxbits_next,
-                                                unsigned* __restrict__ maxbits_w_next, const double* __restrict__ hw,
+                                                double* __restrict__ colE_part, float* __restrict__ rowb,
+                                                const int8_t* __restrict__ Ur, const double* __restrict__ hwmax,
                                                 int64_t m_pad, int64_t n_pad, int gd,
                                                 unsigned long long* __restrict__ argkey_next, int64_t n) {
   __shared__ double colsum[4][32];
-  __shared__ float wmax[4];
-  __shared__ float wmaxw[4];
   __shared__ float amax[4];
   __shared__ unsigned aidx[4];
   const int nct = (int)(n_pad / TILE);
@@ -1559,6 +1633,22 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
   const int64_t col = (int64_t)ct * TILE + l32;
+  // Row bounds of the U-step's fixed-point exponents: |R'_ij h~_j| <=
+  // (|R_ij| + sum_c |U_ic d_c| |V_jc|) h~_j <= rowb_i + max h~ sum_c |U_ic| |d_c|,
+  // inflated for the fp32 rounding of the update (< 2^-12 relative even for
+  // the worst-case accumulation of the 3 x 64 MFMA terms).  The nct
+  // workgroups of a row group share its rows, each row has one owner; the
+  // first row of a thread is loaded here (clamped index, masked use) with
+  // the B fragments, so the update adds no round of latency.
+  const int64_t rg0 = (int64_t)rt0 * TILE, rg1 = (int64_t)rt1 * TILE;
+  const int64_t rchunk = (rg1 - rg0 + nct - 1) / nct;
+  const int64_t rb0 = rg0 + (int64_t)ct * rchunk, rb1 = rb0 + rchunk < rg1 ? rb0 + rchunk : rg1;
+  const int64_t ib = rb0 + threadIdx.x;
+  const int64_t ibc = ib < m_pad ? ib : m_pad - 1;
+  int4 ur4[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) ur4[q] = ((const int4*)(Ur + ibc * BBP))[q];
+  const float rbv = rowb[ibc];
   // B fragments: lane (h, col) holds components 16 ks + 8 h + e.
   v8s Bf[3][4];
   {
@@ -1581,8 +1671,27 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
       }
     }
   }
+  {
+    const double hmax = *hwmax;
+    auto row_update = [&](int64_t i, const int4 (&u4)[4], float rb) {
+      double sd = 0.0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int8_t* ub = (const int8_t*)&u4[q];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sd += (ub[e] != 0 ? 1.0 : 0.0) * fabs((double)dF[16 * q + e]);
+      }
+      rowb[i] = __double2float_ru(((double)rb + hmax * sd) * (1.0 + 0x1p-12));
+    };
+    if (ib < rb1) row_update(ib, ur4, rbv);
+    for (int64_t i = ib + NT; i < rb1; i += NT) {  // more than NT rows per workgroup: very tall matrices
+      int4 u4[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) u4[q] = ((const int4*)(Ur + i * BBP))[q];
+      row_update(i, u4, rowb[i]);
+    }
+  }
   double csum = 0.0;
-  float vmax = 0.0f;
   // TRACK: this lane's first (smallest row) largest |R|; zero entries
   // (including the padding) never replace the start value
   float tmax = 0.0f;
@@ -1624,7 +1733,6 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
       const float v = x[r] - acc[r];
       R[(i0 + row) * n_pad + col] = v;
       csum += (double)v * (double)v;
-      vmax = fmaxf(vmax, fabsf(v));
       if (TRACK && fabsf(v) > tmax) {
         tmax = fabsf(v);
         tidx = (unsigned)((i0 + row) * n + col);
@@ -1633,20 +1741,11 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
   }
   // combine the two half-waves (same column), then the 4 waves in order
   csum += __shfl_down(csum, 32, 64);
-  float vmaxw = weighted_abs_bound(vmax, hw[col]);
-  for (int o = 32; o > 0; o >>= 1) {
-    vmax = fmaxf(vmax, __shfl_down(vmax, o, 64));
-    vmaxw = fmaxf(vmaxw, __shfl_down(vmaxw, o, 64));
-  }
   if (TRACK) wave_argmax(tmax, tidx);
   if (h == 0) colsum[wave][l32] = csum;
-  if (lane == 0) {
-    wmax[wave] = vmax;
-    wmaxw[wave] = vmaxw;
-    if (TRACK) {
-      amax[wave] = tmax;
-      aidx[wave] = tidx;
-    }
+  if (TRACK && lane == 0) {
+    amax[wave] = tmax;
+    aidx[wave] = tidx;
   }
   __syncthreads();
   if (threadIdx.x < 32) {
@@ -1654,10 +1753,6 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
     colE_part[(int64_t)g * n_pad + (int64_t)ct * TILE + threadIdx.x] = s;
   }
   if (threadIdx.x == 0) {
-    const float mx = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
-    const float mxw = fmaxf(fmaxf(wmaxw[0], wmaxw[1]), fmaxf(wmaxw[2], wmaxw[3]));
-    atomicMax(maxbits_next, __float_as_uint(mx));
-    atomicMax(maxbits_w_next, __float_as_uint(mxw));
     if (TRACK) {
       unsigned long long key = 0ull;
       for (int q = 0; q < 4; ++q) {
@@ -1676,12 +1771,10 @@ __global__ __launch_bounds__(NT) void k_deflate(float* __restrict__ R, const v8s
 template <bool TRACK>
 __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64_t lda, int64_t m, int64_t n,
                                               float* __restrict__ R, double* __restrict__ colE_part,
-                                              unsigned* __restrict__ maxbits0, unsigned* __restrict__ maxbits_w0,
-                                              const double* __restrict__ hw, int* flags, int64_t m_pad,
-                                              int64_t n_pad, int gd, unsigned long long* __restrict__ argkey0) {
+                                              float* __restrict__ rowb_part, const double* __restrict__ hw,
+                                              int* flags, int64_t m_pad, int64_t n_pad, int gd,
+                                              unsigned long long* __restrict__ argkey0) {
   __shared__ double colsum[8][32];
-  __shared__ float smax[NT / 64];
-  __shared__ float smaxw[NT / 64];
   __shared__ float amax[NT / 64];
   __shared__ unsigned aidx[NT / 64];
   const int nct = (int)(n_pad / TILE);
@@ -1690,7 +1783,6 @@ __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64
   const int cl = threadIdx.x & 31, rl = threadIdx.x >> 5;
   const int64_t j = (int64_t)ct * TILE + cl;
   double cs = 0.0;
-  float vmax = 0.0f;
   float tmax = 0.0f;            // TRACK: first (smallest row) largest |A| of this thread
   unsigned tidx = 0xFFFFFFFFu;
   int bad = 0;
@@ -1704,26 +1796,22 @@ __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64
     }
     R[i * n_pad + j] = v;
     cs += (double)v * (double)v;
-    vmax = fmaxf(vmax, fabsf(v));
     if (TRACK && fabsf(v) > tmax) {
       tmax = fabsf(v);
       tidx = (unsigned)(i * n + j);
     }
+    // this strip's share of the row bound max_j |R_ij| h~_j: the 32 lanes
+    // of row i (a half-wave) reduced to lane cl = 0
+    float b = weighted_abs_bound(v, hwj);
+#pragma unroll
+    for (int o = 16; o > 0; o >>= 1) b = fmaxf(b, __shfl_xor(b, o, 32));
+    if (cl == 0) rowb_part[(int64_t)ct * m_pad + i] = b;
   }
   colsum[rl][cl] = cs;
-  float vmaxw = weighted_abs_bound(vmax, hwj);
-  for (int o = 32; o > 0; o >>= 1) {
-    vmax = fmaxf(vmax, __shfl_down(vmax, o, 64));
-    vmaxw = fmaxf(vmaxw, __shfl_down(vmaxw, o, 64));
-  }
   if (TRACK) wave_argmax(tmax, tidx);
-  if (lane_id() == 0) {
-    smax[wave_id()] = vmax;
-    smaxw[wave_id()] = vmaxw;
-    if (TRACK) {
-      amax[wave_id()] = tmax;
-      aidx[wave_id()] = tidx;
-    }
+  if (TRACK && lane_id() == 0) {
+    amax[wave_id()] = tmax;
+    aidx[wave_id()] = tidx;
   }
   if (bad) flags[FLAG_NONFINITE] = 1;
   __syncthreads();
@@ -1733,13 +1821,6 @@ __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64
     colE_part[(int64_t)g * n_pad + j] = s;
   }
   if (threadIdx.x == 0) {
-    float mx = 0.0f, mxw = 0.0f;
-    for (int w = 0; w < NT / 64; ++w) {
-      mx = fmaxf(mx, smax[w]);
-      mxw = fmaxf(mxw, smaxw[w]);
-    }
-    atomicMax(maxbits0, __float_as_uint(mx));
-    atomicMax(maxbits_w0, __float_as_uint(mxw));
     if (TRACK) {
       unsigned long long key = 0ull;
       for (int w = 0; w < NT / 64; ++w) {
@@ -1749,6 +1830,17 @@ __global__ __launch_bounds__(NT) void k_stage(const float* __restrict__ A, int64
       atomicMax(argkey0, key);
     }
   }
+}
+
+// Row bounds after staging: rowb_i = max over the column strips' partials.
+// grid: ceil(m_pad / NT).
+__global__ __launch_bounds__(NT) void k_rowb_init(const float* __restrict__ rowb_part, int nct, int64_t m_pad,
+                                                  float* __restrict__ rowb) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i >= m_pad) return;
+  float b = 0.0f;
+  for (int c = 0; c < nct; ++c) b = fmaxf(b, rowb_part[(int64_t)c * m_pad + i]);
+  rowb[i] = b;
 }
 
 // R (padded) -> A (m x n, row-major)
@@ -1765,15 +1857,13 @@ __global__ __launch_bounds__(NT) void k_unstage(const float* __restrict__ R, flo
 // ones when no weights), zero padding; clear counters, flags and the
 // per-block arrays.
 __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_t n, int64_t n_pad,
-                                             double* __restrict__ hw, unsigned* maxbits, unsigned* maxbits_w,
+                                             double* __restrict__ hw, double* __restrict__ hwmax,
                                              double* fro2_hist, double* fro2w_hist, int nblk_cap,
                                              unsigned* counters, int* flags, int* gacc, double lam,
                                              unsigned long long* argkey) {
   __shared__ float smax[NT / 64];
   __shared__ int sbad[NT / 64];
   for (int e = threadIdx.x; e < nblk_cap; e += NT) {
-    maxbits[e] = 0u;
-    maxbits_w[e] = 0u;
     fro2_hist[e] = 0.0;
     fro2w_hist[e] = 0.0;
     argkey[e] = 0ull;
@@ -1783,6 +1873,7 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
   if (threadIdx.x < FLAG_COUNT) flags[threadIdx.x] = 0;
   if (!h) {
     for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? 1.0 : 0.0;
+    if (threadIdx.x == 0) *hwmax = 1.0;
     return;
   }
   float mx = 0.0f;
@@ -1809,12 +1900,17 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
   }
   if (!(gmx > 0.0f)) gbad = 1;
   if (gbad) {
-    if (threadIdx.x == 0) flags[FLAG_BADWEIGHT] = 1;
+    if (threadIdx.x == 0) {
+      flags[FLAG_BADWEIGHT] = 1;
+      *hwmax = 1.0;
+    }
     for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? 1.0 : 0.0;
     return;
   }
   const double dm = (double)gmx;
   for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? (double)h[j] / dm + lam : 0.0;
+  // the largest weight is exactly max(h) / max(h) + lam
+  if (threadIdx.x == 0) *hwmax = 1.0 + lam;
 }
 
 // ---------------------------------------------------------------------------
@@ -1825,7 +1921,7 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void reduce_colE(const double* __restrict__ colE_part, int gd, int64_t n, int64_t n_pad,
                             const double* __restrict__ hw, double* colE, double* out_fro2, double* out_fro2w,
-                            double* shd) {
+                            double* shd, int* cshift) {
   double s = 0.0, sw = 0.0;
   for (int64_t j = threadIdx.x; j < n_pad; j += blockDim.x) {
     double c = 0.0;
@@ -1833,6 +1929,7 @@ __device__ __forceinline__ void reduce_colE(const double* __restrict__ colE_part
     for (int g = 0; g < gd; ++g) c += colE_part[(int64_t)g * n_pad + j];
     if (j >= n) c = 0.0;
     if (colE && j < n) colE[j] = c;
+    cshift[j] = col_shift(c);
     s += c;
     sw += hw[j] * c;
   }
@@ -1849,7 +1946,8 @@ constexpr int SELECT_CACHE = 8;  // keys per thread kept in registers (n <= SELE
 __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__ colE_part, int gd, int64_t n,
                                                       int64_t n_pad, const double* __restrict__ hw,
                                                       double* keys /* n_pad scratch */, double* fro2_out,
-                                                      double* fro2w_out, int bb, int* __restrict__ J) {
+                                                      double* fro2w_out, int bb, int* __restrict__ J,
+                                                      int* __restrict__ cshift) {
   __shared__ double shd[16];
   __shared__ unsigned hist[NT_SELECT / 64][256];  // one histogram per wave
   __shared__ unsigned htot[256];
@@ -1863,7 +1961,7 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
     cand_key[threadIdx.x] = 0ull;
     cand_idx[threadIdx.x] = 0;
   }
-  reduce_colE(colE_part, gd, n, n_pad, hw, keys, fro2_out, fro2w_out, shd);
+  reduce_colE(colE_part, gd, n, n_pad, hw, keys, fro2_out, fro2w_out, shd, cshift);
   __syncthreads();
   // key_j = h~_j ||R_:j||^2 as a 64-bit pattern (non-negative doubles order
   // like their bit patterns); the first SELECT_CACHE keys of each thread
@@ -2046,9 +2144,10 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
 // ||R||^2 after the last block (1 WG).
 __global__ __launch_bounds__(NT_SELECT) void k_finish(const double* __restrict__ colE_part, int gd, int64_t n,
                                                       int64_t n_pad, const double* __restrict__ hw,
-                                                      double* colE_out, double* fro2_out, double* fro2w_out) {
+                                                      double* colE_out, double* fro2_out, double* fro2w_out,
+                                                      int* __restrict__ cshift) {
   __shared__ double shd[16];
-  reduce_colE(colE_part, gd, n, n_pad, hw, colE_out, fro2_out, fro2w_out, shd);
+  reduce_colE(colE_part, gd, n, n_pad, hw, colE_out, fro2_out, fro2w_out, shd, cshift);
 }
 
 // ---------------------------------------------------------------------------
@@ -2193,16 +2292,9 @@ __global__ __launch_bounds__(NT) void k_revisit_load(const uint8_t* __restrict__
                                                      int8_t* __restrict__ Ut, int8_t* __restrict__ Ur,
                                                      unsigned short* __restrict__ Ub, int8_t* __restrict__ Umf,
                                                      int8_t* __restrict__ Vt, int8_t* __restrict__ Vr,
-                                                     int8_t* __restrict__ Vmf, float* __restrict__ dF,
-                                                     unsigned* maxbits, unsigned* maxbits_w, int slot1, int slot2) {
+                                                     int8_t* __restrict__ Vmf, float* __restrict__ dF) {
   if (blockIdx.x == 0) {
     if (threadIdx.x < BBP) dF[threadIdx.x] = (int)threadIdx.x < bb ? -D[c0 + threadIdx.x] : 0.0f;
-    if (threadIdx.x == 0) {
-      maxbits[slot1] = 0u;
-      maxbits[slot2] = 0u;
-      maxbits_w[slot1] = 0u;
-      maxbits_w[slot2] = 0u;
-    }
     return;
   }
   const int nut = (int)(m_pad / TILE);
@@ -2415,7 +2507,7 @@ static inline unsigned grid_for(int64_t total) {
 }
 
 hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s, double lam) {
-  hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.maxbits, w.maxbits_w, w.fro2_hist,
+  hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.hwmax, w.fro2_hist,
                      w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc, lam, w.argkey);
   return hipGetLastError();
 }
@@ -2423,11 +2515,15 @@ hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s, double lam) {
 hipError_t launch_stage(const Ws& w, const float* A, int64_t lda, hipStream_t s, bool track) {
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
   if (track)
-    hipLaunchKernelGGL(k_stage<true>, dim3(grid), dim3(NT), 0, s, A, lda, w.m, w.n, w.R, w.colE_part, w.maxbits,
-                       w.maxbits_w, w.hw, w.flags, w.m_pad, w.n_pad, w.gd, w.argkey);
+    hipLaunchKernelGGL(k_stage<true>, dim3(grid), dim3(NT), 0, s, A, lda, w.m, w.n, w.R, w.colE_part, w.rowb_part,
+                       (const double*)w.hw, w.flags, w.m_pad, w.n_pad, w.gd, w.argkey);
   else
-    hipLaunchKernelGGL(k_stage<false>, dim3(grid), dim3(NT), 0, s, A, lda, w.m, w.n, w.R, w.colE_part, w.maxbits,
-                       w.maxbits_w, w.hw, w.flags, w.m_pad, w.n_pad, w.gd, (unsigned long long*)nullptr);
+    hipLaunchKernelGGL(k_stage<false>, dim3(grid), dim3(NT), 0, s, A, lda, w.m, w.n, w.R, w.colE_part, w.rowb_part,
+                       (const double*)w.hw, w.flags, w.m_pad, w.n_pad, w.gd, (unsigned long long*)nullptr);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_rowb_init, dim3((unsigned)((w.m_pad + NT - 1) / NT)), dim3(NT), 0, s,
+                     (const float*)w.rowb_part, (int)(w.n_pad / TILE), w.m_pad, w.rowb);
   return hipGetLastError();
 }
 
@@ -2438,19 +2534,19 @@ hipError_t launch_unstage(const Ws& w, float* A, hipStream_t s) {
 
 hipError_t launch_select(const Ws& w, int blk, int bb, hipStream_t s) {
   hipLaunchKernelGGL(k_select, dim3(1), dim3(NT_SELECT), 0, s, w.colE_part, w.gd, w.n, w.n_pad, w.hw, w.Y,
-                     w.fro2_hist + blk, w.fro2w_hist + blk, bb, w.J);
+                     w.fro2_hist + blk, w.fro2w_hist + blk, bb, w.J, w.cshift);
   return hipGetLastError();
 }
 
 hipError_t launch_finish(const Ws& w, int blk, hipStream_t s) {
   hipLaunchKernelGGL(k_finish, dim3(1), dim3(NT_SELECT), 0, s, w.colE_part, w.gd, w.n, w.n_pad, w.hw,
-                     (double*)nullptr, w.fro2_hist + blk, w.fro2w_hist + blk);
+                     (double*)nullptr, w.fro2_hist + blk, w.fro2w_hist + blk, w.cshift);
   return hipGetLastError();
 }
 
 hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2, hipStream_t s) {
   hipLaunchKernelGGL(k_finish, dim3(1), dim3(NT_SELECT), 0, s, w.colE_part, w.gd, w.n, w.n_pad, w.hw, colnorm2,
-                     fro2 ? fro2 : (w.fro2_hist + blk), w.fro2w_hist + blk);
+                     fro2 ? fro2 : (w.fro2_hist + blk), w.fro2w_hist + blk, w.cshift);
   return hipGetLastError();
 }
 
@@ -2466,12 +2562,13 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
 
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
   const unsigned grid = (unsigned)(NSIDE_GRAM + (w.n_pad / TILE) * w.gv);
-  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, w.maxbits + blk, w.m_pad,
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, (const int*)w.cshift, w.m_pad,
                                    w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VTARGET, k_vtarget, dim3((unsigned)(w.n_pad / 16)), dim3(NT), 0, s,
-                       (const long long*)w.Pp, w.maxbits + blk, w.n_pad, w.gv, w.ginvU, w.Y, w.n, w.tps, w.tpm, w.tpi);
+                       (const long long*)w.Pp, (const int*)w.cshift, w.n_pad, w.gv, w.ginvU, w.Y, w.n, w.tps, w.tpm,
+                       w.tpi);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, (const double*)w.Y, w.n,
@@ -2504,11 +2601,11 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
     e = launch_gram_w(w, s);
     if (e != hipSuccess) return e;
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
-                                     w.maxbits_w + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096,
+                                     w.rowb, w.m_pad, w.n_pad, bb, w.gacc + 4096,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows);
   } else {
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
-                                     w.maxbits + blk, w.m_pad, w.n_pad, bb, w.gacc + 4096,
+                                     w.rowb, w.m_pad, w.n_pad, bb, w.gacc + 4096,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows);
   }
   e = hipGetLastError();
@@ -2547,7 +2644,7 @@ hipError_t launch_revisit_load(const Ws& w, const uint8_t* Bp, const uint8_t* Cp
                                int64_t k, int slot1, int slot2, hipStream_t s) {
   const unsigned grid = (unsigned)(1 + w.m_pad / TILE + w.n_pad / TILE);
   hipLaunchKernelGGL(k_revisit_load, dim3(grid), dim3(NT), 0, s, Bp, Cp, D, c0, bb, k, w.m, w.m_pad, w.n, w.n_pad,
-                     w.Ut, w.Ur, w.Ub, w.Umf, w.Vt, w.Vr, w.Vmf, w.dF, w.maxbits, w.maxbits_w, slot1, slot2);
+                     w.Ut, w.Ur, w.Ub, w.Umf, w.Vt, w.Vr, w.Vmf, w.dF);
   return hipGetLastError();
 }
 hipError_t launch_revisit_decide(const Ws& w, int bb, float* D_block, bool weighted, int slot_prev, int slot_added,
@@ -2575,11 +2672,11 @@ hipError_t launch_deflate_slot(const Ws& w, int out_slot, hipStream_t s, Timer* 
   const unsigned grid = (unsigned)((w.n_pad / TILE) * w.gd);
   if (track)
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_DEFLATE, k_deflate<true>, dim3(grid), dim3(NT), 0, s, w.R, (const v8s*)w.Ub,
-                         w.Vr, w.dF, w.colE_part, w.maxbits + out_slot, w.maxbits_w + out_slot, w.hw, w.m_pad, w.n_pad,
+                         w.Vr, w.dF, w.colE_part, w.rowb, (const int8_t*)w.Ur, (const double*)w.hwmax, w.m_pad, w.n_pad,
                          w.gd, w.argkey + out_slot, w.n);
   else
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_DEFLATE, k_deflate<false>, dim3(grid), dim3(NT), 0, s, w.R,
-                         (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part, w.maxbits + out_slot, w.maxbits_w + out_slot, w.hw,
+                         (const v8s*)w.Ub, w.Vr, w.dF, w.colE_part, w.rowb, (const int8_t*)w.Ur, (const double*)w.hwmax,
                          w.m_pad, w.n_pad, w.gd, (unsigned long long*)nullptr, w.n);
   return hipGetLastError();
 }

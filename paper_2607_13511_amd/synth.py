@@ -113,6 +113,17 @@ def ragged5003() -> Workload:
     return Workload("ragged5003x3001_mu1.5_tau1.0_b64_imatrix", A, h, 1.5, 1.0, 64, 8, (3001, 4502))
 
 
+def down_reduced(weighted: bool = False, m: int = 2432, n: int = 640) -> Workload:
+    """The 9728x2560 down-projection recipe (t4 std 0.015, row scales
+    exp(N(0, 0.3^2)), optional lognormal(0,1) weights with 1% of columns x50)
+    at a quarter of each side, 2432x640; mu=3 (k=1920), tau=1.0, block=64,
+    8 iters.  Small enough for the sequential oracle to run in minutes."""
+    A = t4_rowscale(m, n, 0.015, 0.3, _rng(7, 0, Q_A), _rng(7, 0, Q_ROWSCALE))
+    h = importance(n, _rng(7, 0, Q_H)) if weighted else None
+    name = f"down{m}x{n}_mu3_tau1.0" + ("_imatrix" if weighted else "")
+    return Workload(name, A, h, 3.0, 1.0, 64, 8, (n, 2 * n, 3 * n))
+
+
 BLOCK_SHAPES = (
     ("q", 2560, 4096), ("k", 2560, 1024), ("v", 2560, 1024), ("o", 4096, 2560),
     ("gate", 2560, 9728), ("up", 2560, 9728), ("down", 9728, 2560),
@@ -140,6 +151,8 @@ def small(kind: str, m: int, n: int, seed: int, std: float = 0.02) -> np.ndarray
         return t4_rowscale(m, n, std, 0.3, rng, np.random.default_rng(np.random.SeedSequence([3, seed, m, n])))
     if kind == "spiky":
         return spiky(m, n, seed)
+    if kind == "t4_outlier1e4":
+        return outlier(t4(m, n, std, rng), seed, 1e4)
     raise ValueError(kind)
 
 
@@ -152,6 +165,16 @@ def spiky(m: int, n: int, seed: int, spikes: int = 3, std: float = 0.05) -> np.n
     for _ in range(spikes):
         A[rng.integers(m), rng.integers(n)] = rng.choice([-1.0, 1.0]) * rng.uniform(1.0, 3.0)
     return A.astype(np.float32)
+
+
+def outlier(A: np.ndarray, seed: int, boost: float) -> np.ndarray:
+    """A copy of A with one entry, at a seeded position and sign, set to
+    boost * max|A| (a residual whose range is dominated by a single entry)."""
+    rng = np.random.default_rng(np.random.SeedSequence([7, seed, A.shape[0], A.shape[1]]))
+    B = np.array(A, dtype=np.float32, copy=True)
+    i, j = int(rng.integers(A.shape[0])), int(rng.integers(A.shape[1]))
+    B[i, j] = np.float32(rng.choice([-1.0, 1.0]) * boost * float(np.max(np.abs(A))))
+    return B
 
 
 def small_importance(n: int, seed: int) -> np.ndarray:

@@ -33,9 +33,11 @@ def test_rank_block_and_workspace_rules():
     for m, n, mu in [(256, 256, 2.0), (2048, 2048, 2.0), (9728, 2560, 3.0), (2560, 1024, 2.5), (10, 10, 0.25),
                      (37, 11, 1.3)]:
         assert binding.rank(m, n, mu) == oracle.rank_of(m, n, mu)
-    for m, n, b in [(256, 256, 1), (9728, 2560, 64), (64, 64, 256), (5, 7, 4), (2048, 2048, 32)]:
-        assert binding.effective_block(m, n, b) == min(oracle.effective_block(m, n, b), binding.MAX_BLOCK)
-    assert binding.effective_block(4096, 4096, 256) == 64
+    for m, n, b in [(256, 256, 1), (9728, 2560, 64), (64, 64, 256), (5, 7, 4), (2048, 2048, 32),
+                    (4096, 4096, 256), (519, 4000, 256), (520, 4000, 256)]:
+        assert binding.effective_block(m, n, b) == oracle.effective_block(m, n, b)
+    # the paper's default b = 256 is capped at floor(min(m, n) / 8) and nothing else
+    assert binding.effective_block(4096, 4096, 256) == 256 and binding.effective_block(519, 4000, 256) == 64
     assert binding.rank(0, 5, 1.0) == -1 and binding.rank(5, 5, 0.0) == -1 and binding.rank(5, 5, float("nan")) == -1
     ws = binding.workspace_bytes(9728, 2560, 7680)
     assert 4 * 9728 * 2560 < ws < 2 * 4 * 9728 * 2560
@@ -67,6 +69,13 @@ def test_argument_errors_before_device_work():
     # unsupported shape
     assert f(dummy, 1 << 16, 1 << 16, 1.0, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None,
              None, dummy, 1 << 40, None) == binding.EUNSUPPORTED
+    # effective block width beyond what the kernels hold: refused, never clamped
+    for ff, extra in [(f, ()), (L.externd_factorize_timed, (dummy,))]:
+        assert ff(dummy, 1024, 1024, 1.0, 0.7, 65, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+                  dummy, 1 << 40, None, *extra) == binding.EUNSUPPORTED
+        assert np.isnan(E.value)
+    assert f(dummy, 4096, 4096, 1.0, 0.7, 256, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+             dummy, 1 << 40, None) == binding.EUNSUPPORTED
     # step entry points
     assert L.externd_step_vstep(None, 10, 10, dummy, 4, 0.7, dummy, None, dummy, 1 << 30, None) == binding.EINVAL
     assert L.externd_step_vstep(dummy, 10, 10, dummy, 65, 0.7, dummy, None, dummy, 1 << 30, None) == binding.EINVAL

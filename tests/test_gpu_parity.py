@@ -126,6 +126,46 @@ def test_scale_parity(ext, kind, m, n, bb, weighted):
     np.testing.assert_allclose(d, d_ref, rtol=1e-8, atol=1e-12 * np.max(np.abs(d_ref)))
 
 
+@pytest.mark.parametrize("mode,weighted", [("duplicate", False), ("duplicate", True), ("near", True)])
+def test_scale_ill_conditioned(ext, mode, weighted):
+    """Eq. (4) with M = (U^T U) o (V^T H V) singular or nearly so.
+    duplicate: components 3 and 5 are copies (M singular; the guard delta
+    makes the system solvable).  near: copies except one trit of v_5, in a
+    column whose weight is 1e-7 of the largest (cond(M) ~ 1e9).  d is then
+    poorly determined (components 3 and 5 may split their share differently
+    on the two sides), so the block's energy decrease 2 d^T g - d^T M d is
+    compared (the rule where cond(M) > 1e6), with the scales of the other,
+    well-determined components."""
+    m, n, bb = 600, 300, 16
+    R = synth.small("t4_rowscale", m, n, 9).astype(np.float64)
+    h = synth.small_importance(n, 9) if weighted else None
+    w = oracle.normalized_weights(h, n)
+    U, _ = oracle.init_block(R, w, bb, 1.0)
+    for _ in range(2):
+        V, _ = oracle.vstep(R, U, 1.0)
+        U, Q, _ = oracle.ustep(R, V, w, 1.0)
+    U, V = U.copy(), V.copy()
+    U[:, 5], V[:, 5] = U[:, 3], V[:, 3]
+    if mode == "near":
+        j = int(np.flatnonzero(V[:, 3])[0])
+        V[j, 5] = 0
+        h = h.copy()
+        h[j] = np.float32(1e-7 * float(np.max(h)))
+        w = oracle.normalized_weights(h, n)
+    Q = R @ (w[:, None] * V.astype(np.float64))
+    Uf, Vf = U.astype(np.float64), V.astype(np.float64)
+    M = (Uf.T @ Uf) * (Vf.T @ (w[:, None] * Vf))
+    g = np.sum(Uf * Q, axis=0)
+    assert np.linalg.cond(M) > 1e6
+    d_ref = oracle.scale_solve(U, V, Q, w)
+    d = host(ext.step_scale(cuda(U), cuda(V), cuda(Q), h=cuda(h) if weighted else None))
+    gain = lambda x: 2.0 * (x @ g) - x @ M @ x
+    assert abs(gain(d) - gain(d_ref)) <= 1e-9 * gain(d_ref)
+    keep = np.ones(bb, dtype=bool)
+    keep[[3, 5]] = False
+    np.testing.assert_allclose(d[keep], d_ref[keep], rtol=1e-6, atol=1e-9 * np.max(np.abs(d_ref)))
+
+
 @pytest.mark.parametrize("kind,m,n,bb", SHAPES)
 def test_deflate_parity(ext, kind, m, n, bb):
     R = synth.small(kind, m, n, 4)
@@ -185,6 +225,8 @@ E2E = [
     ("gauss", 300, 64, 0.5, 0.7, 1, 3, False),     # b = 1 beyond the one-launch shapes: the block kernels
     ("t4", 40, 17000, 1.0, 1.0, 8, 3, True),       # > 512 column strips: one deflation and V-step row group
     ("t4_rowscale", 17000, 40, 1.0, 0.7, 8, 3, False),  # U-step groups of 32 rows beyond one resident pass
+    ("t4_outlier1e4", 300, 200, 1.0, 1.0, 8, 3, False),   # one entry 1e4 x the largest: per-row/column exponents
+    ("t4_outlier1e4", 256, 320, 1.0, 0.7, 16, 3, True),
 ]
 
 
@@ -193,7 +235,7 @@ def test_factorize_parity(ext, kind, m, n, mu, tau, block, iters, weighted):
     A = synth.small(kind, m, n, 6)
     h = synth.small_importance(n, 6) if weighted else None
     res = ext.factorize(cuda(A), mu, tau, block, iters, h=cuda(h) if weighted else None)
-    ref = oracle.factorize_block(A, mu, tau, min(block, 64), iters, h=h)
+    ref = oracle.factorize_block(A, mu, tau, block, iters, h=h)
     assert res.k == ref.k and res.block == ref.block
     np.testing.assert_allclose(res.curve, ref.curve, rtol=0, atol=1e-3)
     if weighted:
@@ -227,6 +269,20 @@ def test_gauss256_sequential_checkpoints(ext):
     ref = oracle.factorize_sequential(w.A, w.mu, w.tau, w.iters)
     ks = np.array(w.checkpoints_k) - 1
     np.testing.assert_allclose(res.curve[ks], ref.curve[ks], rtol=0, atol=1e-3)
+
+
+def test_block_wider_than_kernels_refused(ext):
+    # effective width min(b, floor(min(m, n) / 8)) = 128 > 64: refused, not clamped
+    A = cuda(synth.small("t4", 1024, 1030, 3))
+    with pytest.raises(ext.ExterndError) as e:
+        ext.factorize(A, 0.25, 1.0, 128, 2)
+    assert e.value.status == ext.EUNSUPPORTED
+    # the paper's default b = 256 where its cap brings it to 64 or less
+    A = synth.small("t4", 300, 515, 3)
+    res = ext.factorize(cuda(A), 0.5, 1.0, 256, 2)
+    ref = oracle.factorize_block(A, 0.5, 1.0, 256, 2)
+    assert res.block == ref.block == 37
+    np.testing.assert_allclose(res.curve, ref.curve, rtol=0, atol=1e-3)
 
 
 def test_zero_matrix(ext):
