@@ -33,7 +33,8 @@ INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, published
 # The one-launch sequential path runs in a single workgroup, i.e. on one of
 # the 256 compute units: its ceiling is one CU's share of the published fp32
 # vector rate (157.3 TFLOP/s / 256).
-CU_FP32_PEAK_GFLOPS = 157.3e3 / 256
+CHIP_FP32_PEAK_GFLOPS = 157.3e3
+CU_FP32_PEAK_GFLOPS = CHIP_FP32_PEAK_GFLOPS / 256
 # the kernels and the launch geometry (grid sizes and workspace layout)
 KERNEL_SOURCES = ["paper_2607_13511_amd/csrc/externd_kernels.hip", "paper_2607_13511_amd/csrc/externd_api.hip",
                   "paper_2607_13511_amd/csrc/externd_internal.hpp"]
@@ -117,23 +118,78 @@ def traffic_from_counters(kclass: str):
     return float(ent["fetch_bytes"] + ent["write_bytes"])
 
 
-def cpu_baseline(w, blocks: int):
-    """The CPU oracle (fp64 block ALS, as it stands) on the first `blocks`
-    blocks of the same workload."""
-    import oracle
+def oracle_threads() -> tuple:
+    """Threads the numpy oracle may use on this host: the cores this process
+    may run on, capped by OMP_NUM_THREADS when the environment sets it.
+    Returns (threads, cores in the affinity mask)."""
+    avail = len(os.sched_getaffinity(0))
     try:
-        import threadpoolctl
-        info = threadpoolctl.threadpool_info()
-        cores = max([d.get("num_threads", 1) for d in info] or [1])
+        cap = int(os.environ.get("OMP_NUM_THREADS", "0"))
+    except ValueError:
+        cap = 0
+    return (min(avail, cap) if cap > 0 else avail), avail
+
+
+def cpu_baseline(w, comps: int, blocks: int):
+    """The CPU oracle as it stands, timed on a bounded sample of the same
+    workload: the sequential greedy ALS (Sec. 2.3, one component at a time)
+    on its first `comps` components, and the block ALS (Sec. 2.4) on its
+    first `blocks` blocks.  Every component of a run costs the same (the
+    iteration count is fixed and the residual stays dense), so the time per
+    matrix is the sample time scaled to k.  The BLAS pool is limited to the
+    threads reported."""
+    import oracle
+    threads, avail = oracle_threads()
+    try:
+        from threadpoolctl import threadpool_limits
     except Exception:  # pragma: no cover - threadpoolctl missing
-        cores = 1
-    t0 = time.perf_counter()
-    f = oracle.factorize_block(w.A, w.mu, w.tau, w.block, w.iters, h=w.h, max_blocks=blocks)
-    dt = time.perf_counter() - t0
-    comps = blocks * f.block
-    return {"value": comps / dt, "unit": "components/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {blocks} blocks ({comps} of {f.k} components) of {w.name}, fp64 numpy/OpenBLAS",
-            "seconds": dt, "sec_per_matrix_extrapolated": dt * f.k / comps}
+        threadpool_limits = None
+    import contextlib
+    ctx = threadpool_limits(limits=threads) if threadpool_limits else contextlib.nullcontext()
+    m, n = w.A.shape
+    k = oracle.rank_of(m, n, w.mu)
+    with ctx:
+        t0 = time.perf_counter()
+        oracle.factorize_sequential(w.A, w.mu, w.tau, w.iters, h=w.h, k=comps)
+        dt = time.perf_counter() - t0
+        out = {"value": comps / dt, "unit": "components/s", "cores": int(threads), "kind": "oracle",
+               "sample": f"first {comps} of {k} components of the sequential greedy ALS (oracle.factorize_sequential, "
+                         f"fp64 numpy) on {w.name}", "seconds": dt, "sec_per_matrix_extrapolated": dt * k / comps,
+               "host_cores_in_affinity": int(avail)}
+        if blocks > 0:
+            t0 = time.perf_counter()
+            f = oracle.factorize_block(w.A, w.mu, w.tau, w.block, w.iters, h=w.h, max_blocks=blocks)
+            db = time.perf_counter() - t0
+            bc = blocks * f.block
+            out["block_oracle"] = {"value": bc / db, "unit": "components/s", "seconds": db,
+                                   "sample": f"first {blocks} blocks ({bc} of {f.k} components) of the block ALS "
+                                             f"(oracle.factorize_block, fp64 numpy)",
+                                   "sec_per_matrix_extrapolated": db * f.k / bc}
+    return out
+
+
+def sparsity_and_bpw(res, m: int, n: int, k: int) -> dict:
+    """Zero fractions of the factors, decoded from the packed 2-bit trits
+    (code 00 is zero), and the effective storage of Eq. (5): under mask+sign
+    packing an element costs 2 - sparsity bits, and k (m + n) elements are
+    stored for m n weights, i.e. mu (m + n) / max(m, n) (2 - sparsity) bits
+    per original weight (mu = k / min(m, n))."""
+    import torch
+
+    def zeros(packed, rows, cols):
+        p = packed.reshape(rows, -1)
+        z = 0
+        for t in range(4):
+            code = (p >> (2 * t)) & 3
+            valid = cols - t - 1 >= 4 * torch.arange(p.shape[1], device=p.device)
+            z += int(((code == 0) & valid).sum().item())
+        return z
+
+    zb, zc = zeros(res.B_packed, m, k), zeros(res.C_packed, k, n)
+    sp = (zb + zc) / float(k * (m + n))
+    mu = k / min(m, n)
+    return {"zero_fraction_B": zb / float(m * k), "zero_fraction_C": zc / float(k * n), "sparsity": sp,
+            "bpw_eff": mu * (m + n) / max(m, n) * (2.0 - sp), "bpw_eff_rule": "Eq. (5): mu (m+n)/max(m,n) (2 - sparsity)"}
 
 
 def calibrate_copy(nbytes: int, reps: int):
@@ -176,8 +232,8 @@ def collect_traffic(dbs, copy_bytes: int):
            "fetch_scale": ff, "write_scale": fw, "kernels": {}}
     lines = ["# HBM traffic per launch (rocprofv3 --pmc), 9728x2560 workload", "",
              "Commands (repository root, one MI355X):", "", "```",
-             "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o pmc -- python bench.py --steps 1 --warmup 0 --cpu-blocks 0",
-             "rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o pmc -- python bench.py --steps 1 --warmup 0 --cpu-blocks 0",
+             "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o pmc -- python bench.py --steps 1 --warmup 0 --cpu-comps 0",
+             "rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o pmc -- python bench.py --steps 1 --warmup 0 --cpu-comps 0",
              f"rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_copy_fetch -o pmc -- python bench.py --calibrate-copy {copy_bytes}",
              f"rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_copy_write -o pmc -- python bench.py --calibrate-copy {copy_bytes}",
              "python bench.py --collect-traffic gpurun_out/pmc_fetch/pmc_results.db gpurun_out/pmc_write/pmc_results.db "
@@ -205,13 +261,116 @@ def collect_traffic(dbs, copy_bytes: int):
     print(json.dumps(out))
 
 
+KERNEL_CLASS = {"k_vstep": "vstep_contraction", "k_ustep": "ustep_contraction", "k_ustep<false>": "ustep_contraction",
+                "k_ustep<true>": "ustep_contraction", "k_deflate": "deflate", "k_deflate<false>": "deflate",
+                "k_deflate<true>": "deflate", "k_vtarget": "vstep_target", "k_utarget": "ustep_target",
+                "k_tern_v": "ternarize_v", "k_tern_u": "ternarize_u"}
+
+
+def _short_kernel(name: str) -> str:
+    import re
+    return re.sub(r"\(.*", "", name).replace("void ", "").replace("externd::", "")
+
+
+def render_command() -> str:
+    import shlex
+    return "python " + " ".join(shlex.quote(a) for a in sys.argv)
+
+
+def render_trace(db: str, out_path: str, title: str, command: str, shape=None):
+    """Markdown summary of a rocprofv3 --kernel-trace database: calls, total
+    and average duration per kernel; with the matrix shape, the algorithmic
+    bytes per launch of each timed kernel class (the same rule as the bench
+    line's roofline) over the rocprofv3 average, as GB/s and as a fraction
+    of 8 TB/s."""
+    import sqlite3
+    con = sqlite3.connect(db)
+    cols = [r[1] for r in con.execute("pragma table_info(kernels)")]
+    name_col = "kernel_name" if "kernel_name" in cols else "name"
+    agg = {}
+    for k, c, tot in con.execute(f"select {name_col}, count(*), sum(end - start) from kernels group by {name_col}"):
+        kk = _short_kernel(k)
+        c0, s0 = agg.get(kk, (0, 0.0))
+        agg[kk] = (c0 + c, s0 + tot)
+    total = sum(v[1] for v in agg.values())
+    lines = [f"# {title}", "", "Command (from the repository root, on one MI355X):", "", "```", command, "```", "",
+             "Rendered with:", "", "```", render_command(), "```", "",
+             f"Kernel dispatches summed over the whole run (warm-up and timed steps): {total / 1e6:.1f} ms of GPU time.",
+             ""]
+    if shape:
+        m, n = shape
+        lines += [f"Rates use the algorithmic bytes per launch at m = {m}, n = {n} (bench.py algorithmic_bytes) over "
+                  "the average duration below.", "",
+                  "| kernel | calls | total (us) | average (us) | share | algorithmic GB/s | of 8 TB/s |",
+                  "|---|---:|---:|---:|---:|---:|---:|"]
+    else:
+        lines += ["| kernel | calls | total (us) | average (us) | share |", "|---|---:|---:|---:|---:|"]
+    for k, (c, t) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        row = f"| {k} | {c} | {t / 1e3:.1f} | {t / c / 1e3:.2f} | {100 * t / total:.1f}% |"
+        if shape:
+            cls = KERNEL_CLASS.get(k)
+            if cls:
+                gbs = algorithmic_bytes(cls, *shape) / (t / c * 1e-9) / 1e9
+                row += f" {gbs:.0f} | {gbs / HBM_PEAK_GBS:.3f} |"
+            else:
+                row += " | |"
+        lines.append(row)
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def render_mfma(db: str, out_path: str, command: str, m: int = 9728, n: int = 2560):
+    """Markdown summary of a rocprofv3 --pmc run over the MFMA counters
+    (SQ_VALU_MFMA_BUSY_CYCLES and the int8 / bf16 / fp64 MOPS counters):
+    MFMA operations issued per launch beside the algorithmic count, and the
+    MFMA pipes' busy fraction over the launch."""
+    import sqlite3
+    con = sqlite3.connect(db)
+    data = {}
+    for k, c, v, d, cnt in con.execute("select kernel_name, counter_name, avg(value), avg(duration), count(*) "
+                                      "from counters_collection group by kernel_name, counter_name"):
+        e = data.setdefault(_short_kernel(k), {})
+        e[c], e["dur"], e["n"] = v, d, cnt
+    bb = 64
+    alg = {"vstep_contraction": 4 * 2.0 * m * n * bb, "ustep_contraction": 4 * 2.0 * m * n * bb,
+           "deflate": 3 * 2.0 * m * n * bb}
+    lines = [f"# MFMA counters per launch (rocprofv3 --pmc), {m}x{n} workload (mu=3, tau=1.0, b=64, 8 iterations)",
+             "", "Command (from the repository root, on one MI355X):", "", "```", command, "```", "",
+             "Rendered with:", "", "```", render_command(), "```", "",
+             "MOPS counters count MFMA math operations / 512. `busy` is SQ_VALU_MFMA_BUSY_CYCLES summed over the 1024 "
+             "SIMDs; utilisation = busy / (dispatch duration under the counter run x 2.4 GHz x 1024 SIMDs). The int8 "
+             "count of a contraction is 4 x 2 m n 64 operations per launch (four 8-bit digit planes of the fixed-point "
+             "residual, block width 64); the deflation's bf16 work is 3 x 2 m n 64 (three exact bf16 parts of each "
+             "scale).", "",
+             "| kernel | launches | int8 ops | bf16 ops | fp64 ops | algorithmic MFMA ops | busy cycles | duration (us) "
+             "| MFMA utilisation |", "|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for k in sorted(data, key=lambda k: -data[k].get("SQ_VALU_MFMA_BUSY_CYCLES", 0)):
+        d = data[k]
+        busy = d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0)
+        if busy <= 0:
+            continue
+        i8, b16, f64 = (d.get(f"SQ_INSTS_VALU_MFMA_MOPS_{t}", 0) * 512 for t in ("I8", "BF16", "F64"))
+        a = alg.get(KERNEL_CLASS.get(k, ""), None)
+        util = busy / (d["dur"] * 1e-9 * 2.4e9 * 1024)
+        lines.append(f"| {k} | {d['n']} | {i8:.4g} | {b16:.4g} | {f64:.4g} | {f'{a:.4g}' if a else '—'} | {busy:.4g} "
+                     f"| {d['dur'] / 1e3:.1f} | {100 * util:.1f}% |")
+    lines += ["", "The contractions and the deflation are bound by HBM bandwidth (a pass over the residual), not by "
+              "the matrix cores: at the measured durations their MFMA pipes are busy for the fractions shown."]
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="down9728")
-    ap.add_argument("--cpu-blocks", type=int, default=40, help="oracle sample size in blocks (0 = skip)")
+    ap.add_argument("--cpu-comps", type=int, default=16,
+                    help="sequential-oracle sample in components (0 = skip the CPU baseline)")
+    ap.add_argument("--cpu-blocks", type=int, default=8, help="block-oracle sample in blocks (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0, help="run only a copy of this many bytes")
     ap.add_argument("--collect-traffic", nargs=4, metavar="DB",
                     help="rocprofv3 --pmc databases: FETCH_SIZE, WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE")
@@ -226,7 +385,18 @@ def main():
     ap.add_argument("--target-energy", type=float, default=None,
                     help="time the energy-target run instead (stop at the first block with E >= target, "
                          "mu of the workload as the maximum)")
+    ap.add_argument("--render-trace", nargs=4, metavar=("DB", "OUT", "TITLE", "COMMAND"),
+                    help="write a markdown summary of a rocprofv3 --kernel-trace database (rates for --workload)")
+    ap.add_argument("--render-mfma", nargs=3, metavar=("DB", "OUT", "COMMAND"),
+                    help="write a markdown summary of a rocprofv3 --pmc run over the MFMA counters")
     args = ap.parse_args()
+    if args.render_trace:
+        w = workload(args.workload)
+        render_trace(*args.render_trace, shape=None if w is None else w.A.shape)
+        return
+    if args.render_mfma:
+        render_mfma(*args.render_mfma)
+        return
     if args.collect_traffic:
         collect_traffic(args.collect_traffic, args.copy_bytes)
         return
@@ -292,10 +462,12 @@ def main():
     if dom == "sequential_one_launch":
         flops = seq_flops(m, n, k, w.iters)
         achieved = flops / avg_s / 1e9
-        roofline = {"bound": "alu", "achieved": achieved, "peak": CU_FP32_PEAK_GFLOPS, "unit": "GFLOP/s",
-                    "frac": achieved / CU_FP32_PEAK_GFLOPS, "traffic": None, "kernel": dom,
+        roofline = {"bound": "alu", "achieved": achieved, "peak": CHIP_FP32_PEAK_GFLOPS, "unit": "GFLOP/s",
+                    "frac": achieved / CHIP_FP32_PEAK_GFLOPS, "traffic": None, "kernel": dom,
                     "avg_launch_us": avg_s * 1e6, "algorithmic_flops_per_launch": flops,
-                    "note": "one workgroup on one compute unit; peak = 157.3 TFLOP/s fp32 vector / 256 CUs"}
+                    "one_cu_peak": CU_FP32_PEAK_GFLOPS, "frac_of_one_cu": achieved / CU_FP32_PEAK_GFLOPS,
+                    "note": "one workgroup on one compute unit: peak is the chip's fp32 vector rate "
+                            "(157.3 TFLOP/s = 256 CUs x 2.4 GHz x 256 flop/clk); frac_of_one_cu against 1/256 of it"}
     else:
         abytes = algorithmic_bytes(dom, m, n)
         achieved = abytes / avg_s / 1e9
@@ -326,10 +498,12 @@ def main():
         if 0 <= b < len(res.curve):
             checkpoints[f"k={kk}"] = float(res.curve[b])
 
+    factors = sparsity_and_bpw(res, m, n, k)
     cpu = None
-    if args.cpu_blocks > 0:
-        print(f"bench: CPU oracle on {args.cpu_blocks} blocks", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, args.cpu_blocks)
+    if args.cpu_comps > 0:
+        print(f"bench: CPU oracle on {args.cpu_comps} sequential components and {args.cpu_blocks} blocks",
+              file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, args.cpu_comps, args.cpu_blocks)
 
     out = {
         "metric": METRIC,
@@ -350,6 +524,7 @@ def main():
         "energy": res.E,
         "energy_w": res.E_w,
         "energy_checkpoints": checkpoints,
+        "factors": factors,
         "arithmetic": ("fp32 residual in registers of one workgroup; fp32 per-thread partial sums combined in "
                        "fp64; fp64 thresholds, scales and energies") if dom == "sequential_one_launch" else
                       ("fp32 residual; exact int8-MFMA contractions of 32-bit fixed point; fp64 targets/solves; "
