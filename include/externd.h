@@ -16,11 +16,12 @@
  *    example torch.cuda tensor data pointers); "host" pointers are ordinary
  *    CPU memory.
  *  - Matrices are row-major and dense (leading dimension = column count).
- *  - The caller owns every buffer.  The library keeps no pointer after a
- *    call returns, allocates no device memory and has no global state
- *    besides the loaded code object; calls on distinct workspaces and
- *    streams are independent.  Calls sharing a workspace must be ordered
- *    (same stream or synchronised by the caller).
+ *  - The caller owns every buffer.  The library keeps no pointer to a
+ *    caller buffer after a call returns and allocates no device memory;
+ *    calls on distinct workspaces and streams are independent.  Calls
+ *    sharing a workspace must be ordered (same stream or synchronised by the
+ *    caller).  The one piece of global state is the fixed device scratch of
+ *    externd_apply_noalloc (below), one copy per device.
  *  - `stream` is a hipStream_t (NULL = the default stream).  All device work
  *    is enqueued on it.
  *  - Errors are returned as negative status codes; no exception crosses the
@@ -52,6 +53,8 @@ extern "C" {
 #define EXTERND_ESYNC        -6  /* a bounded wait between the workgroups of one kernel
                                     launch ran out (reserved: no kernel of this version
                                     waits on another workgroup)                          */
+#define EXTERND_ESCRATCH     -7  /* the call needs more than the fixed device scratch of
+                                    an allocation-free entry point                       */
 
 /* Largest effective block width the kernels handle.  A call whose
  * effective width (externd_effective_block) exceeds it returns
@@ -240,6 +243,31 @@ size_t externd_apply_workspace_bytes(int64_t k, int32_t nb);  /* 0 on invalid ar
 int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n,
                   int64_t k, const float* X, int32_t nb, float* Y, void* workspace, size_t workspace_bytes,
                   void* stream);
+
+/*
+ * externd_apply without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, arithmetic, results
+ * (bit for bit) and status codes as externd_apply, with the k x nb
+ * intermediate held in a fixed device array of the library instead:
+ *  - at most EXTERND_APPLY_NOALLOC_MAX_BYTES of intermediate, i.e.
+ *    externd_apply_workspace_bytes(k, nb) <= that bound (k <= 65536 at
+ *    nb = 8, k <= 524288 at nb = 1); larger calls return EXTERND_ESCRATCH
+ *    before any device work;
+ *  - the array is per device: the current device's copy is used, and the
+ *    stream must belong to the current device.  Each device keeps its copy
+ *    until the process ends.  The first call on a device looks up the
+ *    array's address (hipGetSymbolAddress); no call allocates or frees
+ *    device memory;
+ *  - every call on a device shares that device's array: calls that overlap
+ *    on one device (concurrent streams, or several host threads without
+ *    ordering) race and give unspecified results.  Calls ordered on one
+ *    stream are safe; nothing needs to be cleared between calls (every
+ *    entry a call reads is written earlier in the same call).
+ */
+#define EXTERND_APPLY_NOALLOC_MAX_BYTES (2u << 20)
+int externd_apply_noalloc(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n,
+                          int64_t k, const float* X, int32_t nb, float* Y, void* stream);
 
 /* Kernel classes timed by externd_factorize_timed. */
 #define EXTERND_KCLASS_VSTEP   0  /* V-step contraction P = U^T R (+ Gram of U, inverse) */

@@ -17,7 +17,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libexternd.so")
 
-OK, EINVAL, ENONFINITE, EWORKSPACE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+OK, EINVAL, ENONFINITE, EWORKSPACE, EHIP, EUNSUPPORTED, ESYNC, ESCRATCH = 0, -1, -2, -3, -4, -5, -6, -7
+APPLY_NOALLOC_MAX_BYTES = 2 << 20   # EXTERND_APPLY_NOALLOC_MAX_BYTES
 MAX_BLOCK = 64
 
 _lib = None
@@ -49,6 +50,8 @@ _SIGNATURES = {
     "externd_apply_workspace_bytes": (_c_size, [_c_i64, _c_i32]),
     "externd_apply": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i64, _c_i64, _c_ptr, _c_i32, _c_ptr,
                                      _c_ptr, _c_size, _c_ptr]),
+    "externd_apply_noalloc": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i64, _c_i64, _c_ptr, _c_i32,
+                                             _c_ptr, _c_ptr]),
     "externd_factorize_timed": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_ptr,
                                                _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                                _c_ptr, _c_size, _c_ptr, _c_ptr]),
@@ -258,6 +261,26 @@ def apply(B_packed, C_packed, D, m: int, n: int, X, stream=None, workspace=None)
     ws = workspace if workspace is not None else torch.empty(nbytes, dtype=torch.uint8, device=X.device)
     _check(lib().externd_apply(_dev_ptr(B_packed), _dev_ptr(C_packed), _dev_ptr(D), m, n, k, _dev_ptr(X), nb,
                                _dev_ptr(Y), _dev_ptr(ws), ws.numel(), _stream_ptr(torch, stream)), "externd_apply")
+    return Y
+
+
+def apply_noalloc(B_packed, C_packed, D, m: int, n: int, X, Y=None, stream=None):
+    """As ``apply`` through externd_apply_noalloc: no workspace, the
+    intermediate lives in the library's fixed per-device scratch.  ``Y``
+    (nb x m fp32 CUDA tensor) may be given so that the call allocates
+    nothing at all.  Returns Y."""
+    torch = _torch()
+    k = D.shape[0]
+    nb = X.shape[0]
+    _req(X, torch, torch.float32, (nb, n), "X")
+    _req(D, torch, torch.float32, (k,), "D")
+    _req(B_packed, torch, torch.uint8, (m, (k + 3) // 4), "B_packed")
+    _req(C_packed, torch, torch.uint8, (k, (n + 3) // 4), "C_packed")
+    if Y is None:
+        Y = torch.empty((nb, m), dtype=torch.float32, device=X.device)
+    _req(Y, torch, torch.float32, (nb, m), "Y")
+    _check(lib().externd_apply_noalloc(_dev_ptr(B_packed), _dev_ptr(C_packed), _dev_ptr(D), m, n, k, _dev_ptr(X),
+                                       nb, _dev_ptr(Y), _stream_ptr(torch, stream)), "externd_apply_noalloc")
     return Y
 
 

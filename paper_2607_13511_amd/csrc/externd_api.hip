@@ -238,6 +238,7 @@ const char* externd_strerror(int status) {
     case EXTERND_EHIP: return "HIP runtime or launch failure";
     case EXTERND_EUNSUPPORTED: return "unsupported shape";
     case EXTERND_ESYNC: return "device-side synchronisation between workgroups timed out";
+    case EXTERND_ESCRATCH: return "call exceeds the fixed device scratch of an allocation-free entry point";
     default: return "unknown status";
   }
 }

@@ -17,6 +17,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "externd.h"
 #include "externd_internal.hpp"
 
@@ -126,6 +128,53 @@ static hipError_t launch_apply_nb(const uint8_t* Bp, const uint8_t* Cp, const fl
 // The intermediate holds apply_slots(nb) x kp floats.
 static int apply_slots(int nb) { return nb <= 1 ? 1 : nb <= 2 ? 2 : nb <= 4 ? 4 : 8; }
 
+// Allocation-free variant: the k x nb intermediate lives in a file-scope
+// device array of a fixed size.  Each device that runs the code object holds
+// its own copy until the process ends; host code reaches it only through the
+// address hipGetSymbolAddress returns on that device (the array's name in
+// host code is a stand-in, not a device address).
+static __device__ __align__(256) float scratch[EXTERND_APPLY_NOALLOC_MAX_BYTES / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static float* g_scratch_ptr[kMaxDevices];
+
+// The scratch array's device address on the current device, looked up once
+// per device with that device current.
+static int scratch_on_current_device(float** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return EXTERND_EHIP;
+  if (dev < 0 || dev >= kMaxDevices) return EXTERND_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return EXTERND_EHIP;
+    g_scratch_ptr[dev] = (float*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return EXTERND_OK;
+}
+
+static int check_apply_args(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n,
+                            int64_t k, const float* X, int32_t nb, float* Y) {
+  if (!B_packed || !C_packed || !D || !X || !Y) return EXTERND_EINVAL;
+  if (m < 1 || n < 1 || k < 1 || nb < 1 || nb > EXTERND_APPLY_MAX_BATCH) return EXTERND_EINVAL;
+  if (m > ((int64_t)1 << 31) || n > ((int64_t)1 << 31) || k > ((int64_t)1 << 31)) return EXTERND_EUNSUPPORTED;
+  return EXTERND_OK;
+}
+
+static int run_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n,
+                     int64_t k, const float* X, int32_t nb, float* Y, float* T, hipStream_t s) {
+  hipError_t e;
+  switch (apply_slots(nb)) {
+    case 1: e = launch_apply_nb<1>(B_packed, C_packed, D, m, n, k, X, nb, Y, T, s); break;
+    case 2: e = launch_apply_nb<2>(B_packed, C_packed, D, m, n, k, X, nb, Y, T, s); break;
+    case 4: e = launch_apply_nb<4>(B_packed, C_packed, D, m, n, k, X, nb, Y, T, s); break;
+    default: e = launch_apply_nb<8>(B_packed, C_packed, D, m, n, k, X, nb, Y, T, s); break;
+  }
+  return e == hipSuccess ? EXTERND_OK : EXTERND_EHIP;
+}
+
 }  // namespace externd
 
 using namespace externd;
@@ -139,21 +188,24 @@ size_t externd_apply_workspace_bytes(int64_t k, int32_t nb) {
 
 int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n, int64_t k,
                   const float* X, int32_t nb, float* Y, void* workspace, size_t workspace_bytes, void* stream) {
-  if (!B_packed || !C_packed || !D || !X || !Y || !workspace) return EXTERND_EINVAL;
-  if (m < 1 || n < 1 || k < 1 || nb < 1 || nb > EXTERND_APPLY_MAX_BATCH) return EXTERND_EINVAL;
-  if (m > ((int64_t)1 << 31) || n > ((int64_t)1 << 31) || k > ((int64_t)1 << 31)) return EXTERND_EUNSUPPORTED;
+  int st = check_apply_args(B_packed, C_packed, D, m, n, k, X, nb, Y);
+  if (st != EXTERND_OK) return st;
+  if (!workspace) return EXTERND_EINVAL;
   const size_t need = externd_apply_workspace_bytes(k, nb);
   if (need == 0 || workspace_bytes < need || ((uintptr_t)workspace & 15u)) return EXTERND_EWORKSPACE;
-  hipStream_t s = (hipStream_t)stream;
-  float* T = (float*)workspace;
-  hipError_t e;
-  switch (apply_slots(nb)) {
-    case 1: e = launch_apply_nb<1>(B_packed, C_packed, D, m, n, k, X, nb, Y, T, s); break;
-    case 2: e = launch_apply_nb<2>(B_packed, C_packed, D, m, n, k, X, nb, Y, T, s); break;
-    case 4: e = launch_apply_nb<4>(B_packed, C_packed, D, m, n, k, X, nb, Y, T, s); break;
-    default: e = launch_apply_nb<8>(B_packed, C_packed, D, m, n, k, X, nb, Y, T, s); break;
-  }
-  return e == hipSuccess ? EXTERND_OK : EXTERND_EHIP;
+  return run_apply(B_packed, C_packed, D, m, n, k, X, nb, Y, (float*)workspace, (hipStream_t)stream);
+}
+
+int externd_apply_noalloc(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n,
+                          int64_t k, const float* X, int32_t nb, float* Y, void* stream) {
+  int st = check_apply_args(B_packed, C_packed, D, m, n, k, X, nb, Y);
+  if (st != EXTERND_OK) return st;
+  const size_t need = externd_apply_workspace_bytes(k, nb);
+  if (need == 0 || need > (size_t)EXTERND_APPLY_NOALLOC_MAX_BYTES) return EXTERND_ESCRATCH;
+  float* T = nullptr;
+  st = scratch_on_current_device(&T);
+  if (st != EXTERND_OK) return st;
+  return run_apply(B_packed, C_packed, D, m, n, k, X, nb, Y, T, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -138,3 +138,21 @@ def test_unpack_trits_format():
         binding.unpack_trits(np.array([[0b10, 0]], dtype=np.uint8), 5)       # code 10
     with pytest.raises(ValueError):
         binding.unpack_trits(np.array([[0, 0b0100]], dtype=np.uint8), 5)     # padding bit set
+
+
+def test_apply_noalloc_rejects_before_device_work():
+    """The allocation-free inference entry point checks its arguments and its
+    scratch bound on the host: no HIP call is made on these paths."""
+    L = binding.lib()
+    d = ctypes.c_void_p(256)          # never dereferenced: validation fails first
+    f = L.externd_apply_noalloc
+    assert f(None, d, d, 10, 10, 10, d, 1, d, None) == binding.EINVAL
+    assert f(d, d, d, 10, 10, 10, d, 9, d, None) == binding.EINVAL              # nb above the batch limit
+    assert f(d, d, d, 0, 10, 10, d, 1, d, None) == binding.EINVAL
+    assert f(d, d, d, 10, 10, 1 << 32, d, 1, d, None) == binding.EUNSUPPORTED
+    # intermediate of k x slots(nb) floats against the fixed bound
+    assert binding.APPLY_NOALLOC_MAX_BYTES == 2 << 20
+    assert L.externd_apply_workspace_bytes(65536, 8) == binding.APPLY_NOALLOC_MAX_BYTES
+    assert f(d, d, d, 10, 10, 65537, d, 8, d, None) == binding.ESCRATCH
+    assert f(d, d, d, 10, 10, 524289, d, 1, d, None) == binding.ESCRATCH
+    assert L.externd_strerror(binding.ESCRATCH).decode().startswith("call exceeds the fixed device scratch")
