@@ -368,9 +368,9 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="down9728")
-    ap.add_argument("--cpu-comps", type=int, default=16,
+    ap.add_argument("--cpu-comps", type=int, default=96,
                     help="sequential-oracle sample in components (0 = skip the CPU baseline)")
-    ap.add_argument("--cpu-blocks", type=int, default=8, help="block-oracle sample in blocks (0 = skip)")
+    ap.add_argument("--cpu-blocks", type=int, default=32, help="block-oracle sample in blocks (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0, help="run only a copy of this many bytes")
     ap.add_argument("--collect-traffic", nargs=4, metavar="DB",
                     help="rocprofv3 --pmc databases: FETCH_SIZE, WRITE_SIZE, copy FETCH_SIZE, copy WRITE_SIZE")

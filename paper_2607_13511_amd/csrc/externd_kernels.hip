@@ -1943,81 +1943,172 @@ __device__ __forceinline__ void reduce_colE(const double* __restrict__ colE_part
 
 constexpr int SELECT_CACHE = 8;  // keys per thread kept in registers (n <= SELECT_CACHE * NT_SELECT without memory passes)
 
+// Column energies of the NQ columns j = tid + q st of this thread: the gd
+// row-group partials summed in row-group order, GU row groups a round with
+// all their loads issued together (clamped indices, masked afterwards).
+template <int NQ>
+__device__ __forceinline__ void select_energies(const double* __restrict__ colE_part, int gd, int64_t n_pad,
+                                                int64_t st, double (&e)[SELECT_CACHE]) {
+  constexpr int GU = NQ >= 16 ? 1 : 16 / NQ;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < SELECT_CACHE; ++q) e[q] = 0.0;
+  for (int g0 = 0; g0 < gd; g0 += GU) {
+    double v[GU][NQ];
+#pragma unroll
+    for (int u = 0; u < GU; ++u) {
+      const int g = g0 + u < gd ? g0 + u : gd - 1;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int64_t j = tid + q * st;
+        v[u][q] = colE_part[(int64_t)g * n_pad + (j < n_pad ? j : 0)];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < GU; ++u)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        if (g0 + u < gd) e[q] += v[u][q];
+  }
+}
+
 __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__ colE_part, int gd, int64_t n,
                                                       int64_t n_pad, const double* __restrict__ hw,
                                                       double* keys /* n_pad scratch */, double* fro2_out,
                                                       double* fro2w_out, int bb, int* __restrict__ J,
                                                       int* __restrict__ cshift) {
-  __shared__ double shd[16];
-  __shared__ unsigned hist[NT_SELECT / 64][256];  // one histogram per wave
-  __shared__ unsigned htot[256];
+  __shared__ double wred[4][NT_SELECT / 64];
+  __shared__ unsigned hist[256];
   __shared__ unsigned long long s_prefix;
-  __shared__ int s_need, s_exact;
+  __shared__ int s_need, s_exact, s_hi;
   __shared__ int s_cnt;
   __shared__ unsigned long long cand_key[BBP];
   __shared__ int cand_idx[BBP];
   __shared__ int s_scan[NT_SELECT / 64];
-  if (threadIdx.x < BBP) {
-    cand_key[threadIdx.x] = 0ull;
-    cand_idx[threadIdx.x] = 0;
-  }
-  reduce_colE(colE_part, gd, n, n_pad, hw, keys, fro2_out, fro2w_out, shd, cshift);
-  __syncthreads();
-  // key_j = h~_j ||R_:j||^2 as a 64-bit pattern (non-negative doubles order
-  // like their bit patterns); the first SELECT_CACHE keys of each thread
-  // stay in registers, the rest (large n only) are re-read from `keys`
+  __shared__ int s_rank[BBP];
+  const int tid = threadIdx.x;
   const int64_t st = blockDim.x;
-  unsigned long long kc[SELECT_CACHE];
+  const int nw = (int)(blockDim.x >> 6);
+  if (tid < BBP) {
+    cand_key[tid] = 0ull;
+    cand_idx[tid] = 0;
+  }
+  // Column energies ||R_:j||^2 of this thread's columns; the keys
+  // h~_j ||R_:j||^2 stay in registers, columns beyond SELECT_CACHE st (very
+  // wide matrices only) go through `keys`.  Every global store of the
+  // kernel (exponents, norms, the selection) is issued at its end, so that
+  // no barrier waits for one.
+  double hq[SELECT_CACHE];
 #pragma unroll
   for (int q = 0; q < SELECT_CACHE; ++q) {
-    const int64_t j = threadIdx.x + q * st;
-    kc[q] = j < n ? (unsigned long long)__double_as_longlong(hw[j] * keys[j]) : 0ull;
+    const int64_t j = tid + q * st;
+    hq[q] = hw[j < n_pad ? j : 0];
   }
-  for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) keys[j] = hw[j] * keys[j];
-  // radix select over the 64-bit patterns, 8 bits at a time from the top.
-  // Energies share their leading bits, so each wave counts into its own
-  // histogram (no block-wide contention on one bin).  The passes stop early
-  // once the bin holding the bb-th largest key holds exactly the keys still
-  // needed: then the selection is every key >= that bin's lower bound.
-  if (threadIdx.x == 0) {
-    s_prefix = 0ull;
+  double e[SELECT_CACHE];
+  const int64_t nq = (n_pad + st - 1) / st;
+  if (nq <= 1) select_energies<1>(colE_part, gd, n_pad, st, e);
+  else if (nq <= 2) select_energies<2>(colE_part, gd, n_pad, st, e);
+  else if (nq <= 3) select_energies<3>(colE_part, gd, n_pad, st, e);
+  else if (nq <= 4) select_energies<4>(colE_part, gd, n_pad, st, e);
+  else select_energies<SELECT_CACHE>(colE_part, gd, n_pad, st, e);
+  double s = 0.0, sw = 0.0;
+  unsigned long long kc[SELECT_CACHE];
+  int csh[SELECT_CACHE];
+  double kmax = 0.0, kmin = INFINITY;
+#pragma unroll
+  for (int q = 0; q < SELECT_CACHE; ++q) {
+    const int64_t j = tid + q * st;
+    const double c = j < n ? e[q] : 0.0;
+    csh[q] = col_shift(c);
+    s += c;
+    sw += hq[q] * c;
+    const double key = hq[q] * c;
+    kc[q] = j < n ? (unsigned long long)__double_as_longlong(key) : 0ull;
+    if (j < n) {
+      kmax = fmax(kmax, key);
+      kmin = fmin(kmin, key);
+    }
+  }
+  for (int64_t j = tid + SELECT_CACHE * st; j < n_pad; j += st) {
+    double c = 0.0;
+    for (int g = 0; g < gd; ++g) c += colE_part[(int64_t)g * n_pad + j];
+    if (j >= n) c = 0.0;
+    cshift[j] = col_shift(c);
+    s += c;
+    sw += hw[j] * c;
+    if (j < n) {
+      const double key = hw[j] * c;
+      keys[j] = key;
+      kmax = fmax(kmax, key);
+      kmin = fmin(kmin, key);
+    }
+  }
+  // one block reduction for the two norms and the key range (DPP within
+  // each wave, then the waves in order)
+  kmin = -kmin;
+  wave_sum63(s);
+  wave_sum63(sw);
+  wave_max63(kmax);
+  wave_max63(kmin);
+  if (lane_id() == 63) {
+    wred[0][wave_id()] = s;
+    wred[1][wave_id()] = sw;
+    wred[2][wave_id()] = kmax;
+    wred[3][wave_id()] = kmin;
+  }
+  __syncthreads();
+  double f2 = 0.0, f2w = 0.0;
+  if (tid == 0) {
+    double a = 0.0, b = -INFINITY;
+    for (int w = 0; w < nw; ++w) {
+      f2 += wred[0][w];
+      f2w += wred[1][w];
+      a = fmax(a, wred[2][w]);
+      b = fmax(b, wred[3][w]);
+    }
+    // the radix passes start below the leading bits that every key shares
+    // (non-negative doubles order like their bit patterns)
+    const unsigned long long ka = (unsigned long long)__double_as_longlong(a);
+    const unsigned long long kb = (unsigned long long)__double_as_longlong(-b);
+    const unsigned long long d = ka ^ kb;
+    const int hi = d ? 64 - __clzll((long long)d) : 0;
+    s_hi = hi;
+    s_prefix = hi < 64 ? (ka & (~0ull << hi)) : 0ull;
     s_need = bb;
     s_exact = 0;
   }
   __syncthreads();
-  unsigned* whist = hist[wave_id()];
-  for (int pass = 0; pass < 8; ++pass) {
-    const int shift = 56 - 8 * pass;
-    for (int e = threadIdx.x; e < (NT_SELECT / 64) * 256; e += blockDim.x) (&hist[0][0])[e] = 0u;
+  // Radix select of the bb-th largest key over 8-bit windows [lo, hi) from
+  // the first bit where keys differ down to bit 0.  The passes stop early
+  // once the window bin holding the bb-th largest key holds exactly the
+  // keys still needed: then the selection is every key >= that bin's lower
+  // bound.  (All keys equal: hi = 0, no pass, T = that key.)
+  for (int hi = s_hi; hi > 0;) {
+    const int lo = hi > 8 ? hi - 8 : 0;
+    const unsigned dmask = (1u << (hi - lo)) - 1u;
+    if (tid < 256) hist[tid] = 0u;
     __syncthreads();
     const unsigned long long prefix = s_prefix;
-    const unsigned long long hmask = (pass == 0) ? 0ull : (~0ull << (shift + 8));
+    const unsigned long long hmask = hi < 64 ? (~0ull << hi) : 0ull;
 #pragma unroll
     for (int q = 0; q < SELECT_CACHE; ++q) {
-      const int64_t j = threadIdx.x + q * st;
-      if (j < n && (kc[q] & hmask) == prefix) atomicAdd(&whist[(kc[q] >> shift) & 0xff], 1u);
+      const int64_t j = tid + q * st;
+      if (j < n && (kc[q] & hmask) == prefix) atomicAdd(&hist[(unsigned)(kc[q] >> lo) & dmask], 1u);
     }
-    for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) {
+    for (int64_t j = tid + SELECT_CACHE * st; j < n; j += st) {
       const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
-      if ((kb & hmask) == prefix) atomicAdd(&whist[(kb >> shift) & 0xff], 1u);
+      if ((kb & hmask) == prefix) atomicAdd(&hist[(unsigned)(kb >> lo) & dmask], 1u);
     }
     __syncthreads();
-    if (threadIdx.x < 256) {
-      unsigned c = 0;
-#pragma unroll
-      for (int w = 0; w < NT_SELECT / 64; ++w) c += hist[w][threadIdx.x];
-      htot[threadIdx.x] = c;
-    }
-    __syncthreads();
-    if (threadIdx.x < 64) {
+    if (tid < 64) {
       // wave 0: lane l holds digits 255-4l .. 252-4l (descending); the
       // first lane whose inclusive count reaches `need` holds the digit.
-      const int lane = threadIdx.x;
+      const int lane = tid;
       const int need = s_need;
       int c[4], tot = 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        c[q] = (int)htot[255 - 4 * lane - q];
+        c[q] = (int)hist[255 - 4 * lane - q];
         tot += c[q];
       }
       // inclusive scan over the wave on DPP: within rows, then across rows
@@ -2049,12 +2140,13 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
           nn = need - run;
         }
         s_need = nn;
-        s_prefix = prefix | ((unsigned long long)d << shift);
+        s_prefix = prefix | ((unsigned long long)d << lo);
         s_exact = found && cd == nn;
       }
     }
     __syncthreads();
     if (s_exact) break;
+    hi = lo;
   }
   // T = s_prefix: either the exact key of the bb-th largest (keys > T all
   // selected, then the s_need smallest indices with key == T), or, after an
@@ -2064,11 +2156,11 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
   const unsigned long long T = s_prefix;
   const int need_eq = ge ? 0 : s_need;
   auto above = [&](unsigned long long kb) { return ge ? kb >= T : kb > T; };
-  if (threadIdx.x == 0) s_cnt = 0;
+  if (tid == 0) s_cnt = 0;
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < SELECT_CACHE; ++q) {
-    const int64_t j = threadIdx.x + q * st;
+    const int64_t j = tid + q * st;
     if (j < n && above(kc[q])) {
       const int slot = atomicAdd(&s_cnt, 1);
       if (slot < BBP) {
@@ -2077,7 +2169,7 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
       }
     }
   }
-  for (int64_t j = threadIdx.x + SELECT_CACHE * st; j < n; j += st) {
+  for (int64_t j = tid + SELECT_CACHE * st; j < n; j += st) {
     const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
     if (above(kb)) {
       const int slot = atomicAdd(&s_cnt, 1);
@@ -2121,23 +2213,47 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
   };
 #pragma unroll
   for (int q = 0; q < SELECT_CACHE; ++q)
-    if (!done && q < rounds) scan_round(threadIdx.x + q * st, kc[q]);
+    if (!done && q < rounds) scan_round(tid + q * st, kc[q]);
   for (int q = SELECT_CACHE; !done && q < rounds; ++q) {
-    const int64_t j = threadIdx.x + q * st;
+    const int64_t j = tid + q * st;
     scan_round(j, j < n ? (unsigned long long)__double_as_longlong(keys[j]) : 0ull);
   }
   __syncthreads();
-  // order the bb winners by (key desc, index asc)
-  if (threadIdx.x < bb) {
-    const unsigned long long k0 = cand_key[threadIdx.x];
-    const int i0 = cand_idx[threadIdx.x];
-    int rank = 0;
-    for (int q = 0; q < bb; ++q) {
-      const unsigned long long k1 = cand_key[q];
-      const int i1 = cand_idx[q];
-      rank += (k1 > k0) || (k1 == k0 && i1 < i0);
+  // order the bb winners by (key desc, index asc): 16 threads per winner
+  // each compare it with a quarter of the others, summed over the 16 lanes
+  // of a row on DPP
+  {
+    const int a = tid >> 4, b = tid & 15;
+    int r = 0;
+    if (a < bb) {
+      const unsigned long long k0 = cand_key[a];
+      const int i0 = cand_idx[a];
+#pragma unroll
+      for (int u = 0; u < BBP / 16; ++u) {
+        const int q = b + 16 * u;
+        if (q < bb) {
+          const unsigned long long k1 = cand_key[q];
+          const int i1 = cand_idx[q];
+          r += (k1 > k0) || (k1 == k0 && i1 < i0);
+        }
+      }
     }
-    J[rank] = i0;
+    r += __builtin_amdgcn_update_dpp(0, r, DPP_ROW_SHR1, 0xF, 0xF, false);
+    r += __builtin_amdgcn_update_dpp(0, r, DPP_ROW_SHR2, 0xF, 0xF, false);
+    r += __builtin_amdgcn_update_dpp(0, r, DPP_ROW_SHR4, 0xF, 0xF, false);
+    r += __builtin_amdgcn_update_dpp(0, r, DPP_ROW_SHR8, 0xF, 0xF, false);
+    if (b == 15 && a < bb) s_rank[a] = r;
+  }
+  __syncthreads();
+  if (tid < bb) J[s_rank[tid]] = cand_idx[tid];
+  if (tid == 0) {
+    *fro2_out = f2;
+    *fro2w_out = f2w;
+  }
+#pragma unroll
+  for (int q = 0; q < SELECT_CACHE; ++q) {
+    const int64_t j = tid + q * st;
+    if (j < n_pad) cshift[j] = csh[q];
   }
 }
 

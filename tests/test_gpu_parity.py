@@ -203,6 +203,39 @@ def test_init_parity(ext, kind, m, n, bb, weighted):
         assert_tern_parity(U[:, c], R[:, J[c]].astype(np.float64), 0.7, f"init column {c}")
 
 
+def _tie_cases():
+    """Residuals whose selection keys tie exactly (reading R1: descending
+    key, ties to the smaller column index): exact duplicates of the
+    largest column among ordinary ones plus zero columns, every column the
+    same, and the zero matrix."""
+    rng = np.random.default_rng(11)
+    A = (0.02 * rng.standard_normal((200, 300))).astype(np.float32)
+    top = (0.2 * rng.standard_normal(200)).astype(np.float32)
+    for j in (10, 50, 51, 299):
+        A[:, j] = top
+    A[:, 100:120] = 0.0
+    yield "duplicates", A, 16
+    col = (0.05 * rng.standard_normal(64)).astype(np.float32)
+    yield "all_equal", np.repeat(col[:, None], 96, axis=1), 8
+    yield "zero", np.zeros((64, 80), np.float32), 8
+
+
+@pytest.mark.parametrize("case", ["duplicates", "all_equal", "zero"])
+def test_select_exact_ties(ext, case):
+    name, R, bb = next(c for c in _tie_cases() if c[0] == case)
+    m, n = R.shape
+    print(f"[select] {name} {m}x{n} bb={bb}", flush=True)
+    U_ref, J_ref = oracle.init_block(R.astype(np.float64), np.ones(n), bb, 0.7)
+    U, J = ext.step_init(cuda(R), bb, 0.7)
+    U, J = host(U), host(J)
+    # exact ties: the GPU's column energies of identical columns are
+    # identical, so the order is fixed and must match the oracle's
+    np.testing.assert_array_equal(J, J_ref)
+    np.testing.assert_array_equal(U, U_ref)
+    if name == "duplicates":
+        assert list(J[:4]) == [10, 50, 51, 299]
+
+
 # ---------------------------------------------------------------------------
 # end-to-end
 # ---------------------------------------------------------------------------
