@@ -295,8 +295,8 @@ static hipError_t run_sweeps(const Ws& w, int64_t k, int b_eff, double tau, int3
       SWEEP_TRY(launch_deflate_slot(w, S1, s, tm));  // R' = R + U diag(d) V^T
       SWEEP_TRY(launch_finish(w, S1, s));
       for (int it = 0; it < iters; ++it) {
-        SWEEP_TRY(launch_vstep(w, S1, bb, tau, s, tm));
-        SWEEP_TRY(launch_ustep(w, S1, bb, tau, weighted, it == iters - 1, s, tm));
+        SWEEP_TRY(launch_vstep(w, S1, bb, tau, s, tm, weighted));
+        SWEEP_TRY(launch_ustep(w, S1, bb, tau, weighted, it == iters - 1, s, tm, weighted));
       }
       SWEEP_TRY(launch_gram_acc(w, 0, s));
       SWEEP_TRY(launch_revisit_decide(w, bb, D + c0, weighted, S, S1, s));
@@ -386,8 +386,8 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
       HIP_TRY(launch_select(w, (int)blk, bb, s));
       HIP_TRY(launch_init(w, bb, tau, s));
       for (int it = 0; it < iters; ++it) {
-        HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm));
-        HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm));
+        HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm, weighted));
+        HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm, weighted));
       }
       HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
       if (safeguard) HIP_TRY(launch_safeguard(w, (int)blk, bb, D + c0, s));

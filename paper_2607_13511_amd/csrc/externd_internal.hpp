@@ -151,11 +151,15 @@ hipError_t launch_finish(const Ws& w, int blk, hipStream_t s);
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s);
 // The contraction launches build the Gram of their factor themselves (side
 // workgroups); launch_gram_acc serves the scale solve.
-hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr);
+// weighted: V is thresholded by row blocks, which also leaves the partials
+// of V^T diag(h~) V for the next U-step.
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr,
+                        bool weighted = false);
 // final: the last U-step of a block, which also forms g = diag(U^T Q) for
-// the scale solve.
+// the scale solve.  v_partials: the preceding V-step was launched weighted
+// (its partials of V^T diag(h~) V are in place); else they are formed here.
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
-                        Timer* t = nullptr);
+                        Timer* t = nullptr, bool v_partials = false);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
 // The end of a block: scale solve, row-major factor copies, packed B and C, D.
 // revisit: the scales were settled by launch_revisit_decide, whose decision

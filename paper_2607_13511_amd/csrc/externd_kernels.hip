@@ -994,6 +994,137 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   }
 }
 
+// ---------------------------------------------------------------------------
+// Weighted V-step thresholding by row blocks (Sec. 2.5): V <- T_tau(Y^T) for
+// every component over rows [r0, r0 + rows_wg), so that the workgroup holds
+// whole rows of V and adds its share of the weighted Gram V^T diag(h~) V
+// into partw[blockIdx.x] (the k_vprep_w arithmetic: fp64 MFMA, exact
+// products, fixed order); the U-step's side workgroups add the partials.
+// Every workgroup forms the 64 thresholds of Eq. (2) from the per-tile
+// statistics: four threads per component take every fourth tile, combined
+// in a fixed order.  Writes Vt (component-major) and Vmf.
+// grid: ceil(n_pad / rows_wg) <= VPREP_MAX_WG; rows_wg a multiple of 32,
+// at most VPREP_CHUNK.
+// ---------------------------------------------------------------------------
+constexpr int TVW_TS = 40;  // statistics tiles per thread and round
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_tern_vw(
+    const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb, double tau, const double* __restrict__ ps,
+    const double* __restrict__ pm, const int* __restrict__ pi, int ntile, int8_t* __restrict__ Vt,
+    int8_t* __restrict__ Vmf, const double* __restrict__ hw, int rows_wg, double* __restrict__ partw) {
+  __shared__ int8_t tile[VPREP_CHUNK][BBP + 4];
+  __shared__ double hws[VPREP_CHUNK];
+  const int tid = threadIdx.x;
+  const int c = tid >> 2, sub = tid & 3;
+  const int64_t r0 = (int64_t)blockIdx.x * rows_wg;
+  const int nr = (int)(n_pad - r0 < rows_wg ? n_pad - r0 : rows_wg);  // a multiple of 32
+  if (tid < nr) hws[tid] = hw[r0 + tid];
+  // rows r0 + sub * rpt .. + rpt of component c, eight at a time (Vt and
+  // Vmf take them as 8 contiguous bytes); the first eight are loaded before
+  // the statistics, which do not depend on them
+  const int rpt = nr >> 2;  // a multiple of 8
+  const double* yc = Y + (int64_t)c * n_pad;
+  double y[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) y[k] = yc[r0 + sub * rpt + k];
+  // threshold of component c: sum and max of |y| over its tiles
+  const double* psc = ps + (int64_t)c * ntile;
+  const double* pmc = pm + (int64_t)c * ntile;
+  const int* pic = pi + (int64_t)c * ntile;
+  double S = 0.0, M = -1.0;
+  for (int t0 = 0; t0 < ntile; t0 += 4 * TVW_TS) {
+    double a[TVW_TS], b[TVW_TS];
+#pragma unroll
+    for (int u = 0; u < TVW_TS; ++u) {
+      const int t = t0 + sub + 4 * u, tc = t < ntile ? t : 0;
+      a[u] = psc[tc];
+      b[u] = pmc[tc];
+    }
+#pragma unroll
+    for (int u = 0; u < TVW_TS; ++u)
+      if (t0 + sub + 4 * u < ntile) {
+        S += a[u];
+        M = fmax(M, b[u]);
+      }
+  }
+  S += __shfl_xor(S, 1, 64);
+  S += __shfl_xor(S, 2, 64);
+  M = fmax(M, __shfl_xor(M, 1, 64));
+  M = fmax(M, __shfl_xor(M, 2, 64));
+  const double theta = tau * (S / (double)n);
+  const bool zero = c >= bb;
+  const bool keep_max = !(M > theta);
+  int mi = 0x7fffffff;
+  if (keep_max && !zero) {
+    // the smallest index attaining the maximum: the smallest tile argmax
+    // among the tiles whose maximum is M (the four lanes of c agree)
+    for (int t = sub; t < ntile; t += 4)
+      if (pmc[t] == M) mi = min(mi, pic[t]);
+    mi = min(mi, __shfl_xor(mi, 1, 64));
+    mi = min(mi, __shfl_xor(mi, 2, 64));
+  }
+  for (int k0 = 0; k0 < rpt; k0 += 8) {
+    const int64_t j0 = r0 + sub * rpt + k0;
+    if (k0) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) y[k] = yc[j0 + k];
+    }
+    unsigned long long packed = 0ull;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int64_t j = j0 + k;
+      const double yv = y[k];
+      const bool on = !zero && j < n && (keep_max ? (j == mi) : (fabs(yv) > theta));
+      const int8_t t = on ? ((yv > 0.0) ? 1 : ((yv < 0.0) ? -1 : 0)) : 0;
+      tile[j - r0][c] = t;
+      packed |= (unsigned long long)(uint8_t)t << (8 * k);
+    }
+    *(unsigned long long*)(Vt + (int64_t)c * n_pad + j0) = packed;
+    *(unsigned long long*)(Vmf + mf_offset(c, j0)) = packed;
+  }
+  __syncthreads();
+  const int lane = lane_id(), wave = wave_id();
+  const int i16 = lane & 15, kq = lane >> 4;
+  v4d acc[3] = {v4d{}, v4d{}, v4d{}};
+  switch (wave) {
+    case 0: vprep_gram_chunk<0>(tile, hws, nr, i16, kq, acc); break;
+    case 1: vprep_gram_chunk<1>(tile, hws, nr, i16, kq, acc); break;
+    case 2: vprep_gram_chunk<2>(tile, hws, nr, i16, kq, acc); break;
+    default: vprep_gram_chunk<3>(tile, hws, nr, i16, kq, acc); break;
+  }
+  double* mine = partw + (int64_t)blockIdx.x * (BBP * BBP);
+  switch (wave) {
+    case 0: vprep_gram_store<0>(mine, i16, kq, acc); break;
+    case 1: vprep_gram_store<1>(mine, i16, kq, acc); break;
+    case 2: vprep_gram_store<2>(mine, i16, kq, acc); break;
+    default: vprep_gram_store<3>(mine, i16, kq, acc); break;
+  }
+}
+
+// One entry of the weighted Gram from nwg partials, in the order of
+// k_gramw_sum: partials q, q + 4, ... per quarter q, then the quarters in
+// order.
+__device__ __forceinline__ double gramw_entry(const double* __restrict__ partw, int nwg, int e) {
+  double qs[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    double sum = 0.0;
+    const int nk = (nwg - q + 3) / 4;
+    for (int k0 = 0; k0 < nk; k0 += 8) {
+      double v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int g = q + 4 * (k0 + u);
+        v[u] = partw[(int64_t)(g < nwg ? g : 0) * (BBP * BBP) + e];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (k0 + u < nk) sum += v[u];
+    }
+    qs[q] = sum;
+  }
+  return ((qs[0] + qs[1]) + qs[2]) + qs[3];
+}
+
 // The weighted Gram from the partials of k_vprep_w, added in a fixed order
 // (workgroups q, q + 4, ... per quarter q, then the quarters in order), both
 // triangles into gramV.  Workgroup b takes the 64 entries [64 b, 64 b + 64).
@@ -1051,7 +1182,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                               const int8_t* __restrict__ Vr, const double* __restrict__ hw,
                                               double* __restrict__ Q, float* __restrict__ rowb,
                                               int64_t m_pad, int64_t n_pad, int bb, int* gacc, unsigned* counter,
-                                              double* ginvV, double* gramV, int nside, int rows) {
+                                              double* ginvV, double* gramV, int nside, int rows,
+                                              const double* __restrict__ partw, int nwg) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[USTEP_SMEM_LL];
@@ -1061,8 +1193,32 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     double* Gs = (double*)(smem + 2048);
     double* pbuf = Gs + 4096;
     if (WEIGHTED) {
-      // one side workgroup: V^T H V was formed by k_vprep_w / k_gramw_sum
-      for (int e = threadIdx.x; e < 4096; e += NT) Gs[e] = gramV[e];
+      // V^T H V from the nwg partials of the V thresholding (k_tern_vw) or
+      // k_vprep_w: side workgroup b adds the entries [256 b, 256 b + 256) of
+      // the upper triangle (nside * NT = 4096) and writes both triangles of
+      // gramV through to the device-coherent level; the last to arrive takes
+      // the Gram back, adds the ridge and inverts.
+      const int e = (int)blockIdx.x * NT + threadIdx.x, r = e >> 6, cc = e & 63;
+      if (r <= cc) {
+        const double d = gramw_entry(partw, nwg, e);
+        store_coherent(gramV + e, d);
+        store_coherent(gramV + cc * BBP + r, d);
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have been performed
+      __shared__ int s_last;
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        const unsigned old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = (old == (unsigned)(nside - 1));
+      }
+      __syncthreads();
+      if (!s_last) return;
+      if (threadIdx.x == 0) store_coherent(counter, 0u);
+      double v[4096 / NT];
+#pragma unroll
+      for (int j = 0; j < 4096 / NT; ++j) v[j] = load_coherent(gramV + threadIdx.x + NT * j);
+#pragma unroll
+      for (int j = 0; j < 4096 / NT; ++j) Gs[threadIdx.x + NT * j] = v[j];
       __syncthreads();
       ridge_invert_store(Gs, pbuf, bb, ginvV);
       return;
@@ -2676,7 +2832,19 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
+// Rows per weighted-Gram partial: a multiple of 32, at least 32, at most
+// VPREP_MAX_WG partials.
+static void gram_w_geometry(const Ws& w, int64_t& rows_wg, int& nwg) {
+  rows_wg = (w.n_pad + VPREP_MAX_WG - 1) / VPREP_MAX_WG;
+  rows_wg = rows_wg < VPREP_MIN_ROWS ? VPREP_MIN_ROWS : (rows_wg + TILE - 1) / TILE * TILE;
+  nwg = (int)((w.n_pad + rows_wg - 1) / rows_wg);
+}
+
+// The weighted V-step thresholds V by row blocks (k_tern_vw) when a block
+// fits one staged chunk, i.e. n_pad <= VPREP_MAX_WG * VPREP_CHUNK.
+static bool tern_vw_fits(const Ws& w) { return w.n_pad <= (int64_t)VPREP_MAX_WG * VPREP_CHUNK; }
+
+hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm, bool weighted) {
   const unsigned grid = (unsigned)(NSIDE_GRAM + (w.n_pad / TILE) * w.gv);
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, (const int*)w.cshift, w.m_pad,
                                    w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM);
@@ -2687,6 +2855,17 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
                        w.tpi);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (weighted && tern_vw_fits(w)) {
+    // V by row blocks, with the partials of V^T H V for the U-step
+    int64_t rows_wg;
+    int nwg;
+    gram_w_geometry(w, rows_wg, nwg);
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_vw, dim3((unsigned)nwg), dim3(NT), 0, s,
+                         (const double*)w.Y, w.n, w.n_pad, bb, tau, (const double*)w.tps, (const double*)w.tpm,
+                         (const int*)w.tpi, (int)(w.n_pad / 16), w.Vt, w.Vmf, (const double*)w.hw, (int)rows_wg,
+                         w.partw);
+    return hipGetLastError();
+  }
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, (const double*)w.Y, w.n,
                        w.n_pad, bb, tau, (const double*)w.tps, (const double*)w.tpm, (const int*)w.tpi,
                        (int)(w.n_pad / 16), w.nsv, w.Vt, w.Vmf);
@@ -2694,12 +2873,11 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
 }
 
 // Weighted: V row-major and the raw weighted Gram V^T diag(h~) V into
-// gramV, before the U-step launch.
+// gramV (the step entry point of the scale solve).
 hipError_t launch_gram_w(const Ws& w, hipStream_t s) {
-  // rows per preparation workgroup: a multiple of 32, at least 32, at most VPREP_MAX_WG workgroups
-  int64_t rows_wg = (w.n_pad + VPREP_MAX_WG - 1) / VPREP_MAX_WG;
-  rows_wg = rows_wg < VPREP_MIN_ROWS ? VPREP_MIN_ROWS : (rows_wg + TILE - 1) / TILE * TILE;
-  const int nwg = (int)((w.n_pad + rows_wg - 1) / rows_wg);
+  int64_t rows_wg;
+  int nwg;
+  gram_w_geometry(w, rows_wg, nwg);
   hipLaunchKernelGGL(k_vprep_w, dim3((unsigned)nwg), dim3(NT), 0, s, (const int8_t*)w.Vt, w.Vr, w.n_pad,
                      (const double*)w.hw, (int)rows_wg, w.partw);
   hipError_t e = hipGetLastError();
@@ -2709,20 +2887,32 @@ hipError_t launch_gram_w(const Ws& w, hipStream_t s) {
 }
 
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
-                        Timer* tm) {
+                        Timer* tm, bool v_partials) {
   hipError_t e;
-  const unsigned nside = weighted ? 1 : NSIDE_GRAM;
+  const unsigned nside = NSIDE_GRAM;
   const unsigned grid = (unsigned)(nside + w.ntu);
   if (weighted) {
-    e = launch_gram_w(w, s);
-    if (e != hipSuccess) return e;
+    // the side workgroups add the partials of V^T H V: left by the V-step's
+    // row-block thresholding, or formed here from the given V
+    static_assert(NSIDE_GRAM * NT == BBP * BBP, "one weighted-Gram entry per side thread");
+    int64_t rows_wg;
+    int nwg;
+    gram_w_geometry(w, rows_wg, nwg);
+    if (!(v_partials && tern_vw_fits(w))) {
+      hipLaunchKernelGGL(k_vprep_w, dim3((unsigned)nwg), dim3(NT), 0, s, (const int8_t*)w.Vt, w.Vr, w.n_pad,
+                         (const double*)w.hw, (int)rows_wg, w.partw);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.rowb, w.m_pad, w.n_pad, bb, w.gacc + 4096,
-                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows);
+                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows,
+                                     (const double*)w.partw, nwg);
   } else {
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.rowb, w.m_pad, w.n_pad, bb, w.gacc + 4096,
-                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows);
+                                     w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows,
+                                     (const double*)nullptr, 0);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
