@@ -47,6 +47,11 @@ def workload(name: str):
         return synth.down9728(weighted=False)
     if name == "down9728_imatrix":
         return synth.down9728(weighted=True)
+    if name in ("down9728_b256", "down9728_b256_imatrix"):
+        # the same matrix at the paper's default block width (Sec. 2.4)
+        import dataclasses
+        w = synth.down9728(weighted=name.endswith("_imatrix"))
+        return dataclasses.replace(w, name=w.name.replace("_b64", "_b256"), block=256)
     if name == "attn2048":
         return synth.attn2048()
     if name == "gauss256":

@@ -56,10 +56,14 @@ extern "C" {
 #define EXTERND_ESCRATCH     -7  /* the call needs more than the fixed device scratch of
                                     an allocation-free entry point                       */
 
-/* Largest effective block width the kernels handle.  A call whose
+/* Largest effective block width the kernels handle (four quarters of 64
+ * components; the paper's default b = 256, Sec. 2.4).  A call whose
  * effective width (externd_effective_block) exceeds it returns
- * EXTERND_EUNSUPPORTED before any device work; nothing is clamped.       */
-#define EXTERND_MAX_BLOCK 64
+ * EXTERND_EUNSUPPORTED before any device work; nothing is clamped.
+ * Effective widths above 64 run the block as quarters coupled through
+ * their Gram inverses and the joint solve; refinement sweeps and the
+ * safeguard accept effective widths up to 64 only.                      */
+#define EXTERND_MAX_BLOCK 256
 
 /* Ridge of the decorrelated targets, Eq. (3): eps = EXTERND_RIDGE_REL *
  * trace(G) / bb for each Gram matrix G of a block of bb components.      */
@@ -83,9 +87,11 @@ int32_t externd_effective_block(int64_t m, int64_t n, int32_t block);
 
 /* Device workspace, in bytes, for an m x n matrix and inner rank k:
  * k = externd_rank(m, n, mu) for externd_factorize, k = 0 for the step
- * entry points.  Independent of block and of whether weights are given.
- * Dominated by one fp32 copy of the residual (4 m n bytes).  0 on invalid
- * arguments or unsupported shapes.                                       */
+ * entry points.  Independent of block and of whether weights are given:
+ * sized for blocks of EXTERND_MAX_BLOCK components, 4 m n bytes for the
+ * fp32 residual plus about 5.5 kB per row and (2 + 2 gv) kB per column
+ * (gv <= 8 row groups of the V-step's partial contractions) and under
+ * 16 MB of fixed buffers.  0 on invalid arguments or unsupported shapes. */
 size_t externd_workspace_bytes(int64_t m, int64_t n, int64_t k);
 
 /*
@@ -99,10 +105,8 @@ size_t externd_workspace_bytes(int64_t m, int64_t n, int64_t k);
  *  tau        threshold scale of T_tau, Eq. (2); finite, >= 0.
  *  block      requested block width b >= 1 (see externd_effective_block;
  *             block = 1 is the sequential algorithm of Sec. 2.3).  An
- *             effective width above EXTERND_MAX_BLOCK is
- *             EXTERND_EUNSUPPORTED (the paper's default b = 256 runs only
- *             where its cap floor(min(m, n) / 8) brings it to 64 or less,
- *             i.e. min(m, n) < 520).
+ *             effective width above EXTERND_MAX_BLOCK (256) is
+ *             EXTERND_EUNSUPPORTED.
  *  iters      ALS iterations per block, >= 1; one iteration is a V-step
  *             followed by a U-step (Sec. 2.3 order).
  *  importance device fp32[n] per-column weights h (finite, >= 0, max > 0),
@@ -312,7 +316,7 @@ int externd_factorize_timed(const float* A, int64_t m, int64_t n, double mu, dou
  * Step entry points: one step each of the block ALS on caller-given state,
  * for per-step parity checks.  They share the kernels of
  * externd_factorize.  Block matrices are row-major with bb columns:
- * U is m x bb int8 in {-1,0,1}, V is n x bb int8.  1 <= bb <= 64.
+ * U is m x bb int8 in {-1,0,1}, V is n x bb int8.  1 <= bb <= EXTERND_MAX_BLOCK.
  * Every pointer except `h` / `*_or_null` outputs is required.  These calls
  * are asynchronous on `stream`.
  */

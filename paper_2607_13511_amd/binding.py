@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libexternd.so")
 
 OK, EINVAL, ENONFINITE, EWORKSPACE, EHIP, EUNSUPPORTED, ESYNC, ESCRATCH = 0, -1, -2, -3, -4, -5, -6, -7
 APPLY_NOALLOC_MAX_BYTES = 2 << 20   # EXTERND_APPLY_NOALLOC_MAX_BYTES
-MAX_BLOCK = 64
+MAX_BLOCK = 256
 
 _lib = None
 

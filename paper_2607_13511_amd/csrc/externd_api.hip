@@ -23,7 +23,7 @@ struct Layout {
   int64_t m_pad, n_pad;
   int gv, gd, nblk_cap;
   int urows, ntu, nsu, nsv;
-  size_t off[40];
+  size_t off[48];
   size_t total;
 };
 
@@ -50,14 +50,14 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   const int64_t ntmax = nrt > 2 * nct ? nrt : 2 * nct;
   const size_t sizes[] = {
       sizeof(float) * (size_t)(L.m_pad * L.n_pad),     // 0 R
-      (size_t)(BBP * L.m_pad),                         // 1 Ut
-      (size_t)(BBP * L.m_pad),                         // 2 Ur
-      (size_t)(BBP * L.n_pad),                         // 3 Vt
-      (size_t)(BBP * L.n_pad),                         // 4 Vr
-      sizeof(double) * (size_t)(BBP * L.m_pad),        // 5 Q
-      sizeof(double) * (size_t)(BBP * L.m_pad),        // 6 Z
-      sizeof(long long) * (size_t)(L.gv * BBP * L.n_pad),  // 7 Pp
-      sizeof(double) * (size_t)(BBP * L.n_pad),        // 8 Y
+      (size_t)(BMAX * L.m_pad),                        // 1 Ut
+      (size_t)(BMAX * L.m_pad),                        // 2 Ur
+      (size_t)(BMAX * L.n_pad),                        // 3 Vt
+      (size_t)(BMAX * L.n_pad),                        // 4 Vr
+      sizeof(double) * (size_t)(BMAX * L.m_pad),       // 5 Q
+      sizeof(double) * (size_t)(BMAX * L.m_pad),       // 6 Z
+      sizeof(long long) * (size_t)(L.gv * BMAX * L.n_pad),  // 7 Pp
+      sizeof(double) * (size_t)(BMAX * L.n_pad),       // 8 Y
       sizeof(double) * 4096,                           // 9 ginvU
       sizeof(double) * 4096,                           // 10 ginvV
       sizeof(double) * 4096,                           // 11 gramV
@@ -65,27 +65,36 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(int) * 4096 * NSIDE_MAX,                  // 13 gparti
       sizeof(double) * (size_t)(L.gd * L.n_pad),       // 14 colE_part
       sizeof(double) * (size_t)L.n_pad,                // 15 hw
-      sizeof(double) * BBP * TERN_SPLIT_MAX,           // 16 gvec
-      sizeof(double) * BBP,                            // 17 dvec
-      sizeof(float) * BBP,                             // 18 dF
-      sizeof(int) * BBP,                               // 19 J
+      sizeof(double) * BMAX * TERN_SPLIT_MAX,          // 16 gvec
+      sizeof(double) * BMAX,                           // 17 dvec
+      sizeof(float) * BMAX,                            // 18 dF
+      sizeof(int) * BMAX,                              // 19 J
       sizeof(float) * (size_t)L.m_pad,                 // 20 rowb
       sizeof(double) * (size_t)L.nblk_cap,             // 21 fro2_hist
       sizeof(double) * (size_t)L.nblk_cap,             // 22 fro2w_hist
       sizeof(unsigned) * CNT_COUNT,                    // 23 counters
       sizeof(int) * FLAG_COUNT,                        // 24 flags
       sizeof(float) * (size_t)(nct * L.m_pad),         // 25 rowb_part
-      (size_t)(BBP * L.m_pad),                         // 26 Umf
-      (size_t)(BBP * L.n_pad),                         // 27 Vmf
-      sizeof(double) * (size_t)(BBP * ntmax),          // 28 tps
-      sizeof(double) * (size_t)(BBP * ntmax),          // 29 tpm
-      sizeof(int) * (size_t)(BBP * ntmax),             // 30 tpi
-      sizeof(unsigned short) * (size_t)(BBP * L.m_pad),  // 31 Ub
+      (size_t)(BMAX * L.m_pad),                        // 26 Umf
+      (size_t)(BMAX * L.n_pad),                        // 27 Vmf
+      sizeof(double) * (size_t)(BMAX * ntmax),         // 28 tps
+      sizeof(double) * (size_t)(BMAX * ntmax),         // 29 tpm
+      sizeof(int) * (size_t)(BMAX * ntmax),            // 30 tpi
+      sizeof(unsigned short) * (size_t)(BMAX * L.m_pad),  // 31 Ub
       sizeof(unsigned long long) * (size_t)L.nblk_cap, // 32 argkey
       sizeof(int) * 2 * 4096,                          // 33 gacc
       sizeof(double) * 4096 * VPREP_MAX_WG,            // 34 partw
       sizeof(double),                                  // 35 hwmax
       sizeof(int) * (size_t)L.n_pad,                   // 36 cshift
+      sizeof(int) * 4096 * NPAIR_MAX,                  // 37 gaccW
+      sizeof(double) * BMAX * BMAX,                    // 38 gramVW
+      sizeof(double) * BMAX * BMAX,                    // 39 wA0
+      sizeof(double) * BMAX * BMAX,                    // 40 wA1
+      sizeof(double) * 4096,                           // 41 wPinv
+      sizeof(double) * BMAX * BMAX,                    // 42 ginvUW
+      sizeof(double) * BMAX * BMAX,                    // 43 ginvVW
+      sizeof(double) * 4096 * NPAIR_MAX * GW_SLABS,    // 44 partwW
+      sizeof(int) * 64,                                // 45 wflag
   };
   size_t o = 0;
   for (size_t i = 0; i < sizeof(sizes) / sizeof(sizes[0]); ++i) {
@@ -149,7 +158,42 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.partw = (double*)(b + L.off[34]);
   w.hwmax = (double*)(b + L.off[35]);
   w.cshift = (int*)(b + L.off[36]);
+  w.gaccW = (int*)(b + L.off[37]);
+  w.gramVW = (double*)(b + L.off[38]);
+  w.wA0 = (double*)(b + L.off[39]);
+  w.wA1 = (double*)(b + L.off[40]);
+  w.wPinv = (double*)(b + L.off[41]);
+  w.ginvUW = (double*)(b + L.off[42]);
+  w.ginvVW = (double*)(b + L.off[43]);
+  w.partwW = (double*)(b + L.off[44]);
+  w.wflag = (int*)(b + L.off[45]);
+  const int64_t nrt = L.m_pad / TILE, nct = L.n_pad / TILE;
+  w.ntmax = nrt > 2 * nct ? nrt : 2 * nct;
   return true;
+}
+
+Ws quarter_view(const Ws& w, int q) {
+  Ws v = w;
+  const int64_t c0 = (int64_t)BBP * q;
+  v.Ut = w.Ut + c0 * w.m_pad;
+  v.Ur = w.Ur + c0 * w.m_pad;
+  v.Ub = w.Ub + c0 * w.m_pad;
+  v.Umf = w.Umf + c0 * w.m_pad;
+  v.Q = w.Q + c0 * w.m_pad;
+  v.Z = w.Z + c0 * w.m_pad;
+  v.Vt = w.Vt + c0 * w.n_pad;
+  v.Vr = w.Vr + c0 * w.n_pad;
+  v.Vmf = w.Vmf + c0 * w.n_pad;
+  v.Y = w.Y + c0 * w.n_pad;
+  v.Pp = w.Pp + c0 * w.gv * w.n_pad;
+  v.tps = w.tps + c0 * w.ntmax;
+  v.tpm = w.tpm + c0 * w.ntmax;
+  v.tpi = w.tpi + c0 * w.ntmax;
+  v.gvec = w.gvec + c0 * TERN_SPLIT_MAX;
+  v.dvec = w.dvec + c0;
+  v.dF = w.dF + c0;
+  v.J = w.J + c0;
+  return v;
 }
 
 hipError_t Timer::take(int cls, hipEvent_t* a, hipEvent_t* b) {
@@ -342,8 +386,11 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
   if (k < 1) return EXTERND_EINVAL;
   if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
   const int b_eff = externd_effective_block(m, n, block);
-  // the kernels hold at most EXTERND_MAX_BLOCK components of a block
+  // the kernels hold at most EXTERND_MAX_BLOCK components of a block; wide
+  // blocks (more than 64) run without refinement sweeps and the safeguard
   if (b_eff > EXTERND_MAX_BLOCK) return EXTERND_EUNSUPPORTED;
+  const bool wide = b_eff > BBP;
+  if (wide && (sweeps > 0 || safeguard)) return EXTERND_EUNSUPPORTED;
   const int64_t nblk = (k + b_eff - 1) / b_eff;
   Ws w{};
   if (!carve(w, workspace, workspace_bytes, m, n, k)) return EXTERND_EWORKSPACE;
@@ -384,15 +431,26 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
       const int64_t c0 = blk * b_eff;
       const int bb = (int)((k - c0) < b_eff ? (k - c0) : b_eff);
       HIP_TRY(launch_select(w, (int)blk, bb, s));
-      HIP_TRY(launch_init(w, bb, tau, s));
-      for (int it = 0; it < iters; ++it) {
-        HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm, weighted));
-        HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm, weighted));
+      if (bb > BBP) {
+        // a wide block: its quarters coupled through the Gram inverses
+        HIP_TRY(launch_init_wide(w, bb, tau, s));
+        for (int it = 0; it < iters; ++it) {
+          HIP_TRY(launch_vstep_wide(w, (int)blk, bb, tau, s, tm));
+          HIP_TRY(launch_ustep_wide(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm));
+        }
+        HIP_TRY(launch_block_out_wide(w, c0, bb, k, B_packed, C_packed, D, s));
+        HIP_TRY(launch_deflate_wide(w, (int)blk, bb, false, s, tm));
+      } else {
+        HIP_TRY(launch_init(w, bb, tau, s));
+        for (int it = 0; it < iters; ++it) {
+          HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm, weighted));
+          HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm, weighted));
+        }
+        HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
+        if (safeguard) HIP_TRY(launch_safeguard(w, (int)blk, bb, D + c0, s));
+        HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s, false, safeguard));
+        HIP_TRY(launch_deflate(w, (int)blk, false, s, tm, safeguard));
       }
-      HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
-      if (safeguard) HIP_TRY(launch_safeguard(w, (int)blk, bb, D + c0, s));
-      HIP_TRY(launch_block_out(w, c0, bb, k, B_packed, C_packed, D, s, false, safeguard));
-      HIP_TRY(launch_deflate(w, (int)blk, false, s, tm, safeguard));
       if (stop_at_target && blk + 1 < nblk) {
         // energy after this block (||R||^2 history entries 0 and blk + 1)
         HIP_TRY(launch_finish(w, (int)blk + 1, s));
@@ -509,8 +567,23 @@ int externd_factorize_timed(const float* A, int64_t m, int64_t n, double mu, dou
 // ---------------------------------------------------------------------------
 // step entry points
 // ---------------------------------------------------------------------------
+// A caller's factor (len x bb int8, row-major) into the component-major,
+// row-major and MFMA-ready copies of U (which = 0) or V (which = 1), one
+// quarter of 64 components at a time.
+static hipError_t load_factor_quarters(const Ws& w, int which, const int8_t* X, int64_t len, int32_t bb,
+                                       hipStream_t s) {
+  for (int q = 0; q * BBP < bb; ++q) {
+    const Ws v = quarter_view(w, q);
+    const int bq = bb - BBP * q < BBP ? bb - BBP * q : BBP;
+    const hipError_t e = which ? launch_load_factor(v.Vt, v.Vr, v.Vmf, X + BBP * q, len, w.n_pad, bq, s, bb)
+                               : launch_load_factor(v.Ut, v.Ur, v.Umf, X + BBP * q, len, w.m_pad, bq, s, bb);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 static int step_prologue(Ws& w, const float* R, int64_t m, int64_t n, int32_t bb, void* ws, size_t ws_bytes) {
-  if (!R || !ws || m < 1 || n < 1 || bb < 1 || bb > BBP) return EXTERND_EINVAL;
+  if (!R || !ws || m < 1 || n < 1 || bb < 1 || bb > BMAX) return EXTERND_EINVAL;
   if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
   if (!carve(w, ws, ws_bytes, m, n, 0)) return EXTERND_EWORKSPACE;
   return EXTERND_OK;
@@ -526,7 +599,7 @@ int externd_step_init(const float* R, int64_t m, int64_t n, const float* h, int3
   HIP_TRY(launch_prep(w, h, s));
   HIP_TRY(launch_stage(w, R, n, s));
   HIP_TRY(launch_select(w, 0, bb, s));
-  HIP_TRY(launch_init(w, bb, tau, s));
+  HIP_TRY(bb > BBP ? launch_init_wide(w, bb, tau, s) : launch_init(w, bb, tau, s));
   HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
   HIP_TRY(hipMemcpyAsync(J_out, w.J, sizeof(int32_t) * bb, hipMemcpyDeviceToDevice, s));
   return EXTERND_OK;
@@ -542,8 +615,8 @@ int externd_step_vstep(const float* R, int64_t m, int64_t n, const int8_t* U, in
   HIP_TRY(launch_prep(w, nullptr, s));
   HIP_TRY(launch_stage(w, R, n, s));
   HIP_TRY(launch_finish(w, 0, s));  // column energies -> the V-step's per-column exponents
-  HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
-  HIP_TRY(launch_vstep(w, 0, bb, tau, s));
+  HIP_TRY(load_factor_quarters(w, 0, U, m, bb, s));
+  HIP_TRY(bb > BBP ? launch_vstep_wide(w, 0, bb, tau, s) : launch_vstep(w, 0, bb, tau, s));
   HIP_TRY(launch_store_factor(V_out, w.Vt, n, w.n_pad, bb, s));
   if (Y_out_or_null) {
     // Y is bb x n: row c of the component-major buffer, pitch n_pad -> n
@@ -563,8 +636,9 @@ int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, in
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(launch_prep(w, h, s));
   HIP_TRY(launch_stage(w, R, n, s));
-  HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
-  HIP_TRY(launch_ustep(w, 0, bb, tau, h != nullptr, false, s));
+  HIP_TRY(load_factor_quarters(w, 1, V, n, bb, s));
+  HIP_TRY(bb > BBP ? launch_ustep_wide(w, 0, bb, tau, h != nullptr, false, s)
+                   : launch_ustep(w, 0, bb, tau, h != nullptr, false, s));
   HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
   if (Q_out_or_null) HIP_TRY(launch_store_cm(Q_out_or_null, w.Q, m, w.m_pad, bb, s));
   if (Z_out_or_null) HIP_TRY(launch_store_cm(Z_out_or_null, w.Z, m, w.m_pad, bb, s));
@@ -573,19 +647,24 @@ int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, in
 
 int externd_step_scale(const int8_t* U, const int8_t* V, const double* Q, int64_t m, int64_t n, int32_t bb,
                        const float* h, double* d_out, void* ws, size_t ws_bytes, void* stream) {
-  if (!U || !V || !Q || !d_out || !ws || m < 1 || n < 1 || bb < 1 || bb > BBP) return EXTERND_EINVAL;
+  if (!U || !V || !Q || !d_out || !ws || m < 1 || n < 1 || bb < 1 || bb > BMAX) return EXTERND_EINVAL;
   if (!shape_ok(m, n)) return EXTERND_EUNSUPPORTED;
   Ws w{};
   if (!carve(w, ws, ws_bytes, m, n, 0)) return EXTERND_EWORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(launch_prep(w, h, s));
-  HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
-  HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
+  HIP_TRY(load_factor_quarters(w, 0, U, m, bb, s));
+  HIP_TRY(load_factor_quarters(w, 1, V, n, bb, s));
   HIP_TRY(launch_load_cm(w.Q, Q, m, w.m_pad, bb, s));
-  HIP_TRY(launch_gram_only(w, bb, h != nullptr, s));
-  HIP_TRY(launch_gram_acc(w, 0, s));
   HIP_TRY(launch_gvec(w, bb, s));
-  HIP_TRY(launch_scale(w, bb, s));
+  if (bb > BBP) {
+    HIP_TRY(launch_gram_wide_raw(w, bb, h != nullptr, s));  // raw V^T H V
+    HIP_TRY(launch_scale_wide(w, bb, nullptr, s));
+  } else {
+    HIP_TRY(launch_gram_only(w, bb, h != nullptr, s));
+    HIP_TRY(launch_gram_acc(w, 0, s));
+    HIP_TRY(launch_scale(w, bb, s));
+  }
   HIP_TRY(hipMemcpyAsync(d_out, w.dvec, sizeof(double) * bb, hipMemcpyDeviceToDevice, s));
   return EXTERND_OK;
 }
@@ -600,10 +679,10 @@ int externd_step_deflate(float* R, int64_t m, int64_t n, const int8_t* U, const 
   hipStream_t s = (hipStream_t)stream;
   HIP_TRY(launch_prep(w, nullptr, s));
   HIP_TRY(launch_stage(w, R, n, s));
-  HIP_TRY(launch_load_factor(w.Ut, w.Ur, w.Umf, U, m, w.m_pad, bb, s));
-  HIP_TRY(launch_load_factor(w.Vt, w.Vr, w.Vmf, V, n, w.n_pad, bb, s));
+  HIP_TRY(load_factor_quarters(w, 0, U, m, bb, s));
+  HIP_TRY(load_factor_quarters(w, 1, V, n, bb, s));
   HIP_TRY(launch_set_scales(w, d, bb, s));
-  HIP_TRY(launch_deflate(w, 0, true, s));
+  HIP_TRY(bb > BBP ? launch_deflate_wide(w, 0, bb, true, s) : launch_deflate(w, 0, true, s));
   HIP_TRY(launch_unstage(w, R, s));
   if (colnorm2_out || fro2_out) HIP_TRY(launch_colnorms(w, 0, colnorm2_out, fro2_out, s));
   return EXTERND_OK;

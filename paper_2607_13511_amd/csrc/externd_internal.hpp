@@ -15,6 +15,16 @@ namespace externd {
 // are padded to multiples of TILE (zero padding, never touched by updates).
 constexpr int BBP = 64;
 constexpr int TILE = 32;
+// Wide blocks (Sec. 2.4 allows b up to min(m, n) / 8; the paper's default is
+// 256): up to NQMAX quarters of BBP components.  Every per-component buffer
+// holds BMAX components, quarter q at component 64 q; the kernels above run
+// per quarter on a view of the workspace (quarter_view), and the coupling
+// between quarters (the Gram matrices of Eq. (3), the joint solve of
+// Eq. (4)) runs on BMAX x BMAX fp64 matrices in blocks of 64.
+constexpr int NQMAX = 4;
+constexpr int BMAX = NQMAX * BBP;
+constexpr int NPAIR_MAX = NQMAX * (NQMAX + 1) / 2;  // quarter pairs q <= q'
+constexpr int GW_SLABS = 16;                          // row slabs of the wide weighted Gram
 // Workgroups that build integer Gram matrices (int8 MFMA), beside a
 // contraction or in a launch of their own.
 constexpr int NSIDE_INT = 8;   // integer-Gram workgroups of the scale solve
@@ -57,6 +67,7 @@ struct Ws {
   int gd;                // row groups of the deflation / staging passes
   int urows, ntu;        // U-step: rows per workgroup (<= 32) and number of row groups
   int nsu, nsv;          // ternarization workgroups per U / V component
+  int64_t ntmax;         // statistics tiles per component (the larger of the U and V sides)
 
   float* R;              // m_pad x n_pad residual, fp32, row-major
   int8_t* Ut;            // BBP x m_pad, U transposed (component-major)
@@ -93,11 +104,25 @@ struct Ws {
                          // (written with the energy reduction after staging and each deflation)
   unsigned long long* argkey;  // nblk_cap: (max|R| bits << 32) | (2^32 - 1 - first row-major index), safeguard only
   double* partw;               // VPREP_MAX_WG x 64 x 64: partial weighted Grams V^T diag(h~) V
+  // wide blocks
+  int* gaccW;            // NPAIR_MAX x 4096: integer Gram blocks X_q^T X_q' (q <= q') of a factor
+  double* gramVW;        // BMAX x BMAX raw V^T H V (row-major), for the joint solve
+  double* wA0;           // BMAX x BMAX: the matrix being swept (ping)
+  double* wA1;           // BMAX x BMAX: (pong)
+  double* wPinv;         // 64 x 64: inverse of the current pivot block
+  double* ginvUW;        // NQMAX x NQMAX blocks of 4096 (fp64 MFMA operand order): (U^T U + eps I)^{-1}
+  double* ginvVW;        // the same for (V^T H V + eps I)^{-1}
+  double* partwW;        // NPAIR_MAX x GW_SLABS x 4096: partial weighted Gram blocks
+  int* wflag;            // 1: the swept matrix had zero trace
   double* fro2_hist;     // nblk_cap: ||R||^2 before each block, then after the last
   double* fro2w_hist;    // nblk_cap: weighted ||R||^2
   unsigned* counters;    // CNT_COUNT
   int* flags;            // FLAG_COUNT
 };
+
+// The workspace as seen by one quarter of a wide block: every per-component
+// buffer offset to component 64 q (the shared buffers unchanged).
+Ws quarter_view(const Ws& w, int q);
 
 // Optional per-kernel-class event timing (host side).  begin/end record a
 // pair of events on the stream around one launch; collect() sums the
@@ -161,6 +186,17 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
                         Timer* t = nullptr, bool v_partials = false);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
+// Wide blocks (64 < bb <= BMAX): the same steps over the quarters of the
+// block, coupled through the BMAX x BMAX Gram inverses and joint solve.
+hipError_t launch_init_wide(const Ws& w, int bb, double tau, hipStream_t s);
+hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr);
+hipError_t launch_ustep_wide(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
+                             Timer* t = nullptr);
+hipError_t launch_scale_wide(const Ws& w, int bb, float* D_block, hipStream_t s);
+hipError_t launch_gram_wide_raw(const Ws& w, int bb, bool weighted, hipStream_t s);
+hipError_t launch_block_out_wide(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
+                                 hipStream_t s);
+hipError_t launch_deflate_wide(const Ws& w, int blk, int bb, bool transposes, hipStream_t s, Timer* t = nullptr);
 // The end of a block: scale solve, row-major factor copies, packed B and C, D.
 // revisit: the scales were settled by launch_revisit_decide, whose decision
 // selects the new block (written out) or the old one (operands rebuilt from
@@ -168,7 +204,7 @@ hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
 // safeguard: the scales were settled by launch_safeguard, and a block it
 // replaced is written out as its single entry.
 hipError_t launch_block_out(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
-                            hipStream_t s, bool revisit = false, bool safeguard = false);
+                            hipStream_t s, bool revisit = false, bool safeguard = false, bool solve = true);
 // Joint scale solve of the block before slot blk's residual is deflated,
 // with the single-entry option of Proposition 2 (D_block: D + c0).
 hipError_t launch_safeguard(const Ws& w, int blk, int bb, float* D_block, hipStream_t s);
@@ -188,8 +224,9 @@ hipError_t launch_revisit_load(const Ws& w, const uint8_t* Bp, const uint8_t* Cp
 hipError_t launch_revisit_decide(const Ws& w, int bb, float* D_block, bool weighted, int slot_prev, int slot_added,
                                  hipStream_t s);
 // step-entry helpers
+// X: len x bb int8 with leading dimension ld (0: bb).
 hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len, int64_t len_pad,
-                              int bb, hipStream_t s);
+                              int bb, hipStream_t s, int ld = 0);
 hipError_t launch_store_factor(int8_t* X, const int8_t* Xt, int64_t len, int64_t len_pad, int bb, hipStream_t s);
 hipError_t launch_store_cm(double* X, const double* Xcm, int64_t len, int64_t len_pad, int bb,
                            hipStream_t s);

@@ -846,9 +846,16 @@ __device__ __forceinline__ void vtarget_sum16(const long long* __restrict__ Pp, 
   }
 }
 
+// WIDE (a block of nq > 1 quarters, Sec. 2.4 with b up to BMAX): the
+// quarter's targets Y_q = sum_q' G^{-1}[q][q'] P_q', with ginvU the block
+// row q of the nq x nq blocks (block q' at ginvU + 4096 q') and Pp the
+// partials of quarter 0 (quarter q' at Pp + q' pq_stride); Y, ps, pm, pi are
+// the quarter's.
+template <bool WIDE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vtarget(const long long* __restrict__ Pp, const int* __restrict__ cshift,
                                                 int64_t n_pad, int gv, const double* __restrict__ ginvU,
-                                                double* __restrict__ Y, int64_t n, double* ps, double* pm, int* pi) {
+                                                double* __restrict__ Y, int64_t n, double* ps, double* pm, int* pi,
+                                                int nq, int64_t pq_stride) {
   __shared__ double Ps[64 * 17];
   const int tile = blockIdx.x;
   const int ntile = (int)(n_pad / 16);
@@ -858,23 +865,27 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   // the contraction's exponent of the one column this thread sums
   const int s = cshift[j0 + (threadIdx.x & 15)];
   double a[16];
-  load_ginv(ginvU, a);
-  static_assert(GV_MAX == 8, "one case per group count");
-  switch (gv) {
-    case 1: vtarget_sum16<1>(Pp, s, n_pad, j0, Ps); break;
-    case 2: vtarget_sum16<2>(Pp, s, n_pad, j0, Ps); break;
-    case 3: vtarget_sum16<3>(Pp, s, n_pad, j0, Ps); break;
-    case 4: vtarget_sum16<4>(Pp, s, n_pad, j0, Ps); break;
-    case 5: vtarget_sum16<5>(Pp, s, n_pad, j0, Ps); break;
-    case 6: vtarget_sum16<6>(Pp, s, n_pad, j0, Ps); break;
-    case 7: vtarget_sum16<7>(Pp, s, n_pad, j0, Ps); break;
-    default: vtarget_sum16<8>(Pp, s, n_pad, j0, Ps); break;
-  }
-  __syncthreads();
-  // A = G^{-1}[16 w + li][4 ks + lk] (a), B = P[4 ks + lk][li] (LDS)
   v4d y[2] = {v4d{}, v4d{}};
+  static_assert(GV_MAX == 8, "one case per group count");
+  for (int q2 = 0; q2 < (WIDE ? nq : 1); ++q2) {
+    load_ginv(ginvU + (WIDE ? (int64_t)q2 * 4096 : 0), a);
+    const long long* Pq = Pp + (WIDE ? q2 * pq_stride : 0);
+    if (WIDE && q2 > 0) __syncthreads();  // Ps of the previous quarter consumed
+    switch (gv) {
+      case 1: vtarget_sum16<1>(Pq, s, n_pad, j0, Ps); break;
+      case 2: vtarget_sum16<2>(Pq, s, n_pad, j0, Ps); break;
+      case 3: vtarget_sum16<3>(Pq, s, n_pad, j0, Ps); break;
+      case 4: vtarget_sum16<4>(Pq, s, n_pad, j0, Ps); break;
+      case 5: vtarget_sum16<5>(Pq, s, n_pad, j0, Ps); break;
+      case 6: vtarget_sum16<6>(Pq, s, n_pad, j0, Ps); break;
+      case 7: vtarget_sum16<7>(Pq, s, n_pad, j0, Ps); break;
+      default: vtarget_sum16<8>(Pq, s, n_pad, j0, Ps); break;
+    }
+    __syncthreads();
+    // A = G^{-1}[16 w + li][4 ks + lk] (a), B = P[4 ks + lk][li] (LDS)
 #pragma unroll
-  for (int ks = 0; ks < 16; ++ks) y[0] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 17 + li], y[0]);
+    for (int ks = 0; ks < 16; ++ks) y[0] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 17 + li], y[0]);
+  }
 #pragma unroll
   for (int r = 0; r < 4; ++r) Y[(int64_t)(16 * w + lk + 4 * r) * n_pad + j0 + li] = y[0][r];
   // the second half of the 32-wide statistics tile lies past the limit
@@ -1376,30 +1387,37 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // statistics, after the contraction launch (G_V^{-1} from its side path).
 // grid: m_pad / 32 row tiles (statistics per tile).  Rows past m hold
 // Q = 0 (zero residual padding), so their targets are zero.
+// WIDE: Z_q^T = sum_q' G^{-1}[q][q'] Q_q'^T, with ginvV the block row q
+// (block q' at + 4096 q') and Q the contraction of quarter 0 (quarter q' at
+// Q + q' 64 m_pad); Z, ps, pm, pi are the quarter's.
+template <bool WIDE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_utarget(const double* __restrict__ Q, const double* __restrict__ ginvV,
                                                 double* __restrict__ Z, int64_t m, int64_t m_pad, double* ps,
-                                                double* pm, int* pi) {
+                                                double* pm, int* pi, int nq) {
   const int nrt = (int)(m_pad / TILE);
   const int lane = lane_id(), w = wave_id();
   const int li = lane & 15, lk = lane >> 4;
   double a[16];
-  load_ginv(ginvV, a);
   {
     const int rt = (int)blockIdx.x;
     const int64_t i0 = (int64_t)rt * TILE;
-    // B = Q[4 ks + lk][i0 + li (+16)], straight from memory
-    double b0[16], b1[16];
-#pragma unroll
-    for (int ks = 0; ks < 16; ++ks) {
-      const double* qr = Q + (int64_t)(4 * ks + lk) * m_pad + i0 + li;
-      b0[ks] = qr[0];
-      b1[ks] = qr[16];
-    }
     v4d z[2] = {v4d{}, v4d{}};
+    for (int q2 = 0; q2 < (WIDE ? nq : 1); ++q2) {
+      load_ginv(ginvV + (WIDE ? (int64_t)q2 * 4096 : 0), a);
+      // B = Q[4 ks + lk][i0 + li (+16)], straight from memory
+      const double* Qq = Q + (WIDE ? (int64_t)q2 * BBP * m_pad : 0);
+      double b0[16], b1[16];
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks) {
-      z[0] = mfma_f64(a[ks], b0[ks], z[0]);
-      z[1] = mfma_f64(a[ks], b1[ks], z[1]);
+      for (int ks = 0; ks < 16; ++ks) {
+        const double* qr = Qq + (int64_t)(4 * ks + lk) * m_pad + i0 + li;
+        b0[ks] = qr[0];
+        b1[ks] = qr[16];
+      }
+#pragma unroll
+      for (int ks = 0; ks < 16; ++ks) {
+        z[0] = mfma_f64(a[ks], b0[ks], z[0]);
+        z[1] = mfma_f64(a[ks], b1[ks], z[1]);
+      }
     }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -2016,7 +2034,7 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
                                              double* __restrict__ hw, double* __restrict__ hwmax,
                                              double* fro2_hist, double* fro2w_hist, int nblk_cap,
                                              unsigned* counters, int* flags, int* gacc, double lam,
-                                             unsigned long long* argkey) {
+                                             unsigned long long* argkey, int* gaccW) {
   __shared__ float smax[NT / 64];
   __shared__ int sbad[NT / 64];
   for (int e = threadIdx.x; e < nblk_cap; e += NT) {
@@ -2026,6 +2044,7 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
   }
   if (threadIdx.x < CNT_COUNT) counters[threadIdx.x] = 0u;
   for (int e = threadIdx.x; e < 2 * 4096; e += NT) gacc[e] = 0;
+  for (int e = threadIdx.x; e < NPAIR_MAX * 4096; e += NT) gaccW[e] = 0;
   if (threadIdx.x < FLAG_COUNT) flags[threadIdx.x] = 0;
   if (!h) {
     for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? 1.0 : 0.0;
@@ -2138,14 +2157,14 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
   __shared__ unsigned long long s_prefix;
   __shared__ int s_need, s_exact, s_hi;
   __shared__ int s_cnt;
-  __shared__ unsigned long long cand_key[BBP];
-  __shared__ int cand_idx[BBP];
+  __shared__ unsigned long long cand_key[BMAX];
+  __shared__ int cand_idx[BMAX];
   __shared__ int s_scan[NT_SELECT / 64];
-  __shared__ int s_rank[BBP];
+  __shared__ int s_rank[BMAX];
   const int tid = threadIdx.x;
   const int64_t st = blockDim.x;
   const int nw = (int)(blockDim.x >> 6);
-  if (tid < BBP) {
+  if (tid < BMAX) {
     cand_key[tid] = 0ull;
     cand_idx[tid] = 0;
   }
@@ -2319,7 +2338,7 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
     const int64_t j = tid + q * st;
     if (j < n && above(kc[q])) {
       const int slot = atomicAdd(&s_cnt, 1);
-      if (slot < BBP) {
+      if (slot < BMAX) {
         cand_key[slot] = kc[q];
         cand_idx[slot] = (int)j;
       }
@@ -2329,7 +2348,7 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
     const unsigned long long kb = (unsigned long long)__double_as_longlong(keys[j]);
     if (above(kb)) {
       const int slot = atomicAdd(&s_cnt, 1);
-      if (slot < BBP) {
+      if (slot < BMAX) {
         cand_key[slot] = kb;
         cand_idx[slot] = (int)j;
       }
@@ -2359,7 +2378,7 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
       tot += s_scan[w];
     }
     const int pos = carry + woff + v - f;
-    if (f && pos < need_eq && base + pos < BBP) {
+    if (f && pos < need_eq && base + pos < BMAX) {
       cand_key[base + pos] = T;
       cand_idx[base + pos] = (int)j;
     }
@@ -2375,30 +2394,26 @@ __global__ __launch_bounds__(NT_SELECT) void k_select(const double* __restrict__
     scan_round(j, j < n ? (unsigned long long)__double_as_longlong(keys[j]) : 0ull);
   }
   __syncthreads();
-  // order the bb winners by (key desc, index asc): 16 threads per winner
-  // each compare it with a quarter of the others, summed over the 16 lanes
-  // of a row on DPP
+  // order the bb winners by (key desc, index asc): TPW threads per winner
+  // each compare it with every TPW-th other, summed over the TPW lanes
   {
-    const int a = tid >> 4, b = tid & 15;
+    constexpr int TPW = NT_SELECT / BMAX;
+    static_assert(TPW == 4, "four threads per winner");
+    const int a = tid / TPW, b = tid % TPW;
     int r = 0;
     if (a < bb) {
       const unsigned long long k0 = cand_key[a];
       const int i0 = cand_idx[a];
-#pragma unroll
-      for (int u = 0; u < BBP / 16; ++u) {
-        const int q = b + 16 * u;
-        if (q < bb) {
-          const unsigned long long k1 = cand_key[q];
-          const int i1 = cand_idx[q];
-          r += (k1 > k0) || (k1 == k0 && i1 < i0);
-        }
+#pragma unroll 8
+      for (int q = b; q < bb; q += TPW) {
+        const unsigned long long k1 = cand_key[q];
+        const int i1 = cand_idx[q];
+        r += (k1 > k0) || (k1 == k0 && i1 < i0);
       }
     }
-    r += __builtin_amdgcn_update_dpp(0, r, DPP_ROW_SHR1, 0xF, 0xF, false);
-    r += __builtin_amdgcn_update_dpp(0, r, DPP_ROW_SHR2, 0xF, 0xF, false);
-    r += __builtin_amdgcn_update_dpp(0, r, DPP_ROW_SHR4, 0xF, 0xF, false);
-    r += __builtin_amdgcn_update_dpp(0, r, DPP_ROW_SHR8, 0xF, 0xF, false);
-    if (b == 15 && a < bb) s_rank[a] = r;
+    r += __shfl_xor(r, 1, 64);
+    r += __shfl_xor(r, 2, 64);
+    if (b == 0 && a < bb) s_rank[a] = r;
   }
   __syncthreads();
   if (tid < bb) J[s_rank[tid]] = cand_idx[tid];
@@ -2458,11 +2473,11 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                                   const int8_t* __restrict__ Vt, int8_t* __restrict__ Vr, int64_t n,
                                                   int64_t n_pad, uint8_t* __restrict__ Cp,
                                                   const unsigned* __restrict__ decision,
-                                                  const unsigned* __restrict__ sg) {
+                                                  const unsigned* __restrict__ sg, int solve) {
   __shared__ double Gs[4096];
   __shared__ double colbuf[1024];
   if (blockIdx.x == 0) {
-    if (!decision && !sg) scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf);
+    if (solve && !decision && !sg) scale_solve(gacc, bb, gramV, gvec, dvec, dF, Dout, Gs, colbuf);
     return;
   }
   int8_t (*tile)[BBP + 4] = (int8_t (*)[BBP + 4])Gs;  // 32 x 68 bytes
@@ -2681,12 +2696,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // ---------------------------------------------------------------------------
 // X: len x bb row-major int8 -> Xt (BBP x len_pad) and Xr (len_pad x BBP), zero padded.
 __global__ __launch_bounds__(NT) void k_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len,
-                                                    int64_t len_pad, int bb) {
+                                                    int64_t len_pad, int bb, int ld) {
   const int64_t total = len_pad * BBP;
   for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
     const int64_t i = e / BBP;
     const int c = (int)(e % BBP);
-    const int8_t v = (i < len && c < bb) ? X[i * bb + c] : (int8_t)0;
+    const int8_t v = (i < len && c < bb) ? X[i * ld + c] : (int8_t)0;
     Xr[e] = v;
     Xt[(int64_t)c * len_pad + i] = v;
     Xmf[mf_offset(c, i)] = v;
@@ -2713,7 +2728,7 @@ __global__ __launch_bounds__(NT) void k_store_cm(double* X, const double* Xcm, i
 }
 __global__ __launch_bounds__(NT) void k_load_cm(double* Xcm, const double* X, int64_t len, int64_t len_pad,
                                                 int bb) {
-  const int64_t total = len_pad * BBP;
+  const int64_t total = len_pad * (bb > BBP ? BMAX : BBP);
   for (int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x; e < total; e += (int64_t)gridDim.x * NT) {
     const int c = (int)(e / len_pad);
     const int64_t i = e % len_pad;
@@ -2761,7 +2776,7 @@ __global__ __launch_bounds__(NT) void k_gvec(const int8_t* __restrict__ Ut, cons
 // Scales given by the caller: dvec = d, dF = fp32(d), zero beyond bb.
 __global__ void k_set_scales(const double* __restrict__ d, int bb, double* dvec, float* dF) {
   const int c = threadIdx.x;
-  if (c < BBP) {
+  if (c < BMAX) {
     const double v = (c < bb) ? d[c] : 0.0;
     dvec[c] = v;
     dF[c] = (float)v;
@@ -2771,6 +2786,284 @@ __global__ void k_set_scales(const double* __restrict__ d, int bb, double* dvec,
 // ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// Wide blocks (bb up to BMAX = NQMAX x 64 components, Sec. 2.4): the Gram
+// matrices of Eq. (3) and the matrix of the joint solve of Eq. (4) couple
+// the quarters of a block; they are formed here as BMAX x BMAX fp64 matrices
+// (64 x 64 blocks, quarter pairs q <= q') and inverted by a blocked sweep.
+// ---------------------------------------------------------------------------
+// quarter pair p <-> (q, q') with q <= q' < nq, in row order
+__device__ __forceinline__ void pair_of(int p, int nq, int& q, int& q2) {
+  q = 0;
+  while (p >= nq - q) {
+    p -= nq - q;
+    ++q;
+  }
+  q2 = q + p;
+}
+__host__ __device__ __forceinline__ int pair_index(int q, int q2, int nq) {
+  return q * nq - q * (q - 1) / 2 + (q2 - q);
+}
+
+// Integer Gram blocks X_q^T X_q' of a ternary factor (MFMA-ready layout,
+// quarter q at byte 64 q L_pad) for every pair q <= q' < nq, on int8 MFMA,
+// added into gaccW[pair] with integer atomics (exact, order-free); the
+// sweep's first pivot launch clears gaccW again.
+// grid: npairs x nslice workgroups, workgroup (pair, slice) takes a slice of
+// the K steps.
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gram_pairs(
+    const v4i* __restrict__ Xmf, int64_t L_pad, int nq, int nslice, int* __restrict__ gaccW) {
+  __shared__ int red[4 * 4096];
+  const int p = blockIdx.x / nslice, sl = blockIdx.x % nslice;
+  int q, q2;
+  pair_of(p, nq, q, q2);
+  const int nks = (int)(L_pad / TILE);
+  const int ks0 = (int)((long long)sl * nks / nslice), ks1 = (int)((long long)(sl + 1) * nks / nslice);
+  const v4i* Xa = Xmf + (int64_t)q * 4 * L_pad;
+  const v4i* Xb = Xmf + (int64_t)q2 * 4 * L_pad;
+  constexpr int KR = 4;
+  const int lane = lane_id(), wave = wave_id();
+  const int h = lane >> 5, l32 = lane & 31;
+  v16i acc00 = {}, acc01 = {}, acc10 = {}, acc11 = {};
+  for (int ks = ks0 + wave; ks < ks1; ks += 4 * KR) {
+    v4i a[KR][2], b[KR][2];
+#pragma unroll
+    for (int u = 0; u < KR; ++u) {
+      const int kk = ks + 4 * u;
+      if (kk < ks1) {
+        a[u][0] = Xa[(int64_t)kk * 128 + lane];
+        a[u][1] = Xa[(int64_t)kk * 128 + 64 + lane];
+        b[u][0] = Xb[(int64_t)kk * 128 + lane];
+        b[u][1] = Xb[(int64_t)kk * 128 + 64 + lane];
+      } else {
+        a[u][0] = a[u][1] = b[u][0] = b[u][1] = v4i{};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < KR; ++u) {
+      acc00 = mfma_i8(a[u][0], b[u][0], acc00);
+      acc01 = mfma_i8(a[u][0], b[u][1], acc01);
+      acc10 = mfma_i8(a[u][1], b[u][0], acc10);
+      acc11 = mfma_i8(a[u][1], b[u][1], acc11);
+    }
+  }
+  int* mine = red + wave * 4096;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int M = 8 * (r >> 2) + 4 * h + (r & 3);
+    const int N = l32;
+    mine[M * 64 + N] = acc00[r];
+    mine[M * 64 + 32 + N] = acc01[r];
+    mine[(32 + M) * 64 + N] = acc10[r];
+    mine[(32 + M) * 64 + 32 + N] = acc11[r];
+  }
+  __syncthreads();
+  int* g = gaccW + (int64_t)p * 4096;
+  for (int e = threadIdx.x; e < 4096; e += NT) {
+    const int v = red[e] + red[4096 + e] + red[8192 + e] + red[12288 + e];
+    if (v) __hip_atomic_fetch_add(g + e, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Weighted Gram blocks of V (Sec. 2.5): partial V_q^T diag(h~) V_q' over a
+// slab of rows for every pair q <= q', on fp64 MFMA (the products
+// h~_j v_jc v_jc' are exact); wave w takes the 16-row tile w of the block.
+// grid: npairs x GW_SLABS.
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gramw_pairs(
+    const int8_t* __restrict__ Vt, const double* __restrict__ hw, int64_t n_pad, int nq,
+    double* __restrict__ partwW) {
+  const int p = blockIdx.x / GW_SLABS, sl = blockIdx.x % GW_SLABS;
+  int q, q2;
+  pair_of(p, nq, q, q2);
+  const int64_t rs = (n_pad / 4 + GW_SLABS - 1) / GW_SLABS * 4;  // rows per slab, a multiple of 4
+  const int64_t r0 = (int64_t)sl * rs, r1 = r0 + rs < n_pad ? r0 + rs : n_pad;
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+  const int8_t* va = Vt + (int64_t)(BBP * q + 16 * w + li) * n_pad;
+  const int8_t* vb = Vt + (int64_t)(BBP * q2 + li) * n_pad;
+  v4d acc[4] = {v4d{}, v4d{}, v4d{}, v4d{}};
+  for (int64_t j0 = r0; j0 < r1; j0 += 4) {
+    const int64_t j = j0 + lk;
+    const double a = hw[j] * (double)va[j];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma_f64(a, (double)vb[(int64_t)16 * nt * n_pad + j], acc[nt]);
+  }
+  double* out = partwW + ((int64_t)p * GW_SLABS + sl) * 4096;
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) out[(16 * w + lk + 4 * r) * BBP + 16 * nt + li] = acc[nt][r];
+}
+
+// The matrix to sweep, A (BMAX-stride row-major, nq x nq blocks), from one
+// pair block per workgroup (both triangles):
+//   mode 0: (G + eps I) from the integer Gram blocks gaccW, the raw Gram
+//           also into raw (if given);
+//   mode 1: (G + eps I) from the partial weighted blocks partwW (slabs added
+//           in order), the raw Gram into raw;
+//   mode 2: (G_U o G_V + delta I) from gaccW (G_U) and raw (G_V), Eq. (4);
+// with eps or delta = rel * trace / bb over the bb real components and the
+// identity on the padding components.  A zero trace sets wflag[0] (the
+// result is then zero targets, or zero scales) and leaves the identity in A.
+// grid: npairs.
+__global__ __launch_bounds__(NT) void k_wide_prep(int mode, const int* __restrict__ gaccW,
+                                                  const double* __restrict__ partwW, double* raw, int bb, int nq,
+                                                  double rel, double* __restrict__ A, int* __restrict__ wflag) {
+  __shared__ double shd[NT / 64];
+  const int p = blockIdx.x;
+  int q, q2;
+  pair_of(p, nq, q, q2);
+  // trace over the real components, the same arithmetic in every workgroup
+  double dv = 0.0;
+  const int c = threadIdx.x;  // BMAX == NT: one diagonal entry per thread
+  if (c < bb) {
+    const int qc = c / BBP, cl = c % BBP, pd = pair_index(qc, qc, nq);
+    if (mode == 0) dv = (double)gaccW[(int64_t)pd * 4096 + cl * 65];
+    else if (mode == 1) {
+      for (int s = 0; s < GW_SLABS; ++s) dv += partwW[((int64_t)pd * GW_SLABS + s) * 4096 + cl * 65];
+    } else
+      dv = (double)gaccW[(int64_t)pd * 4096 + cl * 65] * raw[(int64_t)c * BMAX + c];
+  }
+  const double tr = block_sum_d(dv, shd);
+  const bool zero = tr == 0.0;
+  if (p == 0 && threadIdx.x == 0) *wflag = zero ? 1 : 0;
+  const double ridge = zero ? 0.0 : rel * tr / (double)bb;
+  for (int e = threadIdx.x; e < 4096; e += NT) {
+    const int r = e >> 6, cc = e & 63;
+    const int gi = BBP * q + r, gj = BBP * q2 + cc;
+    const bool real = gi < bb && gj < bb;
+    double v = 0.0;
+    if (mode == 0) v = (double)gaccW[(int64_t)p * 4096 + e];
+    else if (mode == 1) {
+      for (int s = 0; s < GW_SLABS; ++s) v += partwW[((int64_t)p * GW_SLABS + s) * 4096 + e];
+    } else
+      v = (double)gaccW[(int64_t)p * 4096 + e] * raw[(int64_t)gi * BMAX + gj];
+    if (!real) v = 0.0;
+    if (raw && mode != 2) {
+      raw[(int64_t)gi * BMAX + gj] = v;
+      raw[(int64_t)gj * BMAX + gi] = v;
+    }
+    double a = (gi == gj) ? (real && !zero ? v + ridge : 1.0) : (zero ? 0.0 : v);
+    A[(int64_t)gi * BMAX + gj] = a;
+    A[(int64_t)gj * BMAX + gi] = a;
+  }
+}
+
+// Pivot block k of the sweep: Pinv = A_kk^{-1} (A_kk is symmetric positive
+// definite: the Schur complement of the swept blocks), on one workgroup with
+// the 64 x 64 block sweep; nk: 4 x 4 pivots holding real components.  The
+// first pivot also clears the integer Gram blocks for the next accumulation.
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_wide_pivot(
+    const double* __restrict__ A, int k, int nk, double* __restrict__ Pinv, int* gaccW, int nclear) {
+  __shared__ double Gs[4096];
+  __shared__ double pbuf[1024];
+  for (int e = threadIdx.x; e < 4096; e += NT) Gs[e] = A[(int64_t)(BBP * k + (e >> 6)) * BMAX + BBP * k + (e & 63)];
+  for (int e = threadIdx.x; e < nclear; e += NT) gaccW[e] = 0;
+  __syncthreads();
+  spd_inverse64(Gs, pbuf, nk);
+  for (int e = threadIdx.x; e < 4096; e += NT) Pinv[e] = Gs[e];
+}
+
+// C (64 x 64 block of this workgroup, rows 16 w .. of wave w) += X Y for
+// 64 x 64 operands with leading dimensions ldx, ldy, on fp64 MFMA:
+// acc[nt][r] <-> row 16 w + lane / 16 + 4 r, column 16 nt + lane % 16.
+__device__ __forceinline__ void gemm64(const double* X, int64_t ldx, const double* Y, int64_t ldy, v4d (&acc)[4]) {
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+#pragma unroll 4
+  for (int ks = 0; ks < 16; ++ks) {
+    const double a = X[(int64_t)(16 * w + li) * ldx + 4 * ks + lk];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma_f64(a, Y[(int64_t)(4 * ks + lk) * ldy + 16 * nt + li], acc[nt]);
+  }
+}
+
+// One step of the blocked sweep (pivot block k), A -> B:
+//   B_kk = -P, B_kj = P A_kj, B_ik = A_ik P, B_ij = A_ij - A_ik P A_kj
+// with P = A_kk^{-1}; after all nq pivots B = -A^{-1}.  grid: nq x nq.
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_wide_update(
+    const double* __restrict__ A, double* __restrict__ B, const double* __restrict__ P, int k, int nq) {
+  __shared__ double T[4096];
+  const int i = blockIdx.x / nq, j = blockIdx.x % nq;
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+  const double* Aik = A + (int64_t)BBP * i * BMAX + BBP * k;
+  const double* Akj = A + (int64_t)BBP * k * BMAX + BBP * j;
+  const double* Aij = A + (int64_t)BBP * i * BMAX + BBP * j;
+  double* Bij = B + (int64_t)BBP * i * BMAX + BBP * j;
+  v4d acc[4] = {v4d{}, v4d{}, v4d{}, v4d{}};
+  double sgn = 1.0;
+  if (i == k && j == k) {
+    for (int e = threadIdx.x; e < 4096; e += NT) Bij[(int64_t)(e >> 6) * BMAX + (e & 63)] = -P[e];
+    return;
+  } else if (i == k) {
+    gemm64(P, BBP, Akj, BMAX, acc);
+  } else if (j == k) {
+    gemm64(Aik, BMAX, P, BBP, acc);
+  } else {
+    gemm64(Aik, BMAX, P, BBP, acc);
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) T[(16 * w + lk + 4 * r) * BBP + 16 * nt + li] = acc[nt][r];
+    __syncthreads();
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[nt] = v4d{};
+    gemm64(T, BBP, Akj, BMAX, acc);
+    sgn = -1.0;
+  }
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t o = (int64_t)(16 * w + lk + 4 * r) * BMAX + 16 * nt + li;
+      Bij[o] = (sgn < 0.0 ? Aij[o] : 0.0) + sgn * acc[nt][r];
+    }
+}
+
+// G^{-1} = -S (S: the fully swept matrix) into nq x nq blocks in the fp64
+// MFMA operand order of the target kernels (block (q, q') at
+// ginvW + (q NQMAX + q') 4096); with zero trace (wflag) the inverse is zero
+// on the real components and the identity on the padding.  grid: nq x nq.
+__global__ __launch_bounds__(NT) void k_wide_ginv(const double* __restrict__ S, int nq, int bb,
+                                                  const int* __restrict__ wflag, double* __restrict__ ginvW) {
+  const int i = blockIdx.x / nq, j = blockIdx.x % nq;
+  const bool zero = *wflag != 0;
+  double* out = ginvW + (int64_t)(i * NQMAX + j) * 4096;
+  for (int e = threadIdx.x; e < 4096; e += NT) {
+    const int r = e >> 6, c = e & 63;
+    const int gi = BBP * i + r, gj = BBP * j + c;
+    double v;
+    if (zero) v = (gi >= bb || gj >= bb) ? (gi == gj ? 1.0 : 0.0) : 0.0;
+    else v = -S[(int64_t)gi * BMAX + gj];
+    out[ginv_index(r, c)] = v;
+  }
+}
+
+// Joint scales of a wide block, d = M^{-1} g (Eq. (4)) with M^{-1} = -S and
+// g_c = diag(U^T Q)_c (the per-split partial sums in split order); zero
+// trace: d = 0.  d into dvec, dF (fp32) and D (the block's output).
+// One workgroup; row c of the product by thread c (columns in order).
+__global__ __launch_bounds__(NT) void k_wide_scales(const double* __restrict__ S, const double* __restrict__ gvec,
+                                                    int bb, const int* __restrict__ wflag, double* dvec, float* dF,
+                                                    float* Dout) {
+  __shared__ double g[BMAX];
+  const int c = threadIdx.x;  // BMAX == NT
+  double gc = 0.0;
+  if (c < bb)
+#pragma unroll
+    for (int k = 0; k < TERN_SPLIT_MAX; ++k) gc += gvec[c * TERN_SPLIT_MAX + k];
+  g[c] = gc;
+  __syncthreads();
+  double d = 0.0;
+  if (c < bb && *wflag == 0) {
+    for (int c2 = 0; c2 < bb; ++c2) d += -S[(int64_t)c * BMAX + c2] * g[c2];
+  }
+  dvec[c] = d;
+  dF[c] = (float)d;
+  if (Dout && c < bb) Dout[c] = (float)d;
+}
+
 static inline unsigned grid_for(int64_t total) {
   int64_t g = (total + NT - 1) / NT;
   if (g < 1) g = 1;
@@ -2780,7 +3073,7 @@ static inline unsigned grid_for(int64_t total) {
 
 hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s, double lam) {
   hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.hwmax, w.fro2_hist,
-                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc, lam, w.argkey);
+                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc, lam, w.argkey, w.gaccW);
   return hipGetLastError();
 }
 
@@ -2850,9 +3143,9 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
                                    w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VTARGET, k_vtarget, dim3((unsigned)(w.n_pad / 16)), dim3(NT), 0, s,
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VTARGET, k_vtarget<false>, dim3((unsigned)(w.n_pad / 16)), dim3(NT), 0, s,
                        (const long long*)w.Pp, (const int*)w.cshift, w.n_pad, w.gv, w.ginvU, w.Y, w.n, w.tps, w.tpm,
-                       w.tpi);
+                       w.tpi, 1, (int64_t)0);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (weighted && tern_vw_fits(w)) {
@@ -2916,8 +3209,8 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_UTARGET, k_utarget, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0,
-                       s, (const double*)w.Q, (const double*)w.ginvV, w.Z, w.m, w.m_pad, w.tps, w.tpm, w.tpi);
+  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_UTARGET, k_utarget<false>, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0,
+                       s, (const double*)w.Q, (const double*)w.ginvV, w.Z, w.m, w.m_pad, w.tps, w.tpm, w.tpi, 1);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNU, k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, (const double*)w.Z,
@@ -2926,18 +3219,210 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
   return hipGetLastError();
 }
 
+// ---- wide blocks (nq = ceil(bb / 64) > 1 quarters) ----
+static int nq_of(int bb) { return (bb + BBP - 1) / BBP; }
+static int bb_of_quarter(int bb, int q) { return bb - BBP * q < BBP ? bb - BBP * q : BBP; }
+constexpr int GRAM_PAIR_SLICES = 16;  // K slices per quarter pair of the integer Gram
+
+// Blocked sweep of the matrix prepared in wA0 (nq quarters): every pivot
+// block in turn is inverted (one workgroup) and the nq x nq blocks updated;
+// *out receives the buffer holding -A^{-1}.  The first pivot launch clears
+// the integer Gram blocks.
+static hipError_t wide_sweep(const Ws& w, int bb, hipStream_t s, const double** out) {
+  const int nq = nq_of(bb), npairs = nq * (nq + 1) / 2;
+  double* A = w.wA0;
+  double* B = w.wA1;
+  for (int k = 0; k < nq; ++k) {
+    const int bq = bb_of_quarter(bb, k);
+    hipLaunchKernelGGL(k_wide_pivot, dim3(1), dim3(NT), 0, s, (const double*)A, k, (bq + 3) / 4, w.wPinv, w.gaccW,
+                       k == 0 ? npairs * 4096 : 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_wide_update, dim3((unsigned)(nq * nq)), dim3(NT), 0, s, (const double*)A, B,
+                       (const double*)w.wPinv, k, nq);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    double* t = A;
+    A = B;
+    B = t;
+  }
+  *out = A;
+  return hipSuccess;
+}
+
+// (X^T diag(h~) X + eps I)^{-1} of the block's U (which = 0) or V (which = 1,
+// weighted with h~ when `weighted`) into ginvUW / ginvVW; for V the raw Gram
+// is kept in gramVW for the joint solve.
+static hipError_t wide_gram_inverse(const Ws& w, int which, bool weighted, int bb, hipStream_t s) {
+  static_assert(BMAX == NT, "one diagonal entry per thread in the wide preparation");
+  const int nq = nq_of(bb), npairs = nq * (nq + 1) / 2;
+  hipError_t e;
+  if (which == 1 && weighted) {
+    hipLaunchKernelGGL(k_gramw_pairs, dim3((unsigned)(npairs * GW_SLABS)), dim3(NT), 0, s, (const int8_t*)w.Vt,
+                       (const double*)w.hw, w.n_pad, nq, w.partwW);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_wide_prep, dim3((unsigned)npairs), dim3(NT), 0, s, 1, (const int*)w.gaccW,
+                       (const double*)w.partwW, w.gramVW, bb, nq, EXTERND_RIDGE_REL, w.wA0, w.wflag);
+  } else {
+    const v4i* X = (const v4i*)(which ? w.Vmf : w.Umf);
+    hipLaunchKernelGGL(k_gram_pairs, dim3((unsigned)(npairs * GRAM_PAIR_SLICES)), dim3(NT), 0, s, X,
+                       which ? w.n_pad : w.m_pad, nq, GRAM_PAIR_SLICES, w.gaccW);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_wide_prep, dim3((unsigned)npairs), dim3(NT), 0, s, 0, (const int*)w.gaccW,
+                       (const double*)nullptr, which ? w.gramVW : (double*)nullptr, bb, nq, EXTERND_RIDGE_REL,
+                       w.wA0, w.wflag);
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const double* S = nullptr;
+  e = wide_sweep(w, bb, s, &S);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_wide_ginv, dim3((unsigned)(nq * nq)), dim3(NT), 0, s, S, nq, bb, (const int*)w.wflag,
+                     which ? w.ginvVW : w.ginvUW);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_wide(const Ws& w, int bb, double tau, hipStream_t s) {
+  for (int q = 0; q < nq_of(bb); ++q) {
+    const hipError_t e = launch_init(quarter_view(w, q), bb_of_quarter(bb, q), tau, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
+  const int nq = nq_of(bb);
+  hipError_t e;
+  // P_q = U_q^T R per quarter (contraction launches without a side path)
+  for (int q = 0; q < nq; ++q) {
+    const Ws v = quarter_view(w, q);
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3((unsigned)((w.n_pad / TILE) * w.gv)), dim3(NT), 0,
+                         s, w.R, (const v4i*)v.Umf, v.Pp, (const int*)w.cshift, w.m_pad, w.n_pad, w.gv,
+                         bb_of_quarter(bb, q), w.gacc, w.counters + CNT_GRAM_U, w.ginvU, 0);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  e = wide_gram_inverse(w, 0, false, bb, s);
+  if (e != hipSuccess) return e;
+  for (int q = 0; q < nq; ++q) {
+    const Ws v = quarter_view(w, q);
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VTARGET, k_vtarget<true>, dim3((unsigned)(w.n_pad / 16)), dim3(NT), 0, s,
+                         (const long long*)w.Pp, (const int*)w.cshift, w.n_pad, w.gv,
+                         (const double*)(w.ginvUW + (int64_t)q * NQMAX * 4096), v.Y, w.n, v.tps, v.tpm, v.tpi, nq,
+                         (int64_t)BBP * w.gv * w.n_pad);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, (const double*)v.Y,
+                         w.n, w.n_pad, bb_of_quarter(bb, q), tau, (const double*)v.tps, (const double*)v.tpm,
+                         (const int*)v.tpi, (int)(w.n_pad / 16), w.nsv, v.Vt, v.Vmf);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_ustep_wide(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
+                             Timer* tm) {
+  const int nq = nq_of(bb);
+  hipError_t e;
+  // Q_q = R diag(h~) V_q per quarter (contraction launches without a side path)
+  for (int q = 0; q < nq; ++q) {
+    const Ws v = quarter_view(w, q);
+    const int bq = bb_of_quarter(bb, q);
+    if (weighted)
+      EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3((unsigned)w.ntu), dim3(NT), 0, s, w.R,
+                           (const v4i*)v.Vmf, v.Vr, w.hw, v.Q, w.rowb, w.m_pad, w.n_pad, bq, w.gacc + 4096,
+                           w.counters + CNT_GRAM_V, w.ginvV, w.gramV, 0, w.urows, (const double*)nullptr, 0);
+    else
+      EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3((unsigned)w.ntu), dim3(NT), 0, s, w.R,
+                           (const v4i*)v.Vmf, v.Vr, w.hw, v.Q, w.rowb, w.m_pad, w.n_pad, bq, w.gacc + 4096,
+                           w.counters + CNT_GRAM_V, w.ginvV, w.gramV, 0, w.urows, (const double*)nullptr, 0);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  e = wide_gram_inverse(w, 1, weighted, bb, s);
+  if (e != hipSuccess) return e;
+  for (int q = 0; q < nq; ++q) {
+    const Ws v = quarter_view(w, q);
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_UTARGET, k_utarget<true>, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0,
+                         s, (const double*)w.Q, (const double*)(w.ginvVW + (int64_t)q * NQMAX * 4096), v.Z, w.m,
+                         w.m_pad, v.tps, v.tpm, v.tpi, nq);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNU, k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, (const double*)v.Z,
+                         final ? (const double*)v.Q : nullptr, w.m, w.m_pad, bb_of_quarter(bb, q), tau,
+                         (const double*)v.tps, (const double*)v.tpm, (const int*)v.tpi, (int)(w.m_pad / TILE), w.nsu,
+                         v.Ut, v.Umf, v.gvec);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// The raw V^T H V of a wide block into gramVW (the step entry point of the
+// joint solve; the factorization leaves it from its last U-step).
+hipError_t launch_gram_wide_raw(const Ws& w, int bb, bool weighted, hipStream_t s) {
+  return wide_gram_inverse(w, 1, weighted, bb, s);
+}
+
+// Joint scales of a wide block (Eq. (4)): [(U^T U) o (V^T H V) + delta I]
+// d = g with the raw V^T H V of the last U-step, d into dvec, dF and D_block.
+hipError_t launch_scale_wide(const Ws& w, int bb, float* D_block, hipStream_t s) {
+  const int nq = nq_of(bb), npairs = nq * (nq + 1) / 2;
+  hipLaunchKernelGGL(k_gram_pairs, dim3((unsigned)(npairs * GRAM_PAIR_SLICES)), dim3(NT), 0, s, (const v4i*)w.Umf,
+                     w.m_pad, nq, GRAM_PAIR_SLICES, w.gaccW);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_wide_prep, dim3((unsigned)npairs), dim3(NT), 0, s, 2, (const int*)w.gaccW,
+                     (const double*)nullptr, w.gramVW, bb, nq, EXTERND_SCALE_GUARD_REL, w.wA0, w.wflag);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const double* S = nullptr;
+  e = wide_sweep(w, bb, s, &S);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_wide_scales, dim3(1), dim3(NT), 0, s, S, (const double*)w.gvec, bb, (const int*)w.wflag,
+                     w.dvec, w.dF, D_block);
+  return hipGetLastError();
+}
+
+// Block end of a wide block: joint scales, then per quarter the row-major
+// factor copies and the packed outputs (columns c0 + 64 q ..).
+hipError_t launch_block_out_wide(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
+                                 hipStream_t s) {
+  hipError_t e = launch_scale_wide(w, bb, D + c0, s);
+  if (e != hipSuccess) return e;
+  for (int q = 0; q < nq_of(bb); ++q) {
+    e = launch_block_out(quarter_view(w, q), c0 + (int64_t)BBP * q, bb_of_quarter(bb, q), k, Bp, Cp, D, s, false,
+                         false, false);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// R <- R - sum_q U_q diag(d_q) V_q^T, one deflation launch per quarter (the
+// column energies and the residual bound of the last one are the block's).
+hipError_t launch_deflate_wide(const Ws& w, int blk, int bb, bool transposes, hipStream_t s, Timer* tm) {
+  for (int q = 0; q < nq_of(bb); ++q) {
+    const hipError_t e = launch_deflate(quarter_view(w, q), blk, transposes, s, tm, false);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s) {
   hipLaunchKernelGGL(k_scale, dim3(1), dim3(NT), 0, s, w.gacc, bb, w.gramV, w.gvec, w.dvec, w.dF, (float*)nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_block_out(const Ws& w, int64_t c0, int bb, int64_t k, uint8_t* Bp, uint8_t* Cp, float* D,
-                           hipStream_t s, bool revisit, bool safeguard) {
+                           hipStream_t s, bool revisit, bool safeguard, bool solve) {
   const unsigned grid = (unsigned)(1 + w.m_pad / TILE + w.n_pad / TILE);
   hipLaunchKernelGGL(k_block_out, dim3(grid), dim3(NT), 0, s, w.gacc, bb, w.gramV, w.gvec, w.dvec, w.dF, D + c0,
                      w.Ut, w.Ur, w.Ub, w.m, w.m_pad, c0, k, Bp, w.Vt, w.Vr, w.n, w.n_pad, Cp,
                      revisit ? (const unsigned*)(w.counters + CNT_DECISION) : nullptr,
-                     safeguard ? (const unsigned*)(w.counters + CNT_SG_FIRE) : nullptr);
+                     safeguard ? (const unsigned*)(w.counters + CNT_SG_FIRE) : nullptr, solve ? 1 : 0);
   return hipGetLastError();
 }
 hipError_t launch_safeguard(const Ws& w, int blk, int bb, float* D_block, hipStream_t s) {
@@ -2988,8 +3473,9 @@ hipError_t launch_deflate_slot(const Ws& w, int out_slot, hipStream_t s, Timer* 
 }
 
 hipError_t launch_load_factor(int8_t* Xt, int8_t* Xr, int8_t* Xmf, const int8_t* X, int64_t len, int64_t len_pad,
-                              int bb, hipStream_t s) {
-  hipLaunchKernelGGL(k_load_factor, dim3(grid_for(len_pad * BBP)), dim3(NT), 0, s, Xt, Xr, Xmf, X, len, len_pad, bb);
+                              int bb, hipStream_t s, int ld) {
+  hipLaunchKernelGGL(k_load_factor, dim3(grid_for(len_pad * BBP)), dim3(NT), 0, s, Xt, Xr, Xmf, X, len, len_pad, bb,
+                     ld > 0 ? ld : bb);
   return hipGetLastError();
 }
 hipError_t launch_store_factor(int8_t* X, const int8_t* Xt, int64_t len, int64_t len_pad, int bb, hipStream_t s) {
@@ -3018,11 +3504,11 @@ hipError_t launch_gram_acc(const Ws& w, int which, hipStream_t s) {
 }
 
 hipError_t launch_gvec(const Ws& w, int bb, hipStream_t s) {
-  hipLaunchKernelGGL(k_gvec, dim3(BBP), dim3(NT), 0, s, w.Ut, w.Q, w.m, w.m_pad, bb, w.gvec);
+  hipLaunchKernelGGL(k_gvec, dim3(bb > BBP ? BMAX : BBP), dim3(NT), 0, s, w.Ut, w.Q, w.m, w.m_pad, bb, w.gvec);
   return hipGetLastError();
 }
 hipError_t launch_set_scales(const Ws& w, const double* d, int bb, hipStream_t s) {
-  hipLaunchKernelGGL(k_set_scales, dim3(1), dim3(BBP), 0, s, d, bb, w.dvec, w.dF);
+  hipLaunchKernelGGL(k_set_scales, dim3(1), dim3(BMAX), 0, s, d, bb, w.dvec, w.dF);
   return hipGetLastError();
 }
 

@@ -52,6 +52,11 @@ def cases():
         yield w.name, w.A, w.h, w.mu, w.tau, w.block, w.iters
     w = synth.ragged5003()
     yield w.name, w.A, w.h, w.mu, w.tau, w.block, w.iters
+    # the paper's default block width, 256 (Sec. 2.4), on the down projection
+    for weighted in (False, True):
+        w = synth.down9728(weighted=weighted)
+        yield (f"down9728x2560_mu3_tau1.0_b256" + ("_imatrix" if weighted else ""), w.A, w.h, w.mu, w.tau, 256,
+               w.iters)
     for idx, (mname, m, n) in enumerate(synth.BLOCK_SHAPES):
         _, A, h = synth.transformer_block(idx)
         for mu, tau in BLOCK_POINTS:

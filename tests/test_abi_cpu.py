@@ -40,7 +40,8 @@ def test_rank_block_and_workspace_rules():
     assert binding.effective_block(4096, 4096, 256) == 256 and binding.effective_block(519, 4000, 256) == 64
     assert binding.rank(0, 5, 1.0) == -1 and binding.rank(5, 5, 0.0) == -1 and binding.rank(5, 5, float("nan")) == -1
     ws = binding.workspace_bytes(9728, 2560, 7680)
-    assert 4 * 9728 * 2560 < ws < 2 * 4 * 9728 * 2560
+    # the fp32 residual plus per-row and per-column buffers for 256-wide blocks
+    assert 4 * 9728 * 2560 < ws < 4 * 9728 * 2560 + 6144 * 9728 + 20480 * 2560 + (16 << 20)
     assert binding.workspace_bytes(0, 10, 0) == 0
     assert binding.workspace_bytes(1 << 16, 1 << 16, 0) == 0        # beyond the supported size
     assert binding.workspace_bytes(100, 70, 10000) > binding.workspace_bytes(100, 70, 0)  # per-block history
@@ -69,16 +70,22 @@ def test_argument_errors_before_device_work():
     # unsupported shape
     assert f(dummy, 1 << 16, 1 << 16, 1.0, 0.7, 1, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None,
              None, dummy, 1 << 40, None) == binding.EUNSUPPORTED
-    # effective block width beyond what the kernels hold: refused, never clamped
+    # effective block width beyond what the kernels hold (256): refused, never clamped
     for ff, extra in [(f, ()), (L.externd_factorize_timed, (dummy,))]:
-        assert ff(dummy, 1024, 1024, 1.0, 0.7, 65, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+        assert ff(dummy, 4096, 4096, 1.0, 0.7, 257, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
                   dummy, 1 << 40, None, *extra) == binding.EUNSUPPORTED
         assert np.isnan(E.value)
-    assert f(dummy, 4096, 4096, 1.0, 0.7, 256, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
+    assert f(dummy, 8192, 8192, 1.0, 0.7, 512, 1, None, dummy, dummy, dummy, ctypes.byref(E), None, None, None,
              dummy, 1 << 40, None) == binding.EUNSUPPORTED
+    # wide blocks (effective width above 64) have no refinement sweeps and no safeguard
+    assert L.externd_factorize_refined(dummy, 1024, 1024, 1.0, 0.7, 65, 1, 1, None, dummy, dummy, dummy,
+                                       ctypes.byref(E), None, None, None, None, None, None, dummy, 1 << 40,
+                                       None) == binding.EUNSUPPORTED
+    assert L.externd_factorize_ex(dummy, 1024, 1024, 1.0, 0.7, 65, 1, None, 0.0, 1, dummy, dummy, dummy,
+                                  ctypes.byref(E), None, None, None, None, dummy, 1 << 40, None) == binding.EUNSUPPORTED
     # step entry points
     assert L.externd_step_vstep(None, 10, 10, dummy, 4, 0.7, dummy, None, dummy, 1 << 30, None) == binding.EINVAL
-    assert L.externd_step_vstep(dummy, 10, 10, dummy, 65, 0.7, dummy, None, dummy, 1 << 30, None) == binding.EINVAL
+    assert L.externd_step_vstep(dummy, 10, 10, dummy, 257, 0.7, dummy, None, dummy, 1 << 30, None) == binding.EINVAL
     assert L.externd_step_ustep(dummy, 10, 10, dummy, 0, 0.7, None, dummy, None, None, dummy, 1 << 30,
                                 None) == binding.EINVAL
     assert L.externd_step_scale(dummy, dummy, None, 10, 10, 4, None, dummy, dummy, 1 << 30, None) == binding.EINVAL

@@ -305,10 +305,14 @@ def test_gauss256_sequential_checkpoints(ext):
 
 
 def test_block_wider_than_kernels_refused(ext):
-    # effective width min(b, floor(min(m, n) / 8)) = 128 > 64: refused, not clamped
-    A = cuda(synth.small("t4", 1024, 1030, 3))
+    # effective width min(b, floor(min(m, n) / 8)) = 300 > 256: refused, not clamped
+    A = cuda(synth.small("t4", 2400, 2420, 3))
     with pytest.raises(ext.ExterndError) as e:
-        ext.factorize(A, 0.25, 1.0, 128, 2)
+        ext.factorize(A, 0.25, 1.0, 300, 2)
+    assert e.value.status == ext.EUNSUPPORTED
+    # wide blocks (above 64) have no refinement sweeps
+    with pytest.raises(ext.ExterndError) as e:
+        ext.factorize_refined(cuda(synth.small("t4", 1024, 1030, 3)), 0.25, 1.0, 128, 2, 1)
     assert e.value.status == ext.EUNSUPPORTED
     # the paper's default b = 256 where its cap brings it to 64 or less
     A = synth.small("t4", 300, 515, 3)
