@@ -631,8 +631,9 @@ def bench_block(binding, torch, args):
 def bench_apply(binding, torch, w, args):
     """Time y = B (diag(D) (C x)) on the packed factors of the workload's
     factorization (HIP events on the current stream, 50 launches per batch
-    size).  Bytes per call: the packed B and C, D, the inputs and outputs and
-    the k x nb intermediate (written and read)."""
+    size).  Algorithmic bytes per call: the packed B and C, D, the inputs and
+    outputs and the k x nb fp32 intermediate diag(D) C X^T (written and
+    read)."""
     m, n = w.A.shape
     dev = torch.device("cuda:0")
     A = torch.from_numpy(w.A).to(dev)
@@ -642,7 +643,7 @@ def bench_apply(binding, torch, w, args):
            "n_gpus": 1, "data": "synthetic", "config": {"workload": w.name, "m": m, "n": n, "k": k}, "batches": {}}
     for nb in (1, 8):
         X = torch.randn((nb, n), dtype=torch.float32, device=dev)
-        ws = torch.empty(binding.lib().externd_apply_workspace_bytes(k, nb), dtype=torch.uint8, device=dev)
+        ws = torch.empty(binding.lib().externd_apply_workspace_bytes(m, n, k, nb), dtype=torch.uint8, device=dev)
         for _ in range(3):
             binding.apply(res.B_packed, res.C_packed, res.D, m, n, X, workspace=ws)
         torch.cuda.synchronize()
@@ -654,8 +655,7 @@ def bench_apply(binding, torch, w, args):
         b.record()
         torch.cuda.synchronize()
         us = a.elapsed_time(b) * 1e3 / reps
-        slots = 1 if nb == 1 else 8
-        nbytes = m * ((k + 3) // 4) + k * ((n + 3) // 4) + 4 * k + 4 * nb * (n + m) + 2 * 4 * k * slots
+        nbytes = m * ((k + 3) // 4) + k * ((n + 3) // 4) + 4 * k + 4 * nb * (n + m) + 2 * 4 * k * nb
         out["batches"][str(nb)] = {"us_per_call": us, "bytes_per_call": nbytes, "GB_s": nbytes / us / 1e3,
                                    "frac_of_8TBs": nbytes / us / 1e3 / HBM_PEAK_GBS,
                                    "trit_macs_per_s": nb * k * (m + n) / us / 1e-6}

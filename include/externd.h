@@ -229,21 +229,32 @@ int externd_factorize_refined(const float* A, int64_t m, int64_t n, double mu, d
 /*
  * Inference with a factorization (Sec. 2.6 cost model): for each of nb
  * input vectors x (rows of X), y = B (diag(D) (C x)), computed on the packed
- * trits with fp32 arithmetic and fp32 accumulation (deterministic order).
+ * trits with fp32 accumulation in a fixed order (deterministic).  One
+ * vector runs on fp32 FMA; two or more on bf16 matrix cores with exact
+ * operands (trits are exact in bf16; every fp32 vector entry is split
+ * exactly into three bf16 parts).  Either way the error is that of fp32
+ * sums: at most (n + k + 4) u (|B| (|D| (|C| |x|))) per output, u = 2^-24,
+ * for finite inputs whose nonzero entries are fp32 normals.
  *
  *  B_packed   device, m rows of ceil(k/4) bytes; C_packed device, k rows of
  *             ceil(n/4) bytes; D device fp32[k] -- as written by
  *             externd_factorize (or _to_energy, whose zero components
- *             contribute nothing).
+ *             contribute nothing).  On the matrix-core path, rows of a
+ *             multiple of 8 bytes (nb <= 5) or 16 bytes (nb >= 6) at an
+ *             aligned base take whole-word loads.
  *  X          device fp32, nb x n row-major.  Y device fp32, nb x m
  *             row-major (out).
  *  nb         1 <= nb <= EXTERND_APPLY_MAX_BATCH.
- *  workspace  device, >= externd_apply_workspace_bytes(k, nb) bytes,
- *             16-byte aligned (the k x nb intermediate diag(D) C X^T).
+ *  workspace  device, >= externd_apply_workspace_bytes(m, n, k, nb) bytes,
+ *             256-byte aligned.  nb = 1: the intermediate diag(D) C x
+ *             (4 k bytes).  nb >= 2: its bf16 parts (6 nb k bytes) and
+ *             partial sums over slices of the contracted dimensions (at
+ *             most nb max(n, m) k / 32 bytes, rounded up to whole row
+ *             groups).
  * Asynchronous on `stream`.  m, n, k <= 2^31 (else EXTERND_EUNSUPPORTED).
  */
 #define EXTERND_APPLY_MAX_BATCH 8
-size_t externd_apply_workspace_bytes(int64_t k, int32_t nb);  /* 0 on invalid arguments */
+size_t externd_apply_workspace_bytes(int64_t m, int64_t n, int64_t k, int32_t nb);  /* 0 on invalid arguments */
 int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n,
                   int64_t k, const float* X, int32_t nb, float* Y, void* workspace, size_t workspace_bytes,
                   void* stream);
@@ -252,12 +263,12 @@ int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float*
  * externd_apply without a workspace, for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc).  Same arguments, arithmetic, results
- * (bit for bit) and status codes as externd_apply, with the k x nb
- * intermediate held in a fixed device array of the library instead:
- *  - at most EXTERND_APPLY_NOALLOC_MAX_BYTES of intermediate, i.e.
- *    externd_apply_workspace_bytes(k, nb) <= that bound (k <= 65536 at
- *    nb = 8, k <= 524288 at nb = 1); larger calls return EXTERND_ESCRATCH
- *    before any device work;
+ * (bit for bit) and status codes as externd_apply, with the workspace held
+ * in a fixed device array of the library instead:
+ *  - at most EXTERND_APPLY_NOALLOC_MAX_BYTES, i.e.
+ *    externd_apply_workspace_bytes(m, n, k, nb) <= that bound (m = 9728,
+ *    n = 2560, k = 7680 takes 5.0 MB at nb = 8, 31 kB at nb = 1); larger
+ *    calls return EXTERND_ESCRATCH before any device work;
  *  - the array is per device: the current device's copy is used, and the
  *    stream must belong to the current device.  Each device keeps its copy
  *    until the process ends.  The first call on a device looks up the
@@ -269,7 +280,7 @@ int externd_apply(const uint8_t* B_packed, const uint8_t* C_packed, const float*
  *    stream are safe; nothing needs to be cleared between calls (every
  *    entry a call reads is written earlier in the same call).
  */
-#define EXTERND_APPLY_NOALLOC_MAX_BYTES (2u << 20)
+#define EXTERND_APPLY_NOALLOC_MAX_BYTES (8u << 20)
 int externd_apply_noalloc(const uint8_t* B_packed, const uint8_t* C_packed, const float* D, int64_t m, int64_t n,
                           int64_t k, const float* X, int32_t nb, float* Y, void* stream);
 

@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libexternd.so")
 
 OK, EINVAL, ENONFINITE, EWORKSPACE, EHIP, EUNSUPPORTED, ESYNC, ESCRATCH = 0, -1, -2, -3, -4, -5, -6, -7
-APPLY_NOALLOC_MAX_BYTES = 2 << 20   # EXTERND_APPLY_NOALLOC_MAX_BYTES
+APPLY_NOALLOC_MAX_BYTES = 8 << 20   # EXTERND_APPLY_NOALLOC_MAX_BYTES
 MAX_BLOCK = 256
 
 _lib = None
@@ -47,7 +47,7 @@ _SIGNATURES = {
     "externd_factorize_refined": (ctypes.c_int, [_c_ptr, _c_i64, _c_i64, _c_dbl, _c_dbl, _c_i32, _c_i32, _c_i32,
                                                  _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                                  _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr]),
-    "externd_apply_workspace_bytes": (_c_size, [_c_i64, _c_i32]),
+    "externd_apply_workspace_bytes": (_c_size, [_c_i64, _c_i64, _c_i64, _c_i32]),
     "externd_apply": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i64, _c_i64, _c_ptr, _c_i32, _c_ptr,
                                      _c_ptr, _c_size, _c_ptr]),
     "externd_apply_noalloc": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i64, _c_i64, _c_ptr, _c_i32,
@@ -255,7 +255,7 @@ def apply(B_packed, C_packed, D, m: int, n: int, X, stream=None, workspace=None)
     _req(B_packed, torch, torch.uint8, (m, (k + 3) // 4), "B_packed")
     _req(C_packed, torch, torch.uint8, (k, (n + 3) // 4), "C_packed")
     Y = torch.empty((nb, m), dtype=torch.float32, device=X.device)
-    nbytes = lib().externd_apply_workspace_bytes(k, nb)
+    nbytes = lib().externd_apply_workspace_bytes(m, n, k, nb)
     if nbytes == 0:
         raise ExterndError(EINVAL, "externd_apply_workspace_bytes")
     ws = workspace if workspace is not None else torch.empty(nbytes, dtype=torch.uint8, device=X.device)
@@ -266,7 +266,7 @@ def apply(B_packed, C_packed, D, m: int, n: int, X, stream=None, workspace=None)
 
 def apply_noalloc(B_packed, C_packed, D, m: int, n: int, X, Y=None, stream=None):
     """As ``apply`` through externd_apply_noalloc: no workspace, the
-    intermediate lives in the library's fixed per-device scratch.  ``Y``
+    workspace lives in the library's fixed per-device scratch.  ``Y``
     (nb x m fp32 CUDA tensor) may be given so that the call allocates
     nothing at all.  Returns Y."""
     torch = _torch()

@@ -125,8 +125,18 @@ def test_argument_errors_before_device_work():
              None, dummy, 16, None) == binding.EWORKSPACE
     # inference: batch limits, workspace size and alignment
     ap = L.externd_apply
-    assert L.externd_apply_workspace_bytes(100, 1) == 400 and L.externd_apply_workspace_bytes(100, 3) == 1600
-    assert L.externd_apply_workspace_bytes(100, 9) == 0 and L.externd_apply_workspace_bytes(0, 1) == 0
+    # nb = 1 (vector-ALU path): the intermediate T, k floats (k rounded up to 4), rounded up to 256 bytes
+    wsb = L.externd_apply_workspace_bytes
+    assert wsb(100, 100, 100, 1) == 512 and wsb(100, 100, 101, 1) == 512 and wsb(5, 5, 5, 1) == 256
+    # nb >= 2 (matrix-core path), 100 x 100 x 100: the parts of T (3 nb columns of 128 bf16, rounded up to
+    # 256 bytes); one slice per product, so no partial sums
+    assert wsb(100, 100, 100, 2) == 1536 and wsb(100, 100, 100, 3) == 2304
+    # 9728 x 2560 at k = 7680, nb = 8: the parts of T, then the B side's 15 slices of 9728 rows of partial
+    # sums (the C side's 10 slices of 7680 rows share the region)
+    assert wsb(9728, 2560, 7680, 8) == 24 * 7680 * 2 + 4 * 15 * 9728 * 8
+    assert wsb(9728, 2560, 7680, 8) <= 6 * 8 * 7680 + 8 * 9728 * 7680 // 32 + 4 * 256 * 8 * 15
+    assert wsb(100, 100, 100, 9) == 0 and wsb(0, 100, 100, 1) == 0 and wsb(100, 0, 100, 1) == 0
+    assert wsb(100, 100, 0, 1) == 0 and wsb(100, 100, (1 << 31) + 1, 1) == 0
     assert ap(dummy, dummy, dummy, 10, 10, 5, dummy, 0, dummy, dummy, 1 << 20, None) == binding.EINVAL
     assert ap(dummy, dummy, dummy, 10, 10, 5, dummy, 9, dummy, dummy, 1 << 20, None) == binding.EINVAL
     assert ap(None, dummy, dummy, 10, 10, 5, dummy, 1, dummy, dummy, 1 << 20, None) == binding.EINVAL
@@ -157,9 +167,13 @@ def test_apply_noalloc_rejects_before_device_work():
     assert f(d, d, d, 10, 10, 10, d, 9, d, None) == binding.EINVAL              # nb above the batch limit
     assert f(d, d, d, 0, 10, 10, d, 1, d, None) == binding.EINVAL
     assert f(d, d, d, 10, 10, 1 << 32, d, 1, d, None) == binding.EUNSUPPORTED
-    # intermediate of k x slots(nb) floats against the fixed bound
-    assert binding.APPLY_NOALLOC_MAX_BYTES == 2 << 20
-    assert L.externd_apply_workspace_bytes(65536, 8) == binding.APPLY_NOALLOC_MAX_BYTES
-    assert f(d, d, d, 10, 10, 65537, d, 8, d, None) == binding.ESCRATCH
-    assert f(d, d, d, 10, 10, 524289, d, 1, d, None) == binding.ESCRATCH
+    # the workspace of the call against the fixed bound
+    assert binding.APPLY_NOALLOC_MAX_BYTES == 8 << 20
+    wsb = L.externd_apply_workspace_bytes
+    assert wsb(9728, 2560, 7680, 8) <= binding.APPLY_NOALLOC_MAX_BYTES
+    assert wsb(10, 10, 1 << 21, 1) == binding.APPLY_NOALLOC_MAX_BYTES        # exactly fits (4 k bytes)
+    assert wsb(10, 10, (1 << 21) + 1, 1) > binding.APPLY_NOALLOC_MAX_BYTES
+    assert f(d, d, d, 10, 10, (1 << 21) + 1, d, 1, d, None) == binding.ESCRATCH
+    assert wsb(10, 1 << 20, 10, 8) > binding.APPLY_NOALLOC_MAX_BYTES
+    assert f(d, d, d, 10, 1 << 20, 10, d, 8, d, None) == binding.ESCRATCH
     assert L.externd_strerror(binding.ESCRATCH).decode().startswith("call exceeds the fixed device scratch")

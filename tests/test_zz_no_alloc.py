@@ -3,11 +3,12 @@ externd_apply (the same kernels with a caller workspace) and the oracle's
 fp64 evaluation of y = B (diag(D) (C x)) (Sec. 2.6).
 
 Both entry points run the same kernels in the same order, so their outputs
-must agree bit for bit; against the oracle the fp32 bound of the apply
-tests holds: |y - y_exact| <= (n + k + 2) 2^-24 (|B| (|D| (|C| |x|))).
-Two calls follow each other, the second smaller (fewer rows, components
-and vectors), so that the second runs on the first call's scratch contents;
-then the largest intermediate the scratch holds, and one component more.
+must agree bit for bit; against the oracle the bound of the apply tests
+holds: |y - y_exact| <= (n + k + 4) 2^-24 (|B| (|D| (|C| |x|))).
+Calls follow each other, the second smaller (fewer rows, components and
+vectors), so that it runs on the first call's scratch contents, the third
+with a single vector (the vector-ALU path); then the largest workspace the
+scratch holds along k, and one chunk of components more.
 """
 import numpy as np
 import pytest
@@ -53,13 +54,13 @@ def check_against_oracle(B, C, D, X, Y):
     n, k = C.shape[1], C.shape[0]
     Bd, Cd, Dd, Xd = (a.astype(np.float64) for a in (B, C, D, X))
     ref = oracle.apply(Bd, Cd, Dd, Xd)
-    bnd = (n + k + 2) * U * (np.abs(Bd) @ (np.abs(Dd)[:, None] * (np.abs(Cd) @ np.abs(Xd).T))).T
+    bnd = (n + k + 4) * U * (np.abs(Bd) @ (np.abs(Dd)[:, None] * (np.abs(Cd) @ np.abs(Xd).T))).T
     assert np.all(np.abs(Y.astype(np.float64) - ref) <= bnd)
 
 
 def test_noalloc_matches_apply_two_calls(ext):
-    # the second call is smaller in every dimension
-    for (m, n, k, nb, seed) in [(1000, 777, 3001, 8, 0), (301, 129, 517, 3, 1)]:
+    # the second call is smaller in every dimension; the third takes the single-vector path
+    for (m, n, k, nb, seed) in [(1000, 777, 3001, 8, 0), (301, 129, 517, 3, 1), (257, 100, 301, 1, 2)]:
         print(f"[noalloc] m={m} n={n} k={k} nb={nb}", flush=True)
         host, (Bp, Cp, D, X) = make(m, n, k, nb, seed)
         Y_ref = ext.apply(Bp, Cp, D, m, n, X)
@@ -70,9 +71,15 @@ def test_noalloc_matches_apply_two_calls(ext):
 
 
 def test_noalloc_largest_intermediate_and_caller_output(ext):
-    # k = 65536 at nb = 8 fills the scratch exactly; Y supplied by the caller
-    m, n, k, nb = 64, 40, 65536, 8
-    print(f"[noalloc] m={m} n={n} k={k} nb={nb} (scratch full)", flush=True)
+    # the largest k (a multiple of the 128-component chunk) whose workspace fits the scratch at m = 64,
+    # n = 40, nb = 8; Y supplied by the caller
+    m, n, nb = 64, 40, 8
+    wsb = ext.lib().externd_apply_workspace_bytes
+    k = 128
+    while wsb(m, n, k + 128, nb) <= ext.APPLY_NOALLOC_MAX_BYTES:
+        k += 128
+    assert wsb(m, n, k, nb) <= ext.APPLY_NOALLOC_MAX_BYTES < wsb(m, n, k + 1, nb)
+    print(f"[noalloc] m={m} n={n} k={k} nb={nb} (largest that fits)", flush=True)
     host, (Bp, Cp, D, X) = make(m, n, k, nb, 7)
     Y = torch.empty((nb, m), dtype=torch.float32, device="cuda")
     out = ext.apply_noalloc(Bp, Cp, D, m, n, X, Y=Y)
