@@ -90,7 +90,7 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(double) * BMAX * BMAX,                    // 38 gramVW
       sizeof(double) * BMAX * BMAX,                    // 39 wA0
       sizeof(double) * BMAX * BMAX,                    // 40 wA1
-      sizeof(double) * 4096,                           // 41 wPinv
+      0,                                               // 41 (unused)
       sizeof(double) * BMAX * BMAX,                    // 42 ginvUW
       sizeof(double) * BMAX * BMAX,                    // 43 ginvVW
       sizeof(double) * 4096 * NPAIR_MAX * GW_SLABS,    // 44 partwW
@@ -162,7 +162,6 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.gramVW = (double*)(b + L.off[38]);
   w.wA0 = (double*)(b + L.off[39]);
   w.wA1 = (double*)(b + L.off[40]);
-  w.wPinv = (double*)(b + L.off[41]);
   w.ginvUW = (double*)(b + L.off[42]);
   w.ginvVW = (double*)(b + L.off[43]);
   w.partwW = (double*)(b + L.off[44]);

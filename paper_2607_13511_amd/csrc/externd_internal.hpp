@@ -109,7 +109,6 @@ struct Ws {
   double* gramVW;        // BMAX x BMAX raw V^T H V (row-major), for the joint solve
   double* wA0;           // BMAX x BMAX: the matrix being swept (ping)
   double* wA1;           // BMAX x BMAX: (pong)
-  double* wPinv;         // 64 x 64: inverse of the current pivot block
   double* ginvUW;        // NQMAX x NQMAX blocks of 4096 (fp64 MFMA operand order): (U^T U + eps I)^{-1}
   double* ginvVW;        // the same for (V^T H V + eps I)^{-1}
   double* partwW;        // NPAIR_MAX x GW_SLABS x 4096: partial weighted Gram blocks

@@ -2928,16 +2928,52 @@ __global__ __launch_bounds__(NT) void k_wide_prep(int mode, const int* __restric
   const bool zero = tr == 0.0;
   if (p == 0 && threadIdx.x == 0) *wflag = zero ? 1 : 0;
   const double ridge = zero ? 0.0 : rel * tr / (double)bb;
-  for (int e = threadIdx.x; e < 4096; e += NT) {
+  // The block's values first, every load of a batch issued before any is
+  // used (a loop that stores each value would wait for each load in turn);
+  // the slabs are added in order, as one sum per entry.
+  constexpr int PER = 4096 / NT;
+  static_assert(GW_SLABS % 4 == 0, "slabs in batches of four");
+  double vals[PER];
+  if (mode == 1) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) vals[u] = 0.0;
+    for (int s0 = 0; s0 < GW_SLABS; s0 += 4) {
+      double pv[4][PER];
+#pragma unroll
+      for (int sl = 0; sl < 4; ++sl)
+#pragma unroll
+        for (int u = 0; u < PER; ++u)
+          pv[sl][u] = partwW[((int64_t)p * GW_SLABS + s0 + sl) * 4096 + threadIdx.x + NT * u];
+#pragma unroll
+      for (int sl = 0; sl < 4; ++sl)
+#pragma unroll
+        for (int u = 0; u < PER; ++u) vals[u] += pv[sl][u];
+    }
+  } else if (mode == 2) {
+    int gv[PER];
+    double rv[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = threadIdx.x + NT * u;
+      gv[u] = gaccW[(int64_t)p * 4096 + e];
+      rv[u] = raw[(int64_t)(BBP * q + (e >> 6)) * BMAX + BBP * q2 + (e & 63)];
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) vals[u] = (double)gv[u] * rv[u];
+  } else {
+    int gv[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) gv[u] = gaccW[(int64_t)p * 4096 + threadIdx.x + NT * u];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) vals[u] = (double)gv[u];
+  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + NT * u;
     const int r = e >> 6, cc = e & 63;
     const int gi = BBP * q + r, gj = BBP * q2 + cc;
     const bool real = gi < bb && gj < bb;
-    double v = 0.0;
-    if (mode == 0) v = (double)gaccW[(int64_t)p * 4096 + e];
-    else if (mode == 1) {
-      for (int s = 0; s < GW_SLABS; ++s) v += partwW[((int64_t)p * GW_SLABS + s) * 4096 + e];
-    } else
-      v = (double)gaccW[(int64_t)p * 4096 + e] * raw[(int64_t)gi * BMAX + gj];
+    double v = vals[u];
     if (!real) v = 0.0;
     if (raw && mode != 2) {
       raw[(int64_t)gi * BMAX + gj] = v;
@@ -2947,21 +2983,6 @@ __global__ __launch_bounds__(NT) void k_wide_prep(int mode, const int* __restric
     A[(int64_t)gi * BMAX + gj] = a;
     A[(int64_t)gj * BMAX + gi] = a;
   }
-}
-
-// Pivot block k of the sweep: Pinv = A_kk^{-1} (A_kk is symmetric positive
-// definite: the Schur complement of the swept blocks), on one workgroup with
-// the 64 x 64 block sweep; nk: 4 x 4 pivots holding real components.  The
-// first pivot also clears the integer Gram blocks for the next accumulation.
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_wide_pivot(
-    const double* __restrict__ A, int k, int nk, double* __restrict__ Pinv, int* gaccW, int nclear) {
-  __shared__ double Gs[4096];
-  __shared__ double pbuf[1024];
-  for (int e = threadIdx.x; e < 4096; e += NT) Gs[e] = A[(int64_t)(BBP * k + (e >> 6)) * BMAX + BBP * k + (e & 63)];
-  for (int e = threadIdx.x; e < nclear; e += NT) gaccW[e] = 0;
-  __syncthreads();
-  spd_inverse64(Gs, pbuf, nk);
-  for (int e = threadIdx.x; e < 4096; e += NT) Pinv[e] = Gs[e];
 }
 
 // C (64 x 64 block of this workgroup, rows 16 w .. of wave w) += X Y for
@@ -2978,38 +2999,104 @@ __device__ __forceinline__ void gemm64(const double* X, int64_t ldx, const doubl
   }
 }
 
-// One step of the blocked sweep (pivot block k), A -> B:
-//   B_kk = -P, B_kj = P A_kj, B_ik = A_ik P, B_ij = A_ij - A_ik P A_kj
-// with P = A_kk^{-1}; after all nq pivots B = -A^{-1}.  grid: nq x nq.
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_wide_update(
-    const double* __restrict__ A, double* __restrict__ B, const double* __restrict__ P, int k, int nq) {
-  __shared__ double T[4096];
+// C += X Y for 64 x 64 operands in LDS, both stored K-major: XT[kk][row]
+// (XT = X^T) and Y[kk][col], row strides ldx and ldy (80 doubles: lanes
+// 0..31 of a read then cover all 64 banks); the accumulator layout of
+// gemm64.
+__device__ __forceinline__ void gemm64_kmajor(const double* XT, int ldx, const double* Y, int ldy, v4d (&acc)[4]) {
+  const int lane = lane_id(), w = wave_id();
+  const int li = lane & 15, lk = lane >> 4;
+#pragma unroll 4
+  for (int ks = 0; ks < 16; ++ks) {
+    const double a = XT[(4 * ks + lk) * ldx + 16 * w + li];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma_f64(a, Y[(4 * ks + lk) * ldy + 16 * nt + li], acc[nt]);
+  }
+}
+
+// One step of the blocked sweep as one launch: every workgroup inverts the
+// pivot block itself (the same arithmetic in each, so all hold the same
+// P = A_kk^{-1}) and updates its own block, A -> B:
+//   B_kk = -P, B_kj = P A_kj, B_ik = A_ik P, B_ij = A_ij - (A_ik P) A_kj.
+// The swept matrix stays symmetric, so A_ik^T is the stored block A_ki and
+// P^T = P.  All operand blocks are loaded into LDS at once (one memory
+// latency) and the products read LDS.  nk: 4 x 4 pivots holding real
+// components; step 0 also clears the integer Gram blocks (nclear entries,
+// split over the workgroups) for the next accumulation.  grid: nq x nq.
+constexpr int SWEEP_LD = 80;
+__global__ __launch_bounds__(NT) void k_wide_step(const double* __restrict__ A, double* __restrict__ B, int k,
+                                                  int nq, int nk, int* gaccW, int nclear) {
+  __shared__ double Gs[4096];                   // the pivot block, then P (row stride 64)
+  __shared__ double pbuf[1024];
+  __shared__ double XT[BBP * SWEEP_LD];         // A_ki = A_ik^T, then (A_ik P)^T
+  __shared__ double Ys[BBP * SWEEP_LD];         // A_kj
   const int i = blockIdx.x / nq, j = blockIdx.x % nq;
   const int lane = lane_id(), w = wave_id();
   const int li = lane & 15, lk = lane >> 4;
-  const double* Aik = A + (int64_t)BBP * i * BMAX + BBP * k;
+  if (nclear) {
+    const int per = (nclear + (int)gridDim.x - 1) / (int)gridDim.x;
+    const int e0 = per * (int)blockIdx.x, e1 = e0 + per < nclear ? e0 + per : nclear;
+    for (int e = e0 + threadIdx.x; e < e1; e += NT) gaccW[e] = 0;
+  }
+  const double* Akk = A + (int64_t)BBP * k * BMAX + BBP * k;
+  const double* Aki = A + (int64_t)BBP * k * BMAX + BBP * i;
   const double* Akj = A + (int64_t)BBP * k * BMAX + BBP * j;
   const double* Aij = A + (int64_t)BBP * i * BMAX + BBP * j;
   double* Bij = B + (int64_t)BBP * i * BMAX + BBP * j;
-  v4d acc[4] = {v4d{}, v4d{}, v4d{}, v4d{}};
-  double sgn = 1.0;
-  if (i == k && j == k) {
-    for (int e = threadIdx.x; e < 4096; e += NT) Bij[(int64_t)(e >> 6) * BMAX + (e & 63)] = -P[e];
-    return;
-  } else if (i == k) {
-    gemm64(P, BBP, Akj, BMAX, acc);
-  } else if (j == k) {
-    gemm64(Aik, BMAX, P, BBP, acc);
-  } else {
-    gemm64(Aik, BMAX, P, BBP, acc);
+  const bool gen = i != k && j != k;
+  // A_ij for the general blocks, in the accumulator layout (issued first)
+  double aij[4][4];
+  if (gen) {
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) T[(16 * w + lk + 4 * r) * BBP + 16 * nt + li] = acc[nt][r];
+      for (int r = 0; r < 4; ++r) aij[nt][r] = Aij[(int64_t)(16 * w + lk + 4 * r) * BMAX + 16 * nt + li];
+  }
+  // every load of the three blocks issued before the first LDS store (a
+  // loop that stores each value would wait for each load in turn); blocks
+  // a workgroup does not use read the pivot block again
+  constexpr int PER = 4096 / NT;
+  const double* Xsrc = (j == k || gen) ? Aki : Akk;
+  const double* Ysrc = (i == k || gen) ? Akj : Akk;
+  double gv[PER], xv[PER], yv[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int e = threadIdx.x + NT * q;
+    const int64_t o = (int64_t)(e >> 6) * BMAX + (e & 63);
+    gv[q] = Akk[o];
+    xv[q] = Xsrc[o];
+    yv[q] = Ysrc[o];
+  }
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int e = threadIdx.x + NT * q;
+    const int r = e >> 6, c = e & 63;
+    Gs[e] = gv[q];
+    XT[r * SWEEP_LD + c] = xv[q];
+    Ys[r * SWEEP_LD + c] = yv[q];
+  }
+  __syncthreads();
+  spd_inverse64(Gs, pbuf, nk);  // Gs = P (ends with a barrier)
+  v4d acc[4] = {v4d{}, v4d{}, v4d{}, v4d{}};
+  double sgn = 1.0;
+  if (i == k && j == k) {
+    for (int e = threadIdx.x; e < 4096; e += NT) Bij[(int64_t)(e >> 6) * BMAX + (e & 63)] = -Gs[e];
+    return;
+  } else if (i == k) {
+    gemm64_kmajor(Gs, BBP, Ys, SWEEP_LD, acc);  // P A_kj (P^T = P)
+  } else if (j == k) {
+    gemm64_kmajor(XT, SWEEP_LD, Gs, BBP, acc);  // A_ik P
+  } else {
+    gemm64_kmajor(XT, SWEEP_LD, Gs, BBP, acc);  // T = A_ik P
+    __syncthreads();                            // every wave is done with A_ki
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) XT[(16 * nt + li) * SWEEP_LD + 16 * w + lk + 4 * r] = acc[nt][r];  // T^T
     __syncthreads();
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) acc[nt] = v4d{};
-    gemm64(T, BBP, Akj, BMAX, acc);
+    gemm64_kmajor(XT, SWEEP_LD, Ys, SWEEP_LD, acc);
     sgn = -1.0;
   }
 #pragma unroll
@@ -3017,7 +3104,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int64_t o = (int64_t)(16 * w + lk + 4 * r) * BMAX + 16 * nt + li;
-      Bij[o] = (sgn < 0.0 ? Aij[o] : 0.0) + sgn * acc[nt][r];
+      Bij[o] = (sgn < 0.0 ? aij[nt][r] : 0.0) + sgn * acc[nt][r];
     }
 }
 
@@ -3030,12 +3117,21 @@ __global__ __launch_bounds__(NT) void k_wide_ginv(const double* __restrict__ S, 
   const int i = blockIdx.x / nq, j = blockIdx.x % nq;
   const bool zero = *wflag != 0;
   double* out = ginvW + (int64_t)(i * NQMAX + j) * 4096;
-  for (int e = threadIdx.x; e < 4096; e += NT) {
+  constexpr int PER = 4096 / NT;
+  double sv[PER];  // every load before the first store
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + NT * u;
+    sv[u] = S[(int64_t)(BBP * i + (e >> 6)) * BMAX + BBP * j + (e & 63)];
+  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + NT * u;
     const int r = e >> 6, c = e & 63;
     const int gi = BBP * i + r, gj = BBP * j + c;
     double v;
     if (zero) v = (gi >= bb || gj >= bb) ? (gi == gj ? 1.0 : 0.0) : 0.0;
-    else v = -S[(int64_t)gi * BMAX + gj];
+    else v = -sv[u];
     out[ginv_index(r, c)] = v;
   }
 }
@@ -3224,23 +3320,19 @@ static int nq_of(int bb) { return (bb + BBP - 1) / BBP; }
 static int bb_of_quarter(int bb, int q) { return bb - BBP * q < BBP ? bb - BBP * q : BBP; }
 constexpr int GRAM_PAIR_SLICES = 16;  // K slices per quarter pair of the integer Gram
 
-// Blocked sweep of the matrix prepared in wA0 (nq quarters): every pivot
-// block in turn is inverted (one workgroup) and the nq x nq blocks updated;
-// *out receives the buffer holding -A^{-1}.  The first pivot launch clears
-// the integer Gram blocks.
+// Blocked sweep of the matrix prepared in wA0 (nq quarters): one launch
+// per pivot block (k_wide_step: every workgroup inverts the pivot and
+// updates its block); *out receives the buffer holding -A^{-1}.  The first
+// step clears the integer Gram blocks.
 static hipError_t wide_sweep(const Ws& w, int bb, hipStream_t s, const double** out) {
   const int nq = nq_of(bb), npairs = nq * (nq + 1) / 2;
   double* A = w.wA0;
   double* B = w.wA1;
   for (int k = 0; k < nq; ++k) {
     const int bq = bb_of_quarter(bb, k);
-    hipLaunchKernelGGL(k_wide_pivot, dim3(1), dim3(NT), 0, s, (const double*)A, k, (bq + 3) / 4, w.wPinv, w.gaccW,
-                       k == 0 ? npairs * 4096 : 0);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_wide_update, dim3((unsigned)(nq * nq)), dim3(NT), 0, s, (const double*)A, B,
-                       (const double*)w.wPinv, k, nq);
-    e = hipGetLastError();
+    hipLaunchKernelGGL(k_wide_step, dim3((unsigned)(nq * nq)), dim3(NT), 0, s, (const double*)A, B, k, nq,
+                       (bq + 3) / 4, w.gaccW, k == 0 ? npairs * 4096 : 0);
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     double* t = A;
     A = B;
