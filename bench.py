@@ -61,6 +61,31 @@ def workload(name: str):
     raise SystemExit(f"unknown workload {name}")
 
 
+def sequential_gap(w, curve, block):
+    """GPU energy minus that of the greedy sequential ALS oracle (one component
+    at a time, Sec. 2.3) at the workload's checkpoints, taken from the stored
+    full-size record of that oracle when one exists for this exact input (the
+    record carries the sha256 of the matrix). None when there is no record."""
+    path = os.path.join(ROOT, "tests", "golden", "seq", f"seq_{w.name}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    A = np.ascontiguousarray(w.A, dtype=np.float32)
+    if (rec["m"], rec["n"], rec["block"], rec["iters"]) != (A.shape[0], A.shape[1], w.block, w.iters) \
+            or rec["mu"] != w.mu or rec["tau"] != w.tau or rec["weighted"] != (w.h is not None) \
+            or hashlib.sha256(A.tobytes()).hexdigest() != rec["a_sha256"]:
+        return None
+    seq, stride = rec["seq_curve"], rec["seq_stride"]
+    out = {"record": os.path.relpath(path, ROOT), "oracle_seconds": rec["seq_seconds"], "checkpoints": {}}
+    for kc in rec["checkpoints_k"]:
+        b, s = kc // block - 1, kc // stride - 1
+        if 0 <= b < len(curve) and 0 <= s < len(seq):
+            out["checkpoints"][f"k={kc}"] = {"gpu": float(curve[b]), "sequential": seq[s],
+                                             "gpu_minus_sequential": float(curve[b]) - seq[s]}
+    return out
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
@@ -529,6 +554,7 @@ def main():
         "energy": res.E,
         "energy_w": res.E_w,
         "energy_checkpoints": checkpoints,
+        "sequential_oracle": sequential_gap(w, res.curve, res.block),
         "factors": factors,
         "arithmetic": ("fp32 residual in registers of one workgroup; fp32 per-thread partial sums combined in "
                        "fp64; fp64 thresholds, scales and energies") if dom == "sequential_one_launch" else
