@@ -61,7 +61,7 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(double) * 4096,                           // 9 ginvU
       sizeof(double) * 4096,                           // 10 ginvV
       sizeof(double) * 4096,                           // 11 gramV
-      0,                                               // 12 (unused)
+      sizeof(long long) * 4096,                        // 12 gacc64
       sizeof(int) * 4096 * NSIDE_MAX,                  // 13 gparti
       sizeof(double) * (size_t)(L.gd * L.n_pad),       // 14 colE_part
       sizeof(double) * (size_t)L.n_pad,                // 15 hw
@@ -83,17 +83,17 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       sizeof(unsigned short) * (size_t)(BMAX * L.m_pad),  // 31 Ub
       sizeof(unsigned long long) * (size_t)L.nblk_cap, // 32 argkey
       sizeof(int) * 2 * 4096,                          // 33 gacc
-      sizeof(double) * 4096 * VPREP_MAX_WG,            // 34 partw
-      sizeof(double),                                  // 35 hwmax
+      (size_t)(WDIG * L.n_pad),                        // 34 hdig
+      sizeof(double) * 2,                              // 35 hwmax
       sizeof(int) * (size_t)L.n_pad,                   // 36 cshift
-      sizeof(int) * 4096 * NPAIR_MAX,                  // 37 gaccW
+      sizeof(long long) * 4096 * NPAIR_MAX,            // 37 gaccW (int32 Grams, int64 weighted Grams)
       sizeof(double) * BMAX * BMAX,                    // 38 gramVW
       sizeof(double) * BMAX * BMAX,                    // 39 wA0
       sizeof(double) * BMAX * BMAX,                    // 40 wA1
-      0,                                               // 41 (unused)
+      (size_t)(WDIG * BMAX * L.n_pad),                 // 41 Wmf
       sizeof(double) * BMAX * BMAX,                    // 42 ginvUW
       sizeof(double) * BMAX * BMAX,                    // 43 ginvVW
-      sizeof(double) * 4096 * NPAIR_MAX * GW_SLABS,    // 44 partwW
+      0,                                               // 44 (unused)
       sizeof(int) * 64,                                // 45 wflag
   };
   size_t o = 0;
@@ -155,7 +155,9 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.Ub = (unsigned short*)(b + L.off[31]);
   w.argkey = (unsigned long long*)(b + L.off[32]);
   w.gacc = (int*)(b + L.off[33]);
-  w.partw = (double*)(b + L.off[34]);
+  w.hdig = (int8_t*)(b + L.off[34]);
+  w.Wmf = (int8_t*)(b + L.off[41]);
+  w.gacc64 = (long long*)(b + L.off[12]);
   w.hwmax = (double*)(b + L.off[35]);
   w.cshift = (int*)(b + L.off[36]);
   w.gaccW = (int*)(b + L.off[37]);
@@ -164,7 +166,6 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.wA1 = (double*)(b + L.off[40]);
   w.ginvUW = (double*)(b + L.off[42]);
   w.ginvVW = (double*)(b + L.off[43]);
-  w.partwW = (double*)(b + L.off[44]);
   w.wflag = (int*)(b + L.off[45]);
   const int64_t nrt = L.m_pad / TILE, nct = L.n_pad / TILE;
   w.ntmax = nrt > 2 * nct ? nrt : 2 * nct;
@@ -183,6 +184,7 @@ Ws quarter_view(const Ws& w, int q) {
   v.Vt = w.Vt + c0 * w.n_pad;
   v.Vr = w.Vr + c0 * w.n_pad;
   v.Vmf = w.Vmf + c0 * w.n_pad;
+  v.Wmf = w.Wmf + c0 * w.n_pad;
   v.Y = w.Y + c0 * w.n_pad;
   v.Pp = w.Pp + c0 * w.gv * w.n_pad;
   v.tps = w.tps + c0 * w.ntmax;
@@ -339,7 +341,7 @@ static hipError_t run_sweeps(const Ws& w, int64_t k, int b_eff, double tau, int3
       SWEEP_TRY(launch_finish(w, S1, s));
       for (int it = 0; it < iters; ++it) {
         SWEEP_TRY(launch_vstep(w, S1, bb, tau, s, tm, weighted));
-        SWEEP_TRY(launch_ustep(w, S1, bb, tau, weighted, it == iters - 1, s, tm, weighted));
+        SWEEP_TRY(launch_ustep(w, S1, bb, tau, weighted, it == iters - 1, s, tm));
       }
       SWEEP_TRY(launch_gram_acc(w, 0, s));
       SWEEP_TRY(launch_revisit_decide(w, bb, D + c0, weighted, S, S1, s));
@@ -434,7 +436,7 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
         // a wide block: its quarters coupled through the Gram inverses
         HIP_TRY(launch_init_wide(w, bb, tau, s));
         for (int it = 0; it < iters; ++it) {
-          HIP_TRY(launch_vstep_wide(w, (int)blk, bb, tau, s, tm));
+          HIP_TRY(launch_vstep_wide(w, (int)blk, bb, tau, s, tm, weighted));
           HIP_TRY(launch_ustep_wide(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm));
         }
         HIP_TRY(launch_block_out_wide(w, c0, bb, k, B_packed, C_packed, D, s));
@@ -443,7 +445,7 @@ static int factorize_impl(const float* A, int64_t m, int64_t n, double mu, doubl
         HIP_TRY(launch_init(w, bb, tau, s));
         for (int it = 0; it < iters; ++it) {
           HIP_TRY(launch_vstep(w, (int)blk, bb, tau, s, tm, weighted));
-          HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm, weighted));
+          HIP_TRY(launch_ustep(w, (int)blk, bb, tau, weighted, it == iters - 1, s, tm));
         }
         HIP_TRY(launch_gram_acc(w, 0, s));  // U^T U of the final U, for the scale solve
         if (safeguard) HIP_TRY(launch_safeguard(w, (int)blk, bb, D + c0, s));
@@ -636,6 +638,7 @@ int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, in
   HIP_TRY(launch_prep(w, h, s));
   HIP_TRY(launch_stage(w, R, n, s));
   HIP_TRY(load_factor_quarters(w, 1, V, n, bb, s));
+  if (h) HIP_TRY(launch_vweight(w, bb, s));
   HIP_TRY(bb > BBP ? launch_ustep_wide(w, 0, bb, tau, h != nullptr, false, s)
                    : launch_ustep(w, 0, bb, tau, h != nullptr, false, s));
   HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
@@ -654,6 +657,7 @@ int externd_step_scale(const int8_t* U, const int8_t* V, const double* Q, int64_
   HIP_TRY(launch_prep(w, h, s));
   HIP_TRY(load_factor_quarters(w, 0, U, m, bb, s));
   HIP_TRY(load_factor_quarters(w, 1, V, n, bb, s));
+  if (h) HIP_TRY(launch_vweight(w, bb, s));
   HIP_TRY(launch_load_cm(w.Q, Q, m, w.m_pad, bb, s));
   HIP_TRY(launch_gvec(w, bb, s));
   if (bb > BBP) {

@@ -24,7 +24,6 @@ constexpr int TILE = 32;
 constexpr int NQMAX = 4;
 constexpr int BMAX = NQMAX * BBP;
 constexpr int NPAIR_MAX = NQMAX * (NQMAX + 1) / 2;  // quarter pairs q <= q'
-constexpr int GW_SLABS = 16;                          // row slabs of the wide weighted Gram
 // Workgroups that build integer Gram matrices (int8 MFMA), beside a
 // contraction or in a launch of their own.
 constexpr int NSIDE_INT = 8;   // integer-Gram workgroups of the scale solve
@@ -38,6 +37,11 @@ constexpr int USTEP_SLOTS = 512;
 constexpr int DEFLATE_SLOTS = 512;
 // Threads per workgroup for all kernels except the selection kernel.
 constexpr int NT = 256;
+// Weighted Grams on int8 MFMA: the weights h~_j / max h~ as integers of at
+// most WSHIFT_MAX bits, split into WDIG digit planes of WDIG_BITS bits.
+constexpr int WDIG = 6;
+constexpr int WDIG_BITS = 7;
+constexpr int WSHIFT_MAX = WDIG * WDIG_BITS;
 constexpr int NT_SELECT = 1024;
 // Ternarization: workgroups per component (each takes a 32-aligned chunk
 // of about TERN_CHUNK entries; at most TERN_SPLIT_MAX per component).
@@ -99,19 +103,23 @@ struct Ws {
                          // U-step's fixed-point exponent of row i; measured by every U-step, raised
                          // by every deflation
   float* rowb_part;      // (n_pad/32) x m_pad: per-column-strip row maxima from staging
-  double* hwmax;         // 1: max_j h~_j (1 + lambda with weights, 1 without)
+  double* hwmax;         // 2: max_j h~_j (1 + lambda with weights, 1 without), then the unit of the
+                         // weighted integer Grams (max h~ 2^-wshift)
   int* cshift;           // n_pad: the V-step's fixed-point exponent of column j, from ||R_:j||^2
                          // (written with the energy reduction after staging and each deflation)
   unsigned long long* argkey;  // nblk_cap: (max|R| bits << 32) | (2^32 - 1 - first row-major index), safeguard only
-  double* partw;               // VPREP_MAX_WG x 64 x 64: partial weighted Grams V^T diag(h~) V
+  int8_t* hdig;          // WDIG x n_pad: digit planes of the quantized weights (weighted Grams)
+  int8_t* Wmf;           // WDIG x BMAX x n_pad: V with row j scaled by digit d of the weight, plane d
+                         // at d BMAX n_pad, each plane in the layout of Vmf
+  long long* gacc64;     // 4096: weighted Gram accumulator of the U-step (V^T diag(H) V)
   // wide blocks
-  int* gaccW;            // NPAIR_MAX x 4096: integer Gram blocks X_q^T X_q' (q <= q') of a factor
+  int* gaccW;            // NPAIR_MAX x 4096: integer Gram blocks X_q^T X_q' (q <= q') of a factor (int32;
+                         // int64 for the weighted Grams of V)
   double* gramVW;        // BMAX x BMAX raw V^T H V (row-major), for the joint solve
   double* wA0;           // BMAX x BMAX: the matrix being swept (ping)
   double* wA1;           // BMAX x BMAX: (pong)
   double* ginvUW;        // NQMAX x NQMAX blocks of 4096 (fp64 MFMA operand order): (U^T U + eps I)^{-1}
   double* ginvVW;        // the same for (V^T H V + eps I)^{-1}
-  double* partwW;        // NPAIR_MAX x GW_SLABS x 4096: partial weighted Gram blocks
   int* wflag;            // 1: the swept matrix had zero trace
   double* fro2_hist;     // nblk_cap: ||R||^2 before each block, then after the last
   double* fro2w_hist;    // nblk_cap: weighted ||R||^2
@@ -161,8 +169,6 @@ struct Timer {
   } while (0)
 
 size_t workspace_bytes(int64_t m, int64_t n, int64_t k);
-// Workgroups of the weighted-Gram preparation (each covers >= 32 rows of V).
-constexpr int VPREP_MAX_WG = 128;
 bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k);
 
 // ---- launchers (all asynchronous on `s`) ----
@@ -174,21 +180,22 @@ hipError_t launch_select(const Ws& w, int blk, int bb, hipStream_t s);
 hipError_t launch_finish(const Ws& w, int blk, hipStream_t s);
 hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s);
 // The contraction launches build the Gram of their factor themselves (side
-// workgroups); launch_gram_acc serves the scale solve.
-// weighted: V is thresholded by row blocks, which also leaves the partials
-// of V^T diag(h~) V for the next U-step.
+// workgroups; weighted U-step: V^T diag(H) V from the weights' digit
+// planes); launch_gram_acc serves the scale solve.
+// weighted: the V-step also writes the digit-scaled planes of V (Wmf) for
+// the weighted Gram of the next U-step.
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr,
                         bool weighted = false);
 // final: the last U-step of a block, which also forms g = diag(U^T Q) for
-// the scale solve.  v_partials: the preceding V-step was launched weighted
-// (its partials of V^T diag(h~) V are in place); else they are formed here.
+// the scale solve.
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
-                        Timer* t = nullptr, bool v_partials = false);
+                        Timer* t = nullptr);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
 // Wide blocks (64 < bb <= BMAX): the same steps over the quarters of the
 // block, coupled through the BMAX x BMAX Gram inverses and joint solve.
 hipError_t launch_init_wide(const Ws& w, int bb, double tau, hipStream_t s);
-hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr);
+hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* t = nullptr,
+                             bool weighted = false);
 hipError_t launch_ustep_wide(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
                              Timer* t = nullptr);
 hipError_t launch_scale_wide(const Ws& w, int bb, float* D_block, hipStream_t s);
@@ -234,7 +241,9 @@ hipError_t launch_load_cm(double* Xcm, const double* X, int64_t len, int64_t len
 hipError_t launch_unstage(const Ws& w, float* A, hipStream_t s);
 hipError_t launch_colnorms(const Ws& w, int blk, double* colnorm2, double* fro2, hipStream_t s);
 hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s);
-hipError_t launch_gram_w(const Ws& w, hipStream_t s);
+// The digit-scaled planes of a V loaded from the caller (Wmf), for the
+// weighted Gram of the step entry points.
+hipError_t launch_vweight(const Ws& w, int bb, hipStream_t s);
 hipError_t launch_gvec(const Ws& w, int bb, hipStream_t s);
 // X^T X of the factor in Umf (which = 0) or Vmf (which = 1) into its Gram accumulator.
 hipError_t launch_gram_acc(const Ws& w, int which, hipStream_t s);

@@ -80,14 +80,16 @@ __device__ __forceinline__ unsigned fx_biased(float x, int s) {
 __device__ __forceinline__ unsigned fx_biased_m(float x, float p2s) {
   return (unsigned)(int)__builtin_rintf(x * p2s) + 0x00808080u;
 }
-// Weighted: x fw rounded to the nearest integer (ties to even) in one
-// step.  Adding 1.5 2^52 inside the fma rounds the exact product at unit
-// spacing, so for |x fw| < 2^31 the low word of the result is that integer
-// in two's complement.
-__device__ __forceinline__ unsigned fx_biased_w(float x, double fw) {
-  const double t = __builtin_fma((double)x, fw, 6755399441055744.0);
+// Weighted: x hw 2^s rounded to the nearest integer (ties to even) in one
+// step, with c = 1.5 2^(52 - s) (weighted_round_const).  Adding c inside
+// the fma rounds the exact product x hw at spacing 2^-s, so for
+// |x hw 2^s| < 2^31 the low word of the result is that integer in two's
+// complement.
+__device__ __forceinline__ unsigned fx_biased_w(float x, double hw, double c) {
+  const double t = __builtin_fma((double)x, hw, c);
   return (unsigned)__double2loint(t) + 0x00808080u;
 }
+__device__ __forceinline__ double weighted_round_const(int s) { return ldexp(1.5, 52 - s); }
 
 // Upper bound (fp32) on |v| * hw for the weighted fixed-point scale: the
 // fp64 product rounded to fp32, inflated by 2^-20 so that rounding can never
@@ -682,6 +684,175 @@ __device__ __forceinline__ bool side_gram_acc(const v4i* __restrict__ Xmf, int64
   return true;
 }
 
+// ---------------------------------------------------------------------------
+// Weighted Gram X_a^T diag(h~) X_b of ternary factors (Sec. 2.5) on int8
+// MFMA.  The weights enter as the integers
+//   H_j = min(rint(h~_j / max h~ 2^w), 2^w - 1),  w = min(WSHIFT_MAX, 61 - ceil(log2 n_pad)),
+// split into WDIG planes of WDIG_BITS-bit digits (hdig[d * n_pad + j], digit d
+// of H_j, least significant first; written once per call by k_prep), so that
+//   sum_j H_j x_jc y_jc' = sum_d 128^d sum_j dig_d(j) x_jc y_jc'
+// is an exact integer below 2^61: every product digit x trit lies in
+// [-127, 127] and is itself an int8 MFMA operand.  The Gram is that integer
+// times the unit max h~ 2^-w.  With w = 42 (n_pad <= 2^19) each weight
+// differs from h~_j by at most 2^-43 max h~, the order of the rounding of
+// an fp64 sum over the n weights.  The operands dig_d(j) y_jc are formed
+// where V is made (Wmf: plane d at d * wstride, the MFMA-ready layout of
+// V), so that the Gram itself is loads and MFMAs only.
+// ---------------------------------------------------------------------------
+// Bytes t (trits: 0x00, 0x01, 0xFF) times bytes d (digits 0..127), byte by
+// byte: d where t = 1, -d where t = -1 (two's complement ~d + 1, the + 1
+// added below bit 7 of each byte, so no carry crosses a byte), 0 where t = 0.
+__device__ __forceinline__ int trit_times_digit(int t, int d) {
+  const unsigned tu = (unsigned)t;
+  const unsigned one = tu & 0x01010101u;         // 1 in the bytes where t != 0
+  const unsigned neg = (tu >> 7) & 0x01010101u;  // 1 in the bytes where t < 0
+  const unsigned y = ((unsigned)d & (one * 0xFFu)) ^ (neg * 0xFFu);
+  return (int)(((y & 0x7F7F7F7Fu) + neg) ^ (y & 0x80808080u));
+}
+
+// The accumulator blocks of a 64 x 64 int8-MFMA Gram (00, 01, 10, 11; SAME:
+// 10 = 01^T is neither formed nor stored) to mine (4096 int32, row-major).
+template <bool SAME>
+__device__ __forceinline__ void store_gram_blocks(const v16i* acc, int* mine) {
+  const int lane = lane_id();
+  const int h = lane >> 5, l32 = lane & 31;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int M = 8 * (r >> 2) + 4 * h + (r & 3);
+    const int N = l32;
+    mine[M * 64 + N] = acc[0][r];
+    mine[M * 64 + 32 + N] = acc[1][r];
+    if (!SAME) mine[(32 + M) * 64 + N] = acc[2][r];
+    mine[(32 + M) * 64 + 32 + N] = acc[SAME ? 2 : 3][r];
+  }
+}
+
+// X_a^T diag(H) X_b over the K steps [ks0, ks1) (MFMA-ready layouts: Xa,
+// and Wb = the digit-scaled planes of X_b, plane stride wstride bytes;
+// SAME: X_b = X_a, a symmetric Gram of which the lower-left 32 x 32 block
+// is left out), added into g64 (int64 atomics on the nonzero entries:
+// exact, order-free).  Wave w forms plane w over all the K steps (A) and
+// plane 4 + w / 2 over half of them (B).  The planes are added through LDS
+// in two rounds, A then B, into int64 per entry (every partial sum stays
+// below 2^42 * 32 (ks1 - ks0)).  blockDim == NT.  red: LDS, 4 x 4096 int32.
+static_assert(WDIG == 6 && NT == 256, "planes 0-3 on the four waves, 4-5 on wave pairs");
+template <bool SAME>
+__device__ __forceinline__ void gram_w_accumulate(const v4i* Xa, const int8_t* Wb, int64_t wstride, int ks0,
+                                                  int ks1, long long* g64, int* red) {
+  constexpr int KR = SAME ? 4 : 2;  // K steps of loads in flight (register budget of two waves per SIMD)
+  constexpr int NB = SAME ? 3 : 4;
+  const int lane = lane_id(), wave = wave_id();
+  const int kmid = ks0 + (ks1 - ks0 + 1) / 2;
+  const int kb0 = (wave & 1) ? kmid : ks0, kb1 = (wave & 1) ? ks1 : kmid;
+  const v4i* WA = (const v4i*)(Wb + (int64_t)wave * wstride);
+  const v4i* WB = (const v4i*)(Wb + (int64_t)(4 + (wave >> 1)) * wstride);
+  v16i accA[NB], accB[NB];
+#pragma unroll
+  for (int q = 0; q < NB; ++q) accA[q] = accB[q] = v16i{};
+  for (int ks = ks0; ks < ks1; ks += KR) {
+    v4i a[KR][2], wa[KR][2], wb[KR][2];
+#pragma unroll
+    for (int u = 0; u < KR; ++u) {
+      // every load from a clamped K step (a load under a branch would be
+      // waited for before the next one is issued); the steps past ks1 are
+      // skipped below
+      const int64_t kk = ks + u < ks1 ? ks + u : ks0;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        a[u][t] = Xa[kk * 128 + 64 * t + lane];
+        wa[u][t] = WA[kk * 128 + 64 * t + lane];
+        wb[u][t] = WB[kk * 128 + 64 * t + lane];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < KR; ++u) {
+      const int kk = ks + u;
+      if (kk < ks1) {  // uniform over the wave
+        accA[0] = mfma_i8(a[u][0], wa[u][0], accA[0]);
+        accA[1] = mfma_i8(a[u][0], wa[u][1], accA[1]);
+        if (!SAME) accA[2] = mfma_i8(a[u][1], wa[u][0], accA[2]);
+        accA[NB - 1] = mfma_i8(a[u][1], wa[u][1], accA[NB - 1]);
+        if (kk >= kb0 && kk < kb1) {  // uniform over the wave
+          accB[0] = mfma_i8(a[u][0], wb[u][0], accB[0]);
+          accB[1] = mfma_i8(a[u][0], wb[u][1], accB[1]);
+          if (!SAME) accB[2] = mfma_i8(a[u][1], wb[u][0], accB[2]);
+          accB[NB - 1] = mfma_i8(a[u][1], wb[u][1], accB[NB - 1]);
+        }
+      }
+    }
+  }
+  constexpr int PER = 4096 / NT;
+  long long v[PER];
+  store_gram_blocks<SAME>(accA, red + wave * 4096);
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int e = threadIdx.x + NT * j;
+    const long long r0 = red[e], r1 = red[4096 + e], r2 = red[8192 + e], r3 = red[12288 + e];
+    v[j] = r0 + (r1 << WDIG_BITS) + (r2 << (2 * WDIG_BITS)) + (r3 << (3 * WDIG_BITS));
+  }
+  __syncthreads();  // red is rewritten by round B
+  store_gram_blocks<SAME>(accB, red + wave * 4096);
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int e = threadIdx.x + NT * j;
+    const long long r0 = red[e], r1 = red[4096 + e], r2 = red[8192 + e], r3 = red[12288 + e];
+    v[j] += ((r0 + r1) << (4 * WDIG_BITS)) + ((r2 + r3) << (5 * WDIG_BITS));
+  }
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int e = threadIdx.x + NT * j;
+    const bool stored = !SAME || (e >> 6) < 32 || (e & 63) >= 32;  // SAME: no lower-left block
+    if (stored && v[j]) __hip_atomic_fetch_add(g64 + e, v[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// The symmetric weighted Gram from its accumulator (upper-left, upper-right
+// and lower-right blocks; the lower-left one is the transpose of the
+// upper-right): G (LDS, fp64) = g64 * unit, with coherent loads (the
+// atomics of the other workgroups belong to the same launch); g64 is
+// cleared for the next accumulation.
+__device__ __forceinline__ void take_gram_w(long long* g64, double unit, double* G) {
+  constexpr int PER = 4096 / NT;
+  long long v[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int e = threadIdx.x + NT * j, r = e >> 6, c = e & 63;
+    v[j] = load_coherent(g64 + ((r >= 32 && c < 32) ? c * 64 + r : e));
+  }
+#pragma unroll
+  for (int j = 0; j < PER; ++j) G[threadIdx.x + NT * j] = (double)v[j] * unit;
+  __syncthreads();  // every entry has been read before any is cleared
+#pragma unroll
+  for (int j = 0; j < PER; ++j) g64[threadIdx.x + NT * j] = 0;
+  __syncthreads();
+}
+
+// Side workgroup `side` of `nside` adds its share of the K steps of
+// V^T diag(H) V (V and its digit-scaled planes Wmf) into g64; the last to
+// arrive (arrival counter, reset by it)
+// takes the weighted Gram into G.  red: LDS, 4 x 4096 int32 (may alias G).
+__device__ __forceinline__ bool side_gram_w(const v4i* __restrict__ Vmf, const int8_t* __restrict__ Wmf,
+                                            int64_t wstride, int64_t n_pad, int side, int nside, long long* g64,
+                                            double unit, unsigned* counter, double* G, int* red) {
+  const int nks = (int)(n_pad / TILE);
+  gram_w_accumulate<true>(Vmf, Wmf, wstride, (int)((long long)side * nks / nside),
+                          (int)((long long)(side + 1) * nks / nside), g64, red);
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's atomics have been performed
+  __shared__ int s_last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (old == (unsigned)(nside - 1));
+  }
+  __syncthreads();
+  if (!s_last) return false;
+  if (threadIdx.x == 0) store_coherent(counter, 0u);
+  take_gram_w(g64, unit, G);
+  return true;
+}
+
 // Consumer (a later launch than the producer, so plain accesses suffice):
 // the accumulated Gram into G (LDS, fp64); gacc is cleared for the next
 // accumulation.  blockDim == NT: 16 entries per thread, loaded in one round.
@@ -892,284 +1063,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   tile_stats(y, w, j0, (j0 + 16 < n ? j0 + 16 : n), ntile, tile, ps, pm, pi);
 }
 // ---------------------------------------------------------------------------
-// Weighted U-step preparation (Sec. 2.5): V row-major (Vr) from the
-// component-major Vt, and this workgroup's partial of the weighted Gram
-// V^T diag(h~) V on fp64 MFMA (v_mfma_f64_16x16x4; the products
-// h~_j v_jc v_jc' are exact, the sums fp64 in a fixed order), the 10 16x16
-// tiles of the upper triangle dealt to the 4 waves.  Workgroup g
-// covers rows [g rows_wg, (g + 1) rows_wg), staged in LDS in chunks of
-// VPREP_CHUNK, and writes its partial to partw[g]; k_gramw_sum adds the
-// partials in workgroup order.  Running before the U-step launch, the Gram
-// does not compete with the residual stream.
-// grid: ceil(n_pad / rows_wg) <= VPREP_MAX_WG.
-// ---------------------------------------------------------------------------
-constexpr int VPREP_CHUNK = 128;
-constexpr int VPREP_MIN_ROWS = 32;
-// tile tt in 0..9 of the upper triangle of 16x16 tiles -> (row tile, column
-// tile); the rows of the triangle start at tiles 0, 4, 7, 9.  Wave w takes
-// tiles w, w + 4 and (waves 0, 1) w + 8.
-__host__ __device__ constexpr int vprep_tm(int tt) { return (tt >= 4) + (tt >= 7) + (tt >= 9); }
-__host__ __device__ constexpr int vprep_tn(int tt) {
-  return vprep_tm(tt) + tt - (vprep_tm(tt) == 0 ? 0 : vprep_tm(tt) == 1 ? 4 : vprep_tm(tt) == 2 ? 7 : 9);
-}
-// One chunk of nr staged rows into wave W's accumulators: the tile indices are
-// compile-time, so the accumulators stay in place and the three chains interleave.
-template <int W>
-__device__ __forceinline__ void vprep_gram_chunk(const int8_t (*tile)[BBP + 4], const double* hws, int nr, int i16,
-                                                 int kq, v4d* acc) {
-  constexpr int NTILE = W < 2 ? 3 : 2;
-  // nr is a multiple of 32: eight 4-row steps per pass, their LDS reads batched
-  for (int k0 = 0; k0 < nr / 4; k0 += 8) {
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const int r = 4 * (k0 + kk) + kq;
-      double v[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = (double)tile[r][16 * q + i16];
-      const double wr = hws[r];
-#pragma unroll
-      for (int q = 0; q < NTILE; ++q)
-        acc[q] = mfma_f64(wr * v[vprep_tm(W + 4 * q)], v[vprep_tn(W + 4 * q)], acc[q]);
-    }
-  }
-}
-template <int W>
-__device__ __forceinline__ void vprep_gram_store(double* mine, int i16, int kq, const v4d* acc) {
-  constexpr int NTILE = W < 2 ? 3 : 2;
-#pragma unroll
-  for (int q = 0; q < NTILE; ++q) {
-    const int mt = vprep_tm(W + 4 * q), nt = vprep_tn(W + 4 * q);
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      // v_mfma_f64_16x16x4f64 result: lane l, register r holds row l/16 + 4 r, column l%16
-      mine[(16 * mt + kq + 4 * r) * BBP + 16 * nt + i16] = acc[q][r];
-  }
-}
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vprep_w(const int8_t* __restrict__ Vt, int8_t* __restrict__ Vr, int64_t n_pad,
-                                                const double* __restrict__ hw, int rows_wg,
-                                                double* __restrict__ partw) {
-  __shared__ int8_t tile[VPREP_CHUNK][BBP + 4];
-  __shared__ double hws[VPREP_CHUNK];
-  const int lane = lane_id(), wave = wave_id();
-  const int i16 = lane & 15, kq = lane >> 4;
-  v4d acc[3] = {v4d{}, v4d{}, v4d{}};
-  const int64_t r0 = (int64_t)blockIdx.x * rows_wg;
-  const int64_t r1 = r0 + rows_wg < n_pad ? r0 + rows_wg : n_pad;
-  for (int64_t j0 = r0; j0 < r1; j0 += VPREP_CHUNK) {
-    const int nr = (int)(r1 - j0 < VPREP_CHUNK ? r1 - j0 : VPREP_CHUNK);  // a multiple of 32
-    __syncthreads();  // the previous chunk has been consumed
-    // 16-byte pieces: piece p of component c holds rows j0 + 16 p .. + 15
-    const int npc = nr / 16;
-    int4 piece[2];
-    double hwv = 0.0;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int e = threadIdx.x + NT * u, c = e / npc, p = e % npc;
-      if (e < BBP * npc) piece[u] = *(const int4*)(Vt + (int64_t)c * n_pad + j0 + 16 * p);
-    }
-    if (threadIdx.x < nr) hwv = hw[j0 + threadIdx.x];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int e = threadIdx.x + NT * u, c = e / npc, p = e % npc;
-      if (e < BBP * npc) {
-        const int8_t* b = (const int8_t*)&piece[u];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) tile[16 * p + q][c] = b[q];
-      }
-    }
-    if (threadIdx.x < nr) hws[threadIdx.x] = hwv;
-    __syncthreads();
-    // row-major copy: 16-byte pieces of 64-byte rows
-    for (int e = threadIdx.x; e < nr * (BBP / 16); e += NT) {
-      const int jj = e >> 2, p = e & 3;
-      int4 v;
-      int8_t* vb = (int8_t*)&v;
-#pragma unroll
-      for (int q = 0; q < 16; ++q) vb[q] = tile[jj][16 * p + q];
-      *(int4*)(Vr + (j0 + jj) * BBP + 16 * p) = v;
-    }
-    // wave is uniform: each branch runs one wave's compile-time tile set
-    switch (wave) {
-      case 0: vprep_gram_chunk<0>(tile, hws, nr, i16, kq, acc); break;
-      case 1: vprep_gram_chunk<1>(tile, hws, nr, i16, kq, acc); break;
-      case 2: vprep_gram_chunk<2>(tile, hws, nr, i16, kq, acc); break;
-      default: vprep_gram_chunk<3>(tile, hws, nr, i16, kq, acc); break;
-    }
-  }
-  double* mine = partw + (int64_t)blockIdx.x * (BBP * BBP);
-  switch (wave) {
-    case 0: vprep_gram_store<0>(mine, i16, kq, acc); break;
-    case 1: vprep_gram_store<1>(mine, i16, kq, acc); break;
-    case 2: vprep_gram_store<2>(mine, i16, kq, acc); break;
-    default: vprep_gram_store<3>(mine, i16, kq, acc); break;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Weighted V-step thresholding by row blocks (Sec. 2.5): V <- T_tau(Y^T) for
-// every component over rows [r0, r0 + rows_wg), so that the workgroup holds
-// whole rows of V and adds its share of the weighted Gram V^T diag(h~) V
-// into partw[blockIdx.x] (the k_vprep_w arithmetic: fp64 MFMA, exact
-// products, fixed order); the U-step's side workgroups add the partials.
-// Every workgroup forms the 64 thresholds of Eq. (2) from the per-tile
-// statistics: four threads per component take every fourth tile, combined
-// in a fixed order.  Writes Vt (component-major) and Vmf.
-// grid: ceil(n_pad / rows_wg) <= VPREP_MAX_WG; rows_wg a multiple of 32,
-// at most VPREP_CHUNK.
-// ---------------------------------------------------------------------------
-constexpr int TVW_TS = 40;  // statistics tiles per thread and round
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_tern_vw(
-    const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb, double tau, const double* __restrict__ ps,
-    const double* __restrict__ pm, const int* __restrict__ pi, int ntile, int8_t* __restrict__ Vt,
-    int8_t* __restrict__ Vmf, const double* __restrict__ hw, int rows_wg, double* __restrict__ partw) {
-  __shared__ int8_t tile[VPREP_CHUNK][BBP + 4];
-  __shared__ double hws[VPREP_CHUNK];
-  const int tid = threadIdx.x;
-  const int c = tid >> 2, sub = tid & 3;
-  const int64_t r0 = (int64_t)blockIdx.x * rows_wg;
-  const int nr = (int)(n_pad - r0 < rows_wg ? n_pad - r0 : rows_wg);  // a multiple of 32
-  if (tid < nr) hws[tid] = hw[r0 + tid];
-  // rows r0 + sub * rpt .. + rpt of component c, eight at a time (Vt and
-  // Vmf take them as 8 contiguous bytes); the first eight are loaded before
-  // the statistics, which do not depend on them
-  const int rpt = nr >> 2;  // a multiple of 8
-  const double* yc = Y + (int64_t)c * n_pad;
-  double y[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) y[k] = yc[r0 + sub * rpt + k];
-  // threshold of component c: sum and max of |y| over its tiles
-  const double* psc = ps + (int64_t)c * ntile;
-  const double* pmc = pm + (int64_t)c * ntile;
-  const int* pic = pi + (int64_t)c * ntile;
-  double S = 0.0, M = -1.0;
-  for (int t0 = 0; t0 < ntile; t0 += 4 * TVW_TS) {
-    double a[TVW_TS], b[TVW_TS];
-#pragma unroll
-    for (int u = 0; u < TVW_TS; ++u) {
-      const int t = t0 + sub + 4 * u, tc = t < ntile ? t : 0;
-      a[u] = psc[tc];
-      b[u] = pmc[tc];
-    }
-#pragma unroll
-    for (int u = 0; u < TVW_TS; ++u)
-      if (t0 + sub + 4 * u < ntile) {
-        S += a[u];
-        M = fmax(M, b[u]);
-      }
-  }
-  S += __shfl_xor(S, 1, 64);
-  S += __shfl_xor(S, 2, 64);
-  M = fmax(M, __shfl_xor(M, 1, 64));
-  M = fmax(M, __shfl_xor(M, 2, 64));
-  const double theta = tau * (S / (double)n);
-  const bool zero = c >= bb;
-  const bool keep_max = !(M > theta);
-  int mi = 0x7fffffff;
-  if (keep_max && !zero) {
-    // the smallest index attaining the maximum: the smallest tile argmax
-    // among the tiles whose maximum is M (the four lanes of c agree)
-    for (int t = sub; t < ntile; t += 4)
-      if (pmc[t] == M) mi = min(mi, pic[t]);
-    mi = min(mi, __shfl_xor(mi, 1, 64));
-    mi = min(mi, __shfl_xor(mi, 2, 64));
-  }
-  for (int k0 = 0; k0 < rpt; k0 += 8) {
-    const int64_t j0 = r0 + sub * rpt + k0;
-    if (k0) {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) y[k] = yc[j0 + k];
-    }
-    unsigned long long packed = 0ull;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int64_t j = j0 + k;
-      const double yv = y[k];
-      const bool on = !zero && j < n && (keep_max ? (j == mi) : (fabs(yv) > theta));
-      const int8_t t = on ? ((yv > 0.0) ? 1 : ((yv < 0.0) ? -1 : 0)) : 0;
-      tile[j - r0][c] = t;
-      packed |= (unsigned long long)(uint8_t)t << (8 * k);
-    }
-    *(unsigned long long*)(Vt + (int64_t)c * n_pad + j0) = packed;
-    *(unsigned long long*)(Vmf + mf_offset(c, j0)) = packed;
-  }
-  __syncthreads();
-  const int lane = lane_id(), wave = wave_id();
-  const int i16 = lane & 15, kq = lane >> 4;
-  v4d acc[3] = {v4d{}, v4d{}, v4d{}};
-  switch (wave) {
-    case 0: vprep_gram_chunk<0>(tile, hws, nr, i16, kq, acc); break;
-    case 1: vprep_gram_chunk<1>(tile, hws, nr, i16, kq, acc); break;
-    case 2: vprep_gram_chunk<2>(tile, hws, nr, i16, kq, acc); break;
-    default: vprep_gram_chunk<3>(tile, hws, nr, i16, kq, acc); break;
-  }
-  double* mine = partw + (int64_t)blockIdx.x * (BBP * BBP);
-  switch (wave) {
-    case 0: vprep_gram_store<0>(mine, i16, kq, acc); break;
-    case 1: vprep_gram_store<1>(mine, i16, kq, acc); break;
-    case 2: vprep_gram_store<2>(mine, i16, kq, acc); break;
-    default: vprep_gram_store<3>(mine, i16, kq, acc); break;
-  }
-}
-
-// One entry of the weighted Gram from nwg partials, in the order of
-// k_gramw_sum: partials q, q + 4, ... per quarter q, then the quarters in
-// order.
-__device__ __forceinline__ double gramw_entry(const double* __restrict__ partw, int nwg, int e) {
-  double qs[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    double sum = 0.0;
-    const int nk = (nwg - q + 3) / 4;
-    for (int k0 = 0; k0 < nk; k0 += 8) {
-      double v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int g = q + 4 * (k0 + u);
-        v[u] = partw[(int64_t)(g < nwg ? g : 0) * (BBP * BBP) + e];
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (k0 + u < nk) sum += v[u];
-    }
-    qs[q] = sum;
-  }
-  return ((qs[0] + qs[1]) + qs[2]) + qs[3];
-}
-
-// The weighted Gram from the partials of k_vprep_w, added in a fixed order
-// (workgroups q, q + 4, ... per quarter q, then the quarters in order), both
-// triangles into gramV.  Workgroup b takes the 64 entries [64 b, 64 b + 64).
-// grid: BBP * BBP / 64.
-__global__ __launch_bounds__(NT) void k_gramw_sum(const double* __restrict__ partw, int nwg,
-                                                  double* __restrict__ gramV) {
-  __shared__ double q4[4][64];
-  const int el = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int e = blockIdx.x * 64 + el, c = e >> 6, c2 = e & 63;
-  double v[VPREP_MAX_WG / 4];
-#pragma unroll
-  for (int k = 0; k < VPREP_MAX_WG / 4; ++k) {
-    const int g = q + 4 * k;
-    v[k] = (c <= c2 && g < nwg) ? partw[(int64_t)g * (BBP * BBP) + e] : 0.0;
-  }
-  double sum = 0.0;
-#pragma unroll
-  for (int k = 0; k < VPREP_MAX_WG / 4; ++k) sum += v[k];
-  q4[q][el] = sum;
-  __syncthreads();
-  if (q == 0 && c <= c2) {
-    const double d = ((q4[0][el] + q4[1][el]) + q4[2][el]) + q4[3][el];
-    gramV[e] = d;
-    gramV[c2 * BBP + c] = d;
-  }
-}
-
-// ---------------------------------------------------------------------------
 // U-step Q = R diag(h~) V  (Eq. (3) second half, Sec. 2.5); the target
 // Z = Q G_V^{-1} follows in k_utarget
-// grid: nside side WGs (V^T V on int8 MFMA over K slices, the last of them
-//       adds the ridge and inverts; weighted: one side WG takes V^T H V,
-//       formed by k_vprep_w before the launch, and inverts it; the raw Gram
-//       is kept for the scale solve) followed by ntile row groups of `rows` <= 32 rows, sized so
+// grid: nside side WGs (V^T V on int8 MFMA over K slices, weighted
+//       V^T diag(H) V from the weights' digit planes; the last of them adds
+//       the ridge and inverts; the raw Gram is kept for the scale solve)
+//       followed by ntile row groups of `rows` <= 32 rows, sized so
 //       that the whole grid is resident at two workgroups per CU and every
 //       CU streams the same share of R; each row group stores Q, waits for
 //       G_V^{-1} and writes its Z rows and T_tau statistics.
@@ -1194,7 +1093,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                               double* __restrict__ Q, float* __restrict__ rowb,
                                               int64_t m_pad, int64_t n_pad, int bb, int* gacc, unsigned* counter,
                                               double* ginvV, double* gramV, int nside, int rows,
-                                              const double* __restrict__ partw, int nwg) {
+                                              const int8_t* __restrict__ Wmf, long long* gacc64,
+                                              const double* __restrict__ hwmax) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[USTEP_SMEM_LL];
@@ -1204,34 +1104,15 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     double* Gs = (double*)(smem + 2048);
     double* pbuf = Gs + 4096;
     if (WEIGHTED) {
-      // V^T H V from the nwg partials of the V thresholding (k_tern_vw) or
-      // k_vprep_w: side workgroup b adds the entries [256 b, 256 b + 256) of
-      // the upper triangle (nside * NT = 4096) and writes both triangles of
-      // gramV through to the device-coherent level; the last to arrive takes
-      // the Gram back, adds the ridge and inverts.
-      const int e = (int)blockIdx.x * NT + threadIdx.x, r = e >> 6, cc = e & 63;
-      if (r <= cc) {
-        const double d = gramw_entry(partw, nwg, e);
-        store_coherent(gramV + e, d);
-        store_coherent(gramV + cc * BBP + r, d);
+      // V^T diag(H) V on int8 MFMA from the digit-scaled planes of V; the last
+      // side workgroup keeps the raw Gram for the scale solve, adds the
+      // ridge and inverts
+      if (side_gram_w(Vmf, Wmf, (int64_t)BMAX * n_pad, n_pad, blockIdx.x, nside, gacc64, hwmax[1], counter, Gs,
+                      (int*)smem)) {
+        for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
+        __syncthreads();
+        ridge_invert_store(Gs, pbuf, bb, ginvV);
       }
-      __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have been performed
-      __shared__ int s_last;
-      __syncthreads();
-      if (threadIdx.x == 0) {
-        const unsigned old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (old == (unsigned)(nside - 1));
-      }
-      __syncthreads();
-      if (!s_last) return;
-      if (threadIdx.x == 0) store_coherent(counter, 0u);
-      double v[4096 / NT];
-#pragma unroll
-      for (int j = 0; j < 4096 / NT; ++j) v[j] = load_coherent(gramV + threadIdx.x + NT * j);
-#pragma unroll
-      for (int j = 0; j < 4096 / NT; ++j) Gs[threadIdx.x + NT * j] = v[j];
-      __syncthreads();
-      ridge_invert_store(Gs, pbuf, bb, ginvV);
       return;
     }
     if (side_gram_acc(Vmf, n_pad, blockIdx.x, nside, gacc, counter, Gs, (int*)smem)) {
@@ -1305,7 +1186,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const float rbound = nks >= 4 * (NST_U - 1) ? lds_read1_after<2 * 3>(rba) : lds_read1_after<0>(rba);
   const int s = fx_shift(rbound);
   const float p2s = __builtin_amdgcn_ldexpf(1.0f, s);  // x 2^s = x * p2s exactly
-  const double p2sd = (double)p2s;
+  const double cw = weighted_round_const(s);
   // operand read: row l32, logical chunks 4h .. 4h+3
   const unsigned sw = (unsigned)(l32 & 7);
   const unsigned o0 = l32 * 128 + ((4 * h + 0) ^ sw) * 16, o1 = l32 * 128 + ((4 * h + 1) ^ sw) * 16;
@@ -1331,7 +1212,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
           for (int q = 0; q < 4; ++q)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              y[4 * q + e] = fx_biased_w(x[q][e], wv[(4 * q + e) >> 1][e & 1] * p2sd);
+              y[4 * q + e] = fx_biased_w(x[q][e], wv[(4 * q + e) >> 1][e & 1], cw);
               ymin = min(ymin, (int)y[4 * q + e]);
               ymax = max(ymax, (int)y[4 * q + e]);
             }
@@ -1437,8 +1318,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // component apply the identical threshold.  The statistics loads are
 // issued before the chunk's targets so that the reduction overlaps them.
 // Writes the trits component-major (dst) and into the MFMA-ready layout
-// mf, zero beyond L; with q it returns this chunk's sum_i t_i q_i (fp64,
-// fixed reduction order).  blockDim.x = NT.
+// mf, zero beyond L, and hands each (index, trit) to emit; with q it
+// returns this chunk's sum_i t_i q_i (fp64, fixed reduction order).
+// blockDim.x = NT.
 // ---------------------------------------------------------------------------
 constexpr int TERN_SP = 2;  // statistics tiles per thread loaded up front
 constexpr int TERN_XS = 8;  // chunk entries per thread kept in registers
@@ -1458,10 +1340,11 @@ __device__ __forceinline__ void block_sum_max(double& s, double& m, double* sh /
   m = fmax(fmax(sh[4], sh[5]), fmax(sh[6], sh[7]));
 }
 
+template <typename Emit>
 __device__ __forceinline__ double tern_chunk(const double* __restrict__ x, const double* __restrict__ q, int64_t L,
                                              int64_t i0, int64_t i1, int ntile, const double* __restrict__ ps,
                                              const double* __restrict__ pm, const int* __restrict__ pi, double tau,
-                                             int8_t* __restrict__ dst, int8_t* __restrict__ mf, int c) {
+                                             int8_t* __restrict__ dst, int8_t* __restrict__ mf, int c, Emit emit) {
   __shared__ double shd[8];
   __shared__ int shi[4];
   const int tid = threadIdx.x;
@@ -1527,6 +1410,7 @@ __device__ __forceinline__ double tern_chunk(const double* __restrict__ x, const
       g += (double)t * qc[k];
       dst[i] = t;
       mf[mf_offset(c, i)] = t;
+      emit(i, t);
     }
   }
   for (int64_t i = i0 + tid + (int64_t)TERN_XS * NT; i < i1; i += NT) {
@@ -1535,6 +1419,7 @@ __device__ __forceinline__ double tern_chunk(const double* __restrict__ x, const
     if (q && i < L) g += (double)t * q[i];
     dst[i] = t;
     mf[mf_offset(c, i)] = t;
+    emit(i, t);
   }
   if (!q) return 0.0;
   double dummy = 0.0;
@@ -1550,25 +1435,39 @@ __device__ __forceinline__ void tern_range(int64_t L_pad, int sp, int ns, int64_
   i1 = i0 + chunk < L_pad ? i0 + chunk : L_pad;
 }
 
-// V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.
+// V <- T_tau(Y[c, :]) for c < bb; zero components beyond bb.  Weighted
+// (Wmf given): also the digit-scaled planes of V for the weighted Gram,
+// Wmf[d * wstride + mf_offset(c, j)] = dig_d(j) v_jc.
 // grid: BBP x ns (component c = blockIdx.x / ns, split blockIdx.x % ns).
 __global__ __launch_bounds__(NT) void k_tern_v(const double* __restrict__ Y, int64_t n, int64_t n_pad, int bb, double tau,
                                                const double* __restrict__ ps, const double* __restrict__ pm,
                                                const int* __restrict__ pi, int ntile, int ns, int8_t* __restrict__ Vt,
-                                               int8_t* __restrict__ Vmf) {
+                                               int8_t* __restrict__ Vmf, const int8_t* __restrict__ hdig,
+                                               int8_t* __restrict__ Wmf, int64_t wstride) {
   const int c = blockIdx.x / ns, sp = blockIdx.x % ns;
   int64_t i0, i1;
   tern_range(n_pad, sp, ns, i0, i1);
   int8_t* dst = Vt + (int64_t)c * n_pad;
+  auto emit = [&](int64_t j, int8_t t) {
+    if (Wmf) {  // uniform
+      int8_t dg[WDIG];
+#pragma unroll
+      for (int d = 0; d < WDIG; ++d) dg[d] = hdig[(int64_t)d * n_pad + j];
+      const int64_t o = mf_offset(c, j);
+#pragma unroll
+      for (int d = 0; d < WDIG; ++d) Wmf[(int64_t)d * wstride + o] = (int8_t)(t * dg[d]);
+    }
+  };
   if (c >= bb) {
     for (int64_t j = i0 + threadIdx.x; j < i1; j += NT) {
       dst[j] = 0;
       Vmf[mf_offset(c, j)] = 0;
+      emit(j, (int8_t)0);
     }
     return;
   }
   const int64_t o = (int64_t)c * ntile;
-  tern_chunk(Y + (int64_t)c * n_pad, nullptr, n, i0, i1, ntile, ps + o, pm + o, pi + o, tau, dst, Vmf, c);
+  tern_chunk(Y + (int64_t)c * n_pad, nullptr, n, i0, i1, ntile, ps + o, pm + o, pi + o, tau, dst, Vmf, c, emit);
 }
 
 // U <- T_tau(Z[:, c]).  With Q (the last U-step of a block), also the
@@ -1594,7 +1493,8 @@ __global__ __launch_bounds__(NT) void k_tern_u(const double* __restrict__ Z, con
   } else {
     const int64_t o = (int64_t)c * ntile;
     const double* qrow = Q ? Q + (int64_t)c * m_pad : nullptr;
-    g = tern_chunk(Z + (int64_t)c * m_pad, qrow, m, i0, i1, ntile, ps + o, pm + o, pi + o, tau, dst, Umf, c);
+    g = tern_chunk(Z + (int64_t)c * m_pad, qrow, m, i0, i1, ntile, ps + o, pm + o, pi + o, tau, dst, Umf, c,
+                   [](int64_t, int8_t) {});
   }
   if (Q && threadIdx.x == 0) {
     gpart[c * TERN_SPLIT_MAX + sp] = g;
@@ -2027,6 +1927,24 @@ __global__ __launch_bounds__(NT) void k_unstage(const float* __restrict__ R, flo
   }
 }
 
+// Bits of the weighted Grams' integer weights: w = min(WSHIFT_MAX,
+// 61 - ceil(log2 n_pad)), so that sum_j H_j < n_pad 2^w <= 2^61.
+__device__ __forceinline__ int weight_bits(int64_t n_pad) {
+  int c = 0;
+  while (((int64_t)1 << c) < n_pad) ++c;
+  return 61 - c < WSHIFT_MAX ? 61 - c : WSHIFT_MAX;
+}
+// Digit planes of the weight r = h~_j / max h~ in [0, 1]:
+// H_j = min(rint(r 2^wb), 2^wb - 1), digit d of H_j in hdig[d * n_pad + j].
+__device__ __forceinline__ void put_weight_digits(int8_t* hdig, int64_t n_pad, int64_t j, double r, int wb) {
+  const double q = rint(ldexp(r, wb));
+  const long long top = ((long long)1 << wb) - 1;
+  const long long H = q < (double)top ? (long long)q : top;
+#pragma unroll
+  for (int d = 0; d < WDIG; ++d)
+    hdig[(int64_t)d * n_pad + j] = (int8_t)((H >> (WDIG_BITS * d)) & ((1 << WDIG_BITS) - 1));
+}
+
 // Weights and bookkeeping (1 WG): h~ = h / max(h) + lam in fp64 (Sec. 2.5;
 // ones when no weights), zero padding; clear counters, flags and the
 // per-block arrays.
@@ -2034,7 +1952,8 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
                                              double* __restrict__ hw, double* __restrict__ hwmax,
                                              double* fro2_hist, double* fro2w_hist, int nblk_cap,
                                              unsigned* counters, int* flags, int* gacc, double lam,
-                                             unsigned long long* argkey, int* gaccW) {
+                                             unsigned long long* argkey, int* gaccW, long long* gacc64,
+                                             int8_t* __restrict__ hdig) {
   __shared__ float smax[NT / 64];
   __shared__ int sbad[NT / 64];
   for (int e = threadIdx.x; e < nblk_cap; e += NT) {
@@ -2044,11 +1963,15 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
   }
   if (threadIdx.x < CNT_COUNT) counters[threadIdx.x] = 0u;
   for (int e = threadIdx.x; e < 2 * 4096; e += NT) gacc[e] = 0;
-  for (int e = threadIdx.x; e < NPAIR_MAX * 4096; e += NT) gaccW[e] = 0;
+  for (int e = threadIdx.x; e < 2 * NPAIR_MAX * 4096; e += NT) gaccW[e] = 0;
+  for (int e = threadIdx.x; e < 4096; e += NT) gacc64[e] = 0;
   if (threadIdx.x < FLAG_COUNT) flags[threadIdx.x] = 0;
   if (!h) {
     for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? 1.0 : 0.0;
-    if (threadIdx.x == 0) *hwmax = 1.0;
+    if (threadIdx.x == 0) {
+      hwmax[0] = 1.0;
+      hwmax[1] = ldexp(1.0, -weight_bits(n_pad));
+    }
     return;
   }
   float mx = 0.0f;
@@ -2079,13 +2002,27 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
       flags[FLAG_BADWEIGHT] = 1;
       *hwmax = 1.0;
     }
-    for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? 1.0 : 0.0;
+    const int wb = weight_bits(n_pad);
+    for (int64_t j = threadIdx.x; j < n_pad; j += NT) {
+      hw[j] = (j < n) ? 1.0 : 0.0;
+      put_weight_digits(hdig, n_pad, j, hw[j], wb);
+    }
+    if (threadIdx.x == 0) hwmax[1] = ldexp(1.0, -wb);
     return;
   }
   const double dm = (double)gmx;
-  for (int64_t j = threadIdx.x; j < n_pad; j += NT) hw[j] = (j < n) ? (double)h[j] / dm + lam : 0.0;
   // the largest weight is exactly max(h) / max(h) + lam
-  if (threadIdx.x == 0) *hwmax = 1.0 + lam;
+  const double hmax = 1.0 + lam;
+  const int wb = weight_bits(n_pad);
+  for (int64_t j = threadIdx.x; j < n_pad; j += NT) {
+    const double v = (j < n) ? (double)h[j] / dm + lam : 0.0;
+    hw[j] = v;
+    put_weight_digits(hdig, n_pad, j, v / hmax, wb);
+  }
+  if (threadIdx.x == 0) {
+    hwmax[0] = hmax;
+    hwmax[1] = ldexp(hmax, -wb);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -2737,8 +2674,43 @@ __global__ __launch_bounds__(NT) void k_load_cm(double* Xcm, const double* X, in
 }
 
 
+// Weighted Gram of V alone (raw V^T diag(H) V into gramV), for the scale
+// step entry point: the arithmetic of the U-step's side path in a launch of
+// its own.  grid: NSIDE_GRAM.
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gram_vw(
+    const v4i* __restrict__ Vmf, const int8_t* __restrict__ Wmf, int64_t n_pad, long long* gacc64,
+    const double* __restrict__ hwmax, unsigned* counter, double* gramV) {
+  __shared__ __attribute__((aligned(16))) int red[4 * 4096];
+  __shared__ double Gs[4096];
+  if (!side_gram_w(Vmf, Wmf, (int64_t)BMAX * n_pad, n_pad, blockIdx.x, (int)gridDim.x, gacc64, hwmax[1], counter, Gs,
+                   red))
+    return;
+  for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
+}
+
+// The digit-scaled planes of a V given by the caller (step entry points;
+// in a factorization k_tern_v writes them with V): Wmf[d * wstride + o] =
+// dig_d(j) v_jc for the MFMA-ready byte o of (c, j), for the nq quarters.
+// grid: (n_pad / 32 K steps, nq); thread t < 128 takes the 16 bytes
+// (K step, t) of the quarter.
+__global__ __launch_bounds__(128) void k_vweight(const v4i* __restrict__ Vmf, const int8_t* __restrict__ hdig,
+                                                 int64_t n_pad, int8_t* __restrict__ Wmf, int64_t wstride) {
+  const int64_t ks = blockIdx.x, q = blockIdx.y;
+  const int t = threadIdx.x, h = (t & 63) >> 5;
+  const int64_t e = q * 4 * n_pad + ks * 128 + t;  // v4i index within Vmf
+  const v4i x = Vmf[e];
+#pragma unroll
+  for (int d = 0; d < WDIG; ++d) {
+    const v4i dg = *(const v4i*)(hdig + (int64_t)d * n_pad + ks * TILE + 16 * h);
+    v4i r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) r[k] = trit_times_digit(x[k], dg[k]);
+    ((v4i*)(Wmf + (int64_t)d * wstride))[e] = r;
+  }
+}
+
 // Integer Gram of V alone (raw V^T V and its ridge inverse), for the scale
-// step entry point; the weighted Gram comes from k_vprep_w / k_gramw_sum.
+// step entry point; the weighted Gram comes from k_gram_vw.
 // grid: NSIDE_INT.
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gram_v(const v4i* __restrict__ Vmf, int64_t n_pad, int bb, int* gparti,
                                                unsigned* counter, double* ginvV, double* gramV) {
@@ -2865,49 +2837,38 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   }
 }
 
-// Weighted Gram blocks of V (Sec. 2.5): partial V_q^T diag(h~) V_q' over a
-// slab of rows for every pair q <= q', on fp64 MFMA (the products
-// h~_j v_jc v_jc' are exact); wave w takes the 16-row tile w of the block.
-// grid: npairs x GW_SLABS.
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gramw_pairs(
-    const int8_t* __restrict__ Vt, const double* __restrict__ hw, int64_t n_pad, int nq,
-    double* __restrict__ partwW) {
-  const int p = blockIdx.x / GW_SLABS, sl = blockIdx.x % GW_SLABS;
+// Weighted Gram blocks V_q^T diag(H) V_q' of V (Sec. 2.5) for every pair
+// q <= q' < nq on int8 MFMA from the digit-scaled planes of V (the
+// arithmetic of gram_w_accumulate), added into g64[pair] (int64 atomics, exact and
+// order-free); the sweep's first pivot launch clears g64 again.
+// grid: npairs x nslice workgroups, workgroup (pair, slice) takes a slice of
+// the K steps.
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gram_pairs_w(
+    const v4i* __restrict__ Vmf, const int8_t* __restrict__ Wmf, int64_t n_pad, int nq, int nslice,
+    long long* __restrict__ g64) {
+  __shared__ int red[4 * 4096];
+  const int p = blockIdx.x / nslice, sl = blockIdx.x % nslice;
   int q, q2;
   pair_of(p, nq, q, q2);
-  const int64_t rs = (n_pad / 4 + GW_SLABS - 1) / GW_SLABS * 4;  // rows per slab, a multiple of 4
-  const int64_t r0 = (int64_t)sl * rs, r1 = r0 + rs < n_pad ? r0 + rs : n_pad;
-  const int lane = lane_id(), w = wave_id();
-  const int li = lane & 15, lk = lane >> 4;
-  const int8_t* va = Vt + (int64_t)(BBP * q + 16 * w + li) * n_pad;
-  const int8_t* vb = Vt + (int64_t)(BBP * q2 + li) * n_pad;
-  v4d acc[4] = {v4d{}, v4d{}, v4d{}, v4d{}};
-  for (int64_t j0 = r0; j0 < r1; j0 += 4) {
-    const int64_t j = j0 + lk;
-    const double a = hw[j] * (double)va[j];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma_f64(a, (double)vb[(int64_t)16 * nt * n_pad + j], acc[nt]);
-  }
-  double* out = partwW + ((int64_t)p * GW_SLABS + sl) * 4096;
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) out[(16 * w + lk + 4 * r) * BBP + 16 * nt + li] = acc[nt][r];
+  const int nks = (int)(n_pad / TILE);
+  const int ks0 = (int)((long long)sl * nks / nslice), ks1 = (int)((long long)(sl + 1) * nks / nslice);
+  gram_w_accumulate<false>(Vmf + (int64_t)q * 4 * n_pad, Wmf + (int64_t)q2 * BBP * n_pad, (int64_t)BMAX * n_pad, ks0,
+                           ks1, g64 + (int64_t)p * 4096, red);
 }
 
 // The matrix to sweep, A (BMAX-stride row-major, nq x nq blocks), from one
 // pair block per workgroup (both triangles):
 //   mode 0: (G + eps I) from the integer Gram blocks gaccW, the raw Gram
 //           also into raw (if given);
-//   mode 1: (G + eps I) from the partial weighted blocks partwW (slabs added
-//           in order), the raw Gram into raw;
+//   mode 1: (G + eps I) from the weighted integer Gram blocks g64 times
+//           their unit (hwmax[1]), the raw Gram into raw;
 //   mode 2: (G_U o G_V + delta I) from gaccW (G_U) and raw (G_V), Eq. (4);
 // with eps or delta = rel * trace / bb over the bb real components and the
 // identity on the padding components.  A zero trace sets wflag[0] (the
 // result is then zero targets, or zero scales) and leaves the identity in A.
 // grid: npairs.
 __global__ __launch_bounds__(NT) void k_wide_prep(int mode, const int* __restrict__ gaccW,
-                                                  const double* __restrict__ partwW, double* raw, int bb, int nq,
+                                                  const double* __restrict__ hwmax, double* raw, int bb, int nq,
                                                   double rel, double* __restrict__ A, int* __restrict__ wflag) {
   __shared__ double shd[NT / 64];
   const int p = blockIdx.x;
@@ -2919,36 +2880,26 @@ __global__ __launch_bounds__(NT) void k_wide_prep(int mode, const int* __restric
   if (c < bb) {
     const int qc = c / BBP, cl = c % BBP, pd = pair_index(qc, qc, nq);
     if (mode == 0) dv = (double)gaccW[(int64_t)pd * 4096 + cl * 65];
-    else if (mode == 1) {
-      for (int s = 0; s < GW_SLABS; ++s) dv += partwW[((int64_t)pd * GW_SLABS + s) * 4096 + cl * 65];
-    } else
+    else if (mode == 1)
+      dv = (double)((const long long*)gaccW)[(int64_t)pd * 4096 + cl * 65] * hwmax[1];
+    else
       dv = (double)gaccW[(int64_t)pd * 4096 + cl * 65] * raw[(int64_t)c * BMAX + c];
   }
   const double tr = block_sum_d(dv, shd);
   const bool zero = tr == 0.0;
   if (p == 0 && threadIdx.x == 0) *wflag = zero ? 1 : 0;
   const double ridge = zero ? 0.0 : rel * tr / (double)bb;
-  // The block's values first, every load of a batch issued before any is
-  // used (a loop that stores each value would wait for each load in turn);
-  // the slabs are added in order, as one sum per entry.
+  // The block's values first, every load issued before any is used (a loop
+  // that stores each value would wait for each load in turn).
   constexpr int PER = 4096 / NT;
-  static_assert(GW_SLABS % 4 == 0, "slabs in batches of four");
   double vals[PER];
   if (mode == 1) {
+    const double unit = hwmax[1];
+    long long gv[PER];
 #pragma unroll
-    for (int u = 0; u < PER; ++u) vals[u] = 0.0;
-    for (int s0 = 0; s0 < GW_SLABS; s0 += 4) {
-      double pv[4][PER];
+    for (int u = 0; u < PER; ++u) gv[u] = ((const long long*)gaccW)[(int64_t)p * 4096 + threadIdx.x + NT * u];
 #pragma unroll
-      for (int sl = 0; sl < 4; ++sl)
-#pragma unroll
-        for (int u = 0; u < PER; ++u)
-          pv[sl][u] = partwW[((int64_t)p * GW_SLABS + s0 + sl) * 4096 + threadIdx.x + NT * u];
-#pragma unroll
-      for (int sl = 0; sl < 4; ++sl)
-#pragma unroll
-        for (int u = 0; u < PER; ++u) vals[u] += pv[sl][u];
-    }
+    for (int u = 0; u < PER; ++u) vals[u] = (double)gv[u] * unit;
   } else if (mode == 2) {
     int gv[PER];
     double rv[PER];
@@ -3169,7 +3120,8 @@ static inline unsigned grid_for(int64_t total) {
 
 hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s, double lam) {
   hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.hwmax, w.fro2_hist,
-                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc, lam, w.argkey, w.gaccW);
+                     w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc, lam, w.argkey, w.gaccW, w.gacc64,
+                     w.hdig);
   return hipGetLastError();
 }
 
@@ -3221,18 +3173,6 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Rows per weighted-Gram partial: a multiple of 32, at least 32, at most
-// VPREP_MAX_WG partials.
-static void gram_w_geometry(const Ws& w, int64_t& rows_wg, int& nwg) {
-  rows_wg = (w.n_pad + VPREP_MAX_WG - 1) / VPREP_MAX_WG;
-  rows_wg = rows_wg < VPREP_MIN_ROWS ? VPREP_MIN_ROWS : (rows_wg + TILE - 1) / TILE * TILE;
-  nwg = (int)((w.n_pad + rows_wg - 1) / rows_wg);
-}
-
-// The weighted V-step thresholds V by row blocks (k_tern_vw) when a block
-// fits one staged chunk, i.e. n_pad <= VPREP_MAX_WG * VPREP_CHUNK.
-static bool tern_vw_fits(const Ws& w) { return w.n_pad <= (int64_t)VPREP_MAX_WG * VPREP_CHUNK; }
-
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm, bool weighted) {
   const unsigned grid = (unsigned)(NSIDE_GRAM + (w.n_pad / TILE) * w.gv);
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, (const int*)w.cshift, w.m_pad,
@@ -3244,65 +3184,28 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
                        w.tpi, 1, (int64_t)0);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (weighted && tern_vw_fits(w)) {
-    // V by row blocks, with the partials of V^T H V for the U-step
-    int64_t rows_wg;
-    int nwg;
-    gram_w_geometry(w, rows_wg, nwg);
-    EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_vw, dim3((unsigned)nwg), dim3(NT), 0, s,
-                         (const double*)w.Y, w.n, w.n_pad, bb, tau, (const double*)w.tps, (const double*)w.tpm,
-                         (const int*)w.tpi, (int)(w.n_pad / 16), w.Vt, w.Vmf, (const double*)w.hw, (int)rows_wg,
-                         w.partw);
-    return hipGetLastError();
-  }
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, (const double*)w.Y, w.n,
                        w.n_pad, bb, tau, (const double*)w.tps, (const double*)w.tpm, (const int*)w.tpi,
-                       (int)(w.n_pad / 16), w.nsv, w.Vt, w.Vmf);
-  return hipGetLastError();
-}
-
-// Weighted: V row-major and the raw weighted Gram V^T diag(h~) V into
-// gramV (the step entry point of the scale solve).
-hipError_t launch_gram_w(const Ws& w, hipStream_t s) {
-  int64_t rows_wg;
-  int nwg;
-  gram_w_geometry(w, rows_wg, nwg);
-  hipLaunchKernelGGL(k_vprep_w, dim3((unsigned)nwg), dim3(NT), 0, s, (const int8_t*)w.Vt, w.Vr, w.n_pad,
-                     (const double*)w.hw, (int)rows_wg, w.partw);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_gramw_sum, dim3(BBP * BBP / 64), dim3(NT), 0, s, (const double*)w.partw, nwg, w.gramV);
+                       (int)(w.n_pad / 16), w.nsv, w.Vt, w.Vmf, (const int8_t*)w.hdig, weighted ? w.Wmf : nullptr,
+                       (int64_t)BMAX * w.n_pad);
   return hipGetLastError();
 }
 
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
-                        Timer* tm, bool v_partials) {
+                        Timer* tm) {
   hipError_t e;
   const unsigned nside = NSIDE_GRAM;
   const unsigned grid = (unsigned)(nside + w.ntu);
-  if (weighted) {
-    // the side workgroups add the partials of V^T H V: left by the V-step's
-    // row-block thresholding, or formed here from the given V
-    static_assert(NSIDE_GRAM * NT == BBP * BBP, "one weighted-Gram entry per side thread");
-    int64_t rows_wg;
-    int nwg;
-    gram_w_geometry(w, rows_wg, nwg);
-    if (!(v_partials && tern_vw_fits(w))) {
-      hipLaunchKernelGGL(k_vprep_w, dim3((unsigned)nwg), dim3(NT), 0, s, (const int8_t*)w.Vt, w.Vr, w.n_pad,
-                         (const double*)w.hw, (int)rows_wg, w.partw);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
+  if (weighted)
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.rowb, w.m_pad, w.n_pad, bb, w.gacc + 4096,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows,
-                                     (const double*)w.partw, nwg);
-  } else {
+                                     (const int8_t*)w.Wmf, w.gacc64, (const double*)w.hwmax);
+  else
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.rowb, w.m_pad, w.n_pad, bb, w.gacc + 4096,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows,
-                                     (const double*)nullptr, 0);
-  }
+                                     (const int8_t*)nullptr, (long long*)nullptr, (const double*)nullptr);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_UTARGET, k_utarget<false>, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0,
@@ -3324,14 +3227,15 @@ constexpr int GRAM_PAIR_SLICES = 16;  // K slices per quarter pair of the intege
 // per pivot block (k_wide_step: every workgroup inverts the pivot and
 // updates its block); *out receives the buffer holding -A^{-1}.  The first
 // step clears the integer Gram blocks.
-static hipError_t wide_sweep(const Ws& w, int bb, hipStream_t s, const double** out) {
+static hipError_t wide_sweep(const Ws& w, int bb, hipStream_t s, const double** out, bool clear64 = false) {
   const int nq = nq_of(bb), npairs = nq * (nq + 1) / 2;
+  const int nclear = (clear64 ? 2 : 1) * npairs * 4096;  // int32 words of the Gram blocks used
   double* A = w.wA0;
   double* B = w.wA1;
   for (int k = 0; k < nq; ++k) {
     const int bq = bb_of_quarter(bb, k);
     hipLaunchKernelGGL(k_wide_step, dim3((unsigned)(nq * nq)), dim3(NT), 0, s, (const double*)A, B, k, nq,
-                       (bq + 3) / 4, w.gaccW, k == 0 ? npairs * 4096 : 0);
+                       (bq + 3) / 4, w.gaccW, k == 0 ? nclear : 0);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     double* t = A;
@@ -3350,12 +3254,12 @@ static hipError_t wide_gram_inverse(const Ws& w, int which, bool weighted, int b
   const int nq = nq_of(bb), npairs = nq * (nq + 1) / 2;
   hipError_t e;
   if (which == 1 && weighted) {
-    hipLaunchKernelGGL(k_gramw_pairs, dim3((unsigned)(npairs * GW_SLABS)), dim3(NT), 0, s, (const int8_t*)w.Vt,
-                       (const double*)w.hw, w.n_pad, nq, w.partwW);
+    hipLaunchKernelGGL(k_gram_pairs_w, dim3((unsigned)(npairs * GRAM_PAIR_SLICES)), dim3(NT), 0, s,
+                       (const v4i*)w.Vmf, (const int8_t*)w.Wmf, w.n_pad, nq, GRAM_PAIR_SLICES, (long long*)w.gaccW);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_wide_prep, dim3((unsigned)npairs), dim3(NT), 0, s, 1, (const int*)w.gaccW,
-                       (const double*)w.partwW, w.gramVW, bb, nq, EXTERND_RIDGE_REL, w.wA0, w.wflag);
+                       (const double*)w.hwmax, w.gramVW, bb, nq, EXTERND_RIDGE_REL, w.wA0, w.wflag);
   } else {
     const v4i* X = (const v4i*)(which ? w.Vmf : w.Umf);
     hipLaunchKernelGGL(k_gram_pairs, dim3((unsigned)(npairs * GRAM_PAIR_SLICES)), dim3(NT), 0, s, X,
@@ -3363,13 +3267,13 @@ static hipError_t wide_gram_inverse(const Ws& w, int which, bool weighted, int b
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_wide_prep, dim3((unsigned)npairs), dim3(NT), 0, s, 0, (const int*)w.gaccW,
-                       (const double*)nullptr, which ? w.gramVW : (double*)nullptr, bb, nq, EXTERND_RIDGE_REL,
+                       (const double*)w.hwmax, which ? w.gramVW : (double*)nullptr, bb, nq, EXTERND_RIDGE_REL,
                        w.wA0, w.wflag);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const double* S = nullptr;
-  e = wide_sweep(w, bb, s, &S);
+  e = wide_sweep(w, bb, s, &S, which == 1 && weighted);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_wide_ginv, dim3((unsigned)(nq * nq)), dim3(NT), 0, s, S, nq, bb, (const int*)w.wflag,
                      which ? w.ginvVW : w.ginvUW);
@@ -3384,7 +3288,7 @@ hipError_t launch_init_wide(const Ws& w, int bb, double tau, hipStream_t s) {
   return hipSuccess;
 }
 
-hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm) {
+hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm, bool weighted) {
   const int nq = nq_of(bb);
   hipError_t e;
   // P_q = U_q^T R per quarter (contraction launches without a side path)
@@ -3408,7 +3312,8 @@ hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream
     if (e != hipSuccess) return e;
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, (const double*)v.Y,
                          w.n, w.n_pad, bb_of_quarter(bb, q), tau, (const double*)v.tps, (const double*)v.tpm,
-                         (const int*)v.tpi, (int)(w.n_pad / 16), w.nsv, v.Vt, v.Vmf);
+                         (const int*)v.tpi, (int)(w.n_pad / 16), w.nsv, v.Vt, v.Vmf, (const int8_t*)w.hdig,
+                         weighted ? v.Wmf : nullptr, (int64_t)BMAX * w.n_pad);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -3426,11 +3331,13 @@ hipError_t launch_ustep_wide(const Ws& w, int blk, int bb, double tau, bool weig
     if (weighted)
       EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3((unsigned)w.ntu), dim3(NT), 0, s, w.R,
                            (const v4i*)v.Vmf, v.Vr, w.hw, v.Q, w.rowb, w.m_pad, w.n_pad, bq, w.gacc + 4096,
-                           w.counters + CNT_GRAM_V, w.ginvV, w.gramV, 0, w.urows, (const double*)nullptr, 0);
+                           w.counters + CNT_GRAM_V, w.ginvV, w.gramV, 0, w.urows, (const int8_t*)nullptr,
+                           (long long*)nullptr, (const double*)nullptr);
     else
       EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3((unsigned)w.ntu), dim3(NT), 0, s, w.R,
                            (const v4i*)v.Vmf, v.Vr, w.hw, v.Q, w.rowb, w.m_pad, w.n_pad, bq, w.gacc + 4096,
-                           w.counters + CNT_GRAM_V, w.ginvV, w.gramV, 0, w.urows, (const double*)nullptr, 0);
+                           w.counters + CNT_GRAM_V, w.ginvV, w.gramV, 0, w.urows, (const int8_t*)nullptr,
+                           (long long*)nullptr, (const double*)nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -3583,8 +3490,17 @@ hipError_t launch_load_cm(double* Xcm, const double* X, int64_t len, int64_t len
   return hipGetLastError();
 }
 
+hipError_t launch_vweight(const Ws& w, int bb, hipStream_t s) {
+  hipLaunchKernelGGL(k_vweight, dim3((unsigned)(w.n_pad / TILE), (unsigned)nq_of(bb)), dim3(128), 0, s,
+                     (const v4i*)w.Vmf, (const int8_t*)w.hdig, w.n_pad, w.Wmf, (int64_t)BMAX * w.n_pad);
+  return hipGetLastError();
+}
 hipError_t launch_gram_only(const Ws& w, int bb, bool weighted, hipStream_t s) {
-  if (weighted) return launch_gram_w(w, s);
+  if (weighted) {
+    hipLaunchKernelGGL(k_gram_vw, dim3(NSIDE_GRAM), dim3(NT), 0, s, (const v4i*)w.Vmf, (const int8_t*)w.Wmf,
+                       w.n_pad, w.gacc64, (const double*)w.hwmax, w.counters + CNT_GRAM_V, w.gramV);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_gram_v, dim3(NSIDE_INT), dim3(NT), 0, s, (const v4i*)w.Vmf, w.n_pad, bb, w.gparti,
                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV);
   return hipGetLastError();
