@@ -229,12 +229,20 @@ int externd_factorize_refined(const float* A, int64_t m, int64_t n, double mu, d
 /*
  * Inference with a factorization (Sec. 2.6 cost model): for each of nb
  * input vectors x (rows of X), y = B (diag(D) (C x)), computed on the packed
- * trits with fp32 accumulation in a fixed order (deterministic).  One
- * vector runs on fp32 FMA; two or more on bf16 matrix cores with exact
- * operands (trits are exact in bf16; every fp32 vector entry is split
- * exactly into three bf16 parts).  Either way the error is that of fp32
- * sums: at most (n + k + 4) u (|B| (|D| (|C| |x|))) per output, u = 2^-24,
- * for finite inputs whose nonzero entries are fp32 normals.
+ * trits in a fixed order (deterministic).
+ *  - One vector with n, k <= 10240: integer matrix cores.  x and the
+ *    intermediate t = diag(D) C x enter as 48-bit fixed-point vectors (one
+ *    power-of-two scale each: x's from max |x|, t's from the bound
+ *    max |D| sum_j |x_j|), so every product and sum is exact; the error is
+ *    that of the two conversions and the final rounding: at most
+ *    u |y| + 2^-46 [ (|B| (|D| (|C| 1))) max|x| + (|B| 1) max|D| sum|x| ]
+ *    per output, u = 2^-24 (entries of x within 2^22 of max |x| convert
+ *    exactly).  A NaN or infinite entry of x or D makes every output NaN.
+ *  - Otherwise one vector runs on fp32 FMA and two or more on bf16 matrix
+ *    cores with exact operands (trits are exact in bf16; every fp32 vector
+ *    entry is split exactly into three bf16 parts), with fp32 sums: at most
+ *    (n + k + 4) u (|B| (|D| (|C| |x|))) per output, for finite inputs whose
+ *    nonzero entries are fp32 normals.
  *
  *  B_packed   device, m rows of ceil(k/4) bytes; C_packed device, k rows of
  *             ceil(n/4) bytes; D device fp32[k] -- as written by
@@ -247,7 +255,8 @@ int externd_factorize_refined(const float* A, int64_t m, int64_t n, double mu, d
  *  nb         1 <= nb <= EXTERND_APPLY_MAX_BATCH.
  *  workspace  device, >= externd_apply_workspace_bytes(m, n, k, nb) bytes,
  *             256-byte aligned.  nb = 1: the intermediate diag(D) C x
- *             (4 k bytes).  nb >= 2: its bf16 parts (6 nb k bytes) and
+ *             (n, k <= 10240: its six 8-bit digit planes, 1536 bytes per
+ *             256 entries, and an exponent word; else 4 k bytes).  nb >= 2: its bf16 parts (6 nb k bytes) and
  *             partial sums over slices of the contracted dimensions (at
  *             most nb max(n, m) k / 32 bytes, rounded up to whole row
  *             groups).

@@ -437,6 +437,373 @@ __global__ __launch_bounds__(NT_AP) void k_apply_vec_b(const uint8_t* __restrict
   rows_times_vectors<NB, true>(Bp, m, k, (int64_t)blockIdx.x * VEC_RPW, T, kq, nb, nullptr, Y, m);
 }
 
+// ---- one vector on integer matrix cores (nb = 1, n and k <= GV_MAX_LEN) ----
+//
+// A product y = P v (P: rows x len packed trits, v: len fp32) as an exact
+// integer sum.  v enters as the 48-bit fixed-point vector q = rint(v 2^s),
+// one exponent per vector, in six balanced base-256 digit planes
+// (q = sum_p 256^p d_p, d_p in [-128, 127]); every fp32 entry within 2^22
+// of the largest |v| is exact in it.  The trits enter through bit masks of
+// the packed bytes: for trit position i of a byte (bits 2i, 2i + 1), the
+// byte & (1 << 2i) is 4^i bit0 and the byte & (2 << 2i) is 2 4^i bit1 (for
+// i = 3 the latter reads as the int8 -128), with t = bit0 - 2 bit1.  On
+// v_mfma_i32_16x16x64_i8 (A: 16 rows x 64 masked bytes, B: the digit planes
+// of the components at trit position i of those bytes in columns 0..5)
+// every product and every int32 sum is exact, so per plane
+//   sum_c t_c d_p,c = sum_{i<3} (acc_i,0 - acc_i,1) / 4^i + (acc_3,0 + acc_3,1) / 64
+// (exact divisions) and y = 2^-s sum_p 256^p (...) in int64.  No table
+// lookups and no data-dependent control flow: the decode is eight ANDs per
+// 16 packed bytes.
+//
+// Layout.  A super-step covers 256 components, 64 packed bytes of a row;
+// lane (rr = lane % 16, g = lane / 16) of a wave holds the 16 bytes
+// [64 ss + 16 g, + 16) of row rr of the wave's 16-row tile, i.e. components
+// c = 256 ss + 64 g + 4 e + i (byte e, trit position i).  The digit planes
+// of the vector live in LDS as [ss][i][g][p][e] (16 bytes per (ss, i, g, p);
+// lane (p, g) reads its B operand as one 16-byte read, the 24 lanes p < 6
+// of a super-step position contiguous; lanes p >= 6 read a zero block).
+// A workgroup holds GV_TILES tiles of 16 rows and the whole vector; the
+// super-steps of a tile are split between GV_KSPLIT waves, whose int32
+// plane sums are added through LDS at the end.  Each workgroup covers the
+// whole contracted dimension, so no partial sums leave it and no workgroup
+// depends on another.
+//
+// The C side (t = diag(D) C x) converts x itself (every workgroup the same
+// arithmetic) and writes t already in digit planes, in the layout above, to
+// the workspace; their common exponent comes from a bound every workgroup
+// forms identically, |t_c| <= max|D| sum_j |x_j|, so no workgroup waits for
+// another's result.  The B side copies those planes into LDS.  A non-finite
+// entry of x or D makes every entry of y NaN.
+constexpr int GV_TILES = 2;                       // 16-row tiles per workgroup
+constexpr int GV_KSPLIT = 4;                      // waves per tile (quarters of the super-steps)
+constexpr int GV_NT = 64 * GV_TILES * GV_KSPLIT;  // threads per workgroup
+constexpr int GV_ROWS = 16 * GV_TILES;            // rows per workgroup
+constexpr int GV_SS = 256;                        // components per super-step
+constexpr int GV_PLANES = 6;
+constexpr int GV_SSB = 4 * 4 * GV_PLANES * 16;    // digit bytes per super-step (= 6 x 256)
+constexpr int GV_MAX_LEN = 10240;                 // longest vector held in LDS
+constexpr int GV_MAX_SS = GV_MAX_LEN / GV_SS;
+constexpr int GV_NONFINITE = 0x7fffffff;          // exponent word: a non-finite input
+static_assert(GV_SSB == GV_PLANES * GV_SS, "digit bytes per super-step");
+
+typedef int v4i_g __attribute__((ext_vector_type(4)));
+
+// Byte offset of the digit of plane p of component c in the [ss][i][g][p][e]
+// layout.
+__device__ __forceinline__ int64_t gv_digit_offset(int64_t c, int p) {
+  const int64_t ss = c >> 8;
+  const int g = (int)(c >> 6) & 3, e = (int)(c >> 2) & 15, i = (int)c & 3;
+  return ss * GV_SSB + (((i * 4 + g) * GV_PLANES + p) << 4) + e;
+}
+
+// Balanced base-256 digits of q, |q| < 2^47: q = sum_{p<6} 256^p d_p with
+// d_0..d_4 in [-128, 127] (bytes of q + 0x8080808080 re-centred) and
+// d_5 = (q + 0x8080808080) >> 40 in [-128, 127].
+__device__ __forceinline__ void gv_digits(long long q, int8_t (&d)[GV_PLANES]) {
+  const long long u = q + 0x8080808080ll;
+#pragma unroll
+  for (int p = 0; p < GV_PLANES - 1; ++p) d[p] = (int8_t)((((unsigned long long)u >> (8 * p)) & 0xFFu) ^ 0x80u);
+  d[GV_PLANES - 1] = (int8_t)(u >> 40);
+}
+
+// 48-bit fixed point: s = 46 - e for a magnitude bound b < 2^e (every |v| <=
+// b gives |v 2^s| < 2^46).
+__device__ __forceinline__ int gv_shift(double b) {
+  int e = 0;
+  if (b > 0.0) frexp(b, &e);
+  return 46 - e;
+}
+
+// Sum (fp64) and two maxima over the workgroup, the same tree in every
+// workgroup: butterfly within each wave, then the waves in order.
+// sh: >= 3 x waves.
+__device__ __forceinline__ void gv_sum_max2(double& sum, double& m1, double& m2, double* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    sum += __shfl_xor(sum, o, 64);
+    m1 = fmax(m1, __shfl_xor(m1, o, 64));
+    m2 = fmax(m2, __shfl_xor(m2, o, 64));
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sh[3 * w] = sum;
+    sh[3 * w + 1] = m1;
+    sh[3 * w + 2] = m2;
+  }
+  __syncthreads();
+  sum = 0.0;
+  m1 = m2 = 0.0;
+  for (int q = 0; q < GV_NT / 64; ++q) {
+    sum += sh[3 * q];
+    m1 = fmax(m1, sh[3 * q + 1]);
+    m2 = fmax(m2, sh[3 * q + 2]);
+  }
+}
+
+// The 16 packed bytes of lane (rr, g) for super-step ss of row `row` (rb
+// bytes per row).  ALIGNED: rb and the base are multiples of 16, so a chunk
+// lies wholly inside or wholly past the row; a chunk past it is loaded from
+// the row's start and zeroed where it is used (gv_tile: masking it here
+// would wait for the load).  Else byte loads, zero past the row.
+template <bool ALIGNED>
+__device__ __forceinline__ v4i_g gv_load(const uint8_t* __restrict__ row, int64_t rb, int64_t ss, int g) {
+  const int64_t o = ss * 64 + 16 * g;
+  if (ALIGNED) return *(const v4i_g*)(row + (o < rb ? o : 0));
+  uint8_t b[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) b[e] = row[o + e < rb ? o + e : 0];
+  unsigned w[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    w[q] = 0u;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[q] |= (o + 4 * q + e < rb ? (unsigned)b[4 * q + e] : 0u) << (8 * e);
+  }
+  return v4i_g{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+}
+
+// The wave's share of a tile: super-steps [s0, s1) of row `row` (rows past
+// the matrix read its last row; their results are discarded).
+struct GvWave {
+  const uint8_t* row;
+  int s0, s1;
+};
+__device__ __forceinline__ GvWave gv_wave(const uint8_t* __restrict__ P, int64_t rows, int64_t rb, int nss,
+                                          int64_t r0) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int tile = w / GV_KSPLIT, kh = w % GV_KSPLIT;
+  const int half = (nss + GV_KSPLIT - 1) / GV_KSPLIT;
+  const int64_t rr = r0 + 16 * tile + (lane & 15);
+  GvWave v;
+  v.row = P + (rr < rows ? rr : rows - 1) * rb;
+  v.s0 = kh * half < nss ? kh * half : nss;
+  v.s1 = (kh + 1) * half < nss ? (kh + 1) * half : nss;
+  return v;
+}
+
+// Super-steps per wave at most (the wave's share of the longest vector),
+// and the steps of trit loads a wave keeps in flight.
+constexpr int GV_NSTEP = (GV_MAX_SS + GV_KSPLIT - 1) / GV_KSPLIT;
+constexpr int GV_PF = 6;
+
+// The wave's trit chunk of step j (super-step s0 + j; a step past s1 loads
+// super-step s0 again, its result unused).
+template <bool ALIGNED>
+__device__ __forceinline__ v4i_g gv_step_load(const GvWave& v, int64_t rb, int j) {
+  const int g = (threadIdx.x & 63) >> 4;
+  return gv_load<ALIGNED>(v.row, rb, v.s0 + j < v.s1 ? v.s0 + j : v.s0, g);
+}
+
+// The first GV_PF steps' trit loads (issued before the vector is staged, so
+// that they are in flight meanwhile).
+template <bool ALIGNED>
+__device__ __forceinline__ void gv_prefetch(const GvWave& v, int64_t rb, v4i_g (&buf)[GV_NSTEP]) {
+#pragma unroll
+  for (int j = 0; j < GV_PF; ++j) buf[j] = gv_step_load<ALIGNED>(v, rb, j);
+}
+
+// One wave's int32 plane sums over its super-steps; out[r] = sum over the
+// wave's components of t_c d_p,c for tile row 4 g + r and plane
+// p = lane % 16 (zero for p >= 6).  dig: the digit planes in LDS; zero16: a
+// zeroed 16-byte LDS block; buf: the wave's trit chunks, the first GV_PF
+// loaded by gv_prefetch.  Unrolled over GV_NSTEP steps, without branches (a
+// loop would carry the loads in flight in registers that its back edge
+// copies, and a branch would make the compiler wait for them at its entry):
+// step j issues the load of step j + GV_PF before its own work.
+template <bool ALIGNED>
+__device__ __forceinline__ void gv_tile(const GvWave& v, int64_t rb, v4i_g (&buf)[GV_NSTEP], const uint8_t* dig,
+                                        const uint8_t* zero16, int (&out)[4]) {
+  const int lane = threadIdx.x & 63, p = lane & 15, g = lane >> 4;
+  v4i_g acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i][0] = acc[i][1] = v4i_g{0, 0, 0, 0};
+  const int boff = ((g * GV_PLANES + p) << 4);  // lane's 16 bytes within an (ss, i) group of 384
+  const uint8_t* bsrc = p < GV_PLANES ? dig + (int64_t)v.s0 * GV_SSB + boff : zero16;
+  const int bstep = p < GV_PLANES ? GV_SSB : 0;
+#pragma unroll
+  for (int j = 0; j < GV_NSTEP; ++j) {
+    if (j + GV_PF < GV_NSTEP) buf[j + GV_PF] = gv_step_load<ALIGNED>(v, rb, j + GV_PF);
+    // keep the load here: scheduled after the step's MFMAs it would leave
+    // the memory system idle meanwhile
+    __builtin_amdgcn_sched_barrier(0);
+    // no branch: a step past the wave's share (or a chunk past the row)
+    // multiplies zero trits, its B operands read at a clamped address
+    const int cur = v.s0 + j;
+    const bool live = cur < v.s1 && (!ALIGNED || (int64_t)cur * 64 + 16 * g < rb);
+    const int jb = cur < v.s1 ? j : 0;
+    v4i_g bo[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) bo[i] = *(const v4i_g*)(bsrc + jb * bstep + i * (4 * GV_PLANES * 16));
+    const v4i_g w = live ? buf[j] : v4i_g{0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m0 = 0x01010101 << (2 * i), m1 = 0x02020202 << (2 * i);
+      const v4i_g a0 = w & m0, a1 = w & m1;
+      acc[i][0] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0, bo[i], acc[i][0], 0, 0, 0);
+      acc[i][1] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1, bo[i], acc[i][1], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    out[r] = ((acc[0][0][r] - acc[0][1][r])) + ((acc[1][0][r] - acc[1][1][r]) >> 2) +
+             ((acc[2][0][r] - acc[2][1][r]) >> 4) + ((acc[3][0][r] + acc[3][1][r]) >> 6);
+}
+
+// The tile's plane sums of both K halves added and the planes combined into
+// int64: for lane l < 16 of the first wave of each tile, the exact
+// sum_c t_c q_c of tile row l.
+__device__ __forceinline__ long long gv_combine(const int (&out)[4], int (*xch)[64][4]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) xch[w][lane][r] = out[r];
+  __syncthreads();
+  long long y = 0;
+  if (w % GV_KSPLIT == 0 && lane < 16) {
+    const int g = lane >> 2, r = lane & 3;
+#pragma unroll
+    for (int p = GV_PLANES - 1; p >= 0; --p) {
+      long long sp = 0;
+#pragma unroll
+      for (int h = 0; h < GV_KSPLIT; ++h) sp += xch[w + h][16 * g + p][r];
+      y = y * 256 + sp;
+    }
+  }
+  return y;
+}
+
+// C side: T (digit planes of t = diag(D) C x, layout above, 256 nss_t
+// components, zero past k) and the exponent word *sT (GV_NONFINITE for a
+// non-finite x or D).  grid: ceil(k / GV_ROWS).
+constexpr int GV_XPT = (GV_MAX_LEN + GV_NT - 1) / GV_NT;  // vector entries per thread at most (x, D)
+template <bool ALIGNED>
+__global__ __launch_bounds__(GV_NT) void k_gemv_c(const uint8_t* __restrict__ Cp, const float* __restrict__ D,
+                                                  const float* __restrict__ X, int64_t n, int64_t k, int nss_t,
+                                                  uint8_t* __restrict__ T, int* __restrict__ sT) {
+  __shared__ __attribute__((aligned(16))) uint8_t dig[GV_MAX_SS * GV_SSB];
+  __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
+  __shared__ int xch[GV_NT / 64][64][4];
+  __shared__ double sh[3 * (GV_NT / 64)];
+  const int tid = threadIdx.x;
+  const int nss = (int)((n + GV_SS - 1) / GV_SS);
+  const int64_t rb = (n + 3) >> 2;
+  const int64_t r0 = (int64_t)blockIdx.x * GV_ROWS;
+  // every load of the prologue in one round (component tid + GV_NT j of x
+  // and D); clamped indices, masked below
+  float xv[GV_XPT], dv[GV_XPT];
+#pragma unroll
+  for (int j = 0; j < GV_XPT; ++j) {
+    const int64_t c = tid + (int64_t)GV_NT * j;
+    xv[j] = X[c < n ? c : 0];
+    dv[j] = D[c < k ? c : 0];
+  }
+  // the trit prefetch after them (a wait for x and D then does not wait for it)
+  __builtin_amdgcn_sched_barrier(0);
+  const GvWave v = gv_wave(Cp, k, rb, nss, r0);
+  v4i_g buf[GV_NSTEP];
+  gv_prefetch<ALIGNED>(v, rb, buf);
+  __builtin_amdgcn_sched_barrier(0);
+  if (tid < 4) ((int*)zero16)[tid] = 0;
+  // statistics of x and D: the same arithmetic in every workgroup
+  double sx = 0.0, mx = 0.0, md = 0.0;
+  bool bad = false;
+#pragma unroll
+  for (int j = 0; j < GV_XPT; ++j) {
+    const int64_t c = tid + (int64_t)GV_NT * j;
+    const double a = c < n ? fabs((double)xv[j]) : 0.0;
+    const double b = c < k ? fabs((double)dv[j]) : 0.0;
+    bad |= !(a <= 1.0e300) || !(b <= 1.0e300);
+    sx += a;
+    mx = fmax(mx, a);
+    md = fmax(md, b);
+  }
+  if (bad) mx = INFINITY;
+  gv_sum_max2(sx, mx, md, sh);
+  const bool finite = mx < INFINITY;
+  const int s_x = gv_shift(mx);
+  const int s_t = gv_shift(md * sx);
+  // x in digit planes (zero past n)
+#pragma unroll
+  for (int j = 0; j < GV_XPT; ++j) {
+    const int64_t c = tid + (int64_t)GV_NT * j;
+    if (c < (int64_t)nss * GV_SS) {
+      const float x = (c < n && finite) ? xv[j] : 0.0f;
+      int8_t d[GV_PLANES];
+      gv_digits((long long)rint(ldexp((double)x, s_x)), d);
+#pragma unroll
+      for (int p = 0; p < GV_PLANES; ++p) dig[gv_digit_offset(c, p)] = (uint8_t)d[p];
+    }
+  }
+  __syncthreads();
+  int out[4];
+  gv_tile<ALIGNED>(v, rb, buf, dig, zero16, out);
+  const long long y = gv_combine(out, xch);
+  const int lane = tid & 63, w = tid >> 6;
+  if (w % GV_KSPLIT == 0 && lane < 16) {
+    const int64_t c = r0 + 16 * (w / GV_KSPLIT) + lane;
+    if (c < (int64_t)nss_t * GV_SS) {
+      long long q = 0;
+      if (c < k && finite) q = (long long)rint(ldexp((double)y, s_t - s_x) * (double)D[c]);
+      int8_t d[GV_PLANES];
+      gv_digits(q, d);
+#pragma unroll
+      for (int p = 0; p < GV_PLANES; ++p) T[gv_digit_offset(c, p)] = (uint8_t)d[p];
+    }
+  }
+  // the padding components past the last workgroup's rows
+  if (blockIdx.x == gridDim.x - 1) {
+    for (int64_t c = (int64_t)gridDim.x * GV_ROWS + tid; c < (int64_t)nss_t * GV_SS; c += GV_NT)
+#pragma unroll
+      for (int p = 0; p < GV_PLANES; ++p) T[gv_digit_offset(c, p)] = 0;
+  }
+  if (blockIdx.x == 0 && tid == 0) *sT = finite ? s_t : GV_NONFINITE;
+}
+
+// B side: Y[i] = sum_c B_ic t_c from the digit planes of t.  grid:
+// ceil(m / GV_ROWS).
+template <bool ALIGNED>
+__global__ __launch_bounds__(GV_NT) __attribute__((amdgpu_waves_per_eu(4))) void k_gemv_b(const uint8_t* __restrict__ Bp, const uint8_t* __restrict__ T,
+                                                  const int* __restrict__ sT, int64_t m, int64_t k,
+                                                  float* __restrict__ Y) {
+  __shared__ __attribute__((aligned(16))) uint8_t dig[GV_MAX_SS * GV_SSB];
+  __shared__ __attribute__((aligned(16))) uint8_t zero16[16];
+  __shared__ int xch[GV_NT / 64][64][4];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int nss = (int)((k + GV_SS - 1) / GV_SS);
+  const int64_t rb = (k + 3) >> 2;
+  const int64_t r0 = (int64_t)blockIdx.x * GV_ROWS;
+  // the digit planes of t: every load in one round (16 bytes per piece,
+  // clamped indices), then the trit prefetch, then the LDS stores (the wait
+  // for the pieces leaves the prefetch in flight)
+  constexpr int NCP = (GV_MAX_SS * GV_SSB / 16 + GV_NT - 1) / GV_NT;
+  const int ncp = nss * GV_SSB / 16;
+  v4i_g cp[NCP];
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) {
+    const int e = tid + GV_NT * j;
+    cp[j] = ((const v4i_g*)T)[e < ncp ? e : 0];
+  }
+  const int s_t = *sT;
+  __builtin_amdgcn_sched_barrier(0);
+  const GvWave v = gv_wave(Bp, m, rb, nss, r0);
+  v4i_g buf[GV_NSTEP];
+  gv_prefetch<ALIGNED>(v, rb, buf);
+  __builtin_amdgcn_sched_barrier(0);
+  if (tid < 4) ((int*)zero16)[tid] = 0;
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) {
+    const int e = tid + GV_NT * j;
+    if (e < ncp) ((v4i_g*)dig)[e] = cp[j];
+  }
+  __syncthreads();
+  int out[4];
+  gv_tile<ALIGNED>(v, rb, buf, dig, zero16, out);
+  const long long y = gv_combine(out, xch);
+  if (wv % GV_KSPLIT == 0 && lane < 16) {
+    const int64_t i = r0 + 16 * (wv / GV_KSPLIT) + lane;
+    if (i < m) Y[i] = s_t == GV_NONFINITE ? NAN : (float)ldexp((double)y, -s_t);
+  }
+}
+
 // ---- matrix-core path ----
 
 // Chunks per slice for nch chunks over nrg row groups: the most (a power of
@@ -458,8 +825,18 @@ static size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Workspace (offsets 256-byte aligned): the parts of T (3 nb columns of
 // kp) and the partial sums (shared by the two products, which run one
 // after the other).
+// One vector with both sides short enough for the vector's digit planes to
+// fit in LDS: the integer matrix-core path (k_gemv_c, k_gemv_b).
+static bool gemv_fits(int64_t n, int64_t k, int nb) { return nb == 1 && n <= GV_MAX_LEN && k <= GV_MAX_LEN; }
+
 static ApplyLayout apply_layout(int64_t m, int64_t n, int64_t k, int nb) {
   ApplyLayout L{};
+  if (gemv_fits(n, k, nb)) {
+    // the digit planes of t (256-component super-steps) and the exponent word
+    L.ts = al256((size_t)((k + GV_SS - 1) / GV_SS) * GV_SSB);
+    L.total = L.ts + 256;
+    return L;
+  }
   if (nb <= AP_VEC_MAX) {
     // vector-ALU path: T, nb x kq floats (kq = k rounded up to 4)
     L.total = al256(sizeof(float) * (size_t)nb * (size_t)((k + 3) & ~(int64_t)3));
@@ -526,8 +903,30 @@ static hipError_t run_vec(const uint8_t* Bp, const uint8_t* Cp, const float* D, 
   return hipGetLastError();
 }
 
+static hipError_t run_gemv(const uint8_t* Bp, const uint8_t* Cp, const float* D, int64_t m, int64_t n, int64_t k,
+                           const float* X, float* Y, char* ws, hipStream_t s) {
+  const ApplyLayout L = apply_layout(m, n, k, 1);
+  uint8_t* T = (uint8_t*)ws;
+  int* sT = (int*)(ws + L.ts);
+  const int nss_t = (int)((k + GV_SS - 1) / GV_SS);
+  const int64_t rbc = (n + 3) / 4, rbb = (k + 3) / 4;
+  const dim3 gc((unsigned)((k + GV_ROWS - 1) / GV_ROWS)), gb((unsigned)((m + GV_ROWS - 1) / GV_ROWS));
+  if (rbc % 16 == 0 && ((uintptr_t)Cp % 16) == 0)
+    hipLaunchKernelGGL(k_gemv_c<true>, gc, dim3(GV_NT), 0, s, Cp, D, X, n, k, nss_t, T, sT);
+  else
+    hipLaunchKernelGGL(k_gemv_c<false>, gc, dim3(GV_NT), 0, s, Cp, D, X, n, k, nss_t, T, sT);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (rbb % 16 == 0 && ((uintptr_t)Bp % 16) == 0)
+    hipLaunchKernelGGL(k_gemv_b<true>, gb, dim3(GV_NT), 0, s, Bp, (const uint8_t*)T, (const int*)sT, m, k, Y);
+  else
+    hipLaunchKernelGGL(k_gemv_b<false>, gb, dim3(GV_NT), 0, s, Bp, (const uint8_t*)T, (const int*)sT, m, k, Y);
+  return hipGetLastError();
+}
+
 static hipError_t run_apply_kernels(const uint8_t* Bp, const uint8_t* Cp, const float* D, int64_t m, int64_t n,
                                     int64_t k, const float* X, int nb, float* Y, char* ws, hipStream_t s) {
+  if (gemv_fits(n, k, nb)) return run_gemv(Bp, Cp, D, m, n, k, X, Y, ws, s);
   if (nb <= AP_VEC_MAX) return run_vec<AP_VEC_MAX>(Bp, Cp, D, m, n, k, X, nb, Y, (float*)ws, s);
   const ApplyLayout L = apply_layout(m, n, k, nb);
   unsigned short* TS = (unsigned short*)(ws + L.ts);

@@ -125,9 +125,14 @@ def test_argument_errors_before_device_work():
              None, dummy, 16, None) == binding.EWORKSPACE
     # inference: batch limits, workspace size and alignment
     ap = L.externd_apply
-    # nb = 1 (vector-ALU path): the intermediate T, k floats (k rounded up to 4), rounded up to 256 bytes
+    # nb = 1, n and k <= 10240 (integer matrix-core path): the six digit planes of the intermediate T,
+    # 1536 bytes per 256 components of k, rounded up to 256 bytes, then a 256-byte exponent word
     wsb = L.externd_apply_workspace_bytes
-    assert wsb(100, 100, 100, 1) == 512 and wsb(100, 100, 101, 1) == 512 and wsb(5, 5, 5, 1) == 256
+    assert wsb(100, 100, 100, 1) == 1536 + 256 and wsb(100, 100, 101, 1) == 1536 + 256
+    assert wsb(5, 5, 5, 1) == 1536 + 256 and wsb(9728, 2560, 7680, 1) == 30 * 1536 + 256
+    assert wsb(9728, 10240, 10240, 1) == 40 * 1536 + 256
+    # nb = 1 with n or k above 10240 (vector-ALU path): T, k floats (k rounded up to 4), rounded up to 256 bytes
+    assert wsb(100, 10241, 100, 1) == 512 and wsb(100, 100, 10241, 1) == 41216
     # nb >= 2 (matrix-core path), 100 x 100 x 100: the parts of T (3 nb columns of 128 bf16, rounded up to
     # 256 bytes); one slice per product, so no partial sums
     assert wsb(100, 100, 100, 2) == 1536 and wsb(100, 100, 100, 3) == 2304
