@@ -27,6 +27,11 @@ struct Layout {
   size_t total;
 };
 
+static int64_t stat_tiles(int64_t nrt, int64_t nct, int64_t ntu) {
+  const int64_t a = nrt > 2 * nct ? nrt : 2 * nct;
+  return a > ntu ? a : ntu;
+}
+
 static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   Layout L{};
   L.m_pad = round_up(m, TILE);
@@ -46,8 +51,9 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   L.nsu = clampi((L.m_pad + TERN_CHUNK - 1) / TERN_CHUNK, 1, TERN_SPLIT_MAX);
   L.nsv = clampi((L.n_pad + TERN_CHUNK - 1) / TERN_CHUNK, 1, TERN_SPLIT_MAX);
   L.nblk_cap = (int)(k + 2);  // fro2 before every block and after the last; one spare
-  // statistics tiles: 32-row tiles of the U side, 16-column tiles of the V side
-  const int64_t ntmax = nrt > 2 * nct ? nrt : 2 * nct;
+  // statistics tiles: 32-row tiles (initial gather, wide U-steps) or the
+  // U-step's row groups on the U side, 16-column tiles on the V side
+  const int64_t ntmax = stat_tiles(nrt, nct, L.ntu);
   const size_t sizes[] = {
       sizeof(float) * (size_t)(L.m_pad * L.n_pad),     // 0 R
       (size_t)(BMAX * L.m_pad),                        // 1 Ut
@@ -168,7 +174,7 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.ginvVW = (double*)(b + L.off[43]);
   w.wflag = (int*)(b + L.off[45]);
   const int64_t nrt = L.m_pad / TILE, nct = L.n_pad / TILE;
-  w.ntmax = nrt > 2 * nct ? nrt : 2 * nct;
+  w.ntmax = stat_tiles(nrt, nct, L.ntu);
   return true;
 }
 
@@ -640,7 +646,7 @@ int externd_step_ustep(const float* R, int64_t m, int64_t n, const int8_t* V, in
   HIP_TRY(load_factor_quarters(w, 1, V, n, bb, s));
   if (h) HIP_TRY(launch_vweight(w, bb, s));
   HIP_TRY(bb > BBP ? launch_ustep_wide(w, 0, bb, tau, h != nullptr, false, s)
-                   : launch_ustep(w, 0, bb, tau, h != nullptr, false, s));
+                   : launch_ustep(w, 0, bb, tau, h != nullptr, false, s, nullptr, true));
   HIP_TRY(launch_store_factor(U_out, w.Ut, m, w.m_pad, bb, s));
   if (Q_out_or_null) HIP_TRY(launch_store_cm(Q_out_or_null, w.Q, m, w.m_pad, bb, s));
   if (Z_out_or_null) HIP_TRY(launch_store_cm(Z_out_or_null, w.Z, m, w.m_pad, bb, s));

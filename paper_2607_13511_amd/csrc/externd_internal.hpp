@@ -55,10 +55,13 @@ constexpr int TERN_CHUNK = 640;
 // CNT_SAFEGUARD: blocks replaced by the single-entry step; CNT_SG_*: the
 // last block's single-entry decision (fired, row, column, negative sign);
 // CNT_SEQ_USED: components extracted by the persistent sequential path.
+// CNT_GINV_V: set to 1 by the U-step's side path once G_V^{-1} is stored
+// (the row groups of the same launch wait for it); cleared by k_tern_u.
 enum Counter {
   CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2,
   CNT_DECISION = 5, CNT_ACCEPTED = 6, CNT_SAFEGUARD = 7,
-  CNT_SG_FIRE = 8, CNT_SG_ROW = 9, CNT_SG_COL = 10, CNT_SG_NEG = 11, CNT_SEQ_USED = 12, CNT_COUNT = 16
+  CNT_SG_FIRE = 8, CNT_SG_ROW = 9, CNT_SG_COL = 10, CNT_SG_NEG = 11, CNT_SEQ_USED = 12, CNT_GINV_V = 13,
+  CNT_COUNT = 16
 };
 // Flags written by the device, read by the host.
 enum Flag { FLAG_NONFINITE = 0, FLAG_BADWEIGHT = 1, FLAG_SYNC = 2, FLAG_COUNT = 4 };
@@ -188,8 +191,10 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
                         bool weighted = false);
 // final: the last U-step of a block, which also forms g = diag(U^T Q) for
 // the scale solve.
+// keep_q: store Q also when the step is not the block's last (the step API
+// returns it).
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
-                        Timer* t = nullptr);
+                        Timer* t = nullptr, bool keep_q = false);
 hipError_t launch_scale(const Ws& w, int bb, hipStream_t s);
 // Wide blocks (64 < bb <= BMAX): the same steps over the quarters of the
 // block, coupled through the BMAX x BMAX Gram inverses and joint solve.

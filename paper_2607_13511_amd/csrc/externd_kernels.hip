@@ -186,24 +186,53 @@ __device__ __forceinline__ long long combine_acc(const v16i (&acc)[2][4], int t,
          ((long long)acc[t][3][r] << 24);
 }
 
+// Planes folded in pairs, lo = a0 + 2^8 a1 and hi = a2 + 2^8 a3, so that the
+// tile entry is lo + 2^16 hi.  Every product of a digit (|d| <= 128) and a
+// trit is at most 2^7, a K step adds 32 of them, so after k K steps over all
+// waves |lo|, |hi| <= k 2^12 257: the folded sums stay exact in int32 for
+// k <= FOLD_KMAX.
+constexpr int FOLD_KMAX = 2039;  // floor((2^31 - 1) / (2^12 257))
+__device__ __forceinline__ int2 fold_acc(const v16i (&acc)[2][4], int t, int r) {
+  return make_int2(acc[t][0][r] + acc[t][1][r] * 256, acc[t][2][r] + acc[t][3][r] * 256);
+}
+
 // Sum of the 4 waves' contraction tiles (2 tiles of 32x32, MFMA output
 // layout) through LDS (red: 8192 int64 = 64 KB).  Wave w finishes slots
 // 8w .. 8w + 7; out(t, M, N, v) receives every entry once, M the tile row
-// and N the tile column.  Integer sums: exact and order-free.
+// and N the tile column.  Integer sums: exact and order-free.  With `fold`
+// (at most FOLD_KMAX K steps summed in the workgroup) the planes travel as
+// int32 pairs and only the final entries are widened, a quarter of the
+// 64-bit work of widening every wave's planes.
 template <typename Out>
-__device__ __forceinline__ void reduce_waves(long long* red, const v16i (&acc)[2][4], Out out) {
+__device__ __forceinline__ void reduce_waves(long long* red, const v16i (&acc)[2][4], bool fold, Out out) {
   const int lane = lane_id(), wave = wave_id();
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) red[(wave * 32 + t * 16 + r) * 64 + lane] = combine_acc(acc, t, r);
-  __syncthreads();
   long long v[8];
+  if (fold) {
+    int2* r2 = (int2*)red;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int slot = wave * 8 + i;
-    v[i] = red[slot * 64 + lane] + red[(32 + slot) * 64 + lane] + red[(64 + slot) * 64 + lane] +
-           red[(96 + slot) * 64 + lane];
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) r2[(wave * 32 + t * 16 + r) * 64 + lane] = fold_acc(acc, t, r);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int slot = wave * 8 + i;
+      const int2 a = r2[slot * 64 + lane], b = r2[(32 + slot) * 64 + lane];
+      const int2 c = r2[(64 + slot) * 64 + lane], d = r2[(96 + slot) * 64 + lane];
+      v[i] = (long long)((a.x + b.x) + (c.x + d.x)) + (long long)((a.y + b.y) + (c.y + d.y)) * 65536;
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) red[(wave * 32 + t * 16 + r) * 64 + lane] = combine_acc(acc, t, r);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int slot = wave * 8 + i;
+      v[i] = red[slot * 64 + lane] + red[(32 + slot) * 64 + lane] + red[(64 + slot) * 64 + lane] +
+             red[(96 + slot) * 64 + lane];
+    }
   }
   __syncthreads();  // red may be reused by out()
 #pragma unroll
@@ -374,6 +403,37 @@ __device__ __forceinline__ void load_ginv(const double* ginv, double (&a)[16]) {
   const double* p = ginv + wave_id() * 1024 + lane_id();
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) a[ks] = p[ks * 64];
+}
+// The same for a consumer in the producer's launch: the inverse was
+// written through by a workgroup on any XCD, so the loads bypass the L2.
+__device__ __forceinline__ void load_ginv_coherent(const double* ginv, double (&a)[16]) {
+  const double* p = ginv + wave_id() * 1024 + lane_id();
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(p + ks * 64);
+}
+
+// A flag between the workgroups of one launch.  The producer's stores are
+// coherent (written through); once every one of them has completed
+// (s_waitcnt, then the barrier) one thread sets the flag.  The waiting side
+// polls it with coherent loads for at most SYNC_TICKS of the 100 MHz wall
+// clock (20 ms, against a few microseconds expected); past that it raises
+// FLAG_SYNC, which the host reports as EXTERND_ESYNC, and goes on.
+constexpr unsigned long long SYNC_TICKS = 2000000ull;
+__device__ __forceinline__ void ginv_ready(unsigned* ready) {
+  if (!ready) return;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) store_coherent(ready, 1u);
+}
+__device__ __forceinline__ void await_flag(unsigned* ready, int* flags) {
+  const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+  while (load_coherent(ready) == 0u) {
+    if (__builtin_amdgcn_s_memrealtime() - t0 > SYNC_TICKS) {
+      store_coherent(flags + FLAG_SYNC, 1);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
 }
 
 // nk: pivot blocks to sweep, ceil(bb / 4) for a block of bb real components
@@ -989,7 +1049,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   // out[t][M = component][N = column]: this row group's partial P tile, at
   // the column's fixed-point scale
   long long* Pg = Pp + ((int64_t)g * BBP) * n_pad + (int64_t)ct * TILE;
-  reduce_waves(smem, acc, [&](int t, int M, int N, long long v) { Pg[(int64_t)(32 * t + M) * n_pad + N] = v; });
+  reduce_waves(smem, acc, ks1 - ks0 <= FOLD_KMAX,
+               [&](int t, int M, int N, long long v) { Pg[(int64_t)(32 * t + M) * n_pad + N] = v; });
 }
 
 // V-step target Y = G_U^{-1} P (Eq. (3) first half) and its T_tau
@@ -1094,7 +1155,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
                                               int64_t m_pad, int64_t n_pad, int bb, int* gacc, unsigned* counter,
                                               double* ginvV, double* gramV, int nside, int rows,
                                               const int8_t* __restrict__ Wmf, long long* gacc64,
-                                              const double* __restrict__ hwmax) {
+                                              const double* __restrict__ hwmax, double* __restrict__ Z, double* ps,
+                                              double* pm, int* pi, int64_t m, unsigned* ready, int* flags,
+                                              int storeQ) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 4 waves x NST_U staged K steps (52 KB), then the 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[USTEP_SMEM_LL];
@@ -1112,6 +1175,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
         for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
         __syncthreads();
         ridge_invert_store(Gs, pbuf, bb, ginvV);
+        ginv_ready(ready);
       }
       return;
     }
@@ -1119,6 +1183,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
       for (int e = threadIdx.x; e < 4096; e += NT) gramV[e] = Gs[e];
       __syncthreads();
       ridge_invert_store(Gs, pbuf, bb, ginvV);
+      ginv_ready(ready);
     }
     return;
   }
@@ -1257,11 +1322,35 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   // out[t][M = row][N = component] -> Q[32 t + N][row], via a transposed
   // LDS tile for coalesced stores
   double* tq = (double*)smem;
-  reduce_waves(smem, acc,
+  reduce_waves(smem, acc, nks <= FOLD_KMAX,
                [&](int t, int M, int N, long long v) { tq[(32 * t + N) * 32 + M] = ldexp((double)v, -s_row[M]); });
   __syncthreads();
-  for (int e = threadIdx.x; e < 2048; e += NT)
-    if ((e & 31) < valid) Q[(int64_t)(e >> 5) * m_pad + i0 + (e & 31)] = tq[e];
+  if (storeQ)
+    for (int e = threadIdx.x; e < 2048; e += NT)
+      if ((e & 31) < valid) Q[(int64_t)(e >> 5) * m_pad + i0 + (e & 31)] = tq[e];
+  if (!Z) return;
+  // The target rows Z = Q G_V^{-1} of this row group (Eq. (3) second half)
+  // and their T_tau statistics, once the side path has stored G_V^{-1}.
+  if (threadIdx.x == 0) await_flag(ready, flags);
+  __syncthreads();
+  double a[16];
+  load_ginv_coherent(ginvV, a);
+  const int li = lane & 15, lk = lane >> 4;
+  v4d z[2] = {v4d{}, v4d{}};
+  // A = G^{-1}[16 w + li][4 ks + lk], B = Q^T[4 ks + lk][li (+16)] (LDS)
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) {
+    z[0] = mfma_f64(a[ks], tq[(4 * ks + lk) * 32 + li], z[0]);
+    z[1] = mfma_f64(a[ks], tq[(4 * ks + lk) * 32 + 16 + li], z[1]);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    double* row = Z + (int64_t)(16 * wave + lk + 4 * r) * m_pad + i0;
+    if (li < valid) row[li] = z[0][r];
+    if (16 + li < valid) row[16 + li] = z[1][r];
+  }
+  const int64_t iend = i0 + valid < m ? i0 + valid : m;
+  tile_stats(z, wave, i0, iend, (int)gridDim.x - nside, rt, ps, pm, pi);
 }
 
 // U-step target rows Z = Q G_V^{-1} (Eq. (3) second half) and their T_tau
@@ -1479,8 +1568,9 @@ __global__ __launch_bounds__(NT) void k_tern_u(const double* __restrict__ Z, con
                                                int64_t m_pad, int bb, double tau, const double* __restrict__ ps,
                                                const double* __restrict__ pm, const int* __restrict__ pi, int ntile,
                                                int ns, int8_t* __restrict__ Ut, int8_t* __restrict__ Umf,
-                                               double* __restrict__ gpart) {
+                                               double* __restrict__ gpart, unsigned* ready) {
   const int c = blockIdx.x / ns, sp = blockIdx.x % ns;
+  if (ready && blockIdx.x == 0 && threadIdx.x == 0) *ready = 0u;  // the U-step's G_V^{-1} flag
   int64_t i0, i1;
   tern_range(m_pad, sp, ns, i0, i1);
   int8_t* dst = Ut + (int64_t)c * m_pad;
@@ -3169,7 +3259,7 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, w.Z, (const double*)nullptr, w.m, w.m_pad, bb, tau,
-                     w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec);
+                     w.tps, w.tpm, w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec, (unsigned*)nullptr);
   return hipGetLastError();
 }
 
@@ -3191,30 +3281,34 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
   return hipGetLastError();
 }
 
+// One launch forms Q = R diag(h~) V, G_V^{-1} (side path) and the targets
+// Z = Q G_V^{-1} with their statistics (one tile per row group); Q is
+// stored only where it is read afterwards (g of the last U-step of a block,
+// the step API).
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
-                        Timer* tm) {
+                        Timer* tm, bool keep_q) {
   hipError_t e;
   const unsigned nside = NSIDE_GRAM;
   const unsigned grid = (unsigned)(nside + w.ntu);
+  unsigned* ready = w.counters + CNT_GINV_V;
+  const int storeQ = (final || keep_q) ? 1 : 0;
   if (weighted)
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.rowb, w.m_pad, w.n_pad, bb, w.gacc + 4096,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows,
-                                     (const int8_t*)w.Wmf, w.gacc64, (const double*)w.hwmax);
+                                     (const int8_t*)w.Wmf, w.gacc64, (const double*)w.hwmax, w.Z, w.tps, w.tpm,
+                                     w.tpi, w.m, ready, w.flags, storeQ);
   else
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Vmf, w.Vr, w.hw, w.Q,
                                      w.rowb, w.m_pad, w.n_pad, bb, w.gacc + 4096,
                                      w.counters + CNT_GRAM_V, w.ginvV, w.gramV, (int)nside, w.urows,
-                                     (const int8_t*)nullptr, (long long*)nullptr, (const double*)nullptr);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_UTARGET, k_utarget<false>, dim3((unsigned)(w.m_pad / TILE)), dim3(NT), 0,
-                       s, (const double*)w.Q, (const double*)w.ginvV, w.Z, w.m, w.m_pad, w.tps, w.tpm, w.tpi, 1);
+                                     (const int8_t*)nullptr, (long long*)nullptr, (const double*)nullptr, w.Z,
+                                     w.tps, w.tpm, w.tpi, w.m, ready, w.flags, storeQ);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNU, k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, (const double*)w.Z,
                        final ? (const double*)w.Q : nullptr, w.m, w.m_pad, bb, tau, (const double*)w.tps,
-                       (const double*)w.tpm, (const int*)w.tpi, (int)(w.m_pad / TILE), w.nsu, w.Ut, w.Umf, w.gvec);
+                       (const double*)w.tpm, (const int*)w.tpi, w.ntu, w.nsu, w.Ut, w.Umf, w.gvec, ready);
   return hipGetLastError();
 }
 
@@ -3332,12 +3426,14 @@ hipError_t launch_ustep_wide(const Ws& w, int blk, int bb, double tau, bool weig
       EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<true>), dim3((unsigned)w.ntu), dim3(NT), 0, s, w.R,
                            (const v4i*)v.Vmf, v.Vr, w.hw, v.Q, w.rowb, w.m_pad, w.n_pad, bq, w.gacc + 4096,
                            w.counters + CNT_GRAM_V, w.ginvV, w.gramV, 0, w.urows, (const int8_t*)nullptr,
-                           (long long*)nullptr, (const double*)nullptr);
+                           (long long*)nullptr, (const double*)nullptr, (double*)nullptr, (double*)nullptr,
+                           (double*)nullptr, (int*)nullptr, w.m, (unsigned*)nullptr, (int*)nullptr, 1);
     else
       EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_USTEP, (k_ustep<false>), dim3((unsigned)w.ntu), dim3(NT), 0, s, w.R,
                            (const v4i*)v.Vmf, v.Vr, w.hw, v.Q, w.rowb, w.m_pad, w.n_pad, bq, w.gacc + 4096,
                            w.counters + CNT_GRAM_V, w.ginvV, w.gramV, 0, w.urows, (const int8_t*)nullptr,
-                           (long long*)nullptr, (const double*)nullptr);
+                           (long long*)nullptr, (const double*)nullptr, (double*)nullptr, (double*)nullptr,
+                           (double*)nullptr, (int*)nullptr, w.m, (unsigned*)nullptr, (int*)nullptr, 1);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -3353,7 +3449,7 @@ hipError_t launch_ustep_wide(const Ws& w, int blk, int bb, double tau, bool weig
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNU, k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, (const double*)v.Z,
                          final ? (const double*)v.Q : nullptr, w.m, w.m_pad, bb_of_quarter(bb, q), tau,
                          (const double*)v.tps, (const double*)v.tpm, (const int*)v.tpi, (int)(w.m_pad / TILE), w.nsu,
-                         v.Ut, v.Umf, v.gvec);
+                         v.Ut, v.Umf, v.gvec, (unsigned*)nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
