@@ -99,7 +99,7 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
       (size_t)(WDIG * BMAX * L.n_pad),                 // 41 Wmf
       sizeof(double) * BMAX * BMAX,                    // 42 ginvUW
       sizeof(double) * BMAX * BMAX,                    // 43 ginvVW
-      0,                                               // 44 (unused)
+      sizeof(unsigned) * (size_t)(L.n_pad / TILE),    // 44 vtcnt
       sizeof(int) * 64,                                // 45 wflag
   };
   size_t o = 0;
@@ -173,6 +173,7 @@ bool carve(Ws& w, void* base, size_t bytes, int64_t m, int64_t n, int64_t k) {
   w.ginvUW = (double*)(b + L.off[42]);
   w.ginvVW = (double*)(b + L.off[43]);
   w.wflag = (int*)(b + L.off[45]);
+  w.vtcnt = (unsigned*)(b + L.off[44]);
   const int64_t nrt = L.m_pad / TILE, nct = L.n_pad / TILE;
   w.ntmax = stat_tiles(nrt, nct, L.ntu);
   return true;

@@ -57,11 +57,12 @@ constexpr int TERN_CHUNK = 640;
 // CNT_SEQ_USED: components extracted by the persistent sequential path.
 // CNT_GINV_V: set to 1 by the U-step's side path once G_V^{-1} is stored
 // (the row groups of the same launch wait for it); cleared by k_tern_u.
+// CNT_GINV_U: the same for the V-step's G_U^{-1}; cleared by k_tern_v.
 enum Counter {
   CNT_GRAM_U = 0, CNT_GRAM_V = 1, CNT_SCALE = 2,
   CNT_DECISION = 5, CNT_ACCEPTED = 6, CNT_SAFEGUARD = 7,
   CNT_SG_FIRE = 8, CNT_SG_ROW = 9, CNT_SG_COL = 10, CNT_SG_NEG = 11, CNT_SEQ_USED = 12, CNT_GINV_V = 13,
-  CNT_COUNT = 16
+  CNT_GINV_U = 14, CNT_COUNT = 16
 };
 // Flags written by the device, read by the host.
 enum Flag { FLAG_NONFINITE = 0, FLAG_BADWEIGHT = 1, FLAG_SYNC = 2, FLAG_COUNT = 4 };
@@ -124,6 +125,7 @@ struct Ws {
   double* ginvUW;        // NQMAX x NQMAX blocks of 4096 (fp64 MFMA operand order): (U^T U + eps I)^{-1}
   double* ginvVW;        // the same for (V^T H V + eps I)^{-1}
   int* wflag;            // 1: the swept matrix had zero trace
+  unsigned* vtcnt;       // n_pad / 32 arrival counters of the V-step's column tiles (zero between launches)
   double* fro2_hist;     // nblk_cap: ||R||^2 before each block, then after the last
   double* fro2w_hist;    // nblk_cap: weighted ||R||^2
   unsigned* counters;    // CNT_COUNT

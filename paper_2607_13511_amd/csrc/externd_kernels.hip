@@ -404,13 +404,11 @@ __device__ __forceinline__ void load_ginv(const double* ginv, double (&a)[16]) {
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks) a[ks] = p[ks * 64];
 }
-// The same for a consumer in the producer's launch: the inverse was
-// written through by a workgroup on any XCD, so the loads bypass the L2.
-__device__ __forceinline__ void load_ginv_coherent(const double* ginv, double (&a)[16]) {
-  const double* p = ginv + wave_id() * 1024 + lane_id();
-#pragma unroll
-  for (int ks = 0; ks < 16; ++ks) a[ks] = load_coherent(p + ks * 64);
-}
+// A consumer in the producer's launch loads it the same way once the flag
+// below is seen: the producer wrote it through to memory, and no workgroup
+// of the launch reads those lines before the flag, so no L2 holds an older
+// copy (each launch starts with clean caches); the first workgroup of each
+// XCD fetches them from memory and the others hit in its L2.
 
 // A flag between the workgroups of one launch.  The producer's stores are
 // coherent (written through); once every one of them has completed
@@ -984,7 +982,9 @@ __device__ __forceinline__ void tile_stats(const v4d (&x)[2], int w, int64_t i0,
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_vstep(const float* __restrict__ R, const v4i* __restrict__ Umf,
                                               long long* __restrict__ Pp, const int* __restrict__ cshift,
                                               int64_t m_pad, int64_t n_pad, int gv, int bb, int* gacc,
-                                              unsigned* gcounter, double* ginvU, int nside) {
+                                              unsigned* gcounter, double* ginvU, int nside, double* __restrict__ Y,
+                                              double* ps, double* pm, int* pi, int64_t n, unsigned* tcnt,
+                                              unsigned* ready, int* flags) {
   // side path: ired 16 KB | G 32 KB | inverse scratch 8 KB; contraction:
   // 64 KB wave reduction
   __shared__ __attribute__((aligned(16))) long long smem[8192];
@@ -996,6 +996,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     double* pbuf = Gs + 4096;
     if (!side_gram_acc(Umf, m_pad, blockIdx.x, nside, gacc, gcounter, Gs, (int*)smem)) return;
     ridge_invert_store(Gs, pbuf, bb, ginvU);
+    ginv_ready(ready);
     return;
   }
   const int b = blockIdx.x - nside;
@@ -1049,8 +1050,70 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   // out[t][M = component][N = column]: this row group's partial P tile, at
   // the column's fixed-point scale
   long long* Pg = Pp + ((int64_t)g * BBP) * n_pad + (int64_t)ct * TILE;
+  if (!Y) {
+    reduce_waves(smem, acc, ks1 - ks0 <= FOLD_KMAX,
+                 [&](int t, int M, int N, long long v) { Pg[(int64_t)(32 * t + M) * n_pad + N] = v; });
+    return;
+  }
+  // The partials go out written through, and the last of the column tile's
+  // gv row groups to arrive forms its targets Y = G_U^{-1} P (Eq. (3) first
+  // half) and their T_tau statistics (one 32-column tile).
   reduce_waves(smem, acc, ks1 - ks0 <= FOLD_KMAX,
-               [&](int t, int M, int N, long long v) { Pg[(int64_t)(32 * t + M) * n_pad + N] = v; });
+               [&](int t, int M, int N, long long v) { store_coherent(Pg + (int64_t)(32 * t + M) * n_pad + N, v); });
+  __builtin_amdgcn_s_waitcnt(0);
+  __shared__ int s_last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned old = __hip_atomic_fetch_add(tcnt + ct, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = old == (unsigned)(gv - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  if (threadIdx.x == 0) store_coherent(tcnt + ct, 0u);
+  // P = sum of the partials (exact int64), at the column's scale 2^-s:
+  // Ps[c * 33 + j], thread (c = e / 32, j = e % 32) for e = tid + 256 i
+  double* Ps = (double*)smem;
+  const int64_t j0 = (int64_t)ct * TILE;
+  // thread (c = e / 32, j = e % 32) for e = tid + 256 i, in two rounds of
+  // four entries: the gv partials of each entry, all in flight at once
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    long long v[4][GV_MAX];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = threadIdx.x + NT * (4 * half + i), c = e >> 5, j = e & 31;
+#pragma unroll
+      for (int gg = 0; gg < GV_MAX; ++gg)
+        v[i][gg] = gg < gv ? load_coherent(Pp + ((int64_t)gg * BBP + c) * n_pad + j0 + j) : 0ll;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = threadIdx.x + NT * (4 * half + i), c = e >> 5, j = e & 31;
+      long long sum = 0;
+#pragma unroll
+      for (int gg = 0; gg < GV_MAX; ++gg) sum += v[i][gg];
+      Ps[c * 33 + j] = ldexp((double)sum, -cshift[j0 + j]);
+    }
+  }
+  if (threadIdx.x == 0) await_flag(ready, flags);
+  __syncthreads();
+  double a[16];
+  load_ginv(ginvU, a);
+  const int li = lane & 15, lk = lane >> 4;
+  v4d y[2] = {v4d{}, v4d{}};
+  // A = G^{-1}[16 w + li][4 ks + lk], B = P[4 ks + lk][li (+16)] (LDS)
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) {
+    y[0] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + li], y[0]);
+    y[1] = mfma_f64(a[ks], Ps[(4 * ks + lk) * 33 + 16 + li], y[1]);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    double* row = Y + (int64_t)(16 * wave + lk + 4 * r) * n_pad + j0;
+    row[li] = y[0][r];
+    row[16 + li] = y[1][r];
+  }
+  tile_stats(y, wave, j0, n, (int)(n_pad / TILE), ct, ps, pm, pi);
 }
 
 // V-step target Y = G_U^{-1} P (Eq. (3) first half) and its T_tau
@@ -1334,7 +1397,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   if (threadIdx.x == 0) await_flag(ready, flags);
   __syncthreads();
   double a[16];
-  load_ginv_coherent(ginvV, a);
+  load_ginv(ginvV, a);
   const int li = lane & 15, lk = lane >> 4;
   v4d z[2] = {v4d{}, v4d{}};
   // A = G^{-1}[16 w + li][4 ks + lk], B = Q^T[4 ks + lk][li (+16)] (LDS)
@@ -1532,8 +1595,9 @@ __global__ __launch_bounds__(NT) void k_tern_v(const double* __restrict__ Y, int
                                                const double* __restrict__ ps, const double* __restrict__ pm,
                                                const int* __restrict__ pi, int ntile, int ns, int8_t* __restrict__ Vt,
                                                int8_t* __restrict__ Vmf, const int8_t* __restrict__ hdig,
-                                               int8_t* __restrict__ Wmf, int64_t wstride) {
+                                               int8_t* __restrict__ Wmf, int64_t wstride, unsigned* ready) {
   const int c = blockIdx.x / ns, sp = blockIdx.x % ns;
+  if (ready && blockIdx.x == 0 && threadIdx.x == 0) *ready = 0u;  // the V-step's G_U^{-1} flag
   int64_t i0, i1;
   tern_range(n_pad, sp, ns, i0, i1);
   int8_t* dst = Vt + (int64_t)c * n_pad;
@@ -2043,9 +2107,10 @@ __global__ __launch_bounds__(NT) void k_prep(const float* __restrict__ h, int64_
                                              double* fro2_hist, double* fro2w_hist, int nblk_cap,
                                              unsigned* counters, int* flags, int* gacc, double lam,
                                              unsigned long long* argkey, int* gaccW, long long* gacc64,
-                                             int8_t* __restrict__ hdig) {
+                                             int8_t* __restrict__ hdig, unsigned* vtcnt) {
   __shared__ float smax[NT / 64];
   __shared__ int sbad[NT / 64];
+  for (int64_t e = threadIdx.x; e < n_pad / TILE; e += NT) vtcnt[e] = 0u;
   for (int e = threadIdx.x; e < nblk_cap; e += NT) {
     fro2_hist[e] = 0.0;
     fro2w_hist[e] = 0.0;
@@ -3211,7 +3276,7 @@ static inline unsigned grid_for(int64_t total) {
 hipError_t launch_prep(const Ws& w, const float* h, hipStream_t s, double lam) {
   hipLaunchKernelGGL(k_prep, dim3(1), dim3(NT), 0, s, h, w.n, w.n_pad, w.hw, w.hwmax, w.fro2_hist,
                      w.fro2w_hist, w.nblk_cap, w.counters, w.flags, w.gacc, lam, w.argkey, w.gaccW, w.gacc64,
-                     w.hdig);
+                     w.hdig, w.vtcnt);
   return hipGetLastError();
 }
 
@@ -3263,21 +3328,21 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
   return hipGetLastError();
 }
 
+// One launch forms P = U^T R (gv row-group partials per column tile),
+// G_U^{-1} (side path) and, in the last row group of each column tile, the
+// targets Y = G_U^{-1} P with their statistics (one tile per 32 columns).
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm, bool weighted) {
   const unsigned grid = (unsigned)(NSIDE_GRAM + (w.n_pad / TILE) * w.gv);
+  unsigned* ready = w.counters + CNT_GINV_U;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, (const int*)w.cshift, w.m_pad,
-                                   w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM);
+                                   w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM, w.Y,
+                                   w.tps, w.tpm, w.tpi, w.n, w.vtcnt, ready, w.flags);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VTARGET, k_vtarget<false>, dim3((unsigned)(w.n_pad / 16)), dim3(NT), 0, s,
-                       (const long long*)w.Pp, (const int*)w.cshift, w.n_pad, w.gv, w.ginvU, w.Y, w.n, w.tps, w.tpm,
-                       w.tpi, 1, (int64_t)0);
-  e = hipGetLastError();
   if (e != hipSuccess) return e;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, (const double*)w.Y, w.n,
                        w.n_pad, bb, tau, (const double*)w.tps, (const double*)w.tpm, (const int*)w.tpi,
-                       (int)(w.n_pad / 16), w.nsv, w.Vt, w.Vmf, (const int8_t*)w.hdig, weighted ? w.Wmf : nullptr,
-                       (int64_t)BMAX * w.n_pad);
+                       (int)(w.n_pad / TILE), w.nsv, w.Vt, w.Vmf, (const int8_t*)w.hdig, weighted ? w.Wmf : nullptr,
+                       (int64_t)BMAX * w.n_pad, ready);
   return hipGetLastError();
 }
 
@@ -3390,7 +3455,9 @@ hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream
     const Ws v = quarter_view(w, q);
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3((unsigned)((w.n_pad / TILE) * w.gv)), dim3(NT), 0,
                          s, w.R, (const v4i*)v.Umf, v.Pp, (const int*)w.cshift, w.m_pad, w.n_pad, w.gv,
-                         bb_of_quarter(bb, q), w.gacc, w.counters + CNT_GRAM_U, w.ginvU, 0);
+                         bb_of_quarter(bb, q), w.gacc, w.counters + CNT_GRAM_U, w.ginvU, 0, (double*)nullptr,
+                         (double*)nullptr, (double*)nullptr, (int*)nullptr, w.n, (unsigned*)nullptr,
+                         (unsigned*)nullptr, (int*)nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -3407,7 +3474,7 @@ hipError_t launch_vstep_wide(const Ws& w, int blk, int bb, double tau, hipStream
     EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNV, k_tern_v, dim3(BBP * w.nsv), dim3(NT), 0, s, (const double*)v.Y,
                          w.n, w.n_pad, bb_of_quarter(bb, q), tau, (const double*)v.tps, (const double*)v.tpm,
                          (const int*)v.tpi, (int)(w.n_pad / 16), w.nsv, v.Vt, v.Vmf, (const int8_t*)w.hdig,
-                         weighted ? v.Wmf : nullptr, (int64_t)BMAX * w.n_pad);
+                         weighted ? v.Wmf : nullptr, (int64_t)BMAX * w.n_pad, (unsigned*)nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
