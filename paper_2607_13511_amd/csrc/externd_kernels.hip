@@ -662,53 +662,40 @@ __device__ __forceinline__ bool side_gram_int(const v4i* __restrict__ Xmf, int64
 // (4096 int32) with integer atomics, exact and independent of order.  The
 // launch that needs G^{-1} takes the accumulated Gram and clears gacc.
 // ---------------------------------------------------------------------------
-// Partial Gram over the K steps [ks0, ks1) of X, added into gacc.  Waves
-// 0..3 compute (any blockDim that is a multiple of 256), each keeping KR K
-// steps of loads in flight, and store their tiles to their own LDS region;
-// all threads then sum the four regions and add the nonzero entries into
-// gacc.  red: LDS, 4 x 4096 int32.
+// Partial Gram over the K steps [ks0, ks1) of X, added into gacc.  Wave w
+// of the first four forms the 32 x 32 block (w / 2, w % 2) of X^T X over
+// all the K steps (operands: the two halves of each K step, up to GRAM_KB
+// K steps of loads in flight) and adds it into gacc with integer atomics
+// straight from its accumulator: no LDS, no barrier (blockDim: any
+// multiple of 256).
+constexpr int GRAM_KB = 20;
 __device__ __forceinline__ void gram_accumulate(const v4i* __restrict__ Xmf, int ks0, int ks1, int* gacc, int* red) {
-  constexpr int KR = 8;
+  (void)red;
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
-  if (wave < 4) {
-    v16i acc00 = {}, acc01 = {}, acc10 = {}, acc11 = {};
-    for (int ks = ks0 + wave; ks < ks1; ks += 4 * KR) {
-      v4i a[KR][2];
+  if (wave >= 4) return;
+  const int bx = wave >> 1, by = wave & 1;
+  v16i acc = {};
+  for (int ks = ks0; ks < ks1; ks += GRAM_KB) {
+    v4i ax[GRAM_KB], ay[GRAM_KB];
 #pragma unroll
-      for (int u = 0; u < KR; ++u) {
-        const int kk = ks + 4 * u;
-        if (kk < ks1) {
-          a[u][0] = Xmf[(int64_t)kk * 128 + lane];
-          a[u][1] = Xmf[(int64_t)kk * 128 + 64 + lane];
-        } else {
-          a[u][0] = v4i{};
-          a[u][1] = v4i{};
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < KR; ++u) {
-        acc00 = mfma_i8(a[u][0], a[u][0], acc00);
-        acc01 = mfma_i8(a[u][0], a[u][1], acc01);
-        acc10 = mfma_i8(a[u][1], a[u][0], acc10);
-        acc11 = mfma_i8(a[u][1], a[u][1], acc11);
-      }
+    for (int u = 0; u < GRAM_KB; ++u) {
+      const int kc = ks + u < ks1 ? ks + u : ks1 - 1;
+      ax[u] = Xmf[(int64_t)kc * 128 + 64 * bx + lane];
+      ay[u] = Xmf[(int64_t)kc * 128 + 64 * by + lane];
     }
-    int* mine = red + wave * 4096;
+    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first MFMA
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int M = 8 * (r >> 2) + 4 * h + (r & 3);
-      const int N = l32;
-      mine[M * 64 + N] = acc00[r];
-      mine[M * 64 + 32 + N] = acc01[r];
-      mine[(32 + M) * 64 + N] = acc10[r];
-      mine[(32 + M) * 64 + 32 + N] = acc11[r];
+    for (int u = 0; u < GRAM_KB; ++u) {
+      const bool in = ks + u < ks1;
+      acc = mfma_i8(in ? ax[u] : v4i{}, in ? ay[u] : v4i{}, acc);
     }
   }
-  __syncthreads();
-  for (int e = threadIdx.x; e < 4096; e += blockDim.x) {
-    const int v = red[e] + red[4096 + e] + red[8192 + e] + red[12288 + e];
-    if (v) __hip_atomic_fetch_add(gacc + e, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int M = 8 * (r >> 2) + 4 * h + (r & 3);
+    const int v = acc[r];
+    if (v) __hip_atomic_fetch_add(gacc + (32 * bx + M) * 64 + 32 * by + l32, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -2881,10 +2868,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // Integer Gram of a factor given by the caller (step entry points): adds
 // X^T X into gacc.  grid: NSIDE_GRAM WGs over the K steps.
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_gram_acc(const v4i* __restrict__ Xmf, int64_t L_pad, int* gacc) {
-  __shared__ int red[4 * 4096];
   const int nks = (int)(L_pad / TILE);
   gram_accumulate(Xmf, (int)((long long)blockIdx.x * nks / gridDim.x), (int)((long long)(blockIdx.x + 1) * nks / gridDim.x),
-                  gacc, red);
+                  gacc, nullptr);
 }
 
 // g_c = sum_i U_ic Q_ic (fp64), in slot 0 of the per-split partial sums.
