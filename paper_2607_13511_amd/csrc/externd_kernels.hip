@@ -853,6 +853,52 @@ __device__ __forceinline__ void gram_w_accumulate(const v4i* Xa, const int8_t* W
   }
 }
 
+// The symmetric weighted Gram X^T diag(H) X over the K steps [ks0, ks1) by
+// blocks: wave w in {0, 1, 3} forms block (w / 2, w % 2) over all six
+// digit planes (operands: half w / 2 of each K step of X and half w % 2 of
+// each digit-scaled plane, GRAMW_KB K steps of loads issued before their
+// MFMAs), combines the planes into int64 per entry (sum_d 128^d plane_d)
+// and adds the block into g64 with integer atomics straight from its
+// accumulators: no LDS, no barrier.  The lower-left block is the transpose
+// of the upper-right one and is not formed.
+constexpr int GRAMW_KB = 4;
+__device__ __forceinline__ void gram_w_blocks(const v4i* __restrict__ Xa, const int8_t* __restrict__ Wb,
+                                              int64_t wstride, int ks0, int ks1, long long* g64) {
+  const int lane = lane_id(), wave = wave_id();
+  const int h = lane >> 5, l32 = lane & 31;
+  if (wave >= 4 || wave == 2) return;
+  const int bx = wave >> 1, by = wave & 1;
+  v16i acc[WDIG];
+#pragma unroll
+  for (int d = 0; d < WDIG; ++d) acc[d] = v16i{};
+  for (int ks = ks0; ks < ks1; ks += GRAMW_KB) {
+    v4i a[GRAMW_KB], wv[GRAMW_KB][WDIG];
+#pragma unroll
+    for (int u = 0; u < GRAMW_KB; ++u) {
+      const int64_t kc = ks + u < ks1 ? ks + u : ks0;
+      a[u] = Xa[kc * 128 + 64 * bx + lane];
+#pragma unroll
+      for (int d = 0; d < WDIG; ++d)
+        wv[u][d] = ((const v4i*)(Wb + (int64_t)d * wstride))[kc * 128 + 64 * by + lane];
+    }
+    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first MFMA
+#pragma unroll
+    for (int u = 0; u < GRAMW_KB; ++u) {
+      const v4i x = ks + u < ks1 ? a[u] : v4i{};
+#pragma unroll
+      for (int d = 0; d < WDIG; ++d) acc[d] = mfma_i8(x, wv[u][d], acc[d]);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int M = 8 * (r >> 2) + 4 * h + (r & 3);
+    long long v = 0;
+#pragma unroll
+    for (int d = 0; d < WDIG; ++d) v += (long long)acc[d][r] * (1ll << (WDIG_BITS * d));
+    if (v) __hip_atomic_fetch_add(g64 + (32 * bx + M) * 64 + 32 * by + l32, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 // The symmetric weighted Gram from its accumulator (upper-left, upper-right
 // and lower-right blocks; the lower-left one is the transpose of the
 // upper-right): G (LDS, fp64) = g64 * unit, with coherent loads (the
@@ -882,8 +928,9 @@ __device__ __forceinline__ bool side_gram_w(const v4i* __restrict__ Vmf, const i
                                             int64_t wstride, int64_t n_pad, int side, int nside, long long* g64,
                                             double unit, unsigned* counter, double* G, int* red) {
   const int nks = (int)(n_pad / TILE);
-  gram_w_accumulate<true>(Vmf, Wmf, wstride, (int)((long long)side * nks / nside),
-                          (int)((long long)(side + 1) * nks / nside), g64, red);
+  (void)red;
+  gram_w_blocks(Vmf, Wmf, wstride, (int)((long long)side * nks / nside), (int)((long long)(side + 1) * nks / nside),
+                g64);
   __builtin_amdgcn_s_waitcnt(0);  // this wave's atomics have been performed
   __shared__ int s_last;
   __syncthreads();
