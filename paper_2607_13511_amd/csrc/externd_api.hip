@@ -45,9 +45,11 @@ static Layout make_layout(int64_t m, int64_t n, int64_t k) {
   L.gd = clampi(DEFLATE_SLOTS / nct, 1, nrt < 64 ? nrt : 64);
   // U-step: equal row groups of at most 32 rows, as many as fit beside the
   // side workgroups in one pass of USTEP_SLOTS resident workgroups, so
-  // that every CU streams the same share of R.
-  L.urows = clampi((L.m_pad + (USTEP_SLOTS - NSIDE_MAX) - 1) / (USTEP_SLOTS - NSIDE_MAX), 1, TILE);
-  L.ntu = (int)((L.m_pad + L.urows - 1) / L.urows);
+  // that every CU streams the same share of R.  NSIDE_MAX more slots stay
+  // empty: those that the dispatcher places beside the side workgroups
+  // (ntu counts them; the launch maps them out).
+  L.urows = clampi((L.m_pad + (USTEP_SLOTS - 2 * NSIDE_MAX) - 1) / (USTEP_SLOTS - 2 * NSIDE_MAX), 1, TILE);
+  L.ntu = (int)((L.m_pad + L.urows - 1) / L.urows) + NSIDE_MAX;
   L.nsu = clampi((L.m_pad + TERN_CHUNK - 1) / TERN_CHUNK, 1, TERN_SPLIT_MAX);
   L.nsv = clampi((L.n_pad + TERN_CHUNK - 1) / TERN_CHUNK, 1, TERN_SPLIT_MAX);
   L.nblk_cap = (int)(k + 2);  // fro2 before every block and after the last; one spare

@@ -1284,9 +1284,18 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     }
     return;
   }
-  const int rt = blockIdx.x - nside;
+  // The workgroups are dispatched one per CU first (the side workgroups
+  // take the first nside CUs), then a second one per CU; the second ones
+  // on the side workgroups' CUs (indices 256 .. 256 + nside - 1 of the
+  // grid) are left empty so that the inverse sweep has its CU to itself,
+  // and the row groups after them shift down.  Were the placement
+  // different, those slots would only cost their share of the stream.
+  const int rt0 = blockIdx.x - nside;
+  if (nside && rt0 >= 256 - nside && rt0 < 256) return;
+  const int rt = (nside && rt0 >= 256) ? rt0 - nside : rt0;
   const int64_t i0 = (int64_t)rt * rows;
-  const int valid = (int)(m_pad - i0 < rows ? m_pad - i0 : rows);  // >= 1: ntile = ceil(m_pad / rows)
+  if (i0 >= m_pad) return;  // the slots counted for the empty ones, past the last row group
+  const int valid = (int)(m_pad - i0 < rows ? m_pad - i0 : rows);
   const int lane = lane_id(), wave = wave_id();
   const int h = lane >> 5, l32 = lane & 31;
   // lane (i, h) converts row i0 + i only: its own exponent, from the row's
@@ -1447,7 +1456,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     if (16 + li < valid) row[16 + li] = z[1][r];
   }
   const int64_t iend = i0 + valid < m ? i0 + valid : m;
-  tile_stats(z, wave, i0, iend, (int)gridDim.x - nside, rt, ps, pm, pi);
+  tile_stats(z, wave, i0, iend, (int)gridDim.x - 2 * nside, rt, ps, pm, pi);
 }
 
 // U-step target rows Z = Q G_V^{-1} (Eq. (3) second half) and their T_tau
@@ -3386,6 +3395,7 @@ hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s,
 hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted, bool final, hipStream_t s,
                         Timer* tm, bool keep_q) {
   hipError_t e;
+  static_assert(NSIDE_GRAM == NSIDE_MAX, "the empty row-group slots match the side workgroups");
   const unsigned nside = NSIDE_GRAM;
   const unsigned grid = (unsigned)(nside + w.ntu);
   unsigned* ready = w.counters + CNT_GINV_V;
@@ -3406,7 +3416,8 @@ hipError_t launch_ustep(const Ws& w, int blk, int bb, double tau, bool weighted,
   if (e != hipSuccess) return e;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_TERNU, k_tern_u, dim3(BBP * w.nsu), dim3(NT), 0, s, (const double*)w.Z,
                        final ? (const double*)w.Q : nullptr, w.m, w.m_pad, bb, tau, (const double*)w.tps,
-                       (const double*)w.tpm, (const int*)w.tpi, w.ntu, w.nsu, w.Ut, w.Umf, w.gvec, ready);
+                       (const double*)w.tpm, (const int*)w.tpi, w.ntu - (int)NSIDE_MAX, w.nsu, w.Ut, w.Umf, w.gvec,
+                       ready);
   return hipGetLastError();
 }
 
