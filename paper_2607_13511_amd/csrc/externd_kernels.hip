@@ -1033,8 +1033,13 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     ginv_ready(ready);
     return;
   }
-  const int b = blockIdx.x - nside;
+  // as in the U-step, the second workgroups on the side workgroups' CUs
+  // (grid indices 256 .. 256 + nside - 1) stay empty
+  const int b0 = blockIdx.x - nside;
+  if (nside && b0 >= 256 - nside && b0 < 256) return;
+  const int b = (nside && b0 >= 256) ? b0 - nside : b0;
   const int nct = (int)(n_pad / TILE);
+  if (b >= nct * gv) return;
   const int ct = b % nct, g = b / nct;
   const int nks = (int)(m_pad / TILE);
   const int ks0 = (int)((long long)g * nks / gv), ks1 = (int)((long long)(g + 1) * nks / gv);
@@ -3374,7 +3379,8 @@ hipError_t launch_init(const Ws& w, int bb, double tau, hipStream_t s) {
 // G_U^{-1} (side path) and, in the last row group of each column tile, the
 // targets Y = G_U^{-1} P with their statistics (one tile per 32 columns).
 hipError_t launch_vstep(const Ws& w, int blk, int bb, double tau, hipStream_t s, Timer* tm, bool weighted) {
-  const unsigned grid = (unsigned)(NSIDE_GRAM + (w.n_pad / TILE) * w.gv);
+  const int nsb = (int)((w.n_pad / TILE) * w.gv);  // streaming workgroups, plus the empty slots past 256
+  const unsigned grid = (unsigned)(NSIDE_GRAM + nsb + (nsb > 256 - NSIDE_GRAM ? NSIDE_GRAM : 0));
   unsigned* ready = w.counters + CNT_GINV_U;
   EXTERND_LAUNCH_TIMED(tm, EXTERND_KCLASS_VSTEP, k_vstep, dim3(grid), dim3(NT), 0, s, w.R, (const v4i*)w.Umf, w.Pp, (const int*)w.cshift, w.m_pad,
                                    w.n_pad, w.gv, bb, w.gacc, w.counters + CNT_GRAM_U, w.ginvU, NSIDE_GRAM, w.Y,

@@ -258,6 +258,8 @@ E2E = [
     ("gauss", 300, 64, 0.5, 0.7, 1, 3, False),     # b = 1 beyond the one-launch shapes: the block kernels
     ("t4", 40, 17000, 1.0, 1.0, 8, 3, True),       # > 512 column strips: one deflation and V-step row group
     ("t4_rowscale", 17000, 40, 1.0, 0.7, 8, 3, False),  # U-step groups of 32 rows beyond one resident pass
+    ("t4", 30, 7300, 1.0, 1.0, 4, 3, False),      # 229 V-step workgroups: just below the empty slots at 240
+    ("t4", 30, 7900, 1.0, 1.0, 4, 3, True),       # 247 V-step workgroups: some past the empty slots
     ("t4_outlier1e4", 300, 200, 1.0, 1.0, 8, 3, False),   # one entry 1e4 x the largest: per-row/column exponents
     ("t4_outlier1e4", 256, 320, 1.0, 0.7, 16, 3, True),
 ]
