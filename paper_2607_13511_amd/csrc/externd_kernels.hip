@@ -43,6 +43,8 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef short v8s __attribute__((ext_vector_type(8)));
 typedef double v4d __attribute__((ext_vector_type(4)));
 typedef double v2d __attribute__((ext_vector_type(2)));
+typedef long long v2l __attribute__((ext_vector_type(2)));
+constexpr int GV_ONE = 6;  // V-step row groups summed in one round of loads
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
@@ -1113,25 +1115,57 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   // Ps[c * 33 + j], thread (c = e / 32, j = e % 32) for e = tid + 256 i
   double* Ps = (double*)smem;
   const int64_t j0 = (int64_t)ct * TILE;
-  // thread (c = e / 32, j = e % 32) for e = tid + 256 i, in two rounds of
-  // four entries: the gv partials of each entry, all in flight at once
+  // gv <= 6 (the usual case): thread t takes columns j0 + jp, jp + 1
+  // (jp = 2 (t % 16)) of components t / 16 + 16 i, i < 4, with the gv
+  // partials of its four pairs all in flight at once, as 16-byte plain
+  // loads from clamped row groups (masked in the sum).  Plain loads see the
+  // written-through partials: no workgroup of this launch reads these lines
+  // before the arrival count shows them complete, and each launch starts
+  // with clean caches.
+  if (gv <= GV_ONE) {
+    const int jp = 2 * (threadIdx.x & 15), cq = threadIdx.x >> 4;
+    v2l v[4][GV_ONE];
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    long long v[4][GV_MAX];
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int gg = 0; gg < GV_ONE; ++gg) {
+        const int gc = gg < gv ? gg : 0;
+        v[i][gg] = *(const v2l*)(Pp + ((int64_t)gc * BBP + cq + 16 * i) * n_pad + j0 + jp);
+      }
+    const int sh0 = cshift[j0 + jp], sh1 = cshift[j0 + jp + 1];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int e = threadIdx.x + NT * (4 * half + i), c = e >> 5, j = e & 31;
+      long long s0 = 0, s1 = 0;
 #pragma unroll
-      for (int gg = 0; gg < GV_MAX; ++gg)
-        v[i][gg] = gg < gv ? load_coherent(Pp + ((int64_t)gg * BBP + c) * n_pad + j0 + j) : 0ll;
+      for (int gg = 0; gg < GV_ONE; ++gg) {
+        s0 += gg < gv ? v[i][gg].x : 0ll;
+        s1 += gg < gv ? v[i][gg].y : 0ll;
+      }
+      const int c = cq + 16 * i;
+      Ps[c * 33 + jp] = ldexp((double)s0, -sh0);
+      Ps[c * 33 + jp + 1] = ldexp((double)s1, -sh1);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = threadIdx.x + NT * (4 * half + i), c = e >> 5, j = e & 31;
-      long long sum = 0;
-#pragma unroll
-      for (int gg = 0; gg < GV_MAX; ++gg) sum += v[i][gg];
-      Ps[c * 33 + j] = ldexp((double)sum, -cshift[j0 + j]);
+  } else {
+    // thread (c = e / 32, j = e % 32) for e = tid + 256 i, in two rounds of
+    // four entries: the gv partials of each entry, all in flight at once
+  #pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      long long v[4][GV_MAX];
+  #pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = threadIdx.x + NT * (4 * half + i), c = e >> 5, j = e & 31;
+  #pragma unroll
+        for (int gg = 0; gg < GV_MAX; ++gg)
+          v[i][gg] = gg < gv ? load_coherent(Pp + ((int64_t)gg * BBP + c) * n_pad + j0 + j) : 0ll;
+      }
+  #pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = threadIdx.x + NT * (4 * half + i), c = e >> 5, j = e & 31;
+        long long sum = 0;
+  #pragma unroll
+        for (int gg = 0; gg < GV_MAX; ++gg) sum += v[i][gg];
+        Ps[c * 33 + j] = ldexp((double)sum, -cshift[j0 + j]);
+      }
     }
   }
   if (threadIdx.x == 0) await_flag(ready, flags);
