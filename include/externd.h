@@ -51,9 +51,10 @@ extern "C" {
 #define EXTERND_EHIP         -4  /* HIP runtime or launch failure                       */
 #define EXTERND_EUNSUPPORTED -5  /* shape outside the supported range                   */
 #define EXTERND_ESYNC        -6  /* a bounded wait between the workgroups of one kernel
-                                    launch ran out (the U-step's row groups wait at most
-                                    20 ms for the inverse Gram of the same launch); the
-                                    factors of such a call are not to be used           */
+                                    launch ran out (the U-step's row groups and the
+                                    V-step's last row group of each column tile wait at
+                                    most 20 ms for the inverse Gram of the same launch);
+                                    the factors of such a call are not to be used       */
 #define EXTERND_ESCRATCH     -7  /* the call needs more than the fixed device scratch of
                                     an allocation-free entry point                       */
 
